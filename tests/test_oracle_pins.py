@@ -1,0 +1,10 @@
+"""The float64 oracle against what the paper and the mathematics fix (no GPU)."""
+import pytest
+
+import oracle
+import oracle_pins
+
+
+@pytest.mark.parametrize("pin", oracle_pins.ALL_PINS, ids=lambda f: f.__name__)
+def test_pin(pin):
+    pin(oracle.luna_oracle)

@@ -1,0 +1,147 @@
+/*
+ * luna.h -- C ABI of the LUNA attention forward pass on AMD Instinct MI355X (gfx950).
+ *
+ * LUNA ("Learning Kernels for Linear Attention") replaces the softmax kernel by a
+ * learned positive-definite kernel k(x, y) = phi(x) . phi(y) and evaluates attention
+ * in linear time through the kernelised form, eq. (kernel-attn):
+ *
+ *     out = phi(Q) (phi(K)^T V) / phi(Q) (phi(K)^T 1)          (row by row)
+ *
+ * with the feature map of eq. (phi-def), envelope h = 1 (Table 5, "no gate"):
+ *
+ *     phi(x) = (1/sqrt(M)) [ psi_l(w_i . x + b_i) ]_{i = 1..M, l = 1..L}  in R^{M*L}
+ *
+ * where every channel function psi_l is a scalar MLP 1 -> hidden -> 1 with ReLU
+ * activation and (by default) a ReLU on its output (the paper's listing of the
+ * feature map).  The statistics S = phi(K)^T V and z = phi(K)^T 1 are the key-side
+ * sufficient statistics of the runtime section (section 4).
+ *
+ * Conventions shared by every entry point:
+ *  - Every data pointer is caller-owned DEVICE memory, row-major and contiguous.
+ *    Q, K, V and out are [B, H, n, d]; the library never allocates or frees on a
+ *    call, keeps no pointer after it returns and has no global mutable state, so
+ *    calls on different streams may run concurrently if their workspaces differ.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued on it
+ *    asynchronously; LUNA_OK means "enqueued", not "finished".
+ *  - All arguments are validated on the host before anything is launched.  A
+ *    failed validation returns an error code and enqueues nothing;
+ *    luna_last_error() then describes the reason (thread-local string).
+ *  - Precision follows `dtype`: LUNA_F32 computes in fp32 throughout (fp32 matrix
+ *    cores); LUNA_BF16 takes bf16 Q, K, V and W, multiplies bf16 operands on the
+ *    matrix cores with fp32 accumulation, evaluates psi in fp32, keeps S and z in
+ *    fp32 (rounded to bf16 as matrix-core operands) and writes bf16 output.
+ *  - The denominator gets an additive eps: out = num / (den + eps).  With ReLU
+ *    features a row can have den = 0; it then yields 0.
+ *  - Shapes the kernels are not built for return LUNA_ERR_UNSUPPORTED; there is
+ *    no fallback path.
+ */
+#ifndef LUNA_H_
+#define LUNA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum luna_status {
+  LUNA_OK = 0,
+  LUNA_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, inconsistent parameters */
+  LUNA_ERR_UNSUPPORTED = 2, /* valid problem that the built kernels do not cover */
+  LUNA_ERR_WORKSPACE = 3,   /* ws_bytes smaller than luna_workspace_bytes() */
+  LUNA_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} luna_status;
+
+typedef enum luna_dtype { LUNA_F32 = 0, LUNA_BF16 = 1 } luna_dtype;
+
+/* Operation codes for luna_workspace_bytes(). */
+enum { LUNA_OP_FEATUREMAP = 0, LUNA_OP_ATTN = 1, LUNA_OP_ATTN_CAUSAL = 2 };
+
+/*
+ * Feature-map parameters, eq. (phi-def) and the paper's listing of the feature map.
+ *   M       number of projections w_i (rows of W), 1 <= M <= 64
+ *   L       channels per projection (outputs of the psi_l), 1 <= L <= 16; D = M*L <= 256
+ *   hidden  width of each channel MLP, 1 <= hidden <= 64
+ *   shared_channels 0: L separate MLPs 1 -> hidden -> 1 (the listing's default);
+ *                   1: one MLP 1 -> hidden -> L whose first layer all channels share
+ *   nonneg  1: ReLU on every MLP output, so phi >= 0 (the listing's default); 0: none
+ *   per_head 0: one parameter set shared by all heads (the listing's default);
+ *            1: H sets, stored head-major (leading dimension H on every array)
+ * Arrays (device memory; P = per_head ? H : 1; C1 = shared_channels ? 1 : L):
+ *   W     [P][M][d]        element type = the call's dtype (bf16 or fp32)
+ *   b     [P][M]           fp32 projection bias (the Fig. 3 caption's u = w_i.x + b_i)
+ *   fc1_w [P][C1][hidden]  fp32 first-layer weight (a_lk)
+ *   fc1_b [P][C1][hidden]  fp32 first-layer bias   (c_lk)
+ *   fc2_w [P][L][hidden]   fp32 second-layer weight (f_lk)
+ *   fc2_b [P][L]           fp32 second-layer bias   (g_l)
+ * Channel l computes psi_l(u) = relu(g_l + sum_k f_lk relu(a_lk u + c_lk)) (outer
+ * relu only when nonneg).  The struct is read during the call only.
+ */
+typedef struct luna_phi_params {
+  int32_t M, L, hidden;
+  int32_t shared_channels;
+  int32_t nonneg;
+  int32_t per_head;
+  const void* W;
+  const float* b;
+  const float* fc1_w;
+  const float* fc1_b;
+  const float* fc2_w;
+  const float* fc2_b;
+} luna_phi_params;
+
+/*
+ * Bytes of device workspace an operation needs (0 if the arguments are invalid or
+ * unsupported).  op is LUNA_OP_*; dtype is the call's dtype (for LUNA_OP_FEATUREMAP
+ * the input dtype); chunk is used by LUNA_OP_ATTN_CAUSAL only.  The workspace must
+ * be 256-byte aligned.  The workspace holds
+ * the exact piecewise-linear tables of the channel MLPs, built on the device at the
+ * start of every call, plus partial statistics and counters for long sequences.  It
+ * needs no initialisation; it must stay untouched by other work until the call's
+ * kernels have finished.
+ */
+size_t luna_workspace_bytes(int32_t op, luna_dtype dtype, int64_t B, int64_t H, int64_t n,
+                            int64_t d, const luna_phi_params* p, int32_t chunk);
+
+/*
+ * Feature map phi of eq. (phi-def) applied to every row of X [B, H, n, d].
+ * phi_out [B, H, n, M*L] receives feature i*L + l (channel index fastest) of each
+ * row, in out_dtype.  X and W are in x_dtype.  d must be 32, 64 or 128.
+ */
+luna_status luna_featuremap(const void* X, luna_dtype x_dtype, int64_t B, int64_t H, int64_t n,
+                            int64_t d, const luna_phi_params* p, void* phi_out, luna_dtype out_dtype,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Non-causal LUNA attention, eq. (kernel-attn):
+ *   S = phi(K)^T V, z = phi(K)^T 1 per (b, h);  out = phi(Q) S / (phi(Q) z + eps).
+ * Q, K, V, out: [B, H, n, d] in dtype (value width d_v = d).  d in {32, 64, 128}.
+ */
+luna_status luna_attn_fwd(const void* Q, const void* K, const void* V, luna_dtype dtype,
+                          int64_t B, int64_t H, int64_t n, int64_t d, const luna_phi_params* p,
+                          float eps, void* out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Causal (streaming) LUNA attention: the prefix form of eq. (kernel-attn),
+ *   out_t = phi(q_t)^T S_t / (phi(q_t)^T z_t + eps),
+ *   S_t = sum_{s <= t} phi(k_s) v_s^T,  z_t = sum_{s <= t} phi(k_s)   (diagonal included),
+ * evaluated as a chunked scan: per chunk of `chunk` tokens a masked intra-chunk block
+ * plus the carried state.  chunk must be 64.  Same layouts as luna_attn_fwd.
+ */
+luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, luna_dtype dtype,
+                                 int64_t B, int64_t H, int64_t n, int64_t d,
+                                 const luna_phi_params* p, int32_t chunk, float eps, void* out,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* luna_status_string(luna_status s);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char* luna_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LUNA_H_ */

@@ -1,0 +1,273 @@
+// luna_api.cpp -- host side of the C ABI declared in include/luna.h.
+//
+// Every entry point validates its arguments completely on the host before any HIP
+// call, plans the workspace (piecewise-linear tables first, then per-operation
+// buffers, each 256-byte aligned) and enqueues its kernels on the caller's stream.
+#include "luna.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <string>
+
+#include "luna_kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+luna_status fail(luna_status s, const std::string& why) {
+  g_last_error = why;
+  return s;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Problem {
+  int op;
+  luna_dtype dt;
+  int64_t B, H, n, d;
+  const luna_phi_params* p;
+  int32_t chunk;
+};
+
+int param_sets(const Problem& pb) { return pb.p->per_head ? (int)pb.H : 1; }
+
+// Checks shared by every operation; `why` receives the reason on failure.
+luna_status check_common(const Problem& pb) {
+  const luna_phi_params* p = pb.p;
+  if (p == nullptr) return fail(LUNA_ERR_INVALID_ARG, "params is NULL");
+  if (pb.dt != LUNA_F32 && pb.dt != LUNA_BF16) return fail(LUNA_ERR_INVALID_ARG, "dtype must be LUNA_F32 or LUNA_BF16");
+  if (pb.B < 1 || pb.H < 1 || pb.n < 1) return fail(LUNA_ERR_INVALID_ARG, "B, H and n must be >= 1");
+  if (pb.n > (int64_t)1 << 30) return fail(LUNA_ERR_UNSUPPORTED, "n must be <= 2^30");
+  if (pb.B * pb.H > (int64_t)1 << 24) return fail(LUNA_ERR_UNSUPPORTED, "B*H must be <= 2^24");
+  if (pb.d != 32 && pb.d != 64 && pb.d != 128) return fail(LUNA_ERR_UNSUPPORTED, "d must be 32, 64 or 128");
+  if (p->M < 1 || p->M > 64) return fail(LUNA_ERR_INVALID_ARG, "M must be in [1, 64]");
+  if (p->L < 1 || p->L > 16) return fail(LUNA_ERR_INVALID_ARG, "L must be in [1, 16]");
+  if (p->hidden < 1 || p->hidden > 64) return fail(LUNA_ERR_INVALID_ARG, "hidden must be in [1, 64]");
+  if (p->M * p->L > 256) return fail(LUNA_ERR_INVALID_ARG, "M*L must be <= 256");
+  if (p->shared_channels != 0 && p->shared_channels != 1) return fail(LUNA_ERR_INVALID_ARG, "shared_channels must be 0 or 1");
+  if (p->nonneg != 0 && p->nonneg != 1) return fail(LUNA_ERR_INVALID_ARG, "nonneg must be 0 or 1");
+  if (p->per_head != 0 && p->per_head != 1) return fail(LUNA_ERR_INVALID_ARG, "per_head must be 0 or 1");
+  if (!p->W || !p->b || !p->fc1_w || !p->fc1_b || !p->fc2_w || !p->fc2_b)
+    return fail(LUNA_ERR_INVALID_ARG, "a parameter array is NULL");
+  const int C1 = p->shared_channels ? 1 : p->L;
+  const int units = C1 * p->hidden;
+  if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
+  const int seg_cap = pb.op == LUNA_OP_FEATUREMAP ? luna::kSegCap : luna::attn_seg_cap(p->L);
+  if ((units + 1) * p->L > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "(L*hidden + 1)*L exceeds the segment table");
+  return LUNA_OK;
+}
+
+struct Layout {
+  size_t tables = 0, partial = 0, frags = 0, total = 0;
+  int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, dv_tiles = 1;
+};
+
+luna_status plan(const Problem& pb, Layout* lay) {
+  luna_status st = check_common(pb);
+  if (st != LUNA_OK) return st;
+  const luna::Dt dt = pb.dt == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int d = (int)pb.d, L = pb.p->L, M = pb.p->M;
+  const int64_t heads = pb.B * pb.H;
+  size_t off = 0;
+  lay->tables = off;
+  off = align256(off + (size_t)param_sets(pb) * luna::kTableBytes);
+  if (pb.op == LUNA_OP_FEATUREMAP) {
+    if (!luna::featuremap_supported(dt, d, L, M))
+      return fail(LUNA_ERR_UNSUPPORTED, "no feature-map kernel for this (d, L, M)");
+  } else if (pb.op == LUNA_OP_ATTN) {
+    luna::NoncausalPlan np;
+    if (!luna::noncausal_supported(dt, d, L, M, &np))
+      return fail(LUNA_ERR_UNSUPPORTED, "no non-causal attention kernel for this (dtype, d, L, M)");
+    // enough state workgroups to fill the device, at least 256 tokens each
+    const int64_t want = (512 + heads - 1) / heads;
+    const int64_t maxs = (pb.n + 255) / 256;
+    int64_t splits = want < maxs ? want : maxs;
+    if (splits < 1) splits = 1;
+    int64_t tps = (pb.n + splits - 1) / splits;
+    tps = (tps + 127) / 128 * 128;
+    splits = (pb.n + tps - 1) / tps;
+    lay->splits = (int)splits;
+    lay->tokens_per_split = (int)tps;
+    lay->tile_tokens = 256;
+    lay->tiles = (int)((pb.n + 255) / 256);
+    lay->partial = off;
+    off = align256(off + (size_t)heads * splits * np.DP * (d + 1) * sizeof(float));
+    lay->frags = off;
+    off = align256(off + (size_t)heads * np.frag_elems * (pb.dt == LUNA_BF16 ? 2 : 4));
+  } else if (pb.op == LUNA_OP_ATTN_CAUSAL) {
+    if (pb.chunk != 64) return fail(LUNA_ERR_UNSUPPORTED, "chunk must be 64");
+    int tiles = 1;
+    if (!luna::causal_supported(dt, d, L, M, &tiles))
+      return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernel for this (dtype, d, L, M)");
+    lay->dv_tiles = tiles;
+  } else {
+    return fail(LUNA_ERR_INVALID_ARG, "unknown operation code");
+  }
+  lay->total = off;
+  return LUNA_OK;
+}
+
+luna_status check_ws(const Layout& lay, void* ws, size_t ws_bytes) {
+  if (ws_bytes < lay.total) {
+    char buf[128];
+    snprintf(buf, sizeof buf, "workspace too small: need %zu bytes, got %zu", lay.total, ws_bytes);
+    return fail(LUNA_ERR_WORKSPACE, buf);
+  }
+  if (ws == nullptr) return fail(LUNA_ERR_INVALID_ARG, "workspace is NULL");
+  if (((uintptr_t)ws & 255) != 0) return fail(LUNA_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  return LUNA_OK;
+}
+
+luna_status hip_fail(hipError_t e, const char* what) {
+  return fail(LUNA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+luna_status enqueue_prepare(const Problem& pb, uint8_t* ws, const Layout& lay, hipStream_t s) {
+  const luna_phi_params* p = pb.p;
+  luna::PrepareArgs a{};
+  a.fc1_w = p->fc1_w;
+  a.fc1_b = p->fc1_b;
+  a.fc2_w = p->fc2_w;
+  a.fc2_b = p->fc2_b;
+  a.P = param_sets(pb);
+  a.C1 = p->shared_channels ? 1 : p->L;
+  a.L = p->L;
+  a.hidden = p->hidden;
+  a.M = p->M;
+  a.nonneg = p->nonneg;
+  a.tables = ws + lay.tables;
+  a.zero_ptr = nullptr;
+  a.zero_count = 0;
+  hipError_t e = luna::launch_prepare(a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "table kernel launch");
+}
+
+luna::PhiArgs phi_args(const Problem& pb, uint8_t* ws, const Layout& lay) {
+  luna::PhiArgs f{};
+  f.W = pb.p->W;
+  f.b = pb.p->b;
+  f.tables = ws + lay.tables;
+  f.M = pb.p->M;
+  f.per_head = pb.p->per_head;
+  return f;
+}
+
+bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.0f; }
+
+}  // namespace
+
+extern "C" {
+
+size_t luna_workspace_bytes(int32_t op, luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                            const luna_phi_params* p, int32_t chunk) {
+  Problem pb{op, dtype, B, H, n, d, p, chunk};
+  Layout lay;
+  return plan(pb, &lay) == LUNA_OK ? lay.total : 0;
+}
+
+luna_status luna_featuremap(const void* X, luna_dtype x_dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                            const luna_phi_params* p, void* phi_out, luna_dtype out_dtype, void* ws,
+                            size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  Problem pb{LUNA_OP_FEATUREMAP, x_dtype, B, H, n, d, p, 0};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (out_dtype != LUNA_F32 && out_dtype != LUNA_BF16) return fail(LUNA_ERR_INVALID_ARG, "out_dtype must be LUNA_F32 or LUNA_BF16");
+  if (!X || !phi_out) return fail(LUNA_ERR_INVALID_ARG, "X or phi_out is NULL");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  luna::FeatureMapArgs a{};
+  a.X = X;
+  a.out = phi_out;
+  a.phi = phi_args(pb, w, lay);
+  a.rows_per_head = n;
+  a.H = (int)H;
+  a.heads = B * H;
+  hipError_t e = luna::launch_featuremap(x_dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32,
+                                         out_dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32, (int)d, p->L, a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "feature-map kernel launch");
+}
+
+luna_status luna_attn_fwd(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B, int64_t H,
+                          int64_t n, int64_t d, const luna_phi_params* p, float eps, void* out, void* ws,
+                          size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  Problem pb{LUNA_OP_ATTN, dtype, B, H, n, d, p, 0};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (!Q || !K || !V || !out) return fail(LUNA_ERR_INVALID_ARG, "Q, K, V or out is NULL");
+  if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  luna::NoncausalArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.out = out;
+  a.phi = phi_args(pb, w, lay);
+  a.n = (int)n;
+  a.H = (int)H;
+  a.heads = (int)(B * H);
+  a.splits = lay.splits;
+  a.tokens_per_split = lay.tokens_per_split;
+  a.eps = eps;
+  a.partial = reinterpret_cast<float*>(w + lay.partial);
+  a.frags = w + lay.frags;
+  a.tile_tokens = lay.tile_tokens;
+  a.tiles = lay.tiles;
+  hipError_t e = luna::launch_noncausal(dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32, (int)d, p->L, p->M, a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "attention kernel launch");
+}
+
+luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B,
+                                 int64_t H, int64_t n, int64_t d, const luna_phi_params* p, int32_t chunk, float eps,
+                                 void* out, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  Problem pb{LUNA_OP_ATTN_CAUSAL, dtype, B, H, n, d, p, chunk};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (!Q || !K || !V || !out) return fail(LUNA_ERR_INVALID_ARG, "Q, K, V or out is NULL");
+  if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  luna::CausalArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.out = out;
+  a.phi = phi_args(pb, w, lay);
+  a.n = (int)n;
+  a.H = (int)H;
+  a.heads = (int)(B * H);
+  a.dv_tiles = lay.dv_tiles;
+  a.eps = eps;
+  hipError_t e = luna::launch_causal(dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32, (int)d, p->L, p->M, a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");
+}
+
+const char* luna_status_string(luna_status s) {
+  switch (s) {
+    case LUNA_OK: return "ok";
+    case LUNA_ERR_INVALID_ARG: return "invalid argument";
+    case LUNA_ERR_UNSUPPORTED: return "unsupported problem";
+    case LUNA_ERR_WORKSPACE: return "workspace too small";
+    case LUNA_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* luna_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,205 @@
+// luna_device.hpp -- device building blocks shared by the LUNA kernels (gfx950).
+//
+// Matrix-core fragments.  Every product in this library is built from one
+// abstraction: a 16x16 output block accumulated in fp32 from operands that each
+// hold, per lane, 8 values of the reduction ("k") dimension:
+//
+//   lane l (0..63), group g = l / 16, index r = l % 16
+//   A operand: row r,    k-slots (g, e), e = 0..7
+//   B operand: column r, k-slots (g, e), e = 0..7
+//   C/D:       rows 4g + j (j = 0..3), column r
+//
+// The hardware pairs A's slot (g, e) with B's slot (g, e); which abstract k a
+// slot stands for is chosen by each kernel (the same choice on both operands),
+// so kernels are free to permute k to match the layout their data arrives in.
+// bf16 uses one v_mfma_f32_16x16x32_bf16 per fragment pair; fp32 uses eight
+// v_mfma_f32_16x16x4_f32 (instruction e consumes slot e of every group).
+//
+// Channel functions.  A ReLU MLP of a scalar is continuous and piecewise linear
+// in that scalar.  Its breakpoints -c_k/a_k are merged and sorted once per call
+// (luna_prepare.hip); evaluation is then a branch-free binary search over the
+// breakpoints (stored in heap order) and one fused multiply-add per channel with
+// the segment's slope and intercept.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "luna_kernels.hpp"
+
+namespace luna {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) int i32x4;
+typedef __attribute__((ext_vector_type(2))) int i32x2;
+
+constexpr int kWave = 64;
+
+// Index of the calling wave within its workgroup, as a scalar (SGPR) value.
+// Matrix-core instructions execute for all 64 lanes whatever the EXEC mask is, so
+// every branch that guards one must be taken by the whole wave.  Deriving the wave
+// index through readfirstlane makes the compiler see it as uniform and emit scalar
+// branches instead of EXEC-masked ones; all wave-dependent control flow in these
+// kernels goes through this value.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+}
+
+// ---------------------------------------------------------------------------
+// piecewise-linear tables (layout shared with the host and luna_prepare.hip)
+// ---------------------------------------------------------------------------
+
+// LDS copy of one table, capacity fixed per kernel.
+template <int SEGCAP>
+struct alignas(16) PwlLds {
+  static_assert(SEGCAP % 2 == 0, "segment capacity must be even");
+  float tree[kTreeCap];
+  float2 seg[SEGCAP];
+  int depth;
+  float floor;  // 0 when outputs are clamped at zero, -inf otherwise
+};
+
+// Cooperative copy of a table from global memory into LDS.  Caller syncs after.
+template <int SEGCAP>
+__device__ inline void pwl_load(PwlLds<SEGCAP>& t, const uint8_t* __restrict__ gtab) {
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
+  const int ntree = 1 << hd.depth;
+  const int nseg = (hd.nbp + 1) * hd.L;
+  const float* gtree = reinterpret_cast<const float*>(gtab + kTabTree);
+  const float4* gseg = reinterpret_cast<const float4*>(gtab + kTabSeg);
+  for (int i = threadIdx.x; i < ntree; i += blockDim.x) t.tree[i] = gtree[i];
+  float4* sseg = reinterpret_cast<float4*>(t.seg);
+  for (int i = threadIdx.x; i < (nseg + 1) / 2; i += blockDim.x) sseg[i] = gseg[i];
+  if (threadIdx.x == 0) {
+    t.depth = hd.depth;
+    t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
+  }
+}
+
+// relu that propagates NaN like the listing's ReLU (fmaxf would drop it); one
+// v_maximum3_f32 on gfx950.
+__device__ __forceinline__ float relu_floor(float v, float floor) {
+  return __builtin_elementwise_maximum(v, floor);
+}
+
+// psi_l(u) for l = 0..L-1, already scaled by 1/sqrt(M) (folded into the table).
+template <int L, int SEGCAP>
+__device__ __forceinline__ void pwl_eval(const PwlLds<SEGCAP>& t, int depth, float floor, float u,
+                                         float (&y)[L]) {
+  unsigned idx = 1;
+  for (int s = 0; s < depth; ++s) idx = 2u * idx + (u > t.tree[idx] ? 1u : 0u);
+  const int seg = (int)(idx - (1u << depth));
+  if constexpr (L % 2 == 0) {
+    const float4* st = reinterpret_cast<const float4*>(t.seg + seg * L);
+#pragma unroll
+    for (int q = 0; q < L / 2; ++q) {
+      const float4 v = st[q];
+      y[2 * q] = relu_floor(fmaf(v.x, u, v.y), floor);
+      y[2 * q + 1] = relu_floor(fmaf(v.z, u, v.w), floor);
+    }
+  } else {
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      const float2 v = t.seg[seg * L + l];
+      y[l] = relu_floor(fmaf(v.x, u, v.y), floor);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// element types and fragments
+// ---------------------------------------------------------------------------
+template <typename T>
+struct Frag;
+
+template <>
+struct Frag<__bf16> {
+  bf16x8 v;
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (__bf16)0.0f;
+  }
+  __device__ __forceinline__ void fill(float x) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (__bf16)x;
+  }
+  __device__ __forceinline__ void set(int e, float x) { v[e] = (__bf16)x; }
+  __device__ __forceinline__ float get(int e) const { return (float)v[e]; }
+};
+
+template <>
+struct Frag<float> {
+  float v[8];
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+  }
+  __device__ __forceinline__ void fill(float x) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = x;
+  }
+  __device__ __forceinline__ void set(int e, float x) { v[e] = x; }
+  __device__ __forceinline__ float get(int e) const { return v[e]; }
+};
+
+__device__ __forceinline__ void mma(f32x4& c, const Frag<__bf16>& a, const Frag<__bf16>& b) {
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ void mma(f32x4& c, const Frag<float>& a, const Frag<float>& b) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[e], b.v[e], c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.0f, 0.0f, 0.0f, 0.0f}; }
+
+// 8 consecutive elements from memory (16 B for bf16, 32 B for fp32).
+__device__ __forceinline__ void load8(Frag<__bf16>& f, const __bf16* p) {
+  f.v = *reinterpret_cast<const bf16x8*>(p);
+}
+__device__ __forceinline__ void load8(Frag<float>& f, const float* p) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
+__device__ __forceinline__ void store8(__bf16* p, const Frag<__bf16>& f) {
+  *reinterpret_cast<bf16x8*>(p) = f.v;
+}
+__device__ __forceinline__ void store8(float* p, const Frag<float>& f) {
+  reinterpret_cast<float4*>(p)[0] = float4{f.v[0], f.v[1], f.v[2], f.v[3]};
+  reinterpret_cast<float4*>(p)[1] = float4{f.v[4], f.v[5], f.v[6], f.v[7]};
+}
+
+// 4 consecutive elements from fp32 values.
+__device__ __forceinline__ void store4(__bf16* p, float a, float b, float c, float d) {
+  bf16x4 v;
+  v[0] = (__bf16)a; v[1] = (__bf16)b; v[2] = (__bf16)c; v[3] = (__bf16)d;
+  *reinterpret_cast<bf16x4*>(p) = v;
+}
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = float4{a, b, c, d};
+}
+
+// Load 4 consecutive elements into slots e0..e0+3 of a fragment.
+__device__ __forceinline__ void load4(Frag<__bf16>& f, int e0, const __bf16* p) {
+  const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+  f.v[e0 + 0] = v[0]; f.v[e0 + 1] = v[1]; f.v[e0 + 2] = v[2]; f.v[e0 + 3] = v[3];
+}
+__device__ __forceinline__ void load4(Frag<float>& f, int e0, const float* p) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  f.v[e0 + 0] = v.x; f.v[e0 + 1] = v.y; f.v[e0 + 2] = v.z; f.v[e0 + 3] = v.w;
+}
+
+template <typename T>
+__device__ __forceinline__ T to_t(float x) { return (T)x; }
+
+// Elements of one 16-byte vector load.
+template <typename T>
+struct Vec16 {
+  static constexpr int N = 16 / (int)sizeof(T);
+};
+
+}  // namespace luna

@@ -1,0 +1,117 @@
+// luna_featuremap.hip -- phi(x) of eq. (phi-def) for every row of X.
+//
+// One wave handles 16 rows of one head.  The projections are computed transposed,
+// u^T = W X^T, on the matrix cores: A = W (row = projection, k = d), B = X^T
+// (column = row of X, k = d), so each lane ends up holding four projections
+// 16mb + 4g + j (j = 0..3) of the row r = lane % 16.  The channel functions are
+// evaluated in registers from the piecewise-linear table and the L outputs of each
+// (row, projection) are stored contiguously at feature i*L + l.
+#include "luna_device.hpp"
+#include "luna_kernels.hpp"
+
+namespace luna {
+
+template <typename Tin, typename Tout, int DH, int L>
+__global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
+  constexpr int KS = DH / 32;
+  __shared__ PwlLds<kSegCap> tab;
+
+  const int tiles_per_head = (int)((a.rows_per_head + 63) / 64);
+  const int64_t head = blockIdx.x / tiles_per_head;
+  const int tile = blockIdx.x - (int)(head * tiles_per_head);
+  const int hset = a.phi.per_head ? (int)(head % a.H) : 0;
+  pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+  __syncthreads();
+
+  const int wave = wave_id(), lane = threadIdx.x % kWave;
+  const int g = lane / 16, r = lane % 16;
+  const int64_t n = a.rows_per_head;
+  const int64_t t = (int64_t)tile * 64 + wave * 16 + r;  // this lane's row (B column)
+  const bool row_ok = t < n;
+  const int M = a.phi.M;
+  const int D = M * L;
+  const Tin* X = reinterpret_cast<const Tin*>(a.X) + (head * n + (row_ok ? t : 0)) * DH;
+  const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
+  const float* bias = a.phi.b + (size_t)hset * M;
+  Tout* out = reinterpret_cast<Tout*>(a.out) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
+  const int depth = tab.depth;
+  const float floor = tab.floor;
+
+  Frag<Tin> xf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (row_ok) load8(xf[ks], X + 32 * ks + 8 * g);
+    else xf[ks].zero();
+  }
+
+  const int MB = (M + 15) / 16;
+  for (int mb = 0; mb < MB; ++mb) {
+    const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
+    f32x4 acc = zero4();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      Frag<Tin> wf;
+      if (prow < M) load8(wf, W + (size_t)prow * DH + 32 * ks + 8 * g);
+      else wf.zero();
+      mma(acc, wf, xf[ks]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
+      if (i < M) {
+        const float u = acc[j] + bias[i];
+        float y[L];
+        pwl_eval<L>(tab, depth, floor, u, y);
+        if (row_ok) {
+          Tout* o = out + i * L;
+          if constexpr (L % 4 == 0) {
+#pragma unroll
+            for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
+          } else {
+#pragma unroll
+            for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
+          }
+        }
+      }
+    }
+  }
+}
+
+template <typename Tin, typename Tout, int DH>
+static hipError_t fm_dispatch_L(int L, const FeatureMapArgs& a, hipStream_t s) {
+  const int tiles = (int)((a.rows_per_head + 63) / 64);
+  const dim3 grid((unsigned)(a.heads * tiles)), block(256);
+  switch (L) {
+    case 1: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 4>), grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 8>), grid, block, 0, s, a); break;
+    case 16: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 16>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename Tin, typename Tout>
+static hipError_t fm_dispatch_d(int d, int L, const FeatureMapArgs& a, hipStream_t s) {
+  switch (d) {
+    case 32: return fm_dispatch_L<Tin, Tout, 32>(L, a, s);
+    case 64: return fm_dispatch_L<Tin, Tout, 64>(L, a, s);
+    case 128: return fm_dispatch_L<Tin, Tout, 128>(L, a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+bool featuremap_supported(Dt, int d, int L, int M) {
+  const bool dok = d == 32 || d == 64 || d == 128;
+  const bool lok = L == 1 || L == 2 || L == 4 || L == 8 || L == 16;
+  return dok && lok && M >= 1 && M <= 64;
+}
+
+hipError_t launch_featuremap(Dt in_dt, Dt out_dt, int d, int L, const FeatureMapArgs& a, hipStream_t s) {
+  if (in_dt == Dt::BF16)
+    return out_dt == Dt::BF16 ? fm_dispatch_d<__bf16, __bf16>(d, L, a, s) : fm_dispatch_d<__bf16, float>(d, L, a, s);
+  return out_dt == Dt::BF16 ? fm_dispatch_d<float, __bf16>(d, L, a, s) : fm_dispatch_d<float, float>(d, L, a, s);
+}
+
+}  // namespace luna

@@ -1,0 +1,109 @@
+// luna_kernels.hpp -- interface between the host API (luna_api.cpp) and the kernels.
+// Internal: not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace luna {
+
+// piecewise-linear tables of the channel MLPs (built by luna_prepare.hip)
+constexpr int kTreeCap = 1024;          // heap-ordered breakpoints, indices 1..1023
+constexpr int kSegCap = 5120;           // (slope, intercept) pairs, segment-major
+constexpr int kMaxUnits = kTreeCap - 1; // breakpoints one table can hold
+constexpr size_t kTabHeader = 0;
+constexpr size_t kTabTree = 256;
+constexpr size_t kTabSeg = kTabTree + kTreeCap * 4;
+constexpr size_t kTableBytes = kTabSeg + (size_t)kSegCap * 8;  // 45312, a multiple of 256
+
+struct PwlHeader {
+  int nbp;     // number of breakpoints
+  int depth;   // search steps: smallest D with 2^D - 1 >= nbp
+  int L;       // channels
+  int nonneg;  // 1: relu on the channel outputs
+};
+
+enum class Dt : int { F32 = 0, BF16 = 1 };
+
+// Build the piecewise-linear tables of the channel MLPs (one per parameter set).
+struct PrepareArgs {
+  const float* fc1_w;  // [P][C1][hidden]
+  const float* fc1_b;  // [P][C1][hidden]
+  const float* fc2_w;  // [P][L][hidden]
+  const float* fc2_b;  // [P][L]
+  int P, C1, L, hidden, M, nonneg;
+  uint8_t* tables;     // [P][kTableBytes]
+  int* zero_ptr;       // words cleared by the prepare kernel (may be null)
+  int zero_count;
+};
+
+// Projection and channel-MLP parameters as the kernels see them.
+struct PhiArgs {
+  const void* W;        // [P][M][d], element type of the call
+  const float* b;       // [P][M]
+  const uint8_t* tables;
+  int M;
+  int per_head;         // parameter set = per_head ? h : 0
+};
+
+struct FeatureMapArgs {
+  const void* X;
+  void* out;
+  PhiArgs phi;
+  int64_t rows_per_head;  // n
+  int H;
+  int64_t heads;          // B * H
+};
+
+struct NoncausalArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* out;
+  PhiArgs phi;
+  int n, H, heads;
+  int splits;           // token ranges per head in the state pass
+  int tokens_per_split; // multiple of 32
+  float eps;
+  float* partial;       // [heads][splits][DP][DH + 1] fp32
+  void* frags;          // [heads][frag_elems] statistics as readout fragments (call dtype)
+  int tile_tokens;      // tokens per readout workgroup (multiple of 16)
+  int tiles;            // ceil(n / tile_tokens)
+};
+
+struct CausalArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  void* out;
+  PhiArgs phi;
+  int n, H, heads;
+  int dv_tiles;  // value-column tiles per head
+  float eps;
+};
+
+// Launchers; each returns hipSuccess or the launch error.  `ok` reports whether
+// a kernel exists for the (dtype, d, L, M) combination.
+hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s);
+
+bool featuremap_supported(Dt dt, int d, int L, int M);
+hipError_t launch_featuremap(Dt in_dt, Dt out_dt, int d, int L, const FeatureMapArgs& a, hipStream_t s);
+
+struct NoncausalPlan {
+  int DP;          // padded feature rows of S (16 * MB * L)
+  int NF;          // readout fragments along the feature dimension
+  size_t frag_elems;  // per-head elements of the statistics fragments
+};
+bool noncausal_supported(Dt dt, int d, int L, int M, NoncausalPlan* plan);
+hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s);
+
+bool causal_supported(Dt dt, int d, int L, int M, int* dv_tiles);
+hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s);
+
+// Segment-table capacity of the attention kernels for a given L (pairs).
+constexpr int attn_seg_cap(int L) {
+  return ((64 * L + 1) * L + 1) / 2 * 2 < 4112 ? ((64 * L + 1) * L + 1) / 2 * 2 : 4112;
+}
+
+}  // namespace luna

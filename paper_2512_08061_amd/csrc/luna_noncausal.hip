@@ -1,0 +1,406 @@
+// luna_noncausal.hip -- non-causal LUNA attention, eq. (kernel-attn).
+//
+// Three passes after the table build:
+//
+//  state    one workgroup per (head, token range).  Each wave takes 32-token steps:
+//           u = K W^T on the matrix cores (A = K rows, B = W^T), so a lane holds
+//           projection 16mb + r for eight tokens; psi turns each of those into L
+//           operand fragments "feature (mb, l, r) x 8 tokens".  S += phi(K)^T V and
+//           z += phi(K)^T 1 accumulate in fp32 matrix-core accumulators, with V read
+//           transposed from LDS.  The four waves are summed in LDS in a fixed order
+//           and the range's partial (S | z) is written in fp32.
+//  reduce   one workgroup per head sums the partials in range order (deterministic)
+//           and writes S and z as readout operand fragments in the call's dtype.
+//  readout  one workgroup per (head, 256-token tile).  u^T = W Q^T puts four
+//           projections of one token in each lane, so psi's outputs are directly the
+//           B fragments of num^T = S^T phi(Q)^T and den = z^T phi(Q)^T; the statistics
+//           stay in registers for the whole tile.  out = num * (1 / (den + eps)).
+//
+// Feature order.  The state pass produces rows (mb, l, i16) ("projection-block,
+// channel, projection"); the readout consumes "k-order": fragment kappa, lane group
+// g, slot e stands for list position p = 8 kappa + e of (mb*4 + j)*L + l, i.e.
+// projection 16mb + 4g + j and channel l (zero beyond 4*MB*L).  The reduce pass
+// permutes between the two.
+#include "luna_device.hpp"
+#include "luna_kernels.hpp"
+
+namespace luna {
+
+template <typename T, int DH, int L, int MB>
+struct NcCfg {
+  static constexpr int KS = DH / 32;                 // k-steps over the head dimension
+  static constexpr int CB = DH / 16;                 // value-column blocks
+  static constexpr int NF = (4 * MB * L + 7) / 8;    // readout fragments along features
+  static constexpr int DP = 16 * MB * L;             // state rows (mb, l, i16)
+  static constexpr int SEGCAP = attn_seg_cap(L);
+  static constexpr int VE = 16 / (int)sizeof(T);     // elements per 16-byte load
+  static constexpr int VROW = 36;                    // V^T row length in LDS (padded, 16-B multiple for fp32)
+  static constexpr int NVC = 32 * (DH / VE) / kWave; // V 16-byte chunks per lane per step
+  static constexpr size_t FRAG_ELEMS = (size_t)(CB + 1) * NF * kWave * 8;
+};
+
+// ---------------------------------------------------------------------------
+// state pass
+// ---------------------------------------------------------------------------
+template <typename T, int DH, int L, int MB>
+__global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
+  using C = NcCfg<T, DH, L, MB>;
+  __shared__ PwlLds<C::SEGCAP> tab;
+  __shared__ __attribute__((aligned(16))) T vt[4][DH][C::VROW];
+  __shared__ float red[C::DP][DH + 1];
+
+  const int head = blockIdx.x / a.splits;
+  const int split = blockIdx.x - head * a.splits;
+  const int hset = a.phi.per_head ? head % a.H : 0;
+  pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+
+  const int wave = wave_id(), lane = threadIdx.x % kWave;
+  const int g = lane / 16, r = lane % 16;
+  const int M = a.phi.M;
+  const size_t hoff = (size_t)head * a.n * DH;
+  const T* K = reinterpret_cast<const T*>(a.K) + hoff;
+  const T* V = reinterpret_cast<const T*>(a.V) + hoff;
+  const T* W = reinterpret_cast<const T*>(a.phi.W) + (size_t)hset * M * DH;
+  const float* bias = a.phi.b + (size_t)hset * M;
+
+  // B operand of u = K W^T: column r of block mb is projection 16mb + r.
+  Frag<T> wf[MB][C::KS];
+  float bcol[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int p = 16 * mb + r;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (p < M) load8(wf[mb][ks], W + (size_t)p * DH + 32 * ks + 8 * g);
+      else wf[mb][ks].zero();
+    }
+    bcol[mb] = p < M ? bias[p] : 0.0f;
+  }
+  Frag<T> ones;
+  ones.fill(1.0f);
+
+  f32x4 accS[MB][L][C::CB];
+  f32x4 accZ[MB][L];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      accZ[mb][l] = zero4();
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb) accS[mb][l][cb] = zero4();
+    }
+
+  const int t_begin = split * a.tokens_per_split;
+  const int t_end = min(a.n, t_begin + a.tokens_per_split);
+  const int nsteps = (t_end - t_begin + 31) / 32;
+  const int iters = (nsteps + 3) / 4;
+
+  // registers holding the next step's K fragments and V chunks
+  Frag<T> kn[2][C::KS];
+  i32x4 vn[C::NVC];
+  auto fetch = [&](int it) {
+    const int t0 = t_begin + (it * 4 + wave) * 32;
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int t = t0 + 16 * tb + r;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        if (t < t_end) load8(kn[tb][ks], K + (size_t)t * DH + 32 * ks + 8 * g);
+        else kn[tb][ks].zero();
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < C::NVC; ++q) {
+      const int c = lane + kWave * q;
+      const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
+      const int t = t0 + tt;
+      if (t < t_end) vn[q] = *reinterpret_cast<const i32x4*>(V + (size_t)t * DH + cg * C::VE);
+      else vn[q] = i32x4{0, 0, 0, 0};
+    }
+  };
+
+  __syncthreads();
+  const int tdepth = tab.depth;
+  const float tfloor = tab.floor;
+
+  if (iters > 0) fetch(0);
+  for (int it = 0; it < iters; ++it) {
+    const int t0 = t_begin + (it * 4 + wave) * 32;
+    // V^T of this step into the wave's LDS slice
+#pragma unroll
+    for (int q = 0; q < C::NVC; ++q) {
+      const int c = lane + kWave * q;
+      const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
+      const T* e = reinterpret_cast<const T*>(&vn[q]);
+#pragma unroll
+      for (int x = 0; x < C::VE; ++x) vt[wave][cg * C::VE + x][tt] = e[x];
+    }
+    Frag<T> kc[2][C::KS];
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) kc[tb][ks] = kn[tb][ks];
+    if (it + 1 < iters) fetch(it + 1);
+    __syncthreads();
+
+    // projections and channel functions -> A fragments phi(K)^T
+    Frag<T> af[MB][L];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const bool pok = 16 * mb + r < M;
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int ks = 0; ks < C::KS; ++ks) mma(acc, kc[tb][ks], wf[mb][ks]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const bool ok = pok && (t0 + 16 * tb + 4 * g + j < t_end);
+          float y[L];
+          pwl_eval<L>(tab, tdepth, tfloor, acc[j] + bcol[mb], y);
+#pragma unroll
+          for (int l = 0; l < L; ++l) af[mb][l].set(4 * tb + j, ok ? y[l] : 0.0f);
+        }
+      }
+    }
+    // S += phi(K)^T V, z += phi(K)^T 1
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb) {
+      Frag<T> bv;
+      load4(bv, 0, &vt[wave][16 * cb + r][4 * g]);
+      load4(bv, 4, &vt[wave][16 * cb + r][16 + 4 * g]);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int l = 0; l < L; ++l) mma(accS[mb][l][cb], af[mb][l], bv);
+    }
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int l = 0; l < L; ++l) mma(accZ[mb][l], af[mb][l], ones);
+    __syncthreads();
+  }
+
+  // sum the four waves in a fixed order
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int l = 0; l < L; ++l)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int row = (mb * L + l) * 16 + 4 * g + j;
+#pragma unroll
+            for (int cb = 0; cb < C::CB; ++cb) {
+              float& d = red[row][16 * cb + r];
+              d = (w == 0) ? accS[mb][l][cb][j] : d + accS[mb][l][cb][j];
+            }
+            if (r == 0) {
+              float& d = red[row][DH];
+              d = (w == 0) ? accZ[mb][l][j] : d + accZ[mb][l][j];
+            }
+          }
+    }
+    __syncthreads();
+  }
+  float* part = a.partial + ((size_t)head * a.splits + split) * C::DP * (DH + 1);
+  const float* src = &red[0][0];
+  for (int i = threadIdx.x; i < C::DP * (DH + 1); i += blockDim.x) part[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// reduce pass: partials -> readout fragments
+// ---------------------------------------------------------------------------
+template <typename T, int DH, int L, int MB>
+__global__ __launch_bounds__(256) void nc_reduce_kernel(NoncausalArgs a) {
+  using C = NcCfg<T, DH, L, MB>;
+  __shared__ float red[C::DP * (DH + 1)];
+  const int head = blockIdx.x;
+  const float* part = a.partial + (size_t)head * a.splits * C::DP * (DH + 1);
+  for (int i = threadIdx.x; i < C::DP * (DH + 1); i += blockDim.x) {
+    float s = 0.0f;
+    for (int sp = 0; sp < a.splits; ++sp) s += part[(size_t)sp * C::DP * (DH + 1) + i];
+    red[i] = s;
+  }
+  __syncthreads();
+  T* fr = reinterpret_cast<T*>(a.frags) + (size_t)head * C::FRAG_ELEMS;
+  // fragment (cb, kappa), lane (g, r), slot e; cb == CB holds z
+  for (size_t idx = threadIdx.x; idx < C::FRAG_ELEMS; idx += blockDim.x) {
+    const int e = (int)(idx % 8);
+    const int lane = (int)((idx / 8) % kWave);
+    const int kappa = (int)((idx / (8 * kWave)) % C::NF);
+    const int cb = (int)(idx / (8 * kWave * C::NF));
+    const int g = lane / 16, r = lane % 16;
+    const int p = 8 * kappa + e;
+    float v = 0.0f;
+    if (p < 4 * MB * L) {
+      const int mbj = p / L, l = p % L;
+      const int mb = mbj / 4, j = mbj % 4;
+      const int row = (mb * L + l) * 16 + 4 * g + j;
+      v = (cb < C::CB) ? red[row * (DH + 1) + 16 * cb + r] : red[row * (DH + 1) + DH];
+    }
+    fr[idx] = (T)v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// readout pass
+// ---------------------------------------------------------------------------
+template <typename T, int DH, int L, int MB>
+__global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
+  using C = NcCfg<T, DH, L, MB>;
+  __shared__ PwlLds<C::SEGCAP> tab;
+  const int head = blockIdx.x / a.tiles;
+  const int tile = blockIdx.x - head * a.tiles;
+  const int hset = a.phi.per_head ? head % a.H : 0;
+  pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+
+  const int wave = wave_id(), lane = threadIdx.x % kWave;
+  const int g = lane / 16, r = lane % 16;
+  const int M = a.phi.M;
+  const size_t hoff = (size_t)head * a.n * DH;
+  const T* Q = reinterpret_cast<const T*>(a.Q) + hoff;
+  T* out = reinterpret_cast<T*>(a.out) + hoff;
+  const T* W = reinterpret_cast<const T*>(a.phi.W) + (size_t)hset * M * DH;
+  const float* bias = a.phi.b + (size_t)hset * M;
+  const T* fr = reinterpret_cast<const T*>(a.frags) + (size_t)head * C::FRAG_ELEMS;
+
+  Frag<T> sf[C::CB][C::NF], zf[C::NF];
+#pragma unroll
+  for (int cb = 0; cb < C::CB; ++cb)
+#pragma unroll
+    for (int k = 0; k < C::NF; ++k) load8(sf[cb][k], fr + ((size_t)(cb * C::NF + k) * kWave + lane) * 8);
+#pragma unroll
+  for (int k = 0; k < C::NF; ++k) load8(zf[k], fr + ((size_t)(C::CB * C::NF + k) * kWave + lane) * 8);
+
+  // A operand of u^T = W Q^T: row r of block mb is projection 16mb + r.
+  Frag<T> wf[MB][C::KS];
+  float brow[MB][4];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int p = 16 * mb + r;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (p < M) load8(wf[mb][ks], W + (size_t)p * DH + 32 * ks + 8 * g);
+      else wf[mb][ks].zero();
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 16 * mb + 4 * g + j;
+      brow[mb][j] = i < M ? bias[i] : 0.0f;
+    }
+  }
+  __syncthreads();
+  const int tdepth = tab.depth;
+  const float tfloor = tab.floor;
+
+  const int nblk = a.tile_tokens / 16;
+  for (int blk = wave; blk < nblk; blk += 4) {
+    const int t = tile * a.tile_tokens + blk * 16 + r;
+    const bool ok = t < a.n;
+    Frag<T> qf[C::KS];
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (ok) load8(qf[ks], Q + (size_t)t * DH + 32 * ks + 8 * g);
+      else qf[ks].zero();
+    }
+    Frag<T> pq[C::NF];
+#pragma unroll
+    for (int k = 0; k < C::NF; ++k) pq[k].zero();
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) mma(acc, wf[mb][ks], qf[ks]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool pok = 16 * mb + 4 * g + j < M;
+        float y[L];
+        pwl_eval<L>(tab, tdepth, tfloor, acc[j] + brow[mb][j], y);
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          const int p = (mb * 4 + j) * L + l;
+          pq[p / 8].set(p % 8, pok ? y[l] : 0.0f);
+        }
+      }
+    }
+    f32x4 num[C::CB], den = zero4();
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb) num[cb] = zero4();
+#pragma unroll
+    for (int k = 0; k < C::NF; ++k) {
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb) mma(num[cb], sf[cb][k], pq[k]);
+      mma(den, zf[k], pq[k]);
+    }
+    if (ok) {
+      const float rinv = 1.0f / (den[0] + a.eps);
+      T* o = out + (size_t)t * DH + 4 * g;
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb)
+        store4(o + 16 * cb, num[cb][0] * rinv, num[cb][1] * rinv, num[cb][2] * rinv, num[cb][3] * rinv);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dispatch
+// ---------------------------------------------------------------------------
+template <typename T, int DH, int L, int MB>
+static hipError_t nc_run(const NoncausalArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((nc_state_kernel<T, DH, L, MB>), dim3(a.heads * a.splits), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((nc_reduce_kernel<T, DH, L, MB>), dim3(a.heads), dim3(256), 0, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((nc_readout_kernel<T, DH, L, MB>), dim3(a.heads * a.tiles), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T, int DH, int L, int MB>
+static void nc_plan(NoncausalPlan* p) {
+  using C = NcCfg<T, DH, L, MB>;
+  p->DP = C::DP;
+  p->NF = C::NF;
+  p->frag_elems = C::FRAG_ELEMS;
+}
+
+// (dtype, d, L, projection blocks) combinations that are built.
+#define LUNA_NC_CASES(X)   \
+  X(float, 32, 8, 1)       \
+  X(float, 32, 2, 1)       \
+  X(float, 64, 8, 1)       \
+  X(__bf16, 32, 8, 1)      \
+  X(__bf16, 64, 8, 1)      \
+  X(__bf16, 64, 8, 2)      \
+  X(__bf16, 64, 4, 1)      \
+  X(__bf16, 64, 1, 4)      \
+  X(__bf16, 128, 8, 1)
+
+template <typename T>
+static constexpr Dt dt_of() { return sizeof(T) == 2 ? Dt::BF16 : Dt::F32; }
+
+bool noncausal_supported(Dt dt, int d, int L, int M, NoncausalPlan* plan) {
+  const int MB = (M + 15) / 16;
+#define X(T_, D_, L_, MB_)                                              \
+  if (dt == dt_of<T_>() && d == D_ && L == L_ && MB == MB_) {           \
+    if (plan) nc_plan<T_, D_, L_, MB_>(plan);                           \
+    return true;                                                        \
+  }
+  LUNA_NC_CASES(X)
+#undef X
+  return false;
+}
+
+hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s) {
+  const int MB = (M + 15) / 16;
+#define X(T_, D_, L_, MB_) \
+  if (dt == dt_of<T_>() && d == D_ && L == L_ && MB == MB_) return nc_run<T_, D_, L_, MB_>(a, s);
+  LUNA_NC_CASES(X)
+#undef X
+  return hipErrorInvalidValue;
+}
+
+}  // namespace luna

@@ -1,0 +1,256 @@
+"""Python binding of libluna.so (ctypes), argument marshalling only.
+
+Every function here checks shapes and dtypes, allocates the outputs and the
+workspace with torch on the tensors' device, and calls the C entry point of the
+same name on the current torch stream.  All arithmetic runs in the HIP kernels of
+libluna.so; there is no other code path.  If the library is missing the calls
+raise instead of computing anything.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libluna.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "luna.h")
+
+LUNA_OK, LUNA_ERR_INVALID_ARG, LUNA_ERR_UNSUPPORTED, LUNA_ERR_WORKSPACE, LUNA_ERR_HIP = range(5)
+LUNA_F32, LUNA_BF16 = 0, 1
+OP_FEATUREMAP, OP_ATTN, OP_ATTN_CAUSAL = 0, 1, 2
+
+
+class LunaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+class PhiParamsC(ctypes.Structure):
+    _fields_ = [
+        ("M", ctypes.c_int32), ("L", ctypes.c_int32), ("hidden", ctypes.c_int32),
+        ("shared_channels", ctypes.c_int32), ("nonneg", ctypes.c_int32), ("per_head", ctypes.c_int32),
+        ("W", ctypes.c_void_p), ("b", ctypes.c_void_p),
+        ("fc1_w", ctypes.c_void_p), ("fc1_b", ctypes.c_void_p),
+        ("fc2_w", ctypes.c_void_p), ("fc2_b", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libluna.so (raises LunaError if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise LunaError(LUNA_ERR_HIP, f"{path} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(PhiParamsC)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.luna_workspace_bytes.argtypes = [i32, i32, i64, i64, i64, i64, P, i32]
+    lib.luna_workspace_bytes.restype = sz
+    lib.luna_featuremap.argtypes = [vp, i32, i64, i64, i64, i64, P, vp, i32, vp, sz, vp]
+    lib.luna_featuremap.restype = i32
+    lib.luna_attn_fwd.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, vp, vp, sz, vp]
+    lib.luna_attn_fwd.restype = i32
+    lib.luna_attn_fwd_causal.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float, vp, vp,
+                                         sz, vp]
+    lib.luna_attn_fwd_causal.restype = i32
+    lib.luna_status_string.argtypes = [i32]
+    lib.luna_status_string.restype = ctypes.c_char_p
+    lib.luna_last_error.argtypes = []
+    lib.luna_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def header_functions(path: str = HEADER) -> list[str]:
+    """Names of the functions include/luna.h declares."""
+    txt = open(path).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(luna_[a-z_]+)\s*\(", txt)))
+
+
+def _check(status: int) -> None:
+    if status != LUNA_OK:
+        lib = load_library()
+        raise LunaError(status, f"{lib.luna_status_string(status).decode()}: {lib.luna_last_error().decode()}")
+
+
+# ---------------------------------------------------------------------------
+# torch-facing helpers
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dt(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return LUNA_BF16
+    if t.dtype == torch.float32:
+        return LUNA_F32
+    raise LunaError(LUNA_ERR_INVALID_ARG, f"unsupported dtype {t.dtype}")
+
+
+class PhiParams:
+    """Device-resident feature-map parameters (see luna_phi_params in include/luna.h)."""
+
+    def __init__(self, W, b, fc1_w, fc1_b, fc2_w, fc2_b, M, L, hidden, shared_channels=False, nonneg=True,
+                 per_head=False):
+        self.W, self.b, self.fc1_w, self.fc1_b, self.fc2_w, self.fc2_b = W, b, fc1_w, fc1_b, fc2_w, fc2_b
+        self.M, self.L, self.hidden = int(M), int(L), int(hidden)
+        self.shared_channels, self.nonneg, self.per_head = bool(shared_channels), bool(nonneg), bool(per_head)
+        for name in ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b"):
+            t = getattr(self, name)
+            if not t.is_contiguous():
+                raise LunaError(LUNA_ERR_INVALID_ARG, f"{name} must be contiguous")
+        torch = _torch()
+        for name in ("b", "fc1_w", "fc1_b", "fc2_w", "fc2_b"):
+            if getattr(self, name).dtype != torch.float32:
+                raise LunaError(LUNA_ERR_INVALID_ARG, f"{name} must be float32")
+
+    @classmethod
+    def from_arrays(cls, p: dict, device, dtype):
+        """Upload a parameter dict (NumPy arrays + scalars, as the workload generator returns)."""
+        torch = _torch()
+        f32 = lambda x: torch.as_tensor(x, dtype=torch.float32).contiguous().to(device)  # noqa: E731
+        W = torch.as_tensor(p["W"], dtype=torch.float32).to(dtype).contiguous().to(device)
+        return cls(W, f32(p["b"]), f32(p["fc1_w"]), f32(p["fc1_b"]), f32(p["fc2_w"]), f32(p["fc2_b"]),
+                   p["M"], p["L"], p["hidden"], p.get("shared_channels", False), p.get("nonneg", True),
+                   p.get("per_head", False))
+
+    def c(self) -> PhiParamsC:
+        return PhiParamsC(self.M, self.L, self.hidden, int(self.shared_channels), int(self.nonneg),
+                          int(self.per_head), self.W.data_ptr(), self.b.data_ptr(), self.fc1_w.data_ptr(),
+                          self.fc1_b.data_ptr(), self.fc2_w.data_ptr(), self.fc2_b.data_ptr())
+
+
+def workspace_bytes(op: int, dtype: int, B: int, H: int, n: int, d: int, p: PhiParams | PhiParamsC,
+                    chunk: int = 64) -> int:
+    lib = load_library()
+    pc = p.c() if isinstance(p, PhiParams) else p
+    return int(lib.luna_workspace_bytes(op, dtype, B, H, n, d, ctypes.byref(pc), chunk))
+
+
+def _workspace(nbytes: int, device):
+    torch = _torch()
+    ws = torch.empty(max(nbytes, 256) + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws, ws.data_ptr() + off, max(nbytes, 256)
+
+
+def _stream_ptr(device) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _qkv_shape(*ts):
+    B, H, n, d = ts[0].shape
+    for t in ts:
+        if tuple(t.shape) != (B, H, n, d) or not t.is_contiguous() or t.dtype != ts[0].dtype:
+            raise LunaError(LUNA_ERR_INVALID_ARG, "Q, K, V must be contiguous [B, H, n, d] of one dtype")
+    return B, H, n, d
+
+
+def featuremap(X, p: PhiParams, out_dtype=None):
+    """phi(X) for X [B, H, n, d]; returns [B, H, n, M*L] (feature i*L + l)."""
+    torch = _torch()
+    lib = load_library()
+    if X.dim() != 4 or not X.is_contiguous():
+        raise LunaError(LUNA_ERR_INVALID_ARG, "X must be a contiguous [B, H, n, d] tensor")
+    B, H, n, d = X.shape
+    out_dtype = X.dtype if out_dtype is None else out_dtype
+    out = torch.empty((B, H, n, p.M * p.L), dtype=out_dtype, device=X.device)
+    pc = p.c()
+    dt = _dt(X)
+    nb = lib.luna_workspace_bytes(OP_FEATUREMAP, dt, B, H, n, d, ctypes.byref(pc), 64)
+    if nb == 0:
+        _check(lib.luna_featuremap(X.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), out.data_ptr(), _dt(out),
+                                   None, 0, None))
+    ws, wsp, wsn = _workspace(nb, X.device)
+    _check(lib.luna_featuremap(X.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), out.data_ptr(), _dt(out), wsp, wsn,
+                               _stream_ptr(X.device)))
+    out._luna_ws = ws  # keep the workspace alive until the output is
+    return out
+
+
+def attn_fwd(Q, K, V, p: PhiParams, eps: float = 1e-6, out=None):
+    """Non-causal LUNA attention; returns out [B, H, n, d] in Q's dtype."""
+    torch = _torch()
+    lib = load_library()
+    B, H, n, d = _qkv_shape(Q, K, V)
+    out = torch.empty_like(Q) if out is None else out
+    pc = p.c()
+    dt = _dt(Q)
+    nb = lib.luna_workspace_bytes(OP_ATTN, dt, B, H, n, d, ctypes.byref(pc), 64)
+    if nb == 0:
+        _check(lib.luna_attn_fwd(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), eps,
+                                 out.data_ptr(), None, 0, None))
+    ws, wsp, wsn = _workspace(nb, Q.device)
+    _check(lib.luna_attn_fwd(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), eps,
+                             out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
+    out._luna_ws = ws
+    return out
+
+
+def attn_fwd_causal(Q, K, V, p: PhiParams, chunk: int = 64, eps: float = 1e-6, out=None):
+    """Causal LUNA attention (chunked prefix scan); returns out [B, H, n, d]."""
+    torch = _torch()
+    lib = load_library()
+    B, H, n, d = _qkv_shape(Q, K, V)
+    out = torch.empty_like(Q) if out is None else out
+    pc = p.c()
+    dt = _dt(Q)
+    nb = lib.luna_workspace_bytes(OP_ATTN_CAUSAL, dt, B, H, n, d, ctypes.byref(pc), chunk)
+    if nb == 0:
+        _check(lib.luna_attn_fwd_causal(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc),
+                                        chunk, eps, out.data_ptr(), None, 0, None))
+    ws, wsp, wsn = _workspace(nb, Q.device)
+    _check(lib.luna_attn_fwd_causal(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc),
+                                    chunk, eps, out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
+    out._luna_ws = ws
+    return out
+
+
+class Plan:
+    """A reusable call: output, workspace and the C parameter struct allocated once.
+
+    ``run()`` only enqueues the kernels (for timing loops and graph capture).
+    """
+
+    def __init__(self, op: int, Q, K, V, p: PhiParams, eps: float = 1e-6, chunk: int = 64):
+        torch = _torch()
+        self.lib = load_library()
+        self.op, self.Q, self.K, self.V, self.p = op, Q, K, V, p
+        self.B, self.H, self.n, self.d = _qkv_shape(Q, K, V)
+        self.dt = _dt(Q)
+        self.eps, self.chunk = float(eps), int(chunk)
+        self.pc = p.c()
+        self.out = torch.empty_like(Q)
+        nb = self.lib.luna_workspace_bytes(op, self.dt, self.B, self.H, self.n, self.d, ctypes.byref(self.pc), chunk)
+        if nb == 0:
+            self._call(None, 0, None)  # raises with the reason
+        self.ws, self.wsp, self.wsn = _workspace(nb, Q.device)
+        self.ws_bytes = nb
+
+    def _call(self, wsp, wsn, stream):
+        q, k, v, o = self.Q.data_ptr(), self.K.data_ptr(), self.V.data_ptr(), self.out.data_ptr()
+        if self.op == OP_ATTN:
+            st = self.lib.luna_attn_fwd(q, k, v, self.dt, self.B, self.H, self.n, self.d, ctypes.byref(self.pc),
+                                        self.eps, o, wsp, wsn, stream)
+        else:
+            st = self.lib.luna_attn_fwd_causal(q, k, v, self.dt, self.B, self.H, self.n, self.d,
+                                               ctypes.byref(self.pc), self.chunk, self.eps, o, wsp, wsn, stream)
+        _check(st)
+
+    def run(self, stream=None):
+        s = stream if stream is not None else _stream_ptr(self.Q.device)
+        self._call(self.wsp, self.wsn, s)
+        return self.out

@@ -1,0 +1,104 @@
+"""The C ABI without a GPU: the library loads, exports what include/luna.h declares,
+and rejects bad arguments on the host with the documented status codes."""
+import ctypes
+
+import pytest
+
+from paper_2512_08061_amd import luna
+
+FAKE = 0x10000  # non-null pointer value; validation never dereferences it
+
+
+def _params(M=16, L=8, hidden=64, shared=0, nonneg=1, per_head=0, nullW=False):
+    return luna.PhiParamsC(M, L, hidden, shared, nonneg, per_head, 0 if nullW else FAKE, FAKE, FAKE, FAKE, FAKE,
+                           FAKE)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return luna.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = luna.header_functions()
+    assert set(names) == {"luna_workspace_bytes", "luna_featuremap", "luna_attn_fwd", "luna_attn_fwd_causal",
+                          "luna_status_string", "luna_last_error"}
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.luna_status_string(s)
+    assert lib.luna_status_string(99) == b"unknown status"
+
+
+def _attn(lib, B=2, H=3, n=100, d=64, p=None, eps=1e-6, ws=FAKE, ws_bytes=1 << 40, q=FAKE, dt=luna.LUNA_BF16):
+    p = p or _params()
+    return lib.luna_attn_fwd(q, FAKE, FAKE, dt, B, H, n, d, ctypes.byref(p), eps, FAKE, ws, ws_bytes, None)
+
+
+def _causal(lib, chunk=64, d=128, M=32, dt=luna.LUNA_BF16, **kw):
+    p = _params(M=M)
+    return lib.luna_attn_fwd_causal(FAKE, FAKE, FAKE, dt, 1, 1, 100, d, ctypes.byref(p), chunk, 1e-6, FAKE,
+                                    FAKE, 1 << 40, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=0), luna.LUNA_ERR_INVALID_ARG),
+    (dict(B=0), luna.LUNA_ERR_INVALID_ARG),
+    (dict(d=48), luna.LUNA_ERR_UNSUPPORTED),
+    (dict(q=0), luna.LUNA_ERR_INVALID_ARG),
+    (dict(eps=-1.0), luna.LUNA_ERR_INVALID_ARG),
+    (dict(eps=float("nan")), luna.LUNA_ERR_INVALID_ARG),
+    (dict(ws_bytes=1024), luna.LUNA_ERR_WORKSPACE),
+    (dict(ws=FAKE + 8), luna.LUNA_ERR_INVALID_ARG),
+    (dict(p=_params(M=0)), luna.LUNA_ERR_INVALID_ARG),
+    (dict(p=_params(M=32, L=16)), luna.LUNA_ERR_INVALID_ARG),
+    (dict(p=_params(hidden=65)), luna.LUNA_ERR_INVALID_ARG),
+    (dict(p=_params(nonneg=2)), luna.LUNA_ERR_INVALID_ARG),
+    (dict(p=_params(nullW=True)), luna.LUNA_ERR_INVALID_ARG),
+    (dict(p=_params(L=16, hidden=64)), luna.LUNA_ERR_UNSUPPORTED),
+    (dict(dt=7), luna.LUNA_ERR_INVALID_ARG),
+])
+def test_noncausal_rejects(lib, kw, status):
+    assert _attn(lib, **kw) == status
+    assert lib.luna_last_error()  # a reason is recorded
+
+
+def test_causal_rejects_chunk(lib):
+    assert _causal(lib, chunk=32) == luna.LUNA_ERR_UNSUPPORTED
+    assert b"chunk" in lib.luna_last_error()
+
+
+def test_featuremap_rejects(lib):
+    p = _params()
+    assert lib.luna_featuremap(FAKE, luna.LUNA_BF16, 1, 1, 10, 64, ctypes.byref(p), FAKE, 5, FAKE, 1 << 40,
+                               None) == luna.LUNA_ERR_INVALID_ARG
+    assert lib.luna_featuremap(0, luna.LUNA_BF16, 1, 1, 10, 64, ctypes.byref(p), FAKE, luna.LUNA_BF16, FAKE,
+                               1 << 40, None) == luna.LUNA_ERR_INVALID_ARG
+    p3 = _params(L=3)
+    assert lib.luna_featuremap(FAKE, luna.LUNA_BF16, 1, 1, 10, 64, ctypes.byref(p3), FAKE, luna.LUNA_BF16, FAKE,
+                               1 << 40, None) == luna.LUNA_ERR_UNSUPPORTED
+
+
+def test_workspace_sizes(lib):
+    # the five measured problems all have kernels and finite workspaces
+    for (dt, B, H, n, d, M, op) in [(luna.LUNA_F32, 1, 1, 256, 32, 8, luna.OP_ATTN),
+                                    (luna.LUNA_BF16, 32, 12, 512, 64, 8, luna.OP_ATTN),
+                                    (luna.LUNA_BF16, 64, 12, 197, 64, 16, luna.OP_ATTN),
+                                    (luna.LUNA_BF16, 32, 8, 4096, 64, 16, luna.OP_ATTN),
+                                    (luna.LUNA_BF16, 8, 16, 16384, 128, 32, luna.OP_ATTN_CAUSAL)]:
+        p = _params(M=M)
+        nb = lib.luna_workspace_bytes(op, dt, B, H, n, d, ctypes.byref(p), 64)
+        assert 0 < nb < 1 << 30, (n, nb)
+        assert nb % 256 == 0
+        nbf = lib.luna_workspace_bytes(luna.OP_FEATUREMAP, dt, B, H, n, d, ctypes.byref(p), 64)
+        assert nbf > 0
+    p = _params()
+    assert lib.luna_workspace_bytes(9, luna.LUNA_BF16, 1, 1, 1, 64, ctypes.byref(p), 64) == 0
+    # per-head parameters need one table per head
+    ph = _params(per_head=1)
+    one = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 2, 4, 64, 64, ctypes.byref(p), 64)
+    four = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 2, 4, 64, 64, ctypes.byref(ph), 64)
+    assert four > one

@@ -1,0 +1,244 @@
+"""HIP path (through the C ABI) against the float64 oracle, element by element.
+
+Small problems span several tiles, chunks and a ragged tail and are compared in
+full; the five measured problems run at full size in the launch configuration the
+benchmark times and are compared on sampled heads / rows.  Tolerance: normwise per
+(b, h) slice, 1e-4 for fp32 and 2e-2 for bf16 inputs with fp32 accumulation.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_close, inputs, say, small_workload, to_np, upload
+from paper_2512_08061_amd import luna
+from paper_2512_08061_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    luna.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------------------
+# feature map
+# ---------------------------------------------------------------------------
+
+FM_CASES = [
+    ("f32", 32, 8, 8, 100), ("f32", 64, 16, 8, 77), ("bf16", 64, 16, 8, 300), ("bf16", 128, 32, 8, 65),
+    ("bf16", 64, 64, 1, 33), ("bf16", 32, 5, 4, 50), ("f32", 128, 3, 16, 20), ("bf16", 64, 8, 2, 1),
+]
+
+
+@pytest.mark.parametrize("dtype,d,M,L,n", FM_CASES)
+def test_featuremap_small(dtype, d, M, L, n):
+    w = small_workload(dtype, B=2, H=2, n=n, d=d, M=M, L=L, hidden=64 if L < 16 else 16)
+    say(f"featuremap {w.name}")
+    Q, K, V, p = inputs(w, seed=1)
+    (Xt,), pt = upload(w, [Q], p)
+    phi = to_np(luna.featuremap(Xt, pt))
+    ref = oracle.featuremap(Q, p)
+    assert_close(phi, ref, dtype, "phi")
+    if dtype == "bf16":  # fp32 output from bf16 input is checked at the fp32 bar
+        import torch
+        phi32 = to_np(luna.featuremap(Xt, pt, out_dtype=torch.float32))
+        assert_close(phi32, ref, "f32", "phi fp32 out")
+
+
+@pytest.mark.parametrize("name", list(wl.WORKLOADS))
+def test_featuremap_workload_full_size(name):
+    w = wl.WORKLOADS[name]
+    say(f"featuremap full size {name}")
+    Q, K, V, p = inputs(w, seed=0)
+    (Qt,), pt = upload(w, [Q], p)
+    phi = luna.featuremap(Qt, pt)
+    _sync()
+    rng = np.random.default_rng(5)
+    for _ in range(2):
+        b, h = int(rng.integers(w.B)), int(rng.integers(w.H))
+        assert_close(to_np(phi[b, h]), oracle.featuremap(Q[b, h], p), w.dtype, f"phi[{b},{h}]")
+    del phi
+
+
+# ---------------------------------------------------------------------------
+# non-causal attention
+# ---------------------------------------------------------------------------
+
+NC_CASES = [
+    ("f32", 32, 8, 8), ("f32", 64, 16, 8), ("bf16", 32, 16, 8), ("bf16", 64, 8, 8), ("bf16", 64, 16, 8),
+    ("bf16", 64, 32, 8), ("bf16", 64, 16, 4), ("bf16", 64, 64, 1), ("bf16", 128, 16, 8),
+]
+
+
+@pytest.mark.parametrize("dtype,d,M,L", NC_CASES)
+@pytest.mark.parametrize("n", [1, 97, 600])
+def test_attn_noncausal_small(dtype, d, M, L, n):
+    w = small_workload(dtype, B=2, H=2, n=n, d=d, M=M, L=L)
+    say(f"noncausal {w.name}")
+    Q, K, V, p = inputs(w, seed=2)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps))
+    assert_close(out, oracle.attn_noncausal(Q, K, V, p, eps=w.eps), dtype, "out")
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "text_encoder", "vision_encoder", "long_noncausal"])
+def test_attn_noncausal_workload_full_size(name):
+    w = wl.WORKLOADS[name]
+    say(f"noncausal full size {name}")
+    Q, K, V, p = inputs(w, seed=0)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps)
+    _sync()
+    rng = np.random.default_rng(7)
+    heads = [(0, 0), (w.B - 1, w.H - 1)] + [(int(rng.integers(w.B)), int(rng.integers(w.H))) for _ in range(2)]
+    for b, h in heads:
+        ref = oracle.attn_noncausal(Q[b, h], K[b, h], V[b, h], p, eps=w.eps)
+        assert_close(to_np(out[b, h])[None], ref[None], w.dtype, f"out[{b},{h}]")
+    if name == "tiny_f32":  # also against the O(n^2) kernel form
+        ref = oracle.attn_quadratic(Q, K, V, p, eps=w.eps)
+        assert_close(to_np(out), ref, w.dtype, "out vs kernel form")
+
+
+# ---------------------------------------------------------------------------
+# causal attention
+# ---------------------------------------------------------------------------
+
+CS_CASES = [
+    ("f32", 32, 8, 8), ("f32", 64, 16, 8), ("bf16", 32, 16, 8), ("bf16", 64, 16, 8), ("bf16", 64, 32, 8),
+    ("bf16", 128, 16, 8), ("bf16", 128, 32, 8),
+]
+
+
+@pytest.mark.parametrize("dtype,d,M,L", CS_CASES)
+@pytest.mark.parametrize("n", [1, 64, 65, 333])
+def test_attn_causal_small(dtype, d, M, L, n):
+    w = small_workload(dtype, B=1, H=3, n=n, d=d, M=M, L=L, causal=True)
+    say(f"causal {w.name}")
+    Q, K, V, p = inputs(w, seed=3)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))
+    assert_close(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), dtype, "out")
+
+
+def test_attn_causal_workload_full_size():
+    w = wl.WORKLOADS["long_causal"]
+    say("causal full size long_causal")
+    Q, K, V, p = inputs(w, seed=0)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=w.chunk, eps=w.eps)
+    _sync()
+    # masked kernel form on the first 512 tokens of every head
+    pre = 512
+    got = to_np(out[:, :, :pre])
+    for b in range(w.B):
+        ref = oracle.attn_quadratic(Q[b, :, :pre], K[b, :, :pre], V[b, :, :pre], p, eps=w.eps, causal=True)
+        assert_close(got[b], ref, w.dtype, f"prefix b={b}")
+    # sampled rows deep into the sequence, kernel form one row at a time
+    rng = np.random.default_rng(11)
+    for b, h in [(0, 0), (w.B - 1, w.H - 1), (int(rng.integers(w.B)), int(rng.integers(w.H)))]:
+        rows = np.sort(np.concatenate([rng.integers(0, w.n, 12), [w.n - 1, 4095, 4096]]))
+        ref = oracle.attn_quadratic_rows(Q[b, h], K[b, h], V[b, h], p, rows, eps=w.eps, causal=True)
+        assert_close(to_np(out[b, h, rows])[None], ref[None], w.dtype, f"rows of ({b},{h})")
+
+
+# ---------------------------------------------------------------------------
+# hand-worked example, edge cases, options
+# ---------------------------------------------------------------------------
+
+def _golden_problem():
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    d = 32  # the example has d = 2; zero columns leave every projection unchanged
+    pad = lambda x: np.pad(np.array(x, dtype=np.float32), ((0, 0), (0, d - 2)))  # noqa: E731
+    Q, K, V = pad(g["Q"])[None, None], pad(g["K"])[None, None], pad(g["V"])[None, None]
+    p = {"W": pad(g["W"]), "b": np.array(g["b"], np.float32), "fc1_w": np.array(g["fc1_w"], np.float32),
+         "fc1_b": np.array(g["fc1_b"], np.float32), "fc2_w": np.array(g["fc2_w"], np.float32),
+         "fc2_b": np.array(g["fc2_b"], np.float32), "M": 2, "L": 2, "hidden": 2}
+    frac = lambda x: np.array([[float(Fraction(v)) for v in row] for row in x])  # noqa: E731
+    return g, Q, K, V, p, frac
+
+
+def test_golden_hand_example_on_gpu():
+    g, Q, K, V, p, frac = _golden_problem()
+    w = small_workload("f32", B=1, H=1, n=2, d=32, M=2, L=2, hidden=2)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    phi = to_np(luna.featuremap(Qt, pt))[0, 0]
+    assert np.allclose(phi * math.sqrt(2), frac(g["phi_q_times_sqrtM"]), rtol=0, atol=1e-6)
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt, eps=0.0))[0, 0, :, :2]
+    assert np.allclose(out, frac(g["out_noncausal"]), rtol=0, atol=1e-6)
+    outc = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, eps=0.0))[0, 0, :, :2]
+    assert np.allclose(outc, frac(g["out_causal"]), rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_zero_features_give_zero(causal):
+    w = small_workload("bf16", B=1, H=2, n=70, d=64, M=16, L=8, causal=causal)
+    Q, K, V, p = inputs(w, seed=4)
+    p = dict(p)
+    p["fc2_w"] = np.zeros_like(p["fc2_w"])
+    p["fc2_b"] = -np.ones_like(p["fc2_b"])  # psi = relu(-1) = 0 everywhere
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    f = luna.attn_fwd_causal if causal else luna.attn_fwd
+    out = to_np(f(Qt, Kt, Vt, pt, eps=1e-6))
+    assert np.array_equal(out, np.zeros_like(out))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_options_per_head_shared_signed(causal):
+    # per-head parameters, one shared first layer, no output relu
+    w = small_workload("bf16", B=2, H=3, n=150, d=64, M=16, L=8, causal=causal, per_head=True,
+                       shared_channels=True, nonneg=False)
+    Q, K, V, p = inputs(w, seed=6)
+    # keep denominators away from zero when features may be negative
+    p = dict(p)
+    p["fc2_b"] = p["fc2_b"] + 1.0
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    f = luna.attn_fwd_causal if causal else luna.attn_fwd
+    out = to_np(f(Qt, Kt, Vt, pt, eps=w.eps))
+    ref = (oracle.attn_causal if causal else oracle.attn_noncausal)(Q, K, V, p, eps=w.eps)
+    assert_close(out, ref, "bf16", "options")
+    phi = to_np(luna.featuremap(Qt, pt))
+    assert_close(phi, oracle.featuremap(Q, p), "bf16", "phi options")
+
+
+def test_nan_propagates():
+    w = small_workload("f32", B=1, H=1, n=130, d=32, M=8, L=8)
+    Q, K, V, p = inputs(w, seed=8)
+    Q = Q.copy()
+    Q[0, 0, 5, 3] = np.nan
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt))[0, 0]
+    assert np.isnan(out[5]).all() and np.isfinite(np.delete(out, 5, axis=0)).all()
+    K = K.copy()
+    K[0, 0, 70, 0] = np.nan
+    (Qt, Kt, Vt), pt = upload(w, [np.nan_to_num(Q), K, V], p)
+    outc = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt))[0, 0]
+    assert np.isfinite(outc[:70]).all() and np.isnan(outc[70:]).all()
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_deterministic(causal):
+    w = small_workload("bf16", B=2, H=4, n=1100, d=64, M=16, L=8, causal=causal)
+    Q, K, V, p = inputs(w, seed=9)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    f = luna.attn_fwd_causal if causal else luna.attn_fwd
+    a = f(Qt, Kt, Vt, pt).clone()
+    b = f(Qt, Kt, Vt, pt).clone()
+    import torch
+    assert torch.equal(a, b)

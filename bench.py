@@ -1,0 +1,256 @@
+"""Benchmark of the LUNA attention forward hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+  * non-causal LUNA attention on the long-sequence encoder problem
+    B=32, H=8, n=4096, d=64, M=16 projections x L=8 channels (D=128), bf16;
+  * causal LUNA attention (chunked prefix scan, chunk 64) on the long causal problem
+    B=8, H=16, n=16384, d=128, M=32 x L=8 (D=256), bf16.
+Both read their inputs from HBM (2.7 GB in total, far beyond the 256 MB
+Infinity Cache) and each processes 131072 tokens (a token is one sequence
+position across all heads).  value = tokens of both problems / step time.
+
+The JSON line also carries
+  roofline      for the kernel that takes most of the step: algorithmic HBM bytes
+                per launch (read Q, K, V once, write out once) divided by its
+                average duration from HIP events on the launch stream; traffic is
+                the HBM bytes measured by rocprofv3 counters (see profiles/), or
+                null when the kernel source changed since they were taken;
+  cpu_baseline  the float64 oracle timed on the host cores on a bounded sample,
+                scaled to the same unit.
+Only one GPU is supported: --gpus above 1 exits with a message.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LUNA attn fwd tokens/sec + % HBM/MFMA roofline at n=4096, causal+non"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix cores
+KERNEL_SOURCES = {
+    "causal_kernel": ["luna_causal.hip", "luna_device.hpp", "luna_kernels.hpp"],
+    "nc_state_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
+    "nc_readout_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2512_08061_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if current."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("source_hash") != source_hash(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def flops_per_token_head(w, causal: bool) -> int:
+    """Matrix-core flops per (b, h, token): projections of q and k (4dM), S and the
+    readout (4Dd), z and the denominator (4D), plus the causal intra-chunk blocks
+    P, PV and P1 over full 64x64 blocks (2C(D + d + 1))."""
+    D = w.M * w.L
+    f = 4 * w.d * w.M + 4 * D * w.d + 4 * D
+    if causal:
+        f += 2 * w.chunk * (D + w.d + 1)
+    return f
+
+
+def bytes_per_token_head(w) -> int:
+    """Read q, k, v and write out once, in the storage dtype."""
+    return 4 * w.d * (2 if w.dtype == "bf16" else 4)
+
+
+def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
+    """The float64 oracle on a bounded sample of the same step, scaled to tokens/s."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    threads = len(os.sched_getaffinity(0))
+    nc_heads, cs_tokens = 3, 4096
+    with threadpool_limits(threads):
+        Q, K, V = (a[0, :nc_heads].astype(np.float64) for a in arrs4)
+        t0 = time.perf_counter()
+        oracle.attn_noncausal(Q, K, V, p4, eps=w4.eps)
+        t_nc = time.perf_counter() - t0
+        Q, K, V = (a[0, :1, :cs_tokens].astype(np.float64) for a in arrs5)
+        t0 = time.perf_counter()
+        oracle.attn_causal(Q, K, V, p5, eps=w5.eps)
+        t_cs = time.perf_counter() - t0
+    step = (t_nc * (w4.B * w4.H * w4.n) / (nc_heads * w4.n)
+            + t_cs * (w5.B * w5.H * w5.n) / cs_tokens)
+    tokens = w4.B * w4.n + w5.B * w5.n
+    return {
+        "value": tokens / step,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"float64 oracle: non-causal on {nc_heads} of {w4.B * w4.H} heads "
+                   f"({t_nc:.1f} s) and causal token recurrence on the first {cs_tokens} tokens of 1 of "
+                   f"{w5.B * w5.H} heads ({t_cs:.1f} s), scaled by head-tokens to one full step"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (for scaling HBM counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: LUNA attention shards over (batch, head) with no "
+              "communication, and this build measures the single-GPU kernel; use --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    luna.load_library()
+
+    w4, w5 = wl.WORKLOADS["long_noncausal"], wl.WORKLOADS["long_causal"]
+    t0 = time.perf_counter()
+    arrs4, arrs5 = wl.make_inputs(w4, args.seed), wl.make_inputs(w5, args.seed)
+    p4, p5 = wl.make_params(w4, args.seed), wl.make_params(w5, args.seed)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
+    up = lambda a: torch.from_numpy(a).to(dev).to(torch.bfloat16)  # noqa: E731
+    q4, k4, v4 = (up(a) for a in arrs4)
+    q5, k5, v5 = (up(a) for a in arrs5)
+    pt4 = luna.PhiParams.from_arrays(p4, dev, torch.bfloat16)
+    pt5 = luna.PhiParams.from_arrays(p5, dev, torch.bfloat16)
+    nc = luna.Plan(luna.OP_ATTN, q4, k4, v4, pt4, eps=w4.eps)
+    cs = luna.Plan(luna.OP_ATTN_CAUSAL, q5, k5, v5, pt5, eps=w5.eps, chunk=w5.chunk)
+    torch.cuda.synchronize()
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    for _ in range(args.warmup):
+        nc.run()
+        cs.run()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    stream = torch.cuda.current_stream(dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        nc.run()
+        ev[i][1].record(stream)
+        cs.run()
+        ev[i][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_step = 1e3 * wall / args.steps
+    ms_nc = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    ms_cs = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step (non-causal call {ms_nc:.3f} ms, causal call {ms_cs:.3f} ms)")
+
+    tokens = w4.B * w4.n + w5.B * w5.n
+    parts = {}
+    for name, w, ms, causal, kern in (("long_noncausal", w4, ms_nc, False, "nc_state_kernel+nc_readout_kernel"),
+                                      ("long_causal", w5, ms_cs, True, "causal_kernel")):
+        th = w.B * w.H * w.n
+        gb = bytes_per_token_head(w) * th / 1e9
+        tf = flops_per_token_head(w, causal) * th / 1e12
+        t_hbm, t_mfma = gb / HBM_PEAK_GBS, tf / MFMA_BF16_PEAK_TFLOPS
+        parts[name] = {
+            "shape": {"B": w.B, "H": w.H, "n": w.n, "d": w.d, "M": w.M, "L": w.L, "D": w.M * w.L,
+                      "causal": causal, **({"chunk": w.chunk} if causal else {})},
+            "kernels": kern,
+            "ms_per_call": round(ms, 4),
+            "tokens_per_s": w.B * w.n / (ms / 1e3),
+            "head_tokens_per_s": th / (ms / 1e3),
+            "attn_tflops": tf / (ms / 1e3),
+            "hbm_gbs": gb / (ms / 1e3),
+            "hbm_frac": (gb / (ms / 1e3)) / HBM_PEAK_GBS,
+            "mfma_frac": (tf / (ms / 1e3)) / MFMA_BF16_PEAK_TFLOPS,
+            "bound": "hbm" if t_hbm >= t_mfma else "mfma",
+            "roofline_frac": max(t_hbm, t_mfma) / (ms / 1e3),
+            "algorithmic_bytes": int(gb * 1e9),
+            "algorithmic_flops": int(tf * 1e12),
+        }
+
+    dom = max(parts, key=lambda k: parts[k]["ms_per_call"])
+    P = parts[dom]
+    kname = "causal_kernel" if dom == "long_causal" else "nc_state_kernel"
+    roofline = {
+        "bound": P["bound"],
+        "achieved": round(P["hbm_gbs"] if P["bound"] == "hbm" else P["attn_tflops"], 2),
+        "peak": HBM_PEAK_GBS if P["bound"] == "hbm" else MFMA_BF16_PEAK_TFLOPS,
+        "unit": "GB/s" if P["bound"] == "hbm" else "TFLOP/s",
+        "frac": round(P["roofline_frac"], 4),
+        "traffic": measured_traffic(kname, dom),
+        "kernel": kname,
+        "workload": dom,
+        "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel)",
+    }
+
+    out = {
+        "metric": METRIC,
+        "value": round(tokens / (ms_step / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; shapes and distributions of the paper's encoder and long-context settings)",
+        "config": {
+            "workload": "long_noncausal 32x8x4096x64 D=128 + long_causal 8x16x16384x128 D=256 chunk=64, bf16",
+            "tokens_per_step": tokens,
+            "parts": parts,
+        },
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(w4, arrs4, p4, w5, arrs5, p5)
+        log(f"cpu baseline in {time.perf_counter() - t0:.1f} s")
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -178,6 +178,7 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
       pq[k].zero();
       pk[k].zero();
     }
+    float uu[8 * MB];  // q projections at [4mb + j], k projections at [4MB + 4mb + j]
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       f32x4 aq = zero4(), ak = zero4();
@@ -190,10 +191,20 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
+        uu[4 * mb + j] = aq[j] + brow[mb][j];
+        uu[4 * MB + 4 * mb + j] = ak[j] + brow[mb][j];
+      }
+    }
+    int sg[8 * MB];
+    pwl_search(sm.tab, tdepth, uu, sg);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
         const bool pok = 16 * mb + 4 * g + j < M;
         float yq[L], yk[L];
-        pwl_eval<L>(sm.tab, tdepth, tfloor, aq[j] + brow[mb][j], yq);
-        pwl_eval<L>(sm.tab, tdepth, tfloor, ak[j] + brow[mb][j], yk);
+        pwl_channels<L>(sm.tab, sg[4 * mb + j], tfloor, uu[4 * mb + j], yq);
+        pwl_channels<L>(sm.tab, sg[4 * MB + 4 * mb + j], tfloor, uu[4 * MB + 4 * mb + j], yk);
 #pragma unroll
         for (int l = 0; l < L; ++l) {
           const int p = (mb * 4 + j) * L + l;

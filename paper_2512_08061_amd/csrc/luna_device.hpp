@@ -84,13 +84,29 @@ __device__ __forceinline__ float relu_floor(float v, float floor) {
   return __builtin_elementwise_maximum(v, floor);
 }
 
-// psi_l(u) for l = 0..L-1, already scaled by 1/sqrt(M) (folded into the table).
+// Segment index of each of NU values: the number of breakpoints strictly below u.
+// The NU searches advance together, so each step issues NU independent LDS reads
+// and the lookup latency is paid once per step rather than once per value.  NaN
+// compares false everywhere and lands in segment 0.
+template <int NU, int SEGCAP>
+__device__ __forceinline__ void pwl_search(const PwlLds<SEGCAP>& t, int depth, const float (&u)[NU],
+                                           int (&seg)[NU]) {
+  unsigned idx[NU];
+#pragma unroll
+  for (int i = 0; i < NU; ++i) idx[i] = 1u;
+  for (int s = 0; s < depth; ++s) {
+#pragma unroll
+    for (int i = 0; i < NU; ++i) idx[i] = 2u * idx[i] + (u[i] > t.tree[idx[i]] ? 1u : 0u);
+  }
+#pragma unroll
+  for (int i = 0; i < NU; ++i) seg[i] = (int)(idx[i] - (1u << depth));
+}
+
+// psi_l(u) for l = 0..L-1 on segment `seg`, already scaled by 1/sqrt(M) (folded
+// into the table).
 template <int L, int SEGCAP>
-__device__ __forceinline__ void pwl_eval(const PwlLds<SEGCAP>& t, int depth, float floor, float u,
-                                         float (&y)[L]) {
-  unsigned idx = 1;
-  for (int s = 0; s < depth; ++s) idx = 2u * idx + (u > t.tree[idx] ? 1u : 0u);
-  const int seg = (int)(idx - (1u << depth));
+__device__ __forceinline__ void pwl_channels(const PwlLds<SEGCAP>& t, int seg, float floor, float u,
+                                             float (&y)[L]) {
   if constexpr (L % 2 == 0) {
     const float4* st = reinterpret_cast<const float4*>(t.seg + seg * L);
 #pragma unroll

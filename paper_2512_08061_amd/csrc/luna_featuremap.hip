@@ -55,22 +55,27 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
       else wf.zero();
       mma(acc, wf, xf[ks]);
     }
+    float uu[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
-      if (i < M) {
-        const float u = acc[j] + bias[i];
+      uu[j] = acc[j] + (i < M ? bias[i] : 0.0f);
+    }
+    int sg[4];
+    pwl_search(tab, depth, uu, sg);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 16 * mb + 4 * g + j;
+      if (i < M && row_ok) {
         float y[L];
-        pwl_eval<L>(tab, depth, floor, u, y);
-        if (row_ok) {
-          Tout* o = out + i * L;
-          if constexpr (L % 4 == 0) {
+        pwl_channels<L>(tab, sg[j], floor, uu[j], y);
+        Tout* o = out + i * L;
+        if constexpr (L % 4 == 0) {
 #pragma unroll
-            for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
-          } else {
+          for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
+        } else {
 #pragma unroll
-            for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
-          }
+          for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
         }
       }
     }

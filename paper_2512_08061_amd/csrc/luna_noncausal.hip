@@ -144,23 +144,30 @@ __global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
     __syncthreads();
 
     // projections and channel functions -> A fragments phi(K)^T
-    Frag<T> af[MB][L];
+    float uu[8 * MB];  // [mb][tb][j]
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const bool pok = 16 * mb + r < M;
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
         f32x4 acc = zero4();
 #pragma unroll
         for (int ks = 0; ks < C::KS; ++ks) mma(acc, kc[tb][ks], wf[mb][ks]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const bool ok = pok && (t0 + 16 * tb + 4 * g + j < t_end);
-          float y[L];
-          pwl_eval<L>(tab, tdepth, tfloor, acc[j] + bcol[mb], y);
+        for (int j = 0; j < 4; ++j) uu[8 * mb + 4 * tb + j] = acc[j] + bcol[mb];
+      }
+    int sg[8 * MB];
+    pwl_search(tab, tdepth, uu, sg);
+    Frag<T> af[MB][L];
 #pragma unroll
-          for (int l = 0; l < L; ++l) af[mb][l].set(4 * tb + j, ok ? y[l] : 0.0f);
-        }
+    for (int mb = 0; mb < MB; ++mb) {
+      const bool pok = 16 * mb + r < M;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {  // slot e = 4 tb + j
+        const bool ok = pok && (t0 + 16 * (e / 4) + 4 * g + (e % 4) < t_end);
+        float y[L];
+        pwl_channels<L>(tab, sg[8 * mb + e], tfloor, uu[8 * mb + e], y);
+#pragma unroll
+        for (int l = 0; l < L; ++l) af[mb][l].set(e, ok ? y[l] : 0.0f);
       }
     }
     // S += phi(K)^T V, z += phi(K)^T 1
@@ -308,16 +315,24 @@ __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
     Frag<T> pq[C::NF];
 #pragma unroll
     for (int k = 0; k < C::NF; ++k) pq[k].zero();
+    float uu[4 * MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       f32x4 acc = zero4();
 #pragma unroll
       for (int ks = 0; ks < C::KS; ++ks) mma(acc, wf[mb][ks], qf[ks]);
 #pragma unroll
+      for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
+    }
+    int sg[4 * MB];
+    pwl_search(tab, tdepth, uu, sg);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
       for (int j = 0; j < 4; ++j) {
         const bool pok = 16 * mb + 4 * g + j < M;
         float y[L];
-        pwl_eval<L>(tab, tdepth, tfloor, acc[j] + brow[mb][j], y);
+        pwl_channels<L>(tab, sg[4 * mb + j], tfloor, uu[4 * mb + j], y);
 #pragma unroll
         for (int l = 0; l < L; ++l) {
           const int p = (mb * 4 + j) * L + l;

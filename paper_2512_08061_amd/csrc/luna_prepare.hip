@@ -4,16 +4,19 @@
 // (outer relu when nonneg).  Every hidden unit with a_k != 0 switches state at
 // beta_k = -c_k / a_k; between two consecutive breakpoints each unit is either on
 // (contributes f a u + f c) or off, so the pre-activation output is s u + t there.
+// Segment j is the interval (sorted[j-1], sorted[j]]; the search in the attention
+// kernels returns j = number of breakpoints strictly below u.
+//
 // One workgroup per parameter set:
-//   1. breakpoints beta_k (fp64 quotient rounded to fp32; units with a_k = 0 or a
-//      non-finite quotient are constant: on iff c_k > 0);
-//   2. stable ranks by counting (rank_k = #{beta < beta_k} + #{equal, smaller index});
+//   1. breakpoints beta_k (fp64 quotient rounded to fp32); units with a_k = 0 or a
+//      non-finite quotient are constant (on iff c_k > 0) and get no breakpoint;
+//   2. bitonic sort of (beta, unit) in LDS, ties broken by unit index;
 //   3. heap-ordered search tree over the sorted breakpoints, padded with +inf;
-//   4. per segment j and channel l: s, t summed in fp64 over the units that are on
-//      inside segment j (a > 0: rank < j; a < 0: rank >= j), scaled by 1/sqrt(M),
-//      rounded to fp32.
-// Segment j is the interval (sorted[j-1], sorted[j]]; the search returns
-// j = number of breakpoints strictly below u.
+//   4. per channel l: segment 0 holds the units that are on below every breakpoint
+//      (a < 0, or a = 0 with c > 0); crossing the breakpoint of unit k switches it on
+//      (a > 0) or off (a < 0), changing (s, t) by +-(f a, f c).  The segment values
+//      are these changes prefix-summed in fp64 (32 blocks per channel, block sums
+//      scanned with lane shuffles), scaled by 1/sqrt(M) and rounded to fp32.
 #include <math.h>
 
 #include "luna_device.hpp"
@@ -21,11 +24,20 @@
 
 namespace luna {
 
+namespace {
+constexpr int kSortCap = kMaxUnits + 1;  // 1024
+
+__device__ __forceinline__ bool key_greater(float k1, int i1, float k2, int i2) {
+  return k1 > k2 || (k1 == k2 && i1 > i2);
+}
+}  // namespace
+
 __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
-  __shared__ float beta[kMaxUnits + 1];
-  __shared__ int has_bp[kMaxUnits + 1];
-  __shared__ int rank[kMaxUnits + 1];
-  __shared__ float sorted[kMaxUnits + 1];
+  __shared__ float key[kSortCap];
+  __shared__ int kidx[kSortCap];
+  __shared__ float a_s[kSortCap], c_s[kSortCap], f_s[kSortCap];
+  __shared__ int has_bp[kSortCap];
+  __shared__ float g_s[16];
   __shared__ int s_nbp;
 
   const int set = blockIdx.x;
@@ -40,65 +52,138 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   if (set == 0 && a.zero_ptr != nullptr)
     for (int i = tid; i < a.zero_count; i += blockDim.x) a.zero_ptr[i] = 0;
   if (tid == 0) s_nbp = 0;
+  int N = 2;
+  while (N < units) N *= 2;
   __syncthreads();
 
-  for (int k = tid; k < units; k += blockDim.x) {
-    const float ak = A[k], ck = Cc[k];
-    const float bk = (float)(-(double)ck / (double)ak);
-    const int h = (ak != 0.0f) && isfinite(bk);
-    beta[k] = bk;
-    has_bp[k] = h;
-    if (h) atomicAdd(&s_nbp, 1);
+  // 1. parameters and breakpoints
+  for (int k = tid; k < a.L * a.hidden; k += blockDim.x) f_s[k] = F[k];
+  for (int l = tid; l < a.L; l += blockDim.x) g_s[l] = G[l];
+  for (int k = tid; k < N; k += blockDim.x) {
+    float bk = __builtin_inff();
+    int h = 0;
+    if (k < units) {
+      const float ak = A[k], ck = Cc[k];
+      a_s[k] = ak;
+      c_s[k] = ck;
+      const float q = (float)(-(double)ck / (double)ak);
+      h = (ak != 0.0f) && isfinite(q);
+      if (h) bk = q;
+      has_bp[k] = h;
+      if (h) atomicAdd(&s_nbp, 1);
+    }
+    key[k] = bk;
+    kidx[k] = k;
   }
   __syncthreads();
   const int nbp = s_nbp;
 
-  for (int k = tid; k < units; k += blockDim.x) {
-    int r = -1;
-    if (has_bp[k]) {
-      r = 0;
-      const float bk = beta[k];
-      for (int q = 0; q < units; ++q)
-        r += has_bp[q] && (beta[q] < bk || (beta[q] == bk && q < k));
-      sorted[r] = bk;
+  // 2. bitonic sort of (key, unit), ascending
+  for (int size = 2; size <= N; size <<= 1) {
+    for (int stride = size / 2; stride > 0; stride >>= 1) {
+      for (int i = tid; i < N / 2; i += blockDim.x) {
+        const int lo = 2 * i - (i & (stride - 1));
+        const int hi = lo + stride;
+        const bool asc = (lo & size) == 0;
+        const float k1 = key[lo], k2 = key[hi];
+        const int i1 = kidx[lo], i2 = kidx[hi];
+        if (key_greater(k1, i1, k2, i2) == asc) {
+          key[lo] = k2; key[hi] = k1;
+          kidx[lo] = i2; kidx[hi] = i1;
+        }
+      }
+      __syncthreads();
     }
-    rank[k] = r;
   }
-  __syncthreads();
 
+  // 3. search tree: heap node i holds the breakpoint of in-order rank r(i)
   int depth = 0;
   while ((1 << depth) - 1 < nbp) ++depth;
   float* tree = reinterpret_cast<float*>(tab + kTabTree);
   for (int i = tid; i < (1 << depth); i += blockDim.x) {
     float v = __builtin_inff();
     if (i >= 1) {
-      const int lv = 31 - __clz(i);          // level of heap node i (root = 0)
-      const int ht = depth - 1 - lv;         // its height
-      const int r = (i - (1 << lv)) * (1 << (ht + 1)) + (1 << ht) - 1;  // in-order rank
-      if (r < nbp) v = sorted[r];
+      const int lv = 31 - __clz(i);   // level of heap node i (root = 0)
+      const int ht = depth - 1 - lv;  // its height
+      const int r = (i - (1 << lv)) * (1 << (ht + 1)) + (1 << ht) - 1;
+      if (r < nbp) v = key[r];
     }
     tree[i] = v;
   }
 
+  // 4. segment values by prefix sums over the sorted breakpoints
   const double inv = 1.0 / sqrt((double)a.M);
   const int shared = (a.C1 == 1);
   float2* seg = reinterpret_cast<float2*>(tab + kTabSeg);
-  const int nseg = (nbp + 1) * a.L;
-  for (int idx = tid; idx < nseg; idx += blockDim.x) {
-    const int j = idx / a.L, l = idx - (idx / a.L) * a.L;
+  const int nseg = nbp + 1;
+  const int per = (nseg + 31) / 32;  // segments per block
+  const int b = tid % 32;            // block within the channel
+  for (int l0 = 0; l0 < a.L; l0 += 8) {
+    const int l = l0 + tid / 32;     // 32 consecutive lanes share one channel
+    const bool lok = l < a.L;
     const int k0 = shared ? 0 : l * a.hidden;
-    double s = 0.0, t = (double)G[l];
-    for (int kk = 0; kk < a.hidden; ++kk) {
-      const int k = k0 + kk;
-      const float ak = A[k], ck = Cc[k];
-      const int on = has_bp[k] ? (ak > 0.0f ? (rank[k] < j) : (rank[k] >= j)) : (ck > 0.0f);
-      if (on) {
-        const double f = (double)F[l * a.hidden + kk];
-        s += f * (double)ak;
-        t += f * (double)ck;
+    // change of (s, t) when crossing the breakpoint of rank r
+    auto delta = [&](int r, double& ds, double& dt) {
+      ds = 0.0;
+      dt = 0.0;
+      if (r >= nbp) return;
+      const int k = kidx[r];
+      if (k < k0 || k >= k0 + a.hidden) return;
+      const double f = (double)f_s[l * a.hidden + (k - k0)];
+      const double sg = a_s[k] > 0.0f ? 1.0 : -1.0;
+      ds = sg * f * (double)a_s[k];
+      dt = sg * f * (double)c_s[k];
+    };
+    // units on below every breakpoint, two per lane, reduced over the 32 lanes
+    double bs = 0.0, bt = 0.0;
+    if (lok) {
+      for (int kk = b; kk < a.hidden; kk += 32) {
+        const int k = k0 + kk;
+        const int on = has_bp[k] ? (a_s[k] < 0.0f) : (c_s[k] > 0.0f);
+        if (on) {
+          const double f = (double)f_s[l * a.hidden + kk];
+          bs += f * (double)a_s[k];
+          bt += f * (double)c_s[k];
+        }
       }
     }
-    seg[idx] = make_float2((float)(s * inv), (float)(t * inv));
+    // this block's total change
+    const int j0 = b * per, j1 = min(nseg, j0 + per);
+    double ts = 0.0, tt = 0.0;
+    if (lok)
+      for (int r = j0; r < j1; ++r) {
+        double ds, dt;
+        delta(r, ds, dt);
+        ts += ds;
+        tt += dt;
+      }
+    // reductions and exclusive scans across the 32 lanes of the channel
+    double es = ts, et = tt;  // inclusive scan first
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      const double us = __shfl_up(es, o, 32), ut = __shfl_up(et, o, 32);
+      if (b >= o) {
+        es += us;
+        et += ut;
+      }
+    }
+    es -= ts;
+    et -= tt;
+#pragma unroll
+    for (int o = 16; o > 0; o >>= 1) {
+      bs += __shfl_xor(bs, o, 32);
+      bt += __shfl_xor(bt, o, 32);
+    }
+    if (lok) {
+      double s = bs + es, t = (double)g_s[l] + bt + et;
+      for (int j = j0; j < j1; ++j) {
+        seg[j * a.L + l] = make_float2((float)(s * inv), (float)(t * inv));
+        double ds, dt;
+        delta(j, ds, dt);
+        s += ds;
+        t += dt;
+      }
+    }
   }
   if (tid == 0) {
     PwlHeader* hd = reinterpret_cast<PwlHeader*>(tab + kTabHeader);

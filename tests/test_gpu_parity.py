@@ -62,6 +62,29 @@ def test_featuremap_small(dtype, d, M, L, n):
         assert_close(phi32, ref, "f32", "phi fp32 out")
 
 
+@pytest.mark.parametrize("shared,nonneg", [(False, True), (True, False), (False, False)])
+def test_featuremap_psi_sweep(shared, nonneg):
+    """u swept over [-50, 50] and onto every breakpoint (and its fp32 neighbours):
+    every segment of the piecewise-linear tables is hit."""
+    w = small_workload("f32", B=1, H=1, n=8, d=32, M=1, L=8, shared_channels=shared, nonneg=nonneg)
+    p = wl.make_params(w, seed=12)
+    p = dict(p)
+    p["W"] = np.zeros((1, 32), np.float32)
+    p["W"][0, 0] = 1.0  # u = x_0 + b
+    p["b"] = np.zeros(1, np.float32)
+    a, c = p["fc1_w"].astype(np.float64), p["fc1_b"].astype(np.float64)
+    bp = (-c / a).ravel().astype(np.float32)
+    u = np.concatenate([np.linspace(-50, 50, 4001, dtype=np.float32), bp, np.nextafter(bp, np.float32(np.inf)),
+                        np.nextafter(bp, np.float32(-np.inf)), np.float32([0, 1e-30, -1e-30, 1e4, -1e4])])
+    X = np.zeros((1, 1, u.size, 32), np.float32)
+    X[0, 0, :, 0] = u
+    (Xt,), pt = upload(w.with_(n=u.size), [X], p)
+    phi = to_np(luna.featuremap(Xt, pt))[0, 0]
+    ref = oracle.featuremap(X[0, 0], p)
+    err = np.abs(phi - ref) / np.maximum(1.0, np.abs(u.astype(np.float64)))[:, None]
+    assert err.max() < 2e-6 * max(1.0, np.abs(ref).max()), err.max()
+
+
 @pytest.mark.parametrize("name", list(wl.WORKLOADS))
 def test_featuremap_workload_full_size(name):
     w = wl.WORKLOADS[name]

@@ -56,7 +56,7 @@ luna_status check_common(const Problem& pb) {
   const int units = C1 * p->hidden;
   if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
   const int seg_cap = pb.op == LUNA_OP_FEATUREMAP ? luna::kSegCap : luna::attn_seg_cap(p->L);
-  if ((units + 1) * p->L > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "(L*hidden + 1)*L exceeds the segment table");
+  if ((units + 2) * p->L > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "(L*hidden + 2)*L exceeds the segment table");
   return LUNA_OK;
 }
 

@@ -1,31 +1,34 @@
 // luna_causal.hip -- causal (streaming) LUNA attention as a chunked prefix scan.
 //
 // out_t = phi(q_t)^T S_t / (phi(q_t)^T z_t + eps) with S_t, z_t summed over s <= t.
-// Tokens are processed in chunks of 64; within chunk c (rows of the chunk t, columns s):
+// Tokens are processed in chunks of 64; within chunk c (query rows t, key columns s):
 //
 //   P      = tril(phi(Q_c) phi(K_c)^T)              (diagonal included)
 //   num    = P V_c + phi(Q_c) S_{c-1},   den = P 1 + phi(Q_c) z_{c-1}
 //   S_c    = S_{c-1} + phi(K_c)^T V_c,   z_c = z_{c-1} + phi(K_c)^T 1
 //
-// which regroups the prefix sums exactly.  One workgroup owns one (head, tile of
-// DVT value columns) and walks the chunks in order, keeping its slice of S in fp32
-// matrix-core accumulators and z alongside; there is no cross-workgroup traffic.
+// which regroups the prefix sums exactly.  One workgroup of 8 waves owns one
+// (head, tile of DVT value columns) and walks the chunks in order, keeping its
+// slice of S in fp32 matrix-core accumulators; there is no cross-workgroup traffic.
 //
-// Within a chunk wave w owns query/key token block w (16 tokens):
-//  1. u^T = W Q^T and u^T = W K^T (A = W fragments from LDS), psi -> phi(Q_w), phi(K_w)
-//     as k-order fragments (lane = token, 8 features), see luna_noncausal.hip.
-//  2. phi(K_w) goes to LDS twice: as fragments (for other waves' P blocks) and
-//     transposed, feature x token (for the state update).
-//  3. P^T blocks (j <= w) = phi(K_j) phi(Q_w)^T; the diagonal block is masked.  The
-//     accumulators are already B fragments of num^T += V^T P^T (k = key token);
-//     den += 1^T P^T with an all-ones A operand.
-//  4. num^T += S^T phi(Q_w)^T and den += z^T phi(Q_w)^T, S and z read from LDS as
-//     A fragments (staged at the end of the previous chunk, bf16 for bf16 calls).
-//  5. out = num * (1 / (den + eps)).
-//  6. S += phi(K_c)^T V_c over the chunk (wave w updates row blocks w, w+4, ...),
-//     then S and z are staged to LDS for the next chunk.
-// Two workgroup barriers per chunk; V and the next chunk's Q/K rows are fetched into
-// registers one chunk ahead.
+// Per chunk:
+//  A. waves 0-3 compute phi(Q) and waves 4-7 phi(K) of token block w % 4:
+//     u^T = W X^T on the matrix cores (W fragments from LDS), one batched search of
+//     the piecewise-linear table, L fused multiply-adds per projection.  The result
+//     is k-order fragments (lane = token, 8 features) written to LDS.  Padded
+//     projections and key tokens past n select the table's all-zero segment.
+//  B. wave w answers query block i = (w < 4 ? w : 7 - w) (blocks i and 3 - i share a
+//     SIMD, balancing the triangle) for value-column half w / 4:
+//       P^T blocks j <= i = phi(K_j) phi(Q_i)^T, diagonal block masked; the
+//       accumulators are directly the B operands of num^T += V^T P^T and of
+//       den += 1^T P^T;  num^T += S^T phi(Q_i)^T, den += z^T phi(Q_i)^T from the
+//       staged state;  out = num * (1 / (den + eps)).
+//     Then S += phi(K_c)^T V_c for row blocks w, w + 8 of S (and z alongside).
+//     V^T and phi(K)^T operands come from row-major LDS tiles through the gfx950
+//     transpose read, so no data is stored transposed.
+//  C. S and z are staged to LDS as A fragments for the next chunk.
+// Two workgroup barriers per chunk; each wave's Q/K rows and the V tile are
+// fetched into registers one chunk ahead.
 #include "luna_device.hpp"
 #include "luna_kernels.hpp"
 
@@ -37,29 +40,31 @@ struct CsCfg {
   static constexpr int NF = (4 * MB * L + 7) / 8;   // k-order fragments over features
   static constexpr int FR = NF * 32;                // padded feature rows of S
   static constexpr int RB = FR / 16;                // row blocks of S
-  static constexpr int RBW = (RB + 3) / 4;          // row blocks per wave
+  static constexpr int RBW = (RB + 7) / 8;          // row blocks per wave
   static constexpr int CBT = DVT / 16;              // column blocks of the tile
+  static constexpr int CBH = CBT / 2;               // column blocks per half
   static constexpr int SEGCAP = attn_seg_cap(L);
-  static constexpr int VE = 16 / (int)sizeof(T);
-  static constexpr int TROW = 64 + VE;              // token-row length in LDS (padded)
-  static constexpr int NVC = 64 * (DVT / VE) / 256; // V 16-byte chunks per thread per chunk
-  static_assert(NVC >= 1, "value tile too narrow");
+  static constexpr int VE = 16 / (int)sizeof(T);    // elements per 16-byte chunk
+  static constexpr int VROW = DVT + VE;             // padded V-tile row (elements)
+  static constexpr int VCH = 64 * DVT / VE;         // 16-byte chunks in a V tile
+  static constexpr int NVC = (VCH + 511) / 512;     // per thread
+  static_assert(CBT >= 2 && CBT % 2 == 0, "value tile must hold an even number of 16-column blocks");
 };
 
 template <typename T, int DH, int L, int MB, int DVT>
 struct CsLds {
   using C = CsCfg<T, DH, L, MB, DVT>;
   PwlLds<C::SEGCAP> tab;
-  alignas(16) T wfr[MB][C::KS][kWave][8];   // W as A fragments of u^T = W X^T
-  alignas(16) T pk_tok[4][C::NF][kWave][8]; // phi(K) fragments per token block
-  alignas(16) T pk_t[C::FR][C::TROW];       // phi(K)^T: k-order feature x token
-  alignas(16) T vt[DVT][C::TROW];           // V^T tile: value column x token
+  alignas(16) T wfr[MB][C::KS][kWave][8];      // W as A fragments of u^T = W X^T
+  alignas(16) T pq_tok[4][C::NF][kWave][8];    // phi(Q) fragments per token block
+  alignas(16) T pk_tok[4][C::NF][kWave][8];    // phi(K) fragments per token block
+  alignas(16) T vtile[64][C::VROW];            // V tile, row-major (token x column)
   alignas(16) T sst[C::CBT][C::NF][kWave][8];  // S_{c-1} as A fragments
   alignas(16) T zst[C::NF][4][8];              // z_{c-1} as A fragment slots per lane group
 };
 
 template <typename T, int DH, int L, int MB, int DVT>
-__global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
+__global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   using C = CsCfg<T, DH, L, MB, DVT>;
   __shared__ CsLds<T, DH, L, MB, DVT> sm;
 
@@ -81,8 +86,14 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
   const T* W = reinterpret_cast<const T*>(a.phi.W) + (size_t)hset * M * DH;
   const float* bias = a.phi.b + (size_t)hset * M;
 
+  // phase A role: side (0 = queries, 1 = keys) and token block
+  const int side = wave / 4, tba = wave % 4;
+  // phase B role: query block and value-column half
+  const int qi = wave < 4 ? wave : 7 - wave, hh = wave / 4;
+  const T* X = side ? K : Q;
+
   // W fragments into LDS; S and z start at zero
-  for (int i = tid; i < MB * C::KS * kWave; i += 256) {
+  for (int i = tid; i < MB * C::KS * kWave; i += 512) {
     const int l = i % kWave, ks = (i / kWave) % C::KS, mb = i / (kWave * C::KS);
     const int p = 16 * mb + l % 16;
     Frag<T> f;
@@ -90,22 +101,24 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
     else f.zero();
     store8(&sm.wfr[mb][ks][l][0], f);
   }
-  for (int i = tid; i < C::CBT * C::NF * kWave; i += 256) {
+  for (int i = tid; i < C::CBT * C::NF * kWave; i += 512) {
     Frag<T> f;
     f.zero();
     store8(&sm.sst[0][0][0][0] + (size_t)i * 8, f);
   }
-  for (int i = tid; i < C::NF * 4; i += 256) {
+  for (int i = tid; i < C::NF * 4; i += 512) {
     Frag<T> f;
     f.zero();
     store8(&sm.zst[0][0][0] + (size_t)i * 8, f);
   }
   float brow[MB][4];
+  bool pok[MB][4];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = 16 * mb + 4 * g + j;
+      pok[mb][j] = i < M;
       brow[mb][j] = i < M ? bias[i] : 0.0f;
     }
   Frag<T> ones;
@@ -120,194 +133,196 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
     for (int cb = 0; cb < C::CBT; ++cb) sacc[i][cb] = zero4();
   }
 
-  // one-chunk-ahead register fetch
-  Frag<T> qn[C::KS], kn[C::KS];
+  // one-chunk-ahead register fetch: this wave's X rows and its share of the V tile
+  Frag<T> xn[C::KS];
   i32x4 vn[C::NVC];
   auto fetch = [&](int tc) {
-    const int t = tc + 16 * wave + r;
+    const int t = tc + 16 * tba + r;
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) {
-      if (t < n) {
-        load8(qn[ks], Q + (size_t)t * DH + 32 * ks + 8 * g);
-        load8(kn[ks], K + (size_t)t * DH + 32 * ks + 8 * g);
-      } else {
-        qn[ks].zero();
-        kn[ks].zero();
-      }
+      if (t < n) load8(xn[ks], X + (size_t)t * DH + 32 * ks + 8 * g);
+      else xn[ks].zero();
     }
 #pragma unroll
     for (int q = 0; q < C::NVC; ++q) {
-      const int cidx = tid + 256 * q;
+      const int cidx = tid + 512 * q;
       const int tt = cidx / (DVT / C::VE), cg = cidx % (DVT / C::VE);
       const int tv = tc + tt;
-      if (tv < n) vn[q] = *reinterpret_cast<const i32x4*>(V + (size_t)tv * DH + c0 + cg * C::VE);
+      if (cidx < C::VCH && tv < n) vn[q] = *reinterpret_cast<const i32x4*>(V + (size_t)tv * DH + c0 + cg * C::VE);
       else vn[q] = i32x4{0, 0, 0, 0};
     }
   };
 
   __syncthreads();
   const int tdepth = sm.tab.depth;
+  const int zseg = sm.tab.zero_seg;
   const float tfloor = sm.tab.floor;
   const int nchunks = (n + 63) / 64;
   fetch(0);
 
   for (int c = 0; c < nchunks; ++c) {
     const int tc = 64 * c;
-    // V^T tile of this chunk
+    // V tile of this chunk, row-major
 #pragma unroll
     for (int q = 0; q < C::NVC; ++q) {
-      const int cidx = tid + 256 * q;
-      const int tt = cidx / (DVT / C::VE), cg = cidx % (DVT / C::VE);
-      const T* e = reinterpret_cast<const T*>(&vn[q]);
-#pragma unroll
-      for (int x = 0; x < C::VE; ++x) sm.vt[cg * C::VE + x][tt] = e[x];
+      const int cidx = tid + 512 * q;
+      if (cidx < C::VCH) {
+        const int tt = cidx / (DVT / C::VE), cg = cidx % (DVT / C::VE);
+        *reinterpret_cast<i32x4*>(&sm.vtile[tt][cg * C::VE]) = vn[q];
+      }
     }
-    Frag<T> qc[C::KS], kc[C::KS];
+    Frag<T> xc[C::KS];
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      qc[ks] = qn[ks];
-      kc[ks] = kn[ks];
-    }
+    for (int ks = 0; ks < C::KS; ++ks) xc[ks] = xn[ks];
     if (c + 1 < nchunks) fetch(tc + 64);
 
-    // 1. projections and channel functions of this wave's 16 tokens
-    const bool k_ok = tc + 16 * wave + r < n;
-    Frag<T> pq[C::NF], pk[C::NF];
+    // ---- A. feature map of this wave's (side, token block) ----
+    {
+      const bool tok_ok = tc + 16 * tba + r < n;
+      float uu[4 * MB];
 #pragma unroll
-    for (int k = 0; k < C::NF; ++k) {
-      pq[k].zero();
-      pk[k].zero();
-    }
-    float uu[8 * MB];  // q projections at [4mb + j], k projections at [4MB + 4mb + j]
+      for (int mb = 0; mb < MB; ++mb) {
+        f32x4 acc = zero4();
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      f32x4 aq = zero4(), ak = zero4();
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
-        Frag<T> wa;
-        load8(wa, &sm.wfr[mb][ks][lane][0]);
-        mma(aq, wa, qc[ks]);
-        mma(ak, wa, kc[ks]);
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        uu[4 * mb + j] = aq[j] + brow[mb][j];
-        uu[4 * MB + 4 * mb + j] = ak[j] + brow[mb][j];
-      }
-    }
-    int sg[8 * MB];
-    pwl_search(sm.tab, tdepth, uu, sg);
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bool pok = 16 * mb + 4 * g + j < M;
-        float yq[L], yk[L];
-        pwl_channels<L>(sm.tab, sg[4 * mb + j], tfloor, uu[4 * mb + j], yq);
-        pwl_channels<L>(sm.tab, sg[4 * MB + 4 * mb + j], tfloor, uu[4 * MB + 4 * mb + j], yk);
-#pragma unroll
-        for (int l = 0; l < L; ++l) {
-          const int p = (mb * 4 + j) * L + l;
-          pq[p / 8].set(p % 8, pok ? yq[l] : 0.0f);
-          pk[p / 8].set(p % 8, (pok && k_ok) ? yk[l] : 0.0f);
+        for (int ks = 0; ks < C::KS; ++ks) {
+          Frag<T> wa;
+          load8(wa, &sm.wfr[mb][ks][lane][0]);
+          mma(acc, wa, xc[ks]);
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
       }
-    }
-    // 2. phi(K_w) to LDS
+      int sg[4 * MB];
+      pwl_search(sm.tab, tdepth, uu, sg);
+      const bool kill_tok = side && !tok_ok;  // key rows past n contribute nothing
 #pragma unroll
-    for (int k = 0; k < C::NF; ++k) {
-      store8(&sm.pk_tok[wave][k][lane][0], pk[k]);
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sm.pk_t[32 * k + 8 * g + e][16 * wave + r] = pk[k].v[e];
+        for (int j = 0; j < 4; ++j)
+          if (!pok[mb][j] || kill_tok) sg[4 * mb + j] = zseg;
+      Frag<T> ph[C::NF];
+#pragma unroll
+      for (int k = 0; k < C::NF; ++k) ph[k].zero();
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float y[L];
+          pwl_channels<L>(sm.tab, sg[4 * mb + j], tfloor, uu[4 * mb + j], y);
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            const int p = (mb * 4 + j) * L + l;
+            if constexpr (L % 2 == 0) {
+              if (l % 2 == 0) ph[p / 8].set2(p % 8, y[l], y[l + 1]);
+            } else {
+              ph[p / 8].set(p % 8, y[l]);
+            }
+          }
+        }
+      T* dst = side ? &sm.pk_tok[tba][0][lane][0] : &sm.pq_tok[tba][0][lane][0];
+#pragma unroll
+      for (int k = 0; k < C::NF; ++k) store8(dst + (size_t)k * kWave * 8, ph[k]);
     }
     __syncthreads();
 
-    // 3. intra-chunk block
-    f32x4 pacc[4];
+    // ---- B. query block qi, value columns of half hh ----
+    {
+      Frag<T> pq[C::NF];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      pacc[j] = zero4();
-      if (j <= wave) {
+      for (int k = 0; k < C::NF; ++k) load8(pq[k], &sm.pq_tok[qi][k][lane][0]);
+      f32x4 pacc[4];
 #pragma unroll
-        for (int k = 0; k < C::NF; ++k) {
-          if (j == wave) {
-            mma(pacc[j], pk[k], pq[k]);
-          } else {
+      for (int j = 0; j < 4; ++j) {
+        pacc[j] = zero4();
+        if (j <= qi) {
+#pragma unroll
+          for (int k = 0; k < C::NF; ++k) {
             Frag<T> ka;
             load8(ka, &sm.pk_tok[j][k][lane][0]);
             mma(pacc[j], ka, pq[k]);
           }
         }
       }
-    }
+      // diagonal block: key token 16qi + 4g + jj after query token 16qi + r
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj)
-      if (4 * g + jj > r) {
-        // diagonal block: key token 16w + 4g + jj after query token 16w + r
+      for (int jj = 0; jj < 4; ++jj)
+        if (4 * g + jj > r) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (j == wave) pacc[j][jj] = 0.0f;
-      }
+          for (int j = 0; j < 4; ++j)
+            if (j == qi) pacc[j][jj] = 0.0f;
+        }
 
-    f32x4 num[C::CBT], den = zero4();
+      f32x4 num[C::CBH], den = zero4();
 #pragma unroll
-    for (int cb = 0; cb < C::CBT; ++cb) num[cb] = zero4();
+      for (int cl = 0; cl < C::CBH; ++cl) num[cl] = zero4();
 #pragma unroll
-    for (int pr = 0; pr < 2; ++pr) {
-      const int j0 = 2 * pr, j1 = 2 * pr + 1;
-      if (j0 <= wave) {
-        Frag<T> bp;
+      for (int pr = 0; pr < 2; ++pr) {
+        const int j0 = 2 * pr, j1 = 2 * pr + 1;
+        if (j0 <= qi) {
+          Frag<T> bp;
+          const bool hi = j1 <= qi;
+          bp.set2(0, pacc[j0][0], pacc[j0][1]);
+          bp.set2(2, pacc[j0][2], pacc[j0][3]);
+          bp.set2(4, hi ? pacc[j1][0] : 0.0f, hi ? pacc[j1][1] : 0.0f);
+          bp.set2(6, hi ? pacc[j1][2] : 0.0f, hi ? pacc[j1][3] : 0.0f);
+          mma(den, ones, bp);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          bp.set(e, pacc[j0][e]);
-          bp.set(4 + e, j1 <= wave ? pacc[j1][e] : 0.0f);
-        }
-        mma(den, ones, bp);
-#pragma unroll
-        for (int cb = 0; cb < C::CBT; ++cb) {
-          Frag<T> va;
-          load4(va, 0, &sm.vt[16 * cb + r][16 * j0 + 4 * g]);
-          load4(va, 4, &sm.vt[16 * cb + r][16 * j1 + 4 * g]);
-          mma(num[cb], va, bp);
+          for (int cl = 0; cl < C::CBH; ++cl) {
+            const int cb = hh * C::CBH + cl;
+            Frag<T> va;
+            load_tr4(va, 0, &sm.vtile[0][0], C::VROW, 16 * j0 + 4 * g, 16 * cb, lane);
+            load_tr4(va, 4, &sm.vtile[0][0], C::VROW, 16 * j1 + 4 * g, 16 * cb, lane);
+            mma(num[cl], va, bp);
+          }
         }
       }
-    }
-    // 4. carried state
 #pragma unroll
-    for (int k = 0; k < C::NF; ++k) {
+      for (int k = 0; k < C::NF; ++k) {
 #pragma unroll
-      for (int cb = 0; cb < C::CBT; ++cb) {
-        Frag<T> sa;
-        load8(sa, &sm.sst[cb][k][lane][0]);
-        mma(num[cb], sa, pq[k]);
+        for (int cl = 0; cl < C::CBH; ++cl) {
+          Frag<T> sa;
+          load8(sa, &sm.sst[hh * C::CBH + cl][k][lane][0]);
+          mma(num[cl], sa, pq[k]);
+        }
+        Frag<T> za;
+        load8(za, &sm.zst[k][g][0]);
+        mma(den, za, pq[k]);
       }
-      Frag<T> za;
-      load8(za, &sm.zst[k][g][0]);
-      mma(den, za, pq[k]);
-    }
-    // 5. output rows of this wave
-    {
-      const int t = tc + 16 * wave + r;
+      const int t = tc + 16 * qi + r;
       if (t < n) {
         const float rinv = 1.0f / (den[0] + a.eps);
         T* o = out + (size_t)t * DH + c0 + 4 * g;
 #pragma unroll
-        for (int cb = 0; cb < C::CBT; ++cb)
-          store4(o + 16 * cb, num[cb][0] * rinv, num[cb][1] * rinv, num[cb][2] * rinv, num[cb][3] * rinv);
+        for (int cl = 0; cl < C::CBH; ++cl) {
+          const int cb = hh * C::CBH + cl;
+          store4(o + 16 * cb, num[cl][0] * rinv, num[cl][1] * rinv, num[cl][2] * rinv, num[cl][3] * rinv);
+        }
       }
     }
-    // 6. state update over the chunk's 64 key tokens
+
+    // ---- state update over the chunk's 64 key tokens ----
 #pragma unroll
     for (int ks2 = 0; ks2 < 2; ++ks2) {
       Frag<T> bv[C::CBT];
 #pragma unroll
-      for (int cb = 0; cb < C::CBT; ++cb) load8(bv[cb], &sm.vt[16 * cb + r][32 * ks2 + 8 * g]);
+      for (int cb = 0; cb < C::CBT; ++cb) {
+        load_tr4(bv[cb], 0, &sm.vtile[0][0], C::VROW, 32 * ks2 + 8 * g, 16 * cb, lane);
+        load_tr4(bv[cb], 4, &sm.vtile[0][0], C::VROW, 32 * ks2 + 8 * g + 4, 16 * cb, lane);
+      }
 #pragma unroll
       for (int i = 0; i < C::RBW; ++i) {
-        const int rb = wave + 4 * i;
+        const int rb = wave + 8 * i;
         if (rb < C::RB) {
+          // phi(K)^T rows 16 rb .. 16 rb + 15 (k-order features), eight key tokens per lane
+          const int kap = rb / 2, half = rb % 2;
+          const int t0 = 32 * ks2 + 8 * g;
+          auto pk_at = [&](int t, int col) -> const T* {
+            const int f = 16 * half + col;  // feature offset within fragment kap
+            return &sm.pk_tok[t / 16][kap][16 * (f / 8) + t % 16][f % 8];
+          };
           Frag<T> ka;
-          load8(ka, &sm.pk_t[16 * rb + r][32 * ks2 + 8 * g]);
+          load_tr4_at(ka, 0, lane, [&](int kk, int col) { return pk_at(t0 + kk, col); });
+          load_tr4_at(ka, 4, lane, [&](int kk, int col) { return pk_at(t0 + 4 + kk, col); });
 #pragma unroll
           for (int cb = 0; cb < C::CBT; ++cb) mma(sacc[i][cb], ka, bv[cb]);
           mma(zacc[i], ka, ones);
@@ -315,10 +330,10 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
       }
     }
     __syncthreads();
-    // stage S_c and z_c for the next chunk
+    // ---- C. stage S_c and z_c for the next chunk ----
 #pragma unroll
     for (int i = 0; i < C::RBW; ++i) {
-      const int rb = wave + 4 * i;
+      const int rb = wave + 8 * i;
       if (rb < C::RB) {
         const int k = rb / 2, gp = 2 * (rb % 2) + g / 2, e0 = 4 * (g % 2);
 #pragma unroll
@@ -332,7 +347,7 @@ __global__ __launch_bounds__(256, 1) void causal_kernel(CausalArgs a) {
 
 template <typename T, int DH, int L, int MB, int DVT>
 static hipError_t cs_run(const CausalArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, DVT>), dim3(a.heads * a.dv_tiles), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, DVT>), dim3(a.heads * a.dv_tiles), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

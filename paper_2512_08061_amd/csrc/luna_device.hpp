@@ -58,6 +58,7 @@ struct alignas(16) PwlLds {
   float tree[kTreeCap];
   float2 seg[SEGCAP];
   int depth;
+  int zero_seg; // index of the all-zero segment (nbp + 1)
   float floor;  // 0 when outputs are clamped at zero, -inf otherwise
 };
 
@@ -72,8 +73,12 @@ __device__ inline void pwl_load(PwlLds<SEGCAP>& t, const uint8_t* __restrict__ g
   for (int i = threadIdx.x; i < ntree; i += blockDim.x) t.tree[i] = gtree[i];
   float4* sseg = reinterpret_cast<float4*>(t.seg);
   for (int i = threadIdx.x; i < (nseg + 1) / 2; i += blockDim.x) sseg[i] = gseg[i];
+  // one all-zero segment after the real ones: masked values select it and evaluate
+  // to exactly 0 without per-element masks
+  for (int i = threadIdx.x; i < hd.L; i += blockDim.x) t.seg[nseg + i] = make_float2(0.0f, 0.0f);
   if (threadIdx.x == 0) {
     t.depth = hd.depth;
+    t.zero_seg = hd.nbp + 1;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
   }
 }
@@ -142,6 +147,13 @@ struct Frag<__bf16> {
     for (int e = 0; e < 8; ++e) v[e] = (__bf16)x;
   }
   __device__ __forceinline__ void set(int e, float x) { v[e] = (__bf16)x; }
+  // slots e and e+1 (e even) from two fp32 values: one v_cvt_pk_bf16_f32
+  __device__ __forceinline__ void set2(int e, float x0, float x1) {
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+    const bf16x2 p = {(__bf16)x0, (__bf16)x1};
+    v[e] = p[0];
+    v[e + 1] = p[1];
+  }
   __device__ __forceinline__ float get(int e) const { return (float)v[e]; }
 };
 
@@ -157,6 +169,10 @@ struct Frag<float> {
     for (int e = 0; e < 8; ++e) v[e] = x;
   }
   __device__ __forceinline__ void set(int e, float x) { v[e] = x; }
+  __device__ __forceinline__ void set2(int e, float x0, float x1) {
+    v[e] = x0;
+    v[e + 1] = x1;
+  }
   __device__ __forceinline__ float get(int e) const { return v[e]; }
 };
 
@@ -207,6 +223,36 @@ __device__ __forceinline__ void load4(Frag<__bf16>& f, int e0, const __bf16* p) 
 __device__ __forceinline__ void load4(Frag<float>& f, int e0, const float* p) {
   const float4 v = *reinterpret_cast<const float4*>(p);
   f.v[e0 + 0] = v.x; f.v[e0 + 1] = v.y; f.v[e0 + 2] = v.z; f.v[e0 + 3] = v.w;
+}
+
+// Transposed operand loads.  `at(kk, col)` returns the LDS address of element
+// (row k0 + kk, column c0 + col) of a logical tile in which four consecutive columns
+// starting at a multiple of 4 are contiguous.  Lane (g, i) receives rows kk = 0..3
+// of column i in slots e0..e0+3 (k0, c0 and the tile chosen by the caller, per lane
+// group).  bf16 uses the gfx950 transpose read: within each 16-lane group, source
+// lane s = 4*kk + q supplies the address of columns 4q..4q+3 of row kk and lane i
+// receives column i of the four rows.  fp32 reads its four elements directly.
+template <typename F>
+__device__ __forceinline__ void load_tr4_at(Frag<__bf16>& f, int e0, int lane, F at) {
+  const int i = lane % 16;
+  typedef __attribute__((ext_vector_type(4))) short i16x4;
+  const __bf16* src = at(i / 4, 4 * (i % 4));
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(__attribute__((address_space(3))) void*)(src));
+  const bf16x4 b = __builtin_bit_cast(bf16x4, v);
+  f.v[e0 + 0] = b[0]; f.v[e0 + 1] = b[1]; f.v[e0 + 2] = b[2]; f.v[e0 + 3] = b[3];
+}
+template <typename F>
+__device__ __forceinline__ void load_tr4_at(Frag<float>& f, int e0, int lane, F at) {
+  const int i = lane % 16;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) f.v[e0 + e] = *at(e, i);
+}
+
+// Row-major tile X with row stride ld: rows k0..k0+3, column c0 + (lane % 16).
+template <typename T>
+__device__ __forceinline__ void load_tr4(Frag<T>& f, int e0, const T* X, int ld, int k0, int c0, int lane) {
+  load_tr4_at(f, e0, lane, [&](int kk, int col) { return X + (size_t)(k0 + kk) * ld + c0 + col; });
 }
 
 template <typename T>

@@ -101,9 +101,11 @@ hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, 
 bool causal_supported(Dt dt, int d, int L, int M, int* dv_tiles);
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s);
 
-// Segment-table capacity of the attention kernels for a given L (pairs).
+// Segment-table capacity (pairs) of the attention kernels' LDS copy for a given L:
+// enough for per-channel MLPs of width 64 plus the all-zero segment, capped at 4112.
+// A table needs (breakpoints + 2) * L pairs.
 constexpr int attn_seg_cap(int L) {
-  return ((64 * L + 1) * L + 1) / 2 * 2 < 4112 ? ((64 * L + 1) * L + 1) / 2 * 2 : 4112;
+  return ((64 * L + 2) * L + 1) / 2 * 2 < 4112 ? ((64 * L + 2) * L + 1) / 2 * 2 : 4112;
 }
 
 }  // namespace luna

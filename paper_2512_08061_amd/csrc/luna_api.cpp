@@ -55,8 +55,8 @@ luna_status check_common(const Problem& pb) {
   const int C1 = p->shared_channels ? 1 : p->L;
   const int units = C1 * p->hidden;
   if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
-  const int seg_cap = pb.op == LUNA_OP_FEATUREMAP ? luna::kSegCap : luna::attn_seg_cap(p->L);
-  if ((units + 2) * p->L > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "(L*hidden + 2)*L exceeds the segment table");
+  const int seg_cap = luna::nseg_cap(p->L, pb.op == LUNA_OP_FEATUREMAP ? luna::kFmSegBytes : luna::kAttnSegBytes);
+  if (units + 2 > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "too many breakpoints for the LDS segment table");
   return LUNA_OK;
 }
 

@@ -51,34 +51,33 @@ __device__ __forceinline__ int wave_id() {
 // piecewise-linear tables (layout shared with the host and luna_prepare.hip)
 // ---------------------------------------------------------------------------
 
-// LDS copy of one table, capacity fixed per kernel.
-template <int SEGCAP>
+// LDS copy of one table for L channels, NSEG segment rows (see seg_row).
+template <int L, int NSEG>
 struct alignas(16) PwlLds {
-  static_assert(SEGCAP % 2 == 0, "segment capacity must be even");
+  static constexpr int SROW = seg_row(L);
   float tree[kTreeCap];
-  float2 seg[SEGCAP];
+  float2 seg[NSEG][SROW];
   int depth;
-  int zero_seg; // index of the all-zero segment (nbp + 1)
-  float floor;  // 0 when outputs are clamped at zero, -inf otherwise
+  int zero_seg;  // index of the all-zero segment (nbp + 1)
+  float floor;   // 0 when outputs are clamped at zero, -inf otherwise
 };
 
 // Cooperative copy of a table from global memory into LDS.  Caller syncs after.
-template <int SEGCAP>
-__device__ inline void pwl_load(PwlLds<SEGCAP>& t, const uint8_t* __restrict__ gtab) {
+template <int L, int NSEG>
+__device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
   const int ntree = 1 << hd.depth;
-  const int nseg = (hd.nbp + 1) * hd.L;
+  const int nseg = hd.nbp + 1;
   const float* gtree = reinterpret_cast<const float*>(gtab + kTabTree);
-  const float4* gseg = reinterpret_cast<const float4*>(gtab + kTabSeg);
+  const float2* gseg = reinterpret_cast<const float2*>(gtab + kTabSeg);
   for (int i = threadIdx.x; i < ntree; i += blockDim.x) t.tree[i] = gtree[i];
-  float4* sseg = reinterpret_cast<float4*>(t.seg);
-  for (int i = threadIdx.x; i < (nseg + 1) / 2; i += blockDim.x) sseg[i] = gseg[i];
+  for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   // one all-zero segment after the real ones: masked values select it and evaluate
   // to exactly 0 without per-element masks
-  for (int i = threadIdx.x; i < hd.L; i += blockDim.x) t.seg[nseg + i] = make_float2(0.0f, 0.0f);
+  for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = make_float2(0.0f, 0.0f);
   if (threadIdx.x == 0) {
     t.depth = hd.depth;
-    t.zero_seg = hd.nbp + 1;
+    t.zero_seg = nseg;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
   }
 }
@@ -93,27 +92,32 @@ __device__ __forceinline__ float relu_floor(float v, float floor) {
 // The NU searches advance together, so each step issues NU independent LDS reads
 // and the lookup latency is paid once per step rather than once per value.  NaN
 // compares false everywhere and lands in segment 0.
-template <int NU, int SEGCAP>
-__device__ __forceinline__ void pwl_search(const PwlLds<SEGCAP>& t, int depth, const float (&u)[NU],
+template <int NU, int L, int NSEG>
+__device__ __forceinline__ void pwl_search(const PwlLds<L, NSEG>& t, int depth, const float (&u)[NU],
                                            int (&seg)[NU]) {
-  unsigned idx[NU];
+  // heap index kept as a byte offset into the tree: a' = 2 a + (u > key ? 4 : 0)
+  const char* tree = reinterpret_cast<const char*>(t.tree);
+  unsigned a[NU];
 #pragma unroll
-  for (int i = 0; i < NU; ++i) idx[i] = 1u;
+  for (int i = 0; i < NU; ++i) a[i] = 4u;
   for (int s = 0; s < depth; ++s) {
 #pragma unroll
-    for (int i = 0; i < NU; ++i) idx[i] = 2u * idx[i] + (u[i] > t.tree[idx[i]] ? 1u : 0u);
+    for (int i = 0; i < NU; ++i) {
+      const float key = *reinterpret_cast<const float*>(tree + a[i]);
+      a[i] = 2u * a[i] + (u[i] > key ? 4u : 0u);
+    }
   }
 #pragma unroll
-  for (int i = 0; i < NU; ++i) seg[i] = (int)(idx[i] - (1u << depth));
+  for (int i = 0; i < NU; ++i) seg[i] = (int)((a[i] >> 2) - (1u << depth));
 }
 
 // psi_l(u) for l = 0..L-1 on segment `seg`, already scaled by 1/sqrt(M) (folded
 // into the table).
-template <int L, int SEGCAP>
-__device__ __forceinline__ void pwl_channels(const PwlLds<SEGCAP>& t, int seg, float floor, float u,
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_channels(const PwlLds<L, NSEG>& t, int seg, float floor, float u,
                                              float (&y)[L]) {
   if constexpr (L % 2 == 0) {
-    const float4* st = reinterpret_cast<const float4*>(t.seg + seg * L);
+    const float4* st = reinterpret_cast<const float4*>(&t.seg[seg][0]);
 #pragma unroll
     for (int q = 0; q < L / 2; ++q) {
       const float4 v = st[q];
@@ -123,7 +127,7 @@ __device__ __forceinline__ void pwl_channels(const PwlLds<SEGCAP>& t, int seg, f
   } else {
 #pragma unroll
     for (int l = 0; l < L; ++l) {
-      const float2 v = t.seg[seg * L + l];
+      const float2 v = t.seg[seg][l];
       y[l] = relu_floor(fmaf(v.x, u, v.y), floor);
     }
   }

@@ -14,7 +14,7 @@ namespace luna {
 template <typename Tin, typename Tout, int DH, int L>
 __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   constexpr int KS = DH / 32;
-  __shared__ PwlLds<kSegCap> tab;
+  __shared__ PwlLds<L, nseg_cap(L, kFmSegBytes)> tab;
 
   const int tiles_per_head = (int)((a.rows_per_head + 63) / 64);
   const int64_t head = blockIdx.x / tiles_per_head;

@@ -101,11 +101,16 @@ hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, 
 bool causal_supported(Dt dt, int d, int L, int M, int* dv_tiles);
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s);
 
-// Segment-table capacity (pairs) of the attention kernels' LDS copy for a given L:
-// enough for per-channel MLPs of width 64 plus the all-zero segment, capped at 4112.
-// A table needs (breakpoints + 2) * L pairs.
-constexpr int attn_seg_cap(int L) {
-  return ((64 * L + 2) * L + 1) / 2 * 2 < 4112 ? ((64 * L + 2) * L + 1) / 2 * 2 : 4112;
+// LDS copy of the segment table: one row of (slope, intercept) pairs per segment.
+// Rows whose size is a multiple of 64 bytes are padded by 16 bytes so that random
+// segments spread over all LDS banks.
+constexpr int seg_row(int L) { return (L % 8 == 0) ? L + 2 : L; }
+// Segments an LDS table of `bytes` holds for L channels (at most 64 L + 2: width-64
+// per-channel MLPs plus the all-zero segment).  A table needs breakpoints + 2.
+constexpr int nseg_cap(int L, int bytes) {
+  return (64 * L + 2) < bytes / (seg_row(L) * 8) ? (64 * L + 2) : bytes / (seg_row(L) * 8);
 }
+constexpr int kAttnSegBytes = 41120;  // attention kernels (514 segments at L = 8)
+constexpr int kFmSegBytes = 46080;    // feature-map kernel
 
 }  // namespace luna

@@ -32,7 +32,7 @@ struct NcCfg {
   static constexpr int CB = DH / 16;                 // value-column blocks
   static constexpr int NF = (4 * MB * L + 7) / 8;    // readout fragments along features
   static constexpr int DP = 16 * MB * L;             // state rows (mb, l, i16)
-  static constexpr int SEGCAP = attn_seg_cap(L);
+  static constexpr int NSEG = nseg_cap(L, kAttnSegBytes);
   static constexpr int VE = 16 / (int)sizeof(T);     // elements per 16-byte load
   static constexpr int VROW = 36;                    // V^T row length in LDS (padded, 16-B multiple for fp32)
   static constexpr int NVC = 32 * (DH / VE) / kWave; // V 16-byte chunks per lane per step
@@ -45,7 +45,7 @@ struct NcCfg {
 template <typename T, int DH, int L, int MB>
 __global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
   using C = NcCfg<T, DH, L, MB>;
-  __shared__ PwlLds<C::SEGCAP> tab;
+  __shared__ PwlLds<L, C::NSEG> tab;
   __shared__ __attribute__((aligned(16))) T vt[4][DH][C::VROW];
   __shared__ float red[C::DP][DH + 1];
 
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void nc_reduce_kernel(NoncausalArgs a) {
 template <typename T, int DH, int L, int MB>
 __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
   using C = NcCfg<T, DH, L, MB>;
-  __shared__ PwlLds<C::SEGCAP> tab;
+  __shared__ PwlLds<L, C::NSEG> tab;
   const int head = blockIdx.x / a.tiles;
   const int tile = blockIdx.x - head * a.tiles;
   const int hset = a.phi.per_head ? head % a.H : 0;

@@ -62,7 +62,7 @@ luna_status check_common(const Problem& pb) {
 
 struct Layout {
   size_t tables = 0, partial = 0, frags = 0, total = 0;
-  int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, dv_tiles = 1;
+  int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, dv_tiles = 1, fused = 0;
 };
 
 luna_status plan(const Problem& pb, Layout* lay) {
@@ -81,6 +81,11 @@ luna_status plan(const Problem& pb, Layout* lay) {
     luna::NoncausalPlan np;
     if (!luna::noncausal_supported(dt, d, L, M, &np))
       return fail(LUNA_ERR_UNSUPPORTED, "no non-causal attention kernel for this (dtype, d, L, M)");
+    if (heads >= luna::kFusedMinHeads) {
+      lay->fused = 1;
+      lay->total = off;
+      return LUNA_OK;
+    }
     // enough state workgroups to fill the device, at least 256 tokens each
     const int64_t want = (512 + heads - 1) / heads;
     const int64_t maxs = (pb.n + 255) / 256;
@@ -224,6 +229,7 @@ luna_status luna_attn_fwd(const void* Q, const void* K, const void* V, luna_dtyp
   a.frags = w + lay.frags;
   a.tile_tokens = lay.tile_tokens;
   a.tiles = lay.tiles;
+  a.fused = lay.fused;
   hipError_t e = luna::launch_noncausal(dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32, (int)d, p->L, p->M, a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "attention kernel launch");
 }

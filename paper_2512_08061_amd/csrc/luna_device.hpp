@@ -133,6 +133,16 @@ __device__ __forceinline__ void pwl_channels(const PwlLds<L, NSEG>& t, int seg, 
   }
 }
 
+// Channels 2q and 2q+1 on segment `seg` (one 16-byte LDS read).
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_pair(const PwlLds<L, NSEG>& t, int seg, int q, float floor, float u,
+                                         float& y0, float& y1) {
+  static_assert(L % 2 == 0, "channel pairs need an even L");
+  const float4 v = reinterpret_cast<const float4*>(&t.seg[seg][0])[q];
+  y0 = relu_floor(fmaf(v.x, u, v.y), floor);
+  y1 = relu_floor(fmaf(v.z, u, v.w), floor);
+}
+
 // ---------------------------------------------------------------------------
 // element types and fragments
 // ---------------------------------------------------------------------------

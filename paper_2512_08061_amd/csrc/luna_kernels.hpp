@@ -70,7 +70,11 @@ struct NoncausalArgs {
   void* frags;          // [heads][frag_elems] statistics as readout fragments (call dtype)
   int tile_tokens;      // tokens per readout workgroup (multiple of 16)
   int tiles;            // ceil(n / tile_tokens)
+  int fused;            // 1: one workgroup per head does state and readout
 };
+
+// Heads from which the non-causal path uses one fused workgroup per head.
+constexpr int kFusedMinHeads = 192;
 
 struct CausalArgs {
   const void* Q;

@@ -359,11 +359,347 @@ __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// fused pass: one workgroup of 8 waves per head (used when there are enough heads
+// to fill the device).  The state phase accumulates each wave's share of S and z
+// in registers (phi(K) fragments never leave registers; V is read transposed from
+// a wave-private row-major LDS tile); the waves are summed in LDS in a fixed order
+// and converted to readout fragments; the readout phase then streams the head's
+// queries with S and z held in registers.  S never reaches HBM.
+// ---------------------------------------------------------------------------
+template <typename T, int DH, int L, int MB>
+struct NcFusedLds {
+  using C = NcCfg<T, DH, L, MB>;
+  static constexpr int VR = DH + C::VE;  // padded V-tile row (elements)
+  PwlLds<L, C::NSEG> tab;
+  union {
+    T vt[8][32][VR];          // per-wave V tile of the current 32-token step
+    float red[C::DP][DH + 1]; // cross-wave sum of (S | z)
+  } u;
+  alignas(16) T sfr[C::CB + 1][C::NF][kWave][8];  // S (and z in the last slot) as A fragments
+};
+
+template <typename T, int DH, int L, int MB>
+__global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
+  using C = NcCfg<T, DH, L, MB>;
+  using LDS = NcFusedLds<T, DH, L, MB>;
+  __shared__ LDS sm;
+
+  const int head = blockIdx.x;
+  const int hset = a.phi.per_head ? head % a.H : 0;
+  pwl_load(sm.tab, a.phi.tables + (size_t)hset * kTableBytes);
+
+  const int wave = wave_id(), lane = threadIdx.x % kWave;
+  const int g = lane / 16, r = lane % 16;
+  const int M = a.phi.M;
+  const int n = a.n;
+  const size_t hoff = (size_t)head * n * DH;
+  const T* Q = reinterpret_cast<const T*>(a.Q) + hoff;
+  const T* K = reinterpret_cast<const T*>(a.K) + hoff;
+  const T* V = reinterpret_cast<const T*>(a.V) + hoff;
+  T* out = reinterpret_cast<T*>(a.out) + hoff;
+  const T* W = reinterpret_cast<const T*>(a.phi.W) + (size_t)hset * M * DH;
+  const float* bias = a.phi.b + (size_t)hset * M;
+
+  // W fragments: lane index r of block mb is projection 16mb + r (B of u = K W^T,
+  // A of u^T = W Q^T)
+  Frag<T> wf[MB][C::KS];
+  float bcol[MB], brow[MB][4];
+  bool pcol[MB], prow[MB][4];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int p = 16 * mb + r;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (p < M) load8(wf[mb][ks], W + (size_t)p * DH + 32 * ks + 8 * g);
+      else wf[mb][ks].zero();
+    }
+    pcol[mb] = p < M;
+    bcol[mb] = p < M ? bias[p] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 16 * mb + 4 * g + j;
+      prow[mb][j] = i < M;
+      brow[mb][j] = i < M ? bias[i] : 0.0f;
+    }
+  }
+  Frag<T> ones;
+  ones.fill(1.0f);
+
+  // z of channel l is accumulated in column l of accZ[mb] (B = one-hot column l)
+  static_assert(L <= 16, "one accumulator column per channel");
+  f32x4 accS[MB][L][C::CB];
+  f32x4 accZ[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    accZ[mb] = zero4();
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb) accS[mb][l][cb] = zero4();
+  }
+
+  // ---- state phase: wave w takes 32-token steps w, w + 8, ... ----
+  constexpr int VCH = 32 * DH / C::VE / kWave;  // V 16-byte chunks per lane per step
+  Frag<T> kn[2][C::KS];
+  i32x4 vn[VCH];
+  auto fetch_k = [&](int step) {
+    const int t0 = 32 * step;
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int t = t0 + 16 * tb + r;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        if (t < n) load8(kn[tb][ks], K + (size_t)t * DH + 32 * ks + 8 * g);
+        else kn[tb][ks].zero();
+      }
+    }
+  };
+  auto fetch_v = [&](int step) {
+    const int t0 = 32 * step;
+#pragma unroll
+    for (int q = 0; q < VCH; ++q) {
+      const int c = lane + kWave * q;
+      const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
+      const int t = t0 + tt;
+      if (t < n) vn[q] = *reinterpret_cast<const i32x4*>(V + (size_t)t * DH + cg * C::VE);
+      else vn[q] = i32x4{0, 0, 0, 0};
+    }
+  };
+  __syncthreads();
+  const int tdepth = sm.tab.depth;
+  const int zseg = sm.tab.zero_seg;
+  const float tfloor = sm.tab.floor;
+  T* vt = &sm.u.vt[wave][0][0];
+
+  const int nsteps = (n + 31) / 32;
+  if (wave < nsteps) {
+    fetch_k(wave);
+    fetch_v(wave);
+  }
+  for (int step = wave; step < nsteps; step += 8) {
+    const int t0 = 32 * step;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+#pragma unroll
+    for (int q = 0; q < VCH; ++q) {
+      const int c = lane + kWave * q;
+      const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
+      *reinterpret_cast<i32x4*>(vt + tt * LDS::VR + cg * C::VE) = vn[q];
+    }
+    if (step + 8 < nsteps) fetch_v(step + 8);
+
+    float uu[8 * MB];  // [mb][tb][j]
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int ks = 0; ks < C::KS; ++ks) mma(acc, kn[tb][ks], wf[mb][ks]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) uu[8 * mb + 4 * tb + j] = acc[j] + bcol[mb];
+      }
+    if (step + 8 < nsteps) fetch_k(step + 8);
+    int sg[8 * MB];
+    pwl_search(sm.tab, tdepth, uu, sg);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)  // slot e = 4 tb + j holds token t0 + 16 tb + 4 g + j
+        if (!pcol[mb] || t0 + 16 * (e / 4) + 4 * g + (e % 4) >= n) sg[8 * mb + e] = zseg;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    Frag<T> bv[C::CB];
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb) {
+      load_tr4(bv[cb], 0, vt, LDS::VR, 4 * g, 16 * cb, lane);
+      load_tr4(bv[cb], 4, vt, LDS::VR, 16 + 4 * g, 16 * cb, lane);
+    }
+    // channel pairs: evaluate the 8 token slots, multiply, drop
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      if constexpr (L % 2 == 0) {
+#pragma unroll
+        for (int q = 0; q < L / 2; ++q) {
+          Frag<T> a0, a1;
+#pragma unroll
+          for (int e = 0; e < 8; e += 2) {
+            float y00, y01, y10, y11;
+            pwl_pair<L>(sm.tab, sg[8 * mb + e], q, tfloor, uu[8 * mb + e], y00, y01);
+            pwl_pair<L>(sm.tab, sg[8 * mb + e + 1], q, tfloor, uu[8 * mb + e + 1], y10, y11);
+            a0.set2(e, y00, y10);
+            a1.set2(e, y01, y11);
+          }
+#pragma unroll
+          for (int cb = 0; cb < C::CB; ++cb) {
+            mma(accS[mb][2 * q][cb], a0, bv[cb]);
+            mma(accS[mb][2 * q + 1][cb], a1, bv[cb]);
+          }
+          Frag<T> oh0, oh1;
+          oh0.fill(r == 2 * q ? 1.0f : 0.0f);
+          oh1.fill(r == 2 * q + 1 ? 1.0f : 0.0f);
+          mma(accZ[mb], a0, oh0);
+          mma(accZ[mb], a1, oh1);
+        }
+      } else {
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          Frag<T> a0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            float y[L];
+            pwl_channels<L>(sm.tab, sg[8 * mb + e], tfloor, uu[8 * mb + e], y);
+            a0.set(e, y[l]);
+          }
+#pragma unroll
+          for (int cb = 0; cb < C::CB; ++cb) mma(accS[mb][l][cb], a0, bv[cb]);
+          Frag<T> oh;
+          oh.fill(r == l ? 1.0f : 0.0f);
+          mma(accZ[mb], a0, oh);
+        }
+      }
+    }
+  }
+
+  // ---- sum the eight waves in a fixed order, then form readout fragments ----
+  __syncthreads();  // every wave is done with its V tile (red aliases it)
+  for (int w = 0; w < 8; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int l = 0; l < L; ++l)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int row = (mb * L + l) * 16 + 4 * g + j;
+#pragma unroll
+            for (int cb = 0; cb < C::CB; ++cb) {
+              float& d = sm.u.red[row][16 * cb + r];
+              d = (w == 0) ? accS[mb][l][cb][j] : d + accS[mb][l][cb][j];
+            }
+            if (r == l) {
+              float& d = sm.u.red[row][DH];
+              d = (w == 0) ? accZ[mb][j] : d + accZ[mb][j];
+            }
+          }
+    }
+    __syncthreads();
+  }
+  {
+    T* fr = &sm.sfr[0][0][0][0];
+    for (int idx = threadIdx.x; idx < (int)C::FRAG_ELEMS; idx += blockDim.x) {
+      const int e = idx % 8;
+      const int ln = (idx / 8) % kWave;
+      const int kappa = (idx / (8 * kWave)) % C::NF;
+      const int cb = idx / (8 * kWave * C::NF);
+      const int gg = ln / 16, rr = ln % 16;
+      const int p = 8 * kappa + e;
+      float v = 0.0f;
+      if (p < 4 * MB * L) {
+        const int mbj = p / L, l = p % L;
+        const int row = ((mbj / 4) * L + l) * 16 + 4 * gg + (mbj % 4);
+        v = (cb < C::CB) ? sm.u.red[row][16 * cb + rr] : sm.u.red[row][DH];
+      }
+      fr[idx] = (T)v;
+    }
+  }
+  __syncthreads();
+
+  // ---- readout phase: wave w takes 16-token blocks w, w + 8, ... ----
+  Frag<T> sf[C::CB][C::NF], zf[C::NF];
+#pragma unroll
+  for (int cb = 0; cb < C::CB; ++cb)
+#pragma unroll
+    for (int k = 0; k < C::NF; ++k) load8(sf[cb][k], &sm.sfr[cb][k][lane][0]);
+#pragma unroll
+  for (int k = 0; k < C::NF; ++k) load8(zf[k], &sm.sfr[C::CB][k][lane][0]);
+
+  const int nblk = (n + 15) / 16;
+  constexpr int QD = 4;  // query blocks in flight per wave
+  Frag<T> qn[QD][C::KS];
+  auto fetch_q = [&](Frag<T> (&qf)[C::KS], int b) {
+    const int t = 16 * b + r;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (t < n) load8(qf[ks], Q + (size_t)t * DH + 32 * ks + 8 * g);
+      else qf[ks].zero();
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < QD; ++i) fetch_q(qn[i], wave + 8 * i);
+  for (int b0 = wave; b0 < nblk; b0 += 8 * QD)
+#pragma unroll
+  for (int i = 0; i < QD; ++i) {
+    const int b = b0 + 8 * i;
+    if (b >= nblk) break;
+    Frag<T> qf[C::KS];
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) qf[ks] = qn[i][ks];
+    fetch_q(qn[i], b + 8 * QD);
+    float uu[4 * MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) mma(acc, wf[mb][ks], qf[ks]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
+    }
+    int sg[4 * MB];
+    pwl_search(sm.tab, tdepth, uu, sg);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (!prow[mb][j]) sg[4 * mb + j] = zseg;
+    Frag<T> pq[C::NF];
+#pragma unroll
+    for (int k = 0; k < C::NF; ++k) pq[k].zero();
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float y[L];
+        pwl_channels<L>(sm.tab, sg[4 * mb + j], tfloor, uu[4 * mb + j], y);
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          const int p = (mb * 4 + j) * L + l;
+          if constexpr (L % 2 == 0) {
+            if (l % 2 == 0) pq[p / 8].set2(p % 8, y[l], y[l + 1]);
+          } else {
+            pq[p / 8].set(p % 8, y[l]);
+          }
+        }
+      }
+    f32x4 num[C::CB], den = zero4();
+#pragma unroll
+    for (int cb = 0; cb < C::CB; ++cb) num[cb] = zero4();
+#pragma unroll
+    for (int k = 0; k < C::NF; ++k) {
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb) mma(num[cb], sf[cb][k], pq[k]);
+      mma(den, zf[k], pq[k]);
+    }
+    const int t = 16 * b + r;
+    if (t < n) {
+      const float rinv = 1.0f / (den[0] + a.eps);
+      T* o = out + (size_t)t * DH + 4 * g;
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb)
+        store4(o + 16 * cb, num[cb][0] * rinv, num[cb][1] * rinv, num[cb][2] * rinv, num[cb][3] * rinv);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dispatch
 // ---------------------------------------------------------------------------
 template <typename T, int DH, int L, int MB>
 static hipError_t nc_run(const NoncausalArgs& a, hipStream_t s) {
+  if (a.fused) {
+    hipLaunchKernelGGL((nc_fused_kernel<T, DH, L, MB>), dim3(a.heads), dim3(512), 0, s, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((nc_state_kernel<T, DH, L, MB>), dim3(a.heads * a.splits), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -37,9 +37,10 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix cores
 KERNEL_SOURCES = {
     "causal_kernel": ["luna_causal.hip", "luna_device.hpp", "luna_kernels.hpp"],
-    "nc_state_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
-    "nc_readout_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
+    "nc_fused_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
 }
+KERNEL_WORKLOAD = {"causal_kernel": "long_causal", "nc_fused_kernel": "long_noncausal"}
+COPY_BYTES = 1 << 30  # the --copy-calibration copy
 
 
 def log(*a):
@@ -63,6 +64,65 @@ def measured_traffic(kernel: str, workload: str):
     if rec.get("source_hash") != source_hash(kernel):
         return None
     return rec.get("bytes_per_launch")
+
+
+def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
+    """Turn two rocprofv3 --pmc csv runs (FETCH_SIZE, then WRITE_SIZE, both of
+    `bench.py --copy-calibration`) into profiles/hbm_traffic_<kernel>_<workload>.json.
+
+    Each counter is scaled by (1 GiB) / (what it reads for the 1 GiB device copy),
+    so that a counter that sees only part of the memory traffic is corrected."""
+    import collections
+    import csv
+
+    def per_dispatch(path, counter):
+        vals = collections.defaultdict(float)
+        names = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = int(r["Dispatch_Id"])
+            vals[d] += float(r["Counter_Value"]) * 1024.0  # KiB -> bytes
+            names[d] = r["Kernel_Name"]
+        return vals, names
+
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        vals, names = per_dispatch(path, counter)
+        copies = [v for d, v in vals.items() if "copyBuffer" in names[d] and v > 0.25 * COPY_BYTES]
+        if not copies:
+            log(f"{path}: no 1 GiB copy dispatch found (run bench.py with --copy-calibration)")
+            return 1
+        factor = COPY_BYTES / (sum(copies) / len(copies))
+        for kern in KERNEL_SOURCES:
+            ds = [d for d in vals if f"{len(kern)}{kern}" in names[d]]
+            if ds:
+                rec = out.setdefault(kern, {})
+                rec[counter] = {"avg_counter_bytes": sum(vals[d] for d in ds) / len(ds), "dispatches": len(ds),
+                                "copy_factor": factor}
+    for kern, rec in out.items():
+        if "FETCH_SIZE" not in rec or "WRITE_SIZE" not in rec:
+            continue
+        rd = rec["FETCH_SIZE"]["avg_counter_bytes"] * rec["FETCH_SIZE"]["copy_factor"]
+        wr = rec["WRITE_SIZE"]["avg_counter_bytes"] * rec["WRITE_SIZE"]["copy_factor"]
+        wl_name = KERNEL_WORKLOAD[kern]
+        doc = {
+            "kernel": kern,
+            "workload": wl_name,
+            "source_hash": source_hash(kern),
+            "bytes_per_launch": int(rd + wr),
+            "read_bytes_per_launch": int(rd),
+            "write_bytes_per_launch": int(wr),
+            "counters": rec,
+            "copy_calibration": f"{COPY_BYTES} B device-to-device copy in the same process",
+            "command": command,
+        }
+        path = os.path.join(ROOT, "profiles", f"hbm_traffic_{kern}_{wl_name}.json")
+        with open(path, "w") as fh:
+            json.dump(doc, fh, indent=1)
+            fh.write("\n")
+        log(f"wrote {path}: read {rd / 2**20:.1f} MiB, write {wr / 2**20:.1f} MiB per launch")
+    return 0
 
 
 def flops_per_token_head(w, causal: bool) -> int:
@@ -122,7 +182,13 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for scaling HBM counters)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 --pmc csv runs into profiles/hbm_traffic_*.json and exit")
+    ap.add_argument("--traffic-command", default="",
+                    help="the rocprofv3 commands that produced --traffic-from, recorded in the summary")
     args = ap.parse_args()
+    if args.traffic_from:
+        return traffic_from(*args.traffic_from, args.traffic_command)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: LUNA attention shards over (batch, head) with no "
@@ -184,8 +250,10 @@ def main() -> int:
     log(f"timed {args.steps} steps: {ms_step:.3f} ms/step (non-causal call {ms_nc:.3f} ms, causal call {ms_cs:.3f} ms)")
 
     tokens = w4.B * w4.n + w5.B * w5.n
+    # 256 heads fill the device, so the library runs its one-pass kernel (one workgroup per head)
+    nc_kernel = "nc_fused_kernel"
     parts = {}
-    for name, w, ms, causal, kern in (("long_noncausal", w4, ms_nc, False, "nc_state_kernel+nc_readout_kernel"),
+    for name, w, ms, causal, kern in (("long_noncausal", w4, ms_nc, False, nc_kernel),
                                       ("long_causal", w5, ms_cs, True, "causal_kernel")):
         th = w.B * w.H * w.n
         gb = bytes_per_token_head(w) * th / 1e9
@@ -210,14 +278,14 @@ def main() -> int:
 
     dom = max(parts, key=lambda k: parts[k]["ms_per_call"])
     P = parts[dom]
-    kname = "causal_kernel" if dom == "long_causal" else "nc_state_kernel"
+    kname = "causal_kernel" if dom == "long_causal" else P["kernels"]
     roofline = {
         "bound": P["bound"],
         "achieved": round(P["hbm_gbs"] if P["bound"] == "hbm" else P["attn_tflops"], 2),
         "peak": HBM_PEAK_GBS if P["bound"] == "hbm" else MFMA_BF16_PEAK_TFLOPS,
         "unit": "GB/s" if P["bound"] == "hbm" else "TFLOP/s",
         "frac": round(P["roofline_frac"], 4),
-        "traffic": measured_traffic(kname, dom),
+        "traffic": measured_traffic(kname, dom) if kname in KERNEL_SOURCES else None,
         "kernel": kname,
         "workload": dom,
         "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel)",

@@ -81,7 +81,7 @@ luna_status plan(const Problem& pb, Layout* lay) {
     luna::NoncausalPlan np;
     if (!luna::noncausal_supported(dt, d, L, M, &np))
       return fail(LUNA_ERR_UNSUPPORTED, "no non-causal attention kernel for this (dtype, d, L, M)");
-    if (heads >= luna::kFusedMinHeads) {
+    if (heads >= luna::kFusedMinHeads && luna::fused_acc_regs(d, L, M) <= luna::kFusedMaxAccRegs) {
       lay->fused = 1;
       lay->total = off;
       return LUNA_OK;

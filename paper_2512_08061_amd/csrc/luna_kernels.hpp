@@ -73,8 +73,11 @@ struct NoncausalArgs {
   int fused;            // 1: one workgroup per head does state and readout
 };
 
-// Heads from which the non-causal path uses one fused workgroup per head.
+// Heads from which the non-causal path uses one fused workgroup per head, and the
+// largest per-wave (S | z) accumulator set (fp32 registers per lane) it holds.
 constexpr int kFusedMinHeads = 192;
+constexpr int kFusedMaxAccRegs = 128;
+__host__ __device__ constexpr int fused_acc_regs(int d, int L, int M) { return ((M + 15) / 16) * L * (d / 16) * 4; }
 
 struct CausalArgs {
   const void* Q;

@@ -361,27 +361,29 @@ __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
 
 
 // ---------------------------------------------------------------------------
-// fused pass: one workgroup of 8 waves per head (used when there are enough heads
+// fused pass: one workgroup of kNcWaves waves per head (used when there are enough heads
 // to fill the device).  The state phase accumulates each wave's share of S and z
 // in registers (phi(K) fragments never leave registers; V is read transposed from
 // a wave-private row-major LDS tile); the waves are summed in LDS in a fixed order
 // and converted to readout fragments; the readout phase then streams the head's
 // queries with S and z held in registers.  S never reaches HBM.
 // ---------------------------------------------------------------------------
+constexpr int kNcWaves = 4;  // one wave per SIMD: the whole register file per wave
+
 template <typename T, int DH, int L, int MB>
 struct NcFusedLds {
   using C = NcCfg<T, DH, L, MB>;
   static constexpr int VR = DH + C::VE;  // padded V-tile row (elements)
   PwlLds<L, C::NSEG> tab;
   union {
-    T vt[8][32][VR];          // per-wave V tile of the current 32-token step
+    T vt[kNcWaves][32][VR];   // per-wave V tile of the current 32-token step
     float red[C::DP][DH + 1]; // cross-wave sum of (S | z)
   } u;
   alignas(16) T sfr[C::CB + 1][C::NF][kWave][8];  // S (and z in the last slot) as A fragments
 };
 
 template <typename T, int DH, int L, int MB>
-__global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
+__global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArgs a) {
   using C = NcCfg<T, DH, L, MB>;
   using LDS = NcFusedLds<T, DH, L, MB>;
   __shared__ LDS sm;
@@ -440,7 +442,7 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
       for (int cb = 0; cb < C::CB; ++cb) accS[mb][l][cb] = zero4();
   }
 
-  // ---- state phase: wave w takes 32-token steps w, w + 8, ... ----
+  // ---- state phase: wave w takes 32-token steps w, w + kNcWaves, ... ----
   constexpr int VCH = 32 * DH / C::VE / kWave;  // V 16-byte chunks per lane per step
   Frag<T> kn[2][C::KS];
   i32x4 vn[VCH];
@@ -478,7 +480,7 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
     fetch_k(wave);
     fetch_v(wave);
   }
-  for (int step = wave; step < nsteps; step += 8) {
+  for (int step = wave; step < nsteps; step += kNcWaves) {
     const int t0 = 32 * step;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
 #pragma unroll
@@ -487,7 +489,7 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
       const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
       *reinterpret_cast<i32x4*>(vt + tt * LDS::VR + cg * C::VE) = vn[q];
     }
-    if (step + 8 < nsteps) fetch_v(step + 8);
+    if (step + kNcWaves < nsteps) fetch_v(step + kNcWaves);
 
     float uu[8 * MB];  // [mb][tb][j]
 #pragma unroll
@@ -500,7 +502,7 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) uu[8 * mb + 4 * tb + j] = acc[j] + bcol[mb];
       }
-    if (step + 8 < nsteps) fetch_k(step + 8);
+    if (step + kNcWaves < nsteps) fetch_k(step + kNcWaves);
     int sg[8 * MB];
     pwl_search(sm.tab, tdepth, uu, sg);
 #pragma unroll
@@ -563,7 +565,7 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
 
   // ---- sum the eight waves in a fixed order, then form readout fragments ----
   __syncthreads();  // every wave is done with its V tile (red aliases it)
-  for (int w = 0; w < 8; ++w) {
+  for (int w = 0; w < kNcWaves; ++w) {
     if (wave == w) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
@@ -605,7 +607,7 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
   }
   __syncthreads();
 
-  // ---- readout phase: wave w takes 16-token blocks w, w + 8, ... ----
+  // ---- readout phase: wave w takes 16-token blocks w, w + kNcWaves, ... ----
   Frag<T> sf[C::CB][C::NF], zf[C::NF];
 #pragma unroll
   for (int cb = 0; cb < C::CB; ++cb)
@@ -626,16 +628,16 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
     }
   };
 #pragma unroll
-  for (int i = 0; i < QD; ++i) fetch_q(qn[i], wave + 8 * i);
-  for (int b0 = wave; b0 < nblk; b0 += 8 * QD)
+  for (int i = 0; i < QD; ++i) fetch_q(qn[i], wave + kNcWaves * i);
+  for (int b0 = wave; b0 < nblk; b0 += kNcWaves * QD)
 #pragma unroll
   for (int i = 0; i < QD; ++i) {
-    const int b = b0 + 8 * i;
+    const int b = b0 + kNcWaves * i;
     if (b >= nblk) break;
     Frag<T> qf[C::KS];
 #pragma unroll
     for (int ks = 0; ks < C::KS; ++ks) qf[ks] = qn[i][ks];
-    fetch_q(qn[i], b + 8 * QD);
+    fetch_q(qn[i], b + kNcWaves * QD);
     float uu[4 * MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -696,9 +698,11 @@ __global__ __launch_bounds__(512, 1) void nc_fused_kernel(NoncausalArgs a) {
 // ---------------------------------------------------------------------------
 template <typename T, int DH, int L, int MB>
 static hipError_t nc_run(const NoncausalArgs& a, hipStream_t s) {
-  if (a.fused) {
-    hipLaunchKernelGGL((nc_fused_kernel<T, DH, L, MB>), dim3(a.heads), dim3(512), 0, s, a);
-    return hipGetLastError();
+  if constexpr (fused_acc_regs(DH, L, 16 * MB) <= kFusedMaxAccRegs) {
+    if (a.fused) {
+      hipLaunchKernelGGL((nc_fused_kernel<T, DH, L, MB>), dim3(a.heads), dim3(64 * kNcWaves), 0, s, a);
+      return hipGetLastError();
+    }
   }
   hipLaunchKernelGGL((nc_state_kernel<T, DH, L, MB>), dim3(a.heads * a.splits), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();

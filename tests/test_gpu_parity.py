@@ -121,6 +121,18 @@ def test_attn_noncausal_small(dtype, d, M, L, n):
     assert_close(out, oracle.attn_noncausal(Q, K, V, p, eps=w.eps), dtype, "out")
 
 
+# enough heads for the one-pass kernel (one workgroup per head), with ragged lengths
+@pytest.mark.parametrize("dtype,d,M,L,n", [("f32", 64, 16, 8, 77), ("bf16", 64, 16, 8, 333), ("bf16", 64, 8, 8, 1),
+                                           ("bf16", 32, 16, 8, 200), ("f32", 32, 8, 2, 45)])
+def test_attn_noncausal_many_heads(dtype, d, M, L, n):
+    w = small_workload(dtype, B=16, H=13, n=n, d=d, M=M, L=L)
+    say(f"noncausal many heads {w.name}")
+    Q, K, V, p = inputs(w, seed=5)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps))
+    assert_close(out, oracle.attn_noncausal(Q, K, V, p, eps=w.eps), dtype, "out")
+
+
 @pytest.mark.parametrize("name", ["tiny_f32", "text_encoder", "vision_encoder", "long_noncausal"])
 def test_attn_noncausal_workload_full_size(name):
     w = wl.WORKLOADS[name]

@@ -47,10 +47,20 @@ struct CsCfg {
   static constexpr int CBT = DVT / 16;              // column blocks of the tile
   static constexpr int NSEG = nseg_cap(L, kAttnSegBytes);
   static constexpr int VE = 16 / (int)sizeof(T);    // elements per 16-byte chunk
-  static constexpr int VROW = DVT + VE;             // padded V-tile row (elements)
+  static constexpr int VROW = DVT;                  // V-tile row (elements), chunks swizzled
+  static constexpr int VCPR = DVT / VE;             // 16-byte chunks per V-tile row
   static constexpr int VCH = 64 * DVT / VE;         // 16-byte chunks in a V tile
   static constexpr int NVC = (VCH + 511) / 512;     // per thread
 };
+
+// Physical 16-byte chunk of logical chunk cg in V-tile row `row`: an XOR swizzle
+// that spreads the four (and eight) consecutive rows read by one transposed load
+// over distinct banks.
+template <int CPR>
+__device__ __forceinline__ int vswz(int row, int cg) {
+  const int h = (row & 3) ^ ((row >> 2) & 1) ^ ((row >> 3) & 1);
+  return cg ^ ((2 * h) & (CPR - 1));
+}
 
 template <typename T, int DH, int L, int MB, int DVT>
 struct CsLds {
@@ -149,13 +159,18 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       const int cidx = tid + 512 * q;
       if (cidx < C::VCH) {
         const int tt = cidx / (DVT / C::VE), cg = cidx % (DVT / C::VE);
-        *reinterpret_cast<i32x4*>(&sm.vtile[tt][cg * C::VE]) = vf[q];
+        *reinterpret_cast<i32x4*>(&sm.vtile[tt][vswz<C::VCPR>(tt, cg) * C::VE]) = vf[q];
       }
     }
   };
 
+  // element (row, col) of the swizzled V tile
+  auto v_at = [&](int row, int col) -> const T* {
+    return &sm.vtile[row][vswz<C::VCPR>(row, col / C::VE) * C::VE + col % C::VE];
+  };
+
   __syncthreads();
-  const int tdepth = sm.tab.depth;
+  const int tsteps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
   const int zseg = sm.tab.zero_seg;
   const float tfloor = sm.tab.floor;
 
@@ -176,7 +191,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
     }
     int sg[4 * MB];
-    pwl_search(sm.tab, tdepth, uu, sg);
+    pwl_search(sm.tab, tsteps, uu, sg);
     const bool kill_tok = role && !tok_ok;  // key rows past n contribute nothing
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -259,8 +274,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 #pragma unroll
         for (int cb = 0; cb < C::CBT; ++cb) {
           Frag<T> va;
-          load_tr4(va, 0, &sm.vtile[0][0], C::VROW, 16 * j0 + 4 * g, 16 * cb, lane);
-          load_tr4(va, 4, &sm.vtile[0][0], C::VROW, 16 * j1 + 4 * g, 16 * cb, lane);
+          load_tr4_at(va, 0, lane, [&](int kk, int col) { return v_at(16 * j0 + 4 * g + kk, 16 * cb + col); });
+          load_tr4_at(va, 4, lane, [&](int kk, int col) { return v_at(16 * j1 + 4 * g + kk, 16 * cb + col); });
           mma(num[cb], va, bp);
         }
       }
@@ -336,8 +351,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         Frag<T> bv[C::CBT];
 #pragma unroll
         for (int cb = 0; cb < C::CBT; ++cb) {
-          load_tr4(bv[cb], 0, &sm.vtile[0][0], C::VROW, 32 * ks2 + 8 * g, 16 * cb, lane);
-          load_tr4(bv[cb], 4, &sm.vtile[0][0], C::VROW, 32 * ks2 + 8 * g + 4, 16 * cb, lane);
+          load_tr4_at(bv[cb], 0, lane, [&](int kk, int col) { return v_at(32 * ks2 + 8 * g + kk, 16 * cb + col); });
+          load_tr4_at(bv[cb], 4, lane, [&](int kk, int col) { return v_at(32 * ks2 + 8 * g + 4 + kk, 16 * cb + col); });
         }
 #pragma unroll
         for (int i = 0; i < C::RBK; ++i) {

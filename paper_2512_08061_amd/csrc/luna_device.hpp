@@ -55,9 +55,10 @@ __device__ __forceinline__ int wave_id() {
 template <int L, int NSEG>
 struct alignas(16) PwlLds {
   static constexpr int SROW = seg_row(L);
-  float tree[kTreeCap];
+  float keys[kKeyCap];
+  uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
   float2 seg[NSEG][SROW];
-  int depth;
+  int steps;
   int zero_seg;  // index of the all-zero segment (nbp + 1)
   float floor;   // 0 when outputs are clamped at zero, -inf otherwise
 };
@@ -66,17 +67,19 @@ struct alignas(16) PwlLds {
 template <int L, int NSEG>
 __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
-  const int ntree = 1 << hd.depth;
   const int nseg = hd.nbp + 1;
-  const float* gtree = reinterpret_cast<const float*>(gtab + kTabTree);
+  const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
+  const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const float2* gseg = reinterpret_cast<const float2*>(gtab + kTabSeg);
-  for (int i = threadIdx.x; i < ntree; i += blockDim.x) t.tree[i] = gtree[i];
+  for (int i = threadIdx.x; i < hd.nkeys; i += blockDim.x) t.keys[i] = gkeys[i];
+  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
+  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
   for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   // one all-zero segment after the real ones: masked values select it and evaluate
   // to exactly 0 without per-element masks
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = make_float2(0.0f, 0.0f);
   if (threadIdx.x == 0) {
-    t.depth = hd.depth;
+    t.steps = hd.steps;
     t.zero_seg = nseg;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
   }
@@ -89,26 +92,35 @@ __device__ __forceinline__ float relu_floor(float v, float floor) {
 }
 
 // Segment index of each of NU values: the number of breakpoints strictly below u.
-// The NU searches advance together, so each step issues NU independent LDS reads
-// and the lookup latency is paid once per step rather than once per value.  NaN
-// compares false everywhere and lands in segment 0.
+// The bucket of u gives the start of its key window; `steps` halvings of the
+// window follow (a wave-uniform count, taken from the table).  The NU searches
+// advance together, so each step issues NU independent LDS reads and the lookup
+// latency is paid once per step rather than once per value.  NaN compares false
+// everywhere and ends at the start of its window.
 template <int NU, int L, int NSEG>
-__device__ __forceinline__ void pwl_search(const PwlLds<L, NSEG>& t, int depth, const float (&u)[NU],
+__device__ __forceinline__ void pwl_search(const PwlLds<L, NSEG>& t, int steps, const float (&u)[NU],
                                            int (&seg)[NU]) {
-  // heap index kept as a byte offset into the tree: a' = 2 a + (u > key ? 4 : 0)
-  const char* tree = reinterpret_cast<const char*>(t.tree);
-  unsigned a[NU];
+  const char* keys = reinterpret_cast<const char*>(t.keys);
+  unsigned off[NU];
 #pragma unroll
-  for (int i = 0; i < NU; ++i) a[i] = 4u;
-  for (int s = 0; s < depth; ++s) {
+  for (int i = 0; i < NU; ++i) {
+    const uint32_t bits = __float_as_uint(u[i]);
+    const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
+    int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
+    mm = min(max(mm, 0), kBucketMag - 1);
+    const int idx = kBucketMag + (mm ^ ((int)bits >> 31));
+    off[i] = t.buckets[idx];
+  }
+  for (int s = steps - 1; s >= 0; --s) {
+    const unsigned h4 = 4u << s;
 #pragma unroll
     for (int i = 0; i < NU; ++i) {
-      const float key = *reinterpret_cast<const float*>(tree + a[i]);
-      a[i] = 2u * a[i] + (u[i] > key ? 4u : 0u);
+      const float key = *reinterpret_cast<const float*>(keys + off[i] + h4 - 4u);
+      off[i] += key < u[i] ? h4 : 0u;
     }
   }
 #pragma unroll
-  for (int i = 0; i < NU; ++i) seg[i] = (int)((a[i] >> 2) - (1u << depth));
+  for (int i = 0; i < NU; ++i) seg[i] = (int)(off[i] >> 2);
 }
 
 // psi_l(u) for l = 0..L-1 on segment `seg`, already scaled by 1/sqrt(M) (folded

@@ -34,7 +34,7 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
   const float* bias = a.phi.b + (size_t)hset * M;
   Tout* out = reinterpret_cast<Tout*>(a.out) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
-  const int depth = tab.depth;
+  const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
   const float floor = tab.floor;
 
   Frag<Tin> xf[KS];
@@ -62,7 +62,7 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
       uu[j] = acc[j] + (i < M ? bias[i] : 0.0f);
     }
     int sg[4];
-    pwl_search(tab, depth, uu, sg);
+    pwl_search(tab, steps, uu, sg);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = 16 * mb + 4 * g + j;

@@ -9,20 +9,49 @@
 namespace luna {
 
 // piecewise-linear tables of the channel MLPs (built by luna_prepare.hip)
-constexpr int kTreeCap = 1024;          // heap-ordered breakpoints, indices 1..1023
+//
+// Layout of one table (kTableBytes, a multiple of 256):
+//   header   PwlHeader
+//   keys     the sorted breakpoints, fp32, padded with +inf to PwlHeader::nkeys
+//   buckets  uint16 per bucket of u: byte offset (4 * index) of its search window
+//   segments (slope, intercept) pairs, segment-major, L per segment
+//
+// Search.  The float bits of u pick one of kNumBuckets buckets (bucket_of), an
+// order-preserving partition of the real line: sign, then |u| below 2^-kBucketExp,
+// in [2^-kBucketExp, 2^kBucketExp) split by exponent and the top kBucketMant
+// mantissa bits, or above.  Every breakpoint that can lie below a u of the bucket,
+// beyond those below the whole bucket, sits inside a window of 2^steps - 1 keys
+// starting at the bucket's offset, so `steps` branch-free halvings of the window
+// give the number of breakpoints strictly below u, which is the segment index.
+constexpr int kKeyCap = 1024;           // sorted breakpoints incl. +inf padding
 constexpr int kSegCap = 5120;           // (slope, intercept) pairs, segment-major
-constexpr int kMaxUnits = kTreeCap - 1; // breakpoints one table can hold
+constexpr int kMaxUnits = kKeyCap - 1;  // breakpoints one table can hold
+constexpr int kBucketExp = 6;           // resolved magnitudes: [2^-6, 2^6)
+constexpr int kBucketMant = 6;          // mantissa bits per exponent
+constexpr int kBucketMag = 2 * kBucketExp * (1 << kBucketMant) + 2;  // per sign, incl. under/overflow
+constexpr int kNumBuckets = 2 * kBucketMag;                          // 1540
 constexpr size_t kTabHeader = 0;
-constexpr size_t kTabTree = 256;
-constexpr size_t kTabSeg = kTabTree + kTreeCap * 4;
-constexpr size_t kTableBytes = kTabSeg + (size_t)kSegCap * 8;  // 45312, a multiple of 256
+constexpr size_t kTabKeys = 256;
+constexpr size_t kTabBuckets = kTabKeys + kKeyCap * 4;
+constexpr size_t kTabSeg = kTabBuckets + ((size_t)kNumBuckets * 2 + 15) / 16 * 16;
+constexpr size_t kTableBytes = (kTabSeg + (size_t)kSegCap * 8 + 255) / 256 * 256;
 
 struct PwlHeader {
   int nbp;     // number of breakpoints
-  int depth;   // search steps: smallest D with 2^D - 1 >= nbp
+  int steps;   // halvings per search: smallest s with 2^s - 1 >= the most keys one bucket can need
   int L;       // channels
   int nonneg;  // 1: relu on the channel outputs
+  int nkeys;   // keys stored (breakpoints plus +inf padding), >= 2^steps - 1
 };
+
+// Bucket of u from its float bits; monotone in u (-0.0 and +0.0 fall in the two
+// buckets next to zero, NaN in an outermost one).
+__host__ __device__ constexpr int bucket_of_bits(uint32_t bits) {
+  const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
+  int m = mag - ((127 - kBucketExp) << kBucketMant) + 1;  // 0: underflow, 1..: resolved, last: overflow
+  m = m < 0 ? 0 : (m > kBucketMag - 1 ? kBucketMag - 1 : m);
+  return (bits >> 31) ? kBucketMag - 1 - m : kBucketMag + m;
+}
 
 enum class Dt : int { F32 = 0, BF16 = 1 };
 

@@ -120,7 +120,7 @@ __global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
   };
 
   __syncthreads();
-  const int tdepth = tab.depth;
+  const int tsteps = __builtin_amdgcn_readfirstlane(tab.steps);
   const float tfloor = tab.floor;
 
   if (iters > 0) fetch(0);
@@ -156,7 +156,7 @@ __global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
         for (int j = 0; j < 4; ++j) uu[8 * mb + 4 * tb + j] = acc[j] + bcol[mb];
       }
     int sg[8 * MB];
-    pwl_search(tab, tdepth, uu, sg);
+    pwl_search(tab, tsteps, uu, sg);
     Frag<T> af[MB][L];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -299,7 +299,7 @@ __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
     }
   }
   __syncthreads();
-  const int tdepth = tab.depth;
+  const int tsteps = __builtin_amdgcn_readfirstlane(tab.steps);
   const float tfloor = tab.floor;
 
   const int nblk = a.tile_tokens / 16;
@@ -325,7 +325,7 @@ __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
       for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
     }
     int sg[4 * MB];
-    pwl_search(tab, tdepth, uu, sg);
+    pwl_search(tab, tsteps, uu, sg);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
@@ -470,7 +470,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
     }
   };
   __syncthreads();
-  const int tdepth = sm.tab.depth;
+  const int tsteps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
   const int zseg = sm.tab.zero_seg;
   const float tfloor = sm.tab.floor;
   T* vt = &sm.u.vt[wave][0][0];
@@ -504,7 +504,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
       }
     if (step + kNcWaves < nsteps) fetch_k(step + kNcWaves);
     int sg[8 * MB];
-    pwl_search(sm.tab, tdepth, uu, sg);
+    pwl_search(sm.tab, tsteps, uu, sg);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -648,7 +648,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
       for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
     }
     int sg[4 * MB];
-    pwl_search(sm.tab, tdepth, uu, sg);
+    pwl_search(sm.tab, tsteps, uu, sg);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll

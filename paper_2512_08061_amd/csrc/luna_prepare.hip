@@ -11,7 +11,10 @@
 //   1. breakpoints beta_k (fp64 quotient rounded to fp32); units with a_k = 0 or a
 //      non-finite quotient are constant (on iff c_k > 0) and get no breakpoint;
 //   2. bitonic sort of (beta, unit) in LDS, ties broken by unit index;
-//   3. heap-ordered search tree over the sorted breakpoints, padded with +inf;
+//   3. the sorted breakpoints as search keys, and for every bucket of u (an
+//      order-preserving partition of the reals by float bits) the start of a
+//      window of 2^steps - 1 keys that holds every breakpoint a u of the bucket can
+//      be compared against, steps chosen for the fullest bucket;
 //   4. per channel l: segment 0 holds the units that are on below every breakpoint
 //      (a < 0, or a = 0 with c > 0); crossing the breakpoint of unit k switches it on
 //      (a > 0) or off (a < 0), changing (s, t) by +-(f a, f c).  The segment values
@@ -38,7 +41,9 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   __shared__ float a_s[kSortCap], c_s[kSortCap], f_s[kSortCap];
   __shared__ int has_bp[kSortCap];
   __shared__ float g_s[16];
-  __shared__ int s_nbp;
+  __shared__ int hist[kNumBuckets];
+  __shared__ int wave_tot[4];
+  __shared__ int s_nbp, s_most;
 
   const int set = blockIdx.x;
   const int tid = threadIdx.x;
@@ -51,7 +56,10 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
 
   if (set == 0 && a.zero_ptr != nullptr)
     for (int i = tid; i < a.zero_count; i += blockDim.x) a.zero_ptr[i] = 0;
-  if (tid == 0) s_nbp = 0;
+  if (tid == 0) {
+    s_nbp = 0;
+    s_most = 0;
+  }
   int N = 2;
   while (N < units) N *= 2;
   __syncthreads();
@@ -96,20 +104,56 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
     }
   }
 
-  // 3. search tree: heap node i holds the breakpoint of in-order rank r(i)
-  int depth = 0;
-  while ((1 << depth) - 1 < nbp) ++depth;
-  float* tree = reinterpret_cast<float*>(tab + kTabTree);
-  for (int i = tid; i < (1 << depth); i += blockDim.x) {
-    float v = __builtin_inff();
-    if (i >= 1) {
-      const int lv = 31 - __clz(i);   // level of heap node i (root = 0)
-      const int ht = depth - 1 - lv;  // its height
-      const int r = (i - (1 << lv)) * (1 << (ht + 1)) + (1 << ht) - 1;
-      if (r < nbp) v = key[r];
-    }
-    tree[i] = v;
+  // 3. search keys and bucket windows.  The sorted keys (-0 stored as +0, so that
+  // bucket order and numeric order agree at zero) fall into buckets in order, so
+  // the keys below bucket b are those of the buckets before it: an exclusive
+  // prefix sum of the per-bucket histogram.  A u of bucket b compares against the
+  // keys of bucket b only; the window must hold the fullest bucket.
+  float* keys = reinterpret_cast<float*>(tab + kTabKeys);
+  uint16_t* buckets = reinterpret_cast<uint16_t*>(tab + kTabBuckets);
+  for (int bb = tid; bb < kNumBuckets; bb += blockDim.x) hist[bb] = 0;
+  __syncthreads();
+  for (int i = tid; i < nbp; i += blockDim.x) {
+    const float k = key[i] == 0.0f ? 0.0f : key[i];
+    key[i] = k;
+    atomicAdd(&hist[bucket_of_bits(__float_as_uint(k))], 1);
   }
+  __syncthreads();
+  constexpr int kPer = (kNumBuckets + 255) / 256;  // buckets per thread in the scan
+  int local = 0, most_local = 0;
+  for (int j = 0; j < kPer; ++j) {
+    const int bb = tid * kPer + j;
+    if (bb < kNumBuckets) {
+      local += hist[bb];
+      most_local = max(most_local, hist[bb]);
+    }
+  }
+  atomicMax(&s_most, most_local);
+  // exclusive scan of the 256 per-thread totals: within 64-lane waves, then across waves
+  int incl = local;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if ((tid & 63) >= o) incl += v;
+  }
+  if ((tid & 63) == 63) wave_tot[tid / 64] = incl;
+  __syncthreads();
+  int before = incl - local;
+  for (int w = 0; w < tid / 64; ++w) before += wave_tot[w];
+  const int most = s_most;
+  int steps = 0;
+  while ((1 << steps) - 1 < most) ++steps;
+  const int window = (1 << steps) - 1;
+  const int nkeys = nbp > window ? nbp : window;
+  for (int j = 0; j < kPer; ++j) {
+    const int bb = tid * kPer + j;
+    if (bb < kNumBuckets) {
+      const int start = before < nkeys - window ? before : nkeys - window;
+      buckets[bb] = (uint16_t)(4 * start);
+      before += hist[bb];
+    }
+  }
+  for (int i = tid; i < nkeys; i += blockDim.x) keys[i] = i < nbp ? key[i] : __builtin_inff();
 
   // 4. segment values by prefix sums over the sorted breakpoints
   const double inv = 1.0 / sqrt((double)a.M);
@@ -188,7 +232,8 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   if (tid == 0) {
     PwlHeader* hd = reinterpret_cast<PwlHeader*>(tab + kTabHeader);
     hd->nbp = nbp;
-    hd->depth = depth;
+    hd->steps = steps;
+    hd->nkeys = nkeys;
     hd->L = a.L;
     hd->nonneg = a.nonneg;
   }

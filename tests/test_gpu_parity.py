@@ -85,6 +85,61 @@ def test_featuremap_psi_sweep(shared, nonneg):
     assert err.max() < 2e-6 * max(1.0, np.abs(ref).max()), err.max()
 
 
+def _bucket_edges():
+    """Every boundary of the float-bit buckets the kernels index the breakpoints by
+    (powers of two and 1/64 mantissa steps over [2^-6, 2^6]), both signs, with the
+    fp32 neighbours of each, plus zeros and denormals."""
+    mags = [np.float32(2.0) ** e * np.float32(1 + k / 64) for e in range(-6, 6) for k in range(64)]
+    mags.append(np.float32(64.0))
+    mags = np.array(mags, np.float32)
+    vals = np.concatenate([mags, np.nextafter(mags, np.float32(0)), np.nextafter(mags, np.float32(np.inf))])
+    return np.concatenate([vals, -vals, np.float32([0.0, -0.0, 1e-40, -1e-40, 3e-39, -3e-39, 1e6, -1e6])])
+
+
+def _featuremap_exact(p, u, shared=False, nonneg=True):
+    w = small_workload("f32", B=1, H=1, n=u.size, d=32, M=1, L=p["L"], shared_channels=shared, nonneg=nonneg,
+                       hidden=p["hidden"])
+    p = dict(p)
+    p["W"] = np.zeros((1, 32), np.float32)
+    p["W"][0, 0] = 1.0  # u = x_0
+    p["b"] = np.zeros(1, np.float32)
+    X = np.zeros((1, 1, u.size, 32), np.float32)
+    X[0, 0, :, 0] = u
+    (Xt,), pt = upload(w, [X], p)
+    phi = to_np(luna.featuremap(Xt, pt))[0, 0]
+    ref = oracle.featuremap(X[0, 0], p)
+    err = np.abs(phi - ref) / np.maximum(1.0, np.abs(u.astype(np.float64)))[:, None]
+    assert err.max() < 2e-6 * max(1.0, np.abs(ref).max()), err.max()
+
+
+@pytest.mark.parametrize("layout", ["random", "clustered", "all_equal", "wide", "zero_and_tiny"])
+def test_featuremap_bucket_edges(layout):
+    """psi at every bucket boundary (and its fp32 neighbours) and at every breakpoint,
+    for breakpoint sets that leave buckets sparse, crowd one bucket, make all
+    breakpoints equal, spread them over many decades, or sit at 0 and below 2^-6."""
+    w = small_workload("f32", B=1, H=1, n=8, d=32, M=1, L=8)
+    p = dict(wl.make_params(w, seed=21))
+    rng = np.random.default_rng(22)
+    a = p["fc1_w"].astype(np.float64).copy()
+    if layout == "clustered":      # 300 of the 512 breakpoints inside [0.5, 0.5 + 1/128)
+        beta = np.where(rng.random(a.shape) < 0.6, 0.5 + rng.random(a.shape) / 128, rng.standard_cauchy(a.shape))
+    elif layout == "all_equal":
+        beta = np.full(a.shape, -0.3)
+    elif layout == "wide":
+        beta = rng.choice([-1, 1], a.shape) * 10.0 ** rng.uniform(-9, 9, a.shape)
+    elif layout == "zero_and_tiny":
+        beta = np.where(rng.random(a.shape) < 0.5, 0.0, rng.uniform(-2 ** -6, 2 ** -6, a.shape))
+    else:
+        beta = -p["fc1_b"].astype(np.float64) / a
+    p["fc1_b"] = (-beta * a).astype(np.float32)
+    bp = (-p["fc1_b"].astype(np.float64) / p["fc1_w"].astype(np.float64)).ravel().astype(np.float32)
+    bp = bp[np.isfinite(bp)]
+    u = np.concatenate([_bucket_edges(), bp, np.nextafter(bp, np.float32(np.inf)), np.nextafter(bp, np.float32(-np.inf)),
+                        np.linspace(-3, 3, 601, dtype=np.float32)])
+    say(f"bucket edges {layout}: {u.size} values")
+    _featuremap_exact(p, u)
+
+
 @pytest.mark.parametrize("name", list(wl.WORKLOADS))
 def test_featuremap_workload_full_size(name):
     w = wl.WORKLOADS[name]

@@ -62,7 +62,8 @@ luna_status check_common(const Problem& pb) {
 
 struct Layout {
   size_t tables = 0, partial = 0, frags = 0, total = 0;
-  int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, dv_tiles = 1, fused = 0;
+  int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
+  int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
 };
 
 luna_status plan(const Problem& pb, Layout* lay) {
@@ -104,10 +105,19 @@ luna_status plan(const Problem& pb, Layout* lay) {
     off = align256(off + (size_t)heads * np.frag_elems * (pb.dt == LUNA_BF16 ? 2 : 4));
   } else if (pb.op == LUNA_OP_ATTN_CAUSAL) {
     if (pb.chunk != 64) return fail(LUNA_ERR_UNSUPPORTED, "chunk must be 64");
-    int tiles = 1;
-    if (!luna::causal_supported(dt, d, L, M, &tiles))
+    if (!luna::causal_supported(dt, d, L, M))
       return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernel for this (dtype, d, L, M)");
-    lay->dv_tiles = tiles;
+    // Too few heads to fill the device: cut every head in two.  Part 1 first
+    // rebuilds the state of part 0's tokens from keys and values, which costs
+    // about kPrefixCost of scanning them, so part 0 gets n / (2 - kPrefixCost).
+    if (heads < 256 && pb.n >= 256) {
+      constexpr double kPrefixCost = 0.5;
+      int64_t x = (int64_t)((double)pb.n / (2.0 - kPrefixCost) / 64.0 + 0.5) * 64;
+      if (x >= 64 && x < pb.n) {
+        lay->parts = 2;
+        lay->split = (int)x;
+      }
+    }
   } else {
     return fail(LUNA_ERR_INVALID_ARG, "unknown operation code");
   }
@@ -257,7 +267,8 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   a.n = (int)n;
   a.H = (int)H;
   a.heads = (int)(B * H);
-  a.dv_tiles = lay.dv_tiles;
+  a.parts = lay.parts;
+  a.split = lay.split;
   a.eps = eps;
   hipError_t e = luna::launch_causal(dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32, (int)d, p->L, p->M, a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");

@@ -115,7 +115,8 @@ struct CausalArgs {
   void* out;
   PhiArgs phi;
   int n, H, heads;
-  int dv_tiles;  // value-column tiles per head
+  int parts;     // workgroups per head (1 or 2)
+  int split;     // with 2 parts: first token of part 1 (a multiple of 64)
   float eps;
 };
 
@@ -134,7 +135,7 @@ struct NoncausalPlan {
 bool noncausal_supported(Dt dt, int d, int L, int M, NoncausalPlan* plan);
 hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s);
 
-bool causal_supported(Dt dt, int d, int L, int M, int* dv_tiles);
+bool causal_supported(Dt dt, int d, int L, int M);
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s);
 
 // LDS copy of the segment table: one row of (slope, intercept) pairs per segment.

@@ -15,23 +15,28 @@
 // no readout) and then scans [x, n).  The cut is placed so that both parts take
 // about the same time; nothing is shared between workgroups.
 //
-// Waves.  Wave w owns value columns 16w .. 16w + 15 (d / 16 waves) and keeps the
-// matching slice of S (all features) in fp32 matrix-core accumulators.  Per chunk,
-// with phi(Q_c), phi(K_c) and V_c already in LDS:
-//   - its share of the P^T blocks (P and its row sums to LDS) and of
-//     phi(Q_c) z_{c-1} (to LDS);
-//   - num^T = S_{c-1}^T phi(Q_c)^T for its columns, with S taken straight from the
-//     accumulators: the feature order of S's rows is chosen so that two
-//     accumulator tiles form one k-fragment of S^T;
-//   - S += phi(K_c)^T V_c and z += phi(K_c)^T 1;
-//   - barrier; num^T += V^T P^T; divide; store;
-//   - phi of its 16-row blocks of chunk c + 1 (query rows or key rows) and its
-//     share of V_{c+1} into LDS.
-// Two barriers per chunk.  phi(Q) is kept token-major and phi(K) feature-major in
-// LDS, so every large operand is one 16-byte read per lane; only the P^T blocks
-// (phi(K) rows) and V use the gfx950 transpose read.  Every LDS tile is stored in
-// 16-byte chunks XOR-swizzled by row so that the rows one read touches fall in
-// distinct banks.
+// Roles.  Eight waves, two per SIMD: four matrix waves and four map waves, so that
+// every SIMD pairs matrix-core work with vector and table-lookup work.
+//  - Map wave p computes phi of query rows 16p .. 16p + 15 and key rows
+//    16p .. 16p + 15 of the next chunk (projection on the matrix cores, the
+//    piecewise-linear channel functions in registers) and stages V; phi(Q) is
+//    stored token-major and phi(K) feature-major in LDS.
+//  - Matrix wave m owns value columns 32m .. 32m + 31 (d / 4 of them) and keeps
+//    that slice of S (all features) in fp32 accumulators.  It forms its share of
+//    the P^T blocks and of phi(Q_c) z_{c-1}, then num^T = S_{c-1}^T phi(Q_c)^T with
+//    S taken straight from the accumulators (the feature order of S's rows makes
+//    two accumulator tiles one k-fragment of S^T), then num^T += V^T P^T, the
+//    division and the store, then S += phi(K_c)^T V_c and z += phi(K_c)^T 1.
+// Per chunk c, three barriers:
+//   B1: phi(Q_c), phi(K_c), V_c, z_{c-1} in LDS.
+//       matrix: P^T blocks, phi(Q_c) z_{c-1}, readout.   map: phi(Q_{c+1}) to registers.
+//   B2: P and den parts in LDS; phi(Q_c) no longer read.
+//       matrix: P V, output, state update.
+//       map: phi(Q_{c+1}) to LDS, z_c published, phi(K_{c+1}) to registers.
+//   B3: phi(K_c), V_c no longer read.   map: phi(K_{c+1}), V_{c+1} to LDS.
+// Large operands are one 16-byte LDS read per lane; only the P^T blocks (phi(K)
+// columns) and V use the gfx950 transpose read.  Q, K and V rows are fetched one
+// chunk ahead.
 #include "luna_device.hpp"
 #include "luna_kernels.hpp"
 
@@ -39,19 +44,20 @@ namespace luna {
 
 template <typename T, int DH, int L, int MB>
 struct CsCfg {
-  static constexpr int NW = DH / 16;              // waves, one 16-column block of values each
-  static constexpr int NT = NW * kWave;
-  static constexpr int KS = DH / 32;              // 32-wide k-steps of the projection
-  static constexpr int FP = 16 * MB * L;          // features, projections padded to 16
-  static constexpr int NF = FP / 32;              // 32-feature k-fragments
-  static constexpr int RB = FP / 16;              // 16-feature row blocks of S
-  static constexpr int RBZ = (RB + NW - 1) / NW;  // row blocks of z per wave
-  static constexpr int VE = 16 / (int)sizeof(T);  // elements per 16-byte chunk
-  static constexpr int NTASK = 8 / NW;            // 16-row phi blocks per wave per chunk (4 Q + 4 K)
-  static constexpr int VPT = 64 * DH / VE / NT;   // 16-byte V chunks per thread
-  static constexpr int NDEN = NW >= 4 ? 1 : 4 / NW;  // query blocks whose phi(Q) z a wave forms
+  static constexpr int NCB = DH / 16;                 // 16-column blocks of the value width
+  static constexpr int CBW = NCB >= 4 ? NCB / 4 : 1;  // column blocks per matrix wave
+  static constexpr int NMW = NCB / CBW;               // matrix waves that own columns (2 or 4)
+  static constexpr int KS = DH / 32;                  // 32-wide k-steps of the projection
+  static constexpr int FP = 16 * MB * L;              // features, projections padded to 16
+  static constexpr int NF = FP / 32;                  // 32-feature k-fragments
+  static constexpr int RB = FP / 16;                  // 16-feature row blocks of S
+  static constexpr int NDEN = 4 / NMW;                // query blocks whose phi(Q) z a matrix wave forms
+  static constexpr int VE = 16 / (int)sizeof(T);      // elements per 16-byte chunk
+  static constexpr int NPQ = MB * 4 * L / 8;          // phi(Q) fragments per lane per block
+  static constexpr int NPK = MB * L / 2;              // phi(K) fragments (two channels x four tokens)
+  static constexpr int VPT = 64 * DH / VE / 256;      // 16-byte V chunks per map-wave thread
   static constexpr int NSEG = nseg_cap(L, kAttnSegBytes);
-  static_assert(NW >= 2 && 8 % NW == 0, "d must be 32, 64 or 128");
+  static_assert(NCB == 2 || NCB == 4 || NCB == 8, "d must be 32, 64 or 128");
   static_assert(FP % 32 == 0 && L % 2 == 0, "features must fill 32-wide fragments");
 };
 
@@ -66,7 +72,9 @@ struct CsLds {
   alignas(16) T vt[64 * DH];               // V_c, token-major
   alignas(16) float denp[4][64];           // row sums of P per key block
   alignas(16) float deni[64];              // phi(Q_c) z_{c-1}
-  alignas(16) float zb[2][C::FP];          // z by chunk parity
+  alignas(16) float zp[4][C::FP];          // z_c over each map wave's key rows
+  alignas(16) float zs[2][C::FP];          // z_c, summed, by chunk parity
+  float bias[16 * MB];                     // projection biases, 0 for padded projections
 };
 
 // 16-byte chunk swizzles: physical chunk of logical chunk `cg` in row `row` of a
@@ -125,9 +133,9 @@ __device__ __forceinline__ void sts8(const Frag<float>& f, F at) {
 }
 
 template <typename T, int DH, int L, int MB>
-__global__ __launch_bounds__(64 * (DH / 16), 1) void causal_kernel(CausalArgs a) {
+__global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   using C = CsCfg<T, DH, L, MB>;
-  constexpr int NW = C::NW, KS = C::KS, FP = C::FP, NF = C::NF, RB = C::RB, VE = C::VE;
+  constexpr int KS = C::KS, FP = C::FP, NF = C::NF, RB = C::RB, VE = C::VE, CBW = C::CBW, NMW = C::NMW;
   constexpr int CPQ = FP / VE, CPK = 64 / VE, CPV = DH / VE;
   __shared__ CsLds<T, DH, L, MB> sm;
 
@@ -138,7 +146,10 @@ __global__ __launch_bounds__(64 * (DH / 16), 1) void causal_kernel(CausalArgs a)
 
   const int tid = threadIdx.x;
   const int wave = wave_id(), lane = tid % kWave;
-  const int g = lane / 16, r = lane % 16;
+  // lane coordinates; re-announced at the top of every chunk so that the many
+  // per-lane LDS addresses derived from them are recomputed inside the loop rather
+  // than hoisted out of it and kept live in registers
+  int g = lane / 16, r = lane % 16;
   const int M = a.phi.M;
   const int n = a.n;
   const size_t hoff = (size_t)head * n * DH;
@@ -161,7 +172,7 @@ __global__ __launch_bounds__(64 * (DH / 16), 1) void causal_kernel(CausalArgs a)
   auto vt_at = [&](int t, int c) -> T* { return &sm.vt[t * DH + swz_v<CPV>(t, c / VE) * VE + c % VE]; };
 
   // W fragments into LDS; P (above-diagonal blocks stay zero) and z cleared
-  for (int i = tid; i < MB * KS * kWave; i += C::NT) {
+  for (int i = tid; i < MB * KS * kWave; i += 512) {
     const int l = i % kWave, ks = (i / kWave) % KS, mb = i / (kWave * KS);
     const int p = 16 * mb + l % 16;
     Frag<T> f;
@@ -169,297 +180,393 @@ __global__ __launch_bounds__(64 * (DH / 16), 1) void causal_kernel(CausalArgs a)
     else f.zero();
     store8(&sm.wfr[mb][ks][l][0], f);
   }
-  for (int i = tid; i < 64 * 64; i += C::NT) sm.pm[i] = (T)0.0f;
-  for (int i = tid; i < 2 * FP; i += C::NT) (&sm.zb[0][0])[i] = 0.0f;
-
-  // projection biases: rows 16 mb + 4 g + j (u^T layout) and column 16 mb + r (u layout)
-  float brow[MB][4], bcol[MB];
-  bool prow[MB][4], pcol[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    pcol[mb] = 16 * mb + r < M;
-    bcol[mb] = pcol[mb] ? bias[16 * mb + r] : 0.0f;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = 16 * mb + 4 * g + j;
-      prow[mb][j] = i < M;
-      brow[mb][j] = i < M ? bias[i] : 0.0f;
-    }
-  }
+  for (int i = tid; i < 64 * 64; i += 512) sm.pm[i] = (T)0.0f;
+  for (int i = tid; i < 2 * FP; i += 512) (&sm.zs[0][0])[i] = 0.0f;
+  for (int i = tid; i < 16 * MB; i += 512) sm.bias[i] = i < M ? bias[i] : 0.0f;
   Frag<T> ones;
   ones.fill(1.0f);
 
-  // ---- phi blocks of this wave: task k is block b = wave + NW k (0-3: Q, 4-7: K) ----
-  auto task_q = [&](int k) { return wave + NW * k < 4; };
-  auto task_blk = [&](int k) { return (wave + NW * k) & 3; };
-  // does task k map chunk cc (key blocks always, query blocks only where scanned)
-  auto task_live = [&](int k, int cc) { return cc < c_end && (!task_q(k) || cc >= c_begin); };
-
-  Frag<T> xf[C::NTASK][KS];  // X rows of the next chunk to map
-  auto load_x = [&](int k, int cc) {
-    const T* X = task_q(k) ? Q : K;
-    const int t = 64 * cc + 16 * task_blk(k) + r;
-    const bool live = task_live(k, cc) && t < n;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (live) load8(xf[k][ks], X + (size_t)t * DH + 32 * ks + 8 * g);
-      else xf[k][ks].zero();
-    }
-  };
-
-  // phi of block task k of chunk cc, written to LDS.  Query rows: u^T = W X^T, the
-  // lane holds projections 16 mb + 4 g + j of token r and writes features
-  // (16 mb + 4 g + j) L + l of that token.  Key rows: u = X W^T, the lane holds
-  // projection 16 mb + r of tokens 4 g + j and writes, for each channel l, the four
-  // tokens of feature (16 mb + r) L + l.
-  auto map_block = [&](int k, int cc, int steps, int zseg, float floor) {
-    float uu[4 * MB];
-    const bool isq = task_q(k);
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      f32x4 acc = zero4();
+  if (wave >= 4) {
+    // ============================================================== map waves
+    const int pw = wave - 4;  // query and key rows 16 pw .. 16 pw + 15 of every chunk
+    const int mtid = tid - 256;
+    Frag<T> xq[KS], xk[KS];  // query and key rows of the next chunk to map
+    i32x4 vr[C::VPT];        // V of the next chunk
+    auto load_rows = [&](Frag<T> (&xf)[KS], const T* X, int cc, bool live) {
+      const int t = 64 * cc + 16 * pw + r;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        Frag<T> wf;
-        load8(wf, &sm.wfr[mb][ks][lane][0]);
-        if (isq) mma(acc, wf, xf[k][ks]);
-        else mma(acc, xf[k][ks], wf);
+        if (live && cc < c_end && t < n) load8(xf[ks], X + (size_t)t * DH + 32 * ks + 8 * g);
+        else xf[ks].zero();
       }
+    };
+    auto load_v = [&](i32x4 (&vf)[C::VPT], int cc) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + (isq ? brow[mb][j] : bcol[mb]);
-    }
-    int sg[4 * MB];
-    pwl_search(sm.tab, steps, uu, sg);
-    const int blk = task_blk(k);
-    if (isq) {
-      const int t = 16 * blk + r;
+      for (int q = 0; q < C::VPT; ++q) {
+        const int cidx = mtid + 256 * q;
+        const int tt = cidx / CPV, cg = cidx % CPV;
+        const int t = 64 * cc + tt;
+        if (cc < c_end && t < n) vf[q] = *reinterpret_cast<const i32x4*>(V + (size_t)t * DH + cg * VE);
+        else vf[q] = i32x4{0, 0, 0, 0};
+      }
+    };
+    auto store_v = [&](const i32x4 (&vf)[C::VPT]) {
+#pragma unroll
+      for (int q = 0; q < C::VPT; ++q) {
+        const int cidx = mtid + 256 * q;
+        const int tt = cidx / CPV, cg = cidx % CPV;
+        *reinterpret_cast<i32x4*>(&sm.vt[tt * DH + swz_v<CPV>(tt, cg) * VE]) = vf[q];
+      }
+    };
+    // u for the 16 rows: query rows as u^T = W X^T (lane: projections 16 mb + 4 g + j
+    // of token r), key rows as u = X W^T (lane: projection 16 mb + r of tokens 4 g + j)
+    auto project = [&](const Frag<T> (&xf)[KS], bool isq, float (&uu)[4 * MB]) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          Frag<T> wf;
+          load8(wf, &sm.wfr[mb][ks][lane][0]);
+          if (isq) mma(acc, wf, xf[ks]);
+          else mma(acc, xf[ks], wf);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + sm.bias[16 * mb + (isq ? 4 * g + j : r)];
+      }
+    };
+    Frag<T> qreg[C::NPQ], kreg[C::NPK];
+    // z over this wave's key rows: tile mb has rows = projections 16 mb + 4 g + jj and
+    // column l = channel l, accumulated from phi(K) fragments times one-hot columns
+    f32x4 zacc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) zacc[mb] = zero4();
+    auto add_z = [&]() {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int seg = prow[mb][j] ? sg[4 * mb + j] : zseg;  // padded projections give 0
-          const int f0 = (16 * mb + 4 * g + j) * L;
-          float y[L];
-          pwl_channels<L>(sm.tab, seg, floor, uu[4 * mb + j], y);
-          if constexpr (L % 8 == 0) {
-#pragma unroll
-            for (int h = 0; h < L / 8; ++h) {
-              Frag<T> f;
-#pragma unroll
-              for (int e = 0; e < 8; e += 2) f.set2(e, y[8 * h + e], y[8 * h + e + 1]);
-              sts8(f, [&](int e) { return phq_at(t, f0 + 8 * h + e); });
-            }
-          } else {
-#pragma unroll
-            for (int l = 0; l < L; ++l) *phq_at(t, f0 + l) = (T)y[l];
-          }
+        for (int q = 0; q < L / 2; ++q) {
+          Frag<T> oh;  // slot e holds channel 2q + (e >= 4)
+          const float lo = r == 2 * q ? 1.0f : 0.0f, hi = r == 2 * q + 1 ? 1.0f : 0.0f;
+          oh.set2(0, lo, lo);
+          oh.set2(2, lo, lo);
+          oh.set2(4, hi, hi);
+          oh.set2(6, hi, hi);
+          mma(zacc[mb], kreg[mb * (L / 2) + q], oh);
         }
-    } else {
-      const int t0 = 64 * cc + 16 * blk + 4 * g;
+    };
+    auto write_z = [&]() {
+      if (r < L) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) sm.zp[pw][(16 * mb + 4 * g + jj) * L + r] = zacc[mb][jj];
+      }
+    };
+    // the four parts summed in a fixed order, this wave's quarter of the features
+    auto sum_z = [&](int slot) {
+      for (int f = FP / 4 * pw + lane; f < FP / 4 * (pw + 1); f += kWave)
+        sm.zs[slot][f] = ((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f];
+    };
+    // phi(Q) of chunk cc into qreg: value (mb, j, l) at index (4 mb + j) L + l
+    auto map_q = [&](const Frag<T> (&xf)[KS], int steps, int zseg, float floor) {
+      float uu[4 * MB];
+      project(xf, true, uu);
+      int sg[4 * MB];
+      pwl_search(sm.tab, steps, uu, sg);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          // two values at a time, so that their table reads are not all hoisted together
+          if (j % 2 == 0) __builtin_amdgcn_sched_barrier(0);
+          float y[L];
+          pwl_channels<L>(sm.tab, 16 * mb + 4 * g + j < M ? sg[4 * mb + j] : zseg, floor, uu[4 * mb + j], y);
+#pragma unroll
+          for (int l = 0; l < L; l += 2) {
+            const int idx = (4 * mb + j) * L + l;
+            qreg[idx / 8].set2(idx % 8, y[l], y[l + 1]);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto write_q = [&]() {
+      const int t = 16 * pw + r;
+      if constexpr (L % 8 == 0) {
+#pragma unroll
+        for (int p = 0; p < C::NPQ; ++p) {
+          const int mj = p / (L / 8), h = p % (L / 8);
+          const int f0 = (16 * (mj / 4) + 4 * g + mj % 4) * L + 8 * h;
+          sts8(qreg[p], [&](int e) { return phq_at(t, f0 + e); });
+        }
+      } else {
+#pragma unroll
+        for (int idx = 0; idx < MB * 4 * L; ++idx) {
+          const int mj = idx / L, l = idx % L;
+          *phq_at(t, (16 * (mj / 4) + 4 * g + mj % 4) * L + l) = (T)qreg[idx / 8].get(idx % 8);
+        }
+      }
+    };
+    // phi(K) of chunk cc into kreg: fragment (mb, q) holds channel 2q in slots 0-3 and
+    // channel 2q + 1 in slots 4-7, tokens 4 g + 0..3
+    auto map_k = [&](const Frag<T> (&xf)[KS], int cc, int steps, int zseg, float floor) {
+      float uu[4 * MB];
+      project(xf, false, uu);
+      int sg[4 * MB];
+      pwl_search(sm.tab, steps, uu, sg);
+      const int t0 = 64 * cc + 16 * pw + 4 * g;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        __builtin_amdgcn_sched_barrier(0);
         int seg[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j)  // padded projections and key rows past n give 0
-          seg[j] = (pcol[mb] && t0 + j < n) ? sg[4 * mb + j] : zseg;
+          seg[j] = (16 * mb + r < M && t0 + j < n) ? sg[4 * mb + j] : zseg;
 #pragma unroll
         for (int q = 0; q < L / 2; ++q) {
           float y0[4], y1[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) pwl_pair<L>(sm.tab, seg[j], q, floor, uu[4 * mb + j], y0[j], y1[j]);
-          const int f = (16 * mb + r) * L + 2 * q;
-          store4(phk_at(f, 16 * blk + 4 * g), y0[0], y0[1], y0[2], y0[3]);
-          store4(phk_at(f + 1, 16 * blk + 4 * g), y1[0], y1[1], y1[2], y1[3]);
+          Frag<T>& f = kreg[mb * (L / 2) + q];
+          f.set2(0, y0[0], y0[1]);
+          f.set2(2, y0[2], y0[3]);
+          f.set2(4, y1[0], y1[1]);
+          f.set2(6, y1[2], y1[3]);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto write_k = [&]() {
+      const int t0 = 16 * pw + 4 * g;
+#pragma unroll
+      for (int p = 0; p < C::NPK; ++p) {
+        const int mb = p / (L / 2), q = p % (L / 2);
+        const int f = (16 * mb + r) * L + 2 * q;
+        const Frag<T>& src = kreg[p];
+        store4(phk_at(f, t0), src.get(0), src.get(1), src.get(2), src.get(3));
+        store4(phk_at(f + 1, t0), src.get(4), src.get(5), src.get(6), src.get(7));
+      }
+    };
+    // query rows are needed from chunk c_begin on, key rows and V from chunk 0
+    load_rows(xq, Q, 0, 0 >= c_begin);
+    load_rows(xk, K, 0, true);
+    load_v(vr, 0);
+    __syncthreads();  // tables, W fragments, cleared P and z
+    const int steps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
+    const int zseg = sm.tab.zero_seg;
+    const float tfloor = sm.tab.floor;
+    if (0 >= c_begin) {
+      map_q(xq, steps, zseg, tfloor);
+      write_q();
     }
-  };
-  // V tile of chunk cc through registers
-  i32x4 vpf[C::VPT];
-  auto load_v = [&](int cc) {
-#pragma unroll
-    for (int q = 0; q < C::VPT; ++q) {
-      const int cidx = tid + C::NT * q;
-      const int tt = cidx / CPV, cg = cidx % CPV;
-      const int t = 64 * cc + tt;
-      if (t < n && cc < c_end) vpf[q] = *reinterpret_cast<const i32x4*>(V + (size_t)t * DH + cg * VE);
-      else vpf[q] = i32x4{0, 0, 0, 0};
+    load_rows(xq, Q, 1, 1 >= c_begin);
+    map_k(xk, 0, steps, zseg, tfloor);
+    write_k();
+    add_z();
+    load_rows(xk, K, 1, true);
+    store_v(vr);
+    load_v(vr, 1);
+
+    // iteration c maps chunk c + 1 (rows fetched one chunk ahead)
+    for (int c = 0; c < c_end; ++c) {
+      const int cn = c + 1;
+      asm volatile("" : "+v"(g), "+v"(r));
+      __syncthreads();  // B1
+      const bool qn = cn < c_end && cn >= c_begin;
+      if (qn) map_q(xq, steps, zseg, tfloor);
+      load_rows(xq, Q, cn + 1, cn + 1 >= c_begin);  // also during the state-only chunks
+      __syncthreads();  // B2
+      if (qn) write_q();
+      write_z();  // z_c, before chunk c + 1 is added
+      if (cn < c_end) {
+        map_k(xk, cn, steps, zseg, tfloor);
+        load_rows(xk, K, cn + 1, true);
+        add_z();
+      }
+      __syncthreads();  // B3
+      sum_z(c & 1);
+      if (cn < c_end) {
+        write_k();
+        store_v(vr);
+        load_v(vr, cn + 1);
+      }
     }
-  };
-  auto commit_v = [&]() {
+  } else {
+    // =========================================================== matrix waves
+    const int mw = wave;
+    const bool active = mw < NMW;
+    f32x4 sacc[CBW][RB];
 #pragma unroll
-    for (int q = 0; q < C::VPT; ++q) {
-      const int cidx = tid + C::NT * q;
-      const int tt = cidx / CPV, cg = cidx % CPV;
-      *reinterpret_cast<i32x4*>(&sm.vt[tt * DH + swz_v<CPV>(tt, cg) * VE]) = vpf[q];
-    }
-  };
+    for (int x = 0; x < CBW; ++x)
+#pragma unroll
+      for (int i = 0; i < RB; ++i) sacc[x][i] = zero4();
+    // query blocks dbase + NMW s get their phi(Q) z from this wave
+    const int dbase = (mw + NMW - 2 % NMW) % NMW;
+    __syncthreads();  // tables, W fragments, cleared P and z
 
-  // ---- prologue: chunk 0 into LDS ----
+    for (int c = 0; c < c_end; ++c) {
+      const bool scan = c >= c_begin;
+      const int tc = 64 * c;
+      asm volatile("" : "+v"(g), "+v"(r));
+      __syncthreads();  // B1: phi(Q_c), phi(K_c), V_c and z_{c-1} are in LDS
+      f32x4 num[CBW][4];
+      if (scan && active) {
+        // P^T blocks (query block i >= key block j): rows = key tokens 16 j + 4 g + jj,
+        // column = query token 16 i + r.  Each wave takes runs of blocks that share
+        // their key block, so that phi(K_j) is read once per run.
+        auto p_run = [&](int j, int i0, int i1) {
+          Frag<T> kfr[NF];
 #pragma unroll
-  for (int k = 0; k < C::NTASK; ++k) load_x(k, 0);
-  load_v(0);
-  __syncthreads();  // tables, W fragments, cleared P and z
-  const int steps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
-  const int zseg = sm.tab.zero_seg;
-  const float tfloor = sm.tab.floor;
+          for (int kf = 0; kf < NF; ++kf) {
+            load_tr4_at(kfr[kf], 0, lane, [&](int kk, int col) { return phk_at(32 * kf + 8 * g + kk, 16 * j + col); });
+            load_tr4_at(kfr[kf], 4, lane,
+                        [&](int kk, int col) { return phk_at(32 * kf + 8 * g + 4 + kk, 16 * j + col); });
+          }
+          for (int i = i0; i < i1; ++i) {
+            f32x4 pacc = zero4();
 #pragma unroll
-  for (int k = 0; k < C::NTASK; ++k)
-    if (task_live(k, 0)) map_block(k, 0, steps, zseg, tfloor);
-  commit_v();
+            for (int kf = 0; kf < NF; ++kf) {
+              Frag<T> qb;
+              lds8(qb, [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
+              mma(pacc, kfr[kf], qb);
+            }
+            if (i == j) {
 #pragma unroll
-  for (int k = 0; k < C::NTASK; ++k) load_x(k, 1);
-  load_v(1);
-
-  f32x4 sacc[RB];
-  f32x4 zacc[C::RBZ];
+              for (int jj = 0; jj < 4; ++jj)
+                if (4 * g + jj > r) pacc[jj] = 0.0f;
+            }
+            store4(pm_at(16 * i + r, 16 * j + 4 * g), pacc[0], pacc[1], pacc[2], pacc[3]);
+            float rs = (pacc[0] + pacc[1]) + (pacc[2] + pacc[3]);
+            rs += __shfl_xor(rs, 16, 64);
+            rs += __shfl_xor(rs, 32, 64);
+            if (g == 0) sm.denp[j][16 * i + r] = rs;
+          }
+        };
+        if constexpr (NMW == 4) {
+          if (mw == 0) p_run(0, 0, 3);
+          else if (mw == 1) { p_run(0, 3, 4); p_run(3, 3, 4); }
+          else if (mw == 2) p_run(1, 1, 4);
+          else p_run(2, 2, 4);
+        } else {
+          if (mw == 0) { p_run(0, 0, 4); p_run(2, 2, 4); }
+          else { p_run(1, 1, 4); p_run(3, 3, 4); }
+        }
+        // phi(Q_c) z_{c-1} for this wave's query blocks
+        const float* zprev = sm.zs[(c + 1) & 1];  // z_{c-1}
+        f32x4 dacc[C::NDEN];
 #pragma unroll
-  for (int i = 0; i < RB; ++i) sacc[i] = zero4();
-#pragma unroll
-  for (int i = 0; i < C::RBZ; ++i) zacc[i] = zero4();
-  // query blocks dbase, dbase + NW, ... (below 4) get their phi(Q) z from this wave
-  const int dbase = (wave + NW - 2 % NW) % NW;
-
-  for (int c = 0; c < c_end; ++c) {
-    const bool scan = c >= c_begin;
-    const int tc = 64 * c;
-    __syncthreads();  // chunk c's phi and V, and z_{c-1}, are in LDS
-
-    f32x4 num[4];
-    if (scan) {
-      // P^T blocks (query block i >= key block j), enumerated key block by key
-      // block: rows = key tokens 16 j + 4 g + jj, column = query token 16 i + r
-      for (int task = wave; task < 10; task += NW) {
-        const int j = task < 4 ? 0 : (task < 7 ? 1 : (task < 9 ? 2 : 3));
-        const int i = task - (j == 0 ? 0 : (j == 1 ? 4 : (j == 2 ? 7 : 9))) + j;
-        f32x4 pacc = zero4();
+        for (int s = 0; s < C::NDEN; ++s) dacc[s] = zero4();
 #pragma unroll
         for (int kf = 0; kf < NF; ++kf) {
-          Frag<T> ka, qb;
-          load_tr4_at(ka, 0, lane, [&](int kk, int col) { return phk_at(32 * kf + 8 * g + kk, 16 * j + col); });
-          load_tr4_at(ka, 4, lane, [&](int kk, int col) { return phk_at(32 * kf + 8 * g + 4 + kk, 16 * j + col); });
-          lds8(qb, [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
-          mma(pacc, ka, qb);
-        }
-        if (i == j) {
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-            if (4 * g + jj > r) pacc[jj] = 0.0f;
-        }
-        store4(pm_at(16 * i + r, 16 * j + 4 * g), pacc[0], pacc[1], pacc[2], pacc[3]);
-        float rs = (pacc[0] + pacc[1]) + (pacc[2] + pacc[3]);
-        rs += __shfl_xor(rs, 16, 64);
-        rs += __shfl_xor(rs, 32, 64);
-        if (g == 0) sm.denp[j][16 * i + r] = rs;
-      }
-      // num^T = S_{c-1}^T phi(Q_c)^T; phi(Q_c) z_{c-1} for this wave's query blocks
-      f32x4 dacc[C::NDEN];
-#pragma unroll
-      for (int s = 0; s < C::NDEN; ++s) dacc[s] = zero4();
-#pragma unroll
-      for (int i = 0; i < 4; ++i) num[i] = zero4();
-      const float* zprev = sm.zb[(c + 1) & 1];
-#pragma unroll
-      for (int kf = 0; kf < NF; ++kf) {
-        Frag<T> sa;
-        sa.set2(0, sacc[2 * kf][0], sacc[2 * kf][1]);
-        sa.set2(2, sacc[2 * kf][2], sacc[2 * kf][3]);
-        sa.set2(4, sacc[2 * kf + 1][0], sacc[2 * kf + 1][1]);
-        sa.set2(6, sacc[2 * kf + 1][2], sacc[2 * kf + 1][3]);
-        Frag<T> za;
-        if (dbase < 4) {
+          Frag<T> za;
           const float4 z0 = *reinterpret_cast<const float4*>(&zprev[32 * kf + 8 * g]);
           const float4 z1 = *reinterpret_cast<const float4*>(&zprev[32 * kf + 8 * g + 4]);
           za.set2(0, z0.x, z0.y);
           za.set2(2, z0.z, z0.w);
           za.set2(4, z1.x, z1.y);
           za.set2(6, z1.z, z1.w);
+#pragma unroll
+          for (int s = 0; s < C::NDEN; ++s) {
+            const int i = dbase + NMW * s;
+            Frag<T> qb;
+            lds8(qb, [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
+            mma(dacc[s], za, qb);
+          }
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          Frag<T> qb;
-          lds8(qb, [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
-          mma(num[i], sa, qb);
+        for (int s = 0; s < C::NDEN; ++s)
+          if (g == 0) sm.deni[16 * (dbase + NMW * s) + r] = dacc[s][0];
+        // num^T = S_{c-1}^T phi(Q_c)^T
 #pragma unroll
-          for (int s = 0; s < C::NDEN; ++s)
-            if (dbase + NW * s == i) mma(dacc[s], za, qb);
-        }
-      }
+        for (int x = 0; x < CBW; ++x)
 #pragma unroll
-      for (int s = 0; s < C::NDEN; ++s)
-        if (dbase + NW * s < 4 && g == 0) sm.deni[16 * (dbase + NW * s) + r] = dacc[s][0];
-    }
-
-    // S += phi(K_c)^T V_c (rows in s_feature order), z alongside
-    Frag<T> vf[2];  // V columns 16 w + r, tokens 32 ks + 8 g + e
+          for (int i = 0; i < 4; ++i) num[x][i] = zero4();
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      load_tr4_at(vf[ks], 0, lane, [&](int kk, int col) { return vt_at(32 * ks + 8 * g + kk, 16 * wave + col); });
-      load_tr4_at(vf[ks], 4, lane, [&](int kk, int col) { return vt_at(32 * ks + 8 * g + 4 + kk, 16 * wave + col); });
-    }
+        for (int kf = 0; kf < NF; ++kf) {
+          Frag<T> sa[CBW];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int frow = s_feature(rb, r);
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        Frag<T> ka;
-        lds8(ka, [&](int e) { return phk_at(frow, 32 * ks + 8 * g + e); });
-        mma(sacc[rb], ka, vf[ks]);
-        if (rb % NW == wave) mma(zacc[rb / NW], ka, ones);
-      }
-    }
-    // z_c to LDS: column 0 of the z tiles, rows 4 g + jj = features s_feature(rb, 4 g + jj)
-#pragma unroll
-    for (int i = 0; i < C::RBZ; ++i) {
-      const int rb = wave + NW * i;
-      if (rb < RB && r == 0)
-        *reinterpret_cast<float4*>(&sm.zb[c & 1][s_feature(rb, 4 * g)]) =
-            float4{zacc[i][0], zacc[i][1], zacc[i][2], zacc[i][3]};
-    }
-
-    __syncthreads();  // phi(Q_c), phi(K_c) and V_c are no longer read; P and the den parts are written
-
-    if (scan) {
-      // num^T += V^T P^T over the key tokens at or before each query block
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-          if (2 * ks <= i) {
-            Frag<T> pb;
-            lds8(pb, [&](int e) { return pm_at(16 * i + r, 32 * ks + 8 * g + e); });
-            mma(num[i], vf[ks], pb);
+          for (int x = 0; x < CBW; ++x) {
+            sa[x].set2(0, sacc[x][2 * kf][0], sacc[x][2 * kf][1]);
+            sa[x].set2(2, sacc[x][2 * kf][2], sacc[x][2 * kf][3]);
+            sa[x].set2(4, sacc[x][2 * kf + 1][0], sacc[x][2 * kf + 1][1]);
+            sa[x].set2(6, sacc[x][2 * kf + 1][2], sacc[x][2 * kf + 1][3]);
           }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = 16 * i + r;
-        float den = sm.deni[q];
+          for (int i = 0; i < 4; ++i) {
+            Frag<T> qb;
+            lds8(qb, [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
 #pragma unroll
-        for (int j = 0; j <= i; ++j) den += sm.denp[j][q];
-        const int t = tc + q;
-        if (t < t_end) {
-          const float rinv = 1.0f / (den + a.eps);
-          store4(out + (size_t)t * DH + 16 * wave + 4 * g, num[i][0] * rinv, num[i][1] * rinv, num[i][2] * rinv,
-                 num[i][3] * rinv);
+            for (int x = 0; x < CBW; ++x) mma(num[x][i], sa[x], qb);
+          }
         }
       }
+      __syncthreads();  // B2: P and the den parts are in LDS
+      if (active) {
+        Frag<T> vf[CBW][2];  // V columns 16 cb + r, tokens 32 ks + 8 g + e
+#pragma unroll
+        for (int x = 0; x < CBW; ++x)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const int c0 = 16 * (CBW * mw + x);
+            load_tr4_at(vf[x][ks], 0, lane, [&](int kk, int col) { return vt_at(32 * ks + 8 * g + kk, c0 + col); });
+            load_tr4_at(vf[x][ks], 4, lane,
+                        [&](int kk, int col) { return vt_at(32 * ks + 8 * g + 4 + kk, c0 + col); });
+          }
+        if (scan) {
+          // num^T += V^T P^T over the key tokens at or before each query block
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+              if (2 * ks <= i) {
+                Frag<T> pb;
+                lds8(pb, [&](int e) { return pm_at(16 * i + r, 32 * ks + 8 * g + e); });
+#pragma unroll
+                for (int x = 0; x < CBW; ++x) mma(num[x][i], vf[x][ks], pb);
+              }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int q = 16 * i + r;
+            float den = sm.deni[q];
+#pragma unroll
+            for (int j = 0; j <= i; ++j) den += sm.denp[j][q];
+            const int t = tc + q;
+            if (t < t_end) {
+              const float rinv = 1.0f / (den + a.eps);
+#pragma unroll
+              for (int x = 0; x < CBW; ++x)
+                store4(out + (size_t)t * DH + 16 * (CBW * mw + x) + 4 * g, num[x][i][0] * rinv,
+                       num[x][i][1] * rinv, num[x][i][2] * rinv, num[x][i][3] * rinv);
+            }
+          }
+        }
+        // S += phi(K_c)^T V_c (rows in s_feature order)
+        // fragments read kPre ahead of their use
+        constexpr int kPre = 4;
+        auto ka_read = [&](Frag<T>& f, int idx) {
+          const int rb = idx / 2, ks = idx % 2;
+          lds8(f, [&](int e) { return phk_at(s_feature(rb, r), 32 * ks + 8 * g + e); });
+        };
+        Frag<T> kb[kPre];
+#pragma unroll
+        for (int p = 0; p < kPre; ++p) ka_read(kb[p], p);
+#pragma unroll
+        for (int idx = 0; idx < 2 * RB; ++idx) {
+          const Frag<T> ka = kb[idx % kPre];
+          if (idx + kPre < 2 * RB) ka_read(kb[idx % kPre], idx + kPre);
+#pragma unroll
+          for (int x = 0; x < CBW; ++x) mma(sacc[x][idx / 2], ka, vf[x][idx % 2]);
+        }
+      }
+      __syncthreads();  // B3: phi(K_c) and V_c are no longer read
     }
-
-    // phi and V of chunk c + 1 into LDS, then fetch chunk c + 2
-#pragma unroll
-    for (int k = 0; k < C::NTASK; ++k)
-      if (task_live(k, c + 1)) map_block(k, c + 1, steps, zseg, tfloor);
-    if (c + 1 < c_end) commit_v();
-#pragma unroll
-    for (int k = 0; k < C::NTASK; ++k) load_x(k, c + 2);
-    load_v(c + 2);
   }
 }
 
 template <typename T, int DH, int L, int MB>
 static hipError_t cs_run(const CausalArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((causal_kernel<T, DH, L, MB>), dim3(a.heads * a.parts), dim3(CsCfg<T, DH, L, MB>::NT), 0, s,
-                     a);
+  hipLaunchKernelGGL((causal_kernel<T, DH, L, MB>), dim3(a.heads * a.parts), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

@@ -64,7 +64,7 @@ struct CsCfg {
 template <typename T, int DH, int L, int MB>
 struct CsLds {
   using C = CsCfg<T, DH, L, MB>;
-  PwlLds<L, C::NSEG> tab;
+  typename PwlTab<T, L, C::NSEG>::type tab;
   alignas(16) T wfr[MB][C::KS][kWave][8];  // W fragments (A of u^T = W X^T, B of u = X W^T)
   alignas(16) T phq[64 * C::FP];           // phi(Q_c), token-major
   alignas(16) T phk[C::FP * 64];           // phi(K_c)^T, feature-major
@@ -87,11 +87,14 @@ __device__ __forceinline__ int swz_rows16(int row, int cg) {
   else return cg ^ ((row / (16 / CPR)) & (CPR - 1));
 }
 // phi(K)^T: read in the row order of s_feature (below): 16 rows that differ in
-// bits 0, 1, 3 and 4.
+// bits 0, 1, 3 and 4; written by 16 lanes whose rows differ in bits 3 to 6.
 template <int CPR>
 __device__ __forceinline__ int swz_k(int row, int cg) {
-  if constexpr (CPR >= 16) return cg ^ ((row & 3) | ((row >> 1) & 12));
-  else return cg ^ (((row >> 1) & 1) | ((row >> 2) & 6));
+  const int b = [&] {
+    if constexpr (CPR >= 16) return (row & 3) | ((row >> 1) & 12);
+    else return (((row >> 1) ^ (row >> 5)) & 1) | ((((row >> 3) ^ (row >> 6)) & 1) << 1) | (((row >> 4) & 1) << 2);
+  }();
+  return cg ^ b;
 }
 // V: transpose reads of four (and eight) consecutive rows.
 template <int CPR>
@@ -337,15 +340,39 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       }
       __builtin_amdgcn_sched_barrier(0);
     };
+    // Lanes g and g ^ 1 (16 apart) trade halves so that an even-g lane holds channel
+    // 2q of tokens 4g .. 4g + 7 and an odd-g lane channel 2q + 1 of tokens
+    // 4(g - 1) .. 4(g - 1) + 7: one 16-byte write each instead of two 8-byte ones.
     auto write_k = [&]() {
-      const int t0 = 16 * pw + 4 * g;
+      const bool ev = (g & 1) == 0;
+      const int t0 = 16 * pw + 4 * (g & ~1);
 #pragma unroll
       for (int p = 0; p < C::NPK; ++p) {
         const int mb = p / (L / 2), q = p % (L / 2);
-        const int f = (16 * mb + r) * L + 2 * q;
+        const int f = (16 * mb + r) * L + 2 * q + (ev ? 0 : 1);
         const Frag<T>& src = kreg[p];
-        store4(phk_at(f, t0), src.get(0), src.get(1), src.get(2), src.get(3));
-        store4(phk_at(f + 1, t0), src.get(4), src.get(5), src.get(6), src.get(7));
+        if constexpr (sizeof(T) == 2) {
+          typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+          const i32x4_t w = __builtin_bit_cast(i32x4_t, src.v);
+          const int s0 = ev ? w[2] : w[0], s1 = ev ? w[3] : w[1];
+          const int r0 = __shfl_xor(s0, 16, 64), r1 = __shfl_xor(s1, 16, 64);
+          const i32x4_t o = ev ? i32x4_t{w[0], w[1], r0, r1} : i32x4_t{r0, r1, w[2], w[3]};
+          *reinterpret_cast<i32x4_t*>(phk_at(f, t0)) = o;
+        } else {
+          const float s0 = ev ? src.v[4] : src.v[0], s1 = ev ? src.v[5] : src.v[1];
+          const float s2 = ev ? src.v[6] : src.v[2], s3 = ev ? src.v[7] : src.v[3];
+          const float r0 = __shfl_xor(s0, 16, 64), r1 = __shfl_xor(s1, 16, 64);
+          const float r2 = __shfl_xor(s2, 16, 64), r3 = __shfl_xor(s3, 16, 64);
+          Frag<float> o;
+          if (ev) {
+            o.v[0] = src.v[0]; o.v[1] = src.v[1]; o.v[2] = src.v[2]; o.v[3] = src.v[3];
+            o.v[4] = r0; o.v[5] = r1; o.v[6] = r2; o.v[7] = r3;
+          } else {
+            o.v[0] = r0; o.v[1] = r1; o.v[2] = r2; o.v[3] = r3;
+            o.v[4] = src.v[4]; o.v[5] = src.v[5]; o.v[6] = src.v[6]; o.v[7] = src.v[7];
+          }
+          sts8(o, [&](int e) { return phk_at(f, t0 + e); });
+        }
       }
     };
     // query rows are needed from chunk c_begin on, key rows and V from chunk 0
@@ -482,8 +509,16 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         for (int x = 0; x < CBW; ++x)
 #pragma unroll
           for (int i = 0; i < 4; ++i) num[x][i] = zero4();
+        // phi(Q) fragments of step kf + 1 are read while step kf multiplies
+        Frag<T> qbuf[2][4];
+        auto q_read = [&](Frag<T> (&qs)[4], int kf) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) lds8(qs[i], [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
+        };
+        q_read(qbuf[0], 0);
 #pragma unroll
         for (int kf = 0; kf < NF; ++kf) {
+          if (kf + 1 < NF) q_read(qbuf[(kf + 1) & 1], kf + 1);
           Frag<T> sa[CBW];
 #pragma unroll
           for (int x = 0; x < CBW; ++x) {
@@ -493,12 +528,10 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
             sa[x].set2(6, sacc[x][2 * kf + 1][2], sacc[x][2 * kf + 1][3]);
           }
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            Frag<T> qb;
-            lds8(qb, [&](int e) { return phq_at(16 * i + r, 32 * kf + 8 * g + e); });
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int x = 0; x < CBW; ++x) mma(num[x][i], sa[x], qb);
-          }
+            for (int x = 0; x < CBW; ++x) mma(num[x][i], sa[x], qbuf[kf & 1][i]);
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
       __syncthreads();  // B2: P and the den parts are in LDS
@@ -533,7 +566,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
             for (int j = 0; j <= i; ++j) den += sm.denp[j][q];
             const int t = tc + q;
             if (t < t_end) {
-              const float rinv = 1.0f / (den + a.eps);
+              const float rinv = 1.0f / (den + ldexpf(a.eps, 2 * sm.tab.scale_exp));
 #pragma unroll
               for (int x = 0; x < CBW; ++x)
                 store4(out + (size_t)t * DH + 16 * (CBW * mw + x) + 4 * g, num[x][i][0] * rinv,

@@ -59,8 +59,9 @@ struct alignas(16) PwlLds {
   uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
   float2 seg[NSEG][SROW];
   int steps;
-  int zero_seg;  // index of the all-zero segment (nbp + 1)
-  float floor;   // 0 when outputs are clamped at zero, -inf otherwise
+  int zero_seg;   // index of the all-zero segment (nbp + 1)
+  float floor;    // 0 when outputs are clamped at zero, -inf otherwise
+  int scale_exp;  // 0: these are the unscaled values
 };
 
 // Cooperative copy of a table from global memory into LDS.  Caller syncs after.
@@ -82,6 +83,42 @@ __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ 
     t.steps = hd.steps;
     t.zero_seg = nseg;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
+    t.scale_exp = 0;
+  }
+}
+
+// The same table with fp16 coefficients (bf16 attention paths): 4 bytes per
+// channel instead of 8, read with mixed-precision fused multiply-adds.
+typedef __attribute__((ext_vector_type(2))) _Float16 half2_t;
+template <int L, int NSEG>
+struct alignas(16) PwlLds16 {
+  static constexpr int SROW = seg_row16(L);
+  float keys[kKeyCap];
+  uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
+  half2_t seg[NSEG][SROW];
+  int steps;
+  int zero_seg;
+  float floor;
+  int scale_exp;
+};
+
+template <int L, int NSEG>
+__device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
+  const int nseg = hd.nbp + 1;
+  const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
+  const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
+  const half2_t* gseg = reinterpret_cast<const half2_t*>(gtab + kTabSeg16);
+  for (int i = threadIdx.x; i < hd.nkeys; i += blockDim.x) t.keys[i] = gkeys[i];
+  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
+  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
+  for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
+  if (threadIdx.x == 0) {
+    t.steps = hd.steps;
+    t.zero_seg = nseg;
+    t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
+    t.scale_exp = hd.scale_exp;
   }
 }
 
@@ -97,9 +134,8 @@ __device__ __forceinline__ float relu_floor(float v, float floor) {
 // advance together, so each step issues NU independent LDS reads and the lookup
 // latency is paid once per step rather than once per value.  NaN compares false
 // everywhere and ends at the start of its window.
-template <int NU, int L, int NSEG>
-__device__ __forceinline__ void pwl_search(const PwlLds<L, NSEG>& t, int steps, const float (&u)[NU],
-                                           int (&seg)[NU]) {
+template <int NU, typename Tab>
+__device__ __forceinline__ void pwl_search(const Tab& t, int steps, const float (&u)[NU], int (&seg)[NU]) {
   const char* keys = reinterpret_cast<const char*>(t.keys);
   unsigned off[NU];
 #pragma unroll
@@ -154,6 +190,48 @@ __device__ __forceinline__ void pwl_pair(const PwlLds<L, NSEG>& t, int seg, int 
   y0 = relu_floor(fmaf(v.x, u, v.y), floor);
   y1 = relu_floor(fmaf(v.z, u, v.w), floor);
 }
+
+// fp16-coefficient versions (values scaled by 2^scale_exp)
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_channels(const PwlLds16<L, NSEG>& t, int seg, float floor, float u,
+                                             float (&y)[L]) {
+  if constexpr (L % 4 == 0) {
+    typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
+    const half8_t* st = reinterpret_cast<const half8_t*>(&t.seg[seg][0]);
+#pragma unroll
+    for (int q = 0; q < L / 4; ++q) {
+      const half8_t v = st[q];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
+    }
+  } else {
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      const half2_t v = t.seg[seg][l];
+      y[l] = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
+    }
+  }
+}
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_pair(const PwlLds16<L, NSEG>& t, int seg, int q, float floor, float u,
+                                         float& y0, float& y1) {
+  static_assert(L % 2 == 0, "channel pairs need an even L");
+  typedef __attribute__((ext_vector_type(4))) _Float16 half4_t;
+  const half4_t v = reinterpret_cast<const half4_t*>(&t.seg[seg][0])[q];
+  y0 = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
+  y1 = relu_floor(__builtin_fmaf((float)v[2], u, (float)v[3]), floor);
+}
+
+// Table type of an attention kernel: fp16 coefficients for bf16 data, fp32 otherwise.
+template <typename T, int L, int NSEG>
+struct PwlTab {
+  using type = PwlLds<L, NSEG>;
+};
+template <int L, int NSEG>
+struct PwlTab<__bf16, L, NSEG> {
+  using type = PwlLds16<L, NSEG>;
+};
 
 // ---------------------------------------------------------------------------
 // element types and fragments

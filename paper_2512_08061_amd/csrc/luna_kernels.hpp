@@ -14,7 +14,10 @@ namespace luna {
 //   header   PwlHeader
 //   keys     the sorted breakpoints, fp32, padded with +inf to PwlHeader::nkeys
 //   buckets  uint16 per bucket of u: byte offset (4 * index) of its search window
-//   segments (slope, intercept) pairs, segment-major, L per segment
+//   segments (slope, intercept) pairs, segment-major, L per segment, fp32
+//   segments16 the same pairs scaled by 2^scale_exp in fp16 (bf16 attention paths;
+//            the power of two keeps the largest magnitude near 2^14 and cancels
+//            between numerator and denominator once eps is scaled alike)
 //
 // Search.  The float bits of u pick one of kNumBuckets buckets (bucket_of), an
 // order-preserving partition of the real line: sign, then |u| below 2^-kBucketExp,
@@ -34,7 +37,8 @@ constexpr size_t kTabHeader = 0;
 constexpr size_t kTabKeys = 256;
 constexpr size_t kTabBuckets = kTabKeys + kKeyCap * 4;
 constexpr size_t kTabSeg = kTabBuckets + ((size_t)kNumBuckets * 2 + 15) / 16 * 16;
-constexpr size_t kTableBytes = (kTabSeg + (size_t)kSegCap * 8 + 255) / 256 * 256;
+constexpr size_t kTabSeg16 = kTabSeg + (size_t)kSegCap * 8;
+constexpr size_t kTableBytes = (kTabSeg16 + (size_t)kSegCap * 4 + 255) / 256 * 256;
 
 struct PwlHeader {
   int nbp;     // number of breakpoints
@@ -42,6 +46,7 @@ struct PwlHeader {
   int L;       // channels
   int nonneg;  // 1: relu on the channel outputs
   int nkeys;   // keys stored (breakpoints plus +inf padding), >= 2^steps - 1
+  int scale_exp;  // fp16 segments hold 2^scale_exp times the fp32 values
 };
 
 // Bucket of u from its float bits; monotone in u (-0.0 and +0.0 fall in the two
@@ -142,6 +147,8 @@ hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStr
 // Rows whose size is a multiple of 64 bytes are padded by 16 bytes so that random
 // segments spread over all LDS banks.
 constexpr int seg_row(int L) { return (L % 8 == 0) ? L + 2 : L; }
+// fp16 segment rows (half2 per channel), padded by 16 bytes when 4L is a multiple of 32
+constexpr int seg_row16(int L) { return (4 * L) % 32 == 0 ? L + 4 : L; }
 // Segments an LDS table of `bytes` holds for L channels (at most 64 L + 2: width-64
 // per-channel MLPs plus the all-zero segment).  A table needs breakpoints + 2.
 constexpr int nseg_cap(int L, int bytes) {

@@ -45,7 +45,7 @@ struct NcCfg {
 template <typename T, int DH, int L, int MB>
 __global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
   using C = NcCfg<T, DH, L, MB>;
-  __shared__ PwlLds<L, C::NSEG> tab;
+  __shared__ typename PwlTab<T, L, C::NSEG>::type tab;
   __shared__ __attribute__((aligned(16))) T vt[4][DH][C::VROW];
   __shared__ float red[C::DP][DH + 1];
 
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void nc_reduce_kernel(NoncausalArgs a) {
 template <typename T, int DH, int L, int MB>
 __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
   using C = NcCfg<T, DH, L, MB>;
-  __shared__ PwlLds<L, C::NSEG> tab;
+  __shared__ typename PwlTab<T, L, C::NSEG>::type tab;
   const int head = blockIdx.x / a.tiles;
   const int tile = blockIdx.x - head * a.tiles;
   const int hset = a.phi.per_head ? head % a.H : 0;
@@ -350,7 +350,7 @@ __global__ __launch_bounds__(256, 1) void nc_readout_kernel(NoncausalArgs a) {
       mma(den, zf[k], pq[k]);
     }
     if (ok) {
-      const float rinv = 1.0f / (den[0] + a.eps);
+      const float rinv = 1.0f / (den[0] + ldexpf(a.eps, 2 * tab.scale_exp));
       T* o = out + (size_t)t * DH + 4 * g;
 #pragma unroll
       for (int cb = 0; cb < C::CB; ++cb)
@@ -374,7 +374,7 @@ template <typename T, int DH, int L, int MB>
 struct NcFusedLds {
   using C = NcCfg<T, DH, L, MB>;
   static constexpr int VR = DH + C::VE;  // padded V-tile row (elements)
-  PwlLds<L, C::NSEG> tab;
+  typename PwlTab<T, L, C::NSEG>::type tab;
   union {
     T vt[kNcWaves][32][VR];   // per-wave V tile of the current 32-token step
     float red[C::DP][DH + 1]; // cross-wave sum of (S | z)
@@ -684,7 +684,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
     }
     const int t = 16 * b + r;
     if (t < n) {
-      const float rinv = 1.0f / (den[0] + a.eps);
+      const float rinv = 1.0f / (den[0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
       T* o = out + (size_t)t * DH + 4 * g;
 #pragma unroll
       for (int cb = 0; cb < C::CB; ++cb)

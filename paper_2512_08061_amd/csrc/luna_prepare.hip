@@ -42,6 +42,8 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   __shared__ int has_bp[kSortCap];
   __shared__ float g_s[16];
   __shared__ int hist[kNumBuckets];
+  __shared__ float2 segv[kSegCap];  // segment values before they are written out
+  __shared__ int s_vmax;            // bits of the largest |value| (non-negative float)
   __shared__ int wave_tot[4];
   __shared__ int s_nbp, s_most;
 
@@ -59,6 +61,7 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   if (tid == 0) {
     s_nbp = 0;
     s_most = 0;
+    s_vmax = 0;
   }
   int N = 2;
   while (N < units) N *= 2;
@@ -158,8 +161,8 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   // 4. segment values by prefix sums over the sorted breakpoints
   const double inv = 1.0 / sqrt((double)a.M);
   const int shared = (a.C1 == 1);
-  float2* seg = reinterpret_cast<float2*>(tab + kTabSeg);
   const int nseg = nbp + 1;
+  float vmax = 0.0f;
   const int per = (nseg + 31) / 32;  // segments per block
   const int b = tid % 32;            // block within the channel
   for (int l0 = 0; l0 < a.L; l0 += 8) {
@@ -221,7 +224,9 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
     if (lok) {
       double s = bs + es, t = (double)g_s[l] + bt + et;
       for (int j = j0; j < j1; ++j) {
-        seg[j * a.L + l] = make_float2((float)(s * inv), (float)(t * inv));
+        const float2 v = make_float2((float)(s * inv), (float)(t * inv));
+        segv[j * a.L + l] = v;
+        vmax = fmaxf(vmax, fmaxf(fabsf(v.x), fabsf(v.y)));
         double ds, dt;
         delta(j, ds, dt);
         s += ds;
@@ -229,8 +234,27 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
       }
     }
   }
+  // 5. fp32 segments, and fp16 ones scaled by 2^e so that the largest magnitude
+  // lands in [2^13, 2^14) (e clamped to [-20, 20])
+  atomicMax(&s_vmax, __float_as_int(vmax));
+  __syncthreads();
+  const float vm = __int_as_float(s_vmax);
+  int e = 0;
+  if (vm > 0.0f && isfinite(vm)) {
+    int ex;
+    frexpf(vm, &ex);  // vm = m 2^ex, m in [0.5, 1)
+    e = min(20, max(-20, 14 - ex));
+  }
+  float2* seg = reinterpret_cast<float2*>(tab + kTabSeg);
+  half2_t* seg16 = reinterpret_cast<half2_t*>(tab + kTabSeg16);
+  for (int i = tid; i < nseg * a.L; i += blockDim.x) {
+    const float2 v = segv[i];
+    seg[i] = v;
+    seg16[i] = half2_t{(_Float16)ldexpf(v.x, e), (_Float16)ldexpf(v.y, e)};
+  }
   if (tid == 0) {
     PwlHeader* hd = reinterpret_cast<PwlHeader*>(tab + kTabHeader);
+    hd->scale_exp = e;
     hd->nbp = nbp;
     hd->steps = steps;
     hd->nkeys = nkeys;

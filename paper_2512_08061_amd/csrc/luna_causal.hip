@@ -223,16 +223,15 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     };
     // u for the 16 rows: query rows as u^T = W X^T (lane: projections 16 mb + 4 g + j
     // of token r), key rows as u = X W^T (lane: projection 16 mb + r of tokens 4 g + j)
+    Frag<T> wreg[MB][KS];  // W fragments, loaded once (after the first barrier)
     auto project = [&](const Frag<T> (&xf)[KS], bool isq, float (&uu)[4 * MB]) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         f32x4 acc = zero4();
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          Frag<T> wf;
-          load8(wf, &sm.wfr[mb][ks][lane][0]);
-          if (isq) mma(acc, wf, xf[ks]);
-          else mma(acc, xf[ks], wf);
+          if (isq) mma(acc, wreg[mb][ks], xf[ks]);
+          else mma(acc, xf[ks], wreg[mb][ks]);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + sm.bias[16 * mb + (isq ? 4 * g + j : r)];
@@ -279,10 +278,11 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       pwl_search(sm.tab, steps, uu, sg);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
+        // one projection block (four values) at a time, so that the table reads of
+        // all blocks are not hoisted together
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          // two values at a time, so that their table reads are not all hoisted together
-          if (j % 2 == 0) __builtin_amdgcn_sched_barrier(0);
           float y[L];
           pwl_channels<L>(sm.tab, 16 * mb + 4 * g + j < M ? sg[4 * mb + j] : zseg, floor, uu[4 * mb + j], y);
 #pragma unroll
@@ -355,7 +355,12 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
           typedef __attribute__((ext_vector_type(4))) int i32x4_t;
           const i32x4_t w = __builtin_bit_cast(i32x4_t, src.v);
           const int s0 = ev ? w[2] : w[0], s1 = ev ? w[3] : w[1];
-          const int r0 = __shfl_xor(s0, 16, 64), r1 = __shfl_xor(s1, 16, 64);
+          // v_permlane16_swap of a value with itself hands every lane the value of
+          // lane l ^ 16: even 16-lane rows find it in the second result, odd rows in
+          // the first
+          const auto p0 = __builtin_amdgcn_permlane16_swap((unsigned)s0, (unsigned)s0, false, false);
+          const auto p1 = __builtin_amdgcn_permlane16_swap((unsigned)s1, (unsigned)s1, false, false);
+          const int r0 = (int)(ev ? p0[1] : p0[0]), r1 = (int)(ev ? p1[1] : p1[0]);
           const i32x4_t o = ev ? i32x4_t{w[0], w[1], r0, r1} : i32x4_t{r0, r1, w[2], w[3]};
           *reinterpret_cast<i32x4_t*>(phk_at(f, t0)) = o;
         } else {
@@ -383,6 +388,10 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     const int steps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
     const int zseg = sm.tab.zero_seg;
     const float tfloor = sm.tab.floor;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) load8(wreg[mb][ks], &sm.wfr[mb][ks][lane][0]);
     if (0 >= c_begin) {
       map_q(xq, steps, zseg, tfloor);
       write_q();

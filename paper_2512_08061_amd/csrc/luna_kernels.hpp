@@ -30,9 +30,9 @@ constexpr int kKeyCap = 1024;           // sorted breakpoints incl. +inf padding
 constexpr int kSegCap = 5120;           // (slope, intercept) pairs, segment-major
 constexpr int kMaxUnits = kKeyCap - 1;  // breakpoints one table can hold
 constexpr int kBucketExp = 6;           // resolved magnitudes: [2^-6, 2^6)
-constexpr int kBucketMant = 6;          // mantissa bits per exponent
+constexpr int kBucketMant = 7;          // mantissa bits per exponent
 constexpr int kBucketMag = 2 * kBucketExp * (1 << kBucketMant) + 2;  // per sign, incl. under/overflow
-constexpr int kNumBuckets = 2 * kBucketMag;                          // 1540
+constexpr int kNumBuckets = 2 * kBucketMag;                          // 3076
 constexpr size_t kTabHeader = 0;
 constexpr size_t kTabKeys = 256;
 constexpr size_t kTabBuckets = kTabKeys + kKeyCap * 4;

@@ -159,6 +159,85 @@ __device__ __forceinline__ void pwl_search(const Tab& t, int steps, const float 
   for (int i = 0; i < NU; ++i) seg[i] = (int)(off[i] >> 2);
 }
 
+// The same search, ending in the byte offset 4 seg of the segment's key instead of
+// seg.  The halvings are unrolled for the usual step counts, so that every key read
+// addresses `off` plus a constant that the LDS instruction's offset field carries:
+// a step then costs one compare, one select and one add.
+template <int STEPS, int NU, typename Tab>
+__device__ __forceinline__ void pwl_halvings(const Tab& t, const float (&u)[NU], unsigned (&off)[NU]) {
+  const char* keys = reinterpret_cast<const char*>(t.keys);
+#pragma unroll
+  for (int s = STEPS - 1; s >= 0; --s) {
+    const unsigned h4 = 4u << s;
+#pragma unroll
+    for (int i = 0; i < NU; ++i) {
+      const float key = *reinterpret_cast<const float*>(keys + off[i] + (h4 - 4u));
+      off[i] += key < u[i] ? h4 : 0u;
+    }
+  }
+}
+template <int NU, typename Tab>
+__device__ __forceinline__ void pwl_search_off(const Tab& t, int steps, const float (&u)[NU], unsigned (&off)[NU]) {
+#pragma unroll
+  for (int i = 0; i < NU; ++i) {
+    const uint32_t bits = __float_as_uint(u[i]);
+    const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
+    int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
+    mm = min(max(mm, 0), kBucketMag - 1);
+    const int idx = kBucketMag + (mm ^ ((int)bits >> 31));
+    off[i] = t.buckets[idx];
+  }
+  switch (steps) {
+    case 0: break;
+    case 1: pwl_halvings<1>(t, u, off); break;
+    case 2: pwl_halvings<2>(t, u, off); break;
+    case 3: pwl_halvings<3>(t, u, off); break;
+    case 4: pwl_halvings<4>(t, u, off); break;
+    default: {
+      const char* keys = reinterpret_cast<const char*>(t.keys);
+      for (int s = steps - 1; s >= 0; --s) {
+        const unsigned h4 = 4u << s;
+#pragma unroll
+        for (int i = 0; i < NU; ++i) {
+          const float key = *reinterpret_cast<const float*>(keys + off[i] + h4 - 4u);
+          off[i] += key < u[i] ? h4 : 0u;
+        }
+      }
+    }
+  }
+}
+
+// psi_l(u), l = 0..L-1, on the segment whose key sits at byte offset `off` (4 seg):
+// the segment row starts at off * (row bytes / 4), one multiply-add from `off`.
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_eval_off(const PwlLds<L, NSEG>& t, unsigned off, float floor, float u,
+                                             float (&y)[L]) {
+  constexpr unsigned kRow = sizeof(t.seg[0]);
+  static_assert(kRow % 4 == 0 && L % 2 == 0, "rows of whole float4 pairs");
+  const char* row = reinterpret_cast<const char*>(&t.seg[0][0]) + __umul24(off, kRow / 4);
+#pragma unroll
+  for (int q = 0; q < L / 2; ++q) {
+    const float4 v = reinterpret_cast<const float4*>(row)[q];
+    y[2 * q] = relu_floor(fmaf(v.x, u, v.y), floor);
+    y[2 * q + 1] = relu_floor(fmaf(v.z, u, v.w), floor);
+  }
+}
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_eval_off(const PwlLds16<L, NSEG>& t, unsigned off, float floor, float u,
+                                             float (&y)[L]) {
+  constexpr unsigned kRow = sizeof(t.seg[0]);
+  static_assert(kRow % 4 == 0 && L % 4 == 0, "rows of whole 16-byte channel quads");
+  typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
+  const char* row = reinterpret_cast<const char*>(&t.seg[0][0]) + __umul24(off, kRow / 4);
+#pragma unroll
+  for (int q = 0; q < L / 4; ++q) {
+    const half8_t v = reinterpret_cast<const half8_t*>(row)[q];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
+  }
+}
+
 // psi_l(u) for l = 0..L-1 on segment `seg`, already scaled by 1/sqrt(M) (folded
 // into the table).
 template <int L, int NSEG>
@@ -221,6 +300,80 @@ __device__ __forceinline__ void pwl_pair(const PwlLds16<L, NSEG>& t, int seg, in
   const half4_t v = reinterpret_cast<const half4_t*>(&t.seg[seg][0])[q];
   y0 = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
   y1 = relu_floor(__builtin_fmaf((float)v[2], u, (float)v[3]), floor);
+}
+
+// Search half of a table in LDS: keys and bucket windows only.  The coefficient rows
+// stay in global memory and are fetched through the vector memory path (they are
+// small enough to stay cached), which keeps their data-dependent gathers off the
+// LDS.
+struct alignas(16) PwlKeys {
+  float keys[kKeyCap];
+  uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
+  int steps;
+  float floor;    // 0 when outputs are clamped at zero, -inf otherwise
+  int scale_exp;  // fp16 rows hold 2^scale_exp times the values
+};
+
+__device__ inline void pwl_load_keys(PwlKeys& t, const uint8_t* __restrict__ gtab, bool fp16_rows) {
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
+  const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
+  const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
+  for (int i = threadIdx.x; i < hd.nkeys; i += blockDim.x) t.keys[i] = gkeys[i];
+  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
+  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
+  if (threadIdx.x == 0) {
+    t.steps = hd.steps;
+    t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
+    t.scale_exp = fp16_rows ? hd.scale_exp : 0;
+  }
+}
+
+// Coefficient rows of a table as a range-checked buffer: segment s of L channels at
+// byte s * L * (4 or 8); an offset at or past the end reads as zeros, which
+// evaluates to psi = 0 (the masked value).
+template <bool FP16>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pwl_rows(const uint8_t* gtab, int nseg, int L) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(gtab + (FP16 ? kTabSeg16 : kTabSeg)), (short)0,
+                                           nseg * L * (FP16 ? 4 : 8), 0x00020000);
+}
+constexpr unsigned kPwlMasked = 0x80000000u;  // row offset that reads as zeros
+
+// psi_l(u), l = 0..L-1, of segment `seg` (its row at byte `row`) from the global
+// rows: fp16 pairs (half2 per channel, 4 channels per 16-byte load) ...
+template <int L>
+__device__ __forceinline__ void pwl_fetch(__amdgpu_buffer_rsrc_t rs, unsigned row,
+                                          __attribute__((ext_vector_type(4))) unsigned (&c)[L / 4]) {
+#pragma unroll
+  for (int q = 0; q < L / 4; ++q) c[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, row + 16 * q, 0, 0);
+}
+template <int L>
+__device__ __forceinline__ void pwl_eval16(const __attribute__((ext_vector_type(4))) unsigned (&c)[L / 4],
+                                           float floor, float u, float (&y)[L]) {
+  typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
+#pragma unroll
+  for (int q = 0; q < L / 4; ++q) {
+    const half8_t v = __builtin_bit_cast(half8_t, c[q]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
+  }
+}
+// ... or fp32 pairs (two channels per 16-byte load)
+template <int L>
+__device__ __forceinline__ void pwl_fetch32(__amdgpu_buffer_rsrc_t rs, unsigned row,
+                                            __attribute__((ext_vector_type(4))) unsigned (&c)[L / 2]) {
+#pragma unroll
+  for (int q = 0; q < L / 2; ++q) c[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, row + 16 * q, 0, 0);
+}
+template <int L>
+__device__ __forceinline__ void pwl_eval32(const __attribute__((ext_vector_type(4))) unsigned (&c)[L / 2],
+                                           float floor, float u, float (&y)[L]) {
+#pragma unroll
+  for (int q = 0; q < L / 2; ++q) {
+    const float4 v = __builtin_bit_cast(float4, c[q]);
+    y[2 * q] = relu_floor(fmaf(v.x, u, v.y), floor);
+    y[2 * q + 1] = relu_floor(fmaf(v.z, u, v.w), floor);
+  }
 }
 
 // Table type of an attention kernel: fp16 coefficients for bf16 data, fp32 otherwise.

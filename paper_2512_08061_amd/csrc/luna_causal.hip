@@ -69,6 +69,8 @@ struct CsCfg {
   static constexpr int SP = 64 * SZ + 16;         // P row stride
   static constexpr int VPT = 64 * DH / VE / 256;  // 16-byte V chunks per map-wave thread
   static constexpr int NSEG = nseg_cap(L, kAttnSegBytes);
+  // bf16: fp16 coefficient rows and keys in 4-key groups; fp32: fp32 rows and plain keys
+  using Tab = typename std::conditional<SZ == 2, PwlLdsN<half2_t, L, NSEG>, PwlLds<L, NSEG>>::type;
   static_assert(NCB == 2 || NCB == 4 || NCB == 8, "d must be 32, 64 or 128");
   static_assert(FP % 32 == 0 && L % 2 == 0 && (SZ == 4 || L % 4 == 0), "features must fill 32-wide fragments");
   static_assert(VPT * 256 * VE == 64 * DH, "V chunks must split evenly over the map threads");
@@ -85,7 +87,7 @@ struct CsLds {
   alignas(16) float zp[4][C::FP];          // z_c over each 16-row block of keys
   alignas(16) T zs[2][C::FP];              // z_c, summed, by chunk parity
   float bias[16 * MB];                     // projection biases, 0 for padded projections
-  typename PwlTab<T, L, C::NSEG>::type tab;  // search keys, bucket windows, coefficient rows
+  typename C::Tab tab;  // search keys, bucket windows, coefficient rows
   alignas(16) T wfr[MB][C::KS][kWave][8];  // W fragments (A of u^T = W X^T, B of u = X W^T)
   alignas(16) char pm[64 * C::SP];         // P, query-major (blocks above the diagonal stay 0)
   alignas(16) char phq[64 * C::SQ];        // phi(Q_c), token-major, feature f at position f
@@ -324,10 +326,10 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     // phi of this lane's 4 MB values u, as Pack4<T> per (block, channel) (the four j
     // in order)
     Pack4<T> ph[MB][L];
-    auto map_all = [&](const float (&uu)[4 * MB], bool isk, int steps, unsigned zoff, float floor) {
+    auto map_all = [&](const float (&uu)[4 * MB], bool isk, int steps, int nodes, unsigned zoff, float floor) {
       constexpr int NU = 4 * MB;
       unsigned off[NU];
-      pwl_search_off(sm.tab, steps, uu, off);
+      pwl_search_any(sm.tab, steps, nodes, uu, off);
       if (isk && pad_proj) {  // padded projections select the all-zero segment
 #pragma unroll
         for (int i = 0; i < NU; ++i)
@@ -339,8 +341,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         for (int jp = 0; jp < 2; ++jp) {
           const int i0 = 4 * mb + 2 * jp;
           float y0[L], y1[L];
-          pwl_eval_off<L>(sm.tab, off[i0], floor, uu[i0], y0);
-          pwl_eval_off<L>(sm.tab, off[i0 + 1], floor, uu[i0 + 1], y1);
+          pwl_eval_off(sm.tab, off[i0], floor, uu[i0], y0);
+          pwl_eval_off(sm.tab, off[i0 + 1], floor, uu[i0 + 1], y1);
 #pragma unroll
           for (int l = 0; l < L; ++l) ph[mb][l].set2(2 * jp, y0[l], y1[l]);
         }
@@ -416,17 +418,18 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       }
     }
     const int steps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
+    const int nodes = __builtin_amdgcn_readfirstlane(pwl_nodes(sm.tab));
     const unsigned zoff = 4u * sm.tab.zero_seg;
     const float tfloor = sm.tab.floor;
     float uu[4 * MB];
     if (0 >= c_begin) {
       project(xq, true, uu);
-      map_all(uu, false, steps, zoff, tfloor);
+      map_all(uu, false, steps, nodes, zoff, tfloor);
       write_q();
     }
     load_rows(xq, a.Q, 1, 1 >= c_begin);
     project(xk, false, uu);
-    map_all(uu, true, steps, zoff, tfloor);
+    map_all(uu, true, steps, nodes, zoff, tfloor);
     write_k();
     add_z();
     load_rows(xk, a.K, 1, true);
@@ -440,7 +443,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       const bool qn = cn < c_end && cn >= c_begin;
       if (qn) {
         project(xq, true, uu);
-        map_all(uu, false, steps, zoff, tfloor);
+        map_all(uu, false, steps, nodes, zoff, tfloor);
       }
       load_rows(xq, a.Q, cn + 1, cn + 1 >= c_begin);  // also during the state-only chunks
       __syncthreads();  // B2
@@ -450,7 +453,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         store_v();
         load_v(cn + 1);
         project(xk, false, uu);
-        map_all(uu, true, steps, zoff, tfloor);
+        map_all(uu, true, steps, nodes, zoff, tfloor);
         load_rows(xk, a.K, cn + 1, true);
         add_z();
       }

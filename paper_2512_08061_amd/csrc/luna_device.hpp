@@ -376,6 +376,139 @@ __device__ __forceinline__ void pwl_eval32(const __attribute__((ext_vector_type(
   }
 }
 
+// A table whose keys are stored as overlapping groups: node s holds keys s .. s + 3
+// (+inf past the stored keys), so that the keys one u compares against -- the first
+// 4 or 8 from its bucket's offset when the header's `nodes` is 1 or 2 -- arrive in
+// one or two aligned 16-byte loads instead of a chain of dependent halvings.  RowT
+// is the coefficient pair type: half2_t (fp16, scaled) or float2.
+template <typename RowT, int L, int NSEG>
+struct alignas(16) PwlLdsN {
+  static constexpr bool kHalf = sizeof(RowT) == 4;
+  static constexpr int SROW = kHalf ? seg_row16(L) : seg_row(L);
+  float4 nodes[kKeyCap + 8];
+  uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
+  RowT seg[NSEG][SROW];
+  int steps;
+  int nodes_per_u;  // the header's `nodes`
+  int zero_seg;     // index of the all-zero segment (nbp + 1)
+  float floor;      // 0 when outputs are clamped at zero, -inf otherwise
+  int scale_exp;    // fp16 rows hold 2^scale_exp times the values
+};
+
+template <typename RowT, int L, int NSEG>
+__device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __restrict__ gtab) {
+  using Tab = PwlLdsN<RowT, L, NSEG>;
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
+  const int nseg = hd.nbp + 1;
+  const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
+  const RowT* gseg = reinterpret_cast<const RowT*>(gtab + (Tab::kHalf ? kTabSeg16 : kTabSeg));
+  auto key = [&](int i) { return i < hd.nkeys ? gkeys[i] : __builtin_inff(); };
+  for (int i = threadIdx.x; i < kKeyCap + 8; i += blockDim.x)
+    t.nodes[i] = make_float4(key(i), key(i + 1), key(i + 2), key(i + 3));
+  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
+  const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
+  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
+  for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  // one all-zero segment after the real ones: masked values select it and evaluate
+  // to exactly 0 without per-element masks
+  for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = RowT{};
+  if (threadIdx.x == 0) {
+    t.steps = hd.steps;
+    t.nodes_per_u = hd.nodes;
+    t.zero_seg = nseg;
+    t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
+    t.scale_exp = Tab::kHalf ? hd.scale_exp : 0;
+  }
+}
+
+// Number of the four keys of `k` below u (NaN compares false everywhere).
+__device__ __forceinline__ unsigned keys_below(const float4& k, float u) {
+  return (unsigned)(k.x < u) + (unsigned)(k.y < u) + (unsigned)(k.z < u) + (unsigned)(k.w < u);
+}
+
+// Byte offset 4 seg of the segment of each u (seg = number of breakpoints below u):
+// bucket offset plus the count over its one or two key groups, or, when the table
+// has no node form (`nodes` 0), the halving search over node-strided keys.
+template <int NU, typename RowT, int L, int NSEG>
+__device__ __forceinline__ void pwl_search_n(const PwlLdsN<RowT, L, NSEG>& t, int steps, int nodes,
+                                             const float (&u)[NU], unsigned (&off)[NU]) {
+  const char* nb = reinterpret_cast<const char*>(t.nodes);
+  unsigned s16[NU];  // byte offset of the window's first node: 16 x its first key
+#pragma unroll
+  for (int i = 0; i < NU; ++i) {
+    const uint32_t bits = __float_as_uint(u[i]);
+    const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
+    int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
+    mm = min(max(mm, 0), kBucketMag - 1);
+    const int idx = kBucketMag + (mm ^ ((int)bits >> 31));
+    s16[i] = 4u * t.buckets[idx];
+  }
+  if (nodes == 1) {
+#pragma unroll
+    for (int i = 0; i < NU; ++i)
+      off[i] = (s16[i] >> 2) + 4u * keys_below(*reinterpret_cast<const float4*>(nb + s16[i]), u[i]);
+  } else if (nodes == 2) {
+#pragma unroll
+    for (int i = 0; i < NU; ++i)
+      off[i] = (s16[i] >> 2) + 4u * (keys_below(*reinterpret_cast<const float4*>(nb + s16[i]), u[i]) +
+                                     keys_below(*reinterpret_cast<const float4*>(nb + s16[i] + 64), u[i]));
+  } else {
+    for (int s = steps - 1; s >= 0; --s) {
+      const unsigned h16 = 16u << s;
+#pragma unroll
+      for (int i = 0; i < NU; ++i) {
+        const float key = *reinterpret_cast<const float*>(nb + s16[i] + h16 - 16u);
+        s16[i] += key < u[i] ? h16 : 0u;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NU; ++i) off[i] = s16[i] >> 2;
+  }
+}
+
+// psi_l(u), l = 0..L-1, on the segment at byte offset `off` (4 seg) of a node table.
+template <typename RowT, int L, int NSEG>
+__device__ __forceinline__ void pwl_eval_off(const PwlLdsN<RowT, L, NSEG>& t, unsigned off, float floor, float u,
+                                             float (&y)[L]) {
+  constexpr unsigned kRow = sizeof(t.seg[0]);
+  const char* row = reinterpret_cast<const char*>(&t.seg[0][0]) + __umul24(off, kRow / 4);
+  if constexpr (PwlLdsN<RowT, L, NSEG>::kHalf) {
+    static_assert(kRow % 16 == 0 && L % 4 == 0, "rows of whole 16-byte channel quads");
+    typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
+#pragma unroll
+    for (int q = 0; q < L / 4; ++q) {
+      const half8_t v = reinterpret_cast<const half8_t*>(row)[q];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
+    }
+  } else {
+    static_assert(kRow % 16 == 0 && L % 2 == 0, "rows of whole float4 pairs");
+#pragma unroll
+    for (int q = 0; q < L / 2; ++q) {
+      const float4 v = reinterpret_cast<const float4*>(row)[q];
+      y[2 * q] = relu_floor(fmaf(v.x, u, v.y), floor);
+      y[2 * q + 1] = relu_floor(fmaf(v.z, u, v.w), floor);
+    }
+  }
+}
+
+// Search on either table form: the node table uses its key groups when it has them.
+template <int NU, int L, int NSEG>
+__device__ __forceinline__ void pwl_search_any(const PwlLds<L, NSEG>& t, int steps, int, const float (&u)[NU],
+                                               unsigned (&off)[NU]) {
+  pwl_search_off(t, steps, u, off);
+}
+template <int NU, typename RowT, int L, int NSEG>
+__device__ __forceinline__ void pwl_search_any(const PwlLdsN<RowT, L, NSEG>& t, int steps, int nodes,
+                                               const float (&u)[NU], unsigned (&off)[NU]) {
+  pwl_search_n(t, steps, nodes, u, off);
+}
+template <int L, int NSEG>
+__device__ __forceinline__ int pwl_nodes(const PwlLds<L, NSEG>&) { return 0; }
+template <typename RowT, int L, int NSEG>
+__device__ __forceinline__ int pwl_nodes(const PwlLdsN<RowT, L, NSEG>& t) { return t.nodes_per_u; }
+
 // Table type of an attention kernel: fp16 coefficients for bf16 data, fp32 otherwise.
 template <typename T, int L, int NSEG>
 struct PwlTab {

@@ -13,6 +13,7 @@ namespace luna {
 // Layout of one table (kTableBytes, a multiple of 256):
 //   header   PwlHeader
 //   keys     the sorted breakpoints, fp32, padded with +inf to PwlHeader::nkeys
+//            (one window past the last breakpoint when that fits)
 //   buckets  uint16 per bucket of u: byte offset (4 * index) of its search window
 //   segments (slope, intercept) pairs, segment-major, L per segment, fp32
 //   segments16 the same pairs scaled by 2^scale_exp in fp16 (bf16 attention paths;
@@ -47,6 +48,8 @@ struct PwlHeader {
   int nonneg;  // 1: relu on the channel outputs
   int nkeys;   // keys stored (breakpoints plus +inf padding), >= 2^steps - 1
   int scale_exp;  // fp16 segments hold 2^scale_exp times the fp32 values
+  int nodes;   // 1 or 2: the keys a u compares against are the first 4 or 8 from its
+               // bucket's offset (no window was shifted to fit); 0 otherwise
 };
 
 // Bucket of u from its float bits; monotone in u (-0.0 and +0.0 fall in the two

@@ -147,7 +147,10 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
   int steps = 0;
   while ((1 << steps) - 1 < most) ++steps;
   const int window = (1 << steps) - 1;
-  const int nkeys = nbp > window ? nbp : window;
+  // +inf padding of a whole window past the last breakpoint, so that no window needs
+  // shifting; only when that exceeds the capacity are late windows moved down (their
+  // extra keys lie below the bucket and compare true, so counts stay exact)
+  const int nkeys = nbp + window < kKeyCap ? nbp + window : kKeyCap;
   for (int j = 0; j < kPer; ++j) {
     const int bb = tid * kPer + j;
     if (bb < kNumBuckets) {
@@ -258,6 +261,7 @@ __global__ __launch_bounds__(256) void pwl_prepare_kernel(PrepareArgs a) {
     hd->nbp = nbp;
     hd->steps = steps;
     hd->nkeys = nkeys;
+    hd->nodes = nbp + window > kKeyCap ? 0 : (most <= 4 ? 1 : (most <= 8 ? 2 : 0));
     hd->L = a.L;
     hd->nonneg = a.nonneg;
   }

@@ -85,11 +85,27 @@ def test_featuremap_psi_sweep(shared, nonneg):
     assert err.max() < 2e-6 * max(1.0, np.abs(ref).max()), err.max()
 
 
+# bucket layout of the kernels' table search: magnitudes in [2^-BUCKET_EXP,
+# 2^BUCKET_EXP) split by exponent and BUCKET_MANT mantissa bits
+BUCKET_EXP, BUCKET_MANT = 6, 7
+
+
+def _bucket_of(u):
+    """Bucket index of each float32 u, in the kernels' order (sign, then magnitude)."""
+    bits = np.asarray(u, np.float32).view(np.uint32).astype(np.int64)
+    mag = (bits >> (23 - BUCKET_MANT)) & ((1 << (31 - 23 + BUCKET_MANT)) - 1)
+    nmag = 2 * BUCKET_EXP * (1 << BUCKET_MANT) + 2
+    m = np.clip(mag - ((127 - BUCKET_EXP) << BUCKET_MANT) + 1, 0, nmag - 1)
+    return np.where(bits >> 31, nmag - 1 - m, nmag + m)
+
+
 def _bucket_edges():
     """Every boundary of the float-bit buckets the kernels index the breakpoints by
-    (powers of two and 1/64 mantissa steps over [2^-6, 2^6]), both signs, with the
-    fp32 neighbours of each, plus zeros and denormals."""
-    mags = [np.float32(2.0) ** e * np.float32(1 + k / 64) for e in range(-6, 6) for k in range(64)]
+    (powers of two and 2^-BUCKET_MANT mantissa steps over [2^-6, 2^6]), both signs,
+    with the fp32 neighbours of each, plus zeros and denormals."""
+    steps = 1 << BUCKET_MANT
+    mags = [np.float32(2.0) ** e * np.float32(1 + k / steps) for e in range(-BUCKET_EXP, BUCKET_EXP)
+            for k in range(steps)]
     mags.append(np.float32(64.0))
     mags = np.array(mags, np.float32)
     vals = np.concatenate([mags, np.nextafter(mags, np.float32(0)), np.nextafter(mags, np.float32(np.inf))])
@@ -138,6 +154,43 @@ def test_featuremap_bucket_edges(layout):
                         np.linspace(-3, 3, 601, dtype=np.float32)])
     say(f"bucket edges {layout}: {u.size} values")
     _featuremap_exact(p, u)
+
+
+def _breakpoints(p):
+    bp = (-p["fc1_b"].astype(np.float64) / p["fc1_w"].astype(np.float64)).ravel().astype(np.float32)
+    bp = bp[np.isfinite(bp)]
+    return np.where(bp == 0, np.float32(0), bp)
+
+
+@pytest.mark.parametrize("layout,most_range", [("spread", (1, 4)), ("six", (5, 8)), ("crowded", (9, 10 ** 6))])
+def test_attn_causal_search_paths(layout, most_range):
+    """The bf16 causal kernel's table search, on u placed exactly on breakpoints and
+    at small offsets from them, for breakpoint layouts whose fullest bucket holds at
+    most 4 keys (one 4-key group per search), 5 to 8 (two groups) or more (halving
+    search).  W has one nonzero column, so u = x_0 + b exactly when x_0 = 0."""
+    w = small_workload("bf16", B=1, H=2, n=200, d=128, M=32, L=8, causal=True)
+    Q, K, V, p = inputs(w, seed=31)
+    Q, K, p = Q.copy(), K.copy(), dict(p)
+    rng = np.random.default_rng(32)
+    a = p["fc1_w"].astype(np.float64).copy()
+    beta = -p["fc1_b"].astype(np.float64) / a
+    if layout == "six":     # six breakpoints of channel 0 inside one otherwise empty bucket near 37.3
+        beta[0, :6] = 37.3 + 1e-3 * np.arange(6)
+    elif layout == "crowded":  # three channels' breakpoints all inside one bucket near 0.3
+        beta[:3] = 0.3 + 1e-5 * rng.random(beta[:3].shape)
+    p["fc1_b"] = (-beta * a).astype(np.float32)
+    bp = _breakpoints(p)
+    most = np.bincount(_bucket_of(bp)).max()
+    assert most_range[0] <= most <= most_range[1], most
+    p["W"] = np.zeros_like(p["W"])
+    p["W"][:, 0] = 1.0
+    p["b"] = rng.choice(np.concatenate([bp, _bucket_edges()[::17]]), size=p["b"].shape).astype(np.float32)
+    for X in (Q, K):
+        X[..., 0] = rng.choice(np.float32([0, 0, 0, 2.0 ** -20, -2.0 ** -20, 2.0 ** -9, -2.0 ** -9, 0.75, -1.5]),
+                               size=X.shape[:-1])
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))
+    assert_close(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), "bf16", f"search {layout}")
 
 
 @pytest.mark.parametrize("name", list(wl.WORKLOADS))

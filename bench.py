@@ -149,27 +149,34 @@ def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
     import oracle
 
     threads = len(os.sched_getaffinity(0))
-    nc_heads, cs_tokens = 3, 4096
+    budget = 8.0  # seconds per part: whole heads are added until a part has run this long
     with threadpool_limits(threads):
-        Q, K, V = (a[0, :nc_heads].astype(np.float64) for a in arrs4)
-        t0 = time.perf_counter()
-        oracle.attn_noncausal(Q, K, V, p4, eps=w4.eps)
-        t_nc = time.perf_counter() - t0
-        Q, K, V = (a[0, :1, :cs_tokens].astype(np.float64) for a in arrs5)
-        t0 = time.perf_counter()
-        oracle.attn_causal(Q, K, V, p5, eps=w5.eps)
-        t_cs = time.perf_counter() - t0
-    step = (t_nc * (w4.B * w4.H * w4.n) / (nc_heads * w4.n)
-            + t_cs * (w5.B * w5.H * w5.n) / cs_tokens)
+        nc_heads, t_nc = 0, 0.0
+        while nc_heads < w4.B * w4.H and t_nc < budget:
+            b, h = divmod(nc_heads, w4.H)
+            Q, K, V = (a[b, h:h + 1].astype(np.float64) for a in arrs4)
+            t0 = time.perf_counter()
+            oracle.attn_noncausal(Q, K, V, p4, eps=w4.eps)
+            t_nc += time.perf_counter() - t0
+            nc_heads += 1
+        cs_heads, t_cs = 0, 0.0
+        while cs_heads < w5.B * w5.H and t_cs < budget:
+            b, h = divmod(cs_heads, w5.H)
+            Q, K, V = (a[b, h:h + 1].astype(np.float64) for a in arrs5)
+            t0 = time.perf_counter()
+            oracle.attn_causal(Q, K, V, p5, eps=w5.eps)
+            t_cs += time.perf_counter() - t0
+            cs_heads += 1
+    step = t_nc * (w4.B * w4.H) / nc_heads + t_cs * (w5.B * w5.H) / cs_heads
     tokens = w4.B * w4.n + w5.B * w5.n
     return {
         "value": tokens / step,
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"float64 oracle: non-causal on {nc_heads} of {w4.B * w4.H} heads "
-                   f"({t_nc:.1f} s) and causal token recurrence on the first {cs_tokens} tokens of 1 of "
-                   f"{w5.B * w5.H} heads ({t_cs:.1f} s), scaled by head-tokens to one full step"),
+        "sample": (f"float64 oracle on whole heads: non-causal {nc_heads} of {w4.B * w4.H} heads ({t_nc:.1f} s), "
+                   f"causal token recurrence {cs_heads} of {w5.B * w5.H} heads ({t_cs:.1f} s), "
+                   f"scaled by heads to one full step"),
     }
 
 

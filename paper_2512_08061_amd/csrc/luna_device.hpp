@@ -64,6 +64,19 @@ struct alignas(16) PwlLds {
   int scale_exp;  // 0: these are the unscaled values
 };
 
+// Cooperative 16-byte copies global -> LDS: `n16` chunks, and rows of `row16` chunks
+// from a dense source into a destination with `dst_row16`-chunk rows.
+__device__ inline void copy16(void* dst, const void* src, int n16) {
+  uint4* d = reinterpret_cast<uint4*>(dst);
+  const uint4* sp = reinterpret_cast<const uint4*>(src);
+  for (int i = threadIdx.x; i < n16; i += blockDim.x) d[i] = sp[i];
+}
+__device__ inline void copy16_rows(void* dst, int dst_row16, const void* src, int row16, int rows) {
+  uint4* d = reinterpret_cast<uint4*>(dst);
+  const uint4* sp = reinterpret_cast<const uint4*>(src);
+  for (int i = threadIdx.x; i < rows * row16; i += blockDim.x) d[(i / row16) * dst_row16 + i % row16] = sp[i];
+}
+
 // Cooperative copy of a table from global memory into LDS.  Caller syncs after.
 template <int L, int NSEG>
 __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
@@ -72,10 +85,13 @@ __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ 
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const float2* gseg = reinterpret_cast<const float2*>(gtab + kTabSeg);
-  for (int i = threadIdx.x; i < hd.nkeys; i += blockDim.x) t.keys[i] = gkeys[i];
-  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
-  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
-  for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
+  copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
+  if constexpr ((L * 8) % 16 == 0) {
+    copy16_rows(&t.seg[0][0], sizeof(t.seg[0]) / 16, gseg, L * 8 / 16, nseg);
+  } else {
+    for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  }
   // one all-zero segment after the real ones: masked values select it and evaluate
   // to exactly 0 without per-element masks
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = make_float2(0.0f, 0.0f);
@@ -109,10 +125,13 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const half2_t* gseg = reinterpret_cast<const half2_t*>(gtab + kTabSeg16);
-  for (int i = threadIdx.x; i < hd.nkeys; i += blockDim.x) t.keys[i] = gkeys[i];
-  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
-  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
-  for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
+  copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
+  if constexpr ((L * 4) % 16 == 0) {
+    copy16_rows(&t.seg[0][0], sizeof(t.seg[0]) / 16, gseg, L * 4 / 16, nseg);
+  } else {
+    for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  }
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
   if (threadIdx.x == 0) {
     t.steps = hd.steps;
@@ -402,13 +421,30 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
   const int nseg = hd.nbp + 1;
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const RowT* gseg = reinterpret_cast<const RowT*>(gtab + (Tab::kHalf ? kTabSeg16 : kTabSeg));
-  auto key = [&](int i) { return i < hd.nkeys ? gkeys[i] : __builtin_inff(); };
-  for (int i = threadIdx.x; i < kKeyCap + 8; i += blockDim.x)
-    t.nodes[i] = make_float4(key(i), key(i + 1), key(i + 2), key(i + 3));
-  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
-  const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
-  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
-  for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  // groups 4m .. 4m + 3 from the aligned key quads m and m + 1 (+inf past the stored keys)
+  static_assert((kKeyCap + 8) % 4 == 0, "whole quads of groups");
+  const float kInf = __builtin_inff();
+  for (int m = threadIdx.x; m < (kKeyCap + 8) / 4; m += blockDim.x) {
+    float k[8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = m + h;  // key quad
+      const float4 v = 4 * q < kKeyCap ? reinterpret_cast<const float4*>(gkeys)[q] : make_float4(kInf, kInf, kInf, kInf);
+      k[4 * h + 0] = v.x; k[4 * h + 1] = v.y; k[4 * h + 2] = v.z; k[4 * h + 3] = v.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (4 * m + e >= hd.nkeys) k[e] = kInf;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) t.nodes[4 * m + e] = make_float4(k[e], k[e + 1], k[e + 2], k[e + 3]);
+  }
+  copy16(t.buckets, gtab + kTabBuckets, (kNumBuckets * 2 + 15) / 16);
+  constexpr int kPair = sizeof(RowT);
+  if constexpr ((L * kPair) % 16 == 0) {
+    copy16_rows(&t.seg[0][0], sizeof(t.seg[0]) / 16, gseg, L * kPair / 16, nseg);
+  } else {
+    for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  }
   // one all-zero segment after the real ones: masked values select it and evaluate
   // to exactly 0 without per-element masks
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = RowT{};

@@ -373,13 +373,13 @@ constexpr int kNcWaves = 4;  // one wave per SIMD: the whole register file per w
 template <typename T, int DH, int L, int MB>
 struct NcFusedLds {
   using C = NcCfg<T, DH, L, MB>;
-  static constexpr int VR = DH + C::VE;  // padded V-tile row (elements)
+  static constexpr int VR = DH + C::VE;   // padded V-tile row (elements)
+  static constexpr int NTILE = MB * L * C::CB + MB;  // accumulator tiles of S, then of z
   typename PwlTab<T, L, C::NSEG>::type tab;
   union {
-    T vt[kNcWaves][32][VR];   // per-wave V tile of the current 32-token step
-    float red[C::DP][DH + 1]; // cross-wave sum of (S | z)
+    T vt[kNcWaves][32][VR];             // per-wave V tile of the current 32-token step
+    float4 red[NTILE][kWave];           // cross-wave sum of the accumulator tiles, lane-major
   } u;
-  alignas(16) T sfr[C::CB + 1][C::NF][kWave][8];  // S (and z in the last slot) as A fragments
 };
 
 template <typename T, int DH, int L, int MB>
@@ -563,62 +563,77 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
     }
   }
 
-  // ---- sum the eight waves in a fixed order, then form readout fragments ----
+  // ---- sum the waves' accumulator tiles in a fixed order (deterministic), lane by
+  // lane: every tile is one 16-byte read-modify-write per lane ----
   __syncthreads();  // every wave is done with its V tile (red aliases it)
   for (int w = 0; w < kNcWaves; ++w) {
     if (wave == w) {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < MB; ++mb) {
 #pragma unroll
         for (int l = 0; l < L; ++l)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int row = (mb * L + l) * 16 + 4 * g + j;
-#pragma unroll
-            for (int cb = 0; cb < C::CB; ++cb) {
-              float& d = sm.u.red[row][16 * cb + r];
-              d = (w == 0) ? accS[mb][l][cb][j] : d + accS[mb][l][cb][j];
-            }
-            if (r == l) {
-              float& d = sm.u.red[row][DH];
-              d = (w == 0) ? accZ[mb][j] : d + accZ[mb][j];
-            }
+          for (int cb = 0; cb < C::CB; ++cb) {
+            float4& d = sm.u.red[(mb * L + l) * C::CB + cb][lane];
+            const f32x4 v = accS[mb][l][cb];
+            d = (w == 0) ? make_float4(v[0], v[1], v[2], v[3])
+                         : make_float4(d.x + v[0], d.y + v[1], d.z + v[2], d.w + v[3]);
           }
+        float4& d = sm.u.red[MB * L * C::CB + mb][lane];
+        const f32x4 v = accZ[mb];
+        d = (w == 0) ? make_float4(v[0], v[1], v[2], v[3])
+                     : make_float4(d.x + v[0], d.y + v[1], d.z + v[2], d.w + v[3]);
+      }
     }
     __syncthreads();
   }
-  {
-    T* fr = &sm.sfr[0][0][0][0];
-    for (int idx = threadIdx.x; idx < (int)C::FRAG_ELEMS; idx += blockDim.x) {
-      const int e = idx % 8;
-      const int ln = (idx / 8) % kWave;
-      const int kappa = (idx / (8 * kWave)) % C::NF;
-      const int cb = idx / (8 * kWave * C::NF);
-      const int gg = ln / 16, rr = ln % 16;
-      const int p = 8 * kappa + e;
-      float v = 0.0f;
-      if (p < 4 * MB * L) {
-        const int mbj = p / L, l = p % L;
-        const int row = ((mbj / 4) * L + l) * 16 + 4 * gg + (mbj % 4);
-        v = (cb < C::CB) ? sm.u.red[row][16 * cb + rr] : sm.u.red[row][DH];
-      }
-      fr[idx] = (T)v;
-    }
-  }
-  __syncthreads();
-
-  // ---- readout phase: wave w takes 16-token blocks w, w + kNcWaves, ... ----
+  // Readout fragments.  Tile (mb, l, cb), lane (g, r), element j holds S[feature
+  // (mb, projection 16 mb + 4 g + j, channel l)][column 16 cb + r]; readout fragment
+  // kappa, slot e of the same lane is list position p = 8 kappa + e = (4 mb + j) L + l
+  // of that lane's group, column 16 cb + r: the same value, no lane exchange.  z
+  // (tile column l = channel l) is gathered across lanes: every row of its fragment
+  // is z.
   Frag<T> sf[C::CB][C::NF], zf[C::NF];
 #pragma unroll
   for (int cb = 0; cb < C::CB; ++cb)
 #pragma unroll
-    for (int k = 0; k < C::NF; ++k) load8(sf[cb][k], &sm.sfr[cb][k][lane][0]);
+    for (int k = 0; k < C::NF; ++k) sf[cb][k].zero();
 #pragma unroll
-  for (int k = 0; k < C::NF; ++k) load8(zf[k], &sm.sfr[C::CB][k][lane][0]);
+  for (int k = 0; k < C::NF; ++k) zf[k].zero();
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb) {
+        const float4 v = sm.u.red[(mb * L + l) * C::CB + cb][lane];
+        const float vj[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int p = (4 * mb + j) * L + l;
+          sf[cb][p / 8].set(p % 8, vj[j]);
+        }
+      }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      const float4 v = sm.u.red[MB * L * C::CB + mb][16 * g + l];  // lane (g, l): channel l
+      const float vj[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int p = (4 * mb + j) * L + l;
+        zf[p / 8].set(p % 8, vj[j]);
+      }
+    }
 
+  // ---- readout phase: wave w takes 16-token blocks w, w + kNcWaves, ... ----
   const int nblk = (n + 15) / 16;
-  constexpr int QD = 4;  // query blocks in flight per wave
-  Frag<T> qn[QD][C::KS];
+  // NB query blocks are mapped together, so that their table lookups overlap (one wave
+  // per SIMD has no other wave to hide their latency); blocks past the end read zero
+  // rows and store nothing.  The next group's rows are fetched while one is mapped.
+  constexpr int NB = 4;
+  Frag<T> qn[NB][C::KS];
   auto fetch_q = [&](Frag<T> (&qf)[C::KS], int b) {
     const int t = 16 * b + r;
 #pragma unroll
@@ -628,67 +643,74 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
     }
   };
 #pragma unroll
-  for (int i = 0; i < QD; ++i) fetch_q(qn[i], wave + kNcWaves * i);
-  for (int b0 = wave; b0 < nblk; b0 += kNcWaves * QD)
+  for (int i = 0; i < NB; ++i) fetch_q(qn[i], wave + kNcWaves * i);
+  for (int b0 = wave; b0 < nblk; b0 += kNcWaves * NB) {
+    Frag<T> qf[NB][C::KS];
 #pragma unroll
-  for (int i = 0; i < QD; ++i) {
-    const int b = b0 + kNcWaves * i;
-    if (b >= nblk) break;
-    Frag<T> qf[C::KS];
+    for (int i = 0; i < NB; ++i) {
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) qf[ks] = qn[i][ks];
-    fetch_q(qn[i], b + kNcWaves * QD);
-    float uu[4 * MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      f32x4 acc = zero4();
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) mma(acc, wf[mb][ks], qf[ks]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j] + brow[mb][j];
+      for (int ks = 0; ks < C::KS; ++ks) qf[i][ks] = qn[i][ks];
+      fetch_q(qn[i], b0 + kNcWaves * (NB + i));
     }
-    int sg[4 * MB];
+    float uu[NB * 4 * MB];  // [block][mb][j]
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int ks = 0; ks < C::KS; ++ks) mma(acc, wf[mb][ks], qf[i][ks]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) uu[(i * MB + mb) * 4 + j] = acc[j] + brow[mb][j];
+      }
+    int sg[NB * 4 * MB];
     pwl_search(sm.tab, tsteps, uu, sg);
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int i = 0; i < NB; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (!prow[mb][j]) sg[4 * mb + j] = zseg;
-    Frag<T> pq[C::NF];
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int k = 0; k < C::NF; ++k) pq[k].zero();
+        for (int j = 0; j < 4; ++j)
+          if (!prow[mb][j]) sg[(i * MB + mb) * 4 + j] = zseg;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int i = 0; i < NB; ++i) {
+      Frag<T> pq[C::NF];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float y[L];
-        pwl_channels<L>(sm.tab, sg[4 * mb + j], tfloor, uu[4 * mb + j], y);
+      for (int k = 0; k < C::NF; ++k) pq[k].zero();
 #pragma unroll
-        for (int l = 0; l < L; ++l) {
-          const int p = (mb * 4 + j) * L + l;
-          if constexpr (L % 2 == 0) {
-            if (l % 2 == 0) pq[p / 8].set2(p % 8, y[l], y[l + 1]);
-          } else {
-            pq[p / 8].set(p % 8, y[l]);
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int v = (i * MB + mb) * 4 + j;
+          float y[L];
+          pwl_channels<L>(sm.tab, sg[v], tfloor, uu[v], y);
+#pragma unroll
+          for (int l = 0; l < L; ++l) {
+            const int p = (mb * 4 + j) * L + l;
+            if constexpr (L % 2 == 0) {
+              if (l % 2 == 0) pq[p / 8].set2(p % 8, y[l], y[l + 1]);
+            } else {
+              pq[p / 8].set(p % 8, y[l]);
+            }
           }
         }
+      f32x4 num[C::CB], den = zero4();
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb) num[cb] = zero4();
+#pragma unroll
+      for (int k = 0; k < C::NF; ++k) {
+#pragma unroll
+        for (int cb = 0; cb < C::CB; ++cb) mma(num[cb], sf[cb][k], pq[k]);
+        mma(den, zf[k], pq[k]);
       }
-    f32x4 num[C::CB], den = zero4();
+      const int t = 16 * (b0 + kNcWaves * i) + r;
+      if (t < n) {
+        const float rinv = 1.0f / (den[0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
+        T* o = out + (size_t)t * DH + 4 * g;
 #pragma unroll
-    for (int cb = 0; cb < C::CB; ++cb) num[cb] = zero4();
-#pragma unroll
-    for (int k = 0; k < C::NF; ++k) {
-#pragma unroll
-      for (int cb = 0; cb < C::CB; ++cb) mma(num[cb], sf[cb][k], pq[k]);
-      mma(den, zf[k], pq[k]);
-    }
-    const int t = 16 * b + r;
-    if (t < n) {
-      const float rinv = 1.0f / (den[0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
-      T* o = out + (size_t)t * DH + 4 * g;
-#pragma unroll
-      for (int cb = 0; cb < C::CB; ++cb)
-        store4(o + 16 * cb, num[cb][0] * rinv, num[cb][1] * rinv, num[cb][2] * rinv, num[cb][3] * rinv);
+        for (int cb = 0; cb < C::CB; ++cb)
+          store4(o + 16 * cb, num[cb][0] * rinv, num[cb][1] * rinv, num[cb][2] * rinv, num[cb][3] * rinv);
+      }
     }
   }
 }

@@ -57,6 +57,7 @@ luna_status check_common(const Problem& pb) {
   if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
   const int seg_cap = luna::nseg_cap(p->L, pb.op == LUNA_OP_FEATUREMAP ? luna::kFmSegBytes : luna::kAttnSegBytes);
   if (units + 2 > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "too many breakpoints for the LDS segment table");
+  if ((units + 1) * p->L > luna::kSegCap) return fail(LUNA_ERR_UNSUPPORTED, "too many segments for the table");
   return LUNA_OK;
 }
 
@@ -154,8 +155,6 @@ luna_status enqueue_prepare(const Problem& pb, uint8_t* ws, const Layout& lay, h
   a.M = p->M;
   a.nonneg = p->nonneg;
   a.tables = ws + lay.tables;
-  a.zero_ptr = nullptr;
-  a.zero_count = 0;
   hipError_t e = luna::launch_prepare(a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "table kernel launch");
 }

@@ -71,8 +71,6 @@ struct PrepareArgs {
   const float* fc2_b;  // [P][L]
   int P, C1, L, hidden, M, nonneg;
   uint8_t* tables;     // [P][kTableBytes]
-  int* zero_ptr;       // words cleared by the prepare kernel (may be null)
-  int zero_count;
 };
 
 // Projection and channel-MLP parameters as the kernels see them.

@@ -156,6 +156,22 @@ def test_featuremap_bucket_edges(layout):
     _featuremap_exact(p, u)
 
 
+@pytest.mark.parametrize("L,hidden,shared", [(1, 63, False), (8, 61, False), (16, 19, False), (16, 33, True),
+                                             (4, 64, True)])
+def test_featuremap_unit_counts(L, hidden, shared):
+    """Tables built from odd and uneven numbers of hidden units (the rank sort's
+    padded last pair, one or two units per thread), per-channel and shared first
+    layers, at every breakpoint and its fp32 neighbours."""
+    w = small_workload("f32", B=1, H=1, n=8, d=32, M=1, L=L, hidden=hidden, shared_channels=shared)
+    p = dict(wl.make_params(w, seed=41))
+    bp = (-p["fc1_b"].astype(np.float64) / p["fc1_w"].astype(np.float64)).ravel().astype(np.float32)
+    bp = bp[np.isfinite(bp)]
+    u = np.concatenate([bp, np.nextafter(bp, np.float32(np.inf)), np.nextafter(bp, np.float32(-np.inf)),
+                        np.linspace(-4, 4, 401, dtype=np.float32)])
+    say(f"unit counts L={L} hidden={hidden} shared={shared}: {u.size} values")
+    _featuremap_exact(p, u, shared=shared)
+
+
 def _breakpoints(p):
     bp = (-p["fc1_b"].astype(np.float64) / p["fc1_w"].astype(np.float64)).ravel().astype(np.float32)
     bp = bp[np.isfinite(bp)]

@@ -251,7 +251,9 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   // buffers: rows at or past n (t_end for the output) read as 0 and are not written.
   auto rows_of = [&](const void* base, int cc, int t_lim) {
     const char* p = reinterpret_cast<const char*>(base) + (hoff + (size_t)64 * cc * DH) * SZ;
-    const int rows = max(0, min(64, t_lim - 64 * cc));
+    // uniform, and kept in a scalar register: a vector-held record count would make
+    // every buffer access a readfirstlane loop
+    const int rows = __builtin_amdgcn_readfirstlane(max(0, min(64, t_lim - 64 * cc)));
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(p), (short)0, rows * DH * SZ, kBufferFlags);
   };
 
@@ -324,17 +326,10 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       }
     };
     // phi of this lane's 4 MB values u, as Pack4<T> per (block, channel) (the four j
-    // in order)
-    Pack4<T> ph[MB][L];
-    auto map_all = [&](const float (&uu)[4 * MB], bool isk, int steps, int nodes, unsigned zoff, float floor) {
-      constexpr int NU = 4 * MB;
-      unsigned off[NU];
-      pwl_search_any(sm.tab, steps, nodes, uu, off);
-      if (isk && pad_proj) {  // padded projections select the all-zero segment
-#pragma unroll
-        for (int i = 0; i < NU; ++i)
-          if (16 * (i / 4) + r >= M) off[i] = zoff;
-      }
+    // in order), from the values and their segment offsets; query and key rows
+    Pack4<T> phq_r[MB][L], phk_r[MB][L];
+    auto eval_all = [&](Pack4<T> (&ph)[MB][L], const float (&uu)[4 * MB], const unsigned (&off)[4 * MB],
+                        float floor) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -351,13 +346,13 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int l = 0; l < L; ++l) ph[mb][l].store(q_dst + feat<MB>(16 * mb, l) * SZ);
+        for (int l = 0; l < L; ++l) phq_r[mb][l].store(q_dst + feat<MB>(16 * mb, l) * SZ);
     };
     auto write_k = [&]() {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int l = 0; l < L; ++l) ph[mb][l].store(k_dst + 16 * (mb + MB * l) * SK);
+        for (int l = 0; l < L; ++l) phk_r[mb][l].store(k_dst + 16 * (mb + MB * l) * SK);
     };
     // z over this wave's key rows: tile mb rows = projections 16 mb + 4 g + jj,
     // column l = channel l, accumulated from phi(K) fragments (channels 2q, 2q + 1 of
@@ -377,8 +372,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           Frag<T> kf;
-          ph[mb][2 * q].to_frag(kf, 0);
-          ph[mb][2 * q + 1].to_frag(kf, 4);
+          phk_r[mb][2 * q].to_frag(kf, 0);
+          phk_r[mb][2 * q + 1].to_frag(kf, 4);
           mma(zacc[mb], kf, oh);
         }
       }
@@ -421,45 +416,80 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     const int nodes = __builtin_amdgcn_readfirstlane(pwl_nodes(sm.tab));
     const unsigned zoff = 4u * sm.tab.zero_seg;
     const float tfloor = sm.tab.floor;
-    float uu[4 * MB];
-    if (0 >= c_begin) {
-      project(xq, true, uu);
-      map_all(uu, false, steps, nodes, zoff, tfloor);
-      write_q();
-    }
+    // u of the query rows and the key rows of one chunk and their segment offsets
+    float uq[4 * MB], uk[4 * MB];
+    unsigned oq[4 * MB], ok[4 * MB];
+    // projections of the rows held in xq, xk and the searches, as one batch when the
+    // query rows are live, so that their lookups overlap
+    auto project_search = [&](auto qlive) {
+      constexpr bool kQ = decltype(qlive)::value;
+      if constexpr (kQ) {
+        project(xq, true, uq);
+        project(xk, false, uk);
+        float uu[8 * MB];
+        unsigned oo[8 * MB];
+#pragma unroll
+        for (int i = 0; i < 4 * MB; ++i) {
+          uu[i] = uq[i];
+          uu[4 * MB + i] = uk[i];
+        }
+        pwl_search_any(sm.tab, steps, nodes, uu, oo);
+#pragma unroll
+        for (int i = 0; i < 4 * MB; ++i) {
+          oq[i] = oo[i];
+          ok[i] = oo[4 * MB + i];
+        }
+      } else {
+        project(xk, false, uk);
+        pwl_search_any(sm.tab, steps, nodes, uk, ok);
+      }
+      if (pad_proj) {  // padded projections of the key rows select the all-zero segment
+#pragma unroll
+        for (int i = 0; i < 4 * MB; ++i)
+          if (16 * (i / 4) + r >= M) ok[i] = zoff;
+      }
+    };
+    // phi of the rows held in xq, xk (the query rows when live) into phq_r, phk_r, and
+    // the key rows added to z
+    auto map_rows = [&](auto qlive) {
+      project_search(qlive);
+      if constexpr (decltype(qlive)::value) eval_all(phq_r, uq, oq, tfloor);
+      eval_all(phk_r, uk, ok, tfloor);
+      add_z();
+    };
+    // chunk 0
+    if (0 >= c_begin) map_rows(std::true_type{});
+    else map_rows(std::false_type{});
     load_rows(xq, a.Q, 1, 1 >= c_begin);
-    project(xk, false, uu);
-    map_all(uu, true, steps, nodes, zoff, tfloor);
-    write_k();
-    add_z();
     load_rows(xk, a.K, 1, true);
+    if (0 >= c_begin) write_q();
+    write_k();
+    write_z();  // z through chunk 0
     store_v();
     load_v(1);
 
-    // iteration c maps chunk c + 1 (rows fetched one chunk ahead)
+    // Iteration c: between B1 and B2 the matrix waves read chunk c's tiles while this
+    // wave maps chunk c + 1 (rows fetched one chunk ahead) into registers; after B2 it
+    // writes chunk c + 1's tiles, V and z.
     for (int c = 0; c < c_end; ++c) {
       const int cn = c + 1;
-      __syncthreads();  // B1
-      const bool qn = cn < c_end && cn >= c_begin;
-      if (qn) {
-        project(xq, true, uu);
-        map_all(uu, false, steps, nodes, zoff, tfloor);
-      }
-      load_rows(xq, a.Q, cn + 1, cn + 1 >= c_begin);  // also during the state-only chunks
-      __syncthreads();  // B2
-      if (qn) write_q();
-      write_z();  // z_c, before chunk c + 1 is added
-      if (cn < c_end) {
-        store_v();
-        load_v(cn + 1);
-        project(xk, false, uu);
-        map_all(uu, true, steps, nodes, zoff, tfloor);
-        load_rows(xk, a.K, cn + 1, true);
-        add_z();
-      }
-      __syncthreads();  // B3
+      __syncthreads();  // B1: chunk c's tiles are in LDS; zp holds z through chunk c
       sum_z(c & 1);
-      if (cn < c_end) write_k();
+      const bool kn = cn < c_end, qn = kn && cn >= c_begin;
+      if (qn) map_rows(std::true_type{});
+      else if (kn) map_rows(std::false_type{});
+      // the loads are issued on every path (past the end as empty buffers, which read
+      // nothing), so that the waits for them count the same loads on every path
+      load_rows(xq, a.Q, cn + 1, kn && cn + 1 >= c_begin);
+      load_rows(xk, a.K, cn + 1, kn);
+      __syncthreads();  // B2: chunk c's phi tiles and V are no longer read
+      if (kn) {
+        if (qn) write_q();
+        write_k();
+        write_z();  // z through chunk c + 1
+        store_v();
+      }
+      load_v(cn + 1);
     }
   } else {
     // =========================================================== matrix waves
@@ -481,8 +511,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     for (int x = 0; x < CBW; ++x)
 #pragma unroll
       for (int i = 0; i < RB; ++i) sacc[x][i] = zero4();
-    // num^T = S_{c-1}^T phi(Q_c)^T for the chunk about to be scanned (0 for chunk 0)
-    f32x4 num[CBW][4];
+    f32x4 num[CBW][4];  // num^T of the chunk being scanned
 #pragma unroll
     for (int x = 0; x < CBW; ++x)
 #pragma unroll
@@ -495,6 +524,18 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     // key block j, so that phi(K_j) is read once per run.  k-slot (g, e) of fragment kf
     // is feature 32 kf + 8 g + e: phi(Q) positions 32 kf + 8 g + e, phi(K)^T rows
     // 32 kf + 16 (e / 4) + 4 g + e % 4.  Operands of kf + 1 are read while kf multiplies.
+    // P^T block (j, i) to LDS (entries above the diagonal zeroed) and its row sums
+    auto p_store = [&](f32x4 p, int j, int i) {
+      if (i == j) {
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          if (4 * g + jj > r) p[jj] = 0.0f;
+      }
+      store4(reinterpret_cast<T*>(p_dst + 16 * i * SP + 16 * j * SZ), p[0], p[1], p[2], p[3]);
+      float rs = (p[0] + p[1]) + (p[2] + p[3]);
+      rs = sum_xor32(sum_xor16(rs));
+      if (g == 0) sm.denp[j][16 * i + r] = rs;
+    };
     auto p_run = [&](auto cnt, int j, int i0) {
       constexpr int CNT = decltype(cnt)::value;
       f32x4 pacc[CNT];
@@ -516,19 +557,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
-      for (int b = 0; b < CNT; ++b) {
-        const int i = i0 + b;
-        f32x4 p = pacc[b];
-        if (i == j) {
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-            if (4 * g + jj > r) p[jj] = 0.0f;
-        }
-        store4(reinterpret_cast<T*>(p_dst + 16 * i * SP + 16 * j * SZ), p[0], p[1], p[2], p[3]);
-        float rs = (p[0] + p[1]) + (p[2] + p[3]);
-        rs = sum_xor32(sum_xor16(rs));
-        if (g == 0) sm.denp[j][16 * i + r] = rs;
-      }
+      for (int b = 0; b < CNT; ++b) p_store(pacc[b], j, i0 + b);
     };
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
@@ -549,6 +578,106 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       if (g == 0) sm.deni[16 * i + r] = dacc[0];
     };
 
+    // num^T = S_{c-1}^T phi(Q_c)^T: accumulator tiles 2 kf, 2 kf + 1 of S are the
+    // k-fragment kf of S^T (slot (g, e) = feature 32 kf + 8 g + e); phi(Q) fragments
+    // (step kf, block i) are read in that order kPre ahead of their use
+    auto readout = [&]() {
+#pragma unroll
+      for (int x = 0; x < CBW; ++x)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) num[x][i] = zero4();
+      constexpr int kPre = 4;
+      auto q_read = [&](Frag<T>& f, int idx) { lds8(f, q_src + 16 * (idx % 4) * SQ + 32 * (idx / 4) * SZ); };
+      Frag<T> qb[kPre];
+#pragma unroll
+      for (int p = 0; p < kPre; ++p) q_read(qb[p], p);
+#pragma unroll
+      for (int kf = 0; kf < NF; ++kf) {
+        Frag<T> sa[CBW];
+#pragma unroll
+        for (int x = 0; x < CBW; ++x) {
+          sa[x].set2(0, sacc[x][2 * kf][0], sacc[x][2 * kf][1]);
+          sa[x].set2(2, sacc[x][2 * kf][2], sacc[x][2 * kf][3]);
+          sa[x].set2(4, sacc[x][2 * kf + 1][0], sacc[x][2 * kf + 1][1]);
+          sa[x].set2(6, sacc[x][2 * kf + 1][2], sacc[x][2 * kf + 1][3]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int idx = 4 * kf + i;
+          const Frag<T> qa = qb[idx % kPre];
+          if (idx + kPre < 4 * NF) q_read(qb[idx % kPre], idx + kPre);
+#pragma unroll
+          for (int x = 0; x < CBW; ++x) mma(num[x][i], sa[x], qa);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+
+    // The readout, this wave's P^T runs (key block J0, query blocks I0 .. I0 + C0 - 1,
+    // and J1, I1 .. I1 + C1 - 1) and its den block ID in one pass over phi(Q_c): every
+    // phi(Q) fragment is read once and is the B operand of all three.  phi(K)^T and z
+    // fragments of step kf are read at its start and first used after its readout
+    // products (one buffer: registers are at the limit).
+    auto front = [&](const T* zprev, auto j0c, auto i0c, auto c0c, auto j1c, auto i1c, auto c1c, auto idc) {
+      constexpr int J0 = decltype(j0c)::value, I0 = decltype(i0c)::value, C0 = decltype(c0c)::value;
+      constexpr int J1 = decltype(j1c)::value, I1 = decltype(i1c)::value, C1 = decltype(c1c)::value;
+      constexpr int ID = decltype(idc)::value;
+      f32x4 pa0[C0], pa1[C1 > 0 ? C1 : 1], dacc = zero4();
+#pragma unroll
+      for (int b = 0; b < C0; ++b) pa0[b] = zero4();
+#pragma unroll
+      for (int b = 0; b < C1; ++b) pa1[b] = zero4();
+#pragma unroll
+      for (int x = 0; x < CBW; ++x)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) num[x][i] = zero4();
+      constexpr int kPre = 4;
+      auto q_read = [&](Frag<T>& f, int idx) { lds8(f, q_src + 16 * (idx % 4) * SQ + 32 * (idx / 4) * SZ); };
+      Frag<T> qb[kPre], k0, k1, za;
+#pragma unroll
+      for (int p = 0; p < kPre; ++p) q_read(qb[p], p);
+#pragma unroll
+      for (int kf = 0; kf < NF; ++kf) {
+        load_tr4_rows(k0, 0, kt_src + 32 * kf * SK + 16 * J0 * SZ, SK);
+        load_tr4_rows(k0, 4, kt_src + (32 * kf + 16) * SK + 16 * J0 * SZ, SK);
+        if constexpr (C1 > 0) {
+          load_tr4_rows(k1, 0, kt_src + 32 * kf * SK + 16 * J1 * SZ, SK);
+          load_tr4_rows(k1, 4, kt_src + (32 * kf + 16) * SK + 16 * J1 * SZ, SK);
+        }
+        lds8(za, reinterpret_cast<const char*>(zprev + 32 * kf));
+        Frag<T> sa[CBW];
+#pragma unroll
+        for (int x = 0; x < CBW; ++x) {
+          sa[x].set2(0, sacc[x][2 * kf][0], sacc[x][2 * kf][1]);
+          sa[x].set2(2, sacc[x][2 * kf][2], sacc[x][2 * kf][3]);
+          sa[x].set2(4, sacc[x][2 * kf + 1][0], sacc[x][2 * kf + 1][1]);
+          sa[x].set2(6, sacc[x][2 * kf + 1][2], sacc[x][2 * kf + 1][3]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int idx = 4 * kf + i;
+          const Frag<T> qa = qb[idx % kPre];
+          if (idx + kPre < 4 * NF) q_read(qb[idx % kPre], idx + kPre);
+#pragma unroll
+          for (int x = 0; x < CBW; ++x) mma(num[x][i], sa[x], qa);
+          if (i >= I0 && i < I0 + C0) mma(pa0[i - I0], k0, qa);
+          if constexpr (C1 > 0)
+            if (i >= I1 && i < I1 + C1) mma(pa1[i - I1], k1, qa);
+          if (i == ID) mma(dacc, za, qa);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int b = 0; b < C0; ++b) p_store(pa0[b], J0, I0 + b);
+#pragma unroll
+      for (int b = 0; b < C1; ++b) p_store(pa1[b], J1, I1 + b);
+      if (g == 0) sm.deni[16 * ID + r] = dacc[0];
+    };
+    using I0c = std::integral_constant<int, 0>;
+
+    // Iteration c: between B1 and B2 the readout of chunk c from S_{c-1}, the P^T and
+    // denominator blocks, the V fragments and the S update; after B2, V^T P^T and the
+    // output rows.
     for (int c = 0; c < c_end; ++c) {
       const bool scan = c >= c_begin;
       __syncthreads();  // B1: phi(Q_c), phi(K_c), V_c and z_{c-1} are in LDS
@@ -558,12 +687,12 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
           const T* zprev = zs0 + ((c + 1) & 1) * FP;  // z_{c-1}
           // the ten P^T blocks and four den blocks spread over the matrix waves
           if constexpr (NMW == 4) {
-            if (mw == 0) p_run(I3{}, 0, 0);
-            else if (mw == 1) { p_run(I1{}, 0, 3); p_run(I1{}, 3, 3); }
-            else if (mw == 2) p_run(I3{}, 1, 1);
-            else p_run(I2{}, 2, 2);
-            den_run(zprev, (mw + 2) % 4);
+            if (mw == 0) front(zprev, I0c{}, I0c{}, I3{}, I0c{}, I0c{}, I0c{}, I2{});
+            else if (mw == 1) front(zprev, I0c{}, I3{}, I1{}, I3{}, I3{}, I1{}, I3{});
+            else if (mw == 2) front(zprev, I1{}, I1{}, I3{}, I0c{}, I0c{}, I0c{}, I0c{});
+            else front(zprev, I2{}, I2{}, I2{}, I0c{}, I0c{}, I0c{}, I1{});
           } else {
+            readout();
             if (mw == 0) { p_run(I4{}, 0, 0); p_run(I2{}, 2, 2); }
             else { p_run(I3{}, 1, 1); p_run(I1{}, 3, 3); }
             den_run(zprev, mw);
@@ -580,35 +709,6 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
                 const int t = 32 * ks + 8 * g + 4 * h + kk, cc = 16 * (CBW * mw + x) + col;
                 return &sm.vt[t * DH + swz_v<CPV>(t, cc / VE) * VE + cc % VE];
               });
-      }
-      __syncthreads();  // B2: P and the den parts are in LDS
-      if (active) {
-        if (scan) {
-          // num^T += V^T P^T over the key tokens at or before each query block
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-              if (2 * ks <= i) {
-                Frag<T> pb;
-                lds8(pb, p_src + 16 * i * SP + 32 * ks * SZ);
-#pragma unroll
-                for (int x = 0; x < CBW; ++x) mma(num[x][i], vf[x][ks], pb);
-              }
-          const auto ro = rows_of(a.out, c, t_end);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int q = 16 * i + r;
-            float den = sm.deni[q];
-#pragma unroll
-            for (int j = 0; j <= i; ++j) den += sm.denp[j][q];
-            const float rinv = __builtin_amdgcn_rcpf(den + eps);
-#pragma unroll
-            for (int x = 0; x < CBW; ++x)
-              buf_store4<T>(ro, (q * DH + 16 * (CBW * mw + x) + 4 * g) * SZ, num[x][i][0] * rinv,
-                            num[x][i][1] * rinv, num[x][i][2] * rinv, num[x][i][3] * rinv);
-          }
-        }
         // S += phi(K_c)^T V_c, S row block b = phi(K)^T rows 16 b .. 16 b + 15;
         // fragments read kPre ahead
         constexpr int kPre = 4;
@@ -624,39 +724,31 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
           for (int x = 0; x < CBW; ++x) mma(sacc[x][idx / 2], ka, vf[x][idx % 2]);
         }
       }
-      __syncthreads();  // B3: phi(K_c) is no longer read; phi(Q_{c+1}) is in LDS
-      if (active && c + 1 >= c_begin && c + 1 < c_end) {
-        // num^T = S_c^T phi(Q_{c+1})^T: accumulator tiles 2 kf, 2 kf + 1 of S are the
-        // k-fragment kf of S^T (slot (g, e) = feature 32 kf + 8 g + e); phi(Q)
-        // fragments (step kf, block i) are read in that order kPre ahead of their use
+      __syncthreads();  // B2: P and the den parts are in LDS
+      if (active && scan) {
+        // num^T += V^T P^T over the key tokens at or before each query block
 #pragma unroll
-        for (int x = 0; x < CBW; ++x)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) num[x][i] = zero4();
-        constexpr int kPre = 4;
-        auto q_read = [&](Frag<T>& f, int idx) { lds8(f, q_src + 16 * (idx % 4) * SQ + 32 * (idx / 4) * SZ); };
-        Frag<T> qb[kPre];
+          for (int ks = 0; ks < 2; ++ks)
+            if (2 * ks <= i) {
+              Frag<T> pb;
+              lds8(pb, p_src + 16 * i * SP + 32 * ks * SZ);
 #pragma unroll
-        for (int p = 0; p < kPre; ++p) q_read(qb[p], p);
+              for (int x = 0; x < CBW; ++x) mma(num[x][i], vf[x][ks], pb);
+            }
+        const auto ro = rows_of(a.out, c, t_end);
 #pragma unroll
-        for (int kf = 0; kf < NF; ++kf) {
-          Frag<T> sa[CBW];
+        for (int i = 0; i < 4; ++i) {
+          const int q = 16 * i + r;
+          float den = sm.deni[q];
 #pragma unroll
-          for (int x = 0; x < CBW; ++x) {
-            sa[x].set2(0, sacc[x][2 * kf][0], sacc[x][2 * kf][1]);
-            sa[x].set2(2, sacc[x][2 * kf][2], sacc[x][2 * kf][3]);
-            sa[x].set2(4, sacc[x][2 * kf + 1][0], sacc[x][2 * kf + 1][1]);
-            sa[x].set2(6, sacc[x][2 * kf + 1][2], sacc[x][2 * kf + 1][3]);
-          }
+          for (int j = 0; j <= i; ++j) den += sm.denp[j][q];
+          const float rinv = __builtin_amdgcn_rcpf(den + eps);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int idx = 4 * kf + i;
-            const Frag<T> qa = qb[idx % kPre];
-            if (idx + kPre < 4 * NF) q_read(qb[idx % kPre], idx + kPre);
-#pragma unroll
-            for (int x = 0; x < CBW; ++x) mma(num[x][i], sa[x], qa);
-          }
-          __builtin_amdgcn_sched_barrier(0);
+          for (int x = 0; x < CBW; ++x)
+            buf_store4<T>(ro, (q * DH + 16 * (CBW * mw + x) + 4 * g) * SZ, num[x][i][0] * rinv,
+                          num[x][i][1] * rinv, num[x][i][2] * rinv, num[x][i][3] * rinv);
         }
       }
     }

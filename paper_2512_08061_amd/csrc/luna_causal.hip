@@ -120,7 +120,6 @@ __device__ __forceinline__ int swz_v(int row, int cg) {
   return cg ^ ((2 * h) & (CPR - 1));
 }
 
-constexpr int kBufferFlags = 0x00020000;  // raw 32-bit buffer, range-checked
 typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
 
 // 8 consecutive elements at LDS byte address p (16 B for bf16, 32 B for fp32)
@@ -148,33 +147,6 @@ __device__ __forceinline__ void load_tr4_rows(Frag<__bf16>& f, int e0, const cha
 __device__ __forceinline__ void load_tr4_rows(Frag<float>& f, int e0, const char* p, int stride) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) f.v[e0 + e] = *reinterpret_cast<const float*>(p + e * stride);
-}
-
-// 8 consecutive elements at byte offset `off` of a buffer
-__device__ __forceinline__ void buf_load8(Frag<__bf16>& f, __amdgpu_buffer_rsrc_t rs, int off) {
-  f.v = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-}
-__device__ __forceinline__ void buf_load8(Frag<float>& f, __amdgpu_buffer_rsrc_t rs, int off) {
-  const float4 lo = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-  const float4 hi = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, 0));
-  f.v[0] = lo.x; f.v[1] = lo.y; f.v[2] = lo.z; f.v[3] = lo.w;
-  f.v[4] = hi.x; f.v[5] = hi.y; f.v[6] = hi.z; f.v[7] = hi.w;
-}
-// four consecutive elements to byte offset `off` of a buffer
-template <typename T>
-__device__ __forceinline__ void buf_store4(__amdgpu_buffer_rsrc_t rs, int off, float a, float b, float c, float d);
-template <>
-__device__ __forceinline__ void buf_store4<__bf16>(__amdgpu_buffer_rsrc_t rs, int off, float a, float b, float c,
-                                                   float d) {
-  typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
-  const bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
-  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), rs, off, 0, 0);
-}
-template <>
-__device__ __forceinline__ void buf_store4<float>(__amdgpu_buffer_rsrc_t rs, int off, float a, float b, float c,
-                                                  float d) {
-  typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, float4{a, b, c, d}), rs, off, 0, 0);
 }
 
 // x plus the x of lane l ^ 16 (and l ^ 32).  A permlane swap of a value with itself

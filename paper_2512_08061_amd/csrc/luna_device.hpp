@@ -613,6 +613,52 @@ __device__ __forceinline__ void mma(f32x4& c, const Frag<float>& a, const Frag<f
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.0f, 0.0f, 0.0f, 0.0f}; }
 
+// Range-checked buffers: loads past num_records bytes return 0, stores there are
+// dropped, with no per-lane tests; accesses are always issued, so the waits for them
+// count the same loads on every path.
+constexpr int kBufferFlags = 0x00020000;  // raw 32-bit buffer, range-checked
+// s_waitcnt immediate: vector memory counter 0, the others left at their maximum
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// 8 consecutive elements at byte offset `off` of a buffer
+__device__ __forceinline__ void buf_load8(Frag<__bf16>& f, __amdgpu_buffer_rsrc_t rs, int off) {
+  f.v = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+__device__ __forceinline__ void buf_load8(Frag<float>& f, __amdgpu_buffer_rsrc_t rs, int off) {
+  const float4 lo = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+  const float4 hi = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16, 0, 0));
+  f.v[0] = lo.x; f.v[1] = lo.y; f.v[2] = lo.z; f.v[3] = lo.w;
+  f.v[4] = hi.x; f.v[5] = hi.y; f.v[6] = hi.z; f.v[7] = hi.w;
+}
+
+// four consecutive elements to byte offset `off` of a buffer
+template <typename T>
+__device__ __forceinline__ void buf_store4(__amdgpu_buffer_rsrc_t rs, int off, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void buf_store4<__bf16>(__amdgpu_buffer_rsrc_t rs, int off, float a, float b, float c,
+                                                   float d) {
+  typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+  const bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), rs, off, 0, 0);
+}
+template <>
+__device__ __forceinline__ void buf_store4<float>(__amdgpu_buffer_rsrc_t rs, int off, float a, float b, float c,
+                                                  float d) {
+  typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, float4{a, b, c, d}), rs, off, 0, 0);
+}
+
+// Rows t0 .. t0 + nrows - 1 of a row-major [n][d] array of ESZ-byte elements as a
+// range-checked buffer: rows at or past n read as 0 and are not written.  The row
+// count is uniform and kept in a scalar register (a vector-held count would make
+// every access a readfirstlane loop).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, int t0, int nrows, int n, int d,
+                                                           int esz) {
+  const char* p = reinterpret_cast<const char*>(base) + (size_t)t0 * d * esz;
+  const int rows = __builtin_amdgcn_readfirstlane(max(0, min(nrows, n - t0)));
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(p), (short)0, rows * d * esz, kBufferFlags);
+}
+
 // 8 consecutive elements from memory (16 B for bf16, 32 B for fp32).
 __device__ __forceinline__ void load8(Frag<__bf16>& f, const __bf16* p) {
   f.v = *reinterpret_cast<const bf16x8*>(p);

@@ -444,29 +444,25 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 
   // ---- state phase: wave w takes 32-token steps w, w + kNcWaves, ... ----
   constexpr int VCH = 32 * DH / C::VE / kWave;  // V 16-byte chunks per lane per step
-  Frag<T> kn[2][C::KS];
+  Frag<T> kn[2][C::KS], kq[2][C::KS];  // this step's K rows, the next step's
   i32x4 vn[VCH];
-  auto fetch_k = [&](int step) {
-    const int t0 = 32 * step;
+  // rows of a 32-token step through range-checked buffers (rows past n read as 0)
+  auto fetch_k = [&](Frag<T> (&kf)[2][C::KS], int step) {
+    const auto rs = rows_rsrc(K, 32 * step, 32, n, DH, (int)sizeof(T));
 #pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      const int t = t0 + 16 * tb + r;
+    for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) {
-        if (t < n) load8(kn[tb][ks], K + (size_t)t * DH + 32 * ks + 8 * g);
-        else kn[tb][ks].zero();
-      }
-    }
+      for (int ks = 0; ks < C::KS; ++ks)
+        buf_load8(kf[tb][ks], rs, (int)(((16 * tb + r) * DH + 32 * ks + 8 * g) * sizeof(T)));
   };
   auto fetch_v = [&](int step) {
-    const int t0 = 32 * step;
+    const auto rs = rows_rsrc(V, 32 * step, 32, n, DH, (int)sizeof(T));
 #pragma unroll
     for (int q = 0; q < VCH; ++q) {
       const int c = lane + kWave * q;
       const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
-      const int t = t0 + tt;
-      if (t < n) vn[q] = *reinterpret_cast<const i32x4*>(V + (size_t)t * DH + cg * C::VE);
-      else vn[q] = i32x4{0, 0, 0, 0};
+      vn[q] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            rs, (int)((tt * DH + cg * C::VE) * sizeof(T)), 0, 0));
     }
   };
   __syncthreads();
@@ -476,10 +472,11 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
   T* vt = &sm.u.vt[wave][0][0];
 
   const int nsteps = (n + 31) / 32;
-  if (wave < nsteps) {
-    fetch_k(wave);
-    fetch_v(wave);
-  }
+  // loads are issued on every path (past the last step as empty buffers), so that the
+  // waits for them count the same loads on every path; a step's rows are fetched one
+  // whole step ahead
+  fetch_k(kn, wave);
+  fetch_v(wave);
   for (int step = wave; step < nsteps; step += kNcWaves) {
     const int t0 = 32 * step;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -489,7 +486,8 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
       const int tt = c / (DH / C::VE), cg = c % (DH / C::VE);
       *reinterpret_cast<i32x4*>(vt + tt * LDS::VR + cg * C::VE) = vn[q];
     }
-    if (step + kNcWaves < nsteps) fetch_v(step + kNcWaves);
+    fetch_v(step + kNcWaves);
+    fetch_k(kq, step + kNcWaves);
 
     float uu[8 * MB];  // [mb][tb][j]
 #pragma unroll
@@ -502,7 +500,6 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 #pragma unroll
         for (int j = 0; j < 4; ++j) uu[8 * mb + 4 * tb + j] = acc[j] + bcol[mb];
       }
-    if (step + kNcWaves < nsteps) fetch_k(step + kNcWaves);
     int sg[8 * MB];
     pwl_search(sm.tab, tsteps, uu, sg);
 #pragma unroll
@@ -561,8 +558,30 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
         }
       }
     }
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) kn[tb][ks] = kq[tb][ks];
   }
 
+  // ---- readout rows: wave w takes 16-token blocks w, w + kNcWaves, ... ----
+  const int nblk = (n + 15) / 16;
+  // NB query blocks are mapped together, so that their table lookups overlap (one wave
+  // per SIMD has no other wave to hide their latency); blocks past the end read zero
+  // rows and store nothing.  The next group's rows are fetched while one is mapped.
+  // Loads and stores share one counter and their completions are not ordered, so a
+  // wait for a load also waits for every store issued before it: the group's outputs
+  // are kept until its end and stored after an explicit wait for the next group's
+  // rows, so that no wait has to cover stores issued just before it.
+  constexpr int NB = 4;
+  Frag<T> qf[NB][C::KS];
+  auto fetch_q = [&](Frag<T> (&qf)[C::KS], int b) {
+    const auto rs = rows_rsrc(Q, 16 * b, 16, n, DH, (int)sizeof(T));
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) buf_load8(qf[ks], rs, (int)((r * DH + 32 * ks + 8 * g) * sizeof(T)));
+  };
+#pragma unroll
+  for (int i = 0; i < NB; ++i) fetch_q(qf[i], wave + kNcWaves * i);
   // ---- sum the waves' accumulator tiles in a fixed order (deterministic), lane by
   // lane: every tile is one 16-byte read-modify-write per lane ----
   __syncthreads();  // every wave is done with its V tile (red aliases it)
@@ -628,30 +647,10 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
     }
 
   // ---- readout phase: wave w takes 16-token blocks w, w + kNcWaves, ... ----
-  const int nblk = (n + 15) / 16;
-  // NB query blocks are mapped together, so that their table lookups overlap (one wave
-  // per SIMD has no other wave to hide their latency); blocks past the end read zero
-  // rows and store nothing.  The next group's rows are fetched while one is mapped.
-  constexpr int NB = 4;
-  Frag<T> qn[NB][C::KS];
-  auto fetch_q = [&](Frag<T> (&qf)[C::KS], int b) {
-    const int t = 16 * b + r;
-#pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      if (t < n) load8(qf[ks], Q + (size_t)t * DH + 32 * ks + 8 * g);
-      else qf[ks].zero();
-    }
-  };
-#pragma unroll
-  for (int i = 0; i < NB; ++i) fetch_q(qn[i], wave + kNcWaves * i);
+  // (the first group's rows were fetched before the reduction; every load issued so
+  // far is complete from here on, so the loop's waits see only its own accesses)
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   for (int b0 = wave; b0 < nblk; b0 += kNcWaves * NB) {
-    Frag<T> qf[NB][C::KS];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-#pragma unroll
-      for (int ks = 0; ks < C::KS; ++ks) qf[i][ks] = qn[i][ks];
-      fetch_q(qn[i], b0 + kNcWaves * (NB + i));
-    }
     float uu[NB * 4 * MB];  // [block][mb][j]
 #pragma unroll
     for (int i = 0; i < NB; ++i)
@@ -663,6 +662,8 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 #pragma unroll
         for (int j = 0; j < 4; ++j) uu[(i * MB + mb) * 4 + j] = acc[j] + brow[mb][j];
       }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) fetch_q(qf[i], b0 + kNcWaves * (NB + i));  // rows projected: next group
     int sg[NB * 4 * MB];
     pwl_search(sm.tab, tsteps, uu, sg);
 #pragma unroll
@@ -672,6 +673,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           if (!prow[mb][j]) sg[(i * MB + mb) * 4 + j] = zseg;
+    f32x4 num[NB][C::CB], den[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       Frag<T> pq[C::NF];
@@ -694,23 +696,29 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
             }
           }
         }
-      f32x4 num[C::CB], den = zero4();
+      den[i] = zero4();
 #pragma unroll
-      for (int cb = 0; cb < C::CB; ++cb) num[cb] = zero4();
+      for (int cb = 0; cb < C::CB; ++cb) num[i][cb] = zero4();
 #pragma unroll
       for (int k = 0; k < C::NF; ++k) {
 #pragma unroll
-        for (int cb = 0; cb < C::CB; ++cb) mma(num[cb], sf[cb][k], pq[k]);
-        mma(den, zf[k], pq[k]);
+        for (int cb = 0; cb < C::CB; ++cb) mma(num[i][cb], sf[cb][k], pq[k]);
+        mma(den[i], zf[k], pq[k]);
       }
-      const int t = 16 * (b0 + kNcWaves * i) + r;
-      if (t < n) {
-        const float rinv = 1.0f / (den[0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
-        T* o = out + (size_t)t * DH + 4 * g;
+    }
+    // the next group's rows and the previous group's stores, before this group's stores
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int cb = 0; cb < C::CB; ++cb)
-          store4(o + 16 * cb, num[cb][0] * rinv, num[cb][1] * rinv, num[cb][2] * rinv, num[cb][3] * rinv);
-      }
+    for (int i = 0; i < NB; ++i) {
+      // rows past n are dropped by the range-checked buffer
+      const auto ro = rows_rsrc(out, 16 * (b0 + kNcWaves * i), 16, n, DH, (int)sizeof(T));
+      const float rinv = 1.0f / (den[i][0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
+#pragma unroll
+      for (int cb = 0; cb < C::CB; ++cb)
+        buf_store4<T>(ro, (int)((r * DH + 16 * cb + 4 * g) * sizeof(T)), num[i][cb][0] * rinv,
+                      num[i][cb][1] * rinv, num[i][cb][2] * rinv, num[i][cb][3] * rinv);
     }
   }
 }

@@ -183,8 +183,11 @@ def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The GPU takes some tens of milliseconds under load to reach its full clock: the
+    # default warm-up (about 0.1 s of steps) covers that, so that the timed steps see
+    # the steady state.  Explicit values are used as given.
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",

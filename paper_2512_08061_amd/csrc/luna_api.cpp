@@ -65,6 +65,8 @@ struct Layout {
   size_t tables = 0, partial = 0, frags = 0, total = 0;
   int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
+  size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
+  int pieces = 0, piece_chunks = 0;
 };
 
 luna_status plan(const Problem& pb, Layout* lay) {
@@ -108,15 +110,22 @@ luna_status plan(const Problem& pb, Layout* lay) {
     if (pb.chunk != 64) return fail(LUNA_ERR_UNSUPPORTED, "chunk must be 64");
     if (!luna::causal_supported(dt, d, L, M))
       return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernel for this (dtype, d, L, M)");
-    // Too few heads to fill the device: cut every head in two.  Part 1 first
-    // rebuilds the state of part 0's tokens from keys and values, which costs
-    // about kPrefixCost of scanning them, so part 0 gets n / (2 - kPrefixCost).
+    // Too few heads to fill the device: cut every head in two at a chunk boundary x
+    // near n/2.  A state launch first sums the state of [0, x) in pieces (one
+    // workgroup per head and piece, enough pieces to fill the device); part 1 of the
+    // scan launch starts from the sum of the pieces.
     if (heads < 256 && pb.n >= 256) {
-      constexpr double kPrefixCost = 0.5;
-      int64_t x = (int64_t)((double)pb.n / (2.0 - kPrefixCost) / 64.0 + 0.5) * 64;
-      if (x >= 64 && x < pb.n) {
+      const int64_t cx = pb.n / 64 / 2;  // chunks before the split
+      if (cx >= 1) {
         lay->parts = 2;
-        lay->split = (int)x;
+        lay->split = (int)(cx * 64);
+        int64_t pieces = (256 + heads - 1) / heads;
+        if (pieces > cx) pieces = cx;
+        const int64_t pc = (cx + pieces - 1) / pieces;
+        lay->piece_chunks = (int)pc;
+        lay->pieces = (int)((cx + pc - 1) / pc);  // every piece non-empty
+        lay->state = off;
+        off = align256(off + (size_t)heads * lay->pieces * luna::causal_state_floats(dt, d, L, M) * sizeof(float));
       }
     }
   } else {
@@ -269,7 +278,18 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   a.parts = lay.parts;
   a.split = lay.split;
   a.eps = eps;
-  hipError_t e = luna::launch_causal(dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32, (int)d, p->L, p->M, a, s);
+  const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  if (lay.parts == 2) {
+    float* st = reinterpret_cast<float*>(w + lay.state);
+    a.pieces = lay.pieces;
+    a.piece_chunks = lay.piece_chunks;
+    a.state_out = st;
+    hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
+    if (e != hipSuccess) return hip_fail(e, "causal attention state launch");
+    a.state_out = nullptr;
+    a.state_in = st;
+  }
+  hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");
 }
 

@@ -69,6 +69,9 @@ struct CsCfg {
   static constexpr int SP = 64 * SZ + 16;         // P row stride
   static constexpr int VPT = 64 * DH / VE / 256;  // 16-byte V chunks per map-wave thread
   static constexpr int NSEG = nseg_cap(L, kAttnSegBytes);
+  // one state piece: the matrix waves' S slices (lane-major accumulator tiles), then z
+  static constexpr int SF = NMW * CBW * RB * kWave * 4;
+  static constexpr int STATE = (SF + FP + 63) / 64 * 64;
   // bf16: fp16 coefficient rows and keys in 4-key groups; fp32: fp32 rows and plain keys
   using Tab = typename std::conditional<SZ == 2, PwlLdsN<half2_t, L, NSEG>, PwlLds<L, NSEG>>::type;
   static_assert(NCB == 2 || NCB == 4 || NCB == 8, "d must be 32, 64 or 128");
@@ -199,8 +202,12 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   constexpr bool kF16 = sizeof(T) == 2;  // fp16 coefficient rows for bf16 data
   __shared__ CsLds<T, DH, L, MB> sm;
 
-  const int head = blockIdx.x / a.parts;
-  const int part = blockIdx.x - head * a.parts;
+  // state launch: one workgroup per (head, piece of the first `split` tokens); scan
+  // launch: one per (head, part)
+  const bool state_run = a.state_out != nullptr;
+  const int per_head = state_run ? a.pieces : a.parts;
+  const int head = blockIdx.x / per_head;
+  const int part = blockIdx.x - head * per_head;
   const int hset = a.phi.per_head ? head % a.H : 0;
   const uint8_t* gtab = a.phi.tables + (size_t)hset * kTableBytes;
   pwl_load(sm.tab, gtab);
@@ -214,10 +221,24 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   const T* W = reinterpret_cast<const T*>(a.phi.W) + (size_t)hset * M * DH;
   const float* bias = a.phi.b + (size_t)hset * M;
 
-  // chunks [0, c_begin) only build the state; chunks [c_begin, c_end) are scanned
-  const int t_begin = part == 0 ? 0 : a.split;
-  const int t_end = part == a.parts - 1 ? n : a.split;
-  const int c_begin = t_begin / 64, c_end = (t_end + 63) / 64;
+  // chunks [c_first, c_begin) only build the state; chunks [c_begin, c_end) are scanned
+  int c_first, c_begin, c_end, t_end;
+  if (state_run) {
+    c_first = part * a.piece_chunks;
+    c_end = min(a.split / 64, c_first + a.piece_chunks);
+    c_begin = c_end;
+    t_end = 0;
+  } else {
+    const int t_begin = part == 0 ? 0 : a.split;
+    t_end = part == a.parts - 1 ? n : a.split;
+    c_begin = t_begin / 64;
+    c_end = (t_end + 63) / 64;
+    c_first = (part > 0 && a.state_in != nullptr) ? c_begin : 0;
+  }
+  // part 1 of the scan launch starts from the state of the first c_first chunks: the
+  // sum of the pieces, in piece order
+  const bool seeded = !state_run && c_first > 0;
+  const float* seed = seeded ? a.state_in + (size_t)head * a.pieces * C::STATE : nullptr;
 
   // Q, K, V rows of chunk cc and the output rows of chunk cc as range-checked
   // buffers: rows at or past n (t_end for the output) read as 0 and are not written.
@@ -239,7 +260,13 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     store8(&sm.wfr[mb][ks][l][0], f);
   }
   for (int i = tid; i < 64 * SP / 4; i += C::NT) reinterpret_cast<int*>(sm.pm)[i] = 0;
-  for (int i = tid; i < 2 * FP; i += C::NT) (&sm.zs[0][0])[i] = (T)0.0f;
+  // z_{c_first - 1} in the slot that chunk c_first's denominators read; the other 0
+  for (int i = tid; i < 2 * FP; i += C::NT) {
+    float zv = 0.0f;
+    if (seeded && i / FP == ((c_first + 1) & 1))
+      for (int pc = 0; pc < a.pieces; ++pc) zv += seed[(size_t)pc * C::STATE + C::SF + i % FP];
+    (&sm.zs[0][0])[i] = (T)zv;
+  }
   for (int i = tid; i < 16 * MB; i += C::NT) sm.bias[i] = i < M ? bias[i] : 0.0f;
 
   if (wave >= NMS) {
@@ -332,6 +359,14 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     f32x4 zacc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) zacc[mb] = zero4();
+    if (seeded && rb == 0 && r < L) {  // the prefix's z enters through map wave 0
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          for (int pc = 0; pc < a.pieces; ++pc)
+            zacc[mb][jj] += seed[(size_t)pc * C::STATE + C::SF + feat<MB>(16 * mb + 4 * g, r) + jj];
+    }
     auto add_z = [&]() {
 #pragma unroll
       for (int q = 0; q < L / 2; ++q) {
@@ -369,10 +404,10 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         if (f0 + lane < FW) sm.zs[slot][f] = (T)(((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f]);
       }
     };
-    // query rows are needed from chunk c_begin on, key rows and V from chunk 0
-    load_rows(xq, a.Q, 0, 0 >= c_begin);
-    load_rows(xk, a.K, 0, true);
-    load_v(0);
+    // query rows are needed from chunk c_begin on, key rows and V from chunk c_first
+    load_rows(xq, a.Q, c_first, c_first >= c_begin && c_first < c_end);
+    load_rows(xk, a.K, c_first, c_first < c_end);
+    load_v(c_first);
     __syncthreads();  // tables, W fragments, cleared P and z
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -429,21 +464,21 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       eval_all(phk_r, uk, ok, tfloor);
       add_z();
     };
-    // chunk 0
-    if (0 >= c_begin) map_rows(std::true_type{});
+    // chunk c_first
+    if (c_first >= c_begin) map_rows(std::true_type{});
     else map_rows(std::false_type{});
-    load_rows(xq, a.Q, 1, 1 >= c_begin);
-    load_rows(xk, a.K, 1, true);
-    if (0 >= c_begin) write_q();
+    load_rows(xq, a.Q, c_first + 1, c_first + 1 >= c_begin && c_first + 1 < c_end);
+    load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
+    if (c_first >= c_begin) write_q();
     write_k();
-    write_z();  // z through chunk 0
+    write_z();  // z through chunk c_first
     store_v();
-    load_v(1);
+    load_v(c_first + 1);
 
     // Iteration c: between B1 and B2 the matrix waves read chunk c's tiles while this
     // wave maps chunk c + 1 (rows fetched one chunk ahead) into registers; after B2 it
     // writes chunk c + 1's tiles, V and z.
-    for (int c = 0; c < c_end; ++c) {
+    for (int c = c_first; c < c_end; ++c) {
       const int cn = c + 1;
       __syncthreads();  // B1: chunk c's tiles are in LDS; zp holds z through chunk c
       sum_z(c & 1);
@@ -479,10 +514,19 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
                                         : sm.phk + 4 * g * SK + i16 * SZ;
     const T* zs0 = &sm.zs[0][8 * g];
     f32x4 sacc[CBW][RB];
+    // the state piece layout: S tile (x, b) of matrix wave mw at (mw CBW + x) RB + b,
+    // lane-major 16-byte entries
+    const size_t s_off = ((size_t)mw * CBW * RB * kWave + lane) * 4;
 #pragma unroll
     for (int x = 0; x < CBW; ++x)
 #pragma unroll
-      for (int i = 0; i < RB; ++i) sacc[x][i] = zero4();
+      for (int i = 0; i < RB; ++i) {
+        sacc[x][i] = zero4();
+        if (seeded && active)
+          for (int pc = 0; pc < a.pieces; ++pc)
+            sacc[x][i] += *reinterpret_cast<const f32x4*>(seed + (size_t)pc * C::STATE + s_off +
+                                                          (size_t)(x * RB + i) * kWave * 4);
+      }
     f32x4 num[CBW][4];  // num^T of the chunk being scanned
 #pragma unroll
     for (int x = 0; x < CBW; ++x)
@@ -650,7 +694,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     // Iteration c: between B1 and B2 the readout of chunk c from S_{c-1}, the P^T and
     // denominator blocks, the V fragments and the S update; after B2, V^T P^T and the
     // output rows.
-    for (int c = 0; c < c_end; ++c) {
+    for (int c = c_first; c < c_end; ++c) {
       const bool scan = c >= c_begin;
       __syncthreads();  // B1: phi(Q_c), phi(K_c), V_c and z_{c-1} are in LDS
       Frag<T> vf[CBW][2];  // V columns 16 (CBW mw + x) + r, tokens 32 ks + 8 g + e
@@ -724,12 +768,25 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         }
       }
     }
+    if (state_run && active) {
+      float* so = a.state_out + (size_t)(head * a.pieces + part) * C::STATE + s_off;
+#pragma unroll
+      for (int x = 0; x < CBW; ++x)
+#pragma unroll
+        for (int i = 0; i < RB; ++i) *reinterpret_cast<f32x4*>(so + (size_t)(x * RB + i) * kWave * 4) = sacc[x][i];
+    }
+  }
+  if (state_run) {
+    __syncthreads();  // every map wave's part of z through the piece's last chunk is in zp
+    float* so = a.state_out + (size_t)(head * a.pieces + part) * C::STATE + C::SF;
+    for (int f = tid; f < FP; f += C::NT) so[f] = ((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f];
   }
 }
 
 template <typename T, int DH, int L, int MB>
 static hipError_t cs_run(const CausalArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((causal_kernel<T, DH, L, MB>), dim3(a.heads * a.parts), dim3(512), 0, s, a);
+  const int per_head = a.state_out != nullptr ? a.pieces : a.parts;
+  hipLaunchKernelGGL((causal_kernel<T, DH, L, MB>), dim3(a.heads * per_head), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 
@@ -754,6 +811,15 @@ bool causal_supported(Dt dt, int d, int L, int M) {
   LUNA_CS_CASES(X)
 #undef X
   return false;
+}
+
+size_t causal_state_floats(Dt dt, int d, int L, int M) {
+  const int MB = (M + 15) / 16;
+#define X(T_, D_, L_, MB_) \
+  if (dt == cs_dt_of<T_>() && d == D_ && L == L_ && MB == MB_) return CsCfg<T_, D_, L_, MB_>::STATE;
+  LUNA_CS_CASES(X)
+#undef X
+  return 0;
 }
 
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s) {

@@ -124,6 +124,13 @@ struct CausalArgs {
   int parts;     // workgroups per head (1 or 2)
   int split;     // with 2 parts: first token of part 1 (a multiple of 64)
   float eps;
+  // State of the first `split` tokens of every head, built beforehand in `pieces`
+  // pieces of `piece_chunks` chunks each, one workgroup per (head, piece): the state
+  // launch writes state_out, the scan launch's part 1 starts from the sum of the
+  // pieces in state_in (causal_state_floats() floats per piece, the kernel's own layout).
+  float* state_out;      // non-null: state launch
+  const float* state_in;  // non-null: part 1 of the scan launch starts from the pieces
+  int pieces, piece_chunks;
 };
 
 // Launchers; each returns hipSuccess or the launch error.  `ok` reports whether
@@ -142,6 +149,8 @@ bool noncausal_supported(Dt dt, int d, int L, int M, NoncausalPlan* plan);
 hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s);
 
 bool causal_supported(Dt dt, int d, int L, int M);
+// floats of one state piece (S slices of the matrix waves, then z) for a combination
+size_t causal_state_floats(Dt dt, int d, int L, int M);
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s);
 
 // LDS copy of the segment table: one row of (slope, intercept) pairs per segment.

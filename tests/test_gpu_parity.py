@@ -296,6 +296,23 @@ def test_attn_causal_small(dtype, d, M, L, n):
     assert_close(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), dtype, "out")
 
 
+@pytest.mark.parametrize("B,H,n", [(1, 3, 1000), (4, 25, 650), (8, 20, 300)])
+def test_attn_causal_state_pieces(B, H, n):
+    """With fewer than 256 heads each head is cut at x (n/2 rounded down to whole
+    chunks) and the state of [0, x) is summed in pieces, one workgroup per head and
+    piece: seven one-chunk pieces, uneven pieces (2, 2, 1 chunks), two pieces.
+    Checked against the oracle on sampled heads (the parameters are shared)."""
+    w = small_workload("bf16", B=B, H=H, n=n, d=128, M=32, L=8, causal=True)
+    say(f"causal state pieces B={B} H={H} n={n}")
+    Q, K, V, p = inputs(w, seed=51)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))
+    bs, hs = sorted({0, B - 1}), sorted({0, H // 2, H - 1})
+    pick = lambda X: X[bs][:, hs]  # noqa: E731
+    ref = oracle.attn_causal(pick(Q), pick(K), pick(V), p, eps=w.eps)
+    assert_close(pick(out), ref, "bf16", "out")
+
+
 def test_attn_causal_workload_full_size():
     w = wl.WORKLOADS["long_causal"]
     say("causal full size long_causal")

@@ -10,11 +10,13 @@ Infinity Cache) and each processes 131072 tokens (a token is one sequence
 position across all heads).  value = tokens of both problems / step time.
 
 The JSON line also carries
-  roofline      for the kernel that takes most of the step: algorithmic HBM bytes
-                per launch (read Q, K, V once, write out once) divided by its
-                average duration from HIP events on the launch stream; traffic is
-                the HBM bytes measured by rocprofv3 counters (see profiles/), or
-                null when the kernel source changed since they were taken;
+  roofline      for the call that takes most of the step: algorithmic HBM bytes per
+                call (read Q, K, V once, write out once) divided by its average
+                duration from HIP events on the launch stream (the causal call is
+                the table build, a state launch and the scan launch of one kernel);
+                traffic is the HBM bytes per call measured by rocprofv3 counters
+                (see profiles/), or null when the kernel source changed since they
+                were taken;
   cpu_baseline  the float64 oracle timed on the host cores on a bounded sample,
                 scaled to the same unit.
 Only one GPU is supported: --gpus above 1 exits with a message.
@@ -40,6 +42,9 @@ KERNEL_SOURCES = {
     "nc_fused_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
 }
 KERNEL_WORKLOAD = {"causal_kernel": "long_causal", "nc_fused_kernel": "long_noncausal"}
+# launches of the kernel per ABI call on these workloads: the causal call (128 heads)
+# runs a state launch and then the scan launch
+LAUNCHES_PER_CALL = {"causal_kernel": 2, "nc_fused_kernel": 1}
 COPY_BYTES = 1 << 30  # the --copy-calibration copy
 
 
@@ -56,14 +61,14 @@ def source_hash(kernel: str) -> str:
 
 
 def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if current."""
+    """HBM bytes per call from the committed rocprofv3 counter summary, if current."""
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     if rec.get("source_hash") != source_hash(kernel):
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("bytes_per_call")
 
 
 def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
@@ -98,21 +103,22 @@ def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
             ds = [d for d in vals if f"{len(kern)}{kern}" in names[d]]
             if ds:
                 rec = out.setdefault(kern, {})
-                rec[counter] = {"avg_counter_bytes": sum(vals[d] for d in ds) / len(ds), "dispatches": len(ds),
-                                "copy_factor": factor}
+                calls = len(ds) / LAUNCHES_PER_CALL[kern]
+                rec[counter] = {"counter_bytes_per_call": sum(vals[d] for d in ds) / calls, "dispatches": len(ds),
+                                "launches_per_call": LAUNCHES_PER_CALL[kern], "copy_factor": factor}
     for kern, rec in out.items():
         if "FETCH_SIZE" not in rec or "WRITE_SIZE" not in rec:
             continue
-        rd = rec["FETCH_SIZE"]["avg_counter_bytes"] * rec["FETCH_SIZE"]["copy_factor"]
-        wr = rec["WRITE_SIZE"]["avg_counter_bytes"] * rec["WRITE_SIZE"]["copy_factor"]
+        rd = rec["FETCH_SIZE"]["counter_bytes_per_call"] * rec["FETCH_SIZE"]["copy_factor"]
+        wr = rec["WRITE_SIZE"]["counter_bytes_per_call"] * rec["WRITE_SIZE"]["copy_factor"]
         wl_name = KERNEL_WORKLOAD[kern]
         doc = {
             "kernel": kern,
             "workload": wl_name,
             "source_hash": source_hash(kern),
-            "bytes_per_launch": int(rd + wr),
-            "read_bytes_per_launch": int(rd),
-            "write_bytes_per_launch": int(wr),
+            "bytes_per_call": int(rd + wr),
+            "read_bytes_per_call": int(rd),
+            "write_bytes_per_call": int(wr),
             "counters": rec,
             "copy_calibration": f"{COPY_BYTES} B device-to-device copy in the same process",
             "command": command,
@@ -121,7 +127,7 @@ def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
         with open(path, "w") as fh:
             json.dump(doc, fh, indent=1)
             fh.write("\n")
-        log(f"wrote {path}: read {rd / 2**20:.1f} MiB, write {wr / 2**20:.1f} MiB per launch")
+        log(f"wrote {path}: read {rd / 2**20:.1f} MiB, write {wr / 2**20:.1f} MiB per call")
     return 0
 
 
@@ -298,7 +304,8 @@ def main() -> int:
         "traffic": measured_traffic(kname, dom) if kname in KERNEL_SOURCES else None,
         "kernel": kname,
         "workload": dom,
-        "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel)",
+        "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel; the "
+                  "causal call is a state launch and a scan launch of causal_kernel)",
     }
 
     out = {

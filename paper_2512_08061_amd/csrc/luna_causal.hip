@@ -510,8 +510,14 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         __syncthreads();  // B1: chunk c's tiles are in LDS; zp holds z through chunk c
         sum_z(c & 1);
         const bool kn = cn < c_end, qn = kn && cn >= c_begin;
-        if (qn) map_rows(std::true_type{});
-        else if (kn) map_rows(std::false_type{});
+        // phi(Q) before B2; the key rows are only projected and searched here and
+        // evaluated after B2, where the matrix waves' work is shorter
+        if (qn) {
+          project_search(std::true_type{});
+          eval_all(phq_r, uq, oq, tfloor);
+        } else if (kn) {
+          project_search(std::false_type{});
+        }
         // the loads are issued on every path (past the end as empty buffers, which read
         // nothing), so that the waits for them count the same loads on every path
         load_rows(xq, a.Q, cn + 1, kn && cn + 1 >= c_begin);
@@ -519,6 +525,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         __syncthreads();  // B2: chunk c's phi tiles and V are no longer read
         if (kn) {
           if (qn) write_q();
+          eval_all(phk_r, uk, ok, tfloor);
+          add_z();
           write_k();
           write_z();  // z through chunk c + 1
           store_v();

@@ -3,17 +3,17 @@
  *
  * LUNA ("Learning Kernels for Linear Attention") replaces the softmax kernel by a
  * learned positive-definite kernel k(x, y) = phi(x) . phi(y) and evaluates attention
- * in linear time through the kernelised form, eq. (kernel-attn):
+ * in linear time through the kernelised form, eq. (9) of Section 3.1:
  *
  *     out = phi(Q) (phi(K)^T V) / phi(Q) (phi(K)^T 1)          (row by row)
  *
- * with the feature map of eq. (phi-def), envelope h = 1 (Table 5, "no gate"):
+ * with the feature map of eq. (11) of Section 3.2, envelope h = 1 (Table 5, "no gate"):
  *
  *     phi(x) = (1/sqrt(M)) [ psi_l(w_i . x + b_i) ]_{i = 1..M, l = 1..L}  in R^{M*L}
  *
  * where every channel function psi_l is a scalar MLP 1 -> hidden -> 1 with ReLU
- * activation and (by default) a ReLU on its output (the paper's listing of the
- * feature map).  The statistics S = phi(K)^T V and z = phi(K)^T 1 are the key-side
+ * activation and (by default) a ReLU on its output (Listing 1, the
+ * feature-map code).  The statistics S = phi(K)^T V and z = phi(K)^T 1 are the key-side
  * sufficient statistics of the runtime section (section 4).
  *
  * Conventions shared by every entry point:
@@ -59,14 +59,15 @@ typedef enum luna_dtype { LUNA_F32 = 0, LUNA_BF16 = 1 } luna_dtype;
 enum { LUNA_OP_FEATUREMAP = 0, LUNA_OP_ATTN = 1, LUNA_OP_ATTN_CAUSAL = 2 };
 
 /*
- * Feature-map parameters, eq. (phi-def) and the paper's listing of the feature map.
+ * Feature-map parameters, eq. (11) of Section 3.2 and Listing 1 (the feature-map
+ * code in the Implementation Details appendix).
  *   M       number of projections w_i (rows of W), 1 <= M <= 64
  *   L       channels per projection (outputs of the psi_l), 1 <= L <= 16; D = M*L <= 256
  *   hidden  width of each channel MLP, 1 <= hidden <= 64
- *   shared_channels 0: L separate MLPs 1 -> hidden -> 1 (the listing's default);
+ *   shared_channels 0: L separate MLPs 1 -> hidden -> 1 (Listing 1's default);
  *                   1: one MLP 1 -> hidden -> L whose first layer all channels share
- *   nonneg  1: ReLU on every MLP output, so phi >= 0 (the listing's default); 0: none
- *   per_head 0: one parameter set shared by all heads (the listing's default);
+ *   nonneg  1: ReLU on every MLP output, so phi >= 0 (Listing 1's default); 0: none
+ *   per_head 0: one parameter set shared by all heads (Listing 1's default);
  *            1: H sets, stored head-major (leading dimension H on every array)
  * Arrays (device memory; P = per_head ? H : 1; C1 = shared_channels ? 1 : L):
  *   W     [P][M][d]        element type = the call's dtype (bf16 or fp32)
@@ -105,7 +106,7 @@ size_t luna_workspace_bytes(int32_t op, luna_dtype dtype, int64_t B, int64_t H, 
                             int64_t d, const luna_phi_params* p, int32_t chunk);
 
 /*
- * Feature map phi of eq. (phi-def) applied to every row of X [B, H, n, d].
+ * Feature map phi of eq. (11) of Section 3.2 applied to every row of X [B, H, n, d].
  * phi_out [B, H, n, M*L] receives feature i*L + l (channel index fastest) of each
  * row, in out_dtype.  X and W are in x_dtype.  d must be 32, 64 or 128.
  */
@@ -114,7 +115,7 @@ luna_status luna_featuremap(const void* X, luna_dtype x_dtype, int64_t B, int64_
                             void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Non-causal LUNA attention, eq. (kernel-attn):
+ * Non-causal LUNA attention, eq. (9) of Section 3.1:
  *   S = phi(K)^T V, z = phi(K)^T 1 per (b, h);  out = phi(Q) S / (phi(Q) z + eps).
  * Q, K, V, out: [B, H, n, d] in dtype (value width d_v = d).  d in {32, 64, 128}.
  */
@@ -123,7 +124,7 @@ luna_status luna_attn_fwd(const void* Q, const void* K, const void* V, luna_dtyp
                           float eps, void* out, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Causal (streaming) LUNA attention: the prefix form of eq. (kernel-attn),
+ * Causal (streaming) LUNA attention: the prefix form of eq. (9) of Section 3.1,
  *   out_t = phi(q_t)^T S_t / (phi(q_t)^T z_t + eps),
  *   S_t = sum_{s <= t} phi(k_s) v_s^T,  z_t = sum_{s <= t} phi(k_s)   (diagonal included),
  * evaluated as a chunked scan: per chunk of `chunk` tokens a masked intra-chunk block

@@ -7,24 +7,24 @@ checks it against the paper by eye, so it is slow and direct on purpose.
 
 What it computes (paper: "Learning Kernels for Linear Attention", section 3):
 
-* ``project``      u_i = w_i . x + b_i, the scalar projections of eq. (phi-def)
+* ``project``      u_i = w_i . x + b_i, the scalar projections of eq. (11) of Section 3.2
                    with the per-projection bias that the Fig. 3 caption and the
-                   listing's task-specific projection module add.
+                   Listing 1's task-specific projection module add.
 * ``psi``          the channel functions psi_l, each a scalar MLP
                    1 -> hidden -> 1 (ReLU activation, optional ReLU on the
-                   output), evaluated literally, as in the listing's scalar MLP.
-* ``featuremap``   phi(x) = (1/sqrt(M)) [psi_l(u_i)]_{i,l} of eq. (phi-def)
+                   output), evaluated literally, as in Listing 1's scalar MLP.
+* ``featuremap``   phi(x) = (1/sqrt(M)) [psi_l(u_i)]_{i,l} of eq. (11) of Section 3.2
                    with the envelope h = 1 (the "no gate" default of Table 5);
-                   feature index i*L + l (channel index fastest), the listing's
+                   feature index i*L + l (channel index fastest), Listing 1's
                    view(B,H,N,M,L) -> reshape(..., M*L).
-* ``attn_noncausal``  eq. (kernel-attn): phi(Q) (phi(K)^T V) / phi(Q) (phi(K)^T 1),
+* ``attn_noncausal``  eq. (9) of Section 3.1: phi(Q) (phi(K)^T V) / phi(Q) (phi(K)^T 1),
                    denominator per row, with the sufficient statistics
                    S = phi(K)^T V and z = phi(K)^T 1 of the runtime section.
 * ``attn_causal``  the streaming (prefix) form: S_t and z_t summed over s <= t,
                    evaluated one token at a time.
 * ``attn_quadratic`` / ``attn_quadratic_rows``  the kernel form
                    out_t = sum_s k(q_t, k_s) v_s / sum_s k(q_t, k_s) with the
-                   kernel of eq. (kernel), k(x, y) = (1/M) sum_i <psi(u_i(x)), psi(u_i(y))>
+                   kernel of eq. (10) of Section 3.2, k(x, y) = (1/M) sum_i <psi(u_i(x)), psi(u_i(y))>
                    (optionally restricted to s <= t).
 * ``attn_causal_chunked``  the chunked prefix scan (intra-chunk masked block
                    plus inter-chunk state carry), an exact regrouping of the
@@ -63,7 +63,7 @@ def _f64(x):
 
 
 # ---------------------------------------------------------------------------
-# feature map, eq. (phi-def)
+# feature map, eq. (11) of Section 3.2
 # ---------------------------------------------------------------------------
 
 def project(X, W, b):
@@ -77,7 +77,7 @@ def psi(u, fc1_w, fc1_b, fc2_w, fc2_b, nonneg=True):
 
     Channel l: hidden_k = relu(a_k u + c_k) with (a, c) the first layer of
     channel l (or the shared first layer), then y_l = g_l + sum_k f_lk hidden_k,
-    then relu(y_l) when ``nonneg`` (the listing's scalar MLP forward).
+    then relu(y_l) when ``nonneg`` (Listing 1's scalar MLP forward).
     """
     u = _f64(u)
     a_all, c_all = _f64(fc1_w), _f64(fc1_b)
@@ -124,7 +124,7 @@ def featuremap(X, p):
 
 
 # ---------------------------------------------------------------------------
-# linear attention, eq. (kernel-attn) and the runtime section's statistics
+# linear attention, eq. (9) of Section 3.1 and the runtime section's statistics
 # ---------------------------------------------------------------------------
 
 def sufficient_statistics(phiK, V):
@@ -184,7 +184,7 @@ def attn_causal_chunked(Q, K, V, p, chunk, eps=1e-6):
 
 
 # ---------------------------------------------------------------------------
-# kernel (quadratic) form, eq. (kernel) with the kernel-attention normaliser
+# kernel (quadratic) form, eq. (10) of Section 3.2 with the kernel-attention normaliser
 # ---------------------------------------------------------------------------
 
 def kernel_matrix(Xq, Xk, p):

@@ -9,34 +9,33 @@
 //
 // which regroups the prefix sums exactly.
 //
-// Work split.  One workgroup owns one (head, part of the sequence).  With few heads
-// a head's tokens are cut in two at a chunk boundary x: part 0 scans [0, x) from a
-// zero state; part 1 first accumulates the state of [0, x) (keys and values only,
-// no readout) and then scans [x, n).  The cut is placed so that both parts take
-// about the same time; nothing is shared between workgroups.
+// Work split.  One workgroup owns one (head, part of the sequence).  With fewer heads
+// than compute units each head is cut at a chunk boundary x near n/2 and a call makes
+// two launches: the state launch (a separate instantiation, ST) sums the state of
+// [0, x) in pieces, one workgroup per (head, piece), and writes them in fp32; the scan
+// launch then runs part 0 over [0, x) from a zero state and part 1 over [x, n) from
+// the sum of the pieces.  No workgroup waits for another.
 //
-// Roles.  Matrix waves and map waves, as many of each kind on every SIMD, so that
+// Roles.  Four matrix waves and four map waves, one of each on every SIMD, so that
 // each SIMD pairs matrix-core work with vector and table-lookup work.
-//  - Map wave (b, m) computes phi for rows 16 b .. 16 b + 15 of the next chunk's
-//    queries and keys, projections 16 m .. 16 m + 15 (the projection on the matrix
-//    cores, the piecewise-linear channel functions in registers), and stages a share
-//    of V; phi(Q) is stored token-major and phi(K) feature-major in LDS.
-//  - Matrix wave w owns value columns 16 w .. 16 w + 15 and keeps that slice of S
-//    (all features) in fp32 accumulators.  It forms its share of the P^T blocks and
-//    of phi(Q_c) z_{c-1}, then num^T += V^T P^T, the division and the store, then
-//    S += phi(K_c)^T V_c, then the next chunk's num^T = S_c^T phi(Q_{c+1})^T with S
-//    taken straight from the accumulators.
-// Per chunk c, three barriers:
-//   B1: phi(Q_c), phi(K_c), V_c, z_{c-1} in LDS; num holds phi(Q_c) S_{c-1}.
-//       matrix: P^T blocks, phi(Q_c) z_{c-1}, V_c fragments.
-//       map: phi(Q_{c+1}) to registers.
-//   B2: P and den parts in LDS; phi(Q_c) and V_c no longer read.
-//       matrix: P V, output, state update.
-//       map: phi(Q_{c+1}) and V_{c+1} to LDS, z_c published, phi(K_{c+1}) to registers.
-//   B3: phi(K_c) no longer read; S_c complete; phi(Q_{c+1}) in LDS.
-//       matrix: readout S_c^T phi(Q_{c+1})^T.   map: phi(K_{c+1}) to LDS, z_c summed.
+//  - Map wave b maps rows 16 b .. 16 b + 15 of the next chunk's queries and keys for
+//    all projections (the projection on the matrix cores with W fragments and biases
+//    in registers, then the piecewise-linear channel functions from the LDS table),
+//    stages a share of V, and accumulates z with one-hot matrix-core columns.  phi(Q)
+//    is stored token-major and phi(K) feature-major in LDS.
+//  - Matrix wave w owns value columns 32 w .. 32 w + 31 and keeps that slice of S (all
+//    features) in fp32 accumulators.
+// Per chunk c, two barriers:
+//   B1: phi(Q_c), phi(K_c), V_c and z_{c-1} are in LDS.
+//       matrix: one pass over phi(Q_c) forms the readout S_{c-1}^T phi(Q_c)^T (S taken
+//       straight from the accumulators), this wave's P^T blocks and one block of
+//       phi(Q_c) z_{c-1}; then the V_c fragments and S += phi(K_c)^T V_c.
+//       map: chunk c + 1's projections and table searches; phi(Q_{c+1}) evaluated.
+//   B2: P and the den parts are in LDS; chunk c's tiles are no longer read.
+//       matrix: num^T += V^T P^T, the division and the store.
+//       map: phi(Q_{c+1}) to LDS, phi(K_{c+1}) evaluated and stored, z and V_{c+1}.
 //
-// The loop is bound by vector-instruction issue, so its LDS tiles are laid out for
+// The loop is bound by LDS instructions and their latency, so its tiles are laid out for
 // addressing without arithmetic: rows are padded by 16 bytes instead of swizzled
 // (16 consecutive rows then start on 16 distinct 16-byte bank slots), so that every
 // operand a lane reads or writes is one base register plus a constant the LDS

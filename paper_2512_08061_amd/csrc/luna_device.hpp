@@ -141,7 +141,7 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
   }
 }
 
-// relu that propagates NaN like the listing's ReLU (fmaxf would drop it); one
+// relu that propagates NaN like Listing 1's ReLU (fmaxf would drop it); one
 // v_maximum3_f32 on gfx950.
 __device__ __forceinline__ float relu_floor(float v, float floor) {
   return __builtin_elementwise_maximum(v, floor);

@@ -1,4 +1,4 @@
-// luna_featuremap.hip -- phi(x) of eq. (phi-def) for every row of X.
+// luna_featuremap.hip -- phi(x) of eq. (11) of Section 3.2 for every row of X.
 //
 // One wave handles 16 rows of one head.  The projections are computed transposed,
 // u^T = W X^T, on the matrix cores: A = W (row = projection, k = d), B = X^T

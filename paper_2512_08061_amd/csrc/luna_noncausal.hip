@@ -1,6 +1,18 @@
-// luna_noncausal.hip -- non-causal LUNA attention, eq. (kernel-attn).
+// luna_noncausal.hip -- non-causal LUNA attention, eq. (9) of Section 3.1.
 //
-// Three passes after the table build:
+// Two schedules, chosen per call by the host:
+//
+//  fused    (at least 192 heads and the per-head accumulators fit in registers)
+//           one launch, one workgroup of four waves per head, one wave per SIMD.
+//           Each wave sums its share of S and z over the head's keys in registers,
+//           the four shares are added in LDS in a fixed order and turned into
+//           readout fragments, and the same workgroup then streams the head's
+//           queries in groups of four 16-token blocks.  S never reaches HBM; the
+//           launch is bound by issue of the feature-map arithmetic, not by HBM.
+//  split    (fewer heads) the three passes below, so that a head's keys and
+//           queries are spread over many workgroups.
+//
+// The split schedule's passes, after the table build:
 //
 //  state    one workgroup per (head, token range).  Each wave takes 32-token steps:
 //           u = K W^T on the matrix cores (A = K rows, B = W^T), so a lane holds

@@ -141,6 +141,12 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
   }
 }
 
+// Segment row `seg` of a table (a 24-bit multiply: the 32-bit one is quarter rate).
+template <typename Tab>
+__device__ __forceinline__ const char* seg_ptr(const Tab& t, int seg) {
+  return reinterpret_cast<const char*>(&t.seg[0][0]) + __umul24((unsigned)seg, (unsigned)sizeof(t.seg[0]));
+}
+
 // relu that propagates NaN like Listing 1's ReLU (fmaxf would drop it); one
 // v_maximum3_f32 on gfx950.
 __device__ __forceinline__ float relu_floor(float v, float floor) {
@@ -263,7 +269,7 @@ template <int L, int NSEG>
 __device__ __forceinline__ void pwl_channels(const PwlLds<L, NSEG>& t, int seg, float floor, float u,
                                              float (&y)[L]) {
   if constexpr (L % 2 == 0) {
-    const float4* st = reinterpret_cast<const float4*>(&t.seg[seg][0]);
+    const float4* st = reinterpret_cast<const float4*>(seg_ptr(t, seg));
 #pragma unroll
     for (int q = 0; q < L / 2; ++q) {
       const float4 v = st[q];
@@ -273,7 +279,7 @@ __device__ __forceinline__ void pwl_channels(const PwlLds<L, NSEG>& t, int seg, 
   } else {
 #pragma unroll
     for (int l = 0; l < L; ++l) {
-      const float2 v = t.seg[seg][l];
+      const float2 v = reinterpret_cast<const float2*>(seg_ptr(t, seg))[l];
       y[l] = relu_floor(fmaf(v.x, u, v.y), floor);
     }
   }
@@ -284,7 +290,7 @@ template <int L, int NSEG>
 __device__ __forceinline__ void pwl_pair(const PwlLds<L, NSEG>& t, int seg, int q, float floor, float u,
                                          float& y0, float& y1) {
   static_assert(L % 2 == 0, "channel pairs need an even L");
-  const float4 v = reinterpret_cast<const float4*>(&t.seg[seg][0])[q];
+  const float4 v = reinterpret_cast<const float4*>(seg_ptr(t, seg))[q];
   y0 = relu_floor(fmaf(v.x, u, v.y), floor);
   y1 = relu_floor(fmaf(v.z, u, v.w), floor);
 }
@@ -295,7 +301,7 @@ __device__ __forceinline__ void pwl_channels(const PwlLds16<L, NSEG>& t, int seg
                                              float (&y)[L]) {
   if constexpr (L % 4 == 0) {
     typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
-    const half8_t* st = reinterpret_cast<const half8_t*>(&t.seg[seg][0]);
+    const half8_t* st = reinterpret_cast<const half8_t*>(seg_ptr(t, seg));
 #pragma unroll
     for (int q = 0; q < L / 4; ++q) {
       const half8_t v = st[q];
@@ -306,7 +312,7 @@ __device__ __forceinline__ void pwl_channels(const PwlLds16<L, NSEG>& t, int seg
   } else {
 #pragma unroll
     for (int l = 0; l < L; ++l) {
-      const half2_t v = t.seg[seg][l];
+      const half2_t v = reinterpret_cast<const half2_t*>(seg_ptr(t, seg))[l];
       y[l] = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
     }
   }
@@ -316,7 +322,7 @@ __device__ __forceinline__ void pwl_pair(const PwlLds16<L, NSEG>& t, int seg, in
                                          float& y0, float& y1) {
   static_assert(L % 2 == 0, "channel pairs need an even L");
   typedef __attribute__((ext_vector_type(4))) _Float16 half4_t;
-  const half4_t v = reinterpret_cast<const half4_t*>(&t.seg[seg][0])[q];
+  const half4_t v = reinterpret_cast<const half4_t*>(seg_ptr(t, seg))[q];
   y0 = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
   y1 = relu_floor(__builtin_fmaf((float)v[2], u, (float)v[3]), floor);
 }

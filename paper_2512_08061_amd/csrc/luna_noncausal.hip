@@ -726,7 +726,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
     for (int i = 0; i < NB; ++i) {
       // rows past n are dropped by the range-checked buffer
       const auto ro = rows_rsrc(out, 16 * (b0 + kNcWaves * i), 16, n, DH, (int)sizeof(T));
-      const float rinv = 1.0f / (den[i][0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
+      const float rinv = __builtin_amdgcn_rcpf(den[i][0] + ldexpf(a.eps, 2 * sm.tab.scale_exp));
 #pragma unroll
       for (int cb = 0; cb < C::CB; ++cb)
         buf_store4<T>(ro, (int)((r * DH + 16 * cb + 4 * g) * sizeof(T)), num[i][cb][0] * rinv,

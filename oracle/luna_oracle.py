@@ -8,7 +8,7 @@ checks it against the paper by eye, so it is slow and direct on purpose.
 What it computes (paper: "Learning Kernels for Linear Attention", section 3):
 
 * ``project``      u_i = w_i . x + b_i, the scalar projections of eq. (11) of Section 3.2
-                   with the per-projection bias that the Fig. 3 caption and the
+                   with the per-projection bias that the Fig. 3 caption and
                    Listing 1's task-specific projection module add.
 * ``psi``          the channel functions psi_l, each a scalar MLP
                    1 -> hidden -> 1 (ReLU activation, optional ReLU on the
@@ -22,6 +22,9 @@ What it computes (paper: "Learning Kernels for Linear Attention", section 3):
                    S = phi(K)^T V and z = phi(K)^T 1 of the runtime section.
 * ``attn_causal``  the streaming (prefix) form: S_t and z_t summed over s <= t,
                    evaluated one token at a time.
+* ``causal_state`` / ``attn_causal_step``  the same streaming form split at any
+                   token: the prefix state (S, z) of the first tokens, and the
+                   recurrence continued from a given state over new tokens.
 * ``attn_quadratic`` / ``attn_quadratic_rows``  the kernel form
                    out_t = sum_s k(q_t, k_s) v_s / sum_s k(q_t, k_s) with the
                    kernel of eq. (10) of Section 3.2, k(x, y) = (1/M) sum_i <psi(u_i(x)), psi(u_i(y))>
@@ -159,6 +162,29 @@ def attn_causal(Q, K, V, p, eps=1e-6):
         den = (q * z).sum(axis=-1)
         out[..., t, :] = num / (den + eps)[..., None]
     return out
+
+
+def causal_state(K, V, p):
+    """The prefix state of the streaming form after the tokens of K, V: the
+    key-side statistics S = phi(K)^T V and z = phi(K)^T 1 of the runtime section."""
+    return sufficient_statistics(featuremap(K, p), V)
+
+
+def attn_causal_step(Q, K, V, p, S, z, eps=1e-6):
+    """The streaming form continued from a prefix state (S, z): for each new token t in
+    order, S += phi(k_t) v_t^T and z += phi(k_t), then out_t = phi(q_t)^T S /
+    (phi(q_t)^T z + eps).  Returns (out, S, z) after the new tokens; S = z = 0 gives
+    ``attn_causal``."""
+    phiQ, phiK, V = featuremap(Q, p), featuremap(K, p), _f64(V)
+    S, z = _f64(S).copy(), _f64(z).copy()
+    lead, m, dv = phiQ.shape[:-2], phiQ.shape[-2], V.shape[-1]
+    out = np.empty(lead + (m, dv))
+    for t in range(m):
+        S += phiK[..., t, :, None] * V[..., t, None, :]
+        z += phiK[..., t, :]
+        q = phiQ[..., t, :]
+        out[..., t, :] = (q[..., None, :] @ S)[..., 0, :] / ((q * z).sum(axis=-1) + eps)[..., None]
+    return out, S, z
 
 
 def attn_causal_chunked(Q, K, V, p, chunk, eps=1e-6):

@@ -131,6 +131,37 @@ def pin_causal_equals_masked(o):
     assert _rel(c, a[1, 0, rows]) < 1e-10
 
 
+def pin_step_continues_the_prefix(o):
+    """The streaming form split at any token: from the state of the first n0 tokens,
+    steps over the rest give the masked kernel form's rows n0.. and, at the end, the
+    statistics of the whole sequence; from a zero state, the whole masked form."""
+    rng = np.random.default_rng(31)
+    p = _params(rng, 3, 4, 6, 5)
+    n = 23
+    Q, K, V = _qkv(rng, (2, 2, n, 6), dv=5)
+    full = o.attn_quadratic(Q, K, V, p, eps=1e-6, causal=True)
+    D = 3 * 4
+    out, S, z = o.attn_causal_step(Q, K, V, p, np.zeros((2, 2, D, 5)), np.zeros((2, 2, D)), eps=1e-6)
+    assert _rel(out, full) < 1e-10
+    for n0 in (0, 1, 9, 22):
+        S0, z0 = o.causal_state(K[..., :n0, :], V[..., :n0, :], p)
+        parts, St, zt = [], S0, z0
+        for a, b in ((n0, min(n, n0 + 4)), (min(n, n0 + 4), n)):  # two steps
+            y, St, zt = o.attn_causal_step(Q[..., a:b, :], K[..., a:b, :], V[..., a:b, :], p, St, zt, eps=1e-6)
+            parts.append(y)
+        assert _rel(np.concatenate(parts, axis=-2), full[..., n0:, :]) < 1e-10
+        # the state after the last token: phi(K)^T V and phi(K)^T 1 by brute force over the tokens
+        phiK = o.featuremap(K, p)
+        Sb = sum(np.einsum("...f,...v->...fv", phiK[..., t, :], V[..., t, :]) for t in range(n))
+        zb = sum(phiK[..., t, :] for t in range(n))
+        assert _rel(St, Sb) < 1e-12 and _rel(zt, zb) < 1e-12
+    # the step does not modify the state it is given
+    S0, z0 = o.causal_state(K[..., :5, :], V[..., :5, :], p)
+    S1, z1 = S0.copy(), z0.copy()
+    o.attn_causal_step(Q[..., 5:9, :], K[..., 5:9, :], V[..., 5:9, :], p, S0, z0)
+    assert np.array_equal(S0, S1) and np.array_equal(z0, z1)
+
+
 def pin_chunked_equals_recurrence(o):
     """Chunk sizes 1, 3, 16 and n (n not a multiple of the chunk) give the recurrence."""
     rng = np.random.default_rng(3)

@@ -93,6 +93,24 @@ def _causal_mut(kind):
     return attn_causal
 
 
+def _step_mut(kind):
+    def attn_causal_step(Q, K, V, p, S, z, eps=1e-6):
+        phiQ, phiK, V = O.featuremap(Q, p), O.featuremap(K, p), np.asarray(V, float)
+        S, z = np.array(S, float), np.array(z, float)
+        if kind == "drop_prefix":
+            S, z = np.zeros_like(S), np.zeros_like(z)
+        m = phiQ.shape[-2]
+        out = np.empty(phiQ.shape[:-1] + (V.shape[-1],))
+        for t in range(m):
+            S += phiK[..., t, :, None] * V[..., t, None, :]
+            if kind != "stale_z":
+                z += phiK[..., t, :]
+            q = phiQ[..., t, :]
+            out[..., t, :] = (q[..., None, :] @ S)[..., 0, :] / ((q * z).sum(-1) + eps)[..., None]
+        return out, S, z
+    return attn_causal_step
+
+
 def _chunked_mut(kind):
     def attn_causal_chunked(Q, K, V, p, chunk, eps=1e-6):
         phiQ, phiK, V = O.featuremap(Q, p), O.featuremap(K, p), np.asarray(V, float)
@@ -161,6 +179,8 @@ MUTATIONS = {
     "noncausal_no_eps": ("attn_noncausal", _noncausal_mut("no_eps")),
     "causal_exclusive_prefix": ("attn_causal", _causal_mut("exclusive")),
     "chunked_strict_tril": ("attn_causal_chunked", _chunked_mut("strict_tril")),
+    "step_drops_prefix": ("attn_causal_step", _step_mut("drop_prefix")),
+    "step_stale_z": ("attn_causal_step", _step_mut("stale_z")),
     "chunked_no_carry_den": ("attn_causal_chunked", _chunked_mut("no_carry_den")),
     "kernel_no_average": ("kernel_matrix", _kernel_mut("no_average")),
     "kernel_offset": ("kernel_matrix", _kernel_mut("offset")),

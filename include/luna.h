@@ -56,7 +56,13 @@ typedef enum luna_status {
 typedef enum luna_dtype { LUNA_F32 = 0, LUNA_BF16 = 1 } luna_dtype;
 
 /* Operation codes for luna_workspace_bytes(). */
-enum { LUNA_OP_FEATUREMAP = 0, LUNA_OP_ATTN = 1, LUNA_OP_ATTN_CAUSAL = 2 };
+enum {
+  LUNA_OP_FEATUREMAP = 0,
+  LUNA_OP_ATTN = 1,
+  LUNA_OP_ATTN_CAUSAL = 2,
+  LUNA_OP_STATE = 3,       /* luna_attn_state */
+  LUNA_OP_CAUSAL_STEP = 4  /* luna_attn_causal_step (n = m, the new tokens) */
+};
 
 /*
  * Feature-map parameters, eq. (11) of Section 3.2 and Listing 1 (the feature-map
@@ -134,6 +140,36 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
                                  int64_t B, int64_t H, int64_t n, int64_t d,
                                  const luna_phi_params* p, int32_t chunk, float eps, void* out,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Causal state of a token sequence: the key-side statistics of the runtime section
+ * (section 4), which are the prefix state of the streaming form of eq. (9) of
+ * Section 3.1 after the sequence's last token,
+ *   S = phi(K)^T V   [B, H, M*L, d]   and   z = phi(K)^T 1   [B, H, M*L],
+ * fp32 (caller-owned device memory), feature index i*L + l as in luna_featuremap.
+ * K, V: [B, H, n, d] in dtype.  accumulate 0: S and z are overwritten; 1: the sums
+ * are added to what S and z hold, so that a sequence can be consumed in pieces.
+ * The same (dtype, d, L, M) combinations as luna_attn_fwd are built.
+ */
+luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int64_t B, int64_t H, int64_t n,
+                            int64_t d, const luna_phi_params* p, int32_t accumulate, float* S, float* z,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One streaming (recurrent) step of causal attention, the prefix form of eq. (9) of
+ * Section 3.1 continued from the state (S, z) of the tokens before it (from
+ * luna_attn_state, an earlier step, or zeros for an empty prefix), over m new tokens
+ * per (b, h), in order:
+ *   S += phi(k_t) v_t^T;  z += phi(k_t);  out_t = phi(q_t)^T S / (phi(q_t)^T z + eps).
+ * S [B, H, M*L, d] and z [B, H, M*L] (fp32, feature i*L + l) are read and updated in
+ * place; they must not alias Q, K, V, out or the workspace.  Q, K, V, out:
+ * [B, H, m, d] in dtype.  The state is carried in fp32 throughout.  Stepping a
+ * sequence from zeros gives what luna_attn_fwd_causal computes, up to rounding.
+ * The same (d, L, M) combinations as luna_featuremap are built.
+ */
+luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B,
+                                  int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps, float* S,
+                                  float* z, void* out, void* ws, size_t ws_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* luna_status_string(luna_status s);

@@ -55,7 +55,9 @@ luna_status check_common(const Problem& pb) {
   const int C1 = p->shared_channels ? 1 : p->L;
   const int units = C1 * p->hidden;
   if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
-  const int seg_cap = luna::nseg_cap(p->L, pb.op == LUNA_OP_FEATUREMAP ? luna::kFmSegBytes : luna::kAttnSegBytes);
+  // the feature-map kernel (also the first stage of a streaming step) has the larger LDS table
+  const bool fm_table = pb.op == LUNA_OP_FEATUREMAP || pb.op == LUNA_OP_CAUSAL_STEP;
+  const int seg_cap = luna::nseg_cap(p->L, fm_table ? luna::kFmSegBytes : luna::kAttnSegBytes);
   if (units + 2 > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "too many breakpoints for the LDS segment table");
   if ((units + 1) * p->L > luna::kSegCap) return fail(LUNA_ERR_UNSUPPORTED, "too many segments for the table");
   return LUNA_OK;
@@ -63,11 +65,26 @@ luna_status check_common(const Problem& pb) {
 
 struct Layout {
   size_t tables = 0, partial = 0, frags = 0, total = 0;
+  size_t phiq = 0, phik = 0;  // streaming step: features of the new queries and keys (fp32)
   int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
   size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
   int pieces = 0, piece_chunks = 0;
 };
+
+// Token ranges of the non-causal state pass: enough state workgroups to fill the
+// device, at least 256 tokens each, a multiple of 128 tokens per range.
+void plan_splits(const Problem& pb, int64_t heads, Layout* lay) {
+  const int64_t want = (512 + heads - 1) / heads;
+  const int64_t maxs = (pb.n + 255) / 256;
+  int64_t splits = want < maxs ? want : maxs;
+  if (splits < 1) splits = 1;
+  int64_t tps = (pb.n + splits - 1) / splits;
+  tps = (tps + 127) / 128 * 128;
+  splits = (pb.n + tps - 1) / tps;
+  lay->splits = (int)splits;
+  lay->tokens_per_split = (int)tps;
+}
 
 luna_status plan(const Problem& pb, Layout* lay) {
   luna_status st = check_common(pb);
@@ -90,20 +107,11 @@ luna_status plan(const Problem& pb, Layout* lay) {
       lay->total = off;
       return LUNA_OK;
     }
-    // enough state workgroups to fill the device, at least 256 tokens each
-    const int64_t want = (512 + heads - 1) / heads;
-    const int64_t maxs = (pb.n + 255) / 256;
-    int64_t splits = want < maxs ? want : maxs;
-    if (splits < 1) splits = 1;
-    int64_t tps = (pb.n + splits - 1) / splits;
-    tps = (tps + 127) / 128 * 128;
-    splits = (pb.n + tps - 1) / tps;
-    lay->splits = (int)splits;
-    lay->tokens_per_split = (int)tps;
+    plan_splits(pb, heads, lay);
     lay->tile_tokens = 256;
     lay->tiles = (int)((pb.n + 255) / 256);
     lay->partial = off;
-    off = align256(off + (size_t)heads * splits * np.DP * (d + 1) * sizeof(float));
+    off = align256(off + (size_t)heads * lay->splits * np.DP * (d + 1) * sizeof(float));
     lay->frags = off;
     off = align256(off + (size_t)heads * np.frag_elems * (pb.dt == LUNA_BF16 ? 2 : 4));
   } else if (pb.op == LUNA_OP_ATTN_CAUSAL) {
@@ -128,6 +136,35 @@ luna_status plan(const Problem& pb, Layout* lay) {
         off = align256(off + (size_t)heads * lay->pieces * luna::causal_state_floats(dt, d, L, M) * sizeof(float));
       }
     }
+  } else if (pb.op == LUNA_OP_STATE) {
+    luna::NoncausalPlan np;
+    if (luna::noncausal_supported(dt, d, L, M, &np)) {
+      // the state pass of the non-causal split path
+      plan_splits(pb, heads, lay);
+      lay->partial = off;
+      off = align256(off + (size_t)heads * lay->splits * np.DP * (d + 1) * sizeof(float));
+    } else if (luna::causal_supported(dt, d, L, M)) {
+      // the causal kernel's state launch over every chunk, in pieces
+      const int64_t cx = (pb.n + 63) / 64;
+      int64_t pieces = (256 + heads - 1) / heads;
+      if (pieces > cx) pieces = cx;
+      const int64_t pc = (cx + pieces - 1) / pieces;
+      lay->piece_chunks = (int)pc;
+      lay->pieces = (int)((cx + pc - 1) / pc);
+      lay->split = (int)(cx * 64);
+      lay->state = off;
+      off = align256(off + (size_t)heads * lay->pieces * luna::causal_state_floats(dt, d, L, M) * sizeof(float));
+    } else {
+      return fail(LUNA_ERR_UNSUPPORTED, "no state kernel for this (dtype, d, L, M)");
+    }
+  } else if (pb.op == LUNA_OP_CAUSAL_STEP) {
+    if (!luna::featuremap_supported(dt, d, L, M))
+      return fail(LUNA_ERR_UNSUPPORTED, "no feature-map kernel for this (d, L, M)");
+    const size_t feat_bytes = (size_t)heads * (size_t)pb.n * (size_t)(M * L) * sizeof(float);
+    lay->phiq = off;
+    off = align256(off + feat_bytes);
+    lay->phik = off;
+    off = align256(off + feat_bytes);
   } else {
     return fail(LUNA_ERR_INVALID_ARG, "unknown operation code");
   }
@@ -291,6 +328,104 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   }
   hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");
+}
+
+luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int64_t B, int64_t H, int64_t n,
+                            int64_t d, const luna_phi_params* p, int32_t accumulate, float* S, float* z, void* ws,
+                            size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  Problem pb{LUNA_OP_STATE, dtype, B, H, n, d, p, 0};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (!K || !V || !S || !z) return fail(LUNA_ERR_INVALID_ARG, "K, V, S or z is NULL");
+  if (accumulate != 0 && accumulate != 1) return fail(LUNA_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  if (lay.pieces == 0) {
+    luna::NoncausalArgs a{};
+    a.K = K;
+    a.V = V;
+    a.phi = phi_args(pb, w, lay);
+    a.n = (int)n;
+    a.H = (int)H;
+    a.heads = (int)(B * H);
+    a.splits = lay.splits;
+    a.tokens_per_split = lay.tokens_per_split;
+    a.partial = reinterpret_cast<float*>(w + lay.partial);
+    a.state_S = S;
+    a.state_z = z;
+    a.accumulate = accumulate;
+    hipError_t e = luna::launch_state(dt, (int)d, p->L, p->M, a, s);
+    return e == hipSuccess ? LUNA_OK : hip_fail(e, "state kernel launch");
+  }
+  luna::CausalArgs a{};
+  a.K = K;
+  a.V = V;
+  a.Q = K;  // (the state launch reads no query rows)
+  a.phi = phi_args(pb, w, lay);
+  a.n = (int)n;
+  a.H = (int)H;
+  a.heads = (int)(B * H);
+  a.parts = 2;
+  a.split = lay.split;
+  a.pieces = lay.pieces;
+  a.piece_chunks = lay.piece_chunks;
+  a.state_out = reinterpret_cast<float*>(w + lay.state);
+  hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
+  if (e != hipSuccess) return hip_fail(e, "causal state launch");
+  a.export_S = S;
+  a.export_z = z;
+  a.accumulate = accumulate;
+  e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "state export launch");
+}
+
+luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B,
+                                  int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps, float* S,
+                                  float* z, void* out, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  Problem pb{LUNA_OP_CAUSAL_STEP, dtype, B, H, m, d, p, 0};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (!Q || !K || !V || !S || !z || !out) return fail(LUNA_ERR_INVALID_ARG, "Q, K, V, S, z or out is NULL");
+  if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  luna::FeatureMapArgs f{};
+  f.phi = phi_args(pb, w, lay);
+  f.rows_per_head = m;
+  f.H = (int)H;
+  f.heads = B * H;
+  f.X = Q;
+  f.out = w + lay.phiq;
+  hipError_t e = luna::launch_featuremap(dt, luna::Dt::F32, (int)d, p->L, f, s);
+  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch (queries)");
+  f.X = K;
+  f.out = w + lay.phik;
+  e = luna::launch_featuremap(dt, luna::Dt::F32, (int)d, p->L, f, s);
+  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch (keys)");
+  luna::StepArgs a{};
+  a.phiq = reinterpret_cast<const float*>(w + lay.phiq);
+  a.phik = reinterpret_cast<const float*>(w + lay.phik);
+  a.V = V;
+  a.out = out;
+  a.S = S;
+  a.z = z;
+  a.m = (int)m;
+  a.d = (int)d;
+  a.D = p->M * p->L;
+  a.heads = (int)(B * H);
+  a.eps = eps;
+  e = luna::launch_causal_step(dt, a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "streaming step kernel launch");
 }
 
 const char* luna_status_string(luna_status s) {

@@ -458,8 +458,13 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     };
     // phi of the rows held in xq, xk (the query rows when live) into phq_r, phk_r, and
     // the key rows added to z
-    auto map_rows = [&](auto qlive) {
+    auto map_rows = [&](auto qlive, int cc) {
       project_search(qlive);
+      if constexpr (ST) {  // key rows at or past n (a state of the whole sequence) add nothing
+#pragma unroll
+        for (int i = 0; i < 4 * MB; ++i)
+          if (64 * cc + 16 * rb + 4 * g + i % 4 >= n) ok[i] = zoff;
+      }
       if constexpr (decltype(qlive)::value) eval_all(phq_r, uq, oq, tfloor);
       eval_all(phk_r, uk, ok, tfloor);
       add_z();
@@ -468,7 +473,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       // State launch: every chunk is state-only.  z is only kept in registers; it is
       // written once, for the state piece, after the last chunk.  (Mapping the key
       // rows of two chunks as one batch made this launch slower: 186 against 159 us.)
-      map_rows(std::false_type{});  // chunk c_first
+      map_rows(std::false_type{}, c_first);
       load_rows(xq, a.Q, c_first + 1, false);
       load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
       write_k();
@@ -478,7 +483,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         const int cn = c + 1;
         __syncthreads();  // B1
         const bool kn = cn < c_end;
-        if (kn) map_rows(std::false_type{});
+        if (kn) map_rows(std::false_type{}, cn);
         load_rows(xq, a.Q, cn + 1, false);  // issued on every path (see the scan launch)
         load_rows(xk, a.K, cn + 1, kn);
         __syncthreads();  // B2
@@ -491,8 +496,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       write_z();  // z through the piece's last chunk, summed after the final barrier
     } else {
       // chunk c_first
-      if (c_first >= c_begin) map_rows(std::true_type{});
-      else map_rows(std::false_type{});
+      if (c_first >= c_begin) map_rows(std::true_type{}, c_first);
+      else map_rows(std::false_type{}, c_first);
       load_rows(xq, a.Q, c_first + 1, c_first + 1 >= c_begin && c_first + 1 < c_end);
       load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
       if (c_first >= c_begin) write_q();
@@ -818,8 +823,58 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   }
 }
 
+// State export: the state launch's pieces summed in piece order and written as
+// S [M*L][d], z [M*L] (fp32, feature i*L + l, the coefficient rows' power-of-two scale
+// removed), or added to them.  A piece holds the matrix waves' S tiles, lane-major
+// (tile (mw CBW + x) RB + b: rows krow(f) = 16 b + 4 g + jj, column 16 (CBW mw + x) + r
+// of lane 16 g + r), then z by internal feature.
+template <typename T, int DH, int L, int MB>
+__global__ __launch_bounds__(256) void causal_state_export_kernel(CausalArgs a) {
+  using C = CsCfg<T, DH, L, MB>;
+  const int head = blockIdx.x;
+  const int hset = a.phi.per_head ? head % a.H : 0;
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(a.phi.tables + (size_t)hset * kTableBytes + kTabHeader);
+  const float unscale = sizeof(T) == 2 ? ldexpf(1.0f, -hd.scale_exp) : 1.0f;
+  const int M = a.phi.M;
+  const float* pc = a.state_out + (size_t)head * a.pieces * C::STATE;
+  float* S = a.export_S + (size_t)head * M * L * DH;
+  float* z = a.export_z + (size_t)head * M * L;
+  // internal feature f -> projection and channel (the inverse of feat<MB>)
+  auto proj_chan = [](int f, int& p, int& l) {
+    const int pr = (f & 3) | (((f >> 3) & 3) << 2);
+    const int c = ((f >> 2) & 1) | ((f >> 5) << 1);
+    p = 16 * (c % MB) + pr;
+    l = c / MB;
+  };
+  for (int i = threadIdx.x; i < C::SF + C::FP; i += blockDim.x) {
+    int f, col = -1;
+    if (i < C::SF) {
+      const int jj = i % 4, lane = (i / 4) % kWave, tile = i / (4 * kWave);
+      const int b = tile % C::RB, xw = tile / C::RB;  // xw = CBW mw + x
+      const int rho = 16 * b + 4 * (lane / 16) + jj;
+      f = (rho & ~31) | (rho & 3) | ((rho << 1) & 24) | ((rho >> 2) & 4);  // the inverse of krow
+      col = 16 * xw + lane % 16;
+    } else {
+      f = i - C::SF;
+    }
+    int p, l;
+    proj_chan(f, p, l);
+    if (p >= M) continue;
+    float v = 0.0f;
+    for (int q = 0; q < a.pieces; ++q) v += pc[(size_t)q * C::STATE + i];
+    v *= unscale;
+    const int fp = p * L + l;
+    float* dst = col >= 0 ? &S[(size_t)fp * DH + col] : &z[fp];
+    *dst = a.accumulate ? *dst + v : v;
+  }
+}
+
 template <typename T, int DH, int L, int MB>
 static hipError_t cs_run(const CausalArgs& a, hipStream_t s) {
+  if (a.export_S != nullptr) {  // pieces already written by a state launch
+    hipLaunchKernelGGL((causal_state_export_kernel<T, DH, L, MB>), dim3(a.heads), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   const int per_head = a.state_out != nullptr ? a.pieces : a.parts;
   if (a.state_out != nullptr)
     hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, true>), dim3(a.heads * per_head), dim3(512), 0, s, a);

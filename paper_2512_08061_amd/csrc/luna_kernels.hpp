@@ -106,6 +106,11 @@ struct NoncausalArgs {
   int tile_tokens;      // tokens per readout workgroup (multiple of 16)
   int tiles;            // ceil(n / tile_tokens)
   int fused;            // 1: one workgroup per head does state and readout
+  // state export (luna_attn_state): S [heads][M*L][d] and z [heads][M*L], fp32,
+  // feature i*L + l; accumulate 1 adds to them instead of overwriting
+  float* state_S;
+  float* state_z;
+  int accumulate;
 };
 
 // Heads from which the non-causal path uses one fused workgroup per head, and the
@@ -131,7 +136,27 @@ struct CausalArgs {
   float* state_out;      // non-null: state launch
   const float* state_in;  // non-null: part 1 of the scan launch starts from the pieces
   int pieces, piece_chunks;
+  // non-null: sum the pieces in state_out into S [heads][M*L][d] and z [heads][M*L]
+  // (fp32, feature i*L + l; accumulate 1 adds to them) instead of launching the kernel
+  float* export_S;
+  float* export_z;
+  int accumulate;
 };
+
+// One streaming step of causal attention over m new tokens per head, from the
+// features of the new queries and keys (fp32, feature i*L + l) and the state (S, z),
+// which is updated in place.
+struct StepArgs {
+  const float* phiq;  // [heads][m][D]
+  const float* phik;  // [heads][m][D]
+  const void* V;      // [heads][m][d], element type of the call
+  void* out;          // [heads][m][d]
+  float* S;           // [heads][D][d]
+  float* z;           // [heads][D]
+  int m, d, D, heads;
+  float eps;
+};
+constexpr int kStepMaxD = 256;  // features the step kernel holds per column
 
 // Launchers; each returns hipSuccess or the launch error.  `ok` reports whether
 // a kernel exists for the (dtype, d, L, M) combination.
@@ -147,6 +172,11 @@ struct NoncausalPlan {
 };
 bool noncausal_supported(Dt dt, int d, int L, int M, NoncausalPlan* plan);
 hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s);
+// the state pass of the non-causal split path, then its partials summed into
+// state_S / state_z
+hipError_t launch_state(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s);
+
+hipError_t launch_causal_step(Dt dt, const StepArgs& a, hipStream_t s);
 
 bool causal_supported(Dt dt, int d, int L, int M);
 // floats of one state piece (S slices of the matrix waves, then z) for a combination

@@ -264,6 +264,37 @@ __global__ __launch_bounds__(256) void nc_reduce_kernel(NoncausalArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// state export: the partials summed in range order into S [D][d] and z [D]
+// (feature i*L + l, fp32, the coefficient rows' power-of-two scale removed), or
+// added to them
+// ---------------------------------------------------------------------------
+template <typename T, int DH, int L, int MB>
+__global__ __launch_bounds__(256) void nc_state_export_kernel(NoncausalArgs a) {
+  using C = NcCfg<T, DH, L, MB>;
+  const int head = blockIdx.x;
+  const int hset = a.phi.per_head ? head % a.H : 0;
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(a.phi.tables + (size_t)hset * kTableBytes + kTabHeader);
+  // the state pass evaluates bf16 data with fp16 rows that hold 2^scale_exp times the values
+  const float unscale = sizeof(T) == 2 ? ldexpf(1.0f, -hd.scale_exp) : 1.0f;
+  const int M = a.phi.M;
+  const float* part = a.partial + (size_t)head * a.splits * C::DP * (DH + 1);
+  float* S = a.state_S + (size_t)head * M * L * DH;
+  float* z = a.state_z + (size_t)head * M * L;
+  for (int i = threadIdx.x; i < C::DP * (DH + 1); i += blockDim.x) {
+    const int row = i / (DH + 1), col = i % (DH + 1);
+    // partial row (mb, l, i16) holds projection 16 mb + i16, channel l
+    const int mb = row / (16 * L), l = (row / 16) % L, p = 16 * mb + row % 16;
+    if (p >= M) continue;
+    float v = 0.0f;
+    for (int sp = 0; sp < a.splits; ++sp) v += part[(size_t)sp * C::DP * (DH + 1) + i];
+    v *= unscale;
+    const int f = p * L + l;
+    float* dst = col < DH ? &S[(size_t)f * DH + col] : &z[f];
+    *dst = a.accumulate ? *dst + v : v;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // readout pass
 // ---------------------------------------------------------------------------
 template <typename T, int DH, int L, int MB>
@@ -757,6 +788,15 @@ static hipError_t nc_run(const NoncausalArgs& a, hipStream_t s) {
 }
 
 template <typename T, int DH, int L, int MB>
+static hipError_t state_run(const NoncausalArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((nc_state_kernel<T, DH, L, MB>), dim3(a.heads * a.splits), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((nc_state_export_kernel<T, DH, L, MB>), dim3(a.heads), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T, int DH, int L, int MB>
 static void nc_plan(NoncausalPlan* p) {
   using C = NcCfg<T, DH, L, MB>;
   p->DP = C::DP;
@@ -789,6 +829,15 @@ bool noncausal_supported(Dt dt, int d, int L, int M, NoncausalPlan* plan) {
   LUNA_NC_CASES(X)
 #undef X
   return false;
+}
+
+hipError_t launch_state(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s) {
+  const int MB = (M + 15) / 16;
+#define X(T_, D_, L_, MB_) \
+  if (dt == dt_of<T_>() && d == D_ && L == L_ && MB == MB_) return state_run<T_, D_, L_, MB_>(a, s);
+  LUNA_NC_CASES(X)
+#undef X
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_noncausal(Dt dt, int d, int L, int M, const NoncausalArgs& a, hipStream_t s) {

@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "luna.h")
 
 LUNA_OK, LUNA_ERR_INVALID_ARG, LUNA_ERR_UNSUPPORTED, LUNA_ERR_WORKSPACE, LUNA_ERR_HIP = range(5)
 LUNA_F32, LUNA_BF16 = 0, 1
-OP_FEATUREMAP, OP_ATTN, OP_ATTN_CAUSAL = 0, 1, 2
+OP_FEATUREMAP, OP_ATTN, OP_ATTN_CAUSAL, OP_STATE, OP_CAUSAL_STEP = 0, 1, 2, 3, 4
 
 
 class LunaError(RuntimeError):
@@ -60,6 +60,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.luna_attn_fwd_causal.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float, vp, vp,
                                          sz, vp]
     lib.luna_attn_fwd_causal.restype = i32
+    lib.luna_attn_state.argtypes = [vp, vp, i32, i64, i64, i64, i64, P, i32, vp, vp, vp, sz, vp]
+    lib.luna_attn_state.restype = i32
+    lib.luna_attn_causal_step.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, vp, vp, vp, vp,
+                                          sz, vp]
+    lib.luna_attn_causal_step.restype = i32
     lib.luna_status_string.argtypes = [i32]
     lib.luna_status_string.restype = ctypes.c_char_p
     lib.luna_last_error.argtypes = []
@@ -215,6 +220,60 @@ def attn_fwd_causal(Q, K, V, p: PhiParams, chunk: int = 64, eps: float = 1e-6, o
     ws, wsp, wsn = _workspace(nb, Q.device)
     _check(lib.luna_attn_fwd_causal(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc),
                                     chunk, eps, out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
+    out._luna_ws = ws
+    return out
+
+
+def _state_tensors(B, H, D, d, device, S, z):
+    torch = _torch()
+    if S is None:
+        S = torch.zeros((B, H, D, d), dtype=torch.float32, device=device)
+    if z is None:
+        z = torch.zeros((B, H, D), dtype=torch.float32, device=device)
+    if tuple(S.shape) != (B, H, D, d) or S.dtype != torch.float32 or not S.is_contiguous():
+        raise LunaError(LUNA_ERR_INVALID_ARG, "S must be a contiguous fp32 [B, H, M*L, d] tensor")
+    if tuple(z.shape) != (B, H, D) or z.dtype != torch.float32 or not z.is_contiguous():
+        raise LunaError(LUNA_ERR_INVALID_ARG, "z must be a contiguous fp32 [B, H, M*L] tensor")
+    return S, z
+
+
+def attn_state(K, V, p: PhiParams, S=None, z=None, accumulate: bool = False):
+    """Causal state of the tokens of K, V: S = phi(K)^T V [B, H, M*L, d] and z = phi(K)^T 1
+    [B, H, M*L] (fp32), written into S, z (allocated when None) or added to them."""
+    lib = load_library()
+    B, H, n, d = _qkv_shape(K, V)
+    S, z = _state_tensors(B, H, p.M * p.L, d, K.device, S, z)
+    pc = p.c()
+    dt = _dt(K)
+    nb = lib.luna_workspace_bytes(OP_STATE, dt, B, H, n, d, ctypes.byref(pc), 64)
+    if nb == 0:
+        _check(lib.luna_attn_state(K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), int(accumulate),
+                                   S.data_ptr(), z.data_ptr(), None, 0, None))
+    ws, wsp, wsn = _workspace(nb, K.device)
+    _check(lib.luna_attn_state(K.data_ptr(), V.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), int(accumulate),
+                               S.data_ptr(), z.data_ptr(), wsp, wsn, _stream_ptr(K.device)))
+    S._luna_ws = ws
+    return S, z
+
+
+def attn_causal_step(Q, K, V, p: PhiParams, S, z, eps: float = 1e-6, out=None):
+    """One streaming step over the m new tokens of Q, K, V [B, H, m, d] from the state
+    (S, z), which is updated in place; returns out [B, H, m, d]."""
+    torch = _torch()
+    lib = load_library()
+    B, H, m, d = _qkv_shape(Q, K, V)
+    S, z = _state_tensors(B, H, p.M * p.L, d, Q.device, S, z)
+    out = torch.empty_like(Q) if out is None else out
+    pc = p.c()
+    dt = _dt(Q)
+    nb = lib.luna_workspace_bytes(OP_CAUSAL_STEP, dt, B, H, m, d, ctypes.byref(pc), 64)
+    if nb == 0:
+        _check(lib.luna_attn_causal_step(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, m, d,
+                                         ctypes.byref(pc), eps, S.data_ptr(), z.data_ptr(), out.data_ptr(), None, 0,
+                                         None))
+    ws, wsp, wsn = _workspace(nb, Q.device)
+    _check(lib.luna_attn_causal_step(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, m, d, ctypes.byref(pc), eps,
+                                     S.data_ptr(), z.data_ptr(), out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
     out._luna_ws = ws
     return out
 

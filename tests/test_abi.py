@@ -22,7 +22,7 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     names = luna.header_functions()
     assert set(names) == {"luna_workspace_bytes", "luna_featuremap", "luna_attn_fwd", "luna_attn_fwd_causal",
-                          "luna_status_string", "luna_last_error"}
+                          "luna_attn_state", "luna_attn_causal_step", "luna_status_string", "luna_last_error"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -80,6 +80,37 @@ def test_featuremap_rejects(lib):
     p3 = _params(L=3)
     assert lib.luna_featuremap(FAKE, luna.LUNA_BF16, 1, 1, 10, 64, ctypes.byref(p3), FAKE, luna.LUNA_BF16, FAKE,
                                1 << 40, None) == luna.LUNA_ERR_UNSUPPORTED
+
+
+def test_state_and_step_reject(lib):
+    p = _params()
+    st = lambda **kw: lib.luna_attn_state(kw.get("k", FAKE), FAKE, luna.LUNA_BF16, 2, 3, kw.get("n", 100), 64,
+                                          ctypes.byref(kw.get("p", p)), kw.get("acc", 0), kw.get("S", FAKE), FAKE,
+                                          FAKE, kw.get("ws_bytes", 1 << 40), None)
+    assert st(k=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(S=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(acc=2) == luna.LUNA_ERR_INVALID_ARG
+    assert st(n=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(ws_bytes=256) == luna.LUNA_ERR_WORKSPACE
+    assert st(p=_params(L=3)) == luna.LUNA_ERR_UNSUPPORTED
+    stp = lambda **kw: lib.luna_attn_causal_step(FAKE, FAKE, FAKE, luna.LUNA_BF16, 2, 3, kw.get("m", 4), 64,
+                                                 ctypes.byref(kw.get("p", p)), kw.get("eps", 1e-6),
+                                                 kw.get("S", FAKE), FAKE, kw.get("out", FAKE), FAKE,
+                                                 kw.get("ws_bytes", 1 << 40), None)
+    assert stp(S=0) == luna.LUNA_ERR_INVALID_ARG
+    assert stp(out=0) == luna.LUNA_ERR_INVALID_ARG
+    assert stp(eps=-1.0) == luna.LUNA_ERR_INVALID_ARG
+    assert stp(m=0) == luna.LUNA_ERR_INVALID_ARG
+    assert stp(ws_bytes=256) == luna.LUNA_ERR_WORKSPACE
+    assert stp(p=_params(L=3)) == luna.LUNA_ERR_UNSUPPORTED
+    assert lib.luna_last_error()
+    # workspace: tables plus the new tokens' features (fp32) for a step; tables plus
+    # partial statistics for the state
+    nb1 = lib.luna_workspace_bytes(luna.OP_CAUSAL_STEP, luna.LUNA_BF16, 2, 3, 1, 64, ctypes.byref(p), 64)
+    nb9 = lib.luna_workspace_bytes(luna.OP_CAUSAL_STEP, luna.LUNA_BF16, 2, 3, 9, 64, ctypes.byref(p), 64)
+    assert 0 < nb1 < nb9 and nb9 % 256 == 0
+    assert lib.luna_workspace_bytes(luna.OP_STATE, luna.LUNA_BF16, 8, 16, 16384, 128, ctypes.byref(_params(M=32)),
+                                    64) > 0
 
 
 def test_workspace_sizes(lib):

@@ -1,0 +1,124 @@
+"""The streaming form of causal attention on the GPU, through the C ABI, against the
+float64 oracle: the causal state of a sequence (luna_attn_state) and the recurrent
+step over new tokens (luna_attn_causal_step), alone and chained (state of a prefix,
+then steps), with ragged step sizes, one-token decode and partial last chunks.
+Tolerance: normwise per (b, h) slice, 1e-4 for fp32 and 2e-2 for bf16 inputs."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_close, inputs, say, small_workload, to_np, upload
+from paper_2512_08061_amd import luna
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    luna.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _col(z):
+    """z [..., D] as [..., D, 1], so that the normwise check runs per (b, h)."""
+    return np.asarray(z)[..., None]
+
+
+# (dtype, d, M, L, n, B, H): the first ones take the non-causal state pass, the
+# (bf16, 128, 32, 8) ones the causal kernel's state launch (pieces, then export)
+STATE_CASES = [
+    ("f32", 32, 8, 8, 100, 2, 3), ("f32", 64, 16, 8, 65, 1, 2), ("bf16", 64, 16, 8, 300, 2, 3),
+    ("bf16", 64, 32, 8, 130, 1, 3), ("bf16", 64, 64, 1, 97, 1, 2),
+    ("bf16", 128, 32, 8, 1, 2, 2), ("bf16", 128, 32, 8, 64, 1, 3), ("bf16", 128, 32, 8, 200, 1, 1),
+    ("bf16", 128, 32, 8, 700, 2, 5),
+]
+
+
+@pytest.mark.parametrize("dtype,d,M,L,n,B,H", STATE_CASES)
+def test_attn_state(dtype, d, M, L, n, B, H):
+    import torch
+    w = small_workload(dtype, B=B, H=H, n=n, d=d, M=M, L=L, causal=True)
+    say(f"state {w.name} B={B} H={H}")
+    Q, K, V, p = inputs(w, seed=7)
+    (Kt, Vt), pt = upload(w, [K, V], p)
+    S, z = luna.attn_state(Kt, Vt, pt)
+    Sr, zr = oracle.causal_state(K, V, p)
+    assert_close(to_np(S), Sr, dtype, "S")
+    assert_close(_col(to_np(z)), _col(zr), dtype, "z")
+    # accumulate onto a given state: S0 + state
+    rng = np.random.default_rng(1)
+    S0 = rng.standard_normal(Sr.shape) * np.abs(Sr).max()
+    z0 = np.abs(rng.standard_normal(zr.shape)) * np.abs(zr).max()
+    St = torch.from_numpy(S0).float().cuda().contiguous()
+    zt = torch.from_numpy(z0).float().cuda().contiguous()
+    luna.attn_state(Kt, Vt, pt, St, zt, accumulate=True)
+    assert_close(to_np(St), S0 + Sr, dtype, "S accumulated")
+    assert_close(_col(to_np(zt)), _col(z0 + zr), dtype, "z accumulated")
+
+
+# (dtype, d, M, L, n, m): every step but the last has m tokens
+STEP_CASES = [
+    ("f32", 32, 8, 8, 37, 5), ("f32", 64, 16, 8, 20, 1), ("bf16", 64, 16, 8, 100, 16), ("bf16", 128, 32, 8, 70, 33),
+    ("bf16", 32, 5, 4, 20, 1), ("bf16", 64, 64, 4, 40, 17), ("bf16", 128, 3, 8, 9, 4),
+]
+
+
+@pytest.mark.parametrize("dtype,d,M,L,n,m", STEP_CASES)
+def test_causal_step_from_zero(dtype, d, M, L, n, m):
+    """Steps of m tokens from the empty prefix give the causal form and, at the end,
+    the state of the whole sequence."""
+    import torch
+    w = small_workload(dtype, B=2, H=2, n=n, d=d, M=M, L=L, causal=True)
+    say(f"step {w.name} m={m}")
+    Q, K, V, p = inputs(w, seed=11)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    D = M * L
+    S = torch.zeros((2, 2, D, d), dtype=torch.float32, device="cuda")
+    z = torch.zeros((2, 2, D), dtype=torch.float32, device="cuda")
+    outs = []
+    for a in range(0, n, m):
+        b = min(n, a + m)
+        sl = lambda X: X[:, :, a:b].contiguous()  # noqa: E731
+        outs.append(to_np(luna.attn_causal_step(sl(Qt), sl(Kt), sl(Vt), pt, S, z, eps=w.eps)))
+    out = np.concatenate(outs, axis=2)
+    assert_close(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), dtype, "out")
+    Sr, zr = oracle.causal_state(K, V, p)
+    assert_close(to_np(S), Sr, dtype, "S")
+    assert_close(_col(to_np(z)), _col(zr), dtype, "z")
+
+
+@pytest.mark.parametrize("dtype,d,M,L,n0", [("bf16", 128, 32, 8, 150), ("bf16", 64, 16, 8, 64), ("f32", 32, 8, 8, 33)])
+def test_prefill_then_decode(dtype, d, M, L, n0):
+    """The state of a prefix from luna_attn_state, then one-token steps: the rows of
+    the causal form after the prefix, and the same rows as the chunked scan."""
+    w = small_workload(dtype, B=1, H=3, n=n0 + 8, d=d, M=M, L=L, causal=True)
+    say(f"prefill {n0} then decode 8: {w.name}")
+    Q, K, V, p = inputs(w, seed=13)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    S, z = luna.attn_state(Kt[:, :, :n0].contiguous(), Vt[:, :, :n0].contiguous(), pt)
+    outs = []
+    for t in range(n0, n0 + 8):
+        sl = lambda X: X[:, :, t:t + 1].contiguous()  # noqa: E731
+        outs.append(to_np(luna.attn_causal_step(sl(Qt), sl(Kt), sl(Vt), pt, S, z, eps=w.eps)))
+    out = np.concatenate(outs, axis=2)
+    ref = oracle.attn_causal(Q, K, V, p, eps=w.eps)[:, :, n0:]
+    assert_close(out, ref, dtype, "decoded rows")
+    scan = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))[:, :, n0:]
+    assert_close(out, scan, dtype, "decoded rows against the chunked scan")
+
+
+def test_step_rejects_bad_state():
+    """Malformed state tensors are refused before anything runs."""
+    import torch
+    w = small_workload("bf16", B=1, H=2, n=5, d=64, M=16, L=8, causal=True)
+    Q, K, V, p = inputs(w, seed=17)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    S = torch.zeros((1, 2, 128, 64), dtype=torch.float32, device="cuda")
+    z = torch.zeros((1, 2, 128), dtype=torch.float32, device="cuda")
+    with pytest.raises(luna.LunaError):
+        luna.attn_causal_step(Qt, Kt, Vt, pt, S[:, :, :64].contiguous(), z, eps=w.eps)
+    with pytest.raises(luna.LunaError):
+        luna.attn_causal_step(Qt, Kt, Vt, pt, S.half(), z, eps=w.eps)

@@ -186,6 +186,79 @@ def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
     }
 
 
+def decode_bench(args) -> int:
+    """Streaming steps of m tokens per head from the state of a 16384-token prefix on
+    the long causal problem's shape (B=8, H=16, d=128, M=32 x L=8, bf16).  Each step
+    reads and writes the fp32 state S [128 heads][256][128] and z once."""
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only; use --gpus 1.", file=sys.stderr)
+        return 2
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    luna.load_library()
+    w = wl.WORKLOADS["long_causal"]
+    m = int(args.decode)
+    Q, K, V = wl.make_inputs(w, args.seed)
+    p = wl.make_params(w, args.seed)
+    up = lambda a: torch.from_numpy(a).to(dev).to(torch.bfloat16).contiguous()  # noqa: E731
+    kt, vt = up(K), up(V)
+    pt = luna.PhiParams.from_arrays(p, dev, torch.bfloat16)
+    S, z = luna.attn_state(kt, vt, pt)  # the prefix
+    del kt, vt
+    rng = __import__("numpy").random.default_rng(args.seed + 1)
+    new = [up(rng.standard_normal((w.B, w.H, m, w.d)).astype("float32")) for _ in range(3)]
+    # one persistent workspace: the first step builds the channel tables, the others reuse them
+    plan = luna.StepPlan(pt, w.B, w.H, m, w.d, torch.bfloat16, dev, eps=w.eps)
+    out = torch.empty_like(new[0])
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        plan.run(new[0], new[1], new[2], S, z, out, stream.cuda_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    heads, D = w.B * w.H, w.M * w.L
+    state_bytes = 2 * heads * D * (w.d + 1) * 4  # S and z, read and written once
+    io_bytes = 4 * heads * m * w.d * 2            # q, k, v read, out written
+    gbs = (state_bytes + io_bytes) / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "LUNA causal streaming step tokens/sec (decode)",
+        "value": heads * m / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded)",
+        "config": {"workload": f"streaming step of {m} token(s) per head after a 16384-token prefix, "
+                               "B=8 H=16 d=128 M=32 L=8 (D=256), bf16, fp32 state", "m": m},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "causal_step_kernel",
+                     "bytes_per_call": state_bytes + io_bytes,
+                     "timing": "HIP events around the ABI calls (tables built by the first, reused after): "
+                               "one feature-map launch for the new queries and keys, then the step kernel"},
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,9 +275,15 @@ def main() -> int:
                     help="summarise two rocprofv3 --pmc csv runs into profiles/hbm_traffic_*.json and exit")
     ap.add_argument("--traffic-command", default="",
                     help="the rocprofv3 commands that produced --traffic-from, recorded in the summary")
+    ap.add_argument("--decode", type=int, default=0, metavar="M",
+                    help="instead of the hot-path step: time streaming steps of M new tokens per head "
+                         "(luna_attn_causal_step) on the long causal problem's shape, after the state of "
+                         "its 16384-token prefix, and print their JSON line")
     args = ap.parse_args()
     if args.traffic_from:
         return traffic_from(*args.traffic_from, args.traffic_command)
+    if args.decode:
+        return decode_bench(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: LUNA attention shards over (batch, head) with no "

@@ -162,14 +162,21 @@ luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int6
  * per (b, h), in order:
  *   S += phi(k_t) v_t^T;  z += phi(k_t);  out_t = phi(q_t)^T S / (phi(q_t)^T z + eps).
  * S [B, H, M*L, d] and z [B, H, M*L] (fp32, feature i*L + l) are read and updated in
- * place; they must not alias Q, K, V, out or the workspace.  Q, K, V, out:
+ * place; they must not alias Q, K, V, out or the workspace, and S must be 16-byte
+ * aligned.  Q, K, V, out:
  * [B, H, m, d] in dtype.  The state is carried in fp32 throughout.  Stepping a
  * sequence from zeros gives what luna_attn_fwd_causal computes, up to rounding.
+ * tables_ready 0: the call builds the channel tables in the workspace, as every
+ * other entry point does; 1: it uses the tables an earlier luna_attn_causal_step
+ * left in the same workspace, enqueued before it on the same stream, with the same
+ * parameters (same arrays, unchanged contents) -- for decode loops, where the table
+ * build would otherwise cost as much as the step itself.
  * The same (d, L, M) combinations as luna_featuremap are built.
  */
 luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B,
-                                  int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps, float* S,
-                                  float* z, void* out, void* ws, size_t ws_bytes, void* stream);
+                                  int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps,
+                                  int32_t tables_ready, float* S, float* z, void* out, void* ws, size_t ws_bytes,
+                                  void* stream);
 
 /* Static description of a status code. */
 const char* luna_status_string(luna_status s);

@@ -385,33 +385,41 @@ luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int6
 }
 
 luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B,
-                                  int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps, float* S,
-                                  float* z, void* out, void* ws, size_t ws_bytes, void* stream) {
+                                  int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps,
+                                  int32_t tables_ready, float* S, float* z, void* out, void* ws, size_t ws_bytes,
+                                  void* stream) {
   g_last_error.clear();
   Problem pb{LUNA_OP_CAUSAL_STEP, dtype, B, H, m, d, p, 0};
   Layout lay;
   luna_status st = plan(pb, &lay);
   if (st != LUNA_OK) return st;
   if (!Q || !K || !V || !S || !z || !out) return fail(LUNA_ERR_INVALID_ARG, "Q, K, V, S, z or out is NULL");
+  if (((uintptr_t)S & 15) != 0) return fail(LUNA_ERR_INVALID_ARG, "S must be 16-byte aligned");
   if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (tables_ready != 0 && tables_ready != 1) return fail(LUNA_ERR_INVALID_ARG, "tables_ready must be 0 or 1");
   if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* w = static_cast<uint8_t*>(ws);
-  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  if (!tables_ready && (st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
   const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
-  luna::FeatureMapArgs f{};
+  luna::FeatureMapArgs f{};  // queries and keys in one launch
   f.phi = phi_args(pb, w, lay);
   f.rows_per_head = m;
   f.H = (int)H;
   f.heads = B * H;
+  if (!p->per_head && B * H * m <= ((int64_t)1 << 30)) {
+    // one parameter set: the rows of all heads are one contiguous array, mapped in
+    // 64-row tiles across heads (a one-token step then needs B*H/64 tiles, not B*H)
+    f.rows_per_head = B * H * m;
+    f.H = 1;
+    f.heads = 1;
+  }
   f.X = Q;
   f.out = w + lay.phiq;
+  f.X2 = K;
+  f.out2 = w + lay.phik;
   hipError_t e = luna::launch_featuremap(dt, luna::Dt::F32, (int)d, p->L, f, s);
-  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch (queries)");
-  f.X = K;
-  f.out = w + lay.phik;
-  e = luna::launch_featuremap(dt, luna::Dt::F32, (int)d, p->L, f, s);
-  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch (keys)");
+  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch");
   luna::StepArgs a{};
   a.phiq = reinterpret_cast<const float*>(w + lay.phiq);
   a.phik = reinterpret_cast<const float*>(w + lay.phik);

@@ -831,7 +831,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 template <typename T, int DH, int L, int MB>
 __global__ __launch_bounds__(256) void causal_state_export_kernel(CausalArgs a) {
   using C = CsCfg<T, DH, L, MB>;
-  const int head = blockIdx.x;
+  const int head = blockIdx.x;  // blockIdx.y: a slice of the head's elements
   const int hset = a.phi.per_head ? head % a.H : 0;
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(a.phi.tables + (size_t)hset * kTableBytes + kTabHeader);
   const float unscale = sizeof(T) == 2 ? ldexpf(1.0f, -hd.scale_exp) : 1.0f;
@@ -846,7 +846,7 @@ __global__ __launch_bounds__(256) void causal_state_export_kernel(CausalArgs a) 
     p = 16 * (c % MB) + pr;
     l = c / MB;
   };
-  for (int i = threadIdx.x; i < C::SF + C::FP; i += blockDim.x) {
+  for (int i = blockIdx.y * blockDim.x + threadIdx.x; i < C::SF + C::FP; i += gridDim.y * blockDim.x) {
     int f, col = -1;
     if (i < C::SF) {
       const int jj = i % 4, lane = (i / 4) % kWave, tile = i / (4 * kWave);
@@ -872,7 +872,7 @@ __global__ __launch_bounds__(256) void causal_state_export_kernel(CausalArgs a) 
 template <typename T, int DH, int L, int MB>
 static hipError_t cs_run(const CausalArgs& a, hipStream_t s) {
   if (a.export_S != nullptr) {  // pieces already written by a state launch
-    hipLaunchKernelGGL((causal_state_export_kernel<T, DH, L, MB>), dim3(a.heads), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((causal_state_export_kernel<T, DH, L, MB>), dim3(a.heads, 16), dim3(256), 0, s, a);
     return hipGetLastError();
   }
   const int per_head = a.state_out != nullptr ? a.pieces : a.parts;

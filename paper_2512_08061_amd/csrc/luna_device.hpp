@@ -66,15 +66,38 @@ struct alignas(16) PwlLds {
 
 // Cooperative 16-byte copies global -> LDS: `n16` chunks, and rows of `row16` chunks
 // from a dense source into a destination with `dst_row16`-chunk rows.
+// Each thread issues up to kCopyBatch loads before it stores them, so that a copy
+// costs about one memory round trip rather than one per chunk it moves.  The loads
+// are unconditional (indices clamped to the last chunk): conditional ones would make
+// the compiler keep the batch in scratch memory.
+constexpr int kCopyBatch = 8;
 __device__ inline void copy16(void* dst, const void* src, int n16) {
   uint4* d = reinterpret_cast<uint4*>(dst);
   const uint4* sp = reinterpret_cast<const uint4*>(src);
-  for (int i = threadIdx.x; i < n16; i += blockDim.x) d[i] = sp[i];
+  const int nt = blockDim.x;
+  for (int base = threadIdx.x; base < n16; base += kCopyBatch * nt) {
+    uint4 v[kCopyBatch];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) v[u] = sp[min(base + u * nt, n16 - 1)];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u)
+      if (base + u * nt < n16) d[base + u * nt] = v[u];
+  }
 }
 __device__ inline void copy16_rows(void* dst, int dst_row16, const void* src, int row16, int rows) {
   uint4* d = reinterpret_cast<uint4*>(dst);
   const uint4* sp = reinterpret_cast<const uint4*>(src);
-  for (int i = threadIdx.x; i < rows * row16; i += blockDim.x) d[(i / row16) * dst_row16 + i % row16] = sp[i];
+  const int n16 = rows * row16, nt = blockDim.x;
+  for (int base = threadIdx.x; base < n16; base += kCopyBatch * nt) {
+    uint4 v[kCopyBatch];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) v[u] = sp[min(base + u * nt, n16 - 1)];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      const int i = base + u * nt;
+      if (i < n16) d[(i / row16) * dst_row16 + i % row16] = v[u];
+    }
+  }
 }
 
 // Cooperative copy of a table from global memory into LDS.  Caller syncs after.

@@ -17,11 +17,18 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   __shared__ PwlLds<L, nseg_cap(L, kFmSegBytes)> tab;
 
   const int tiles_per_head = (int)((a.rows_per_head + 63) / 64);
-  const int64_t head = blockIdx.x / tiles_per_head;
-  const int tile = blockIdx.x - (int)(head * tiles_per_head);
+  // with a second input the grid is doubled: its second half maps X2 into out2
+  int64_t bid = blockIdx.x;
+  const void* Xsrc = a.X;
+  void* Odst = a.out;
+  if (bid >= a.heads * tiles_per_head) {
+    bid -= a.heads * tiles_per_head;
+    Xsrc = a.X2;
+    Odst = a.out2;
+  }
+  const int64_t head = bid / tiles_per_head;
+  const int tile = (int)(bid - head * tiles_per_head);
   const int hset = a.phi.per_head ? (int)(head % a.H) : 0;
-  pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
-  __syncthreads();
 
   const int wave = wave_id(), lane = threadIdx.x % kWave;
   const int g = lane / 16, r = lane % 16;
@@ -30,37 +37,51 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   const bool row_ok = t < n;
   const int M = a.phi.M;
   const int D = M * L;
-  const Tin* X = reinterpret_cast<const Tin*>(a.X) + (head * n + (row_ok ? t : 0)) * DH;
+  const Tin* X = reinterpret_cast<const Tin*>(Xsrc) + (head * n + (row_ok ? t : 0)) * DH;
   const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
   const float* bias = a.phi.b + (size_t)hset * M;
-  Tout* out = reinterpret_cast<Tout*>(a.out) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
-  const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
-  const float floor = tab.floor;
+  Tout* out = reinterpret_cast<Tout*>(Odst) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
 
+  // the row, W fragments and biases are fetched before the table, so that their
+  // loads overlap its copy
+  constexpr int kMaxMB = 4;  // M <= 64
+  const int MB = (M + 15) / 16;
   Frag<Tin> xf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     if (row_ok) load8(xf[ks], X + 32 * ks + 8 * g);
     else xf[ks].zero();
   }
-
-  const int MB = (M + 15) / 16;
-  for (int mb = 0; mb < MB; ++mb) {
+  Frag<Tin> wfr[kMaxMB][KS];
+  float bz[kMaxMB][4];
+#pragma unroll
+  for (int mb = 0; mb < kMaxMB; ++mb) {
     const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
-    f32x4 acc = zero4();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      Frag<Tin> wf;
-      if (prow < M) load8(wf, W + (size_t)prow * DH + 32 * ks + 8 * g);
-      else wf.zero();
-      mma(acc, wf, xf[ks]);
+      if (mb < MB && prow < M) load8(wfr[mb][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
+      else wfr[mb][ks].zero();
     }
-    float uu[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
-      uu[j] = acc[j] + (i < M ? bias[i] : 0.0f);
+      bz[mb][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
     }
+  }
+  pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+  __syncthreads();
+  const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
+  const float floor = tab.floor;
+
+#pragma unroll
+  for (int mb = 0; mb < kMaxMB; ++mb) {
+    if (mb >= MB) break;
+    f32x4 acc = zero4();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mb][ks], xf[ks]);
+    float uu[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) uu[j] = acc[j] + bz[mb][j];
     int sg[4];
     pwl_search(tab, steps, uu, sg);
 #pragma unroll
@@ -85,7 +106,7 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
 template <typename Tin, typename Tout, int DH>
 static hipError_t fm_dispatch_L(int L, const FeatureMapArgs& a, hipStream_t s) {
   const int tiles = (int)((a.rows_per_head + 63) / 64);
-  const dim3 grid((unsigned)(a.heads * tiles)), block(256);
+  const dim3 grid((unsigned)(a.heads * tiles * (a.X2 != nullptr ? 2 : 1))), block(256);
   switch (L) {
     case 1: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 1>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 2>), grid, block, 0, s, a); break;

@@ -85,6 +85,8 @@ struct PhiArgs {
 struct FeatureMapArgs {
   const void* X;
   void* out;
+  const void* X2;  // non-null: a second input of the same shape, mapped into out2
+  void* out2;
   PhiArgs phi;
   int64_t rows_per_head;  // n
   int H;

@@ -280,7 +280,7 @@ __global__ __launch_bounds__(256) void nc_state_export_kernel(NoncausalArgs a) {
   const float* part = a.partial + (size_t)head * a.splits * C::DP * (DH + 1);
   float* S = a.state_S + (size_t)head * M * L * DH;
   float* z = a.state_z + (size_t)head * M * L;
-  for (int i = threadIdx.x; i < C::DP * (DH + 1); i += blockDim.x) {
+  for (int i = blockIdx.y * blockDim.x + threadIdx.x; i < C::DP * (DH + 1); i += gridDim.y * blockDim.x) {
     const int row = i / (DH + 1), col = i % (DH + 1);
     // partial row (mb, l, i16) holds projection 16 mb + i16, channel l
     const int mb = row / (16 * L), l = (row / 16) % L, p = 16 * mb + row % 16;
@@ -792,7 +792,7 @@ static hipError_t state_run(const NoncausalArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((nc_state_kernel<T, DH, L, MB>), dim3(a.heads * a.splits), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((nc_state_export_kernel<T, DH, L, MB>), dim3(a.heads), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((nc_state_export_kernel<T, DH, L, MB>), dim3(a.heads, 8), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

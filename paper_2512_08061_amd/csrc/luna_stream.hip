@@ -8,14 +8,15 @@
 // queries and keys come from the feature-map kernel (fp32); this kernel carries the
 // state.
 //
-// One workgroup per (head, block of 32 value columns): thread (g, j) holds S[f][j] for
-// the features f = g + 8 i of its group g (interleaved, so that the eight groups read
-// eight consecutive LDS words of a feature row) and the same features of z, all in
-// fp32 registers for the whole step.  Per token it adds the key's outer product and
-// forms its partial numerator and denominator; the eight groups' partials are summed
-// through LDS in group order (deterministic), one barrier per token.  The state is
-// read once at the start and written once at the end, so a step of m tokens costs one
-// pass over S whatever m is.
+// One workgroup per (head, block of 32 value columns).  Thread (g, q) holds, for the
+// features f = g + 32 i of its group g (i < 8; interleaved, so that the groups of a
+// wave read consecutive LDS words of a feature row), the four columns 4q .. 4q + 3 of
+// S as float4 and the same features of z, in fp32 registers for the whole step.  Per
+// token it adds the key's outer product and forms its partial numerator (four
+// columns) and denominator; the eight groups of a wave are added with lane shuffles
+// and the four waves through LDS, in a fixed order (deterministic), one barrier per
+// token.  The state is read once at the start and written once at the end (16-byte
+// accesses), so a step of m tokens costs one pass over S whatever m is.
 #include "luna_device.hpp"
 #include "luna_kernels.hpp"
 
@@ -23,24 +24,26 @@ namespace luna {
 
 namespace {
 
-constexpr int kStepCols = 32;                     // value columns per workgroup
-constexpr int kStepGroups = 8;                    // feature groups (threads per column)
+constexpr int kStepCols = 32;                       // value columns per workgroup
+constexpr int kStepQuads = kStepCols / 4;           // column quads per workgroup
+constexpr int kStepGroups = 256 / kStepQuads;       // feature groups
 constexpr int kStepFeat = kStepMaxD / kStepGroups;  // features per thread
-constexpr int kStepTokens = 16;                   // tokens staged in LDS at a time
+constexpr int kStepTokens = 16;                     // tokens staged in LDS at a time
 
 template <typename T>
 __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   __shared__ float sq[kStepTokens][kStepMaxD];
   __shared__ float sk[kStepTokens][kStepMaxD];
-  __shared__ float red[2][kStepGroups][kStepCols + 1];  // partial numerators, then the denominator
+  __shared__ __attribute__((aligned(16))) float sv[kStepTokens][kStepCols];
+  __shared__ float red[2][4][kStepQuads][5];  // per wave and column quad: four numerators, the denominator
 
   const int nblk = a.d / kStepCols;
   const int head = blockIdx.x / nblk;
   const int cblk = blockIdx.x - head * nblk;
-  const int j = threadIdx.x % kStepCols;
-  const int grp = threadIdx.x / kStepCols;
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int q = tid % kStepQuads, grp = tid / kStepQuads;
   const int D = a.D, d = a.d, m = a.m;
-  const int col = cblk * kStepCols + j;
+  const int col0 = cblk * kStepCols + 4 * q;
   float* S = a.S + (size_t)head * D * d;
   float* z = a.z + (size_t)head * D;
   const float* PQ = a.phiq + (size_t)head * m * D;
@@ -48,52 +51,77 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   const T* V = reinterpret_cast<const T*>(a.V) + (size_t)head * m * d;
   T* out = reinterpret_cast<T*>(a.out) + (size_t)head * m * d;
 
-  float s[kStepFeat], zz[kStepFeat];
+  float4 s[kStepFeat];
+  float zz[kStepFeat];
 #pragma unroll
   for (int i = 0; i < kStepFeat; ++i) {
     const int f = grp + kStepGroups * i;
-    s[i] = f < D ? S[(size_t)f * d + col] : 0.0f;
+    s[i] = f < D ? *reinterpret_cast<const float4*>(&S[(size_t)f * d + col0]) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     zz[i] = f < D ? z[f] : 0.0f;
   }
 
   for (int t0 = 0; t0 < m; t0 += kStepTokens) {
     const int tn = min(kStepTokens, m - t0);
-    __syncthreads();  // the previous stage's features are no longer read
-    for (int idx = threadIdx.x; idx < kStepTokens * kStepMaxD; idx += blockDim.x) {
+    __syncthreads();  // the previous stage's tokens are no longer read
+    // features past D and tokens past the step stage as zeros
+    for (int idx = tid; idx < kStepTokens * kStepMaxD; idx += blockDim.x) {
       const int tt = idx / kStepMaxD, f = idx % kStepMaxD;
       const bool ok = tt < tn && f < D;
       sq[tt][f] = ok ? PQ[(size_t)(t0 + tt) * D + f] : 0.0f;
       sk[tt][f] = ok ? PK[(size_t)(t0 + tt) * D + f] : 0.0f;
     }
-    float vv[kStepTokens];
-#pragma unroll
-    for (int tt = 0; tt < kStepTokens; ++tt) vv[tt] = tt < tn ? (float)V[(size_t)(t0 + tt) * d + col] : 0.0f;
+    for (int idx = tid; idx < kStepTokens * kStepCols; idx += blockDim.x) {
+      const int tt = idx / kStepCols, c = idx % kStepCols;
+      sv[tt][c] = tt < tn ? (float)V[(size_t)(t0 + tt) * d + cblk * kStepCols + c] : 0.0f;
+    }
     __syncthreads();
 #pragma unroll
     for (int tt = 0; tt < kStepTokens; ++tt) {
       if (tt < tn) {  // (uniform)
-        float num = 0.0f, den = 0.0f;
+        const float4 v = *reinterpret_cast<const float4*>(&sv[tt][4 * q]);
+        float4 num = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        float den = 0.0f;
 #pragma unroll
         for (int i = 0; i < kStepFeat; ++i) {
           const int f = grp + kStepGroups * i;
           const float kf = sk[tt][f], qf = sq[tt][f];
-          s[i] = fmaf(kf, vv[tt], s[i]);
+          s[i].x = fmaf(kf, v.x, s[i].x);
+          s[i].y = fmaf(kf, v.y, s[i].y);
+          s[i].z = fmaf(kf, v.z, s[i].z);
+          s[i].w = fmaf(kf, v.w, s[i].w);
           zz[i] += kf;
-          num = fmaf(qf, s[i], num);
+          num.x = fmaf(qf, s[i].x, num.x);
+          num.y = fmaf(qf, s[i].y, num.y);
+          num.z = fmaf(qf, s[i].z, num.z);
+          num.w = fmaf(qf, s[i].w, num.w);
           den = fmaf(qf, zz[i], den);
         }
+        // the eight groups of this wave (lane bits 3..5)
+#pragma unroll
+        for (int off = kStepQuads; off < kWave; off *= 2) {
+          num.x += __shfl_xor(num.x, off);
+          num.y += __shfl_xor(num.y, off);
+          num.z += __shfl_xor(num.z, off);
+          num.w += __shfl_xor(num.w, off);
+          den += __shfl_xor(den, off);
+        }
         const int b = (t0 + tt) & 1;  // alternating buffers: one barrier per token
-        red[b][grp][j] = num;
-        if (j == 0) red[b][grp][kStepCols] = den;
+        if (lane < kStepQuads) {
+          red[b][wave][q][0] = num.x;
+          red[b][wave][q][1] = num.y;
+          red[b][wave][q][2] = num.z;
+          red[b][wave][q][3] = num.w;
+          red[b][wave][q][4] = den;
+        }
         __syncthreads();
-        if (grp == 0) {
+        if (tid < kStepCols) {
           float nu = 0.0f, de = 0.0f;
 #pragma unroll
-          for (int g2 = 0; g2 < kStepGroups; ++g2) {
-            nu += red[b][g2][j];
-            de += red[b][g2][kStepCols];
+          for (int w = 0; w < 4; ++w) {
+            nu += red[b][w][tid / 4][tid % 4];
+            de += red[b][w][tid / 4][4];
           }
-          out[(size_t)(t0 + tt) * d + col] = (T)(nu / (de + a.eps));
+          out[(size_t)(t0 + tt) * d + cblk * kStepCols + tid] = (T)(nu / (de + a.eps));
         }
       }
     }
@@ -103,8 +131,8 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   for (int i = 0; i < kStepFeat; ++i) {
     const int f = grp + kStepGroups * i;
     if (f < D) {
-      S[(size_t)f * d + col] = s[i];
-      if (cblk == 0 && j == 0) z[f] = zz[i];  // every column block carries the same z
+      *reinterpret_cast<float4*>(&S[(size_t)f * d + col0]) = s[i];
+      if (cblk == 0 && q == 0) z[f] = zz[i];  // every column block carries the same z
     }
   }
 }

@@ -62,8 +62,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.luna_attn_fwd_causal.restype = i32
     lib.luna_attn_state.argtypes = [vp, vp, i32, i64, i64, i64, i64, P, i32, vp, vp, vp, sz, vp]
     lib.luna_attn_state.restype = i32
-    lib.luna_attn_causal_step.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, vp, vp, vp, vp,
-                                          sz, vp]
+    lib.luna_attn_causal_step.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, i32, vp, vp, vp,
+                                          vp, sz, vp]
     lib.luna_attn_causal_step.restype = i32
     lib.luna_status_string.argtypes = [i32]
     lib.luna_status_string.restype = ctypes.c_char_p
@@ -269,13 +269,41 @@ def attn_causal_step(Q, K, V, p: PhiParams, S, z, eps: float = 1e-6, out=None):
     nb = lib.luna_workspace_bytes(OP_CAUSAL_STEP, dt, B, H, m, d, ctypes.byref(pc), 64)
     if nb == 0:
         _check(lib.luna_attn_causal_step(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, m, d,
-                                         ctypes.byref(pc), eps, S.data_ptr(), z.data_ptr(), out.data_ptr(), None, 0,
-                                         None))
+                                         ctypes.byref(pc), eps, 0, S.data_ptr(), z.data_ptr(), out.data_ptr(), None,
+                                         0, None))
     ws, wsp, wsn = _workspace(nb, Q.device)
     _check(lib.luna_attn_causal_step(Q.data_ptr(), K.data_ptr(), V.data_ptr(), dt, B, H, m, d, ctypes.byref(pc), eps,
-                                     S.data_ptr(), z.data_ptr(), out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
+                                     0, S.data_ptr(), z.data_ptr(), out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
     out._luna_ws = ws
     return out
+
+
+class StepPlan:
+    """Streaming steps of m tokens per head with one persistent workspace: the first
+    ``run`` builds the channel tables in it, later ones reuse them (tables_ready = 1).
+    The parameters must stay unchanged between runs."""
+
+    def __init__(self, p: PhiParams, B: int, H: int, m: int, d: int, dtype, device, eps: float = 1e-6):
+        self.lib = load_library()
+        self.p, self.pc = p, p.c()
+        self.B, self.H, self.m, self.d, self.eps = B, H, m, d, float(eps)
+        self.dt = LUNA_BF16 if str(dtype).endswith("bfloat16") else LUNA_F32
+        nb = self.lib.luna_workspace_bytes(OP_CAUSAL_STEP, self.dt, B, H, m, d, ctypes.byref(self.pc), 64)
+        if nb == 0:
+            raise LunaError(LUNA_ERR_UNSUPPORTED, "no streaming step for this problem")
+        self.ws, self.wsp, self.wsn = _workspace(nb, device)
+        self.tables_ready = 0
+
+    def run(self, Q, K, V, S, z, out, stream=None):
+        if _qkv_shape(Q, K, V) != (self.B, self.H, self.m, self.d) or _dt(Q) != self.dt:
+            raise LunaError(LUNA_ERR_INVALID_ARG, "Q, K, V do not match the plan")
+        _state_tensors(self.B, self.H, self.p.M * self.p.L, self.d, Q.device, S, z)
+        s = stream if stream is not None else _stream_ptr(Q.device)
+        _check(self.lib.luna_attn_causal_step(Q.data_ptr(), K.data_ptr(), V.data_ptr(), self.dt, self.B, self.H,
+                                              self.m, self.d, ctypes.byref(self.pc), self.eps, self.tables_ready,
+                                              S.data_ptr(), z.data_ptr(), out.data_ptr(), self.wsp, self.wsn, s))
+        self.tables_ready = 1
+        return out
 
 
 class Plan:

@@ -95,12 +95,13 @@ def test_state_and_step_reject(lib):
     assert st(p=_params(L=3)) == luna.LUNA_ERR_UNSUPPORTED
     stp = lambda **kw: lib.luna_attn_causal_step(FAKE, FAKE, FAKE, luna.LUNA_BF16, 2, 3, kw.get("m", 4), 64,
                                                  ctypes.byref(kw.get("p", p)), kw.get("eps", 1e-6),
-                                                 kw.get("S", FAKE), FAKE, kw.get("out", FAKE), FAKE,
-                                                 kw.get("ws_bytes", 1 << 40), None)
+                                                 kw.get("ready", 0), kw.get("S", FAKE), FAKE, kw.get("out", FAKE),
+                                                 FAKE, kw.get("ws_bytes", 1 << 40), None)
     assert stp(S=0) == luna.LUNA_ERR_INVALID_ARG
     assert stp(out=0) == luna.LUNA_ERR_INVALID_ARG
     assert stp(eps=-1.0) == luna.LUNA_ERR_INVALID_ARG
     assert stp(m=0) == luna.LUNA_ERR_INVALID_ARG
+    assert stp(ready=2) == luna.LUNA_ERR_INVALID_ARG
     assert stp(ws_bytes=256) == luna.LUNA_ERR_WORKSPACE
     assert stp(p=_params(L=3)) == luna.LUNA_ERR_UNSUPPORTED
     assert lib.luna_last_error()

@@ -122,3 +122,24 @@ def test_step_rejects_bad_state():
         luna.attn_causal_step(Qt, Kt, Vt, pt, S[:, :, :64].contiguous(), z, eps=w.eps)
     with pytest.raises(luna.LunaError):
         luna.attn_causal_step(Qt, Kt, Vt, pt, S.half(), z, eps=w.eps)
+
+
+def test_step_plan_reuses_tables():
+    """Steps through a plan (tables built by the first call, reused after) give the
+    same bits as steps that build the tables every time."""
+    import torch
+    w = small_workload("bf16", B=2, H=3, n=12, d=128, M=32, L=8, causal=True)
+    Q, K, V, p = inputs(w, seed=19)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    D = 256
+    Sa = torch.zeros((2, 3, D, 128), dtype=torch.float32, device="cuda")
+    za = torch.zeros((2, 3, D), dtype=torch.float32, device="cuda")
+    Sb, zb = Sa.clone(), za.clone()
+    plan = luna.StepPlan(pt, 2, 3, 4, 128, torch.bfloat16, Qt.device, eps=w.eps)
+    for a in range(0, 12, 4):
+        sl = lambda X: X[:, :, a:a + 4].contiguous()  # noqa: E731
+        oa = luna.attn_causal_step(sl(Qt), sl(Kt), sl(Vt), pt, Sa, za, eps=w.eps)
+        ob = plan.run(sl(Qt), sl(Kt), sl(Vt), Sb, zb, torch.empty_like(sl(Qt)))
+        assert torch.equal(oa, ob)
+    assert torch.equal(Sa, Sb) and torch.equal(za, zb)
+    assert plan.tables_ready == 1

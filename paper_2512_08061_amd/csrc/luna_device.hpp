@@ -100,6 +100,53 @@ __device__ inline void copy16_rows(void* dst, int dst_row16, const void* src, in
   }
 }
 
+// One round of loads for n16 16-byte chunks: every thread issues all its loads
+// (kTabBatch per round, indices clamped so that none is conditional) before it stores
+// any.  ld(i) reads chunk i, st(i, v) writes it.
+constexpr int kTabBatch = 16;
+template <typename LD, typename ST>
+__device__ inline void batched_copy(int n16, LD ld, ST st) {
+  const int nt = blockDim.x;
+  for (int base = threadIdx.x; base < n16; base += kTabBatch * nt) {
+    uint4 v[kTabBatch];
+#pragma unroll
+    for (int u = 0; u < kTabBatch; ++u) v[u] = ld(min(base + u * nt, n16 - 1));
+#pragma unroll
+    for (int u = 0; u < kTabBatch; ++u)
+      if (base + u * nt < n16) st(base + u * nt, v[u]);
+  }
+}
+
+// The bucket windows and NROWS coefficient rows (SRC16 chunks each in global memory,
+// DST16 in LDS) of a table, plus PRE leading chunks of keys, in one round of loads.
+// The loads cover the capacities, not the table's own counts, so that none waits for
+// the header; only the first rows_kept rows are stored (the caller writes the row
+// after them).
+template <int PRE, int NROWS, int SRC16, int DST16>
+__device__ inline void copy_table_regions(void* keys_dst, void* bk_dst, void* seg_dst, const uint8_t* gtab,
+                                          size_t seg_off, int rows_kept) {
+  constexpr int NB = (kNumBuckets * 2 + 15) / 16;
+  const uint4* gk = reinterpret_cast<const uint4*>(gtab + kTabKeys);
+  const uint4* gb = reinterpret_cast<const uint4*>(gtab + kTabBuckets);
+  const uint4* gs = reinterpret_cast<const uint4*>(gtab + seg_off);
+  uint4* kd = reinterpret_cast<uint4*>(keys_dst);
+  uint4* bd = reinterpret_cast<uint4*>(bk_dst);
+  uint4* sd = reinterpret_cast<uint4*>(seg_dst);
+  batched_copy(
+      PRE + NB + NROWS * SRC16,
+      [&](int i) { return i < PRE ? gk[i] : (i < PRE + NB ? gb[i - PRE] : gs[i - PRE - NB]); },
+      [&](int i, uint4 v) {
+        if (i < PRE) {
+          kd[i] = v;
+        } else if (i < PRE + NB) {
+          bd[i - PRE] = v;
+        } else {
+          const int j = i - PRE - NB;
+          if (j / SRC16 < rows_kept) sd[(j / SRC16) * DST16 + j % SRC16] = v;  // (the rest may be written after)
+        }
+      });
+}
+
 // Cooperative copy of a table from global memory into LDS.  Caller syncs after.
 template <int L, int NSEG>
 __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
@@ -108,11 +155,13 @@ __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ 
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const float2* gseg = reinterpret_cast<const float2*>(gtab + kTabSeg);
-  copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
-  copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
+  static_assert(NSEG * L <= kSegCap, "the LDS rows must lie inside the table's segment region");
   if constexpr ((L * 8) % 16 == 0) {
-    copy16_rows(&t.seg[0][0], sizeof(t.seg[0]) / 16, gseg, L * 8 / 16, nseg);
+    copy_table_regions<kKeyCap / 4, NSEG, L * 8 / 16, sizeof(t.seg[0]) / 16>(t.keys, t.buckets, &t.seg[0][0], gtab,
+                                                                             kTabSeg, nseg);
   } else {
+    copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
+    copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
     for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   }
   // one all-zero segment after the real ones: masked values select it and evaluate
@@ -148,11 +197,13 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const half2_t* gseg = reinterpret_cast<const half2_t*>(gtab + kTabSeg16);
-  copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
-  copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
+  static_assert(NSEG * L <= kSegCap, "the LDS rows must lie inside the table's segment region");
   if constexpr ((L * 4) % 16 == 0) {
-    copy16_rows(&t.seg[0][0], sizeof(t.seg[0]) / 16, gseg, L * 4 / 16, nseg);
+    copy_table_regions<kKeyCap / 4, NSEG, L * 4 / 16, sizeof(t.seg[0]) / 16>(t.keys, t.buckets, &t.seg[0][0], gtab,
+                                                                             kTabSeg16, nseg);
   } else {
+    copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
+    copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
     for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   }
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
@@ -453,12 +504,29 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
   // groups 4m .. 4m + 3 from the aligned key quads m and m + 1 (+inf past the stored keys)
   static_assert((kKeyCap + 8) % 4 == 0, "whole quads of groups");
   const float kInf = __builtin_inff();
-  for (int m = threadIdx.x; m < (kKeyCap + 8) / 4; m += blockDim.x) {
+  constexpr int kGroups = (kKeyCap + 8) / 4;
+  // this thread's first node group's key quads, loaded before the other regions'
+  // round of loads so that they arrive together
+  const float4* gq = reinterpret_cast<const float4*>(gkeys);
+  const int m0 = threadIdx.x;
+  const float4 q0 = gq[min(m0, kKeyCap / 4 - 1)], q1 = gq[min(m0 + 1, kKeyCap / 4 - 1)];
+  constexpr int kPair = sizeof(RowT);
+  static_assert(NSEG * L <= kSegCap, "the LDS rows must lie inside the table's segment region");
+  if constexpr ((L * kPair) % 16 == 0) {
+    copy_table_regions<0, NSEG, L * kPair / 16, sizeof(t.seg[0]) / 16>(nullptr, t.buckets, &t.seg[0][0], gtab,
+                                                                       Tab::kHalf ? kTabSeg16 : kTabSeg, nseg);
+  } else {
+    copy16(t.buckets, gtab + kTabBuckets, (kNumBuckets * 2 + 15) / 16);
+    for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
+  }
+  // groups 4m .. 4m + 3 from the aligned key quads m and m + 1 (+inf past the stored keys)
+  for (int m = m0; m < kGroups; m += blockDim.x) {
     float k[8];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int q = m + h;  // key quad
-      const float4 v = 4 * q < kKeyCap ? reinterpret_cast<const float4*>(gkeys)[q] : make_float4(kInf, kInf, kInf, kInf);
+      float4 v = m == m0 ? (h == 0 ? q0 : q1) : gq[min(q, kKeyCap / 4 - 1)];
+      if (4 * q >= kKeyCap) v = make_float4(kInf, kInf, kInf, kInf);
       k[4 * h + 0] = v.x; k[4 * h + 1] = v.y; k[4 * h + 2] = v.z; k[4 * h + 3] = v.w;
     }
 #pragma unroll
@@ -466,13 +534,6 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
       if (4 * m + e >= hd.nkeys) k[e] = kInf;
 #pragma unroll
     for (int e = 0; e < 4; ++e) t.nodes[4 * m + e] = make_float4(k[e], k[e + 1], k[e + 2], k[e + 3]);
-  }
-  copy16(t.buckets, gtab + kTabBuckets, (kNumBuckets * 2 + 15) / 16);
-  constexpr int kPair = sizeof(RowT);
-  if constexpr ((L * kPair) % 16 == 0) {
-    copy16_rows(&t.seg[0][0], sizeof(t.seg[0]) / 16, gseg, L * kPair / 16, nseg);
-  } else {
-    for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   }
   // one all-zero segment after the real ones: masked values select it and evaluate
   // to exactly 0 without per-element masks

@@ -17,86 +17,97 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   __shared__ PwlLds<L, nseg_cap(L, kFmSegBytes)> tab;
 
   const int tiles_per_head = (int)((a.rows_per_head + 63) / 64);
-  // with a second input the grid is doubled: its second half maps X2 into out2
-  int64_t bid = blockIdx.x;
-  const void* Xsrc = a.X;
-  void* Odst = a.out;
-  if (bid >= a.heads * tiles_per_head) {
-    bid -= a.heads * tiles_per_head;
-    Xsrc = a.X2;
-    Odst = a.out2;
-  }
-  const int64_t head = bid / tiles_per_head;
-  const int tile = (int)(bid - head * tiles_per_head);
-  const int hset = a.phi.per_head ? (int)(head % a.H) : 0;
+  // work items: 64-row tiles of every head; with a second input the items double and
+  // the second half maps X2 into out2.  A workgroup takes items blockIdx.x,
+  // blockIdx.x + gridDim.x, ..., so that its table copy serves many tiles.
+  const int64_t per_input = a.heads * tiles_per_head;
+  const int64_t items = per_input * (a.X2 != nullptr ? 2 : 1);
+  int loaded = -1;
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    int64_t bid = item;
+    const void* Xsrc = a.X;
+    void* Odst = a.out;
+    if (bid >= per_input) {
+      bid -= per_input;
+      Xsrc = a.X2;
+      Odst = a.out2;
+    }
+    const int64_t head = bid / tiles_per_head;
+    const int tile = (int)(bid - head * tiles_per_head);
+    const int hset = a.phi.per_head ? (int)(head % a.H) : 0;
 
-  const int wave = wave_id(), lane = threadIdx.x % kWave;
-  const int g = lane / 16, r = lane % 16;
-  const int64_t n = a.rows_per_head;
-  const int64_t t = (int64_t)tile * 64 + wave * 16 + r;  // this lane's row (B column)
-  const bool row_ok = t < n;
-  const int M = a.phi.M;
-  const int D = M * L;
-  const Tin* X = reinterpret_cast<const Tin*>(Xsrc) + (head * n + (row_ok ? t : 0)) * DH;
-  const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
-  const float* bias = a.phi.b + (size_t)hset * M;
-  Tout* out = reinterpret_cast<Tout*>(Odst) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
+    const int wave = wave_id(), lane = threadIdx.x % kWave;
+    const int g = lane / 16, r = lane % 16;
+    const int64_t n = a.rows_per_head;
+    const int64_t t = (int64_t)tile * 64 + wave * 16 + r;  // this lane's row (B column)
+    const bool row_ok = t < n;
+    const int M = a.phi.M;
+    const int D = M * L;
+    const Tin* X = reinterpret_cast<const Tin*>(Xsrc) + (head * n + (row_ok ? t : 0)) * DH;
+    const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
+    const float* bias = a.phi.b + (size_t)hset * M;
+    Tout* out = reinterpret_cast<Tout*>(Odst) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
 
-  // the row, W fragments and biases are fetched before the table, so that their
-  // loads overlap its copy
-  constexpr int kMaxMB = 4;  // M <= 64
-  const int MB = (M + 15) / 16;
-  Frag<Tin> xf[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    if (row_ok) load8(xf[ks], X + 32 * ks + 8 * g);
-    else xf[ks].zero();
-  }
-  Frag<Tin> wfr[kMaxMB][KS];
-  float bz[kMaxMB][4];
-#pragma unroll
-  for (int mb = 0; mb < kMaxMB; ++mb) {
-    const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
+    // the row, W fragments and biases are fetched before the table, so that their
+    // loads overlap its copy
+    constexpr int kMaxMB = 4;  // M <= 64
+    const int MB = (M + 15) / 16;
+    Frag<Tin> xf[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      if (mb < MB && prow < M) load8(wfr[mb][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
-      else wfr[mb][ks].zero();
+      if (row_ok) load8(xf[ks], X + 32 * ks + 8 * g);
+      else xf[ks].zero();
     }
+    Frag<Tin> wfr[kMaxMB][KS];
+    float bz[kMaxMB][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
-      bz[mb][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
+    for (int mb = 0; mb < kMaxMB; ++mb) {
+      const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (mb < MB && prow < M) load8(wfr[mb][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
+        else wfr[mb][ks].zero();
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
+        bz[mb][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
+      }
     }
-  }
-  pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
-  __syncthreads();
-  const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
-  const float floor = tab.floor;
+    if (hset != loaded) {  // (uniform) a workgroup loads a table once per parameter set it meets
+      __syncthreads();     // every wave is done with the previous table
+      pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+      __syncthreads();
+      loaded = hset;
+    }
+    const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
+    const float floor = tab.floor;
 
 #pragma unroll
-  for (int mb = 0; mb < kMaxMB; ++mb) {
-    if (mb >= MB) break;
-    f32x4 acc = zero4();
+    for (int mb = 0; mb < kMaxMB; ++mb) {
+      if (mb >= MB) break;
+      f32x4 acc = zero4();
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mb][ks], xf[ks]);
-    float uu[4];
+      for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mb][ks], xf[ks]);
+      float uu[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) uu[j] = acc[j] + bz[mb][j];
-    int sg[4];
-    pwl_search(tab, steps, uu, sg);
+      for (int j = 0; j < 4; ++j) uu[j] = acc[j] + bz[mb][j];
+      int sg[4];
+      pwl_search(tab, steps, uu, sg);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = 16 * mb + 4 * g + j;
-      if (i < M && row_ok) {
-        float y[L];
-        pwl_channels<L>(tab, sg[j], floor, uu[j], y);
-        Tout* o = out + i * L;
-        if constexpr (L % 4 == 0) {
+      for (int j = 0; j < 4; ++j) {
+        const int i = 16 * mb + 4 * g + j;
+        if (i < M && row_ok) {
+          float y[L];
+          pwl_channels<L>(tab, sg[j], floor, uu[j], y);
+          Tout* o = out + i * L;
+          if constexpr (L % 4 == 0) {
 #pragma unroll
-          for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
-        } else {
+            for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
+          } else {
 #pragma unroll
-          for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
+            for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
+          }
         }
       }
     }
@@ -105,8 +116,10 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
 
 template <typename Tin, typename Tout, int DH>
 static hipError_t fm_dispatch_L(int L, const FeatureMapArgs& a, hipStream_t s) {
-  const int tiles = (int)((a.rows_per_head + 63) / 64);
-  const dim3 grid((unsigned)(a.heads * tiles * (a.X2 != nullptr ? 2 : 1))), block(256);
+  const int64_t tiles = (a.rows_per_head + 63) / 64;
+  const int64_t items = a.heads * tiles * (a.X2 != nullptr ? 2 : 1);
+  // three workgroups per CU fit next to their LDS tables; more items loop
+  const dim3 grid((unsigned)(items < 768 ? items : 768)), block(256);
   switch (L) {
     case 1: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 1>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 2>), grid, block, 0, s, a); break;

@@ -114,6 +114,10 @@ __device__ __forceinline__ constexpr int feat(int p, int l) {
 __device__ __forceinline__ constexpr int krow(int f) {
   return (f & ~31) | (f & 3) | ((f >> 1) & 12) | ((f << 2) & 16);
 }
+// The feature held in row rho (the inverse of krow).
+__device__ __forceinline__ constexpr int krow_inv(int rho) {
+  return (rho & ~31) | (rho & 3) | ((rho << 1) & 24) | ((rho >> 2) & 4);
+}
 
 // V: transpose reads of four (and eight) consecutive rows.
 template <int CPR>
@@ -467,12 +471,13 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       }
       if constexpr (decltype(qlive)::value) eval_all(phq_r, uq, oq, tfloor);
       eval_all(phk_r, uk, ok, tfloor);
-      add_z();
+      if constexpr (!ST) add_z();  // (the state launch's z comes from matrix wave 0)
     };
     if constexpr (ST) {
-      // State launch: every chunk is state-only.  z is only kept in registers; it is
-      // written once, for the state piece, after the last chunk.  (Mapping the key
-      // rows of two chunks as one batch made this launch slower: 186 against 159 us.)
+      // State launch: every chunk is state-only; z is summed by matrix wave 0 along
+      // with its slice of S (one-hot products here would lengthen the map waves'
+      // chain, which sets this launch's pace).  (Mapping the key rows of two chunks as
+      // one batch made this launch slower: 186 against 159 us.)
       map_rows(std::false_type{}, c_first);
       load_rows(xq, a.Q, c_first + 1, false);
       load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
@@ -493,7 +498,6 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         }
         load_v(cn + 1);
       }
-      write_z();  // z through the piece's last chunk, summed after the final barrier
     } else {
       // chunk c_first
       if (c_first >= c_begin) map_rows(std::true_type{}, c_first);
@@ -554,6 +558,12 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
                                         : sm.phk + 4 * g * SK + i16 * SZ;
     const T* zs0 = &sm.zs[0][8 * g];
     f32x4 sacc[CBW][RB];
+    // state launch: z of the chunks, summed by matrix wave 0 from its phi(K)^T fragments
+    f32x4 zst[ST ? RB : 1];
+#pragma unroll
+    for (int i = 0; i < (ST ? RB : 1); ++i) zst[i] = zero4();
+    Frag<T> ones;
+    ones.fill(1.0f);
     // the state piece layout: S tile (x, b) of matrix wave mw at (mw CBW + x) RB + b,
     // lane-major 16-byte entries
     const size_t s_off = ((size_t)mw * CBW * RB * kWave + lane) * 4;
@@ -778,6 +788,8 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
           if (idx + kPre < 2 * RB) ka_read(kb[idx % kPre], idx + kPre);
 #pragma unroll
           for (int x = 0; x < CBW; ++x) mma(sacc[x][idx / 2], ka, vf[x][idx % 2]);
+          if constexpr (ST)
+            if (mw == 0) mma(zst[idx / 2], ka, ones);  // z: every column of the tile is z
         }
       }
       __syncthreads();  // B2: P and the den parts are in LDS
@@ -808,18 +820,22 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         }
       }
     }
-    if (ST && active) {  // (every wave goes on to the final barrier)
+    if (ST && active) {
       float* so = a.state_out + (size_t)(head * a.pieces + part) * C::STATE + s_off;
 #pragma unroll
       for (int x = 0; x < CBW; ++x)
 #pragma unroll
         for (int i = 0; i < RB; ++i) *reinterpret_cast<f32x4*>(so + (size_t)(x * RB + i) * kWave * 4) = sacc[x][i];
+      if constexpr (ST) {
+        if (mw == 0 && r == 0) {  // z of the piece, by internal feature
+          float* zo = a.state_out + (size_t)(head * a.pieces + part) * C::STATE + C::SF;
+#pragma unroll
+          for (int b = 0; b < RB; ++b)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) zo[krow_inv(16 * b + 4 * g + jj)] = zst[b][jj];
+        }
+      }
     }
-  }
-  if constexpr (ST) {
-    __syncthreads();  // every map wave's part of z through the piece's last chunk is in zp
-    float* so = a.state_out + (size_t)(head * a.pieces + part) * C::STATE + C::SF;
-    for (int f = tid; f < FP; f += C::NT) so[f] = ((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f];
   }
 }
 

@@ -393,6 +393,20 @@ def test_options_per_head_shared_signed(causal):
     assert_close(phi, oracle.featuremap(Q, p), "bf16", "phi options")
 
 
+@pytest.mark.parametrize("per_head", [False, True])
+def test_featuremap_many_tiles(per_head):
+    """More 64-row tiles than workgroups (each workgroup loops over tiles, loading a
+    table when the parameter set changes): 313 tiles per head, six heads; checked on
+    sampled rows of every head."""
+    w = small_workload("bf16", B=2, H=3, n=20000, d=64, M=16, L=8, per_head=per_head)
+    say(f"featuremap many tiles per_head={per_head}")
+    Q, K, V, p = inputs(w, seed=8)
+    (Xt,), pt = upload(w, [Q], p)
+    phi = to_np(luna.featuremap(Xt, pt))
+    rows = np.concatenate([np.arange(0, 20000, 97), [19999]])
+    assert_close(phi[:, :, rows], oracle.featuremap(Q[:, :, rows], p), "bf16", "phi sampled")
+
+
 def test_nan_propagates():
     w = small_workload("f32", B=1, H=1, n=130, d=32, M=8, L=8)
     Q, K, V, p = inputs(w, seed=8)

@@ -7,7 +7,7 @@
 //           Each wave sums its share of S and z over the head's keys in registers,
 //           the four shares are added in LDS in a fixed order and turned into
 //           readout fragments, and the same workgroup then streams the head's
-//           queries in groups of four 16-token blocks.  S never reaches HBM; the
+//           queries in groups of two 16-token blocks.  S never reaches HBM; the
 //           launch is bound by issue of the feature-map arithmetic, not by HBM.
 //  split    (fewer heads) the three passes below, so that a head's keys and
 //           queries are spread over many workgroups.
@@ -616,7 +616,7 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
   // wait for a load also waits for every store issued before it: the group's outputs
   // are kept until its end and stored after an explicit wait for the next group's
   // rows, so that no wait has to cover stores issued just before it.
-  constexpr int NB = 4;
+  constexpr int NB = 2;
   Frag<T> qf[NB][C::KS];
   auto fetch_q = [&](Frag<T> (&qf)[C::KS], int b) {
     const auto rs = rows_rsrc(Q, 16 * b, 16, n, DH, (int)sizeof(T));

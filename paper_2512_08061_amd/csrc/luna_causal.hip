@@ -14,7 +14,9 @@
 // two launches: the state launch (a separate instantiation, ST) sums the state of
 // [0, x) in pieces, one workgroup per (head, piece), and writes them in fp32; the scan
 // launch then runs part 0 over [0, x) from a zero state and part 1 over [x, n) from
-// the sum of the pieces.  No workgroup waits for another.
+// the sum of the pieces.  No workgroup waits for another.  Run over every chunk (key
+// rows past n mapped to the all-zero segment), the state launch also gives the state
+// of a whole sequence, which causal_state_export_kernel writes in the public layout.
 //
 // Roles.  Four matrix waves and four map waves, one of each on every SIMD, so that
 // each SIMD pairs matrix-core work with vector and table-lookup work.

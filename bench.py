@@ -223,10 +223,21 @@ def decode_bench(args) -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    run = step
+    if args.graph:  # one call captured (the tables are built by then), replayed
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            plan.run(new[0], new[1], new[2], S, z, out)
+        torch.cuda.synchronize()
+        run = g.replay
+        stream = torch.cuda.current_stream(dev)
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
-        step()
+        run()
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
@@ -248,12 +259,14 @@ def decode_bench(args) -> int:
         "dtype": "bf16",
         "data": "synthetic (seeded)",
         "config": {"workload": f"streaming step of {m} token(s) per head after a 16384-token prefix, "
-                               "B=8 H=16 d=128 M=32 L=8 (D=256), bf16, fp32 state", "m": m},
+                               "B=8 H=16 d=128 M=32 L=8 (D=256), bf16, fp32 state", "m": m,
+                   "graph": bool(args.graph)},
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "causal_step_kernel",
                      "bytes_per_call": state_bytes + io_bytes,
-                     "timing": "HIP events around the ABI calls (tables built by the first, reused after): "
-                               "one feature-map launch for the new queries and keys, then the step kernel"},
+                     "timing": ("replays of a HIP graph holding one call" if args.graph else
+                                "HIP events around the ABI calls (tables built by the first, reused after)") +
+                               ": one feature-map launch for the new queries and keys, then the step kernel"},
     }
     print(json.dumps(line), flush=True)
     return 0
@@ -275,6 +288,8 @@ def main() -> int:
                     help="summarise two rocprofv3 --pmc csv runs into profiles/hbm_traffic_*.json and exit")
     ap.add_argument("--traffic-command", default="",
                     help="the rocprofv3 commands that produced --traffic-from, recorded in the summary")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --decode: capture one streaming call in a HIP graph and time its replays")
     ap.add_argument("--decode", type=int, default=0, metavar="M",
                     help="instead of the hot-path step: time streaming steps of M new tokens per head "
                          "(luna_attn_causal_step) on the long causal problem's shape, after the state of "

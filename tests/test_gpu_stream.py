@@ -143,3 +143,38 @@ def test_step_plan_reuses_tables():
         assert torch.equal(oa, ob)
     assert torch.equal(Sa, Sb) and torch.equal(za, zb)
     assert plan.tables_ready == 1
+
+
+def test_step_graph_replays():
+    """A streaming call captured in a HIP graph (tables already built) and replayed
+    advances the state exactly as eager calls do, replay after replay, with eager
+    work and synchronisations between the replays."""
+    import torch
+    w = small_workload("bf16", B=2, H=3, n=4, d=128, M=32, L=8, causal=True)
+    Q, K, V, p = inputs(w, seed=23)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    D = 256
+    S0 = torch.randn((2, 3, D, 128), device="cuda") * 0.1
+    z0 = torch.rand((2, 3, D), device="cuda") + 1.0
+    Se, ze = S0.clone(), z0.clone()
+    Sg, zg = S0.clone(), z0.clone()
+    plan_e = luna.StepPlan(pt, 2, 3, 4, 128, torch.bfloat16, Qt.device, eps=w.eps)
+    plan_g = luna.StepPlan(pt, 2, 3, 4, 128, torch.bfloat16, Qt.device, eps=w.eps)
+    out_g = torch.empty_like(Qt)
+    # first call outside the graph: it builds the tables
+    Sw, zw = Sg.clone(), zg.clone()
+    plan_g.run(Qt, Kt, Vt, Sw, zw, torch.empty_like(Qt))
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        plan_g.run(Qt, Kt, Vt, Sg, zg, out_g)
+    torch.cuda.synchronize()
+    Sg.copy_(S0)
+    zg.copy_(z0)
+    for rep in range(4):
+        out_e = plan_e.run(Qt, Kt, Vt, Se, ze, torch.empty_like(Qt))
+        graph.replay()
+        torch.cuda.synchronize()
+        _ = (Qt.float() * 2).sum().item()  # eager work between replays
+        assert torch.equal(out_g, out_e), f"replay {rep}: output"
+        assert torch.equal(Sg, Se) and torch.equal(zg, ze), f"replay {rep}: state"

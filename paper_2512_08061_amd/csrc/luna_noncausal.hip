@@ -234,18 +234,14 @@ __global__ __launch_bounds__(256, 1) void nc_state_kernel(NoncausalArgs a) {
 template <typename T, int DH, int L, int MB>
 __global__ __launch_bounds__(256) void nc_reduce_kernel(NoncausalArgs a) {
   using C = NcCfg<T, DH, L, MB>;
-  __shared__ float red[C::DP * (DH + 1)];
+  // blockIdx.y: a slice of the head's fragment elements; every element sums its own
+  // partials in range order (deterministic), so the slices need no exchange
   const int head = blockIdx.x;
   const float* part = a.partial + (size_t)head * a.splits * C::DP * (DH + 1);
-  for (int i = threadIdx.x; i < C::DP * (DH + 1); i += blockDim.x) {
-    float s = 0.0f;
-    for (int sp = 0; sp < a.splits; ++sp) s += part[(size_t)sp * C::DP * (DH + 1) + i];
-    red[i] = s;
-  }
-  __syncthreads();
   T* fr = reinterpret_cast<T*>(a.frags) + (size_t)head * C::FRAG_ELEMS;
   // fragment (cb, kappa), lane (g, r), slot e; cb == CB holds z
-  for (size_t idx = threadIdx.x; idx < C::FRAG_ELEMS; idx += blockDim.x) {
+  for (size_t idx = (size_t)blockIdx.y * blockDim.x + threadIdx.x; idx < C::FRAG_ELEMS;
+       idx += (size_t)gridDim.y * blockDim.x) {
     const int e = (int)(idx % 8);
     const int lane = (int)((idx / 8) % kWave);
     const int kappa = (int)((idx / (8 * kWave)) % C::NF);
@@ -257,7 +253,8 @@ __global__ __launch_bounds__(256) void nc_reduce_kernel(NoncausalArgs a) {
       const int mbj = p / L, l = p % L;
       const int mb = mbj / 4, j = mbj % 4;
       const int row = (mb * L + l) * 16 + 4 * g + j;
-      v = (cb < C::CB) ? red[row * (DH + 1) + 16 * cb + r] : red[row * (DH + 1) + DH];
+      const int src = row * (DH + 1) + (cb < C::CB ? 16 * cb + r : DH);
+      for (int sp = 0; sp < a.splits; ++sp) v += part[(size_t)sp * C::DP * (DH + 1) + src];
     }
     fr[idx] = (T)v;
   }
@@ -780,7 +777,11 @@ static hipError_t nc_run(const NoncausalArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((nc_state_kernel<T, DH, L, MB>), dim3(a.heads * a.splits), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((nc_reduce_kernel<T, DH, L, MB>), dim3(a.heads), dim3(256), 0, s, a);
+  {
+    using C = NcCfg<T, DH, L, MB>;
+    constexpr int kSlices = (int)((C::FRAG_ELEMS + 255) / 256);
+    hipLaunchKernelGGL((nc_reduce_kernel<T, DH, L, MB>), dim3(a.heads, kSlices), dim3(256), 0, s, a);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((nc_readout_kernel<T, DH, L, MB>), dim3(a.heads * a.tiles), dim3(256), 0, s, a);

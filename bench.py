@@ -272,6 +272,136 @@ def decode_bench(args) -> int:
     return 0
 
 
+MFMA_F32_PEAK_TFLOPS = 157.3  # dense fp32 matrix cores
+
+
+def config_cases():
+    """(label, workload) pairs of the per-configuration report: the five synthetic
+    problems, the sequence-length sweep n = 1024 .. 16384 at the long encoder
+    problem's other sizes (B=32, H=8, d=64, M=16 x L=8), non-causal and causal, and
+    the one-channel variants (L=1, M = D) of the two long problems."""
+    from paper_2512_08061_amd import workloads as wl
+
+    W = wl.WORKLOADS
+    cases = [(name, W[name]) for name in ("tiny_f32", "text_encoder", "vision_encoder", "long_noncausal",
+                                          "long_causal")]
+    for causal in (False, True):
+        for n in (1024, 2048, 4096, 8192, 16384):
+            tag = "causal" if causal else "noncausal"
+            cases.append((f"sweep_{tag}_n{n}", W["long_noncausal"].with_(n=n, causal=causal, name=f"sweep_{n}")))
+    cases.append(("long_noncausal_L1", W["long_noncausal"].with_(M=128, L=1)))
+    cases.append(("long_causal_L1", W["long_causal"].with_(M=256, L=1)))
+    return cases
+
+
+def configs_bench(args) -> int:
+    """One timed ABI call per configuration, each on its own seeded inputs, with the
+    caches flushed before every timed call (a 1 GiB buffer is read, which evicts the
+    256 MB Infinity Cache and the L2s without leaving dirty lines whose write-back
+    would fall into the timed call), so that the small problems, whose inputs would
+    otherwise stay cached between calls, read them from HBM.  Prints one
+    JSON line per configuration (median and 10th / 90th percentile call time from HIP
+    events on the launch stream; the table build is part of every call)."""
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    luna.load_library()
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    sink = torch.empty((), dtype=torch.float32, device=dev)
+    rows = []
+    only = set(filter(None, args.configs_only.split(",")))
+    for label, w in config_cases():
+        if only and label not in only:
+            continue
+        tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        arrs = wl.make_inputs(w, args.seed)
+        p = wl.make_params(w, args.seed)
+        q, k, v = (torch.from_numpy(a).to(dev).to(tdt) for a in arrs)
+        del arrs
+        rec = {"config": label, "shape": {"B": w.B, "H": w.H, "n": w.n, "d": w.d, "M": w.M, "L": w.L,
+                                          "D": w.M * w.L, "causal": w.causal, "dtype": w.dtype, "dist": w.dist}}
+        try:
+            pt = luna.PhiParams.from_arrays(p, dev, tdt)
+            plan = luna.Plan(luna.OP_ATTN_CAUSAL if w.causal else luna.OP_ATTN, q, k, v, pt, eps=w.eps,
+                             chunk=w.chunk)
+            plan.run()  # an unsupported (d, M, L) is reported here, before anything is launched
+        except luna.LunaError as e:
+            rec["status"] = f"not run: {e}"
+            log(f"{label}: {rec['status']}")
+            rows.append(rec)
+            print(json.dumps(rec), flush=True)
+            continue
+        # flushes, calls and events are queued back to back with one synchronisation at
+        # the end, so that the GPU never idles (it keeps its clock) and the host's launch
+        # time is hidden behind the flush that precedes each call
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        for i in range(args.warmup):
+            torch.amax(flush, dim=0, out=sink)
+            plan.run()
+        for i, (e0, e1) in enumerate(ev):
+            torch.amax(flush, dim=0, out=sink)
+            e0.record(stream)
+            plan.run()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        times = sorted(e0.elapsed_time(e1) for e0, e1 in ev)
+        pick = lambda f: times[min(len(times) - 1, int(f * len(times)))]  # noqa: E731
+        ms = pick(0.5)
+        th = w.B * w.H * w.n
+        gb = bytes_per_token_head(w) * th / 1e9
+        tf = flops_per_token_head(w, w.causal) * th / 1e12
+        mfma_peak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
+        t_hbm, t_mfma = gb / HBM_PEAK_GBS, tf / mfma_peak
+        rec.update({
+            "status": "ok",
+            "ms_median": round(ms, 5), "ms_p10": round(pick(0.1), 5), "ms_p90": round(pick(0.9), 5),
+            "tokens_per_s": w.B * w.n / (ms / 1e3),
+            "head_tokens_per_s": th / (ms / 1e3),
+            "attn_tflops": tf / (ms / 1e3),
+            "hbm_gbs": gb / (ms / 1e3),
+            "bound": "hbm" if t_hbm >= t_mfma else "mfma",
+            "roofline_frac": max(t_hbm, t_mfma) / (ms / 1e3),
+            "floor_us": 1e6 * max(t_hbm, t_mfma),
+        })
+        log(f"{label}: {ms * 1e3:.1f} us, {rec['roofline_frac']:.1%} of the {rec['bound']} roofline")
+        rows.append(rec)
+        print(json.dumps(rec), flush=True)
+        del plan, q, k, v
+        torch.cuda.synchronize()
+    if args.configs_table:
+        with open(args.configs_table, "w") as fh:
+            fh.write("# LUNA attention forward per configuration on one MI355X\n\n")
+            fh.write(f"Command: `python bench.py --configs --steps {args.steps} --warmup {args.warmup} "
+                     f"--configs-table {args.configs_table}`\n\n")
+            fh.write("One ABI call per row (table build included), median of the timed calls with the 10th and "
+                     "90th percentiles, HIP events on the launch stream, caches flushed by a 1 GiB read before "
+                     "every timed call. tokens/s counts B*n (a token is one position across all heads); "
+                     "TFLOP/s counts the matrix-core work (projections, S, readout, z, denominators, and for "
+                     "causal the full 64x64 intra-chunk blocks); the floor is the larger of the HBM time of the "
+                     "algorithmic bytes (read Q, K, V, write out) at 8 TB/s and the MFMA time at the dtype's "
+                     "dense peak.\n\n")
+            fh.write("| config | B,H,n,d | M x L | dtype | causal | median us (p10-p90) | tokens/s | head-tokens/s "
+                     "| TFLOP/s | GB/s | floor us | roofline |\n|---|---|---|---|---|---|---|---|---|---|---|---|\n")
+            for r in rows:
+                s = r["shape"]
+                head = (f"| {r['config']} | {s['B']},{s['H']},{s['n']},{s['d']} | {s['M']} x {s['L']} | "
+                        f"{s['dtype']} | {'yes' if s['causal'] else 'no'} |")
+                if r["status"] != "ok":
+                    fh.write(head + f" {r['status']} | | | | | | |\n")
+                    continue
+                fh.write(head + f" {1e3 * r['ms_median']:.1f} ({1e3 * r['ms_p10']:.1f}-{1e3 * r['ms_p90']:.1f}) | "
+                         f"{r['tokens_per_s']:.3g} | {r['head_tokens_per_s']:.3g} | {r['attn_tflops']:.1f} | "
+                         f"{r['hbm_gbs']:.0f} | {r['floor_us']:.1f} | {r['roofline_frac']:.1%} {r['bound']} |\n")
+        log(f"wrote {args.configs_table}")
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -294,11 +424,24 @@ def main() -> int:
                     help="instead of the hot-path step: time streaming steps of M new tokens per head "
                          "(luna_attn_causal_step) on the long causal problem's shape, after the state of "
                          "its 16384-token prefix, and print their JSON line")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the hot-path step: time one call per synthetic configuration, a "
+                         "sequence-length sweep and the one-channel variants, each with the caches flushed "
+                         "before every timed call, and print one JSON line per configuration")
+    ap.add_argument("--configs-table", default="", metavar="PATH",
+                    help="with --configs: also write the results as a markdown table to PATH")
+    ap.add_argument("--configs-only", default="", metavar="NAMES",
+                    help="with --configs: comma-separated configuration labels to run (default: all)")
     args = ap.parse_args()
     if args.traffic_from:
         return traffic_from(*args.traffic_from, args.traffic_command)
+    if args.gpus != 1 and (args.decode or args.configs):
+        print("bench.py runs on one GPU only; use --gpus 1.", file=sys.stderr)
+        return 2
     if args.decode:
         return decode_bench(args)
+    if args.configs:
+        return configs_bench(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: LUNA attention shards over (batch, head) with no "

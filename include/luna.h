@@ -170,7 +170,11 @@ luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int6
  * other entry point does; 1: it uses the tables an earlier luna_attn_causal_step
  * left in the same workspace, enqueued before it on the same stream, with the same
  * parameters (same arrays, unchanged contents) -- for decode loops, where the table
- * build would otherwise cost as much as the step itself.
+ * build would otherwise cost as much as the step itself.  With tables_ready = 1 and
+ * a workspace that holds no tables built that way the results are undefined (the
+ * kernels clamp what they read from it, so the call still ends and stays inside its
+ * buffers).  The call also keeps a copy of z in the workspace for the duration of
+ * its kernels.
  * The same (d, L, M) combinations as luna_featuremap are built.
  */
 luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, luna_dtype dtype, int64_t B,

@@ -66,6 +66,7 @@ luna_status check_common(const Problem& pb) {
 struct Layout {
   size_t tables = 0, partial = 0, frags = 0, total = 0;
   size_t phiq = 0, phik = 0;  // streaming step: features of the new queries and keys (fp32)
+  size_t zcopy = 0;           // streaming step: z as it was before the call
   int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
   size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
@@ -165,6 +166,8 @@ luna_status plan(const Problem& pb, Layout* lay) {
     off = align256(off + feat_bytes);
     lay->phik = off;
     off = align256(off + feat_bytes);
+    lay->zcopy = off;
+    off = align256(off + (size_t)heads * (size_t)(M * L) * sizeof(float));
   } else {
     return fail(LUNA_ERR_INVALID_ARG, "unknown operation code");
   }
@@ -420,6 +423,10 @@ luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, l
   f.out2 = w + lay.phik;
   hipError_t e = luna::launch_featuremap(dt, luna::Dt::F32, (int)d, p->L, f, s);
   if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch");
+  // z before the step, for every column block of a head to read (block 0 rewrites z)
+  const size_t zbytes = (size_t)(B * H) * (size_t)(p->M * p->L) * sizeof(float);
+  e = hipMemcpyAsync(w + lay.zcopy, z, zbytes, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "copy of z");
   luna::StepArgs a{};
   a.phiq = reinterpret_cast<const float*>(w + lay.phiq);
   a.phik = reinterpret_cast<const float*>(w + lay.phik);
@@ -427,6 +434,7 @@ luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, l
   a.out = out;
   a.S = S;
   a.z = z;
+  a.z_in = reinterpret_cast<const float*>(w + lay.zcopy);
   a.m = (int)m;
   a.d = (int)d;
   a.D = p->M * p->L;

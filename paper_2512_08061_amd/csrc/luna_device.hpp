@@ -51,6 +51,27 @@ __device__ __forceinline__ int wave_id() {
 // piecewise-linear tables (layout shared with the host and luna_prepare.hip)
 // ---------------------------------------------------------------------------
 
+// Header fields as the kernels use them, clamped to what an LDS table of NSEG rows
+// can hold.  The tables are built on the device at the start of a call (or, for
+// streaming steps, by an earlier call on the same workspace); a workspace that never
+// held them gives wrong results but no LDS access out of range and no unbounded
+// search loop.
+struct PwlDims {
+  int nseg;   // real segments (breakpoints + 1); the all-zero segment follows them
+  int steps;  // halvings per search, <= 10 (windows of at most kKeyCap - 1 keys)
+  int nkeys;  // stored keys, <= kKeyCap
+  int nodes;  // 0, 1 or 2 (PwlHeader::nodes)
+};
+template <int NSEG>
+__device__ __forceinline__ PwlDims pwl_dims(const PwlHeader& hd) {
+  PwlDims r;
+  r.nseg = min(max(hd.nbp, 0), NSEG - 2) + 1;
+  r.steps = min(max(hd.steps, 0), 10);
+  r.nkeys = min(max(hd.nkeys, 0), kKeyCap);
+  r.nodes = (hd.nodes == 1 || hd.nodes == 2) ? hd.nodes : 0;
+  return r;
+}
+
 // LDS copy of one table for L channels, NSEG segment rows (see seg_row).
 template <int L, int NSEG>
 struct alignas(16) PwlLds {
@@ -64,8 +85,7 @@ struct alignas(16) PwlLds {
   int scale_exp;  // 0: these are the unscaled values
 };
 
-// Cooperative 16-byte copies global -> LDS: `n16` chunks, and rows of `row16` chunks
-// from a dense source into a destination with `dst_row16`-chunk rows.
+// Cooperative 16-byte copies global -> LDS: `n16` chunks.
 // Each thread issues up to kCopyBatch loads before it stores them, so that a copy
 // costs about one memory round trip rather than one per chunk it moves.  The loads
 // are unconditional (indices clamped to the last chunk): conditional ones would make
@@ -84,22 +104,6 @@ __device__ inline void copy16(void* dst, const void* src, int n16) {
       if (base + u * nt < n16) d[base + u * nt] = v[u];
   }
 }
-__device__ inline void copy16_rows(void* dst, int dst_row16, const void* src, int row16, int rows) {
-  uint4* d = reinterpret_cast<uint4*>(dst);
-  const uint4* sp = reinterpret_cast<const uint4*>(src);
-  const int n16 = rows * row16, nt = blockDim.x;
-  for (int base = threadIdx.x; base < n16; base += kCopyBatch * nt) {
-    uint4 v[kCopyBatch];
-#pragma unroll
-    for (int u = 0; u < kCopyBatch; ++u) v[u] = sp[min(base + u * nt, n16 - 1)];
-#pragma unroll
-    for (int u = 0; u < kCopyBatch; ++u) {
-      const int i = base + u * nt;
-      if (i < n16) d[(i / row16) * dst_row16 + i % row16] = v[u];
-    }
-  }
-}
-
 // One round of loads for n16 16-byte chunks: every thread issues all its loads
 // (kTabBatch per round, indices clamped so that none is conditional) before it stores
 // any.  ld(i) reads chunk i, st(i, v) writes it.
@@ -151,7 +155,8 @@ __device__ inline void copy_table_regions(void* keys_dst, void* bk_dst, void* se
 template <int L, int NSEG>
 __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
-  const int nseg = hd.nbp + 1;
+  const PwlDims dm = pwl_dims<NSEG>(hd);
+  const int nseg = dm.nseg;
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const float2* gseg = reinterpret_cast<const float2*>(gtab + kTabSeg);
@@ -160,7 +165,7 @@ __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ 
     copy_table_regions<kKeyCap / 4, NSEG, L * 8 / 16, sizeof(t.seg[0]) / 16>(t.keys, t.buckets, &t.seg[0][0], gtab,
                                                                              kTabSeg, nseg);
   } else {
-    copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
+    copy16(t.keys, gkeys, (dm.nkeys + 3) / 4);
     copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
     for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   }
@@ -168,7 +173,7 @@ __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ 
   // to exactly 0 without per-element masks
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = make_float2(0.0f, 0.0f);
   if (threadIdx.x == 0) {
-    t.steps = hd.steps;
+    t.steps = dm.steps;
     t.zero_seg = nseg;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
     t.scale_exp = 0;
@@ -193,7 +198,8 @@ struct alignas(16) PwlLds16 {
 template <int L, int NSEG>
 __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
-  const int nseg = hd.nbp + 1;
+  const PwlDims dm = pwl_dims<NSEG>(hd);
+  const int nseg = dm.nseg;
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
   const half2_t* gseg = reinterpret_cast<const half2_t*>(gtab + kTabSeg16);
@@ -202,13 +208,13 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
     copy_table_regions<kKeyCap / 4, NSEG, L * 4 / 16, sizeof(t.seg[0]) / 16>(t.keys, t.buckets, &t.seg[0][0], gtab,
                                                                              kTabSeg16, nseg);
   } else {
-    copy16(t.keys, gkeys, (hd.nkeys + 3) / 4);
+    copy16(t.keys, gkeys, (dm.nkeys + 3) / 4);
     copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
     for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
   }
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
   if (threadIdx.x == 0) {
-    t.steps = hd.steps;
+    t.steps = dm.steps;
     t.zero_seg = nseg;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
     t.scale_exp = hd.scale_exp;
@@ -401,80 +407,6 @@ __device__ __forceinline__ void pwl_pair(const PwlLds16<L, NSEG>& t, int seg, in
   y1 = relu_floor(__builtin_fmaf((float)v[2], u, (float)v[3]), floor);
 }
 
-// Search half of a table in LDS: keys and bucket windows only.  The coefficient rows
-// stay in global memory and are fetched through the vector memory path (they are
-// small enough to stay cached), which keeps their data-dependent gathers off the
-// LDS.
-struct alignas(16) PwlKeys {
-  float keys[kKeyCap];
-  uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
-  int steps;
-  float floor;    // 0 when outputs are clamped at zero, -inf otherwise
-  int scale_exp;  // fp16 rows hold 2^scale_exp times the values
-};
-
-__device__ inline void pwl_load_keys(PwlKeys& t, const uint8_t* __restrict__ gtab, bool fp16_rows) {
-  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
-  const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
-  const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
-  for (int i = threadIdx.x; i < hd.nkeys; i += blockDim.x) t.keys[i] = gkeys[i];
-  uint32_t* bk = reinterpret_cast<uint32_t*>(t.buckets);
-  for (int i = threadIdx.x; i < kNumBuckets / 2; i += blockDim.x) bk[i] = gbk[i];
-  if (threadIdx.x == 0) {
-    t.steps = hd.steps;
-    t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
-    t.scale_exp = fp16_rows ? hd.scale_exp : 0;
-  }
-}
-
-// Coefficient rows of a table as a range-checked buffer: segment s of L channels at
-// byte s * L * (4 or 8); an offset at or past the end reads as zeros, which
-// evaluates to psi = 0 (the masked value).
-template <bool FP16>
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t pwl_rows(const uint8_t* gtab, int nseg, int L) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(gtab + (FP16 ? kTabSeg16 : kTabSeg)), (short)0,
-                                           nseg * L * (FP16 ? 4 : 8), 0x00020000);
-}
-constexpr unsigned kPwlMasked = 0x80000000u;  // row offset that reads as zeros
-
-// psi_l(u), l = 0..L-1, of segment `seg` (its row at byte `row`) from the global
-// rows: fp16 pairs (half2 per channel, 4 channels per 16-byte load) ...
-template <int L>
-__device__ __forceinline__ void pwl_fetch(__amdgpu_buffer_rsrc_t rs, unsigned row,
-                                          __attribute__((ext_vector_type(4))) unsigned (&c)[L / 4]) {
-#pragma unroll
-  for (int q = 0; q < L / 4; ++q) c[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, row + 16 * q, 0, 0);
-}
-template <int L>
-__device__ __forceinline__ void pwl_eval16(const __attribute__((ext_vector_type(4))) unsigned (&c)[L / 4],
-                                           float floor, float u, float (&y)[L]) {
-  typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
-#pragma unroll
-  for (int q = 0; q < L / 4; ++q) {
-    const half8_t v = __builtin_bit_cast(half8_t, c[q]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
-  }
-}
-// ... or fp32 pairs (two channels per 16-byte load)
-template <int L>
-__device__ __forceinline__ void pwl_fetch32(__amdgpu_buffer_rsrc_t rs, unsigned row,
-                                            __attribute__((ext_vector_type(4))) unsigned (&c)[L / 2]) {
-#pragma unroll
-  for (int q = 0; q < L / 2; ++q) c[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, row + 16 * q, 0, 0);
-}
-template <int L>
-__device__ __forceinline__ void pwl_eval32(const __attribute__((ext_vector_type(4))) unsigned (&c)[L / 2],
-                                           float floor, float u, float (&y)[L]) {
-#pragma unroll
-  for (int q = 0; q < L / 2; ++q) {
-    const float4 v = __builtin_bit_cast(float4, c[q]);
-    y[2 * q] = relu_floor(fmaf(v.x, u, v.y), floor);
-    y[2 * q + 1] = relu_floor(fmaf(v.z, u, v.w), floor);
-  }
-}
-
 // A table whose keys are stored as overlapping groups: node s holds keys s .. s + 3
 // (+inf past the stored keys), so that the keys one u compares against -- the first
 // 4 or 8 from its bucket's offset when the header's `nodes` is 1 or 2 -- arrive in
@@ -498,7 +430,8 @@ template <typename RowT, int L, int NSEG>
 __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __restrict__ gtab) {
   using Tab = PwlLdsN<RowT, L, NSEG>;
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
-  const int nseg = hd.nbp + 1;
+  const PwlDims dm = pwl_dims<NSEG>(hd);
+  const int nseg = dm.nseg;
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const RowT* gseg = reinterpret_cast<const RowT*>(gtab + (Tab::kHalf ? kTabSeg16 : kTabSeg));
   // groups 4m .. 4m + 3 from the aligned key quads m and m + 1 (+inf past the stored keys)
@@ -531,7 +464,7 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-      if (4 * m + e >= hd.nkeys) k[e] = kInf;
+      if (4 * m + e >= dm.nkeys) k[e] = kInf;
 #pragma unroll
     for (int e = 0; e < 4; ++e) t.nodes[4 * m + e] = make_float4(k[e], k[e + 1], k[e + 2], k[e + 3]);
   }
@@ -539,8 +472,8 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
   // to exactly 0 without per-element masks
   for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = RowT{};
   if (threadIdx.x == 0) {
-    t.steps = hd.steps;
-    t.nodes_per_u = hd.nodes;
+    t.steps = dm.steps;
+    t.nodes_per_u = dm.nodes;
     t.zero_seg = nseg;
     t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
     t.scale_exp = Tab::kHalf ? hd.scale_exp : 0;

@@ -154,7 +154,9 @@ struct StepArgs {
   const void* V;      // [heads][m][d], element type of the call
   void* out;          // [heads][m][d]
   float* S;           // [heads][D][d]
-  float* z;           // [heads][D]
+  float* z;           // [heads][D], written by the column block 0 of each head
+  const float* z_in;  // [heads][D], z as it was before the call: every column block of a
+                      // head reads this copy, never z, which block 0 overwrites
   int m, d, D, heads;
   float eps;
 };

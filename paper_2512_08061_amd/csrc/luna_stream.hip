@@ -16,7 +16,9 @@
 // columns) and denominator; the eight groups of a wave are added with lane shuffles
 // and the four waves through LDS, in a fixed order (deterministic), one barrier per
 // token.  The state is read once at the start and written once at the end (16-byte
-// accesses), so a step of m tokens costs one pass over S whatever m is.
+// accesses), so a step of m tokens costs one pass over S whatever m is.  z is read
+// from a copy taken before the launch: the column blocks of a head are not ordered
+// against one another, and block 0 writes the new z in place.
 #include "luna_device.hpp"
 #include "luna_kernels.hpp"
 
@@ -46,6 +48,7 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   const int col0 = cblk * kStepCols + 4 * q;
   float* S = a.S + (size_t)head * D * d;
   float* z = a.z + (size_t)head * D;
+  const float* z0 = a.z_in + (size_t)head * D;
   const float* PQ = a.phiq + (size_t)head * m * D;
   const float* PK = a.phik + (size_t)head * m * D;
   const T* V = reinterpret_cast<const T*>(a.V) + (size_t)head * m * d;
@@ -57,7 +60,7 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   for (int i = 0; i < kStepFeat; ++i) {
     const int f = grp + kStepGroups * i;
     s[i] = f < D ? *reinterpret_cast<const float4*>(&S[(size_t)f * d + col0]) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    zz[i] = f < D ? z[f] : 0.0f;
+    zz[i] = f < D ? z0[f] : 0.0f;
   }
 
   for (int t0 = 0; t0 < m; t0 += kStepTokens) {

@@ -110,6 +110,35 @@ def test_prefill_then_decode(dtype, d, M, L, n0):
     assert_close(out, scan, dtype, "decoded rows against the chunked scan")
 
 
+def test_step_many_heads_from_state():
+    """Enough heads that the step kernel's grid runs in several rounds of workgroups
+    (2048 heads x 4 column blocks): every column block of a head must read z as it was
+    before the call, although the head's block 0 rewrites z in place.  Started from a
+    random state, against the oracle's recurrence."""
+    import torch
+    B, H, m, d, M, L = 16, 128, 3, 128, 32, 8
+    w = small_workload("bf16", B=B, H=H, n=m, d=d, M=M, L=L, causal=True)
+    say(f"step from a random state, {B * H} heads: {w.name}")
+    Q, K, V, p = inputs(w, seed=29)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    D = M * L
+    rng = np.random.default_rng(3)
+    S0 = rng.standard_normal((B, H, D, d)) * 0.05
+    z0 = rng.random((B, H, D)) + 0.5
+    S = torch.from_numpy(S0).float().cuda().contiguous()
+    z = torch.from_numpy(z0).float().cuda().contiguous()
+    S0 = to_np(S)
+    z0 = to_np(z)
+    out = to_np(luna.attn_causal_step(Qt, Kt, Vt, pt, S, z, eps=w.eps))
+    ro, rS, rz = oracle.attn_causal_step(Q, K, V, p, S0, z0, eps=w.eps)
+    assert_close(out, ro, "bf16", "out")
+    assert_close(to_np(S), rS, "bf16", "S")
+    assert_close(_col(to_np(z)), _col(rz), "bf16", "z")
+    # z is summed once per call: a second read of the rewritten z would add the new
+    # keys' features twice, which this bound (far below one key's share) rules out
+    assert np.abs(to_np(z) - rz).max() <= 1e-3 * np.abs(rz - z0).max(), "z updated more than once"
+
+
 def test_step_rejects_bad_state():
     """Malformed state tensors are refused before anything runs."""
     import torch

@@ -19,8 +19,9 @@
  * Conventions shared by every entry point:
  *  - Every data pointer is caller-owned DEVICE memory, row-major and contiguous.
  *    Q, K, V and out are [B, H, n, d]; the library never allocates or frees on a
- *    call, keeps no pointer after it returns and has no global mutable state, so
- *    calls on different streams may run concurrently if their workspaces differ.
+ *    call, keeps no pointer after it returns and, apart from the static scratch of
+ *    luna_attn_fwd_causal_noalloc, has no global mutable state, so calls on
+ *    different streams may run concurrently if their workspaces differ.
  *  - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued on it
  *    asynchronously; LUNA_OK means "enqueued", not "finished".
  *  - All arguments are validated on the host before anything is launched.  A
@@ -140,6 +141,29 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
                                  int64_t B, int64_t H, int64_t n, int64_t d,
                                  const luna_phi_params* p, int32_t chunk, float eps, void* out,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * luna_attn_fwd_causal without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops and
+ * harnesses that forbid allocation.  It computes exactly what luna_attn_fwd_causal
+ * computes (the same kernels) and allocates nothing: its workspace is a static
+ * array of luna_noalloc_scratch_bytes() bytes (64 MiB) in the library's code object,
+ * one per device, held from the library's load until the process ends, on the
+ * calling thread's current device (which must be the stream's device).  Problems
+ * whose workspace (luna_workspace_bytes with LUNA_OP_ATTN_CAUSAL) exceeds it return
+ * LUNA_ERR_WORKSPACE before anything is enqueued.  Every call on a device shares that
+ * device's array and needs nothing from an earlier call (every buffer in it is
+ * written before it is read), but two calls whose kernels overlap in time on one
+ * device -- on different streams, or from different threads -- race on it; order
+ * them on one stream.
+ */
+luna_status luna_attn_fwd_causal_noalloc(const void* Q, const void* K, const void* V, luna_dtype dtype,
+                                         int64_t B, int64_t H, int64_t n, int64_t d,
+                                         const luna_phi_params* p, int32_t chunk, float eps, void* out,
+                                         void* stream);
+
+/* Size in bytes of the static scratch of luna_attn_fwd_causal_noalloc. */
+size_t luna_noalloc_scratch_bytes(void);
 
 /*
  * Causal state of a token sequence: the key-side statistics of the runtime section

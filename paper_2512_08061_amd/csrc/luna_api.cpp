@@ -9,6 +9,7 @@
 
 #include <cmath>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "luna_kernels.hpp"
@@ -220,6 +221,34 @@ luna::PhiArgs phi_args(const Problem& pb, uint8_t* ws, const Layout& lay) {
 
 bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.0f; }
 
+// Scratch of luna_attn_fwd_causal_noalloc: one array per device, part of the code
+// object, so that calls need no allocation.  Host code never uses the array's name as
+// an address (on the host it only stands in for the symbol): the device address comes
+// from hipGetSymbolAddress, once per device, and is kept here.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch.
+luna_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(LUNA_ERR_UNSUPPORTED, "device index must be below 64");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress of the scratch array");
+    if (ptr == nullptr || ((uintptr_t)ptr & 255) != 0) return fail(LUNA_ERR_HIP, "scratch array address not 256-byte aligned");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return LUNA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -332,6 +361,27 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");
 }
+
+luna_status luna_attn_fwd_causal_noalloc(const void* Q, const void* K, const void* V, luna_dtype dtype,
+                                         int64_t B, int64_t H, int64_t n, int64_t d, const luna_phi_params* p,
+                                         int32_t chunk, float eps, void* out, void* stream) {
+  g_last_error.clear();
+  Problem pb{LUNA_OP_ATTN_CAUSAL, dtype, B, H, n, d, p, chunk};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (lay.total > kScratchBytes) {
+    char buf[160];
+    snprintf(buf, sizeof buf, "problem needs %zu bytes of scratch; the static scratch holds %zu", lay.total,
+             kScratchBytes);
+    return fail(LUNA_ERR_WORKSPACE, buf);
+  }
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws)) != LUNA_OK) return st;
+  return luna_attn_fwd_causal(Q, K, V, dtype, B, H, n, d, p, chunk, eps, out, ws, kScratchBytes, stream);
+}
+
+size_t luna_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
 luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int64_t B, int64_t H, int64_t n,
                             int64_t d, const luna_phi_params* p, int32_t accumulate, float* S, float* z, void* ws,

@@ -60,6 +60,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.luna_attn_fwd_causal.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float, vp, vp,
                                          sz, vp]
     lib.luna_attn_fwd_causal.restype = i32
+    lib.luna_attn_fwd_causal_noalloc.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float,
+                                                 vp, vp]
+    lib.luna_attn_fwd_causal_noalloc.restype = i32
+    lib.luna_noalloc_scratch_bytes.argtypes = []
+    lib.luna_noalloc_scratch_bytes.restype = sz
     lib.luna_attn_state.argtypes = [vp, vp, i32, i64, i64, i64, i64, P, i32, vp, vp, vp, sz, vp]
     lib.luna_attn_state.restype = i32
     lib.luna_attn_causal_step.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, i32, vp, vp, vp,
@@ -222,6 +227,28 @@ def attn_fwd_causal(Q, K, V, p: PhiParams, chunk: int = 64, eps: float = 1e-6, o
                                     chunk, eps, out.data_ptr(), wsp, wsn, _stream_ptr(Q.device)))
     out._luna_ws = ws
     return out
+
+
+def attn_fwd_causal_noalloc(Q, K, V, p: PhiParams, chunk: int = 64, eps: float = 1e-6, out=None):
+    """luna_attn_fwd_causal_noalloc: the causal forward with the library's static
+    scratch as workspace (no allocation in the call; pass ``out`` to allocate nothing
+    here either).  Returns out [B, H, n, d]."""
+    torch = _torch()
+    lib = load_library()
+    B, H, n, d = _qkv_shape(Q, K, V)
+    if out is None:
+        out = torch.empty_like(Q)
+    elif out.shape != Q.shape or out.dtype != Q.dtype or not out.is_contiguous() or out.device != Q.device:
+        raise LunaError(LUNA_ERR_INVALID_ARG, "out must be a contiguous tensor of Q's shape, dtype and device")
+    pc = p.c()
+    _check(lib.luna_attn_fwd_causal_noalloc(Q.data_ptr(), K.data_ptr(), V.data_ptr(), _dt(Q), B, H, n, d,
+                                            ctypes.byref(pc), chunk, eps, out.data_ptr(), _stream_ptr(Q.device)))
+    return out
+
+
+def noalloc_scratch_bytes() -> int:
+    """Bytes of the static scratch behind attn_fwd_causal_noalloc."""
+    return int(load_library().luna_noalloc_scratch_bytes())
 
 
 def _state_tensors(B, H, D, d, device, S, z):

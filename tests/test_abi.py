@@ -22,7 +22,8 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     names = luna.header_functions()
     assert set(names) == {"luna_workspace_bytes", "luna_featuremap", "luna_attn_fwd", "luna_attn_fwd_causal",
-                          "luna_attn_state", "luna_attn_causal_step", "luna_status_string", "luna_last_error"}
+                          "luna_attn_state", "luna_attn_causal_step", "luna_status_string", "luna_last_error",
+                          "luna_attn_fwd_causal_noalloc", "luna_noalloc_scratch_bytes"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -134,3 +135,15 @@ def test_workspace_sizes(lib):
     one = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 2, 4, 64, 64, ctypes.byref(p), 64)
     four = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 2, 4, 64, 64, ctypes.byref(ph), 64)
     assert four > one
+
+
+def test_noalloc_refuses_beyond_scratch_on_host(lib):
+    """A causal problem whose workspace exceeds the static scratch is refused before
+    any HIP call (per-head parameters: one table per head, 1024 heads)."""
+    p = _params(M=32, per_head=1)
+    need = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 1, 1024, 64, 128, ctypes.byref(p), 64)
+    assert need > lib.luna_noalloc_scratch_bytes() == 64 << 20
+    st = lib.luna_attn_fwd_causal_noalloc(FAKE, FAKE, FAKE, luna.LUNA_BF16, 1, 1024, 64, 128, ctypes.byref(p), 64,
+                                          1e-6, FAKE, None)
+    assert st == luna.LUNA_ERR_WORKSPACE
+    assert b"static scratch" in lib.luna_last_error()

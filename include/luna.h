@@ -29,8 +29,14 @@
  *    luna_last_error() then describes the reason (thread-local string).
  *  - Precision follows `dtype`: LUNA_F32 computes in fp32 throughout (fp32 matrix
  *    cores); LUNA_BF16 takes bf16 Q, K, V and W, multiplies bf16 operands on the
- *    matrix cores with fp32 accumulation, evaluates psi in fp32, keeps S and z in
- *    fp32 (rounded to bf16 as matrix-core operands) and writes bf16 output.
+ *    matrix cores with fp32 accumulation, keeps S and z in fp32 (rounded to bf16
+ *    as matrix-core operands) and writes bf16 output.  Its channel functions psi
+ *    are evaluated in fp32 arithmetic from their exact piecewise-linear form with
+ *    fp16 coefficients: on each segment psi = slope (u - a) + value, with a the
+ *    segment's breakpoint (fp32) and the value at a, so that the coefficients'
+ *    rounding costs at most 2^-11 (|slope (u - a)| + |value|) per element, against
+ *    the 2^-8 |phi| of phi's rounding to a bf16 operand.  luna_featuremap and the
+ *    streaming step use fp32 coefficients.
  *  - The denominator gets an additive eps: out = num / (den + eps).  With ReLU
  *    features a row can have den = 0; it then yields 0.
  *  - Shapes the kernels are not built for return LUNA_ERR_UNSUPPORTED; there is

@@ -60,7 +60,8 @@ luna_status check_common(const Problem& pb) {
   const bool fm_table = pb.op == LUNA_OP_FEATUREMAP || pb.op == LUNA_OP_CAUSAL_STEP;
   const int seg_cap = luna::nseg_cap(p->L, fm_table ? luna::kFmSegBytes : luna::kAttnSegBytes);
   if (units + 2 > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "too many breakpoints for the LDS segment table");
-  if ((units + 1) * p->L > luna::kSegCap) return fail(LUNA_ERR_UNSUPPORTED, "too many segments for the table");
+  if ((units + 1) * p->L > luna::kSegCap || (size_t)(units + 1) * luna::seg16_row_bytes(p->L) > luna::kSeg16Bytes)
+    return fail(LUNA_ERR_UNSUPPORTED, "too many segments for the table");
   return LUNA_OK;
 }
 

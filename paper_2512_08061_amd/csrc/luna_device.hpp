@@ -17,9 +17,12 @@
 //
 // Channel functions.  A ReLU MLP of a scalar is continuous and piecewise linear
 // in that scalar.  Its breakpoints -c_k/a_k are merged and sorted once per call
-// (luna_prepare.hip); evaluation is then a branch-free binary search over the
-// breakpoints (stored in heap order) and one fused multiply-add per channel with
-// the segment's slope and intercept.
+// (luna_prepare.hip); evaluation is then a lookup of u's bucket (an order-preserving
+// partition of the reals by float bits), which gives the start of a short window of
+// sorted keys, a count of the window's keys below u (branch-free halvings, or one or
+// two 16-byte reads of 4-key groups), and one fused multiply-add per channel: slope
+// u + intercept (fp32 rows) or slope (u - anchor) + value at the anchor (fp16 rows of
+// the bf16 paths).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -180,12 +183,13 @@ __device__ inline void pwl_load(PwlLds<L, NSEG>& t, const uint8_t* __restrict__ 
   }
 }
 
-// The same table with fp16 coefficients (bf16 attention paths): 4 bytes per
-// channel instead of 8, read with mixed-precision fused multiply-adds.
+// The same table with fp16 rows (bf16 attention paths): per channel the slope and
+// the value at the segment's anchor, then the anchor in fp32 (seg16_row_bytes), read
+// with mixed-precision fused multiply-adds: psi_l(u) = slope (u - anchor) + value.
 typedef __attribute__((ext_vector_type(2))) _Float16 half2_t;
 template <int L, int NSEG>
 struct alignas(16) PwlLds16 {
-  static constexpr int SROW = seg_row16(L);
+  static constexpr int SROW = seg16_row_bytes(L) / 4;
   float keys[kKeyCap];
   uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
   half2_t seg[NSEG][SROW];
@@ -202,17 +206,13 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
   const int nseg = dm.nseg;
   const float* gkeys = reinterpret_cast<const float*>(gtab + kTabKeys);
   const uint32_t* gbk = reinterpret_cast<const uint32_t*>(gtab + kTabBuckets);
-  const half2_t* gseg = reinterpret_cast<const half2_t*>(gtab + kTabSeg16);
-  static_assert(NSEG * L <= kSegCap, "the LDS rows must lie inside the table's segment region");
-  if constexpr ((L * 4) % 16 == 0) {
-    copy_table_regions<kKeyCap / 4, NSEG, L * 4 / 16, sizeof(t.seg[0]) / 16>(t.keys, t.buckets, &t.seg[0][0], gtab,
-                                                                             kTabSeg16, nseg);
-  } else {
-    copy16(t.keys, gkeys, (dm.nkeys + 3) / 4);
-    copy16(t.buckets, gbk, (kNumBuckets * 2 + 15) / 16);
-    for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
-  }
-  for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
+  constexpr int R16 = seg16_row_bytes(L) / 16;
+  static_assert(sizeof(t.seg[0]) == 16 * R16, "LDS rows are the global rows");
+  static_assert(NSEG * 16 * R16 <= (int)kSeg16Bytes, "the LDS rows must lie inside the table's fp16 region");
+  copy_table_regions<kKeyCap / 4, NSEG, R16, R16>(t.keys, t.buckets, &t.seg[0][0], gtab, kTabSeg16, nseg);
+  // the all-zero segment (its anchor 0 too, so that it evaluates to 0 for finite u)
+  for (int i = threadIdx.x; i < PwlLds16<L, NSEG>::SROW; i += blockDim.x)
+    t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
   if (threadIdx.x == 0) {
     t.steps = dm.steps;
     t.zero_seg = nseg;
@@ -225,6 +225,17 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
 template <typename Tab>
 __device__ __forceinline__ const char* seg_ptr(const Tab& t, int seg) {
   return reinterpret_cast<const char*>(&t.seg[0][0]) + __umul24((unsigned)seg, (unsigned)sizeof(t.seg[0]));
+}
+
+// Argument of the segment's linear form: u - anchor for fp16 rows, u for fp32 rows
+// (whose intercepts are at u = 0).
+template <int L, int NSEG>
+__device__ __forceinline__ float pwl_local(const PwlLds<L, NSEG>&, int, float u) {
+  return u;
+}
+template <int L, int NSEG>
+__device__ __forceinline__ float pwl_local(const PwlLds16<L, NSEG>& t, int seg, float u) {
+  return u - *reinterpret_cast<const float*>(seg_ptr(t, seg) + 4 * L);
 }
 
 // relu that propagates NaN like Listing 1's ReLU (fmaxf would drop it); one
@@ -375,10 +386,12 @@ __device__ __forceinline__ void pwl_pair(const PwlLds<L, NSEG>& t, int seg, int 
   y1 = relu_floor(fmaf(v.z, u, v.w), floor);
 }
 
-// fp16-coefficient versions (values scaled by 2^scale_exp)
+// fp16-row versions (slopes and values scaled by 2^scale_exp): u is the raw
+// projection, the anchor is read from the row
 template <int L, int NSEG>
 __device__ __forceinline__ void pwl_channels(const PwlLds16<L, NSEG>& t, int seg, float floor, float u,
                                              float (&y)[L]) {
+  const float x = pwl_local(t, seg, u);
   if constexpr (L % 4 == 0) {
     typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
     const half8_t* st = reinterpret_cast<const half8_t*>(seg_ptr(t, seg));
@@ -387,24 +400,31 @@ __device__ __forceinline__ void pwl_channels(const PwlLds16<L, NSEG>& t, int seg
       const half8_t v = st[q];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
+        y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], x, (float)v[2 * i + 1]), floor);
     }
   } else {
 #pragma unroll
     for (int l = 0; l < L; ++l) {
       const half2_t v = reinterpret_cast<const half2_t*>(seg_ptr(t, seg))[l];
-      y[l] = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
+      y[l] = relu_floor(__builtin_fmaf((float)v[0], x, (float)v[1]), floor);
     }
   }
 }
+// Channels 2q and 2q+1 from the segment's local argument x = pwl_local(t, seg, u)
+// (taken once per value by the caller, which evaluates the channels pair by pair).
 template <int L, int NSEG>
-__device__ __forceinline__ void pwl_pair(const PwlLds16<L, NSEG>& t, int seg, int q, float floor, float u,
-                                         float& y0, float& y1) {
+__device__ __forceinline__ void pwl_pair_local(const PwlLds16<L, NSEG>& t, int seg, int q, float floor, float x,
+                                               float& y0, float& y1) {
   static_assert(L % 2 == 0, "channel pairs need an even L");
   typedef __attribute__((ext_vector_type(4))) _Float16 half4_t;
   const half4_t v = reinterpret_cast<const half4_t*>(seg_ptr(t, seg))[q];
-  y0 = relu_floor(__builtin_fmaf((float)v[0], u, (float)v[1]), floor);
-  y1 = relu_floor(__builtin_fmaf((float)v[2], u, (float)v[3]), floor);
+  y0 = relu_floor(__builtin_fmaf((float)v[0], x, (float)v[1]), floor);
+  y1 = relu_floor(__builtin_fmaf((float)v[2], x, (float)v[3]), floor);
+}
+template <int L, int NSEG>
+__device__ __forceinline__ void pwl_pair_local(const PwlLds<L, NSEG>& t, int seg, int q, float floor, float x,
+                                               float& y0, float& y1) {
+  pwl_pair(t, seg, q, floor, x, y0, y1);
 }
 
 // A table whose keys are stored as overlapping groups: node s holds keys s .. s + 3
@@ -415,7 +435,7 @@ __device__ __forceinline__ void pwl_pair(const PwlLds16<L, NSEG>& t, int seg, in
 template <typename RowT, int L, int NSEG>
 struct alignas(16) PwlLdsN {
   static constexpr bool kHalf = sizeof(RowT) == 4;
-  static constexpr int SROW = kHalf ? seg_row16(L) : seg_row(L);
+  static constexpr int SROW = kHalf ? seg16_row_bytes(L) / 4 : seg_row(L);
   float4 nodes[kKeyCap + 8];
   uint16_t buckets[(kNumBuckets + 7) / 8 * 8];
   RowT seg[NSEG][SROW];
@@ -444,10 +464,15 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
   const int m0 = threadIdx.x;
   const float4 q0 = gq[min(m0, kKeyCap / 4 - 1)], q1 = gq[min(m0 + 1, kKeyCap / 4 - 1)];
   constexpr int kPair = sizeof(RowT);
-  static_assert(NSEG * L <= kSegCap, "the LDS rows must lie inside the table's segment region");
-  if constexpr ((L * kPair) % 16 == 0) {
+  if constexpr (Tab::kHalf) {
+    constexpr int R16 = seg16_row_bytes(L) / 16;
+    static_assert(sizeof(t.seg[0]) == 16 * R16, "LDS rows are the global rows");
+    static_assert(NSEG * 16 * R16 <= (int)kSeg16Bytes, "the LDS rows must lie inside the table's fp16 region");
+    copy_table_regions<0, NSEG, R16, R16>(nullptr, t.buckets, &t.seg[0][0], gtab, kTabSeg16, nseg);
+  } else if constexpr ((L * kPair) % 16 == 0) {
+    static_assert(NSEG * L <= kSegCap, "the LDS rows must lie inside the table's segment region");
     copy_table_regions<0, NSEG, L * kPair / 16, sizeof(t.seg[0]) / 16>(nullptr, t.buckets, &t.seg[0][0], gtab,
-                                                                       Tab::kHalf ? kTabSeg16 : kTabSeg, nseg);
+                                                                       kTabSeg, nseg);
   } else {
     copy16(t.buckets, gtab + kTabBuckets, (kNumBuckets * 2 + 15) / 16);
     for (int i = threadIdx.x; i < nseg * L; i += blockDim.x) t.seg[i / L][i % L] = gseg[i];
@@ -468,9 +493,9 @@ __device__ inline void pwl_load(PwlLdsN<RowT, L, NSEG>& t, const uint8_t* __rest
 #pragma unroll
     for (int e = 0; e < 4; ++e) t.nodes[4 * m + e] = make_float4(k[e], k[e + 1], k[e + 2], k[e + 3]);
   }
-  // one all-zero segment after the real ones: masked values select it and evaluate
-  // to exactly 0 without per-element masks
-  for (int i = threadIdx.x; i < L; i += blockDim.x) t.seg[nseg][i] = RowT{};
+  // one all-zero segment after the real ones (fp16 rows: its anchor 0 too): masked
+  // values select it and evaluate to exactly 0 without per-element masks
+  for (int i = threadIdx.x; i < Tab::SROW; i += blockDim.x) t.seg[nseg][i] = RowT{};
   if (threadIdx.x == 0) {
     t.steps = dm.steps;
     t.nodes_per_u = dm.nodes;
@@ -534,12 +559,13 @@ __device__ __forceinline__ void pwl_eval_off(const PwlLdsN<RowT, L, NSEG>& t, un
   if constexpr (PwlLdsN<RowT, L, NSEG>::kHalf) {
     static_assert(kRow % 16 == 0 && L % 4 == 0, "rows of whole 16-byte channel quads");
     typedef __attribute__((ext_vector_type(8))) _Float16 half8_t;
+    const float x = u - *reinterpret_cast<const float*>(row + 4 * L);  // the segment's anchor
 #pragma unroll
     for (int q = 0; q < L / 4; ++q) {
       const half8_t v = reinterpret_cast<const half8_t*>(row)[q];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], u, (float)v[2 * i + 1]), floor);
+        y[4 * q + i] = relu_floor(__builtin_fmaf((float)v[2 * i], x, (float)v[2 * i + 1]), floor);
     }
   } else {
     static_assert(kRow % 16 == 0 && L % 2 == 0, "rows of whole float4 pairs");

@@ -15,10 +15,17 @@ namespace luna {
 //   keys     the sorted breakpoints, fp32, padded with +inf to PwlHeader::nkeys
 //            (one window past the last breakpoint when that fits)
 //   buckets  uint16 per bucket of u: byte offset (4 * index) of its search window
-//   segments (slope, intercept) pairs, segment-major, L per segment, fp32
-//   segments16 the same pairs scaled by 2^scale_exp in fp16 (bf16 attention paths;
-//            the power of two keeps the largest magnitude near 2^14 and cancels
-//            between numerator and denominator once eps is scaled alike)
+//   segments (slope, intercept) pairs, segment-major, L per segment, fp32:
+//            psi_l(u) = slope u + intercept on the segment
+//   segments16 rows of seg16_row_bytes(L) bytes for the bf16 attention paths: per
+//            channel an fp16 pair (slope, value at the anchor), then the segment's
+//            anchor a (fp32): psi_l(u) = slope (u - a) + value.  The anchor is the
+//            segment's left breakpoint (the first segment's right one; 0 without
+//            breakpoints), so |u - a| stays within the segment and the fp16 rounding
+//            of slope and value is relative to the channel's size there, not to an
+//            intercept that cancels against slope u.  Slopes and values are scaled by
+//            2^scale_exp (the largest magnitude lands near 2^14), which cancels between
+//            numerator and denominator once eps is scaled alike.
 //
 // Search.  The float bits of u pick one of kNumBuckets buckets (bucket_of), an
 // order-preserving partition of the real line: sign, then |u| below 2^-kBucketExp,
@@ -39,7 +46,8 @@ constexpr size_t kTabKeys = 256;
 constexpr size_t kTabBuckets = kTabKeys + kKeyCap * 4;
 constexpr size_t kTabSeg = kTabBuckets + ((size_t)kNumBuckets * 2 + 15) / 16 * 16;
 constexpr size_t kTabSeg16 = kTabSeg + (size_t)kSegCap * 8;
-constexpr size_t kTableBytes = (kTabSeg16 + (size_t)kSegCap * 4 + 255) / 256 * 256;
+constexpr size_t kSeg16Bytes = 40960;  // fp16 rows with anchors
+constexpr size_t kTableBytes = (kTabSeg16 + kSeg16Bytes + 255) / 256 * 256;
 
 struct PwlHeader {
   int nbp;     // number of breakpoints
@@ -47,7 +55,7 @@ struct PwlHeader {
   int L;       // channels
   int nonneg;  // 1: relu on the channel outputs
   int nkeys;   // keys stored (breakpoints plus +inf padding), >= 2^steps - 1
-  int scale_exp;  // fp16 segments hold 2^scale_exp times the fp32 values
+  int scale_exp;  // fp16 slopes and values are 2^scale_exp times the fp32 ones
   int nodes;   // 1 or 2: the keys a u compares against are the first 4 or 8 from its
                // bucket's offset (no window was shifted to fit); 0 otherwise
 };
@@ -191,8 +199,12 @@ hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStr
 // Rows whose size is a multiple of 64 bytes are padded by 16 bytes so that random
 // segments spread over all LDS banks.
 constexpr int seg_row(int L) { return (L % 8 == 0) ? L + 2 : L; }
-// fp16 segment rows (half2 per channel), padded by 16 bytes when 4L is a multiple of 32
-constexpr int seg_row16(int L) { return (4 * L) % 32 == 0 ? L + 4 : L; }
+// fp16 segment rows: L (slope, value) half2 pairs and the fp32 anchor, in whole
+// 16-byte chunks, padded by 16 more bytes when that is a multiple of 64 (so that
+// random rows spread over all LDS banks); the same bytes in global memory and LDS
+constexpr int seg16_row_bytes(int L) {
+  return ((4 * L + 4 + 15) / 16 * 16) % 64 == 0 ? (4 * L + 4 + 15) / 16 * 16 + 16 : (4 * L + 4 + 15) / 16 * 16;
+}
 // Segments an LDS table of `bytes` holds for L channels (at most 64 L + 2: width-64
 // per-channel MLPs plus the all-zero segment).  A table needs breakpoints + 2.
 constexpr int nseg_cap(int L, int bytes) {

@@ -547,6 +547,10 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 #pragma unroll
       for (int e = 0; e < 8; ++e)  // slot e = 4 tb + j holds token t0 + 16 tb + 4 g + j
         if (!pcol[mb] || t0 + 16 * (e / 4) + 4 * g + (e % 4) >= n) sg[8 * mb + e] = zseg;
+    // each value's argument on its segment, taken once for the L / 2 channel pairs
+    float xx[8 * MB];
+#pragma unroll
+    for (int v = 0; v < 8 * MB; ++v) xx[v] = pwl_local(sm.tab, sg[v], uu[v]);
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     Frag<T> bv[C::CB];
 #pragma unroll
@@ -564,8 +568,8 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 #pragma unroll
           for (int e = 0; e < 8; e += 2) {
             float y00, y01, y10, y11;
-            pwl_pair<L>(sm.tab, sg[8 * mb + e], q, tfloor, uu[8 * mb + e], y00, y01);
-            pwl_pair<L>(sm.tab, sg[8 * mb + e + 1], q, tfloor, uu[8 * mb + e + 1], y10, y11);
+            pwl_pair_local<L>(sm.tab, sg[8 * mb + e], q, tfloor, xx[8 * mb + e], y00, y01);
+            pwl_pair_local<L>(sm.tab, sg[8 * mb + e + 1], q, tfloor, xx[8 * mb + e + 1], y10, y11);
             a0.set2(e, y00, y10);
             a1.set2(e, y01, y11);
           }

@@ -21,7 +21,11 @@
 //      (a < 0, or a = 0 with c > 0); crossing the breakpoint of unit k switches it on
 //      (a > 0) or off (a < 0), changing (s, t) by +-(f a, f c).  The segment values
 //      are these changes prefix-summed in fp64 (32 blocks per channel, block sums
-//      scanned with lane shuffles), scaled by 1/sqrt(M) and rounded to fp32.
+//      scanned with lane shuffles), scaled by 1/sqrt(M) and rounded to fp32;
+//   5. the fp16 rows of the bf16 paths: per segment and channel the slope and the
+//      value at the segment's anchor (its left breakpoint; the first segment's right
+//      one), formed in fp64 before rounding, so that the fp16 value carries no
+//      cancellation between slope u and a large intercept.
 #include <math.h>
 
 #include "luna_device.hpp"
@@ -56,8 +60,9 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
   __shared__ float g_s[16];
   __shared__ int hist[kHist];                      // counts, then exclusive starts
   __shared__ __attribute__((aligned(16))) uint16_t bstart[(kNumBuckets + 7) / 8 * 8];
-  __shared__ float2 segv[kSegCap];  // segment values before they are written out
-  __shared__ int s_vmax;            // bits of the largest |value| (non-negative float)
+  __shared__ float2 segv[kSegCap];  // segment (slope, intercept) before they are written out
+  __shared__ float segy[kSegCap];   // value at the segment's anchor
+  __shared__ int s_vmax;            // bits of the largest fp16-row magnitude (non-negative float)
   __shared__ int wave_tot[kThreads / 64];
   __shared__ int s_nbp, s_most;
 
@@ -286,7 +291,10 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
           if (j < j1) {
             const float2 v = make_float2((float)(s * inv), (float)(t * inv));
             segv[j * a.L + l] = v;
-            vmax = fmaxf(vmax, fmaxf(fabsf(v.x), fabsf(v.y)));
+            const double anc = j > 0 ? (double)key[j - 1] : (nbp > 0 ? (double)key[0] : 0.0);
+            const float y = (float)((s * anc + t) * inv);
+            segy[j * a.L + l] = y;
+            vmax = fmaxf(vmax, fmaxf(fabsf(v.x), fabsf(y)));
           }
           s += ds[u];
           t += dt[u];
@@ -294,8 +302,10 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
       }
     }
   }
-  // 5. fp32 segments, and fp16 ones scaled by 2^e so that the largest magnitude
-  // lands in [2^13, 2^14) (e clamped to [-20, 20])
+  // 5. fp32 segments, and the fp16 rows scaled by 2^e so that their largest magnitude
+  // lands in [2^13, 2^14).  e is clamped to [-50, 20], which keeps eps 2^(2e) a
+  // normal fp32 number; magnitudes beyond 2^64, where the fp16 rows would overflow,
+  // overflow fp32 in the state sums of any path as well.
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o, 64));
   if (lane == 0) atomicMax(&s_vmax, __float_as_int(vmax));
@@ -305,7 +315,7 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
   if (vm > 0.0f && isfinite(vm)) {
     int ex;
     frexpf(vm, &ex);  // vm = m 2^ex, m in [0.5, 1)
-    e = min(20, max(-20, 14 - ex));
+    e = min(20, max(-50, 14 - ex));
   }
   {
     const uint4* src = reinterpret_cast<const uint4*>(bstart);
@@ -313,12 +323,17 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
     for (int i = tid; i < (kNumBuckets + 7) / 8; i += kThreads) dst[i] = src[i];
   }
   float2* seg = reinterpret_cast<float2*>(tab + kTabSeg);
-  half2_t* seg16 = reinterpret_cast<half2_t*>(tab + kTabSeg16);
+  uint8_t* seg16 = tab + kTabSeg16;
+  const int r16 = seg16_row_bytes(a.L);
   for (int i = tid; i < nseg * a.L; i += kThreads) {
     const float2 v = segv[i];
     seg[i] = v;
-    seg16[i] = half2_t{(_Float16)ldexpf(v.x, e), (_Float16)ldexpf(v.y, e)};
+    const int j = i / a.L, l = i - j * a.L;
+    *reinterpret_cast<half2_t*>(seg16 + (size_t)j * r16 + 4 * l) =
+        half2_t{(_Float16)ldexpf(v.x, e), (_Float16)ldexpf(segy[i], e)};
   }
+  for (int j = tid; j < nseg; j += kThreads)
+    *reinterpret_cast<float*>(seg16 + (size_t)j * r16 + 4 * a.L) = j > 0 ? key[j - 1] : (nbp > 0 ? key[0] : 0.0f);
   if (tid == 0) {
     PwlHeader* hd = reinterpret_cast<PwlHeader*>(tab + kTabHeader);
     hd->scale_exp = e;

@@ -18,7 +18,9 @@ The JSON line also carries
                 (see profiles/), or null when the kernel source changed since they
                 were taken;
   cpu_baseline  the float64 oracle timed on the host cores on a bounded sample,
-                scaled to the same unit.
+                scaled to the same unit;
+  parity        the last timed step's outputs against the oracle's outputs for the
+                heads of that sample (largest per-row normwise error).
 Only one GPU is supported: --gpus above 1 exits with a message.
 """
 
@@ -147,8 +149,10 @@ def bytes_per_token_head(w) -> int:
     return 4 * w.d * (2 if w.dtype == "bf16" else 4)
 
 
-def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
-    """The float64 oracle on a bounded sample of the same step, scaled to tokens/s."""
+def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5, refs=None):
+    """The float64 oracle on a bounded sample of the same step, scaled to tokens/s.
+    The oracle's outputs for the sampled heads go into `refs` (name -> list of
+    ((b, h), out)) for the parity check of the GPU's outputs."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
@@ -162,17 +166,21 @@ def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
             b, h = divmod(nc_heads, w4.H)
             Q, K, V = (a[b, h:h + 1].astype(np.float64) for a in arrs4)
             t0 = time.perf_counter()
-            oracle.attn_noncausal(Q, K, V, p4, eps=w4.eps)
+            o = oracle.attn_noncausal(Q, K, V, p4, eps=w4.eps)
             t_nc += time.perf_counter() - t0
             nc_heads += 1
+            if refs is not None:
+                refs.setdefault("long_noncausal", []).append(((b, h), o[0]))
         cs_heads, t_cs = 0, 0.0
         while cs_heads < w5.B * w5.H and t_cs < budget:
             b, h = divmod(cs_heads, w5.H)
             Q, K, V = (a[b, h:h + 1].astype(np.float64) for a in arrs5)
             t0 = time.perf_counter()
-            oracle.attn_causal(Q, K, V, p5, eps=w5.eps)
+            o = oracle.attn_causal(Q, K, V, p5, eps=w5.eps)
             t_cs += time.perf_counter() - t0
             cs_heads += 1
+            if refs is not None:
+                refs.setdefault("long_causal", []).append(((b, h), o[0]))
     step = t_nc * (w4.B * w4.H) / nc_heads + t_cs * (w5.B * w5.H) / cs_heads
     tokens = w4.B * w4.n + w5.B * w5.n
     return {
@@ -184,6 +192,26 @@ def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5):
                    f"causal token recurrence {cs_heads} of {w5.B * w5.H} heads ({t_cs:.1f} s), "
                    f"scaled by heads to one full step"),
     }
+
+
+def parity_check(refs, outs) -> dict:
+    """The GPU's outputs of the last timed step against the oracle's outputs for the
+    heads the CPU baseline ran: the largest per-row normwise error
+    max|gpu - ref| / max|ref| (the tests' metric for bf16, tolerance 2e-2)."""
+    import numpy as np
+
+    res = {"tol": 2e-2, "metric": "max over rows of max|gpu - oracle| / max|oracle| per row"}
+    ok = True
+    for name, lst in refs.items():
+        worst = 0.0
+        for (b, h), ref in lst:
+            got = outs[name][b, h].float().cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-30)
+            worst = max(worst, float(err.max()))
+        res[name] = {"heads_checked": len(lst), "max_row_err": worst}
+        ok = ok and worst <= res["tol"]
+    res["pass"] = ok
+    return res
 
 
 def decode_bench(args) -> int:
@@ -565,11 +593,15 @@ def main() -> int:
         },
         "roofline": roofline,
         "cpu_baseline": None,
+        "parity": None,
     }
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
-        out["cpu_baseline"] = cpu_baseline(w4, arrs4, p4, w5, arrs5, p5)
+        refs = {}
+        out["cpu_baseline"] = cpu_baseline(w4, arrs4, p4, w5, arrs5, p5, refs)
         log(f"cpu baseline in {time.perf_counter() - t0:.1f} s")
+        out["parity"] = parity_check(refs, {"long_noncausal": nc.out, "long_causal": cs.out})
+        log(f"parity of the timed outputs against the oracle: {out['parity']}")
     print(json.dumps(out), flush=True)
     return 0
 

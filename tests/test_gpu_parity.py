@@ -14,7 +14,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import assert_close, inputs, say, small_workload, to_np, upload
+from gpu_util import assert_close, assert_close_rows, inputs, oracle_per_batch, say, small_workload, to_np, upload
 from paper_2512_08061_amd import luna
 from paper_2512_08061_amd import workloads as wl
 
@@ -259,20 +259,18 @@ def test_attn_noncausal_many_heads(dtype, d, M, L, n):
 
 @pytest.mark.parametrize("name", ["tiny_f32", "text_encoder", "vision_encoder", "long_noncausal"])
 def test_attn_noncausal_workload_full_size(name):
+    """Every head of every non-causal workload, in the launch configuration the
+    benchmark times, against the oracle's linear form."""
     w = wl.WORKLOADS[name]
-    say(f"noncausal full size {name}")
+    say(f"noncausal full size {name}: all {w.B * w.H} heads")
     Q, K, V, p = inputs(w, seed=0)
     (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
-    out = luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps)
-    _sync()
-    rng = np.random.default_rng(7)
-    heads = [(0, 0), (w.B - 1, w.H - 1)] + [(int(rng.integers(w.B)), int(rng.integers(w.H))) for _ in range(2)]
-    for b, h in heads:
-        ref = oracle.attn_noncausal(Q[b, h], K[b, h], V[b, h], p, eps=w.eps)
-        assert_close(to_np(out[b, h])[None], ref[None], w.dtype, f"out[{b},{h}]")
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps))
+    ref = oracle_per_batch(oracle.attn_noncausal, Q, K, V, p, w.eps)
+    assert_close(out, ref, w.dtype, "out, every head")
     if name == "tiny_f32":  # also against the O(n^2) kernel form
         ref = oracle.attn_quadratic(Q, K, V, p, eps=w.eps)
-        assert_close(to_np(out), ref, w.dtype, "out vs kernel form")
+        assert_close(out, ref, w.dtype, "out vs kernel form")
 
 
 # ---------------------------------------------------------------------------
@@ -293,7 +291,7 @@ def test_attn_causal_small(dtype, d, M, L, n):
     Q, K, V, p = inputs(w, seed=3)
     (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
     out = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))
-    assert_close(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), dtype, "out")
+    assert_close_rows(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), dtype, "out")
 
 
 @pytest.mark.parametrize("B,H,n", [(1, 3, 1000), (4, 25, 650), (8, 20, 300)])
@@ -310,7 +308,7 @@ def test_attn_causal_state_pieces(B, H, n):
     bs, hs = sorted({0, B - 1}), sorted({0, H // 2, H - 1})
     pick = lambda X: X[bs][:, hs]  # noqa: E731
     ref = oracle.attn_causal(pick(Q), pick(K), pick(V), p, eps=w.eps)
-    assert_close(pick(out), ref, "bf16", "out")
+    assert_close_rows(pick(out), ref, "bf16", "out")
 
 
 def test_attn_causal_workload_full_size():
@@ -325,13 +323,21 @@ def test_attn_causal_workload_full_size():
     got = to_np(out[:, :, :pre])
     for b in range(w.B):
         ref = oracle.attn_quadratic(Q[b, :, :pre], K[b, :, :pre], V[b, :, :pre], p, eps=w.eps, causal=True)
-        assert_close(got[b], ref, w.dtype, f"prefix b={b}")
-    # sampled rows deep into the sequence, kernel form one row at a time
+        assert_close_rows(got[b], ref, w.dtype, f"prefix b={b}")
+    # whole sequences (every row of both parts of the split: the second starts from
+    # the state pieces) of four heads, against the oracle's chunked scan (pinned to
+    # the token recurrence and the masked kernel form)
     rng = np.random.default_rng(11)
-    for b, h in [(0, 0), (w.B - 1, w.H - 1), (int(rng.integers(w.B)), int(rng.integers(w.H)))]:
-        rows = np.sort(np.concatenate([rng.integers(0, w.n, 12), [w.n - 1, 4095, 4096]]))
+    heads = [(0, 0), (w.B - 1, w.H - 1), (int(rng.integers(w.B)), int(rng.integers(w.H))), (3, 5)]
+    full = to_np(out[[b for b, _ in heads], [h for _, h in heads]])
+    for i, (b, h) in enumerate(heads):
+        ref = oracle.attn_causal_chunked(Q[b, h], K[b, h], V[b, h], p, chunk=w.chunk, eps=w.eps)
+        assert_close_rows(full[i], ref, w.dtype, f"all rows of ({b},{h})")
+    # rows deep into the sequence, kernel form one row at a time
+    for b, h in heads[:2]:
+        rows = np.sort(np.concatenate([rng.integers(0, w.n, 12), [w.n - 1, 8191, 8192]]))
         ref = oracle.attn_quadratic_rows(Q[b, h], K[b, h], V[b, h], p, rows, eps=w.eps, causal=True)
-        assert_close(to_np(out[b, h, rows])[None], ref[None], w.dtype, f"rows of ({b},{h})")
+        assert_close_rows(to_np(out[b, h, rows]), ref, w.dtype, f"rows of ({b},{h})")
 
 
 # ---------------------------------------------------------------------------

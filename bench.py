@@ -214,6 +214,146 @@ def parity_check(refs, outs) -> dict:
     return res
 
 
+def featuremap_bench(args) -> int:
+    """luna_featuremap on the long encoder problem's queries (B=32, H=8, n=4096, d=64,
+    M=16 x L=8, bf16 in and out): HIP events around each call (table build included),
+    algorithmic bytes = rows x (d + D) x 2 (read x, write phi)."""
+    import ctypes
+
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    lib = luna.load_library()
+    w = wl.WORKLOADS["long_noncausal"]
+    Q, _, _ = wl.make_inputs(w, args.seed)
+    p = wl.make_params(w, args.seed)
+    x = torch.from_numpy(Q).to(dev).to(torch.bfloat16).contiguous()
+    del Q
+    pt = luna.PhiParams.from_arrays(p, dev, torch.bfloat16)
+    pc = pt.c()
+    D = w.M * w.L
+    out = torch.empty((w.B, w.H, w.n, D), dtype=torch.bfloat16, device=dev)
+    nb = luna.workspace_bytes(luna.OP_FEATUREMAP, luna.LUNA_BF16, w.B, w.H, w.n, w.d, pt)
+    ws = torch.empty(nb + 256, dtype=torch.uint8, device=dev)
+    wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
+    stream = torch.cuda.current_stream(dev)
+
+    def call():
+        st = lib.luna_featuremap(x.data_ptr(), luna.LUNA_BF16, w.B, w.H, w.n, w.d, ctypes.byref(pc), out.data_ptr(),
+                                 luna.LUNA_BF16, wsp, nb, stream.cuda_stream)
+        assert st == luna.LUNA_OK, lib.luna_last_error()
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        call()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = sum(e0.elapsed_time(e1) for e0, e1 in ev) / args.steps
+    rows = w.B * w.H * w.n
+    nbytes = rows * (w.d + D) * 2
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "LUNA feature map rows/sec (luna_featuremap)",
+        "value": rows / (ms * 1e-3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded)",
+        "config": {"workload": "phi of the long encoder problem's queries, B=32 H=8 n=4096 d=64, M=16 x L=8 "
+                               "(D=128), bf16 in and out"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "featuremap_kernel",
+                     "bytes_per_call": nbytes,
+                     "timing": "HIP events around each ABI call (table build and feature-map kernel)"},
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+# Counters that `--counters-from` summarises, with what each derived figure means.
+COUNTER_RATIOS = [
+    ("VALU instructions per wave", "SQ_INSTS_VALU", "SQ_WAVES", 1.0),
+    ("MFMA instructions per wave", "SQ_INSTS_MFMA", "SQ_WAVES", 1.0),
+    ("LDS instructions per wave", "SQ_INSTS_LDS", "SQ_WAVES", 1.0),
+    ("SALU instructions per wave", "SQ_INSTS_SALU", "SQ_WAVES", 1.0),
+    ("vector memory reads per wave", "SQ_INSTS_VMEM_RD", "SQ_WAVES", 1.0),
+    ("vector memory writes per wave", "SQ_INSTS_VMEM_WR", "SQ_WAVES", 1.0),
+    ("wave lifetime, cycles per wave (SQ_WAVE_CYCLES counts 4-cycle units)", "SQ_WAVE_CYCLES", "SQ_WAVES", 4.0),
+    ("share of wave lifetime issuing VALU", "SQ_ACTIVE_INST_VALU", "SQ_WAVE_CYCLES", 1.0),
+    ("share of wave lifetime issuing LDS", "SQ_ACTIVE_INST_LDS", "SQ_WAVE_CYCLES", 1.0),
+    ("share of wave lifetime issuing anything", "SQ_ACTIVE_INST_ANY", "SQ_WAVE_CYCLES", 1.0),
+    ("share of wave lifetime waiting on dependencies (s_waitcnt)", "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES", 1.0),
+    ("share of wave lifetime waiting on LDS", "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES", 1.0),
+    ("LDS bank-conflict cycles per LDS-active cycle", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", 1.0),
+]
+# (figure, counter, units): counter / (GRBM_GUI_ACTIVE (GPU cycles of the dispatch) x units)
+COUNTER_UTIL = [
+    ("MFMA busy, share of all SIMD cycles (1024 SIMDs)", "SQ_VALU_MFMA_BUSY_CYCLES", 1024),
+    ("LDS active, share of all CU cycles (256 CUs)", "SQ_LDS_IDX_ACTIVE", 256),
+    ("SQ busy, share of all CU cycles (256 CUs)", "SQ_BUSY_CU_CYCLES", 256),
+]
+COUNTER_KERNELS = {  # kernel-name pattern (mangled or not) -> (file tag, workload, kernel whose sources are hashed)
+    r"nc_fused_kernel(<|I)": ("nc_fused_kernel", "long_noncausal", "nc_fused_kernel"),
+    r"(13causal_kernelI.*Lb1E|\bcausal_kernel<.*true>)": ("causal_kernel_state_launch", "long_causal", "causal_kernel"),
+    r"(13causal_kernelI.*Lb0E|\bcausal_kernel<.*false>)": ("causal_kernel_scan_launch", "long_causal", "causal_kernel"),
+    r"pwl_prepare_kernel": ("pwl_prepare_kernel", "bench_step", None),
+    r"featuremap_kernel(<|I)": ("featuremap_kernel", "featuremap_long_noncausal", None),
+}
+
+
+def counters_from(csvs, command: str) -> int:
+    """Average every counter per dispatch, per kernel, over rocprofv3 --pmc csv files
+    (one file per pass), and write profiles/counters_<kernel>_<workload>.md."""
+    import collections
+    import csv
+    import re
+
+    per = collections.defaultdict(dict)  # (kernel, counter) -> {(file, dispatch): value}
+    names = set()
+    for path in csvs:
+        for r in csv.DictReader(open(path)):
+            key = (r["Kernel_Name"], r["Counter_Name"])
+            d = (path, int(r["Dispatch_Id"]))
+            per[key][d] = per[key].get(d, 0.0) + float(r["Counter_Value"])
+            names.add(r["Kernel_Name"])
+    written = 0
+    for pat, (tag, wl_name, src) in COUNTER_KERNELS.items():
+        kern = sorted(k for k in names if re.search(pat, k))
+        if not kern:
+            continue
+        vals = {}
+        for (k, c), d in per.items():
+            if k in kern:
+                vals[c] = sum(d.values()) / len(d)
+        rows = []
+        for label, a, b, mul in COUNTER_RATIOS:
+            if a in vals and b in vals and vals[b] > 0:
+                rows.append((label, mul * vals[a] / vals[b], (f"{mul:g} x " if mul != 1 else "") + f"{a} / {b}"))
+        for label, a, units in COUNTER_UTIL:
+            if a in vals and vals.get("GRBM_GUI_ACTIVE", 0) > 0:
+                rows.append((label, vals[a] / (vals["GRBM_GUI_ACTIVE"] * units), f"{a} / (GRBM_GUI_ACTIVE x {units})"))
+        path = os.path.join(ROOT, "profiles", f"counters_{tag}_{wl_name}.md")
+        lines = [f"# rocprofv3 counters: {tag} ({wl_name})", "", f"Kernel: `{kern[0]}`", ""]
+        if src:
+            lines += [f"Source hash of its files (as bench.py's traffic records): `{source_hash(src)}`", ""]
+        lines += ["Commands (one counter pass each; every counter averaged per dispatch of the kernel):", "",
+                  "```", command, "```", "", "| figure | value | from |", "|---|---|---|"]
+        lines += [f"| {label} | {v:.4g} | `{how}` |" for label, v, how in rows]
+        lines += ["", "| counter | mean per dispatch |", "|---|---|"]
+        lines += [f"| {c} | {vals[c]:.6g} |" for c in sorted(vals)]
+        with open(path, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        log(f"wrote {path}")
+        written += 1
+    return 0 if written else 1
+
+
 def decode_bench(args) -> int:
     """Streaming steps of m tokens per head from the state of a 16384-token prefix on
     the long causal problem's shape (B=8, H=16, d=128, M=32 x L=8, bf16).  Each step
@@ -446,6 +586,13 @@ def main() -> int:
                     help="summarise two rocprofv3 --pmc csv runs into profiles/hbm_traffic_*.json and exit")
     ap.add_argument("--traffic-command", default="",
                     help="the rocprofv3 commands that produced --traffic-from, recorded in the summary")
+    ap.add_argument("--featuremap", action="store_true",
+                    help="instead of the hot-path step: time luna_featuremap on the long encoder problem's queries")
+    ap.add_argument("--counters-from", nargs="+", metavar="CSV",
+                    help="summarise rocprofv3 --pmc csv runs (one per counter pass) into "
+                         "profiles/counters_<kernel>_<workload>.md and exit")
+    ap.add_argument("--counters-command", default="",
+                    help="the rocprofv3 commands that produced --counters-from, recorded in the summaries")
     ap.add_argument("--graph", action="store_true",
                     help="with --decode: capture one streaming call in a HIP graph and time its replays")
     ap.add_argument("--decode", type=int, default=0, metavar="M",
@@ -463,11 +610,15 @@ def main() -> int:
     args = ap.parse_args()
     if args.traffic_from:
         return traffic_from(*args.traffic_from, args.traffic_command)
-    if args.gpus != 1 and (args.decode or args.configs):
+    if args.counters_from:
+        return counters_from(args.counters_from, args.counters_command)
+    if args.gpus != 1 and (args.decode or args.configs or args.featuremap):
         print("bench.py runs on one GPU only; use --gpus 1.", file=sys.stderr)
         return 2
     if args.decode:
         return decode_bench(args)
+    if args.featuremap:
+        return featuremap_bench(args)
     if args.configs:
         return configs_bench(args)
 

@@ -6,7 +6,8 @@ anchored fp16 rows from a (slope, intercept) fp16 form.
 The bf16 kernels evaluate channel l of projection i on the segment j of u_i as
     psi_l = slope_l (u - a_j) + value_l,
 with slope and value rounded to fp16 (unit roundoff 2^-11) and the anchor a_j the
-segment's left breakpoint (the first segment's right one), then round phi to bf16
+segment's left breakpoint (the first segment's right one), clamped to [-64, 64],
+then round phi to bf16
 (unit roundoff 2^-8) as a matrix-core operand.  Per element that gives
     |phi_gpu - phi| <= 2^-8 |phi| + (2^-11 (|slope (u - a)| + |value|) + |slope| du) / sqrt(M)
 up to fp32 roundings, where du bounds the fp32 error of the projection u.  The
@@ -24,15 +25,22 @@ from paper_2512_08061_amd import workloads as wl
 U_BF16 = 2.0 ** -8
 U_FP16 = 2.0 ** -11
 U_FP32 = 2.0 ** -24
+ANCHOR_MAX = 64.0  # anchors (segment breakpoints) are clamped to [-64, 64]
 
 
-def wide_params(d: int, M: int, L: int, hidden: int = 64, nonneg: bool = True, seed: int = 0) -> dict:
+def wide_params(d: int, M: int, L: int, hidden: int = 64, nonneg: bool = True, seed: int = 0,
+                outliers: bool = False) -> dict:
     """Channel MLPs whose breakpoints -c/a all lie at 2 <= |beta| <= 64 (slopes of order
     one), projections N(0, 1/d): far from u = 0 a segment's intercept is much larger
-    than the channel's value there, which is where an fp16 intercept loses it."""
+    than the channel's value there, which is where an fp16 intercept loses it.  With
+    `outliers`, one unit per channel breaks at |beta| = 1e20 (a tiny first-layer
+    weight), whose far segment must not set the scale of the fp16 rows."""
     rng = np.random.default_rng(np.random.SeedSequence([seed, 2000]))
     a = rng.standard_normal((L, hidden))
     beta = rng.uniform(2.0, 64.0, (L, hidden)) * rng.choice([-1.0, 1.0], (L, hidden))
+    if outliers:
+        a[:, 0] = 1e-20 * rng.choice([-1.0, 1.0], L)
+        beta[:, 0] = 1e20 * rng.choice([-1.0, 1.0], L)
     p = {
         "W": wl.round_bf16(rng.standard_normal((M, d)) / math.sqrt(d)),
         "b": (rng.standard_normal(M) / math.sqrt(d)).astype(np.float32),
@@ -53,6 +61,7 @@ def rows_near_breakpoints(p: dict, rows: int, seed: int = 0) -> np.ndarray:
     W = np.asarray(p["W"], np.float64)
     b = np.asarray(p["b"], np.float64)
     beta = (-np.asarray(p["fc1_b"], np.float64) / np.asarray(p["fc1_w"], np.float64)).ravel()
+    beta = beta[np.abs(beta) <= 64.0]  # (outlying breakpoints are not targets)
     M = W.shape[0]
     target = rng.choice(beta, (rows, M)) + rng.uniform(0.0, 0.05, (rows, M))
     X = np.linalg.lstsq(W, (target - b).T, rcond=None)[0].T
@@ -69,7 +78,7 @@ def local_terms(X: np.ndarray, p: dict):
     u = X @ W.T + b                                                    # [..., n, M]
     du = (X.shape[-1] + 2) * U_FP32 * (np.abs(X) @ np.abs(W).T + np.abs(b))
     j = np.searchsorted(bp, u, side="left")                            # segment
-    anchor = np.where(j > 0, bp[np.maximum(j - 1, 0)], bp[0] if bp.size else 0.0)
+    anchor = np.clip(np.where(j > 0, bp[np.maximum(j - 1, 0)], bp[0] if bp.size else 0.0), -ANCHOR_MAX, ANCHOR_MAX)
     sj, tj = s[j], t[j]                                                # [..., n, M, L]
     value = sj * anchor[..., None] + tj
     M, L = W.shape[0], s.shape[1]
@@ -91,7 +100,7 @@ def fp16_rows_emulated(X: np.ndarray, p: dict, anchored: bool) -> np.ndarray:
     u = np.asarray(X, np.float64) @ W.T + np.asarray(p["b"], np.float64)
     j = np.searchsorted(bp, u, side="left")
     M = W.shape[0]
-    seg_anchor = np.concatenate([[bp[0] if bp.size else 0.0], bp])   # anchor of segment j
+    seg_anchor = np.clip(np.concatenate([[bp[0] if bp.size else 0.0], bp]), -ANCHOR_MAX, ANCHOR_MAX)
     v = s * seg_anchor[:, None] + t if anchored else t
     e = 14 - math.frexp(max(np.abs(s).max(), np.abs(v).max()) / math.sqrt(M))[1]
     q16 = lambda x: np.ldexp(np.ldexp(x / math.sqrt(M), e).astype(np.float16).astype(np.float64), -e)  # noqa: E731

@@ -40,12 +40,15 @@ def _dev(x):
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda().to(torch.bfloat16).contiguous()
 
 
-@pytest.mark.parametrize("d,M,nonneg", [(64, 16, True), (64, 16, False), (128, 32, True), (128, 32, False)])
-def test_phi_elementwise_through_state(d, M, nonneg):
-    """z of one-token sequences = bf16(phi(k)) against the oracle's phi, per element."""
+@pytest.mark.parametrize("d,M,nonneg,outliers", [(64, 16, True, False), (64, 16, False, False),
+                                                  (128, 32, True, False), (128, 32, False, False),
+                                                  (64, 16, True, True), (128, 32, False, True)])
+def test_phi_elementwise_through_state(d, M, nonneg, outliers):
+    """z of one-token sequences = bf16(phi(k)) against the oracle's phi, per element;
+    with outliers, one breakpoint per channel at |beta| = 1e20."""
     import torch
     L, B, H = 8, 2, 128
-    p = pb.wide_params(d, M, L, nonneg=nonneg, seed=d + int(nonneg))
+    p = pb.wide_params(d, M, L, nonneg=nonneg, seed=d + int(nonneg), outliers=outliers)
     X = pb.rows_near_breakpoints(p, B * H, seed=d + 10 * int(nonneg))
     say(f"phi through luna_attn_state: d={d} M={M} L={L} nonneg={nonneg}, {B * H} one-token heads")
     Kt = _dev(X.reshape(B, H, 1, d))

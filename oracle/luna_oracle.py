@@ -34,6 +34,12 @@ What it computes (paper: "Learning Kernels for Linear Attention", section 3):
                    causal sums.
 * ``pwl_tables`` / ``psi_pwl``  the exact piecewise-linear form of a ReLU
                    channel MLP (a derived identity, not in the paper).
+* ``featuremap_backward``, ``attn_noncausal_backward``, ``attn_causal_backward``
+                   gradients of a loss L = sum(dO * out) (dO the upstream gradient)
+                   with respect to Q, K, V and every feature-map parameter, by the
+                   chain rule through the definitions above, for training the
+                   feature map end to end (section 5.1) and for the conversion
+                   fine-tuning (section 5.2).  ReLU'(0) is taken as 0.
 
 Readings where the paper is silent (each is listed in the design notes):
 the MLP activation is ReLU; h = 1; the causal prefix includes the diagonal
@@ -302,3 +308,139 @@ def psi_pwl(u, tables, nonneg=True):
     j = np.searchsorted(bp, u, side="left")  # number of breakpoints < u
     y = s[j] * u[..., None] + t[j]
     return np.maximum(y, 0.0) if nonneg else y
+
+
+# ---------------------------------------------------------------------------
+# gradients (chain rule through the definitions above; ReLU'(0) = 0)
+# ---------------------------------------------------------------------------
+
+PARAM_NAMES = ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")
+
+
+def _psi_backward(u, dpsi, fc1_w, fc1_b, fc2_w, fc2_b, nonneg=True):
+    """Gradients of sum(dpsi * psi(u)) for scalars u [N] and dpsi [N, L]: returns
+    (du [N], dfc1_w, dfc1_b, dfc2_w, dfc2_b).  Channel l: pre_k = a_k u + c_k,
+    h_k = relu(pre_k), y_l = g_l + sum_k f_lk h_k, psi_l = relu(y_l) when ``nonneg``."""
+    u = _f64(u)
+    a_all, c_all = _f64(fc1_w), _f64(fc1_b)
+    f_all, g_all = _f64(fc2_w), _f64(fc2_b)
+    L = f_all.shape[0]
+    shared = a_all.shape[0] == 1
+    du = np.zeros(u.shape)
+    d1w, d1b = np.zeros(a_all.shape), np.zeros(c_all.shape)
+    d2w, d2b = np.zeros(f_all.shape), np.zeros(g_all.shape)
+    for s in range(0, u.size, _PSI_CHUNK):
+        uu, dp = u[s:s + _PSI_CHUNK], dpsi[s:s + _PSI_CHUNK]
+        for l in range(L):
+            i = 0 if shared else l
+            pre = uu[:, None] * a_all[i][None, :] + c_all[i][None, :]
+            hid = np.maximum(pre, 0.0)
+            y = hid @ f_all[l] + g_all[l]
+            dy = dp[:, l] * (y > 0.0) if nonneg else dp[:, l]
+            d2w[l] += hid.T @ dy
+            d2b[l] += dy.sum()
+            dpre = (dy[:, None] * f_all[l][None, :]) * (pre > 0.0)
+            d1w[i] += (dpre * uu[:, None]).sum(axis=0)
+            d1b[i] += dpre.sum(axis=0)
+            du[s:s + _PSI_CHUNK] += dpre @ a_all[i]
+    return du, d1w, d1b, d2w, d2b
+
+
+def featuremap_backward(X, p, dphi):
+    """Gradients of sum(dphi * featuremap(X, p)): returns (dX, grads) with dX shaped
+    like X and grads a dict of the parameter gradients (PARAM_NAMES, shaped like the
+    parameters), summed over every row.  phi_{iL+l} = psi_l(u_i) / sqrt(M) with
+    u = X W^T + b."""
+    X, dphi = _f64(X), _f64(dphi)
+    if p.get("per_head", False):
+        H = X.shape[-3]
+        dX = np.empty(X.shape)
+        grads = {k: np.zeros(np.shape(p[k])) for k in PARAM_NAMES}
+        for h in range(H):
+            dXh, gh = featuremap_backward(X[..., h, :, :], _head_params(p, h), dphi[..., h, :, :])
+            dX[..., h, :, :] = dXh
+            for k in PARAM_NAMES:
+                grads[k][h] += gh[k]
+        return dX, grads
+    W = _f64(p["W"])
+    M, L = W.shape[0], _f64(p["fc2_b"]).shape[0]
+    u = project(X, p["W"], p["b"])                                        # [..., n, M]
+    dpsi = dphi.reshape(u.shape + (L,)) / math.sqrt(M)
+    du, d1w, d1b, d2w, d2b = _psi_backward(u.reshape(-1), dpsi.reshape(-1, L), p["fc1_w"], p["fc1_b"],
+                                           p["fc2_w"], p["fc2_b"], p["nonneg"])
+    du = du.reshape(u.shape)
+    dX = du @ W
+    grads = {
+        "W": du.reshape(-1, M).T @ X.reshape(-1, X.shape[-1]),
+        "b": du.reshape(-1, M).sum(axis=0),
+        "fc1_w": d1w, "fc1_b": d1b, "fc2_w": d2w, "fc2_b": d2b,
+    }
+    return dX, grads
+
+
+def _add_grads(g1, g2):
+    return {k: g1[k] + g2[k] for k in PARAM_NAMES}
+
+
+def attn_noncausal_backward(Q, K, V, p, dO, eps=1e-6):
+    """Gradients of L = sum(dO * attn_noncausal(Q, K, V, p, eps)) with respect to Q, K,
+    V and the feature-map parameters: returns (dQ, dK, dV, grads).
+
+    With num = phi(Q) S, den = phi(Q) z + eps and out = num / den per row:
+    dnum = dO / den, dden = -(dO . num) / den^2, dphi(Q) = dnum S^T + dden z^T,
+    dS = phi(Q)^T dnum, dz = phi(Q)^T dden, dphi(K) = V dS^T + 1 dz^T, dV = phi(K) dS."""
+    V, dO = _f64(V), _f64(dO)
+    phiQ, phiK = featuremap(Q, p), featuremap(K, p)
+    S, z = sufficient_statistics(phiK, V)
+    num = phiQ @ S
+    den = (phiQ @ z[..., :, None])[..., 0] + eps
+    dnum = dO / den[..., None]
+    dden = -(dO * num).sum(axis=-1) / den ** 2
+    dphiQ = dnum @ np.swapaxes(S, -1, -2) + dden[..., None] * z[..., None, :]
+    dS = np.swapaxes(phiQ, -1, -2) @ dnum
+    dz = (np.swapaxes(phiQ, -1, -2) @ dden[..., None])[..., 0]
+    dphiK = V @ np.swapaxes(dS, -1, -2) + dz[..., None, :]
+    dV = phiK @ dS
+    dQ, gq = featuremap_backward(Q, p, dphiQ)
+    dK, gk = featuremap_backward(K, p, dphiK)
+    return dQ, dK, dV, _add_grads(gq, gk)
+
+
+def attn_causal_backward(Q, K, V, p, dO, eps=1e-6):
+    """Gradients of L = sum(dO * attn_causal(Q, K, V, p, eps)): returns (dQ, dK, dV, grads).
+
+    Query t sees the prefix state (S_t, z_t) over s <= t, so dphi(q_t) = S_t dnum_t +
+    z_t dden_t, taken in a forward pass over the tokens; key s feeds every query t >= s,
+    so with the suffix sums dS_s = sum_{t >= s} phi(q_t) dnum_t^T and dz_s = sum_{t >= s}
+    phi(q_t) dden_t, dphi(k_s) = dS_s v_s + dz_s and dv_s = dS_s^T phi(k_s), taken in a
+    backward pass."""
+    V, dO = _f64(V), _f64(dO)
+    phiQ, phiK = featuremap(Q, p), featuremap(K, p)
+    lead, n, D = phiQ.shape[:-2], phiQ.shape[-2], phiQ.shape[-1]
+    dv = V.shape[-1]
+    S = np.zeros(lead + (D, dv))
+    z = np.zeros(lead + (D,))
+    dnum = np.empty(lead + (n, dv))
+    dden = np.empty(lead + (n,))
+    dphiQ = np.empty(phiQ.shape)
+    for t in range(n):
+        S += phiK[..., t, :, None] * V[..., t, None, :]
+        z += phiK[..., t, :]
+        q = phiQ[..., t, :]
+        num = (q[..., None, :] @ S)[..., 0, :]
+        den = (q * z).sum(axis=-1) + eps
+        dnum[..., t, :] = dO[..., t, :] / den[..., None]
+        dden[..., t] = -(dO[..., t, :] * num).sum(axis=-1) / den ** 2
+        dphiQ[..., t, :] = (S @ dnum[..., t, :, None])[..., 0] + z * dden[..., t, None]
+    dS = np.zeros(lead + (D, dv))
+    dz = np.zeros(lead + (D,))
+    dphiK = np.empty(phiK.shape)
+    dV = np.empty(V.shape)
+    for t in range(n - 1, -1, -1):
+        dS += phiQ[..., t, :, None] * dnum[..., t, None, :]
+        dz += phiQ[..., t, :] * dden[..., t, None]
+        dphiK[..., t, :] = (dS @ V[..., t, :, None])[..., 0] + dz
+        dV[..., t, :] = (phiK[..., t, None, :] @ dS)[..., 0, :]
+    dQ, gq = featuremap_backward(Q, p, dphiQ)
+    dK, gk = featuremap_backward(K, p, dphiK)
+    return dQ, dK, dV, _add_grads(gq, gk)

@@ -311,4 +311,119 @@ def pin_pwl_identity(o):
         assert np.max(np.abs(got - want) / scale) < 1e-12
 
 
+# ---------------------------------------------------------------------------
+# gradients
+# ---------------------------------------------------------------------------
+
+def _grad_problems(rng):
+    """Tiny problems for the gradient pins: (causal, p, Q, K, V, dO), with per-channel
+    and shared first layers, output ReLU on and off (denominators kept away from 0)."""
+    out = []
+    for causal in (False, True):
+        for shared, nonneg in ((False, True), (True, False)):
+            p = _params(rng, M=2, L=3, d=4, hidden=5, shared=shared, nonneg=nonneg, scale=0.7)
+            if not nonneg:
+                p["fc2_b"] = p["fc2_b"] + 2.0
+            Q, K, V = _qkv(rng, (1, 2, 6, 4), dv=3)
+            dO = rng.standard_normal((1, 2, 6, 3))
+            out.append((causal, p, Q, K, V, dO))
+    return out
+
+
+def _grads(o, causal, p, Q, K, V, dO, eps):
+    f = o.attn_causal_backward if causal else o.attn_noncausal_backward
+    dQ, dK, dV, g = f(Q, K, V, p, dO, eps=eps)
+    return {"Q": dQ, "K": dK, "V": dV, **g}
+
+
+def pin_backward_finite_differences(o):
+    """Every gradient of L = sum(dO * out) against central differences of the oracle's
+    own forward pass (both forms, per-channel and shared first layers, output ReLU
+    on and off), element by element."""
+    rng = np.random.default_rng(21)
+    eps, h = 1e-6, 1e-6
+    for causal, p, Q, K, V, dO in _grad_problems(rng):
+        fwd = o.attn_causal if causal else o.attn_noncausal
+        g = _grads(o, causal, p, Q, K, V, dO, eps)
+        inputs = {"Q": Q, "K": K, "V": V}
+
+        def loss(inp, prm):
+            return float((fwd(inp["Q"], inp["K"], inp["V"], prm, eps=eps) * dO).sum())
+
+        for name in list(inputs) + ["W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b"]:
+            base = inputs[name] if name in inputs else p[name]
+            fd = np.zeros(np.shape(base))
+            for idx in np.ndindex(*np.shape(base)):
+                vals = []
+                for sgn in (1.0, -1.0):
+                    x = np.array(base, dtype=np.float64, copy=True)
+                    x[idx] += sgn * h
+                    inp, prm = dict(inputs), dict(p)
+                    if name in inputs:
+                        inp[name] = x
+                    else:
+                        prm[name] = x
+                    vals.append(loss(inp, prm))
+                fd[idx] = (vals[0] - vals[1]) / (2 * h)
+            assert _rel(g[name], fd) < 1e-5, (causal, name, _rel(g[name], fd))
+
+
+def _torch_forward(torch, Q, K, V, prm, causal, eps, nonneg):
+    """The forward pass written with torch operations (float64, CPU), for autograd."""
+    def phi(X):
+        u = X @ prm["W"].T + prm["b"]
+        shared = prm["fc1_w"].shape[0] == 1
+        L = prm["fc2_w"].shape[0]
+        chans = []
+        for l in range(L):
+            i = 0 if shared else l
+            hid = torch.relu(u[..., None] * prm["fc1_w"][i] + prm["fc1_b"][i])
+            y = hid @ prm["fc2_w"][l] + prm["fc2_b"][l]
+            chans.append(torch.relu(y) if nonneg else y)
+        y = torch.stack(chans, dim=-1)                       # [..., n, M, L]
+        return y.reshape(y.shape[:-2] + (-1,)) / math.sqrt(prm["W"].shape[0])
+    pq, pk = phi(Q), phi(K)
+    if causal:
+        S = torch.cumsum(pk[..., :, :, None] * V[..., :, None, :], dim=-3)   # [..., n, D, dv]
+        z = torch.cumsum(pk, dim=-2)
+        num = (pq[..., :, :, None] * S).sum(dim=-2)
+        den = (pq * z).sum(dim=-1)
+    else:
+        S = pk.transpose(-1, -2) @ V
+        z = pk.sum(dim=-2)
+        num = pq @ S
+        den = pq @ z[..., :, None]
+        den = den[..., 0]
+    return num / (den + eps)[..., None]
+
+
+def pin_backward_matches_autograd(o):
+    """The oracle's gradients against torch autograd of the forward written with torch
+    operations (float64), including rows whose pre-activations are exactly 0, where both
+    take ReLU'(0) = 0."""
+    import torch
+    rng = np.random.default_rng(22)
+    eps = 1e-6
+    problems = _grad_problems(rng)
+    # kinks: x = 0 rows, b = 0 and c = 0 for one unit give pre-activations a u + c = 0
+    causal, p, Q, K, V, dO = problems[0]
+    p = dict(p)
+    p["b"] = np.zeros_like(p["b"])
+    p["fc1_b"] = p["fc1_b"].copy()
+    p["fc1_b"][:, 0] = 0.0
+    Q, K = Q.copy(), K.copy()
+    Q[..., 1, :] = 0.0
+    K[..., 2, :] = 0.0
+    problems.append((causal, p, Q, K, V, dO))
+    for causal, p, Q, K, V, dO in problems:
+        g = _grads(o, causal, p, Q, K, V, dO, eps)
+        t = {k: torch.tensor(np.asarray(v, dtype=np.float64), requires_grad=True)
+             for k, v in (("Q", Q), ("K", K), ("V", V), *((n, p[n]) for n in ("W", "b", "fc1_w", "fc1_b", "fc2_w",
+                                                                              "fc2_b")))}
+        out = _torch_forward(torch, t["Q"], t["K"], t["V"], t, causal, eps, p["nonneg"])
+        (out * torch.tensor(dO)).sum().backward()
+        for name, tv in t.items():
+            assert _rel(g[name], tv.grad.numpy()) < 1e-12, (causal, name, _rel(g[name], tv.grad.numpy()))
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

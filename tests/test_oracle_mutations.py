@@ -14,7 +14,8 @@ from oracle import luna_oracle as O
 
 _orig = {k: getattr(O, k) for k in ("project", "psi", "featuremap", "attn_noncausal", "attn_causal",
                                     "attn_causal_chunked", "kernel_matrix", "psi_pwl", "pwl_tables",
-                                    "sufficient_statistics", "attn_quadratic_rows")}
+                                    "sufficient_statistics", "attn_quadratic_rows", "_psi_backward",
+                                    "featuremap_backward", "attn_noncausal_backward", "attn_causal_backward")}
 
 
 def _psi_mut(kind):
@@ -162,7 +163,114 @@ def _pwl_mut(kind):
     return psi_pwl
 
 
+def _psi_backward_mut(kind):
+    def _psi_backward(u, dpsi, fc1_w, fc1_b, fc2_w, fc2_b, nonneg=True):
+        u = np.asarray(u, float)
+        a_all, c_all, f_all, g_all = (np.asarray(x, float) for x in (fc1_w, fc1_b, fc2_w, fc2_b))
+        L = f_all.shape[0]
+        shared = a_all.shape[0] == 1
+        du = np.zeros(u.shape)
+        d1w, d1b, d2w, d2b = (np.zeros(x.shape) for x in (a_all, c_all, f_all, g_all))
+        for l in range(L):
+            i = 0 if shared else l
+            pre = u[:, None] * a_all[i] + c_all[i]
+            hid = np.maximum(pre, 0.0)
+            y = hid @ f_all[l] + g_all[l]
+            mask = (y > 0.0) if (nonneg and kind != "no_output_mask") else 1.0
+            dy = dpsi[:, l] * mask
+            d2w[l] += hid.T @ dy
+            d2b[l] += dy.sum()
+            gate = (pre >= 0.0) if kind == "relu_at_zero_passes" else (pre > 0.0)
+            dpre = (dy[:, None] * f_all[l]) * gate
+            d1w[i] += (dpre * u[:, None]).sum(axis=0) * (0.0 if kind == "drop_dfc1_w" else 1.0)
+            d1b[i] += dpre.sum(axis=0)
+            du += dpre @ a_all[i]
+        return du, d1w, d1b, d2w, d2b
+    return _psi_backward
+
+
+def _fm_backward_mut(kind):
+    def featuremap_backward(X, p, dphi):
+        dX, g = _orig["featuremap_backward"](X, p, dphi)
+        if kind == "scale_missing":
+            M = np.shape(p["W"])[-2]
+            dX, g = dX * math.sqrt(M), {k: v * math.sqrt(M) for k, v in g.items()}
+        if kind == "dW_no_bias_grad":
+            g = dict(g)
+            g["b"] = np.zeros_like(g["b"])
+        return dX, g
+    return featuremap_backward
+
+
+def _nc_backward_mut(kind):
+    def attn_noncausal_backward(Q, K, V, p, dO, eps=1e-6):
+        V, dO = np.asarray(V, float), np.asarray(dO, float)
+        phiQ, phiK = O.featuremap(Q, p), O.featuremap(K, p)
+        S, z = O.sufficient_statistics(phiK, V)
+        num = phiQ @ S
+        den = (phiQ @ z[..., :, None])[..., 0] + eps
+        dnum = dO / den[..., None]
+        dden = -(dO * num).sum(-1) / den ** 2 * (0.0 if kind == "drop_dden" else 1.0)
+        dphiQ = dnum @ np.swapaxes(S, -1, -2) + dden[..., None] * z[..., None, :]
+        dS = np.swapaxes(phiQ, -1, -2) @ dnum
+        dz = (np.swapaxes(phiQ, -1, -2) @ dden[..., None])[..., 0]
+        dphiK = V @ np.swapaxes(dS, -1, -2) + (0.0 if kind == "dphik_no_dz" else dz[..., None, :])
+        dV = (phiQ if kind == "dv_from_q" else phiK) @ dS
+        dQ, gq = O.featuremap_backward(Q, p, dphiQ)
+        dK, gk = O.featuremap_backward(K, p, dphiK)
+        return dQ, dK, dV, {k: gq[k] + gk[k] for k in gq}
+    return attn_noncausal_backward
+
+
+def _cs_backward_mut(kind):
+    def attn_causal_backward(Q, K, V, p, dO, eps=1e-6):
+        if kind == "as_noncausal":
+            return _orig["attn_noncausal_backward"](Q, K, V, p, dO, eps)
+        V, dO = np.asarray(V, float), np.asarray(dO, float)
+        phiQ, phiK = O.featuremap(Q, p), O.featuremap(K, p)
+        lead, n, D = phiQ.shape[:-2], phiQ.shape[-2], phiQ.shape[-1]
+        S, z = np.zeros(lead + (D, V.shape[-1])), np.zeros(lead + (D,))
+        dnum, dden = np.empty(lead + (n, V.shape[-1])), np.empty(lead + (n,))
+        dphiQ = np.empty(phiQ.shape)
+        for t in range(n):
+            S += phiK[..., t, :, None] * V[..., t, None, :]
+            z += phiK[..., t, :]
+            q = phiQ[..., t, :]
+            num = (q[..., None, :] @ S)[..., 0, :]
+            den = (q * z).sum(-1) + eps
+            dnum[..., t, :] = dO[..., t, :] / den[..., None]
+            dden[..., t] = -(dO[..., t, :] * num).sum(-1) / den ** 2
+            dphiQ[..., t, :] = (S @ dnum[..., t, :, None])[..., 0] + z * dden[..., t, None]
+        dS, dz = np.zeros(S.shape), np.zeros(z.shape)
+        dphiK, dV = np.empty(phiK.shape), np.empty(V.shape)
+        order = range(n) if kind == "prefix_for_keys" else range(n - 1, -1, -1)
+        for t in order:
+            if kind != "exclusive_suffix":
+                dS += phiQ[..., t, :, None] * dnum[..., t, None, :]
+                dz += phiQ[..., t, :] * dden[..., t, None]
+            dphiK[..., t, :] = (dS @ V[..., t, :, None])[..., 0] + dz
+            dV[..., t, :] = (phiK[..., t, None, :] @ dS)[..., 0, :]
+            if kind == "exclusive_suffix":
+                dS += phiQ[..., t, :, None] * dnum[..., t, None, :]
+                dz += phiQ[..., t, :] * dden[..., t, None]
+        dQ, gq = O.featuremap_backward(Q, p, dphiQ)
+        dK, gk = O.featuremap_backward(K, p, dphiK)
+        return dQ, dK, dV, {k: gq[k] + gk[k] for k in gq}
+    return attn_causal_backward
+
+
 MUTATIONS = {
+    "bwd_psi_relu_at_zero_passes": ("_psi_backward", _psi_backward_mut("relu_at_zero_passes")),
+    "bwd_psi_no_output_mask": ("_psi_backward", _psi_backward_mut("no_output_mask")),
+    "bwd_psi_drop_dfc1_w": ("_psi_backward", _psi_backward_mut("drop_dfc1_w")),
+    "bwd_featuremap_scale_missing": ("featuremap_backward", _fm_backward_mut("scale_missing")),
+    "bwd_featuremap_no_bias_grad": ("featuremap_backward", _fm_backward_mut("dW_no_bias_grad")),
+    "bwd_noncausal_drop_dden": ("attn_noncausal_backward", _nc_backward_mut("drop_dden")),
+    "bwd_noncausal_dphik_no_dz": ("attn_noncausal_backward", _nc_backward_mut("dphik_no_dz")),
+    "bwd_noncausal_dv_from_q": ("attn_noncausal_backward", _nc_backward_mut("dv_from_q")),
+    "bwd_causal_as_noncausal": ("attn_causal_backward", _cs_backward_mut("as_noncausal")),
+    "bwd_causal_prefix_for_keys": ("attn_causal_backward", _cs_backward_mut("prefix_for_keys")),
+    "bwd_causal_exclusive_suffix": ("attn_causal_backward", _cs_backward_mut("exclusive_suffix")),
     "psi_drop_g": ("psi", _psi_mut("drop_g")),
     "psi_sign_c": ("psi", _psi_mut("sign_c")),
     "psi_no_output_relu": ("psi", _psi_mut("no_output_relu")),

@@ -276,6 +276,60 @@ def featuremap_bench(args) -> int:
     return 0
 
 
+def backward_bench(args) -> int:
+    """luna_attn_bwd (input and parameter gradients) on the long encoder problem and on
+    the long causal problem: HIP events around each call.  The algorithmic bytes are
+    reading Q, K, V, dO and writing dQ, dK, dV once (7 d elements per token and head)."""
+    import numpy as np
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    luna.load_library()
+    stream = torch.cuda.current_stream(dev)
+    for name in ("long_noncausal", "long_causal"):
+        w = wl.WORKLOADS[name]
+        arrs = wl.make_inputs(w, args.seed)
+        p = wl.make_params(w, args.seed)
+        q, k, v = (torch.from_numpy(a).to(dev).to(torch.bfloat16) for a in arrs)
+        del arrs
+        do = torch.from_numpy(np.random.default_rng(args.seed + 7).standard_normal(q.shape).astype(np.float32))
+        do = do.to(dev).to(torch.bfloat16)
+        pt = luna.PhiParams.from_arrays(p, dev, torch.bfloat16)
+        for _ in range(args.warmup):
+            luna.attn_bwd(q, k, v, do, pt, causal=w.causal, eps=w.eps)
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for e0, e1 in ev:
+            e0.record(stream)
+            luna.attn_bwd(q, k, v, do, pt, causal=w.causal, eps=w.eps)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[len(ev) // 2]
+        th = w.B * w.H * w.n
+        nbytes = 7 * w.d * 2 * th
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        line = {
+            "metric": "LUNA attention backward tokens/sec (luna_attn_bwd, input and parameter gradients)",
+            "value": w.B * w.n / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded)",
+            "config": {"workload": f"{name} {w.B}x{w.H}x{w.n}x{w.d} D={w.M * w.L} "
+                                   f"{'causal chunk=64' if w.causal else 'non-causal'}, bf16 in, fp32 arithmetic"},
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "bytes_per_call": nbytes,
+                         "timing": "HIP events around each ABI call (median); workspace allocated per call by the "
+                                   "binding"},
+        }
+        print(json.dumps(line), flush=True)
+        del q, k, v, do, pt
+        torch.cuda.synchronize()
+    return 0
+
+
 # Counters that `--counters-from` summarises, with what each derived figure means.
 COUNTER_RATIOS = [
     ("VALU instructions per wave", "SQ_INSTS_VALU", "SQ_WAVES", 1.0),
@@ -586,6 +640,8 @@ def main() -> int:
                     help="summarise two rocprofv3 --pmc csv runs into profiles/hbm_traffic_*.json and exit")
     ap.add_argument("--traffic-command", default="",
                     help="the rocprofv3 commands that produced --traffic-from, recorded in the summary")
+    ap.add_argument("--backward", action="store_true",
+                    help="instead of the hot-path step: time luna_attn_bwd on the two long problems")
     ap.add_argument("--featuremap", action="store_true",
                     help="instead of the hot-path step: time luna_featuremap on the long encoder problem's queries")
     ap.add_argument("--counters-from", nargs="+", metavar="CSV",
@@ -612,13 +668,15 @@ def main() -> int:
         return traffic_from(*args.traffic_from, args.traffic_command)
     if args.counters_from:
         return counters_from(args.counters_from, args.counters_command)
-    if args.gpus != 1 and (args.decode or args.configs or args.featuremap):
+    if args.gpus != 1 and (args.decode or args.configs or args.featuremap or args.backward):
         print("bench.py runs on one GPU only; use --gpus 1.", file=sys.stderr)
         return 2
     if args.decode:
         return decode_bench(args)
     if args.featuremap:
         return featuremap_bench(args)
+    if args.backward:
+        return backward_bench(args)
     if args.configs:
         return configs_bench(args)
 

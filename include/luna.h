@@ -68,7 +68,9 @@ enum {
   LUNA_OP_ATTN = 1,
   LUNA_OP_ATTN_CAUSAL = 2,
   LUNA_OP_STATE = 3,       /* luna_attn_state */
-  LUNA_OP_CAUSAL_STEP = 4  /* luna_attn_causal_step (n = m, the new tokens) */
+  LUNA_OP_CAUSAL_STEP = 4, /* luna_attn_causal_step (n = m, the new tokens) */
+  LUNA_OP_ATTN_BWD = 5,    /* luna_attn_bwd, causal = 0 */
+  LUNA_OP_ATTN_CAUSAL_BWD = 6  /* luna_attn_bwd, causal = 1 */
 };
 
 /*
@@ -211,6 +213,42 @@ luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, l
                                   int64_t H, int64_t m, int64_t d, const luna_phi_params* p, float eps,
                                   int32_t tables_ready, float* S, float* z, void* out, void* ws, size_t ws_bytes,
                                   void* stream);
+
+/*
+ * Gradients of the feature-map parameters (fp32 device memory, shaped like the
+ * parameter arrays of luna_phi_params: W [P][M][d] (fp32 whatever the call's dtype),
+ * b [P][M], fc1_w and fc1_b [P][C1][hidden], fc2_w [P][L][hidden], fc2_b [P][L]).
+ */
+typedef struct luna_phi_grads {
+  float* W;
+  float* b;
+  float* fc1_w;
+  float* fc1_b;
+  float* fc2_w;
+  float* fc2_b;
+} luna_phi_grads;
+
+/*
+ * Backward pass of luna_attn_fwd (causal = 0) or luna_attn_fwd_causal (causal = 1),
+ * for training the feature map end to end (section 5.1) and the fine-tuning of
+ * converted models (section 5.2): for a loss L with dO = dL/dout [B, H, n, d], writes
+ *   dQ, dK, dV = dL/dQ, dL/dK, dL/dV   [B, H, n, d] in dtype (overwritten), and, if
+ *   grads is not NULL, the gradients of every feature-map parameter (overwritten),
+ * by the chain rule through out = phi(Q) S / (phi(Q) z + eps) (eq. (9) of Section 3.1,
+ * prefix states for the causal form) and phi of eq. (11) of Section 3.2 (Listing 1's
+ * channel MLPs, ReLU'(0) = 0).  Q, K, V, dO: [B, H, n, d] in dtype; same parameters and
+ * eps as the forward call.  All arithmetic is fp32 (the features are recomputed; the
+ * channel functions through their exact piecewise-linear form, whose slopes give
+ * dpsi/du).  Supported: d <= 128 (any of 32, 64, 128), M <= 64, L in {1, 2, 4, 8,
+ * 16}.  The workspace (LUNA_OP_ATTN_BWD / LUNA_OP_ATTN_CAUSAL_BWD in
+ * luna_workspace_bytes) holds the features, the per-chunk states and the partial
+ * parameter sums: about 4 (2 M L + 3 (d + 1)) bytes per token and head, plus
+ * 2 x 4 M L (d + 1) per chunk of 64 tokens for the causal form.
+ */
+luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const void* dO, luna_dtype dtype,
+                          int64_t B, int64_t H, int64_t n, int64_t d, const luna_phi_params* p,
+                          int32_t causal, float eps, void* dQ, void* dK, void* dV,
+                          const luna_phi_grads* grads, void* ws, size_t ws_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* luna_status_string(luna_status s);

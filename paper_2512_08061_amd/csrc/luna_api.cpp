@@ -57,7 +57,8 @@ luna_status check_common(const Problem& pb) {
   const int units = C1 * p->hidden;
   if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
   // the feature-map kernel (also the first stage of a streaming step) has the larger LDS table
-  const bool fm_table = pb.op == LUNA_OP_FEATUREMAP || pb.op == LUNA_OP_CAUSAL_STEP;
+  const bool fm_table = pb.op == LUNA_OP_FEATUREMAP || pb.op == LUNA_OP_CAUSAL_STEP || pb.op == LUNA_OP_ATTN_BWD ||
+                        pb.op == LUNA_OP_ATTN_CAUSAL_BWD;
   const int seg_cap = luna::nseg_cap(p->L, fm_table ? luna::kFmSegBytes : luna::kAttnSegBytes);
   if (units + 2 > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "too many breakpoints for the LDS segment table");
   if ((units + 1) * p->L > luna::kSegCap || (size_t)(units + 1) * luna::seg16_row_bytes(p->L) > luna::kSeg16Bytes)
@@ -69,6 +70,12 @@ struct Layout {
   size_t tables = 0, partial = 0, frags = 0, total = 0;
   size_t phiq = 0, phik = 0;  // streaming step: features of the new queries and keys (fp32)
   size_t zcopy = 0;           // streaming step: z as it was before the call
+  // backward pass: [V | 1], [num | den] then [dnum | dden], per-chunk states and their
+  // gradients, intra-chunk P and R (causal), feature gradients, dV in fp32 (bf16
+  // calls), per-workgroup parameter partials, their fp64 sums and moment prefixes
+  size_t vx = 0, y = 0, sx = 0, dsx = 0, pm = 0, rm = 0, dphiq = 0, dphik = 0, dvtmp = 0;
+  size_t bpart = 0, sum = 0, pre = 0;
+  int chunk = 0, nch = 1, groups = 0, part_floats = 0;
   int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
   size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
@@ -170,6 +177,38 @@ luna_status plan(const Problem& pb, Layout* lay) {
     off = align256(off + feat_bytes);
     lay->zcopy = off;
     off = align256(off + (size_t)heads * (size_t)(M * L) * sizeof(float));
+  } else if (pb.op == LUNA_OP_ATTN_BWD || pb.op == LUNA_OP_ATTN_CAUSAL_BWD) {
+    if (!luna::bwd_supported(d, L, M) || !luna::featuremap_supported(dt, d, L, M))
+      return fail(LUNA_ERR_UNSUPPORTED, "no backward kernels for this (d, L, M)");
+    const int64_t P = param_sets(pb);
+    if (P > 65535) return fail(LUNA_ERR_UNSUPPORTED, "at most 65535 parameter sets in the backward pass");
+    const bool causal = pb.op == LUNA_OP_ATTN_CAUSAL_BWD;
+    if (causal && pb.n > ((int64_t)1 << 30) / 64) return fail(LUNA_ERR_UNSUPPORTED, "n too large");
+    lay->chunk = causal ? 64 : (int)pb.n;
+    lay->nch = causal ? (int)((pb.n + 63) / 64) : 1;
+    const size_t D = (size_t)M * L, rows = (size_t)heads * (size_t)pb.n, states = (size_t)heads * lay->nch;
+    auto take = [&](size_t& at, size_t bytes) {
+      at = off;
+      off = align256(off + bytes);
+    };
+    take(lay->phiq, rows * D * 4);
+    take(lay->phik, rows * D * 4);
+    take(lay->vx, rows * (d + 1) * 4);
+    take(lay->y, rows * (d + 1) * 4);
+    take(lay->sx, states * D * (d + 1) * 4);
+    take(lay->dsx, states * D * (d + 1) * 4);
+    if (causal) {
+      take(lay->pm, states * 64 * 64 * 4);
+      take(lay->rm, states * 64 * 64 * 4);
+    }
+    take(lay->dphiq, rows * D * 4);
+    take(lay->dphik, rows * D * 4);
+    if (pb.dt == LUNA_BF16) take(lay->dvtmp, rows * d * 4);
+    lay->groups = luna::bwd_phi_groups(pb.n * (heads / P));
+    lay->part_floats = (int)luna::bwd_part_floats(d, L, M);
+    take(lay->bpart, (size_t)P * lay->groups * lay->part_floats * 4);
+    take(lay->sum, (size_t)P * lay->part_floats * 8);
+    take(lay->pre, (size_t)P * L * (luna::bwd_nseg_cap(L) + 1) * 2 * 8);
   } else {
     return fail(LUNA_ERR_INVALID_ARG, "unknown operation code");
   }
@@ -493,6 +532,162 @@ luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, l
   a.eps = eps;
   e = luna::launch_causal_step(dt, a, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "streaming step kernel launch");
+}
+
+luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const void* dO, luna_dtype dtype, int64_t B,
+                          int64_t H, int64_t n, int64_t d, const luna_phi_params* p, int32_t causal, float eps,
+                          void* dQ, void* dK, void* dV, const luna_phi_grads* grads, void* ws, size_t ws_bytes,
+                          void* stream) {
+  g_last_error.clear();
+  if (causal != 0 && causal != 1) return fail(LUNA_ERR_INVALID_ARG, "causal must be 0 or 1");
+  Problem pb{causal ? LUNA_OP_ATTN_CAUSAL_BWD : LUNA_OP_ATTN_BWD, dtype, B, H, n, d, p, 64};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (!Q || !K || !V || !dO || !dQ || !dK || !dV) return fail(LUNA_ERR_INVALID_ARG, "an input or output is NULL");
+  if (grads && (!grads->W || !grads->b || !grads->fc1_w || !grads->fc1_b || !grads->fc2_w || !grads->fc2_b))
+    return fail(LUNA_ERR_INVALID_ARG, "a parameter-gradient array is NULL");
+  if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int M = p->M, L = p->L, D = M * L, dd = (int)d, E = dd + 1;
+  const int heads = (int)(B * H), C = lay.chunk, nch = lay.nch;
+  const int64_t nD = n * D, nE = n * E, st_el = (int64_t)D * E, cc = (int64_t)C * C;
+  float* phiq = reinterpret_cast<float*>(w + lay.phiq);
+  float* phik = reinterpret_cast<float*>(w + lay.phik);
+  float* vx = reinterpret_cast<float*>(w + lay.vx);
+  float* y = reinterpret_cast<float*>(w + lay.y);
+  float* sx = reinterpret_cast<float*>(w + lay.sx);
+  float* dsx = reinterpret_cast<float*>(w + lay.dsx);
+  float* pm = reinterpret_cast<float*>(w + lay.pm);
+  float* rm = reinterpret_cast<float*>(w + lay.rm);
+  float* dphiq = reinterpret_cast<float*>(w + lay.dphiq);
+  float* dphik = reinterpret_cast<float*>(w + lay.dphik);
+  float* dvf = dt == luna::Dt::BF16 ? reinterpret_cast<float*>(w + lay.dvtmp) : static_cast<float*>(dV);
+  hipError_t e;
+#define LUNA_TRY(expr, what) \
+  if ((e = (expr)) != hipSuccess) return hip_fail(e, what)
+  // features of the queries and keys in fp32 (one launch)
+  luna::FeatureMapArgs f{};
+  f.phi = phi_args(pb, w, lay);
+  f.rows_per_head = n;
+  f.H = (int)H;
+  f.heads = B * H;
+  f.X = Q;
+  f.out = phiq;
+  f.X2 = K;
+  f.out2 = phik;
+  LUNA_TRY(luna::launch_featuremap(dt, luna::Dt::F32, dd, L, f, s), "feature-map kernel launch");
+  LUNA_TRY(luna::launch_bwd_pack(dt, V, vx, (int64_t)heads * n, dd, s), "pack kernel launch");
+  // C (+)= A B over (head, chunk); strides of (head, chunk, row, column) per operand
+  auto gemm = [&](const float* A, int64_t ah, int64_t ac, int64_t ai, int64_t ak, const float* Bm, int64_t bh,
+                  int64_t bc, int64_t bk, int64_t bj, float* Cm, int64_t ch, int64_t c2, int64_t ci, int64_t cj, int Mm,
+                  int Nn, int Kk, int mc, int nc, int kc, int lower, int acc) {
+    luna::BwdGemm g{};
+    g.A = A; g.sAh = ah; g.sAc = ac; g.sAi = ai; g.sAk = ak;
+    g.B = Bm; g.sBh = bh; g.sBc = bc; g.sBk = bk; g.sBj = bj;
+    g.C = Cm; g.sCh = ch; g.sCc = c2; g.sCi = ci; g.sCj = cj;
+    g.M = Mm; g.N = Nn; g.K = Kk;
+    g.heads = heads; g.chunks = nch; g.chunk = C; g.seq = (int)n;
+    g.m_chunk = mc; g.n_chunk = nc; g.k_chunk = kc; g.lower = lower; g.accumulate = acc;
+    return luna::launch_bwd_gemm(g, s);
+  };
+  const int64_t sh = (int64_t)nch * st_el;  // head stride of the per-chunk states
+  // per-chunk [S | z] = phi(K_c)^T [V_c | 1], then exclusive prefix over chunks (causal)
+  LUNA_TRY(gemm(phik, nD, (int64_t)C * D, 1, D, vx, nE, (int64_t)C * E, E, 1, sx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
+                0, 0), "state GEMM");
+  if (causal) LUNA_TRY(luna::launch_bwd_scan(sx, heads, nch, st_el, 0, s), "state scan");
+  // [num | den - eps] = phi(Q_c) [S_c | z_c] (+ P_c [V_c | 1], P_c = tril(phi(Q_c) phi(K_c)^T))
+  LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, sx, sh, st_el, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, D, 1, 0, 0,
+                0, 0), "readout GEMM");
+  if (causal) {
+    LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, phik, nD, (int64_t)C * D, 1, D, pm, nch * cc, cc, C, 1, C, C, D, 1,
+                  1, 0, 1, 0), "P GEMM");
+    LUNA_TRY(gemm(pm, nch * cc, cc, C, 1, vx, nE, (int64_t)C * E, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, C, 1, 0,
+                  1, 0, 1), "intra-chunk GEMM");
+  }
+  LUNA_TRY(luna::launch_bwd_g(dt, y, dO, (int64_t)heads * n, dd, eps, s), "denominator kernel launch");
+  // dphi(Q_c) = G_c [S_c | z_c]^T (+ R_c phi(K_c), R_c = tril(G_c [V_c | 1]^T))
+  LUNA_TRY(gemm(y, nE, (int64_t)C * E, E, 1, sx, sh, st_el, 1, E, dphiq, nD, (int64_t)C * D, D, 1, C, D, E, 1, 0, 0,
+                0, 0), "dphi(Q) GEMM");
+  if (causal) {
+    LUNA_TRY(gemm(y, nE, (int64_t)C * E, E, 1, vx, nE, (int64_t)C * E, 1, E, rm, nch * cc, cc, C, 1, C, C, E, 1, 1, 0,
+                  1, 0), "R GEMM");
+    LUNA_TRY(gemm(rm, nch * cc, cc, C, 1, phik, nD, (int64_t)C * D, D, 1, dphiq, nD, (int64_t)C * D, D, 1, C, D, C, 1,
+                  0, 1, 0, 1), "dphi(Q) intra-chunk GEMM");
+  }
+  // per-chunk [dS | dz] = phi(Q_c)^T G_c, then exclusive suffix over chunks (causal)
+  LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, 1, D, y, nE, (int64_t)C * E, E, 1, dsx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
+                0, 0), "state-gradient GEMM");
+  if (causal) LUNA_TRY(luna::launch_bwd_scan(dsx, heads, nch, st_el, 1, s), "state-gradient scan");
+  // dphi(K_c) = [V_c | 1] [dS_c | dz_c]^T (+ R_c^T phi(Q_c)); dV_c = phi(K_c) dS_c (+ P_c^T dnum_c)
+  LUNA_TRY(gemm(vx, nE, (int64_t)C * E, E, 1, dsx, sh, st_el, 1, E, dphik, nD, (int64_t)C * D, D, 1, C, D, E, 1, 0, 0,
+                0, 0), "dphi(K) GEMM");
+  LUNA_TRY(gemm(phik, nD, (int64_t)C * D, D, 1, dsx, sh, st_el, E, 1, dvf, n * dd, (int64_t)C * dd, dd, 1, C, dd, D, 1,
+                0, 0, 0, 0), "dV GEMM");
+  if (causal) {
+    LUNA_TRY(gemm(rm, nch * cc, cc, 1, C, phiq, nD, (int64_t)C * D, D, 1, dphik, nD, (int64_t)C * D, D, 1, C, D, C, 1,
+                  0, 1, 0, 1), "dphi(K) intra-chunk GEMM");
+    LUNA_TRY(gemm(pm, nch * cc, cc, 1, C, y, nE, (int64_t)C * E, E, 1, dvf, n * dd, (int64_t)C * dd, dd, 1, C, dd, C, 1,
+                  0, 1, 0, 1), "dV intra-chunk GEMM");
+  }
+  if (dt == luna::Dt::BF16) LUNA_TRY(luna::launch_bwd_convert(dt, dvf, dV, (int64_t)heads * n * dd, s), "dV convert");
+  // through the feature map: dQ, dK and the parameter partials
+  const int P = param_sets(pb);
+  luna::BwdPhi ph{};
+  ph.Q = Q;
+  ph.K = K;
+  ph.dphiq = dphiq;
+  ph.dphik = dphik;
+  ph.dQ = dQ;
+  ph.dK = dK;
+  ph.W = p->W;
+  ph.b = p->b;
+  ph.tables = w + lay.tables;
+  ph.partial = reinterpret_cast<float*>(w + lay.bpart);
+  ph.n = n;
+  ph.heads = B * H;
+  ph.H = (int)H;
+  ph.M = M;
+  ph.d = dd;
+  ph.per_head = p->per_head;
+  ph.part_floats = lay.part_floats;
+  LUNA_TRY(luna::launch_bwd_phi(dt, L, ph, lay.groups, P, s), "feature-map backward kernel launch");
+  if (grads) {
+    const int units = (p->shared_channels ? 1 : L) * p->hidden;
+    const int used = M * dd + M + 2 * (units + 1) * L;
+    double* sum = reinterpret_cast<double*>(w + lay.sum);
+    double* pre = reinterpret_cast<double*>(w + lay.pre);
+    LUNA_TRY(luna::launch_bwd_reduce(ph.partial, sum, lay.groups, lay.part_floats, used, P, s), "reduce kernel launch");
+    LUNA_TRY(luna::launch_bwd_prefix(sum, pre, w + lay.tables, M, dd, L, lay.part_floats, luna::bwd_nseg_cap(L), P, s),
+             "prefix kernel launch");
+    luna::BwdMlp m{};
+    m.sum = sum;
+    m.pre = pre;
+    m.tables = w + lay.tables;
+    m.fc1_w = p->fc1_w;
+    m.fc1_b = p->fc1_b;
+    m.fc2_w = p->fc2_w;
+    m.dW = grads->W;
+    m.db = grads->b;
+    m.dfc1_w = grads->fc1_w;
+    m.dfc1_b = grads->fc1_b;
+    m.dfc2_w = grads->fc2_w;
+    m.dfc2_b = grads->fc2_b;
+    m.M = M;
+    m.d = dd;
+    m.L = L;
+    m.hidden = p->hidden;
+    m.C1 = p->shared_channels ? 1 : L;
+    m.part_floats = lay.part_floats;
+    m.nseg_cap = luna::bwd_nseg_cap(L);
+    LUNA_TRY(luna::launch_bwd_mlp(m, P, s), "parameter-gradient kernel launch");
+  }
+#undef LUNA_TRY
+  return LUNA_OK;
 }
 
 const char* luna_status_string(luna_status s) {

@@ -170,6 +170,74 @@ struct StepArgs {
 };
 constexpr int kStepMaxD = 256;  // features the step kernel holds per column
 
+// Backward pass (luna_backward.hip).  Batched C (+)= A B over (head, chunk) with
+// strided fp32 operands: element (i, k) of A at A + h sAh + c sAc + i sAi + k sAk, and
+// so on.  Dimensions marked *_chunk are token dimensions of a chunk of `chunk`
+// tokens of a `seq`-token sequence (shorter in a ragged last chunk).  lower: entries
+// above the diagonal (j > i) of the product are stored as 0.
+struct BwdGemm {
+  const float* A;
+  const float* B;
+  float* C;
+  int M, N, K;
+  int64_t sAh, sAc, sAi, sAk;
+  int64_t sBh, sBc, sBk, sBj;
+  int64_t sCh, sCc, sCi, sCj;
+  int heads, chunks, chunk, seq;
+  int m_chunk, n_chunk, k_chunk;
+  int lower, accumulate;
+};
+
+// Feature-map backward over the rows of Q and K of every head.
+struct BwdPhi {
+  const void* Q;
+  const void* K;
+  const float* dphiq;  // [heads][n][M*L]
+  const float* dphik;
+  void* dQ;            // [heads][n][d], element type of the call
+  void* dK;
+  const void* W;       // [P][M][d]
+  const float* b;      // [P][M]
+  const uint8_t* tables;
+  float* partial;      // [P][groups][part_floats]: dW, db, then (segment, channel) moments
+  int64_t n, heads;
+  int H, M, d, per_head;
+  int part_floats;
+};
+
+// Channel-MLP parameter gradients from the reduced partials.
+struct BwdMlp {
+  const double* sum;   // [P][part_floats] (fp64)
+  const double* pre;   // [P][L][nseg_cap + 1][2]: exclusive prefix sums of the moments
+  const uint8_t* tables;
+  const float* fc1_w;
+  const float* fc1_b;
+  const float* fc2_w;
+  float* dW;
+  float* db;
+  float* dfc1_w;
+  float* dfc1_b;
+  float* dfc2_w;
+  float* dfc2_b;
+  int M, d, L, hidden, C1, part_floats, nseg_cap;
+};
+
+bool bwd_supported(int d, int L, int M);
+size_t bwd_part_floats(int d, int L, int M);
+int bwd_phi_groups(int64_t rows_per_set);
+int bwd_nseg_cap(int L);
+hipError_t launch_bwd_pack(Dt dt, const void* V, float* Vx, int64_t rows, int d, hipStream_t s);
+hipError_t launch_bwd_convert(Dt dt, const float* src, void* dst, int64_t n, hipStream_t s);
+hipError_t launch_bwd_gemm(const BwdGemm& g, hipStream_t s);
+hipError_t launch_bwd_scan(float* X, int heads, int chunks, int64_t elems, int suffix, hipStream_t s);
+hipError_t launch_bwd_g(Dt dt, float* Y, const void* dO, int64_t rows, int d, float eps, hipStream_t s);
+hipError_t launch_bwd_phi(Dt dt, int L, const BwdPhi& a, int groups, int sets, hipStream_t s);
+hipError_t launch_bwd_reduce(const float* partial, double* sum, int groups, int part_floats, int used, int sets,
+                             hipStream_t s);
+hipError_t launch_bwd_prefix(const double* sum, double* pre, const uint8_t* tables, int M, int d, int L,
+                             int part_floats, int nseg_cap, int sets, hipStream_t s);
+hipError_t launch_bwd_mlp(const BwdMlp& a, int sets, hipStream_t s);
+
 // Launchers; each returns hipSuccess or the launch error.  `ok` reports whether
 // a kernel exists for the (dtype, d, L, M) combination.
 hipError_t launch_prepare(const PrepareArgs& a, hipStream_t s);

@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "luna.h")
 
 LUNA_OK, LUNA_ERR_INVALID_ARG, LUNA_ERR_UNSUPPORTED, LUNA_ERR_WORKSPACE, LUNA_ERR_HIP = range(5)
 LUNA_F32, LUNA_BF16 = 0, 1
-OP_FEATUREMAP, OP_ATTN, OP_ATTN_CAUSAL, OP_STATE, OP_CAUSAL_STEP = 0, 1, 2, 3, 4
+OP_FEATUREMAP, OP_ATTN, OP_ATTN_CAUSAL, OP_STATE, OP_CAUSAL_STEP, OP_ATTN_BWD, OP_ATTN_CAUSAL_BWD = range(7)
 
 
 class LunaError(RuntimeError):
@@ -36,6 +36,10 @@ class PhiParamsC(ctypes.Structure):
         ("fc1_w", ctypes.c_void_p), ("fc1_b", ctypes.c_void_p),
         ("fc2_w", ctypes.c_void_p), ("fc2_b", ctypes.c_void_p),
     ]
+
+
+class PhiGradsC(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")]
 
 
 _lib = None
@@ -70,6 +74,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.luna_attn_causal_step.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, i32, vp, vp, vp,
                                           vp, sz, vp]
     lib.luna_attn_causal_step.restype = i32
+    lib.luna_attn_bwd.argtypes = [vp, vp, vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float, vp, vp, vp,
+                                  ctypes.POINTER(PhiGradsC), vp, sz, vp]
+    lib.luna_attn_bwd.restype = i32
     lib.luna_status_string.argtypes = [i32]
     lib.luna_status_string.restype = ctypes.c_char_p
     lib.luna_last_error.argtypes = []
@@ -249,6 +256,35 @@ def attn_fwd_causal_noalloc(Q, K, V, p: PhiParams, chunk: int = 64, eps: float =
 def noalloc_scratch_bytes() -> int:
     """Bytes of the static scratch behind attn_fwd_causal_noalloc."""
     return int(load_library().luna_noalloc_scratch_bytes())
+
+
+def attn_bwd(Q, K, V, dO, p: PhiParams, causal: bool = False, eps: float = 1e-6, param_grads: bool = True):
+    """Backward pass of attn_fwd (causal False) or attn_fwd_causal (causal True) for the
+    upstream gradient dO: returns (dQ, dK, dV, grads) with dQ, dK, dV like Q and grads a
+    dict of fp32 parameter gradients shaped like p's arrays (None if not param_grads)."""
+    torch = _torch()
+    lib = load_library()
+    B, H, n, d = _qkv_shape(Q, K, V)
+    if dO.shape != Q.shape or dO.dtype != Q.dtype or not dO.is_contiguous():
+        raise LunaError(LUNA_ERR_INVALID_ARG, "dO must be a contiguous tensor of Q's shape and dtype")
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    grads, gc = None, None
+    if param_grads:
+        grads = {name: torch.empty(getattr(p, name).shape, dtype=torch.float32, device=Q.device)
+                 for name in ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")}
+        gc = PhiGradsC(*(grads[k].data_ptr() for k in ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")))
+    pc = p.c()
+    dt = _dt(Q)
+    op = OP_ATTN_CAUSAL_BWD if causal else OP_ATTN_BWD
+    nb = lib.luna_workspace_bytes(op, dt, B, H, n, d, ctypes.byref(pc), 64)
+    args = (Q.data_ptr(), K.data_ptr(), V.data_ptr(), dO.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), int(causal), eps,
+            dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(), ctypes.byref(gc) if gc is not None else None)
+    if nb == 0:
+        _check(lib.luna_attn_bwd(*args, None, 0, None))
+    ws, wsp, wsn = _workspace(nb, Q.device)
+    _check(lib.luna_attn_bwd(*args, wsp, wsn, _stream_ptr(Q.device)))
+    dQ._luna_ws = ws
+    return dQ, dK, dV, grads
 
 
 def _state_tensors(B, H, D, d, device, S, z):

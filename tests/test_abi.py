@@ -23,7 +23,7 @@ def test_exports_every_declared_symbol(lib):
     names = luna.header_functions()
     assert set(names) == {"luna_workspace_bytes", "luna_featuremap", "luna_attn_fwd", "luna_attn_fwd_causal",
                           "luna_attn_state", "luna_attn_causal_step", "luna_status_string", "luna_last_error",
-                          "luna_attn_fwd_causal_noalloc", "luna_noalloc_scratch_bytes"}
+                          "luna_attn_fwd_causal_noalloc", "luna_noalloc_scratch_bytes", "luna_attn_bwd"}
     for name in names:
         assert hasattr(lib, name), name
 

@@ -74,6 +74,7 @@ struct Layout {
   // gradients, intra-chunk P and R (causal), feature gradients, dV in fp32 (bf16
   // calls), per-workgroup parameter partials, their fp64 sums and moment prefixes
   size_t vx = 0, y = 0, sx = 0, dsx = 0, pm = 0, rm = 0, dphiq = 0, dphik = 0, dvtmp = 0;
+  size_t xq = 0, xk = 0, wx = 0, uq = 0, uk = 0, duq = 0, duk = 0, dwh = 0;  // feature-map backward
   size_t bpart = 0, sum = 0, pre = 0;
   int chunk = 0, nch = 1, groups = 0, part_floats = 0;
   int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
@@ -184,8 +185,10 @@ luna_status plan(const Problem& pb, Layout* lay) {
     if (P > 65535) return fail(LUNA_ERR_UNSUPPORTED, "at most 65535 parameter sets in the backward pass");
     const bool causal = pb.op == LUNA_OP_ATTN_CAUSAL_BWD;
     if (causal && pb.n > ((int64_t)1 << 30) / 64) return fail(LUNA_ERR_UNSUPPORTED, "n too large");
-    lay->chunk = causal ? 64 : (int)pb.n;
-    lay->nch = causal ? (int)((pb.n + 63) / 64) : 1;
+    // causal: the 64-token chunks of the scan; non-causal: 512-token pieces of the sums
+    // over tokens, for parallelism only
+    lay->chunk = causal ? 64 : 512;
+    lay->nch = (int)((pb.n + lay->chunk - 1) / lay->chunk);
     const size_t D = (size_t)M * L, rows = (size_t)heads * (size_t)pb.n, states = (size_t)heads * lay->nch;
     auto take = [&](size_t& at, size_t bytes) {
       at = off;
@@ -204,7 +207,15 @@ luna_status plan(const Problem& pb, Layout* lay) {
     take(lay->dphiq, rows * D * 4);
     take(lay->dphik, rows * D * 4);
     if (pb.dt == LUNA_BF16) take(lay->dvtmp, rows * d * 4);
-    lay->groups = luna::bwd_phi_groups(pb.n * (heads / P));
+    take(lay->xq, rows * (d + 1) * 4);
+    take(lay->xk, rows * (d + 1) * 4);
+    take(lay->wx, (size_t)P * M * (d + 1) * 4);
+    take(lay->uq, rows * M * 4);
+    take(lay->uk, rows * M * 4);
+    take(lay->duq, rows * M * 4);
+    take(lay->duk, rows * M * 4);
+    take(lay->dwh, (size_t)heads * M * (d + 1) * 4);
+    lay->groups = luna::bwd_phi_groups(2 * pb.n * (heads / P) * M);
     lay->part_floats = (int)luna::bwd_part_floats(d, L, M);
     take(lay->bpart, (size_t)P * lay->groups * lay->part_floats * 4);
     take(lay->sum, (size_t)P * lay->part_floats * 8);
@@ -599,7 +610,7 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
   // per-chunk [S | z] = phi(K_c)^T [V_c | 1], then exclusive prefix over chunks (causal)
   LUNA_TRY(gemm(phik, nD, (int64_t)C * D, 1, D, vx, nE, (int64_t)C * E, E, 1, sx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
                 0, 0), "state GEMM");
-  if (causal) LUNA_TRY(luna::launch_bwd_scan(sx, heads, nch, st_el, 0, s), "state scan");
+  LUNA_TRY(luna::launch_bwd_scan(sx, heads, nch, st_el, causal ? 0 : 2, s), "state scan");
   // [num | den - eps] = phi(Q_c) [S_c | z_c] (+ P_c [V_c | 1], P_c = tril(phi(Q_c) phi(K_c)^T))
   LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, sx, sh, st_el, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, D, 1, 0, 0,
                 0, 0), "readout GEMM");
@@ -622,7 +633,7 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
   // per-chunk [dS | dz] = phi(Q_c)^T G_c, then exclusive suffix over chunks (causal)
   LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, 1, D, y, nE, (int64_t)C * E, E, 1, dsx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
                 0, 0), "state-gradient GEMM");
-  if (causal) LUNA_TRY(luna::launch_bwd_scan(dsx, heads, nch, st_el, 1, s), "state-gradient scan");
+  LUNA_TRY(luna::launch_bwd_scan(dsx, heads, nch, st_el, causal ? 1 : 2, s), "state-gradient scan");
   // dphi(K_c) = [V_c | 1] [dS_c | dz_c]^T (+ R_c^T phi(Q_c)); dV_c = phi(K_c) dS_c (+ P_c^T dnum_c)
   LUNA_TRY(gemm(vx, nE, (int64_t)C * E, E, 1, dsx, sh, st_el, 1, E, dphik, nD, (int64_t)C * D, D, 1, C, D, E, 1, 0, 0,
                 0, 0), "dphi(K) GEMM");
@@ -635,30 +646,72 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
                   0, 1, 0, 1), "dV intra-chunk GEMM");
   }
   if (dt == luna::Dt::BF16) LUNA_TRY(luna::launch_bwd_convert(dt, dvf, dV, (int64_t)heads * n * dd, s), "dV convert");
-  // through the feature map: dQ, dK and the parameter partials
+  // through the feature map: u = [x | 1] [W | b]^T, du (elementwise on the tables),
+  // [dW | db] = du^T [x | 1] and dx = du [W | b]
   const int P = param_sets(pb);
+  const int Hh = (int)H, Bb = (int)B;
+  float* xq = reinterpret_cast<float*>(w + lay.xq);
+  float* xk = reinterpret_cast<float*>(w + lay.xk);
+  float* wx = reinterpret_cast<float*>(w + lay.wx);
+  float* uq = reinterpret_cast<float*>(w + lay.uq);
+  float* uk = reinterpret_cast<float*>(w + lay.uk);
+  float* duq = reinterpret_cast<float*>(w + lay.duq);
+  float* duk = reinterpret_cast<float*>(w + lay.duk);
+  float* dwh = reinterpret_cast<float*>(w + lay.dwh);
+  LUNA_TRY(luna::launch_bwd_pack(dt, Q, xq, (int64_t)heads * n, dd, s), "pack kernel launch");
+  LUNA_TRY(luna::launch_bwd_pack(dt, K, xk, (int64_t)heads * n, dd, s), "pack kernel launch");
+  LUNA_TRY(luna::launch_bwd_packw(dt, p->W, p->b, wx, P * M, dd, s), "pack kernel launch");
+  // products over (batch, head) pairs: the batch index is the GEMM's head, the head its
+  // chunk, so that per-head parameters are addressed by stride
+  const int64_t wsc = p->per_head ? (int64_t)M * E : 0;
+  auto gemm_bh = [&](const float* A, int64_t ah, int64_t ac, int64_t ai, int64_t ak, const float* Bm, int64_t bh,
+                     int64_t bc, int64_t bk, int64_t bj, float* Cm, int64_t ch, int64_t c2, int64_t ci, int64_t cj, int Mm,
+                     int Nn, int Kk, int acc) {
+    luna::BwdGemm g{};
+    g.A = A; g.sAh = ah; g.sAc = ac; g.sAi = ai; g.sAk = ak;
+    g.B = Bm; g.sBh = bh; g.sBc = bc; g.sBk = bk; g.sBj = bj;
+    g.C = Cm; g.sCh = ch; g.sCc = c2; g.sCi = ci; g.sCj = cj;
+    g.M = Mm; g.N = Nn; g.K = Kk;
+    g.heads = Bb; g.chunks = Hh; g.chunk = (int)n; g.seq = (int)n;
+    g.accumulate = acc;
+    return luna::launch_bwd_gemm(g, s);
+  };
+  const int64_t nM = n * M, ME = (int64_t)M * E;
+  for (int side = 0; side < 2; ++side) {
+    const float* x = side ? xk : xq;
+    float* u = side ? uk : uq;
+    LUNA_TRY(gemm_bh(x, Hh * nE, nE, E, 1, wx, 0, wsc, 1, E, u, Hh * nM, nM, M, 1, (int)n, M, E, 0), "projection GEMM");
+  }
   luna::BwdPhi ph{};
-  ph.Q = Q;
-  ph.K = K;
+  ph.uq = uq;
+  ph.uk = uk;
   ph.dphiq = dphiq;
   ph.dphik = dphik;
-  ph.dQ = dQ;
-  ph.dK = dK;
-  ph.W = p->W;
-  ph.b = p->b;
+  ph.duq = duq;
+  ph.duk = duk;
   ph.tables = w + lay.tables;
   ph.partial = reinterpret_cast<float*>(w + lay.bpart);
   ph.n = n;
   ph.heads = B * H;
-  ph.H = (int)H;
+  ph.H = Hh;
   ph.M = M;
-  ph.d = dd;
   ph.per_head = p->per_head;
   ph.part_floats = lay.part_floats;
-  LUNA_TRY(luna::launch_bwd_phi(dt, L, ph, lay.groups, P, s), "feature-map backward kernel launch");
+  LUNA_TRY(luna::launch_bwd_phi(L, ph, lay.groups, P, s), "feature-map backward kernel launch");
+  for (int side = 0; side < 2; ++side) {
+    float* x = side ? xk : xq;
+    const float* du = side ? duk : duq;
+    if (grads)  // [dW | db] per (batch, head), both sides added
+      LUNA_TRY(gemm_bh(du, Hh * nM, nM, 1, M, x, Hh * nE, nE, E, 1, dwh, Hh * ME, ME, E, 1, M, E, (int)n, side),
+               "weight-gradient GEMM");
+    // dx = du [W | b] into x's rows (x is not read again), then its first d columns
+    LUNA_TRY(gemm_bh(du, Hh * nM, nM, M, 1, wx, 0, wsc, E, 1, x, Hh * nE, nE, E, 1, (int)n, E, M, 0), "dx GEMM");
+    LUNA_TRY(luna::launch_bwd_cols(dt, x, side ? dK : dQ, (int64_t)heads * n, dd, s), "dx convert");
+  }
   if (grads) {
+    LUNA_TRY(luna::launch_bwd_dw(dwh, grads->W, grads->b, Bb, Hh, M, dd, p->per_head, s), "weight-gradient sum");
     const int units = (p->shared_channels ? 1 : L) * p->hidden;
-    const int used = M * dd + M + 2 * (units + 1) * L;
+    const int used = 2 * (units + 1) * L;
     double* sum = reinterpret_cast<double*>(w + lay.sum);
     double* pre = reinterpret_cast<double*>(w + lay.pre);
     LUNA_TRY(luna::launch_bwd_reduce(ph.partial, sum, lay.groups, lay.part_floats, used, P, s), "reduce kernel launch");
@@ -671,14 +724,10 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
     m.fc1_w = p->fc1_w;
     m.fc1_b = p->fc1_b;
     m.fc2_w = p->fc2_w;
-    m.dW = grads->W;
-    m.db = grads->b;
     m.dfc1_w = grads->fc1_w;
     m.dfc1_b = grads->fc1_b;
     m.dfc2_w = grads->fc2_w;
     m.dfc2_b = grads->fc2_b;
-    m.M = M;
-    m.d = dd;
     m.L = L;
     m.hidden = p->hidden;
     m.C1 = p->shared_channels ? 1 : L;

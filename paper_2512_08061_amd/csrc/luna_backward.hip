@@ -18,20 +18,25 @@
 // and with the exclusive suffix state [dS_c | dz_c] after chunk c,
 //   dphi(K_c) = [V_c | 1] [dS_c | dz_c]^T + R_c^T phi(Q_c),
 //   dV_c = phi(K_c) dS_c + P_c^T dnum_c,
-// an exact regrouping of the sums.  The non-causal form is the same with one chunk of
-// the whole sequence, the total state in place of the prefix and suffix states and no
-// intra-chunk terms.
+// an exact regrouping of the sums.  The non-causal form is the same with the total
+// state in place of the prefix and suffix states and no intra-chunk terms (its
+// chunks only split the sums over tokens among more workgroups).
 //
 // Kernels (all arithmetic in fp32):
 //   bwd_pack_kernel     V -> [V | 1] in fp32;
 //   bwd_gemm_kernel     batched C (+)= A B over (head, chunk) with strided operands, a
 //                       lower-triangular output mask and ragged last chunks;
-//   bwd_scan_kernel     exclusive prefix or suffix sums of the per-chunk states;
+//   bwd_scan_kernel     exclusive prefix or suffix sums of the per-chunk states (or, for
+//                       the non-causal form, split into chunks only for parallelism,
+//                       their total);
 //   bwd_g_kernel        [num | den - eps] -> G = [dnum | dden];
-//   bwd_phi_kernel      dphi -> du (slopes of the piecewise-linear channel functions,
-//                       zero where the output ReLU is off) -> dx = du W, with per
-//                       workgroup partial dW, db and, per (segment, channel), the
-//                       moments sum dy and sum dy u of the channel outputs' gradients;
+//   bwd_packw_kernel    [W | b] in fp32: u = [x | 1] [W | b]^T, dx = du [W | b] (first d
+//                       columns), [dW | db] = du^T [x | 1] are GEMMs;
+//   bwd_phi_kernel      dphi -> du, one thread per (row, projection): the slopes of the
+//                       piecewise-linear channel functions, zero where the output ReLU
+//                       is off, and per workgroup the (segment, channel) moments sum dy
+//                       and sum dy u of the channel outputs' gradients;
+//   bwd_dw_kernel       [dW | db] summed over the (batch, head) products;
 //   bwd_reduce_kernel   the partials summed over workgroups (fp64);
 //   bwd_prefix_kernel   exclusive prefix sums of the moments over segments, per channel;
 //   bwd_mlp_kernel      the channel-MLP parameter gradients from the moments: unit k
@@ -70,13 +75,17 @@ __global__ __launch_bounds__(256) void bwd_convert_kernel(const float* __restric
 }
 
 // ---------------------------------------------------------------------------
-// batched strided GEMM, 64 x 64 output tiles, 16-deep k slices through LDS
+// batched strided GEMM on the fp32 matrix cores: 64 x 64 output tiles, four waves
+// of 32 x 32 (2 x 2 blocks of 16 x 16), 32-deep k slices through LDS.  A tile is kept
+// row-major (i, k) and B transposed (j, k), so that a lane's fragment -- row (or
+// column) lane % 16, k = 8 (lane / 16) + e for e < 8 -- is two 16-byte reads.  Tile
+// loads let consecutive threads walk the operand's unit-stride index.
 // ---------------------------------------------------------------------------
-constexpr int kGT = 64, kGK = 16;
+constexpr int kGT = 64, kGK = 32, kGP = kGK + 4;  // tile, k slice, LDS row (floats)
 
 __global__ __launch_bounds__(256) void bwd_gemm_kernel(BwdGemm g) {
-  __shared__ float As[kGK][kGT + 1];
-  __shared__ float Bs[kGK][kGT + 1];
+  __shared__ __attribute__((aligned(16))) float As[kGT][kGP];
+  __shared__ __attribute__((aligned(16))) float Bt[kGT][kGP];
   const int bz = blockIdx.z;
   const int h = bz / g.chunks, c = bz - h * g.chunks;
   const int rows_left = g.seq - c * g.chunk;  // tokens of this chunk (ragged last chunk)
@@ -88,69 +97,82 @@ __global__ __launch_bounds__(256) void bwd_gemm_kernel(BwdGemm g) {
   float* C = g.C + h * g.sCh + c * g.sCc;
   const int i0 = blockIdx.y * kGT, j0 = blockIdx.x * kGT;
   if (i0 >= Mv || j0 >= Nv) return;  // (uniform) tile outside this chunk's rows
-  const int tid = threadIdx.x;
-  const int ti = tid / 16, tj = tid % 16;  // 4 x 4 outputs: rows ti + 16 r, columns tj + 16 q
-  float acc[4][4];
+  const int tid = threadIdx.x, lane = tid % kWave, wave = wave_id();
+  const int grp = lane / 16, r = lane % 16;
+  const int wi = 32 * (wave / 2), wj = 32 * (wave % 2);  // this wave's 32 x 32 sub-tile
+  const bool a_krow = g.sAk == 1, b_jrow = g.sBj == 1;   // unit stride along k (A) or j (B)
+  f32x4 acc[2][2];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[r][q] = 0.0f;
+    for (int y = 0; y < 2; ++y) acc[x][y] = zero4();
   for (int k0 = 0; k0 < Kv; k0 += kGK) {
 #pragma unroll
     for (int e = 0; e < (kGK * kGT) / 256; ++e) {
       const int idx = tid + 256 * e;
-      const int kk = idx / kGT, ii = idx % kGT;
-      const int k = k0 + kk;
-      const int ia = i0 + ii, jb = j0 + ii;
-      As[kk][ii] = (k < Kv && ia < Mv) ? A[ia * g.sAi + k * g.sAk] : 0.0f;
-      Bs[kk][ii] = (k < Kv && jb < Nv) ? B[k * g.sBk + jb * g.sBj] : 0.0f;
+      int ii, kk;
+      if (a_krow) { kk = idx % kGK; ii = idx / kGK; }
+      else { ii = idx % kGT; kk = idx / kGT; }
+      const int ia = i0 + ii, ka = k0 + kk;
+      As[ii][kk] = (ka < Kv && ia < Mv) ? A[ia * g.sAi + ka * g.sAk] : 0.0f;
+      int jj, kb;
+      if (b_jrow) { jj = idx % kGT; kb = idx / kGT; }
+      else { kb = idx % kGK; jj = idx / kGK; }
+      const int jb = j0 + jj, kbb = k0 + kb;
+      Bt[jj][kb] = (kbb < Kv && jb < Nv) ? B[kbb * g.sBk + jb * g.sBj] : 0.0f;
     }
     __syncthreads();
+    Frag<float> af[2], bf[2];
 #pragma unroll
-    for (int kk = 0; kk < kGK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) a[r] = As[kk][ti + 16 * r];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) b[q] = Bs[kk][tj + 16 * q];
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[r][q] = fmaf(a[r], b[q], acc[r][q]);
+    for (int x = 0; x < 2; ++x) {
+      const float4* pa = reinterpret_cast<const float4*>(&As[wi + 16 * x + r][8 * grp]);
+      const float4* pb = reinterpret_cast<const float4*>(&Bt[wj + 16 * x + r][8 * grp]);
+      const float4 a0 = pa[0], a1 = pa[1], b0 = pb[0], b1 = pb[1];
+      af[x].v[0] = a0.x; af[x].v[1] = a0.y; af[x].v[2] = a0.z; af[x].v[3] = a0.w;
+      af[x].v[4] = a1.x; af[x].v[5] = a1.y; af[x].v[6] = a1.z; af[x].v[7] = a1.w;
+      bf[x].v[0] = b0.x; bf[x].v[1] = b0.y; bf[x].v[2] = b0.z; bf[x].v[3] = b0.w;
+      bf[x].v[4] = b1.x; bf[x].v[5] = b1.y; bf[x].v[6] = b1.z; bf[x].v[7] = b1.w;
     }
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y) mma(acc[x][y], af[x], bf[y]);
     __syncthreads();
   }
+  // acc[x][y] holds rows 4 grp + q (q < 4), column r of block (x, y)
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int i = i0 + ti + 16 * r;
-    if (i >= Mv) continue;
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = j0 + tj + 16 * q;
-      if (j >= Nv) continue;
-      float v = (g.lower && j > i) ? 0.0f : acc[r][q];
-      float* p = C + i * g.sCi + j * g.sCj;
-      if (g.accumulate) v += *p;
-      *p = v;
-    }
-  }
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + wi + 16 * x + 4 * grp + q, j = j0 + wj + 16 * y + r;
+        if (i >= Mv || j >= Nv) continue;
+        float v = (g.lower && j > i) ? 0.0f : acc[x][y][q];
+        float* pc = C + i * g.sCi + j * g.sCj;
+        if (g.accumulate) v += *pc;
+        *pc = v;
+      }
 }
 
 // ---------------------------------------------------------------------------
 // exclusive prefix (forward) or suffix (backward) sums over chunks, in place
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void bwd_scan_kernel(float* X, int heads, int chunks, int64_t elems, int suffix) {
+// mode 0: exclusive prefix, 1: exclusive suffix, 2: the total in every chunk
+__global__ __launch_bounds__(256) void bwd_scan_kernel(float* X, int heads, int chunks, int64_t elems, int mode) {
   const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   const int h = blockIdx.y;
   if (e >= elems || h >= heads) return;
   float* base = X + (int64_t)h * chunks * elems + e;
   float run = 0.0f;
   for (int i = 0; i < chunks; ++i) {
-    const int c = suffix ? chunks - 1 - i : i;
+    const int c = mode == 1 ? chunks - 1 - i : i;
     const float v = base[(int64_t)c * elems];
-    base[(int64_t)c * elems] = run;
+    if (mode != 2) base[(int64_t)c * elems] = run;
     run += v;
   }
+  if (mode == 2)
+    for (int c = 0; c < chunks; ++c) base[(int64_t)c * elems] = run;
 }
 
 // ---------------------------------------------------------------------------
@@ -175,120 +197,133 @@ __global__ __launch_bounds__(256) void bwd_g_kernel(float* __restrict__ Y, const
 }
 
 // ---------------------------------------------------------------------------
-// feature-map backward
+// [W | b] in fp32, per parameter set: the projection u = [x | 1] [W | b]^T
 // ---------------------------------------------------------------------------
-constexpr int kPhiRows = 32;  // rows per tile
-constexpr int kPhiMaxM = 64, kPhiMaxD = 128;
+template <typename T>
+__global__ __launch_bounds__(256) void bwd_packw_kernel(const T* __restrict__ W, const float* __restrict__ b,
+                                                        float* __restrict__ Wx, int rows, int d) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * (d + 1)) return;
+  const int r = i / (d + 1), c = i - r * (d + 1);
+  Wx[i] = c < d ? (float)W[(size_t)r * d + c] : b[r];
+}
 
-template <typename T, int L>
+// ---------------------------------------------------------------------------
+// feature-map backward: one thread per (row, projection).  From u and dphi of the
+// row, on u's segment: y'_l = s'_l u + t'_l (the table's slope and intercept, scaled by
+// 1/sqrt(M)), g_l = dphi_l where the output ReLU passes (y' > 0, or always without
+// it), du = sum_l g_l s'_l, and into the (segment, channel) moments dy_l = g_l / sqrt(M)
+// and dy_l u (LDS, one copy per workgroup, written out as partials).
+// ---------------------------------------------------------------------------
+template <int L>
 __global__ __launch_bounds__(256) void bwd_phi_kernel(BwdPhi a) {
   constexpr int NSEG = nseg_cap(L, kFmSegBytes);
   __shared__ PwlLds<L, NSEG> tab;
-  __shared__ float Ws[kPhiMaxM * kPhiMaxD];
-  __shared__ float xs[kPhiRows][kPhiMaxD + 1];
-  __shared__ float dus[kPhiRows][kPhiMaxM + 1];
-  __shared__ float mom[NSEG * L][2];  // per (segment, channel): sum dy, sum dy u
-
-  const int set = blockIdx.y;  // parameter set; its workgroups share the tiles of its heads
-  const int tid = threadIdx.x;
-  const int M = a.M, d = a.d, D = M * L;
-  const float* bias = a.b + (size_t)set * M;
-  const T* W = reinterpret_cast<const T*>(a.W) + (size_t)set * M * d;
+  // per (channel, segment): sum dy and sum dy u, channel-major so that the lanes of
+  // one atomic instruction (one channel, random segments) spread over the banks
+  __shared__ float m0[L][NSEG], m1[L][NSEG];
+  const int set = blockIdx.y, tid = threadIdx.x;
+  const int M = a.M, D = M * L;
   pwl_load(tab, a.tables + (size_t)set * kTableBytes);
-  for (int i = tid; i < M * d; i += blockDim.x) Ws[i] = (float)W[i];
-  for (int i = tid; i < NSEG * L; i += blockDim.x) mom[i][0] = mom[i][1] = 0.0f;
+  for (int i = tid; i < NSEG * L; i += blockDim.x) {
+    m0[i / NSEG][i % NSEG] = 0.0f;
+    m1[i / NSEG][i % NSEG] = 0.0f;
+  }
   __syncthreads();
   const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
   const float floor = tab.floor;
   const float rsm = 1.0f / sqrtf((float)M);
-
-  // this thread's share of the partial dW (rows i, columns c: entries tid, tid + 256, ...)
-  constexpr int kMaxW = kPhiMaxM * kPhiMaxD / 256;
-  float dw[kMaxW];
-#pragma unroll
-  for (int e = 0; e < kMaxW; ++e) dw[e] = 0.0f;
-  float dbias = 0.0f;  // thread i < M: partial db_i
-
-  // tiles: rows of the heads of this parameter set, Q rows then K rows
   const int64_t heads_in_set = a.per_head ? a.heads / a.H : a.heads;
-  const int64_t tiles_per_head = (a.n + kPhiRows - 1) / kPhiRows;
-  const int64_t tiles = 2 * heads_in_set * tiles_per_head;
-  const int r = tid / 8, pg = tid % 8;  // row of the tile, projection group (i = pg, pg + 8, ...)
-  for (int64_t it = blockIdx.x; it < tiles; it += gridDim.x) {
-    const int side = (int)(it / (heads_in_set * tiles_per_head));  // 0: Q rows, 1: K rows
-    const int64_t rest = it - side * heads_in_set * tiles_per_head;
-    const int64_t hs = rest / tiles_per_head;
-    const int64_t t0 = (rest - hs * tiles_per_head) * kPhiRows;
-    const int64_t head = a.per_head ? hs * a.H + set : hs;
-    const T* X = reinterpret_cast<const T*>(side ? a.K : a.Q) + head * a.n * d;
-    const float* dphi = (side ? a.dphik : a.dphiq) + head * a.n * D;
-    T* dX = reinterpret_cast<T*>(side ? a.dK : a.dQ) + head * a.n * d;
-    const int rows = (int)min((int64_t)kPhiRows, a.n - t0);
-    __syncthreads();  // the previous tile's xs and dus are no longer read
-    for (int i = tid; i < kPhiRows * d; i += blockDim.x) {
-      const int rr = i / d, cc = i - rr * d;
-      xs[rr][cc] = rr < rows ? (float)X[(t0 + rr) * d + cc] : 0.0f;
-    }
-    __syncthreads();
-    if (r < rows) {
-      const float* g = dphi + (t0 + r) * D;
-      for (int i = pg; i < M; i += 8) {
-        float u = bias[i];
-        for (int cc = 0; cc < d; ++cc) u = fmaf(Ws[i * d + cc], xs[r][cc], u);
-        float uu[1] = {u};
-        int sg[1];
-        pwl_search(tab, steps, uu, sg);
-        const float4* row = reinterpret_cast<const float4*>(seg_ptr(tab, sg[0]));
-        float du = 0.0f;
+  const int64_t per_side = heads_in_set * a.n * M;  // elements (row, projection) of one side
+  const int64_t total = 2 * per_side;
+  // NB elements per thread and round, their loads issued before any is used
+  constexpr int NB = 4;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e0 = blockIdx.x * (int64_t)blockDim.x + tid; e0 < total; e0 += NB * stride) {
+    float u[NB], gv[NB][L];
+    int64_t ui[NB];
+    int side[NB];
 #pragma unroll
-        for (int l = 0; l < L; ++l) {
-          const float2 st = reinterpret_cast<const float2*>(row)[l];
-          const float y = fmaf(st.x, u, st.y);                 // pre-ReLU channel output / sqrt(M)
-          const float gl = (y > floor) ? g[i * L + l] : 0.0f;  // floor: 0 (output ReLU) or -inf
-          du = fmaf(gl, st.x, du);
-          const float dy = gl * rsm;                            // dL / dy_l
-          atomicAdd(&mom[sg[0] * L + l][0], dy);
-          atomicAdd(&mom[sg[0] * L + l][1], dy * u);
+    for (int b = 0; b < NB; ++b) {
+      const int64_t e = min(e0 + b * stride, total - 1);  // (clamped: loads stay in range)
+      side[b] = e >= per_side;
+      const int64_t el = e - side[b] * per_side;
+      const int64_t hs = el / (a.n * M);
+      const int64_t rest = el - hs * a.n * M;  // t M + i
+      const int i = (int)(rest % M);
+      const int64_t head = a.per_head ? hs * a.H + set : hs;
+      ui[b] = head * a.n * M + rest;
+      u[b] = (side[b] ? a.uk : a.uq)[ui[b]];
+      const float* g = (side[b] ? a.dphik : a.dphiq) + head * a.n * D + (rest - i) / M * D + (int64_t)i * L;
+      if constexpr (L % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < L / 4; ++q) {
+          const float4 v = reinterpret_cast<const float4*>(g)[q];
+          gv[b][4 * q] = v.x; gv[b][4 * q + 1] = v.y; gv[b][4 * q + 2] = v.z; gv[b][4 * q + 3] = v.w;
         }
-        dus[r][i] = du;
-      }
-    }
-    __syncthreads();
-    // dx = du W for the tile's rows; partial dW += du^T x; db += du
-    for (int i = tid; i < kPhiRows * d; i += blockDim.x) {
-      const int rr = i / d, cc = i - rr * d;
-      if (rr < rows) {
-        float s = 0.0f;
-        for (int p = 0; p < M; ++p) s = fmaf(dus[rr][p], Ws[p * d + cc], s);
-        dX[(t0 + rr) * d + cc] = (T)s;
-      }
-    }
+      } else {
 #pragma unroll
-    for (int e = 0; e < kMaxW; ++e) {
-      const int idx = tid + 256 * e;
-      if (idx < M * d) {
-        const int i = idx / d, cc = idx - i * d;
-        float s = 0.0f;
-        for (int rr = 0; rr < rows; ++rr) s = fmaf(dus[rr][i], xs[rr][cc], s);
-        dw[e] += s;
+        for (int l = 0; l < L; ++l) gv[b][l] = g[l];
       }
     }
-    if (tid < M)
-      for (int rr = 0; rr < rows; ++rr) dbias += dus[rr][tid];
+    int sg[NB];
+    pwl_search(tab, steps, u, sg);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (e0 + b * stride >= total) break;
+      const float2* row = reinterpret_cast<const float2*>(seg_ptr(tab, sg[b]));
+      float du = 0.0f;
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        const float2 st = row[l];
+        const float gl = fmaf(st.x, u[b], st.y) > floor ? gv[b][l] : 0.0f;  // floor: 0 (output ReLU) or -inf
+        du = fmaf(gl, st.x, du);
+        if (gl != 0.0f) {  // (channels cut by the output ReLU add nothing)
+          const float dy = gl * rsm;
+          atomicAdd(&m0[l][sg[b]], dy);
+          atomicAdd(&m1[l][sg[b]], dy * u[b]);
+        }
+      }
+      (side[b] ? a.duk : a.duq)[ui[b]] = du;
+    }
   }
   __syncthreads();
-  // partials of this workgroup
   float* part = a.partial + ((size_t)set * gridDim.x + blockIdx.x) * a.part_floats;
-#pragma unroll
-  for (int e = 0; e < kMaxW; ++e) {
-    const int idx = tid + 256 * e;
-    if (idx < M * d) part[idx] = dw[e];
-  }
-  if (tid < M) part[M * d + tid] = dbias;
   const int nm = tab.zero_seg * L;  // real segments x channels
-  for (int i = tid; i < nm; i += blockDim.x) {
-    part[M * d + M + 2 * i] = mom[i][0];
-    part[M * d + M + 2 * i + 1] = mom[i][1];
+  for (int i = tid; i < nm; i += blockDim.x) {  // partials as [segment][channel][2]
+    part[2 * i] = m0[i % L][i / L];
+    part[2 * i + 1] = m1[i % L][i / L];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// [dW | db] per parameter set from the per-(batch, head) products dU^T [X | 1]
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void bwd_dw_kernel(const float* __restrict__ dwh, float* __restrict__ dW,
+                                                     float* __restrict__ db, int B, int H, int M, int d,
+                                                     int per_head) {
+  const int E = d + 1;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;  // (set, i, c)
+  const int sets = per_head ? H : 1;
+  if (idx >= sets * M * E) return;
+  const int set = idx / (M * E), rest = idx - set * M * E;
+  double s = 0.0;
+  for (int bb = 0; bb < B; ++bb)
+    for (int hh = per_head ? set : 0; hh < (per_head ? set + 1 : H); ++hh)
+      s += (double)dwh[((size_t)bb * H + hh) * M * E + rest];
+  const int i = rest / E, c = rest - i * E;
+  if (c < d) dW[((size_t)set * M + i) * d + c] = (float)s;
+  else db[(size_t)set * M + i] = (float)s;
+}
+
+// dX rows [rows][d + 1] (fp32, the last column unused) -> [rows][d] in the call's dtype
+template <typename T>
+__global__ __launch_bounds__(256) void bwd_cols_kernel(const float* __restrict__ src, T* __restrict__ dst, int64_t rows,
+                                                       int d) {
+  const int64_t n = rows * d;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / d;
+    dst[i] = (T)src[i + r];  // row r starts at r (d + 1)
   }
 }
 
@@ -319,7 +354,7 @@ __global__ __launch_bounds__(1024) void bwd_prefix_kernel(const double* __restri
   const int l = blockIdx.x, set = blockIdx.y, tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
   const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(tables + (size_t)set * kTableBytes + kTabHeader);
   const int nseg = min(max(hd.nbp, 0) + 1, nseg_cap);
-  const double* mom = sum + (size_t)set * part_floats + (size_t)M * d + M;  // [nseg][L][2]
+  const double* mom = sum + (size_t)set * part_floats;  // [nseg][L][2]
   double* out = pre + ((size_t)set * L + l) * (nseg_cap + 1) * 2;
   double run0 = 0.0, run1 = 0.0;  // the sums of the previous 1024-segment blocks
   for (int j0 = 0; j0 <= nseg; j0 += 1024) {
@@ -374,11 +409,7 @@ __global__ __launch_bounds__(256) void bwd_mlp_kernel(BwdMlp a) {
   const int nseg = nbp + 1;
   const float* gkeys = reinterpret_cast<const float*>(tab + kTabKeys);
   for (int i = tid; i < nbp; i += blockDim.x) keys[i] = gkeys[i];
-  const double* sum = a.sum + (size_t)set * a.part_floats;
-  const int M = a.M, d = a.d, L = a.L, hidden = a.hidden, C1 = a.C1;
-  // dW and db straight from the sums
-  for (int i = tid; i < M * d; i += blockDim.x) a.dW[(size_t)set * M * d + i] = (float)sum[i];
-  for (int i = tid; i < M; i += blockDim.x) a.db[(size_t)set * M + i] = (float)sum[M * d + i];
+  const int L = a.L, hidden = a.hidden, C1 = a.C1;
   __syncthreads();
   const float* A = a.fc1_w + (size_t)set * C1 * hidden;
   const float* Cc = a.fc1_b + (size_t)set * C1 * hidden;
@@ -475,12 +506,12 @@ hipError_t launch_bwd_gemm(const BwdGemm& g, hipStream_t s) {
   return hipSuccess;
 }
 
-hipError_t launch_bwd_scan(float* X, int heads, int chunks, int64_t elems, int suffix, hipStream_t s) {
+hipError_t launch_bwd_scan(float* X, int heads, int chunks, int64_t elems, int mode, hipStream_t s) {
   for (int h0 = 0; h0 < heads; h0 += 65535) {  // at most 65535 heads per launch
     const int hn = std::min(65535, heads - h0);
     const dim3 grid((unsigned)((elems + 255) / 256), (unsigned)hn);
     hipLaunchKernelGGL(bwd_scan_kernel, grid, dim3(256), 0, s, X + (int64_t)h0 * chunks * elems, hn, chunks, elems,
-                       suffix);
+                       mode);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -495,35 +526,49 @@ hipError_t launch_bwd_g(Dt dt, float* Y, const void* dO, int64_t rows, int d, fl
 }
 
 int bwd_phi_groups(int64_t rows_per_set) {
-  const int64_t tiles = 2 * ((rows_per_set + kPhiRows - 1) / kPhiRows);
-  return (int)std::max<int64_t>(1, std::min<int64_t>(tiles, 256));
+  return (int)std::max<int64_t>(1, std::min<int64_t>((rows_per_set + 1023) / 1024, 512));
 }
 
 bool bwd_supported(int d, int L, int M) {
   const bool lok = L == 1 || L == 2 || L == 4 || L == 8 || L == 16;
-  return lok && M >= 1 && M <= kPhiMaxM && d >= 1 && d <= kPhiMaxD;
+  return lok && M >= 1 && M <= 64 && d >= 1 && d <= 128;
 }
 
-size_t bwd_part_floats(int d, int L, int M) {
-  return (size_t)M * d + M + 2 * (size_t)nseg_cap(L, kFmSegBytes) * L;
+size_t bwd_part_floats(int, int L, int) { return 2 * (size_t)nseg_cap(L, kFmSegBytes) * L; }
+
+hipError_t launch_bwd_packw(Dt dt, const void* W, const float* b, float* Wx, int rows, int d, hipStream_t s) {
+  const dim3 grid((unsigned)((rows * (d + 1) + 255) / 256)), block(256);
+  if (dt == Dt::BF16) hipLaunchKernelGGL(bwd_packw_kernel<__bf16>, grid, block, 0, s, (const __bf16*)W, b, Wx, rows, d);
+  else hipLaunchKernelGGL(bwd_packw_kernel<float>, grid, block, 0, s, (const float*)W, b, Wx, rows, d);
+  return hipGetLastError();
 }
 
-template <typename T>
-static hipError_t phi_dispatch(int L, const BwdPhi& a, dim3 grid, hipStream_t s) {
+hipError_t launch_bwd_phi(int L, const BwdPhi& a, int groups, int sets, hipStream_t s) {
+  const dim3 grid((unsigned)groups, (unsigned)sets);
   switch (L) {
-    case 1: hipLaunchKernelGGL((bwd_phi_kernel<T, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((bwd_phi_kernel<T, 2>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((bwd_phi_kernel<T, 4>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((bwd_phi_kernel<T, 8>), grid, dim3(256), 0, s, a); break;
-    case 16: hipLaunchKernelGGL((bwd_phi_kernel<T, 16>), grid, dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL(bwd_phi_kernel<1>, grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL(bwd_phi_kernel<2>, grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL(bwd_phi_kernel<4>, grid, dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL(bwd_phi_kernel<8>, grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL(bwd_phi_kernel<16>, grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_phi(Dt dt, int L, const BwdPhi& a, int groups, int sets, hipStream_t s) {
-  const dim3 grid((unsigned)groups, (unsigned)sets);
-  return dt == Dt::BF16 ? phi_dispatch<__bf16>(L, a, grid, s) : phi_dispatch<float>(L, a, grid, s);
+hipError_t launch_bwd_dw(const float* dwh, float* dW, float* db, int B, int H, int M, int d, int per_head,
+                         hipStream_t s) {
+  const int total = (per_head ? H : 1) * M * (d + 1);
+  hipLaunchKernelGGL(bwd_dw_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, dwh, dW, db, B, H, M, d,
+                     per_head);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_cols(Dt dt, const float* src, void* dst, int64_t rows, int d, hipStream_t s) {
+  const dim3 grid((unsigned)std::min<int64_t>((rows * d + 255) / 256, 65536)), block(256);
+  if (dt == Dt::BF16) hipLaunchKernelGGL(bwd_cols_kernel<__bf16>, grid, block, 0, s, src, (__bf16*)dst, rows, d);
+  else hipLaunchKernelGGL(bwd_cols_kernel<float>, grid, block, 0, s, src, (float*)dst, rows, d);
+  return hipGetLastError();
 }
 
 hipError_t launch_bwd_reduce(const float* partial, double* sum, int groups, int part_floats, int used, int sets,

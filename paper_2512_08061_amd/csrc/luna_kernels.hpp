@@ -188,20 +188,19 @@ struct BwdGemm {
   int lower, accumulate;
 };
 
-// Feature-map backward over the rows of Q and K of every head.
+// Feature-map backward over the rows of Q and K of every head, one thread per
+// (row, projection): du from dphi and u, and the (segment, channel) moments.
 struct BwdPhi {
-  const void* Q;
-  const void* K;
+  const float* uq;     // [heads][n][M] projections u = x W^T + b
+  const float* uk;
   const float* dphiq;  // [heads][n][M*L]
   const float* dphik;
-  void* dQ;            // [heads][n][d], element type of the call
-  void* dK;
-  const void* W;       // [P][M][d]
-  const float* b;      // [P][M]
+  float* duq;          // [heads][n][M]
+  float* duk;
   const uint8_t* tables;
-  float* partial;      // [P][groups][part_floats]: dW, db, then (segment, channel) moments
+  float* partial;      // [P][groups][part_floats]: (segment, channel) moments
   int64_t n, heads;
-  int H, M, d, per_head;
+  int H, M, per_head;
   int part_floats;
 };
 
@@ -213,13 +212,11 @@ struct BwdMlp {
   const float* fc1_w;
   const float* fc1_b;
   const float* fc2_w;
-  float* dW;
-  float* db;
   float* dfc1_w;
   float* dfc1_b;
   float* dfc2_w;
   float* dfc2_b;
-  int M, d, L, hidden, C1, part_floats, nseg_cap;
+  int L, hidden, C1, part_floats, nseg_cap;
 };
 
 bool bwd_supported(int d, int L, int M);
@@ -229,9 +226,13 @@ int bwd_nseg_cap(int L);
 hipError_t launch_bwd_pack(Dt dt, const void* V, float* Vx, int64_t rows, int d, hipStream_t s);
 hipError_t launch_bwd_convert(Dt dt, const float* src, void* dst, int64_t n, hipStream_t s);
 hipError_t launch_bwd_gemm(const BwdGemm& g, hipStream_t s);
-hipError_t launch_bwd_scan(float* X, int heads, int chunks, int64_t elems, int suffix, hipStream_t s);
+hipError_t launch_bwd_scan(float* X, int heads, int chunks, int64_t elems, int mode, hipStream_t s);
 hipError_t launch_bwd_g(Dt dt, float* Y, const void* dO, int64_t rows, int d, float eps, hipStream_t s);
-hipError_t launch_bwd_phi(Dt dt, int L, const BwdPhi& a, int groups, int sets, hipStream_t s);
+hipError_t launch_bwd_packw(Dt dt, const void* W, const float* b, float* Wx, int rows, int d, hipStream_t s);
+hipError_t launch_bwd_phi(int L, const BwdPhi& a, int groups, int sets, hipStream_t s);
+hipError_t launch_bwd_dw(const float* dwh, float* dW, float* db, int B, int H, int M, int d, int per_head,
+                         hipStream_t s);
+hipError_t launch_bwd_cols(Dt dt, const float* src, void* dst, int64_t rows, int d, hipStream_t s);
 hipError_t launch_bwd_reduce(const float* partial, double* sum, int groups, int part_floats, int used, int sets,
                              hipStream_t s);
 hipError_t launch_bwd_prefix(const double* sum, double* pre, const uint8_t* tables, int M, int d, int L,

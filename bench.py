@@ -580,8 +580,12 @@ def configs_bench(args) -> int:
         tf = flops_per_token_head(w, w.causal) * th / 1e12
         mfma_peak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
         t_hbm, t_mfma = gb / HBM_PEAK_GBS, tf / mfma_peak
+        # shapes without a fused kernel run the fp32 GEMM path, whose workspace holds the
+        # fp32 features of the queries and keys (8 M L bytes per token and head)
+        generic = plan.ws_bytes >= 8 * w.M * w.L * th
         rec.update({
             "status": "ok",
+            "path": "fp32 GEMM" if generic else "fused",
             "ms_median": round(ms, 5), "ms_p10": round(pick(0.1), 5), "ms_p90": round(pick(0.9), 5),
             "tokens_per_s": w.B * w.n / (ms / 1e3),
             "head_tokens_per_s": th / (ms / 1e3),
@@ -607,17 +611,19 @@ def configs_bench(args) -> int:
                      "TFLOP/s counts the matrix-core work (projections, S, readout, z, denominators, and for "
                      "causal the full 64x64 intra-chunk blocks); the floor is the larger of the HBM time of the "
                      "algorithmic bytes (read Q, K, V, write out) at 8 TB/s and the MFMA time at the dtype's "
-                     "dense peak.\n\n")
-            fh.write("| config | B,H,n,d | M x L | dtype | causal | median us (p10-p90) | tokens/s | head-tokens/s "
-                     "| TFLOP/s | GB/s | floor us | roofline |\n|---|---|---|---|---|---|---|---|---|---|---|---|\n")
+                     "dense peak. path: fused attention kernels, or the fp32 GEMM path of the shapes that have "
+                     "none (features in the workspace, all arithmetic fp32).\n\n")
+            fh.write("| config | B,H,n,d | M x L | dtype | causal | path | median us (p10-p90) | tokens/s "
+                     "| head-tokens/s | TFLOP/s | GB/s | floor us | roofline |\n"
+                     "|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")
             for r in rows:
                 s = r["shape"]
                 head = (f"| {r['config']} | {s['B']},{s['H']},{s['n']},{s['d']} | {s['M']} x {s['L']} | "
                         f"{s['dtype']} | {'yes' if s['causal'] else 'no'} |")
                 if r["status"] != "ok":
-                    fh.write(head + f" {r['status']} | | | | | | |\n")
+                    fh.write(head + f" | {r['status']} | | | | | | |\n")
                     continue
-                fh.write(head + f" {1e3 * r['ms_median']:.1f} ({1e3 * r['ms_p10']:.1f}-{1e3 * r['ms_p90']:.1f}) | "
+                fh.write(head + f" {r['path']} | {1e3 * r['ms_median']:.1f} ({1e3 * r['ms_p10']:.1f}-{1e3 * r['ms_p90']:.1f}) | "
                          f"{r['tokens_per_s']:.3g} | {r['head_tokens_per_s']:.3g} | {r['attn_tflops']:.1f} | "
                          f"{r['hbm_gbs']:.0f} | {r['floor_us']:.1f} | {r['roofline_frac']:.1%} {r['bound']} |\n")
         log(f"wrote {args.configs_table}")

@@ -39,8 +39,20 @@
  *    streaming step use fp32 coefficients.
  *  - The denominator gets an additive eps: out = num / (den + eps).  With ReLU
  *    features a row can have den = 0; it then yields 0.
- *  - Shapes the kernels are not built for return LUNA_ERR_UNSUPPORTED; there is
- *    no fallback path.
+ *  - Every problem with d in {32, 64, 128}, L in {1, 2, 4, 8, 16} and M*L <= 256
+ *    runs on the GPU.  The shapes below have fused attention kernels (Q, K and V
+ *    read once, out written once); the others (one channel per projection with
+ *    M = 128 or 256, fp32 at d = 128, ...) take a path of fp32 matrix-core GEMMs
+ *    and scans over 64-token chunks (causal) or 512-token pieces (non-causal) with
+ *    the features in the workspace: the same results to fp32 rounding, slower, and
+ *    about 4 (2 M L + 2 (d + 1)) bytes of workspace per token and head plus
+ *    4 M L (d + 1) per chunk or piece (and 16 KiB per causal chunk).
+ *      non-causal, (dtype, d, L, M): (f32, 32, 8 or 2, <= 16), (f32, 64, 8, <= 16),
+ *        (bf16, 32, 8, <= 16), (bf16, 64, 8, <= 32), (bf16, 64, 4, <= 16),
+ *        (bf16, 64, 1, 49..64 or 113..128), (bf16, 128, 8, <= 16);
+ *      causal: (f32, 32, 8 or 2, <= 16), (f32, 64, 8, <= 16), (bf16, 32, 8, <= 16),
+ *        (bf16, 64, 8, <= 32), (bf16, 128, 8, <= 32).
+ *    Other shapes return LUNA_ERR_UNSUPPORTED; there is no host fallback.
  */
 #ifndef LUNA_H_
 #define LUNA_H_
@@ -76,7 +88,7 @@ enum {
 /*
  * Feature-map parameters, eq. (11) of Section 3.2 and Listing 1 (the feature-map
  * code in the Implementation Details appendix).
- *   M       number of projections w_i (rows of W), 1 <= M <= 64
+ *   M       number of projections w_i (rows of W), 1 <= M <= 256
  *   L       channels per projection (outputs of the psi_l), 1 <= L <= 16; D = M*L <= 256
  *   hidden  width of each channel MLP, 1 <= hidden <= 64
  *   shared_channels 0: L separate MLPs 1 -> hidden -> 1 (Listing 1's default);
@@ -239,8 +251,8 @@ typedef struct luna_phi_grads {
  * channel MLPs, ReLU'(0) = 0).  Q, K, V, dO: [B, H, n, d] in dtype; same parameters and
  * eps as the forward call.  All arithmetic is fp32 (the features are recomputed; the
  * channel functions through their exact piecewise-linear form, whose slopes give
- * dpsi/du).  Supported: d <= 128 (any of 32, 64, 128), M <= 64, L in {1, 2, 4, 8,
- * 16}.  The workspace (LUNA_OP_ATTN_BWD / LUNA_OP_ATTN_CAUSAL_BWD in
+ * dpsi/du).  Supported: d in {32, 64, 128}, L in {1, 2, 4, 8, 16}, M*L <= 256 and
+ * H <= 65535.  The workspace (LUNA_OP_ATTN_BWD / LUNA_OP_ATTN_CAUSAL_BWD in
  * luna_workspace_bytes) holds the features, the per-chunk states and the partial
  * parameter sums: about 4 (2 M L + 3 (d + 1)) bytes per token and head, plus
  * 2 x 4 M L (d + 1) per chunk of 64 tokens for the causal form.

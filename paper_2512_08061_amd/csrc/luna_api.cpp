@@ -44,7 +44,7 @@ luna_status check_common(const Problem& pb) {
   if (pb.n > (int64_t)1 << 30) return fail(LUNA_ERR_UNSUPPORTED, "n must be <= 2^30");
   if (pb.B * pb.H > (int64_t)1 << 24) return fail(LUNA_ERR_UNSUPPORTED, "B*H must be <= 2^24");
   if (pb.d != 32 && pb.d != 64 && pb.d != 128) return fail(LUNA_ERR_UNSUPPORTED, "d must be 32, 64 or 128");
-  if (p->M < 1 || p->M > 64) return fail(LUNA_ERR_INVALID_ARG, "M must be in [1, 64]");
+  if (p->M < 1 || p->M > 256) return fail(LUNA_ERR_INVALID_ARG, "M must be in [1, 256]");
   if (p->L < 1 || p->L > 16) return fail(LUNA_ERR_INVALID_ARG, "L must be in [1, 16]");
   if (p->hidden < 1 || p->hidden > 64) return fail(LUNA_ERR_INVALID_ARG, "hidden must be in [1, 64]");
   if (p->M * p->L > 256) return fail(LUNA_ERR_INVALID_ARG, "M*L must be <= 256");
@@ -81,7 +81,33 @@ struct Layout {
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
   size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
   int pieces = 0, piece_chunks = 0;
+  int generic = 0;  // forward in fp32 GEMMs and scans (shapes without a fused kernel)
 };
+
+// Buffers of the forward pass in fp32 GEMMs (the forward of shapes without a fused
+// kernel, and the recomputation that starts the backward pass): features of the keys
+// (and queries), [V | 1], [num | den - eps] and the per-chunk states, plus P for the
+// causal form.  Causal chunks are the 64-token chunks of the scan; the non-causal form
+// cuts its sums over tokens into 512-token pieces, for parallelism only.
+luna_status plan_f32_forward(const Problem& pb, bool causal, bool queries, Layout* lay, size_t* off) {
+  const int d = (int)pb.d, D = pb.p->M * pb.p->L;
+  lay->chunk = causal ? 64 : 512;
+  const int64_t nch = (pb.n + lay->chunk - 1) / lay->chunk;
+  if (nch > 65535) return fail(LUNA_ERR_UNSUPPORTED, causal ? "n must be <= 65535 * 64" : "n must be <= 65535 * 512");
+  lay->nch = (int)nch;
+  const size_t rows = (size_t)(pb.B * pb.H) * (size_t)pb.n, states = (size_t)(pb.B * pb.H) * lay->nch;
+  auto take = [&](size_t& at, size_t bytes) {
+    at = *off;
+    *off = align256(*off + bytes);
+  };
+  if (queries) take(lay->phiq, rows * D * 4);
+  take(lay->phik, rows * D * 4);
+  take(lay->vx, rows * (d + 1) * 4);
+  if (queries) take(lay->y, rows * (d + 1) * 4);
+  take(lay->sx, states * D * (d + 1) * 4);
+  if (causal && queries) take(lay->pm, states * 64 * 64 * 4);
+  return LUNA_OK;
+}
 
 // Token ranges of the non-causal state pass: enough state workgroups to fill the
 // device, at least 256 tokens each, a multiple of 128 tokens per range.
@@ -111,8 +137,14 @@ luna_status plan(const Problem& pb, Layout* lay) {
       return fail(LUNA_ERR_UNSUPPORTED, "no feature-map kernel for this (d, L, M)");
   } else if (pb.op == LUNA_OP_ATTN) {
     luna::NoncausalPlan np;
-    if (!luna::noncausal_supported(dt, d, L, M, &np))
-      return fail(LUNA_ERR_UNSUPPORTED, "no non-causal attention kernel for this (dtype, d, L, M)");
+    if (!luna::noncausal_supported(dt, d, L, M, &np)) {
+      if (!luna::featuremap_supported(dt, d, L, M))
+        return fail(LUNA_ERR_UNSUPPORTED, "no non-causal attention kernels for this (dtype, d, L, M)");
+      lay->generic = 1;
+      if ((st = plan_f32_forward(pb, false, true, lay, &off)) != LUNA_OK) return st;
+      lay->total = off;
+      return LUNA_OK;
+    }
     if (heads >= luna::kFusedMinHeads && luna::fused_acc_regs(d, L, M) <= luna::kFusedMaxAccRegs) {
       lay->fused = 1;
       lay->total = off;
@@ -127,8 +159,14 @@ luna_status plan(const Problem& pb, Layout* lay) {
     off = align256(off + (size_t)heads * np.frag_elems * (pb.dt == LUNA_BF16 ? 2 : 4));
   } else if (pb.op == LUNA_OP_ATTN_CAUSAL) {
     if (pb.chunk != 64) return fail(LUNA_ERR_UNSUPPORTED, "chunk must be 64");
-    if (!luna::causal_supported(dt, d, L, M))
-      return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernel for this (dtype, d, L, M)");
+    if (!luna::causal_supported(dt, d, L, M)) {
+      if (!luna::featuremap_supported(dt, d, L, M))
+        return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernels for this (dtype, d, L, M)");
+      lay->generic = 1;
+      if ((st = plan_f32_forward(pb, true, true, lay, &off)) != LUNA_OK) return st;
+      lay->total = off;
+      return LUNA_OK;
+    }
     // Too few heads to fill the device: cut every head in two at a chunk boundary x
     // near n/2.  A state launch first sums the state of [0, x) in pieces (one
     // workgroup per head and piece, enough pieces to fill the device); part 1 of the
@@ -165,8 +203,11 @@ luna_status plan(const Problem& pb, Layout* lay) {
       lay->split = (int)(cx * 64);
       lay->state = off;
       off = align256(off + (size_t)heads * lay->pieces * luna::causal_state_floats(dt, d, L, M) * sizeof(float));
+    } else if (luna::featuremap_supported(dt, d, L, M)) {
+      lay->generic = 1;
+      if ((st = plan_f32_forward(pb, false, false, lay, &off)) != LUNA_OK) return st;
     } else {
-      return fail(LUNA_ERR_UNSUPPORTED, "no state kernel for this (dtype, d, L, M)");
+      return fail(LUNA_ERR_UNSUPPORTED, "no state kernels for this (dtype, d, L, M)");
     }
   } else if (pb.op == LUNA_OP_CAUSAL_STEP) {
     if (!luna::featuremap_supported(dt, d, L, M))
@@ -183,27 +224,16 @@ luna_status plan(const Problem& pb, Layout* lay) {
       return fail(LUNA_ERR_UNSUPPORTED, "no backward kernels for this (d, L, M)");
     const int64_t P = param_sets(pb);
     if (P > 65535) return fail(LUNA_ERR_UNSUPPORTED, "at most 65535 parameter sets in the backward pass");
+    if (pb.H > 65535) return fail(LUNA_ERR_UNSUPPORTED, "at most 65535 heads in the backward pass");
     const bool causal = pb.op == LUNA_OP_ATTN_CAUSAL_BWD;
-    if (causal && pb.n > ((int64_t)1 << 30) / 64) return fail(LUNA_ERR_UNSUPPORTED, "n too large");
-    // causal: the 64-token chunks of the scan; non-causal: 512-token pieces of the sums
-    // over tokens, for parallelism only
-    lay->chunk = causal ? 64 : 512;
-    lay->nch = (int)((pb.n + lay->chunk - 1) / lay->chunk);
+    if ((st = plan_f32_forward(pb, causal, true, lay, &off)) != LUNA_OK) return st;
     const size_t D = (size_t)M * L, rows = (size_t)heads * (size_t)pb.n, states = (size_t)heads * lay->nch;
     auto take = [&](size_t& at, size_t bytes) {
       at = off;
       off = align256(off + bytes);
     };
-    take(lay->phiq, rows * D * 4);
-    take(lay->phik, rows * D * 4);
-    take(lay->vx, rows * (d + 1) * 4);
-    take(lay->y, rows * (d + 1) * 4);
-    take(lay->sx, states * D * (d + 1) * 4);
     take(lay->dsx, states * D * (d + 1) * 4);
-    if (causal) {
-      take(lay->pm, states * 64 * 64 * 4);
-      take(lay->rm, states * 64 * 64 * 4);
-    }
+    if (causal) take(lay->rm, states * 64 * 64 * 4);
     take(lay->dphiq, rows * D * 4);
     take(lay->dphik, rows * D * 4);
     if (pb.dt == LUNA_BF16) take(lay->dvtmp, rows * d * 4);
@@ -271,6 +301,88 @@ luna::PhiArgs phi_args(const Problem& pb, uint8_t* ws, const Layout& lay) {
 }
 
 bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.0f; }
+
+// C (+)= A B (fp32) over (head, chunk) batches; strides of (head, chunk, row, column)
+// for each operand; m/n/k_chunk: that dimension is the chunk's (ragged last chunk);
+// lower: only the lower triangle of C (with the diagonal) is formed.
+struct ChunkGemm {
+  int heads, chunks, chunk, seq;
+  hipStream_t s;
+  hipError_t operator()(const float* A, int64_t ah, int64_t ac, int64_t ai, int64_t ak, const float* Bm, int64_t bh,
+                        int64_t bc, int64_t bk, int64_t bj, float* Cm, int64_t ch, int64_t c2, int64_t ci, int64_t cj,
+                        int Mm, int Nn, int Kk, int mc, int nc, int kc, int lower, int acc) const {
+    luna::BwdGemm g{};
+    g.A = A; g.sAh = ah; g.sAc = ac; g.sAi = ai; g.sAk = ak;
+    g.B = Bm; g.sBh = bh; g.sBc = bc; g.sBk = bk; g.sBj = bj;
+    g.C = Cm; g.sCh = ch; g.sCc = c2; g.sCi = ci; g.sCj = cj;
+    g.M = Mm; g.N = Nn; g.K = Kk;
+    g.heads = heads; g.chunks = chunks; g.chunk = chunk; g.seq = seq;
+    g.m_chunk = mc; g.n_chunk = nc; g.k_chunk = kc; g.lower = lower; g.accumulate = acc;
+    return luna::launch_bwd_gemm(g, s);
+  }
+};
+
+// The forward pass in fp32 (eq. (9) of Section 3.1, the causal form in 64-token
+// chunks): features of the keys (and queries), [V | 1], per-chunk [S_c | z_c] =
+// phi(K_c)^T [V_c | 1], their exclusive prefix over chunks (causal) or total, and with
+// queries [num | den - eps] = phi(Q_c) [S_c | z_c] (+ P_c [V_c | 1], P_c =
+// tril(phi(Q_c) phi(K_c)^T)).  Q == nullptr: the state only.
+luna_status enqueue_f32_forward(const Problem& pb, uint8_t* w, const Layout& lay, const void* Q, const void* K,
+                                const void* V, bool causal, hipStream_t s) {
+  const luna::Dt dt = pb.dt == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int L = pb.p->L, D = pb.p->M * L, dd = (int)pb.d, E = dd + 1;
+  const int heads = (int)(pb.B * pb.H), C = lay.chunk, nch = lay.nch;
+  const int64_t n = pb.n, nD = n * D, nE = n * E, st_el = (int64_t)D * E, cc = (int64_t)C * C;
+  float* phiq = reinterpret_cast<float*>(w + lay.phiq);
+  float* phik = reinterpret_cast<float*>(w + lay.phik);
+  float* vx = reinterpret_cast<float*>(w + lay.vx);
+  float* y = reinterpret_cast<float*>(w + lay.y);
+  float* sx = reinterpret_cast<float*>(w + lay.sx);
+  float* pm = reinterpret_cast<float*>(w + lay.pm);
+  hipError_t e;
+#define LUNA_TRY(expr, what) \
+  if ((e = (expr)) != hipSuccess) return hip_fail(e, what)
+  luna::FeatureMapArgs f{};  // queries and keys in one launch
+  f.phi = phi_args(pb, w, lay);
+  f.rows_per_head = n;
+  f.H = (int)pb.H;
+  f.heads = pb.B * pb.H;
+  f.X = K;
+  f.out = phik;
+  if (Q) {
+    f.X2 = Q;
+    f.out2 = phiq;
+  }
+  LUNA_TRY(luna::launch_featuremap(dt, luna::Dt::F32, dd, L, f, s), "feature-map kernel launch");
+  LUNA_TRY(luna::launch_bwd_pack(dt, V, vx, (int64_t)heads * n, dd, s), "pack kernel launch");
+  const ChunkGemm gemm{heads, nch, C, (int)n, s};
+  const int64_t sh = (int64_t)nch * st_el;  // head stride of the per-chunk states
+  LUNA_TRY(gemm(phik, nD, (int64_t)C * D, 1, D, vx, nE, (int64_t)C * E, E, 1, sx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
+                0, 0), "state GEMM");
+  LUNA_TRY(luna::launch_bwd_scan(sx, heads, nch, st_el, causal ? 0 : 2, s), "state scan");
+  if (!Q) return LUNA_OK;
+  LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, sx, sh, st_el, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, D, 1, 0, 0,
+                0, 0), "readout GEMM");
+  if (causal) {
+    LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, phik, nD, (int64_t)C * D, 1, D, pm, nch * cc, cc, C, 1, C, C, D, 1,
+                  1, 0, 1, 0), "P GEMM");
+    LUNA_TRY(gemm(pm, nch * cc, cc, C, 1, vx, nE, (int64_t)C * E, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, C, 1, 0,
+                  1, 0, 1), "intra-chunk GEMM");
+  }
+#undef LUNA_TRY
+  return LUNA_OK;
+}
+
+// The generic forward: the fp32 forward, then out = num / den in the call's dtype.
+luna_status enqueue_generic_attn(const Problem& pb, uint8_t* w, const Layout& lay, const void* Q, const void* K,
+                                 const void* V, float eps, void* out, bool causal, hipStream_t s) {
+  luna_status st = enqueue_f32_forward(pb, w, lay, Q, K, V, causal, s);
+  if (st != LUNA_OK) return st;
+  const hipError_t e = luna::launch_fwd_out(pb.dt == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32,
+                                            reinterpret_cast<const float*>(w + lay.y), out, pb.B * pb.H * pb.n,
+                                            (int)pb.d, eps, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "output kernel launch");
+}
 
 // Scratch of luna_attn_fwd_causal_noalloc: one array per device, part of the code
 // object, so that calls need no allocation.  Host code never uses the array's name as
@@ -351,6 +463,7 @@ luna_status luna_attn_fwd(const void* Q, const void* K, const void* V, luna_dtyp
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* w = static_cast<uint8_t*>(ws);
   if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  if (lay.generic) return enqueue_generic_attn(pb, w, lay, Q, K, V, eps, out, false, s);
   luna::NoncausalArgs a{};
   a.Q = Q;
   a.K = K;
@@ -386,6 +499,7 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   uint8_t* w = static_cast<uint8_t*>(ws);
   if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  if (lay.generic) return enqueue_generic_attn(pb, w, lay, Q, K, V, eps, out, true, s);
   luna::CausalArgs a{};
   a.Q = Q;
   a.K = K;
@@ -449,6 +563,15 @@ luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int6
   uint8_t* w = static_cast<uint8_t*>(ws);
   if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
   const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  if (lay.generic) {
+    if ((st = enqueue_f32_forward(pb, w, lay, nullptr, K, V, false, s)) != LUNA_OK) return st;
+    // every piece holds the total after the scan: export the first
+    const int D = p->M * p->L;
+    const hipError_t e = luna::launch_fwd_export(reinterpret_cast<const float*>(w + lay.sx),
+                                                 (int64_t)lay.nch * D * (d + 1), S, z, (int)(B * H), D, (int)d,
+                                                 accumulate, s);
+    return e == hipSuccess ? LUNA_OK : hip_fail(e, "state export kernel launch");
+  }
   if (lay.pieces == 0) {
     luna::NoncausalArgs a{};
     a.K = K;
@@ -581,45 +704,10 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
   hipError_t e;
 #define LUNA_TRY(expr, what) \
   if ((e = (expr)) != hipSuccess) return hip_fail(e, what)
-  // features of the queries and keys in fp32 (one launch)
-  luna::FeatureMapArgs f{};
-  f.phi = phi_args(pb, w, lay);
-  f.rows_per_head = n;
-  f.H = (int)H;
-  f.heads = B * H;
-  f.X = Q;
-  f.out = phiq;
-  f.X2 = K;
-  f.out2 = phik;
-  LUNA_TRY(luna::launch_featuremap(dt, luna::Dt::F32, dd, L, f, s), "feature-map kernel launch");
-  LUNA_TRY(luna::launch_bwd_pack(dt, V, vx, (int64_t)heads * n, dd, s), "pack kernel launch");
-  // C (+)= A B over (head, chunk); strides of (head, chunk, row, column) per operand
-  auto gemm = [&](const float* A, int64_t ah, int64_t ac, int64_t ai, int64_t ak, const float* Bm, int64_t bh,
-                  int64_t bc, int64_t bk, int64_t bj, float* Cm, int64_t ch, int64_t c2, int64_t ci, int64_t cj, int Mm,
-                  int Nn, int Kk, int mc, int nc, int kc, int lower, int acc) {
-    luna::BwdGemm g{};
-    g.A = A; g.sAh = ah; g.sAc = ac; g.sAi = ai; g.sAk = ak;
-    g.B = Bm; g.sBh = bh; g.sBc = bc; g.sBk = bk; g.sBj = bj;
-    g.C = Cm; g.sCh = ch; g.sCc = c2; g.sCi = ci; g.sCj = cj;
-    g.M = Mm; g.N = Nn; g.K = Kk;
-    g.heads = heads; g.chunks = nch; g.chunk = C; g.seq = (int)n;
-    g.m_chunk = mc; g.n_chunk = nc; g.k_chunk = kc; g.lower = lower; g.accumulate = acc;
-    return luna::launch_bwd_gemm(g, s);
-  };
+  // the forward pass in fp32: features, [V | 1], states, [num | den - eps] (and P)
+  if ((st = enqueue_f32_forward(pb, w, lay, Q, K, V, causal != 0, s)) != LUNA_OK) return st;
+  const ChunkGemm gemm{heads, nch, C, (int)n, s};
   const int64_t sh = (int64_t)nch * st_el;  // head stride of the per-chunk states
-  // per-chunk [S | z] = phi(K_c)^T [V_c | 1], then exclusive prefix over chunks (causal)
-  LUNA_TRY(gemm(phik, nD, (int64_t)C * D, 1, D, vx, nE, (int64_t)C * E, E, 1, sx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
-                0, 0), "state GEMM");
-  LUNA_TRY(luna::launch_bwd_scan(sx, heads, nch, st_el, causal ? 0 : 2, s), "state scan");
-  // [num | den - eps] = phi(Q_c) [S_c | z_c] (+ P_c [V_c | 1], P_c = tril(phi(Q_c) phi(K_c)^T))
-  LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, sx, sh, st_el, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, D, 1, 0, 0,
-                0, 0), "readout GEMM");
-  if (causal) {
-    LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, phik, nD, (int64_t)C * D, 1, D, pm, nch * cc, cc, C, 1, C, C, D, 1,
-                  1, 0, 1, 0), "P GEMM");
-    LUNA_TRY(gemm(pm, nch * cc, cc, C, 1, vx, nE, (int64_t)C * E, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, C, 1, 0,
-                  1, 0, 1), "intra-chunk GEMM");
-  }
   LUNA_TRY(luna::launch_bwd_g(dt, y, dO, (int64_t)heads * n, dd, eps, s), "denominator kernel launch");
   // dphi(Q_c) = G_c [S_c | z_c]^T (+ R_c phi(K_c), R_c = tril(G_c [V_c | 1]^T))
   LUNA_TRY(gemm(y, nE, (int64_t)C * E, E, 1, sx, sh, st_el, 1, E, dphiq, nD, (int64_t)C * D, D, 1, C, D, E, 1, 0, 0,

@@ -44,6 +44,12 @@
 //                       (a_k < 0) its breakpoint, where h_k = a_k u + c_k, so
 //                       dfc2_lk = a_k sum_on dy_l u + c_k sum_on dy_l,
 //                       dfc1_(l)k = f_lk sum_on dy_l u, dfc1_b likewise, dfc2_b_l = sum dy_l.
+//
+// The same pack, GEMM and scan kernels carry the forward pass of the shapes that have
+// no fused kernel (any d, L and M the feature-map kernel takes: one channel per
+// projection with M up to 256, fp32 at d = 128, ...), in fp32 throughout, with two more:
+//   fwd_out_kernel      [num | den - eps] -> out = num / den in the call's dtype;
+//   fwd_export_kernel   the total [S | z] of a head into (or added to) the caller's S, z.
 #include <algorithm>
 
 #include "luna_device.hpp"
@@ -194,6 +200,35 @@ __global__ __launch_bounds__(256) void bwd_g_kernel(float* __restrict__ Y, const
   const float inv = 1.0f / den;
   for (int c = lane; c < d; c += kWave) y[c] = (float)go[c] * inv;
   if (lane == 0) y[d] = -dot * inv * inv;
+}
+
+// ---------------------------------------------------------------------------
+// forward readout of the generic path: out = num / (den - eps + eps), one wave per row
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void fwd_out_kernel(const float* __restrict__ Y, T* __restrict__ out, int64_t rows,
+                                                      int d, float eps) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t r = blockIdx.x * (int64_t)(blockDim.x / kWave) + threadIdx.x / kWave;
+  if (r >= rows) return;
+  const float* y = Y + r * (d + 1);
+  const float inv = 1.0f / (y[d] + eps);
+  for (int c = lane; c < d; c += kWave) out[r * d + c] = (T)(y[c] * inv);
+}
+
+// [S | z] of each head ([D][d + 1], fp32) -> S [D][d] and z [D], set or added
+__global__ __launch_bounds__(256) void fwd_export_kernel(const float* __restrict__ X, int64_t head_stride,
+                                                         float* __restrict__ S, float* __restrict__ z, int heads,
+                                                         int D, int d, int accumulate) {
+  const int64_t per = (int64_t)D * (d + 1);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < (int64_t)heads * per;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t h = i / per, rest = i - h * per;
+    const int f = (int)(rest / (d + 1)), c = (int)(rest - (int64_t)f * (d + 1));
+    const float v = X[h * head_stride + rest];
+    float* dst = c < d ? &S[(h * D + f) * d + c] : &z[h * D + f];
+    *dst = accumulate ? *dst + v : v;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -531,7 +566,7 @@ int bwd_phi_groups(int64_t rows_per_set) {
 
 bool bwd_supported(int d, int L, int M) {
   const bool lok = L == 1 || L == 2 || L == 4 || L == 8 || L == 16;
-  return lok && M >= 1 && M <= 64 && d >= 1 && d <= 128;
+  return lok && M >= 1 && M <= 256 && M * L <= 256 && d >= 1 && d <= 128;
 }
 
 size_t bwd_part_floats(int, int L, int) { return 2 * (size_t)nseg_cap(L, kFmSegBytes) * L; }
@@ -591,5 +626,20 @@ hipError_t launch_bwd_mlp(const BwdMlp& a, int sets, hipStream_t s) {
 }
 
 int bwd_nseg_cap(int L) { return nseg_cap(L, kFmSegBytes); }
+
+hipError_t launch_fwd_out(Dt dt, const float* Y, void* out, int64_t rows, int d, float eps, hipStream_t s) {
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  if (dt == Dt::BF16) hipLaunchKernelGGL(fwd_out_kernel<__bf16>, grid, block, 0, s, Y, (__bf16*)out, rows, d, eps);
+  else hipLaunchKernelGGL(fwd_out_kernel<float>, grid, block, 0, s, Y, (float*)out, rows, d, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_export(const float* X, int64_t head_stride, float* S, float* z, int heads, int D, int d,
+                             int accumulate, hipStream_t s) {
+  const int64_t total = (int64_t)heads * D * (d + 1);
+  const dim3 grid((unsigned)std::min<int64_t>((total + 255) / 256, 65536)), block(256);
+  hipLaunchKernelGGL(fwd_export_kernel, grid, block, 0, s, X, head_stride, S, z, heads, D, d, accumulate);
+  return hipGetLastError();
+}
 
 }  // namespace luna

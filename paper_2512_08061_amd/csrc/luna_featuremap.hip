@@ -49,8 +49,9 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
     Tout* out = reinterpret_cast<Tout*>(Odst) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
 
     // the row, W fragments and biases are fetched before the table, so that their
-    // loads overlap its copy
-    constexpr int kMaxMB = 4;  // M <= 64
+    // loads overlap its copy; projections go in groups of four 16-projection blocks
+    // (W fragments of one group in registers)
+    constexpr int kMaxMB = 4;
     const int MB = (M + 15) / 16;
     Frag<Tin> xf[KS];
 #pragma unroll
@@ -58,55 +59,59 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
       if (row_ok) load8(xf[ks], X + 32 * ks + 8 * g);
       else xf[ks].zero();
     }
-    Frag<Tin> wfr[kMaxMB][KS];
-    float bz[kMaxMB][4];
+    for (int mg = 0; mg < MB; mg += kMaxMB) {
+      Frag<Tin> wfr[kMaxMB][KS];
+      float bz[kMaxMB][4];
 #pragma unroll
-    for (int mb = 0; mb < kMaxMB; ++mb) {
-      const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
+      for (int mbl = 0; mbl < kMaxMB; ++mbl) {
+        const int mb = mg + mbl;
+        const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        if (mb < MB && prow < M) load8(wfr[mb][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
-        else wfr[mb][ks].zero();
+        for (int ks = 0; ks < KS; ++ks) {
+          if (mb < MB && prow < M) load8(wfr[mbl][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
+          else wfr[mbl][ks].zero();
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
+          bz[mbl][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
+        }
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
-        bz[mb][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
+      if (mg == 0 && hset != loaded) {  // (uniform) a workgroup loads a table once per parameter set it meets
+        __syncthreads();                // every wave is done with the previous table
+        pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+        __syncthreads();
+        loaded = hset;
       }
-    }
-    if (hset != loaded) {  // (uniform) a workgroup loads a table once per parameter set it meets
-      __syncthreads();     // every wave is done with the previous table
-      pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
-      __syncthreads();
-      loaded = hset;
-    }
-    const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
-    const float floor = tab.floor;
+      const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
+      const float floor = tab.floor;
 
 #pragma unroll
-    for (int mb = 0; mb < kMaxMB; ++mb) {
-      if (mb >= MB) break;
-      f32x4 acc = zero4();
+      for (int mbl = 0; mbl < kMaxMB; ++mbl) {
+        const int mb = mg + mbl;
+        if (mb >= MB) break;
+        f32x4 acc = zero4();
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mb][ks], xf[ks]);
-      float uu[4];
+        for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mbl][ks], xf[ks]);
+        float uu[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) uu[j] = acc[j] + bz[mb][j];
-      int sg[4];
-      pwl_search(tab, steps, uu, sg);
+        for (int j = 0; j < 4; ++j) uu[j] = acc[j] + bz[mbl][j];
+        int sg[4];
+        pwl_search(tab, steps, uu, sg);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = 16 * mb + 4 * g + j;
-        if (i < M && row_ok) {
-          float y[L];
-          pwl_channels<L>(tab, sg[j], floor, uu[j], y);
-          Tout* o = out + i * L;
-          if constexpr (L % 4 == 0) {
+        for (int j = 0; j < 4; ++j) {
+          const int i = 16 * mb + 4 * g + j;
+          if (i < M && row_ok) {
+            float y[L];
+            pwl_channels<L>(tab, sg[j], floor, uu[j], y);
+            Tout* o = out + i * L;
+            if constexpr (L % 4 == 0) {
 #pragma unroll
-            for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
-          } else {
+              for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
+            } else {
 #pragma unroll
-            for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
+              for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
+            }
           }
         }
       }
@@ -144,7 +149,7 @@ static hipError_t fm_dispatch_d(int d, int L, const FeatureMapArgs& a, hipStream
 bool featuremap_supported(Dt, int d, int L, int M) {
   const bool dok = d == 32 || d == 64 || d == 128;
   const bool lok = L == 1 || L == 2 || L == 4 || L == 8 || L == 16;
-  return dok && lok && M >= 1 && M <= 64;
+  return dok && lok && M >= 1 && M <= 256 && M * L <= 256;
 }
 
 hipError_t launch_featuremap(Dt in_dt, Dt out_dt, int d, int L, const FeatureMapArgs& a, hipStream_t s) {

@@ -238,6 +238,10 @@ hipError_t launch_bwd_reduce(const float* partial, double* sum, int groups, int 
 hipError_t launch_bwd_prefix(const double* sum, double* pre, const uint8_t* tables, int M, int d, int L,
                              int part_floats, int nseg_cap, int sets, hipStream_t s);
 hipError_t launch_bwd_mlp(const BwdMlp& a, int sets, hipStream_t s);
+// forward pass of the shapes without a fused kernel (fp32 GEMMs and scans as above)
+hipError_t launch_fwd_out(Dt dt, const float* Y, void* out, int64_t rows, int d, float eps, hipStream_t s);
+hipError_t launch_fwd_export(const float* X, int64_t head_stride, float* S, float* z, int heads, int D, int d,
+                             int accumulate, hipStream_t s);
 
 // Launchers; each returns hipSuccess or the launch error.  `ok` reports whether
 // a kernel exists for the (dtype, d, L, M) combination.

@@ -819,6 +819,7 @@ static void nc_plan(NoncausalPlan* p) {
   X(__bf16, 64, 8, 2)      \
   X(__bf16, 64, 4, 1)      \
   X(__bf16, 64, 1, 4)      \
+  X(__bf16, 64, 1, 8)      \
   X(__bf16, 128, 8, 1)
 
 template <typename T>

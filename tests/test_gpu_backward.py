@@ -75,6 +75,7 @@ def _check(w, seed, causal, **opt):
 CASES = [  # (dtype, d, M, L, n)
     ("f32", 32, 8, 8, 1), ("f32", 32, 8, 8, 37), ("f32", 64, 16, 8, 130), ("f32", 128, 32, 8, 70),
     ("f32", 64, 64, 1, 65), ("f32", 64, 8, 4, 200), ("bf16", 64, 16, 8, 333), ("bf16", 128, 32, 8, 150),
+    ("bf16", 128, 256, 1, 100), ("f32", 64, 128, 1, 70),  # one channel per projection, M = D
 ]
 
 

@@ -44,6 +44,7 @@ def _sync():
 FM_CASES = [
     ("f32", 32, 8, 8, 100), ("f32", 64, 16, 8, 77), ("bf16", 64, 16, 8, 300), ("bf16", 128, 32, 8, 65),
     ("bf16", 64, 64, 1, 33), ("bf16", 32, 5, 4, 50), ("f32", 128, 3, 16, 20), ("bf16", 64, 8, 2, 1),
+    ("bf16", 64, 128, 1, 70), ("bf16", 128, 256, 1, 33), ("f32", 32, 100, 2, 130),  # more than 64 projections
 ]
 
 
@@ -231,6 +232,8 @@ def test_featuremap_workload_full_size(name):
 NC_CASES = [
     ("f32", 32, 8, 8), ("f32", 64, 16, 8), ("bf16", 32, 16, 8), ("bf16", 64, 8, 8), ("bf16", 64, 16, 8),
     ("bf16", 64, 32, 8), ("bf16", 64, 16, 4), ("bf16", 64, 64, 1), ("bf16", 128, 16, 8),
+    # one channel per projection, M = D = 128 (fused); shapes on the fp32 GEMM path
+    ("bf16", 64, 128, 1), ("bf16", 64, 100, 1), ("bf16", 128, 256, 1), ("f32", 128, 16, 8), ("f32", 64, 32, 4),
 ]
 
 
@@ -280,6 +283,8 @@ def test_attn_noncausal_workload_full_size(name):
 CS_CASES = [
     ("f32", 32, 8, 8), ("f32", 64, 16, 8), ("bf16", 32, 16, 8), ("bf16", 64, 16, 8), ("bf16", 64, 32, 8),
     ("bf16", 128, 16, 8), ("bf16", 128, 32, 8),
+    # shapes on the fp32 GEMM path: one channel per projection (M = D = 256, 128), fp32 at d = 128
+    ("bf16", 128, 256, 1), ("bf16", 64, 128, 1), ("f32", 128, 16, 8), ("f32", 32, 24, 2),
 ]
 
 
@@ -336,6 +341,44 @@ def test_attn_causal_workload_full_size():
     # rows deep into the sequence, kernel form one row at a time
     for b, h in heads[:2]:
         rows = np.sort(np.concatenate([rng.integers(0, w.n, 12), [w.n - 1, 8191, 8192]]))
+        ref = oracle.attn_quadratic_rows(Q[b, h], K[b, h], V[b, h], p, rows, eps=w.eps, causal=True)
+        assert_close_rows(to_np(out[b, h, rows]), ref, w.dtype, f"rows of ({b},{h})")
+
+
+def test_attn_noncausal_one_channel_full_size():
+    """The one-channel variant of the long non-causal problem (L = 1, M = D = 128),
+    every head, on the launch the benchmark times."""
+    w = wl.WORKLOADS["long_noncausal"].with_(M=128, L=1)
+    say(f"noncausal full size one-channel: all {w.B * w.H} heads")
+    Q, K, V, p = inputs(w, seed=0)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps))
+    ref = oracle_per_batch(oracle.attn_noncausal, Q, K, V, p, w.eps)
+    assert_close(out, ref, w.dtype, "out, every head")
+
+
+def test_attn_causal_one_channel_full_size():
+    """The one-channel variant of the long causal problem (L = 1, M = D = 256, fp32
+    GEMM path): the masked kernel form on the first 512 tokens of every head, whole
+    sequences of two heads against the chunked scan, and single rows deep in them."""
+    w = wl.WORKLOADS["long_causal"].with_(M=256, L=1)
+    say("causal full size one-channel")
+    Q, K, V, p = inputs(w, seed=0)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=w.chunk, eps=w.eps)
+    _sync()
+    pre = 512
+    got = to_np(out[:, :, :pre])
+    for b in range(w.B):
+        ref = oracle.attn_quadratic(Q[b, :, :pre], K[b, :, :pre], V[b, :, :pre], p, eps=w.eps, causal=True)
+        assert_close_rows(got[b], ref, w.dtype, f"prefix b={b}")
+    heads = [(0, 0), (w.B - 1, w.H - 1)]
+    full = to_np(out[[b for b, _ in heads], [h for _, h in heads]])
+    rng = np.random.default_rng(12)
+    for i, (b, h) in enumerate(heads):
+        ref = oracle.attn_causal_chunked(Q[b, h], K[b, h], V[b, h], p, chunk=w.chunk, eps=w.eps)
+        assert_close_rows(full[i], ref, w.dtype, f"all rows of ({b},{h})")
+        rows = np.sort(np.concatenate([rng.integers(0, w.n, 8), [w.n - 1]]))
         ref = oracle.attn_quadratic_rows(Q[b, h], K[b, h], V[b, h], p, rows, eps=w.eps, causal=True)
         assert_close_rows(to_np(out[b, h, rows]), ref, w.dtype, f"rows of ({b},{h})")
 

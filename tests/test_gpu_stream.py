@@ -28,12 +28,15 @@ def _col(z):
 
 
 # (dtype, d, M, L, n, B, H): the first ones take the non-causal state pass, the
-# (bf16, 128, 32, 8) ones the causal kernel's state launch (pieces, then export)
+# (bf16, 128, 32, 8) ones the causal kernel's state launch (pieces, then export), the
+# last ones the fp32 GEMM path
 STATE_CASES = [
     ("f32", 32, 8, 8, 100, 2, 3), ("f32", 64, 16, 8, 65, 1, 2), ("bf16", 64, 16, 8, 300, 2, 3),
     ("bf16", 64, 32, 8, 130, 1, 3), ("bf16", 64, 64, 1, 97, 1, 2),
     ("bf16", 128, 32, 8, 1, 2, 2), ("bf16", 128, 32, 8, 64, 1, 3), ("bf16", 128, 32, 8, 200, 1, 1),
     ("bf16", 128, 32, 8, 700, 2, 5),
+    # the fp32 GEMM path (512-token pieces, the last ragged)
+    ("bf16", 128, 256, 1, 1100, 2, 3), ("f32", 128, 16, 8, 600, 1, 2), ("bf16", 64, 100, 1, 97, 1, 2),
 ]
 
 

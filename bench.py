@@ -580,12 +580,14 @@ def configs_bench(args) -> int:
         tf = flops_per_token_head(w, w.causal) * th / 1e12
         mfma_peak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
         t_hbm, t_mfma = gb / HBM_PEAK_GBS, tf / mfma_peak
-        # shapes without a fused kernel run the fp32 GEMM path, whose workspace holds the
-        # fp32 features of the queries and keys (8 M L bytes per token and head)
-        generic = plan.ws_bytes >= 8 * w.M * w.L * th
+        # the path, from the workspace: the fp32 GEMM path holds fp32 features of the
+        # queries and keys (8 M L bytes per token and head), the causal kernel with the
+        # features given bf16 ones (4 M L), the fused kernels neither
+        fb = plan.ws_bytes / (w.M * w.L * th)
+        path = "fp32 GEMM" if fb >= 8 else "features mapped, then scan" if fb >= 4 else "fused"
         rec.update({
             "status": "ok",
-            "path": "fp32 GEMM" if generic else "fused",
+            "path": path,
             "ms_median": round(ms, 5), "ms_p10": round(pick(0.1), 5), "ms_p90": round(pick(0.9), 5),
             "tokens_per_s": w.B * w.n / (ms / 1e3),
             "head_tokens_per_s": th / (ms / 1e3),

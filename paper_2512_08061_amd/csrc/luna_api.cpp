@@ -82,6 +82,7 @@ struct Layout {
   size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
   int pieces = 0, piece_chunks = 0;
   int generic = 0;  // forward in fp32 GEMMs and scans (shapes without a fused kernel)
+  int given = 0;    // causal: features mapped beforehand (bf16, in phiq / phik), then the scan kernel
 };
 
 // Buffers of the forward pass in fp32 GEMMs (the forward of shapes without a fused
@@ -159,9 +160,21 @@ luna_status plan(const Problem& pb, Layout* lay) {
     off = align256(off + (size_t)heads * np.frag_elems * (pb.dt == LUNA_BF16 ? 2 : 4));
   } else if (pb.op == LUNA_OP_ATTN_CAUSAL) {
     if (pb.chunk != 64) return fail(LUNA_ERR_UNSUPPORTED, "chunk must be 64");
-    if (!luna::causal_supported(dt, d, L, M)) {
-      if (!luna::featuremap_supported(dt, d, L, M))
-        return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernels for this (dtype, d, L, M)");
+    size_t state_floats = 0;
+    if (luna::causal_supported(dt, d, L, M)) {
+      state_floats = luna::causal_state_floats(dt, d, L, M);
+    } else if (!luna::featuremap_supported(dt, d, L, M)) {
+      return fail(LUNA_ERR_UNSUPPORTED, "no causal attention kernels for this (dtype, d, L, M)");
+    } else if (luna::causal_given_supported(dt, d, M * L)) {
+      // the features of Q and K in bf16, mapped by the feature-map kernel
+      lay->given = 1;
+      state_floats = luna::causal_given_state_floats(d, M * L);
+      const size_t feat_bytes = (size_t)heads * (size_t)pb.n * (size_t)(M * L) * 2;
+      lay->phiq = off;
+      off = align256(off + feat_bytes);
+      lay->phik = off;
+      off = align256(off + feat_bytes);
+    } else {
       lay->generic = 1;
       if ((st = plan_f32_forward(pb, true, true, lay, &off)) != LUNA_OK) return st;
       lay->total = off;
@@ -182,7 +195,7 @@ luna_status plan(const Problem& pb, Layout* lay) {
         lay->piece_chunks = (int)pc;
         lay->pieces = (int)((cx + pc - 1) / pc);  // every piece non-empty
         lay->state = off;
-        off = align256(off + (size_t)heads * lay->pieces * luna::causal_state_floats(dt, d, L, M) * sizeof(float));
+        off = align256(off + (size_t)heads * lay->pieces * state_floats * sizeof(float));
       }
     }
   } else if (pb.op == LUNA_OP_STATE) {
@@ -513,17 +526,36 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   a.split = lay.split;
   a.eps = eps;
   const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int D = p->M * p->L;
+  if (lay.given) {  // phi(Q), phi(K) in bf16 first (one launch)
+    luna::FeatureMapArgs f{};
+    f.phi = a.phi;
+    f.rows_per_head = n;
+    f.H = (int)H;
+    f.heads = B * H;
+    f.X = Q;
+    f.out = w + lay.phiq;
+    f.X2 = K;
+    f.out2 = w + lay.phik;
+    hipError_t e = luna::launch_featuremap(dt, luna::Dt::BF16, (int)d, p->L, f, s);
+    if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch");
+    a.phiq = w + lay.phiq;
+    a.phik = w + lay.phik;
+  }
+  auto launch = [&]() {
+    return lay.given ? luna::launch_causal_given((int)d, D, a, s) : luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
+  };
   if (lay.parts == 2) {
     float* st = reinterpret_cast<float*>(w + lay.state);
     a.pieces = lay.pieces;
     a.piece_chunks = lay.piece_chunks;
     a.state_out = st;
-    hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
+    hipError_t e = launch();
     if (e != hipSuccess) return hip_fail(e, "causal attention state launch");
     a.state_out = nullptr;
     a.state_in = st;
   }
-  hipError_t e = luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
+  hipError_t e = launch();
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");
 }
 

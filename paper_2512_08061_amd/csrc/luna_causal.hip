@@ -19,7 +19,11 @@
 // of a whole sequence, which causal_state_export_kernel writes in the public layout.
 //
 // Roles.  Four matrix waves and four map waves, one of each on every SIMD, so that
-// each SIMD pairs matrix-core work with vector and table-lookup work.
+// each SIMD pairs matrix-core work with vector and table-lookup work.  (With PF, the
+// features are given: phi(Q) and phi(K) in bf16, [head][token][FP], written by the
+// feature-map kernel, for feature maps whose projections and tables do not fit the map
+// waves' registers and LDS, such as one channel per projection with M = 256.  The map
+// waves then only copy phi(Q) rows, transpose phi(K) in registers and sum z.)
 //  - Map wave b maps rows 16 b .. 16 b + 15 of the next chunk's queries and keys for
 //    all projections (the projection on the matrix cores with W fragments and biases
 //    in registers, then the piecewise-linear channel functions from the LDS table),
@@ -52,7 +56,7 @@
 
 namespace luna {
 
-template <typename T, int DH, int L, int MB>
+template <typename T, int DH, int L, int MB, bool PF = false>
 struct CsCfg {
   static constexpr int NCB = DH / 16;             // 16-column blocks of the value width
   static constexpr int NMW = NCB < 4 ? NCB : 4;   // matrix waves that own value columns
@@ -73,26 +77,33 @@ struct CsCfg {
   // one state piece: the matrix waves' S slices (lane-major accumulator tiles), then z
   static constexpr int SF = NMW * CBW * RB * kWave * 4;
   static constexpr int STATE = (SF + FP + 63) / 64 * 64;
-  // bf16: fp16 coefficient rows and keys in 4-key groups; fp32: fp32 rows and plain keys
-  using Tab = typename std::conditional<SZ == 2, PwlLdsN<half2_t, L, NSEG>, PwlLds<L, NSEG>>::type;
+  // bf16: fp16 coefficient rows and keys in 4-key groups; fp32: fp32 rows and plain keys;
+  // features given: no table
+  struct NoTab {};
+  using Tab = typename std::conditional<
+      PF, NoTab, typename std::conditional<SZ == 2, PwlLdsN<half2_t, L, NSEG>, PwlLds<L, NSEG>>::type>::type;
+  static constexpr int WMB = PF ? 1 : MB;  // W fragment blocks held in LDS
   static_assert(NCB == 2 || NCB == 4 || NCB == 8, "d must be 32, 64 or 128");
-  static_assert(FP % 32 == 0 && L % 2 == 0 && (SZ == 4 || L % 4 == 0), "features must fill 32-wide fragments");
+  static_assert(FP % 32 == 0 && (PF || (L % 2 == 0 && (SZ == 4 || L % 4 == 0))),
+                "features must fill 32-wide fragments");
+  static_assert(!PF || (SZ == 2 && L == 1 && (FP == 128 || FP == 256)),
+                "given features: bf16, 128 or 256 of them");
   static_assert(VPT * 256 * VE == 64 * DH, "V chunks must split evenly over the map threads");
 };
 
 // The small arrays that are addressed with constant indices come first, and the
 // table's keys right after them: below 64 KiB their addresses fit the 16-bit
 // offset of an LDS instruction, so that such accesses need no address register.
-template <typename T, int DH, int L, int MB>
+template <typename T, int DH, int L, int MB, bool PF>
 struct CsLds {
-  using C = CsCfg<T, DH, L, MB>;
+  using C = CsCfg<T, DH, L, MB, PF>;
   alignas(16) float denp[4][64];           // row sums of P per key block
   alignas(16) float deni[64];              // phi(Q_c) z_{c-1}
   alignas(16) float zp[4][C::FP];          // z_c over each 16-row block of keys
   alignas(16) T zs[2][C::FP];              // z_c, summed, by chunk parity
   float bias[16 * MB];                     // projection biases, 0 for padded projections
   typename C::Tab tab;  // search keys, bucket windows, coefficient rows
-  alignas(16) T wfr[MB][C::KS][kWave][8];  // W fragments (A of u^T = W X^T, B of u = X W^T)
+  alignas(16) T wfr[C::WMB][C::KS][kWave][8];  // W fragments (A of u^T = W X^T, B of u = X W^T)
   alignas(16) char pm[64 * C::SP];         // P, query-major (blocks above the diagonal stay 0)
   alignas(16) char phq[64 * C::SQ];        // phi(Q_c), token-major, feature f at position f
   alignas(16) char phk[C::FP * C::SK];     // phi(K_c)^T, feature f in row krow(f)
@@ -199,14 +210,15 @@ struct Pack4<float> {
   }
 };
 
-// ST: the state launch (state-only chunks, S and z dumped); otherwise the scan launch
-template <typename T, int DH, int L, int MB, bool ST>
+// ST: the state launch (state-only chunks, S and z dumped); otherwise the scan launch.
+// PF: the features are given (a.phiq, a.phik); L = 1 and MB = FP / 16.
+template <typename T, int DH, int L, int MB, bool ST, bool PF>
 __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
-  using C = CsCfg<T, DH, L, MB>;
+  using C = CsCfg<T, DH, L, MB, PF>;
   constexpr int KS = C::KS, FP = C::FP, NF = C::NF, RB = C::RB, VE = C::VE, NMW = C::NMW, NMS = C::NMS;
   constexpr int CBW = C::CBW, SZ = C::SZ, SQ = C::SQ, SK = C::SK, SP = C::SP, CPV = DH / VE;
   constexpr bool kF16 = sizeof(T) == 2;  // fp16 coefficient rows for bf16 data
-  __shared__ CsLds<T, DH, L, MB> sm;
+  __shared__ CsLds<T, DH, L, MB, PF> sm;
 
   // state launch: one workgroup per (head, piece of the first `split` tokens); scan
   // launch: one per (head, part)
@@ -215,8 +227,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   const int head = blockIdx.x / per_head;
   const int part = blockIdx.x - head * per_head;
   const int hset = a.phi.per_head ? head % a.H : 0;
-  const uint8_t* gtab = a.phi.tables + (size_t)hset * kTableBytes;
-  pwl_load(sm.tab, gtab);
+  if constexpr (!PF) pwl_load(sm.tab, a.phi.tables + (size_t)hset * kTableBytes);
 
   const int tid = threadIdx.x;
   const int wave = wave_id();
@@ -257,7 +268,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   };
 
   // W fragments into LDS; P (above-diagonal blocks stay zero) and z cleared
-  for (int i = tid; i < MB * KS * kWave; i += C::NT) {
+  for (int i = tid; i < (PF ? 0 : MB * KS * kWave); i += C::NT) {
     const int l = i % kWave, ks = (i / kWave) % KS, mb = i / (kWave * KS);
     const int p = 16 * mb + l % 16;
     Frag<T> f;
@@ -273,275 +284,414 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       for (int pc = 0; pc < a.pieces; ++pc) zv += seed[(size_t)pc * C::STATE + C::SF + i % FP];
     (&sm.zs[0][0])[i] = (T)zv;
   }
-  for (int i = tid; i < 16 * MB; i += C::NT) sm.bias[i] = i < M ? bias[i] : 0.0f;
+  if constexpr (!PF)
+    for (int i = tid; i < 16 * MB; i += C::NT) sm.bias[i] = i < M ? bias[i] : 0.0f;
 
   if (wave >= NMS) {
-    // ============================================================== map waves
-    // The map work is a chain of dependent table lookups: its LDS requests are issued
-    // ahead of the matrix waves' bursts of operand reads.
-    __builtin_amdgcn_s_setprio(3);
-    const int rb = wave - NMS;  // rows 16 rb .. 16 rb + 15 of every chunk, all projections
-    const int mtid = tid - 64 * NMS;
-    const bool pad_proj = 16 * MB > M;  // padded projections exist (phi(K) of them is set to 0)
-    // byte offsets of this lane's pieces
-    const int x_off = ((16 * rb + r) * DH + 8 * g) * SZ;  // its slice of a Q or K row in a chunk
-    // phi(Q) of token 16 rb + r, projection 16 mb + 4 g + j, channel l: feature
-    // feat(4 g, 0) + feat(16 mb, l) + j
-    char* q_dst = sm.phq + (16 * rb + r) * SQ + feat<MB>(4 * g, 0) * SZ;
-    // phi(K)^T row 16 (mb + MB l) + r (projection 16 mb + r, channel l), tokens 16 rb + 4 g ..
-    char* k_dst = sm.phk + r * SK + (16 * rb + 4 * g) * SZ;
-    Frag<T> xq[KS], xk[KS];  // query and key rows of the next chunk to map
-    i32x4 vr[C::VPT];        // this thread's share of V of the next chunk
-    auto load_rows = [&](Frag<T> (&xf)[KS], const void* X, int cc, bool live) {
-      const auto rs = rows_of(X, cc, live ? n : 0);
+    if constexpr (PF) {
+      // ============================================== map waves, features given
+      // Map wave b moves rows 16 b .. 16 b + 15 of the next chunk: phi(Q) copied
+      // token-major (feature f at position f), phi(K) transposed in registers (feature f
+      // to phi(K)^T row krow(f)), a share of V, and running sums of its key rows'
+      // features for z.  Lane (tg, fc) holds features 8 fc .. 8 fc + 7 of TPL consecutive
+      // tokens.
+      __builtin_amdgcn_s_setprio(3);
+      constexpr int CPR = FP / 8, TG = kWave / CPR, TPL = 16 / TG;
+      const int rb = wave - NMS, mtid = tid - 64 * NMS;
+      const int fc = lane % CPR, tg = lane / CPR;
+      const int t0 = 16 * rb + TPL * tg;  // this lane's first token in the chunk
+      i32x4 qv[TPL], kv[TPL];
+      i32x4 vr[C::VPT];
+      float zrun[8];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) buf_load8(xf[ks], rs, x_off + 32 * ks * SZ);
-    };
-    auto load_v = [&](int cc) {
-      const auto rs = rows_of(a.V, cc, n);
+      for (int e = 0; e < 8; ++e) zrun[e] = 0.0f;
+      if (seeded && rb == 0 && tg == 0)  // the prefix's z enters through map wave 0
+        for (int pc = 0; pc < a.pieces; ++pc)
 #pragma unroll
-      for (int q = 0; q < C::VPT; ++q)
-        vr[q] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * (mtid + 256 * q), 0, 0));
-    };
-    auto store_v = [&]() {
+          for (int e = 0; e < 8; ++e) zrun[e] += seed[(size_t)pc * C::STATE + C::SF + 8 * fc + e];
+      auto load_feat = [&](i32x4 (&dst)[TPL], const void* X, int cc, bool live) {
+        const char* base = reinterpret_cast<const char*>(X) + ((size_t)head * n + (size_t)64 * cc) * FP * SZ;
+        const int rows = __builtin_amdgcn_readfirstlane(max(0, min(64, (live ? n : 0) - 64 * cc)));
+        const auto rs =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), (short)0, rows * FP * SZ, kBufferFlags);
 #pragma unroll
-      for (int q = 0; q < C::VPT; ++q) {
-        const int cidx = mtid + 256 * q;
-        const int tt = cidx / CPV, cg = cidx % CPV;
-        *reinterpret_cast<i32x4*>(&sm.vt[tt * DH + swz_v<CPV>(tt, cg) * VE]) = vr[q];
-      }
-    };
-    // W fragments and biases of all projections, held in registers
-    Frag<T> wreg[MB][KS];
-    f32x4 bq[MB], bk[MB];
-    // u for the 16 rows: query rows as u^T = W X^T (lane: projections 16 mb + 4 g + j
-    // of token r), key rows as u = X W^T (lane: projection 16 mb + r of tokens 4 g + j);
-    // the accumulators start at the biases
-    auto project = [&](const Frag<T> (&xf)[KS], bool isq, float (&uu)[4 * MB]) {
+        for (int k = 0; k < TPL; ++k)
+          dst[k] = __builtin_bit_cast(
+              i32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, ((t0 + k) * FP + 8 * fc) * SZ, 0, 0));
+      };
+      auto load_v = [&](int cc) {
+        const auto rs = rows_of(a.V, cc, n);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        f32x4 acc = isq ? bq[mb] : bk[mb];
+        for (int q = 0; q < C::VPT; ++q)
+          vr[q] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * (mtid + 256 * q), 0, 0));
+      };
+      auto store_v = [&]() {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          if (isq) mma(acc, wreg[mb][ks], xf[ks]);
-          else mma(acc, xf[ks], wreg[mb][ks]);
+        for (int q = 0; q < C::VPT; ++q) {
+          const int cidx = mtid + 256 * q;
+          const int tt = cidx / CPV, cg = cidx % CPV;
+          *reinterpret_cast<i32x4*>(&sm.vt[tt * DH + swz_v<CPV>(tt, cg) * VE]) = vr[q];
         }
+      };
+      auto write_q = [&]() {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j];
-      }
-    };
-    // phi of this lane's 4 MB values u, as Pack4<T> per (block, channel) (the four j
-    // in order), from the values and their segment offsets; query and key rows
-    Pack4<T> phq_r[MB][L], phk_r[MB][L];
-    auto eval_all = [&](Pack4<T> (&ph)[MB][L], const float (&uu)[4 * MB], const unsigned (&off)[4 * MB],
-                        float floor) {
+        for (int k = 0; k < TPL; ++k) *reinterpret_cast<i32x4*>(sm.phq + (t0 + k) * SQ + 16 * fc) = qv[k];
+      };
+      // feature 8 fc + e of the TPL tokens: one store into its phi(K)^T row
+      auto write_k = [&]() {
+        typedef __attribute__((ext_vector_type(TPL))) __bf16 bf16xT;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
+        for (int e = 0; e < 8; ++e) {
+          bf16xT col;
 #pragma unroll
-        for (int jp = 0; jp < 2; ++jp) {
-          const int i0 = 4 * mb + 2 * jp;
-          float y0[L], y1[L];
-          pwl_eval_off(sm.tab, off[i0], floor, uu[i0], y0);
-          pwl_eval_off(sm.tab, off[i0 + 1], floor, uu[i0 + 1], y1);
-#pragma unroll
-          for (int l = 0; l < L; ++l) ph[mb][l].set2(2 * jp, y0[l], y1[l]);
+          for (int k = 0; k < TPL; ++k) col[k] = __builtin_bit_cast(bf16x8, kv[k])[e];
+          *reinterpret_cast<bf16xT*>(sm.phk + krow(8 * fc + e) * SK + t0 * SZ) = col;
         }
-    };
-    auto write_q = [&]() {
+      };
+      auto add_z = [&]() {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
+        for (int k = 0; k < TPL; ++k)
 #pragma unroll
-        for (int l = 0; l < L; ++l) phq_r[mb][l].store(q_dst + feat<MB>(16 * mb, l) * SZ);
-    };
-    auto write_k = [&]() {
+          for (int e = 0; e < 8; ++e) zrun[e] += (float)__builtin_bit_cast(bf16x8, kv[k])[e];
+      };
+      // z over this wave's key rows through the chunk just written (lanes of one fc summed)
+      auto write_z = [&]() {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int l = 0; l < L; ++l) phk_r[mb][l].store(k_dst + 16 * (mb + MB * l) * SK);
-    };
-    // z over this wave's key rows: tile mb rows = projections 16 mb + 4 g + jj,
-    // column l = channel l, accumulated from phi(K) fragments (channels 2q, 2q + 1 of
-    // tokens 4 g .. 4 g + 3) times one-hot columns
-    f32x4 zacc[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) zacc[mb] = zero4();
-    if (seeded && rb == 0 && r < L) {  // the prefix's z enters through map wave 0
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          for (int pc = 0; pc < a.pieces; ++pc)
-            zacc[mb][jj] += seed[(size_t)pc * C::STATE + C::SF + feat<MB>(16 * mb + 4 * g, r) + jj];
-    }
-    auto add_z = [&]() {
-#pragma unroll
-      for (int q = 0; q < L / 2; ++q) {
-        Frag<T> oh;
-        const float lo = r == 2 * q ? 1.0f : 0.0f, hi = r == 2 * q + 1 ? 1.0f : 0.0f;
-        oh.set2(0, lo, lo);
-        oh.set2(2, lo, lo);
-        oh.set2(4, hi, hi);
-        oh.set2(6, hi, hi);
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          Frag<T> kf;
-          phk_r[mb][2 * q].to_frag(kf, 0);
-          phk_r[mb][2 * q + 1].to_frag(kf, 4);
-          mma(zacc[mb], kf, oh);
+        for (int e = 0; e < 8; ++e) {
+          float zz = sum_xor32(zrun[e]);
+          if constexpr (TG == 4) zz = sum_xor16(zz);
+          if (tg == 0) sm.zp[rb][8 * fc + e] = zz;
         }
-      }
-    };
-    auto write_z = [&]() {
-      if (r < L) {
+      };
+      auto sum_z = [&](int slot) {
+        constexpr int FW = FP / 4;
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          float* zp = &sm.zp[rb][feat<MB>(16 * mb + 4 * g, r)];
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) zp[jj] = zacc[mb][jj];
+        for (int f0 = 0; f0 < FW; f0 += kWave) {
+          const int f = FW * rb + f0 + lane;
+          if (f0 + lane < FW) sm.zs[slot][f] = (T)(((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f]);
         }
-      }
-    };
-    // the four row-block parts summed in a fixed order, this wave's quarter of the features
-    auto sum_z = [&](int slot) {
-      constexpr int FW = FP / 4;
-#pragma unroll
-      for (int f0 = 0; f0 < FW; f0 += kWave) {
-        const int f = FW * rb + f0 + lane;
-        if (f0 + lane < FW) sm.zs[slot][f] = (T)(((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f]);
-      }
-    };
-    // query rows are needed from chunk c_begin on, key rows and V from chunk c_first
-    load_rows(xq, a.Q, c_first, c_first >= c_begin && c_first < c_end);
-    load_rows(xk, a.K, c_first, c_first < c_end);
-    load_v(c_first);
-    __syncthreads();  // tables, W fragments, cleared P and z
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) load8(wreg[mb][ks], &sm.wfr[mb][ks][lane][0]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bq[mb][j] = sm.bias[16 * mb + 4 * g + j];
-        bk[mb][j] = sm.bias[16 * mb + r];
-      }
-    }
-    const int steps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
-    const int nodes = __builtin_amdgcn_readfirstlane(pwl_nodes(sm.tab));
-    const unsigned zoff = 4u * sm.tab.zero_seg;
-    const float tfloor = sm.tab.floor;
-    // u of the query rows and the key rows of one chunk and their segment offsets
-    float uq[4 * MB], uk[4 * MB];
-    unsigned oq[4 * MB], ok[4 * MB];
-    // projections of the rows held in xq, xk and the searches, as one batch when the
-    // query rows are live, so that their lookups overlap
-    auto project_search = [&](auto qlive) {
-      constexpr bool kQ = decltype(qlive)::value;
-      if constexpr (kQ) {
-        project(xq, true, uq);
-        project(xk, false, uk);
-        float uu[8 * MB];
-        unsigned oo[8 * MB];
-#pragma unroll
-        for (int i = 0; i < 4 * MB; ++i) {
-          uu[i] = uq[i];
-          uu[4 * MB + i] = uk[i];
-        }
-        pwl_search_any(sm.tab, steps, nodes, uu, oo);
-#pragma unroll
-        for (int i = 0; i < 4 * MB; ++i) {
-          oq[i] = oo[i];
-          ok[i] = oo[4 * MB + i];
+      };
+      if constexpr (ST) {
+        // state launch: phi(K) and V only (z is summed by matrix wave 0)
+        load_feat(kv, a.phik, c_first, c_first < c_end);
+        load_v(c_first);
+        __syncthreads();  // cleared P and z
+        write_k();
+        store_v();
+        load_feat(kv, a.phik, c_first + 1, c_first + 1 < c_end);
+        load_v(c_first + 1);
+        for (int c = c_first; c < c_end; ++c) {
+          const int cn = c + 1;
+          __syncthreads();  // B1
+          __syncthreads();  // B2
+          if (cn < c_end) {
+            write_k();
+            store_v();
+          }
+          load_feat(kv, a.phik, cn + 1, cn + 1 < c_end);
+          load_v(cn + 1);
         }
       } else {
-        project(xk, false, uk);
-        pwl_search_any(sm.tab, steps, nodes, uk, ok);
-      }
-      if (pad_proj) {  // padded projections of the key rows select the all-zero segment
-#pragma unroll
-        for (int i = 0; i < 4 * MB; ++i)
-          if (16 * (i / 4) + r >= M) ok[i] = zoff;
-      }
-    };
-    // phi of the rows held in xq, xk (the query rows when live) into phq_r, phk_r, and
-    // the key rows added to z
-    auto map_rows = [&](auto qlive, int cc) {
-      project_search(qlive);
-      if constexpr (ST) {  // key rows at or past n (a state of the whole sequence) add nothing
-#pragma unroll
-        for (int i = 0; i < 4 * MB; ++i)
-          if (64 * cc + 16 * rb + 4 * g + i % 4 >= n) ok[i] = zoff;
-      }
-      if constexpr (decltype(qlive)::value) eval_all(phq_r, uq, oq, tfloor);
-      eval_all(phk_r, uk, ok, tfloor);
-      if constexpr (!ST) add_z();  // (the state launch's z comes from matrix wave 0)
-    };
-    if constexpr (ST) {
-      // State launch: every chunk is state-only; z is summed by matrix wave 0 along
-      // with its slice of S (one-hot products here would lengthen the map waves'
-      // chain, which sets this launch's pace).  (Mapping the key rows of two chunks as
-      // one batch made this launch slower: 186 against 159 us.)
-      map_rows(std::false_type{}, c_first);
-      load_rows(xq, a.Q, c_first + 1, false);
-      load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
-      write_k();
-      store_v();
-      load_v(c_first + 1);
-      for (int c = c_first; c < c_end; ++c) {
-        const int cn = c + 1;
-        __syncthreads();  // B1
-        const bool kn = cn < c_end;
-        if (kn) map_rows(std::false_type{}, cn);
-        load_rows(xq, a.Q, cn + 1, false);  // issued on every path (see the scan launch)
-        load_rows(xk, a.K, cn + 1, kn);
-        __syncthreads();  // B2
-        if (kn) {
-          write_k();
-          store_v();
+        const bool q0 = c_first >= c_begin;
+        load_feat(qv, a.phiq, c_first, q0 && c_first < c_end);
+        load_feat(kv, a.phik, c_first, c_first < c_end);
+        load_v(c_first);
+        __syncthreads();  // cleared P and z
+        if (q0) write_q();
+        write_k();
+        add_z();
+        write_z();  // z through chunk c_first
+        store_v();
+        load_feat(qv, a.phiq, c_first + 1, c_first + 1 >= c_begin && c_first + 1 < c_end);
+        load_feat(kv, a.phik, c_first + 1, c_first + 1 < c_end);
+        load_v(c_first + 1);
+        // iteration c: chunk c + 1's rows (loaded one iteration ahead) are written after B2
+        for (int c = c_first; c < c_end; ++c) {
+          const int cn = c + 1;
+          __syncthreads();  // B1: chunk c's tiles are in LDS; zp holds z through chunk c
+          sum_z(c & 1);
+          __syncthreads();  // B2: chunk c's phi tiles and V are no longer read
+          const bool kn = cn < c_end, qn = kn && cn >= c_begin;
+          if (kn) {
+            if (qn) write_q();
+            write_k();
+            add_z();
+            write_z();  // z through chunk c + 1
+            store_v();
+          }
+          load_feat(qv, a.phiq, cn + 1, kn && cn + 1 >= c_begin && cn + 1 < c_end);
+          load_feat(kv, a.phik, cn + 1, cn + 1 < c_end);
+          load_v(cn + 1);
         }
-        load_v(cn + 1);
       }
     } else {
-      // chunk c_first
-      if (c_first >= c_begin) map_rows(std::true_type{}, c_first);
-      else map_rows(std::false_type{}, c_first);
-      load_rows(xq, a.Q, c_first + 1, c_first + 1 >= c_begin && c_first + 1 < c_end);
-      load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
-      if (c_first >= c_begin) write_q();
-      write_k();
-      write_z();  // z through chunk c_first
-      store_v();
-      load_v(c_first + 1);
+      // ============================================================== map waves
+      // The map work is a chain of dependent table lookups: its LDS requests are issued
+      // ahead of the matrix waves' bursts of operand reads.
+      __builtin_amdgcn_s_setprio(3);
+      const int rb = wave - NMS;  // rows 16 rb .. 16 rb + 15 of every chunk, all projections
+      const int mtid = tid - 64 * NMS;
+      const bool pad_proj = 16 * MB > M;  // padded projections exist (phi(K) of them is set to 0)
+      // byte offsets of this lane's pieces
+      const int x_off = ((16 * rb + r) * DH + 8 * g) * SZ;  // its slice of a Q or K row in a chunk
+      // phi(Q) of token 16 rb + r, projection 16 mb + 4 g + j, channel l: feature
+      // feat(4 g, 0) + feat(16 mb, l) + j
+      char* q_dst = sm.phq + (16 * rb + r) * SQ + feat<MB>(4 * g, 0) * SZ;
+      // phi(K)^T row 16 (mb + MB l) + r (projection 16 mb + r, channel l), tokens 16 rb + 4 g ..
+      char* k_dst = sm.phk + r * SK + (16 * rb + 4 * g) * SZ;
+      Frag<T> xq[KS], xk[KS];  // query and key rows of the next chunk to map
+      i32x4 vr[C::VPT];        // this thread's share of V of the next chunk
+      auto load_rows = [&](Frag<T> (&xf)[KS], const void* X, int cc, bool live) {
+        const auto rs = rows_of(X, cc, live ? n : 0);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) buf_load8(xf[ks], rs, x_off + 32 * ks * SZ);
+      };
+      auto load_v = [&](int cc) {
+        const auto rs = rows_of(a.V, cc, n);
+#pragma unroll
+        for (int q = 0; q < C::VPT; ++q)
+          vr[q] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * (mtid + 256 * q), 0, 0));
+      };
+      auto store_v = [&]() {
+#pragma unroll
+        for (int q = 0; q < C::VPT; ++q) {
+          const int cidx = mtid + 256 * q;
+          const int tt = cidx / CPV, cg = cidx % CPV;
+          *reinterpret_cast<i32x4*>(&sm.vt[tt * DH + swz_v<CPV>(tt, cg) * VE]) = vr[q];
+        }
+      };
+      // W fragments and biases of all projections, held in registers
+      Frag<T> wreg[MB][KS];
+      f32x4 bq[MB], bk[MB];
+      // u for the 16 rows: query rows as u^T = W X^T (lane: projections 16 mb + 4 g + j
+      // of token r), key rows as u = X W^T (lane: projection 16 mb + r of tokens 4 g + j);
+      // the accumulators start at the biases
+      auto project = [&](const Frag<T> (&xf)[KS], bool isq, float (&uu)[4 * MB]) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          f32x4 acc = isq ? bq[mb] : bk[mb];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            if (isq) mma(acc, wreg[mb][ks], xf[ks]);
+            else mma(acc, xf[ks], wreg[mb][ks]);
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) uu[4 * mb + j] = acc[j];
+        }
+      };
+      // phi of this lane's 4 MB values u, as Pack4<T> per (block, channel) (the four j
+      // in order), from the values and their segment offsets; query and key rows
+      Pack4<T> phq_r[MB][L], phk_r[MB][L];
+      auto eval_all = [&](Pack4<T> (&ph)[MB][L], const float (&uu)[4 * MB], const unsigned (&off)[4 * MB],
+                          float floor) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int jp = 0; jp < 2; ++jp) {
+            const int i0 = 4 * mb + 2 * jp;
+            float y0[L], y1[L];
+            pwl_eval_off(sm.tab, off[i0], floor, uu[i0], y0);
+            pwl_eval_off(sm.tab, off[i0 + 1], floor, uu[i0 + 1], y1);
+#pragma unroll
+            for (int l = 0; l < L; ++l) ph[mb][l].set2(2 * jp, y0[l], y1[l]);
+          }
+      };
+      auto write_q = [&]() {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int l = 0; l < L; ++l) phq_r[mb][l].store(q_dst + feat<MB>(16 * mb, l) * SZ);
+      };
+      auto write_k = [&]() {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int l = 0; l < L; ++l) phk_r[mb][l].store(k_dst + 16 * (mb + MB * l) * SK);
+      };
+      // z over this wave's key rows: tile mb rows = projections 16 mb + 4 g + jj,
+      // column l = channel l, accumulated from phi(K) fragments (channels 2q, 2q + 1 of
+      // tokens 4 g .. 4 g + 3) times one-hot columns
+      f32x4 zacc[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) zacc[mb] = zero4();
+      if (seeded && rb == 0 && r < L) {  // the prefix's z enters through map wave 0
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            for (int pc = 0; pc < a.pieces; ++pc)
+              zacc[mb][jj] += seed[(size_t)pc * C::STATE + C::SF + feat<MB>(16 * mb + 4 * g, r) + jj];
+      }
+      auto add_z = [&]() {
+#pragma unroll
+        for (int q = 0; q < L / 2; ++q) {
+          Frag<T> oh;
+          const float lo = r == 2 * q ? 1.0f : 0.0f, hi = r == 2 * q + 1 ? 1.0f : 0.0f;
+          oh.set2(0, lo, lo);
+          oh.set2(2, lo, lo);
+          oh.set2(4, hi, hi);
+          oh.set2(6, hi, hi);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            Frag<T> kf;
+            phk_r[mb][2 * q].to_frag(kf, 0);
+            phk_r[mb][2 * q + 1].to_frag(kf, 4);
+            mma(zacc[mb], kf, oh);
+          }
+        }
+      };
+      auto write_z = [&]() {
+        if (r < L) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            float* zp = &sm.zp[rb][feat<MB>(16 * mb + 4 * g, r)];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) zp[jj] = zacc[mb][jj];
+          }
+        }
+      };
+      // the four row-block parts summed in a fixed order, this wave's quarter of the features
+      auto sum_z = [&](int slot) {
+        constexpr int FW = FP / 4;
+#pragma unroll
+        for (int f0 = 0; f0 < FW; f0 += kWave) {
+          const int f = FW * rb + f0 + lane;
+          if (f0 + lane < FW) sm.zs[slot][f] = (T)(((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f]);
+        }
+      };
+      // query rows are needed from chunk c_begin on, key rows and V from chunk c_first
+      load_rows(xq, a.Q, c_first, c_first >= c_begin && c_first < c_end);
+      load_rows(xk, a.K, c_first, c_first < c_end);
+      load_v(c_first);
+      __syncthreads();  // tables, W fragments, cleared P and z
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) load8(wreg[mb][ks], &sm.wfr[mb][ks][lane][0]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          bq[mb][j] = sm.bias[16 * mb + 4 * g + j];
+          bk[mb][j] = sm.bias[16 * mb + r];
+        }
+      }
+      const int steps = __builtin_amdgcn_readfirstlane(sm.tab.steps);
+      const int nodes = __builtin_amdgcn_readfirstlane(pwl_nodes(sm.tab));
+      const unsigned zoff = 4u * sm.tab.zero_seg;
+      const float tfloor = sm.tab.floor;
+      // u of the query rows and the key rows of one chunk and their segment offsets
+      float uq[4 * MB], uk[4 * MB];
+      unsigned oq[4 * MB], ok[4 * MB];
+      // projections of the rows held in xq, xk and the searches, as one batch when the
+      // query rows are live, so that their lookups overlap
+      auto project_search = [&](auto qlive) {
+        constexpr bool kQ = decltype(qlive)::value;
+        if constexpr (kQ) {
+          project(xq, true, uq);
+          project(xk, false, uk);
+          float uu[8 * MB];
+          unsigned oo[8 * MB];
+#pragma unroll
+          for (int i = 0; i < 4 * MB; ++i) {
+            uu[i] = uq[i];
+            uu[4 * MB + i] = uk[i];
+          }
+          pwl_search_any(sm.tab, steps, nodes, uu, oo);
+#pragma unroll
+          for (int i = 0; i < 4 * MB; ++i) {
+            oq[i] = oo[i];
+            ok[i] = oo[4 * MB + i];
+          }
+        } else {
+          project(xk, false, uk);
+          pwl_search_any(sm.tab, steps, nodes, uk, ok);
+        }
+        if (pad_proj) {  // padded projections of the key rows select the all-zero segment
+#pragma unroll
+          for (int i = 0; i < 4 * MB; ++i)
+            if (16 * (i / 4) + r >= M) ok[i] = zoff;
+        }
+      };
+      // phi of the rows held in xq, xk (the query rows when live) into phq_r, phk_r, and
+      // the key rows added to z
+      auto map_rows = [&](auto qlive, int cc) {
+        project_search(qlive);
+        if constexpr (ST) {  // key rows at or past n (a state of the whole sequence) add nothing
+#pragma unroll
+          for (int i = 0; i < 4 * MB; ++i)
+            if (64 * cc + 16 * rb + 4 * g + i % 4 >= n) ok[i] = zoff;
+        }
+        if constexpr (decltype(qlive)::value) eval_all(phq_r, uq, oq, tfloor);
+        eval_all(phk_r, uk, ok, tfloor);
+        if constexpr (!ST) add_z();  // (the state launch's z comes from matrix wave 0)
+      };
+      if constexpr (ST) {
+        // State launch: every chunk is state-only; z is summed by matrix wave 0 along
+        // with its slice of S (one-hot products here would lengthen the map waves'
+        // chain, which sets this launch's pace).  (Mapping the key rows of two chunks as
+        // one batch made this launch slower: 186 against 159 us.)
+        map_rows(std::false_type{}, c_first);
+        load_rows(xq, a.Q, c_first + 1, false);
+        load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
+        write_k();
+        store_v();
+        load_v(c_first + 1);
+        for (int c = c_first; c < c_end; ++c) {
+          const int cn = c + 1;
+          __syncthreads();  // B1
+          const bool kn = cn < c_end;
+          if (kn) map_rows(std::false_type{}, cn);
+          load_rows(xq, a.Q, cn + 1, false);  // issued on every path (see the scan launch)
+          load_rows(xk, a.K, cn + 1, kn);
+          __syncthreads();  // B2
+          if (kn) {
+            write_k();
+            store_v();
+          }
+          load_v(cn + 1);
+        }
+      } else {
+        // chunk c_first
+        if (c_first >= c_begin) map_rows(std::true_type{}, c_first);
+        else map_rows(std::false_type{}, c_first);
+        load_rows(xq, a.Q, c_first + 1, c_first + 1 >= c_begin && c_first + 1 < c_end);
+        load_rows(xk, a.K, c_first + 1, c_first + 1 < c_end);
+        if (c_first >= c_begin) write_q();
+        write_k();
+        write_z();  // z through chunk c_first
+        store_v();
+        load_v(c_first + 1);
 
-      // Iteration c: between B1 and B2 the matrix waves read chunk c's tiles while this
-      // wave maps chunk c + 1 (rows fetched one chunk ahead) into registers; after B2 it
-      // writes chunk c + 1's tiles, V and z.
-      for (int c = c_first; c < c_end; ++c) {
-        const int cn = c + 1;
-        __syncthreads();  // B1: chunk c's tiles are in LDS; zp holds z through chunk c
-        sum_z(c & 1);
-        const bool kn = cn < c_end, qn = kn && cn >= c_begin;
-        // phi(Q) before B2; the key rows are only projected and searched here and
-        // evaluated after B2, where the matrix waves' work is shorter
-        if (qn) {
-          project_search(std::true_type{});
-          eval_all(phq_r, uq, oq, tfloor);
-        } else if (kn) {
-          project_search(std::false_type{});
+        // Iteration c: between B1 and B2 the matrix waves read chunk c's tiles while this
+        // wave maps chunk c + 1 (rows fetched one chunk ahead) into registers; after B2 it
+        // writes chunk c + 1's tiles, V and z.
+        for (int c = c_first; c < c_end; ++c) {
+          const int cn = c + 1;
+          __syncthreads();  // B1: chunk c's tiles are in LDS; zp holds z through chunk c
+          sum_z(c & 1);
+          const bool kn = cn < c_end, qn = kn && cn >= c_begin;
+          // phi(Q) before B2; the key rows are only projected and searched here and
+          // evaluated after B2, where the matrix waves' work is shorter
+          if (qn) {
+            project_search(std::true_type{});
+            eval_all(phq_r, uq, oq, tfloor);
+          } else if (kn) {
+            project_search(std::false_type{});
+          }
+          // the loads are issued on every path (past the end as empty buffers, which read
+          // nothing), so that the waits for them count the same loads on every path
+          load_rows(xq, a.Q, cn + 1, kn && cn + 1 >= c_begin);
+          load_rows(xk, a.K, cn + 1, kn);
+          __syncthreads();  // B2: chunk c's phi tiles and V are no longer read
+          if (kn) {
+            if (qn) write_q();
+            eval_all(phk_r, uk, ok, tfloor);
+            add_z();
+            write_k();
+            write_z();  // z through chunk c + 1
+            store_v();
+          }
+          load_v(cn + 1);
         }
-        // the loads are issued on every path (past the end as empty buffers, which read
-        // nothing), so that the waits for them count the same loads on every path
-        load_rows(xq, a.Q, cn + 1, kn && cn + 1 >= c_begin);
-        load_rows(xk, a.K, cn + 1, kn);
-        __syncthreads();  // B2: chunk c's phi tiles and V are no longer read
-        if (kn) {
-          if (qn) write_q();
-          eval_all(phk_r, uk, ok, tfloor);
-          add_z();
-          write_k();
-          write_z();  // z through chunk c + 1
-          store_v();
-        }
-        load_v(cn + 1);
       }
     }
   } else {
@@ -585,7 +735,9 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) num[x][i] = zero4();
     __syncthreads();  // tables, W fragments, cleared P and z
-    const float eps = ldexpf(a.eps, 2 * sm.tab.scale_exp);
+    // (the bf16 tables' coefficient rows carry a power-of-two scale, which eps takes too)
+    float eps = a.eps;
+    if constexpr (!PF) eps = ldexpf(a.eps, 2 * sm.tab.scale_exp);
 
     // P^T blocks (query block i >= key block j): rows = key tokens 16 j + 4 g + jj,
     // column = query token 16 i + r, for CNT query blocks i0 .. i0 + CNT - 1 that share
@@ -895,9 +1047,22 @@ static hipError_t cs_run(const CausalArgs& a, hipStream_t s) {
   }
   const int per_head = a.state_out != nullptr ? a.pieces : a.parts;
   if (a.state_out != nullptr)
-    hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, true>), dim3(a.heads * per_head), dim3(512), 0, s, a);
+    hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, true, false>), dim3(a.heads * per_head), dim3(512), 0, s, a);
   else
-    hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, false>), dim3(a.heads * per_head), dim3(512), 0, s, a);
+    hipLaunchKernelGGL((causal_kernel<T, DH, L, MB, false, false>), dim3(a.heads * per_head), dim3(512), 0, s, a);
+  return hipGetLastError();
+}
+
+// features given: FP bf16 features per token in a.phiq, a.phik
+template <int DH, int FP>
+static hipError_t cs_run_given(const CausalArgs& a, hipStream_t s) {
+  const int per_head = a.state_out != nullptr ? a.pieces : a.parts;
+  if (a.state_out != nullptr)
+    hipLaunchKernelGGL((causal_kernel<__bf16, DH, 1, FP / 16, true, true>), dim3(a.heads * per_head), dim3(512), 0,
+                       s, a);
+  else
+    hipLaunchKernelGGL((causal_kernel<__bf16, DH, 1, FP / 16, false, true>), dim3(a.heads * per_head), dim3(512), 0,
+                       s, a);
   return hipGetLastError();
 }
 
@@ -931,6 +1096,35 @@ size_t causal_state_floats(Dt dt, int d, int L, int M) {
   LUNA_CS_CASES(X)
 #undef X
   return 0;
+}
+
+// (d, features) combinations built with the features given (bf16)
+#define LUNA_CS_GIVEN_CASES(X) \
+  X(128, 256)                  \
+  X(64, 128)
+
+bool causal_given_supported(Dt dt, int d, int D) {
+#define X(D_, F_) \
+  if (dt == Dt::BF16 && d == D_ && D == F_) return true;
+  LUNA_CS_GIVEN_CASES(X)
+#undef X
+  return false;
+}
+
+size_t causal_given_state_floats(int d, int D) {
+#define X(D_, F_) \
+  if (d == D_ && D == F_) return CsCfg<__bf16, D_, 1, F_ / 16, true>::STATE;
+  LUNA_CS_GIVEN_CASES(X)
+#undef X
+  return 0;
+}
+
+hipError_t launch_causal_given(int d, int D, const CausalArgs& a, hipStream_t s) {
+#define X(D_, F_) \
+  if (d == D_ && D == F_) return cs_run_given<D_, F_>(a, s);
+  LUNA_CS_GIVEN_CASES(X)
+#undef X
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s) {

@@ -86,33 +86,40 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
       const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
       const float floor = tab.floor;
 
+      // the group's projections, then one search over all of them, so that the
+      // searches' dependent LDS reads overlap
+      float uu[4 * kMaxMB];
 #pragma unroll
       for (int mbl = 0; mbl < kMaxMB; ++mbl) {
-        const int mb = mg + mbl;
-        if (mb >= MB) break;
         f32x4 acc = zero4();
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mbl][ks], xf[ks]);
-        float uu[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) uu[j] = acc[j] + bz[mbl][j];
-        int sg[4];
-        pwl_search(tab, steps, uu, sg);
+        for (int j = 0; j < 4; ++j) uu[4 * mbl + j] = acc[j] + bz[mbl][j];
+      }
+      int sg[4 * kMaxMB];
+      pwl_search(tab, steps, uu, sg);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int i = 16 * mb + 4 * g + j;
-          if (i < M && row_ok) {
-            float y[L];
-            pwl_channels<L>(tab, sg[j], floor, uu[j], y);
-            Tout* o = out + i * L;
-            if constexpr (L % 4 == 0) {
+      for (int mbl = 0; mbl < kMaxMB; ++mbl) {
+        const int mb = mg + mbl;
+        if (mb >= MB || !row_ok) break;
+        const int i0 = 16 * mb + 4 * g;  // projections i0 .. i0 + 3 of this lane
+        float y[4][L];
 #pragma unroll
-              for (int q = 0; q < L / 4; ++q) store4(o + 4 * q, y[4 * q], y[4 * q + 1], y[4 * q + 2], y[4 * q + 3]);
-            } else {
+        for (int j = 0; j < 4; ++j) pwl_channels<L>(tab, sg[4 * mbl + j], floor, uu[4 * mbl + j], y[j]);
+        Tout* o = out + i0 * L;
+        if (i0 + 3 < M) {  // the four projections' 4 L features are contiguous
 #pragma unroll
-              for (int l = 0; l < L; ++l) o[l] = (Tout)y[l];
-            }
+          for (int q = 0; q < L; ++q) {
+            const float* f = &y[0][0] + 4 * q;  // features 4 q .. 4 q + 3 of the four
+            store4(o + 4 * q, f[0], f[1], f[2], f[3]);
           }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (i0 + j < M)
+#pragma unroll
+              for (int l = 0; l < L; ++l) o[j * L + l] = (Tout)y[j][l];
         }
       }
     }

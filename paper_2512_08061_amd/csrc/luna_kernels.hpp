@@ -151,6 +151,9 @@ struct CausalArgs {
   float* export_S;
   float* export_z;
   int accumulate;
+  // features given (launch_causal_given): phi(Q), phi(K) [heads][n][D] in bf16
+  const void* phiq;
+  const void* phik;
 };
 
 // One streaming step of causal attention over m new tokens per head, from the
@@ -267,6 +270,11 @@ bool causal_supported(Dt dt, int d, int L, int M);
 // floats of one state piece (S slices of the matrix waves, then z) for a combination
 size_t causal_state_floats(Dt dt, int d, int L, int M);
 hipError_t launch_causal(Dt dt, int d, int L, int M, const CausalArgs& a, hipStream_t s);
+// The causal kernel with the features given in bf16 (D of them per token), for the
+// feature maps whose projections and tables the fused kernel cannot hold.
+bool causal_given_supported(Dt dt, int d, int D);
+size_t causal_given_state_floats(int d, int D);
+hipError_t launch_causal_given(int d, int D, const CausalArgs& a, hipStream_t s);
 
 // LDS copy of the segment table: one row of (slope, intercept) pairs per segment.
 // Rows whose size is a multiple of 64 bytes are padded by 16 bytes so that random

@@ -142,13 +142,18 @@ def test_generic_path_planning(lib):
     features, [V | 1], [num | den - eps] and the per-chunk states (and P, causal), and
     its chunk count is capped; M above 256 is invalid."""
     d, n, B, H = 128, 16384, 8, 16
-    p1 = _params(M=256, L=1)
-    for op, chunk_bytes in [(luna.OP_ATTN_CAUSAL, 256 * 129 * 4 + 64 * 64 * 4), (luna.OP_ATTN, 256 * 129 * 4)]:
+    rows = B * H * n
+    p200 = _params(M=200, L=1)
+    for op, chunk_bytes in [(luna.OP_ATTN_CAUSAL, 200 * 129 * 4 + 64 * 64 * 4), (luna.OP_ATTN, 200 * 129 * 4)]:
         chunk = 64 if op == luna.OP_ATTN_CAUSAL else 512
-        nb = lib.luna_workspace_bytes(op, luna.LUNA_BF16, B, H, n, d, ctypes.byref(p1), 64)
-        rows = B * H * n
-        floor = rows * (2 * 256 + 2 * 129) * 4 + B * H * (n // chunk) * chunk_bytes
+        nb = lib.luna_workspace_bytes(op, luna.LUNA_BF16, B, H, n, d, ctypes.byref(p200), 64)
+        floor = rows * (2 * 200 + 2 * 129) * 4 + B * H * (n // chunk) * chunk_bytes
         assert floor <= nb <= floor + (1 << 20), (op, nb, floor)
+    # one channel per projection with 256 features at d = 128, causal: the features of
+    # Q and K in bf16, then the scan kernel (its state pieces are a few MB)
+    p1 = _params(M=256, L=1)
+    nb = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, B, H, n, d, ctypes.byref(p1), 64)
+    assert rows * 256 * 2 * 2 <= nb <= rows * 256 * 2 * 2 + (64 << 20), nb
     # fused shapes keep their small workspaces
     assert lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, B, H, n, d, ctypes.byref(_params(M=32)),
                                     64) < 1 << 30
@@ -157,11 +162,13 @@ def test_generic_path_planning(lib):
                                     64) < 1 << 20
     assert lib.luna_workspace_bytes(luna.OP_STATE, luna.LUNA_BF16, 2, 3, 1000, 128, ctypes.byref(p1), 64) > 0
     # chunk counts above 65535 are refused before anything runs
-    big = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 1, 1, 65535 * 64 + 1, d, ctypes.byref(p1), 64)
+    big = lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 1, 1, 65535 * 64 + 1, d, ctypes.byref(p200),
+                                   64)
     assert big == 0
-    assert lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 1, 1, 65535 * 64, d, ctypes.byref(p1),
+    assert lib.luna_workspace_bytes(luna.OP_ATTN_CAUSAL, luna.LUNA_BF16, 1, 1, 65535 * 64, d, ctypes.byref(p200),
                                     64) > 0
-    assert lib.luna_workspace_bytes(luna.OP_ATTN, luna.LUNA_BF16, 1, 1, 65535 * 512 + 1, d, ctypes.byref(p1), 64) == 0
+    assert lib.luna_workspace_bytes(luna.OP_ATTN, luna.LUNA_BF16, 1, 1, 65535 * 512 + 1, d, ctypes.byref(p200),
+                                    64) == 0
     p257 = _params(M=257, L=1)
     assert lib.luna_workspace_bytes(luna.OP_ATTN, luna.LUNA_BF16, 1, 1, 64, d, ctypes.byref(p257), 64) == 0
     assert _attn(lib, p=p257) == luna.LUNA_ERR_INVALID_ARG

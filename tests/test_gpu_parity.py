@@ -283,8 +283,10 @@ def test_attn_noncausal_workload_full_size(name):
 CS_CASES = [
     ("f32", 32, 8, 8), ("f32", 64, 16, 8), ("bf16", 32, 16, 8), ("bf16", 64, 16, 8), ("bf16", 64, 32, 8),
     ("bf16", 128, 16, 8), ("bf16", 128, 32, 8),
-    # shapes on the fp32 GEMM path: one channel per projection (M = D = 256, 128), fp32 at d = 128
-    ("bf16", 128, 256, 1), ("bf16", 64, 128, 1), ("f32", 128, 16, 8), ("f32", 32, 24, 2),
+    # one channel per projection (M = D = 256, 128: features mapped beforehand, then the
+    # scan kernel); the fp32 GEMM path: fp32 at d = 128, L = 2 with M > 16, L = 4, 128 features at d = 128
+    ("bf16", 128, 256, 1), ("bf16", 64, 128, 1), ("f32", 128, 16, 8), ("f32", 32, 24, 2), ("bf16", 64, 16, 4),
+    ("bf16", 128, 128, 1),
 ]
 
 
@@ -299,14 +301,16 @@ def test_attn_causal_small(dtype, d, M, L, n):
     assert_close_rows(out, oracle.attn_causal(Q, K, V, p, eps=w.eps), dtype, "out")
 
 
+@pytest.mark.parametrize("M,L", [(32, 8), (256, 1)])
 @pytest.mark.parametrize("B,H,n", [(1, 3, 1000), (4, 25, 650), (8, 20, 300)])
-def test_attn_causal_state_pieces(B, H, n):
+def test_attn_causal_state_pieces(B, H, n, M, L):
     """With fewer than 256 heads each head is cut at x (n/2 rounded down to whole
     chunks) and the state of [0, x) is summed in pieces, one workgroup per head and
     piece: seven one-chunk pieces, uneven pieces (2, 2, 1 chunks), two pieces.
-    Checked against the oracle on sampled heads (the parameters are shared)."""
-    w = small_workload("bf16", B=B, H=H, n=n, d=128, M=32, L=8, causal=True)
-    say(f"causal state pieces B={B} H={H} n={n}")
+    Checked against the oracle on sampled heads (the parameters are shared).  M = 256,
+    L = 1: the features are mapped beforehand and the kernel reads them."""
+    w = small_workload("bf16", B=B, H=H, n=n, d=128, M=M, L=L, causal=True)
+    say(f"causal state pieces B={B} H={H} n={n} M={M} L={L}")
     Q, K, V, p = inputs(w, seed=51)
     (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
     out = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))

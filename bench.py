@@ -42,11 +42,13 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix cores
 KERNEL_SOURCES = {
     "causal_kernel": ["luna_causal.hip", "luna_device.hpp", "luna_kernels.hpp"],
     "nc_fused_kernel": ["luna_noncausal.hip", "luna_device.hpp", "luna_kernels.hpp"],
+    "featuremap_kernel": ["luna_featuremap.hip", "luna_device.hpp", "luna_kernels.hpp"],
 }
-KERNEL_WORKLOAD = {"causal_kernel": "long_causal", "nc_fused_kernel": "long_noncausal"}
+KERNEL_WORKLOAD = {"causal_kernel": "long_causal", "nc_fused_kernel": "long_noncausal",
+                   "featuremap_kernel": "featuremap_long_noncausal"}
 # launches of the kernel per ABI call on these workloads: the causal call (128 heads)
 # runs a state launch and then the scan launch
-LAUNCHES_PER_CALL = {"causal_kernel": 2, "nc_fused_kernel": 1}
+LAUNCHES_PER_CALL = {"causal_kernel": 2, "nc_fused_kernel": 1, "featuremap_kernel": 1}
 COPY_BYTES = 1 << 30  # the --copy-calibration copy
 
 
@@ -71,6 +73,22 @@ def measured_traffic(kernel: str, workload: str):
     if rec.get("source_hash") != source_hash(kernel):
         return None
     return rec.get("bytes_per_call")
+
+
+def measured_figure(tag: str, workload: str, kernel: str, figure: str):
+    """A figure of the committed rocprofv3 counter summary of `tag` on `workload`, if
+    the summary was taken on the kernel's current sources."""
+    import re
+
+    path = os.path.join(ROOT, "profiles", f"counters_{tag}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"Source hash of its files[^`]*`([0-9a-f]+)`", text)
+    if not m or m.group(1) != source_hash(kernel):
+        return None
+    m = re.search(r"^\| " + re.escape(figure) + r"[^|]*\| ([0-9.e+-]+) \|", text, re.M)
+    return float(m.group(1)) if m else None
 
 
 def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
@@ -99,6 +117,9 @@ def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
         copies = [v for d, v in vals.items() if "copyBuffer" in names[d] and v > 0.25 * COPY_BYTES]
         if not copies:
             log(f"{path}: no 1 GiB copy dispatch found (run bench.py with --copy-calibration)")
+            return 1
+        if not any(f"{len(k)}{k}" in nm for k in KERNEL_SOURCES for nm in names.values()):
+            log(f"{path}: none of the measured kernels")
             return 1
         factor = COPY_BYTES / (sum(copies) / len(copies))
         for kern in KERNEL_SOURCES:
@@ -131,6 +152,19 @@ def traffic_from(fetch_csv: str, write_csv: str, command: str) -> int:
             fh.write("\n")
         log(f"wrote {path}: read {rd / 2**20:.1f} MiB, write {wr / 2**20:.1f} MiB per call")
     return 0
+
+
+def copy_calibration(dev) -> None:
+    """Three 1 GiB device-to-device copies: the known traffic that rocprofv3's
+    FETCH_SIZE / WRITE_SIZE readings are scaled by."""
+    import torch
+
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def flops_per_token_head(w, causal: bool) -> int:
@@ -241,6 +275,8 @@ def featuremap_bench(args) -> int:
     ws = torch.empty(nb + 256, dtype=torch.uint8, device=dev)
     wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
     stream = torch.cuda.current_stream(dev)
+    if args.copy_calibration:
+        copy_calibration(dev)
 
     def call():
         st = lib.luna_featuremap(x.data_ptr(), luna.LUNA_BF16, w.B, w.H, w.n, w.d, ctypes.byref(pc), out.data_ptr(),
@@ -346,7 +382,10 @@ COUNTER_RATIOS = [
     ("share of wave lifetime waiting on LDS", "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES", 1.0),
     ("LDS bank-conflict cycles per LDS-active cycle", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", 1.0),
 ]
-# (figure, counter, units): counter / (GRBM_GUI_ACTIVE (GPU cycles of the dispatch) x units)
+# (figure, counter, units): counter / (cycles of the dispatch x units), the dispatch's
+# cycles being GRBM_GUI_ACTIVE / 8: rocprofv3 sums that counter over the 8 XCDs (it
+# reads 8x the kernel's duration in GPU clocks)
+XCDS = 8
 COUNTER_UTIL = [
     ("MFMA busy, share of all SIMD cycles (1024 SIMDs)", "SQ_VALU_MFMA_BUSY_CYCLES", 1024),
     ("LDS active, share of all CU cycles (256 CUs)", "SQ_LDS_IDX_ACTIVE", 256),
@@ -354,8 +393,10 @@ COUNTER_UTIL = [
 ]
 COUNTER_KERNELS = {  # kernel-name pattern (mangled or not) -> (file tag, workload, kernel whose sources are hashed)
     r"nc_fused_kernel(<|I)": ("nc_fused_kernel", "long_noncausal", "nc_fused_kernel"),
-    r"(13causal_kernelI.*Lb1E|\bcausal_kernel<.*true>)": ("causal_kernel_state_launch", "long_causal", "causal_kernel"),
-    r"(13causal_kernelI.*Lb0E|\bcausal_kernel<.*false>)": ("causal_kernel_scan_launch", "long_causal", "causal_kernel"),
+    r"(13causal_kernelI.*Lb1ELb0EE|\bcausal_kernel<.*true, false>)": ("causal_kernel_state_launch", "long_causal",
+                                                                         "causal_kernel"),
+    r"(13causal_kernelI.*Lb0ELb0EE|\bcausal_kernel<.*false, false>)": ("causal_kernel_scan_launch", "long_causal",
+                                                                          "causal_kernel"),
     r"pwl_prepare_kernel": ("pwl_prepare_kernel", "bench_step", None),
     r"featuremap_kernel(<|I)": ("featuremap_kernel", "featuremap_long_noncausal", None),
 }
@@ -389,9 +430,13 @@ def counters_from(csvs, command: str) -> int:
         for label, a, b, mul in COUNTER_RATIOS:
             if a in vals and b in vals and vals[b] > 0:
                 rows.append((label, mul * vals[a] / vals[b], (f"{mul:g} x " if mul != 1 else "") + f"{a} / {b}"))
+        if vals.get("GRBM_GUI_ACTIVE", 0) > 0:
+            rows.append(("dispatch duration, GPU cycles", vals["GRBM_GUI_ACTIVE"] / XCDS,
+                         f"GRBM_GUI_ACTIVE / {XCDS} (summed over the XCDs)"))
         for label, a, units in COUNTER_UTIL:
             if a in vals and vals.get("GRBM_GUI_ACTIVE", 0) > 0:
-                rows.append((label, vals[a] / (vals["GRBM_GUI_ACTIVE"] * units), f"{a} / (GRBM_GUI_ACTIVE x {units})"))
+                rows.append((label, vals[a] * XCDS / (vals["GRBM_GUI_ACTIVE"] * units),
+                             f"{a} / (GRBM_GUI_ACTIVE / {XCDS} x {units})"))
         path = os.path.join(ROOT, "profiles", f"counters_{tag}_{wl_name}.md")
         lines = [f"# rocprofv3 counters: {tag} ({wl_name})", "", f"Kernel: `{kern[0]}`", ""]
         if src:
@@ -717,12 +762,7 @@ def main() -> int:
     torch.cuda.synchronize()
 
     if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration(dev)
 
     for _ in range(args.warmup):
         nc.run()
@@ -784,6 +824,10 @@ def main() -> int:
         "unit": "GB/s" if P["bound"] == "hbm" else "TFLOP/s",
         "frac": round(P["roofline_frac"], 4),
         "traffic": measured_traffic(kname, dom) if kname in KERNEL_SOURCES else None,
+        # matrix-core busy share of the kernel's (scan launch's) SIMD cycles, from the
+        # committed counter summary (null once the kernel has changed since)
+        "mfma_busy": measured_figure("causal_kernel_scan_launch" if kname == "causal_kernel" else kname, dom,
+                                     kname, "MFMA busy") if kname in KERNEL_SOURCES else None,
         "kernel": kname,
         "workload": dom,
         "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel; the "

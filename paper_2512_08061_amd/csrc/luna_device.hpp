@@ -244,35 +244,14 @@ __device__ __forceinline__ float relu_floor(float v, float floor) {
   return __builtin_elementwise_maximum(v, floor);
 }
 
-// Segment index of each of NU values: the number of breakpoints strictly below u.
-// The bucket of u gives the start of its key window; `steps` halvings of the
-// window follow (a wave-uniform count, taken from the table).  The NU searches
-// advance together, so each step issues NU independent LDS reads and the lookup
-// latency is paid once per step rather than once per value.  NaN compares false
-// everywhere and ends at the start of its window.
-template <int NU, typename Tab>
-__device__ __forceinline__ void pwl_search(const Tab& t, int steps, const float (&u)[NU], int (&seg)[NU]) {
-  const char* keys = reinterpret_cast<const char*>(t.keys);
-  unsigned off[NU];
-#pragma unroll
-  for (int i = 0; i < NU; ++i) {
-    const uint32_t bits = __float_as_uint(u[i]);
-    const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
-    int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
-    mm = min(max(mm, 0), kBucketMag - 1);
-    const int idx = kBucketMag + (mm ^ ((int)bits >> 31));
-    off[i] = t.buckets[idx];
-  }
-  for (int s = steps - 1; s >= 0; --s) {
-    const unsigned h4 = 4u << s;
-#pragma unroll
-    for (int i = 0; i < NU; ++i) {
-      const float key = *reinterpret_cast<const float*>(keys + off[i] + h4 - 4u);
-      off[i] += key < u[i] ? h4 : 0u;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < NU; ++i) seg[i] = (int)(off[i] >> 2);
+// Bucket of u: its float bits' sign, then exponent and top mantissa bits over
+// [2^-kBucketExp, 2^kBucketExp), clamped into the underflow and overflow buckets.
+__device__ __forceinline__ int pwl_bucket(float u) {
+  const uint32_t bits = __float_as_uint(u);
+  const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
+  int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
+  mm = min(max(mm, 0), kBucketMag - 1);
+  return kBucketMag + (mm ^ ((int)bits >> 31));
 }
 
 // The same search, ending in the byte offset 4 seg of the segment's key instead of
@@ -295,14 +274,7 @@ __device__ __forceinline__ void pwl_halvings(const Tab& t, const float (&u)[NU],
 template <int NU, typename Tab>
 __device__ __forceinline__ void pwl_search_off(const Tab& t, int steps, const float (&u)[NU], unsigned (&off)[NU]) {
 #pragma unroll
-  for (int i = 0; i < NU; ++i) {
-    const uint32_t bits = __float_as_uint(u[i]);
-    const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
-    int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
-    mm = min(max(mm, 0), kBucketMag - 1);
-    const int idx = kBucketMag + (mm ^ ((int)bits >> 31));
-    off[i] = t.buckets[idx];
-  }
+  for (int i = 0; i < NU; ++i) off[i] = t.buckets[pwl_bucket(u[i])];
   switch (steps) {
     case 0: break;
     case 1: pwl_halvings<1>(t, u, off); break;
@@ -321,6 +293,32 @@ __device__ __forceinline__ void pwl_search_off(const Tab& t, int steps, const fl
       }
     }
   }
+}
+
+// Segment index of each of NU values: the number of breakpoints strictly below u.
+// The bucket of u gives the start of its key window; `steps` halvings of the
+// window follow (a wave-uniform count, taken from the table).  The NU searches
+// advance together, so each step issues NU independent LDS reads and the lookup
+// latency is paid once per step rather than once per value.  NaN compares false
+// everywhere and ends at the start of its window.
+template <int NU, typename Tab>
+__device__ __forceinline__ void pwl_search(const Tab& t, int steps, const float (&u)[NU], int (&seg)[NU]) {
+  // (one loop over the steps: unrolled halvings, as in pwl_search_off, measured 1-3%
+  // slower in the non-causal kernel, whose code they make a fifth longer)
+  const char* keys = reinterpret_cast<const char*>(t.keys);
+  unsigned off[NU];
+#pragma unroll
+  for (int i = 0; i < NU; ++i) off[i] = t.buckets[pwl_bucket(u[i])];
+  for (int s = steps - 1; s >= 0; --s) {
+    const unsigned h4 = 4u << s;
+#pragma unroll
+    for (int i = 0; i < NU; ++i) {
+      const float key = *reinterpret_cast<const float*>(keys + off[i] + h4 - 4u);
+      off[i] += key < u[i] ? h4 : 0u;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NU; ++i) seg[i] = (int)(off[i] >> 2);
 }
 
 // psi_l(u), l = 0..L-1, on the segment whose key sits at byte offset `off` (4 seg):
@@ -519,14 +517,7 @@ __device__ __forceinline__ void pwl_search_n(const PwlLdsN<RowT, L, NSEG>& t, in
   const char* nb = reinterpret_cast<const char*>(t.nodes);
   unsigned s16[NU];  // byte offset of the window's first node: 16 x its first key
 #pragma unroll
-  for (int i = 0; i < NU; ++i) {
-    const uint32_t bits = __float_as_uint(u[i]);
-    const int mag = (int)((bits >> (23 - kBucketMant)) & ((1u << (31 - 23 + kBucketMant)) - 1u));
-    int mm = mag - ((127 - kBucketExp) << kBucketMant) + 1;
-    mm = min(max(mm, 0), kBucketMag - 1);
-    const int idx = kBucketMag + (mm ^ ((int)bits >> 31));
-    s16[i] = 4u * t.buckets[idx];
-  }
+  for (int i = 0; i < NU; ++i) s16[i] = 4u * t.buckets[pwl_bucket(u[i])];
   if (nodes == 1) {
 #pragma unroll
     for (int i = 0; i < NU; ++i)

@@ -11,7 +11,11 @@
 
 namespace luna {
 
-template <typename Tin, typename Tout, int DH, int L>
+// HOLD: at most four 16-projection blocks, whose W fragments and biases stay in
+// registers for every item of the parameter set; maps with more blocks reload them
+// per group (held across items they would cost the registers that keep those maps'
+// occupancy).
+template <typename Tin, typename Tout, int DH, int L, bool HOLD>
 __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   constexpr int KS = DH / 32;
   __shared__ PwlLds<L, nseg_cap(L, kFmSegBytes)> tab;
@@ -22,8 +26,24 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   // blockIdx.x + gridDim.x, ..., so that its table copy serves many tiles.
   const int64_t per_input = a.heads * tiles_per_head;
   const int64_t items = per_input * (a.X2 != nullptr ? 2 : 1);
-  int loaded = -1;
-  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+  const int wave = wave_id(), lane = threadIdx.x % kWave;
+  const int g = lane / 16, r = lane % 16;
+  const int64_t n = a.rows_per_head;
+  const int M = a.phi.M;
+  const int D = M * L;
+  // projections go in groups of four 16-projection blocks (W fragments of one group
+  // in registers; with at most four blocks they stay there for every item of the
+  // parameter set)
+  constexpr int kMaxMB = 4;
+  const int MB = (M + 15) / 16;
+  // item -> its input, output, parameter set and this lane's row (B column)
+  struct Item {
+    const Tin* X;
+    Tout* out;
+    int hset;
+    bool row_ok;
+  };
+  auto locate = [&](int64_t item) {
     int64_t bid = item;
     const void* Xsrc = a.X;
     void* Odst = a.out;
@@ -34,112 +54,144 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
     }
     const int64_t head = bid / tiles_per_head;
     const int tile = (int)(bid - head * tiles_per_head);
-    const int hset = a.phi.per_head ? (int)(head % a.H) : 0;
-
-    const int wave = wave_id(), lane = threadIdx.x % kWave;
-    const int g = lane / 16, r = lane % 16;
-    const int64_t n = a.rows_per_head;
-    const int64_t t = (int64_t)tile * 64 + wave * 16 + r;  // this lane's row (B column)
-    const bool row_ok = t < n;
-    const int M = a.phi.M;
-    const int D = M * L;
-    const Tin* X = reinterpret_cast<const Tin*>(Xsrc) + (head * n + (row_ok ? t : 0)) * DH;
-    const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
-    const float* bias = a.phi.b + (size_t)hset * M;
-    Tout* out = reinterpret_cast<Tout*>(Odst) + (head * n + (row_ok ? t : 0)) * (int64_t)D;
-
-    // the row, W fragments and biases are fetched before the table, so that their
-    // loads overlap its copy; projections go in groups of four 16-projection blocks
-    // (W fragments of one group in registers)
-    constexpr int kMaxMB = 4;
-    const int MB = (M + 15) / 16;
-    Frag<Tin> xf[KS];
+    const int64_t t = (int64_t)tile * 64 + wave * 16 + r;
+    Item it;
+    it.row_ok = t < n;
+    it.hset = a.phi.per_head ? (int)(head % a.H) : 0;
+    it.X = reinterpret_cast<const Tin*>(Xsrc) + (head * n + (it.row_ok ? t : 0)) * DH;
+    it.out = reinterpret_cast<Tout*>(Odst) + (head * n + (it.row_ok ? t : 0)) * (int64_t)D;
+    return it;
+  };
+  auto load_row = [&](Frag<Tin> (&xf)[KS], const Item& it) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      if (row_ok) load8(xf[ks], X + 32 * ks + 8 * g);
+      if (it.row_ok) load8(xf[ks], it.X + 32 * ks + 8 * g);
       else xf[ks].zero();
     }
-    for (int mg = 0; mg < MB; mg += kMaxMB) {
-      Frag<Tin> wfr[kMaxMB][KS];
-      float bz[kMaxMB][4];
+  };
+  int loaded = -1;
+  {
+    int wset = -1;
+    Frag<Tin> wfr[kMaxMB][KS];
+    float bz[kMaxMB][4];
+    for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+      const Item cur = locate(item);
+      const int hset = cur.hset;
+      const bool row_ok = cur.row_ok;
+      Tout* out = cur.out;
+      const Tin* W = reinterpret_cast<const Tin*>(a.phi.W) + (size_t)hset * M * DH;
+      const float* bias = a.phi.b + (size_t)hset * M;
+      // the row, W fragments and biases are fetched before the table, so that their
+      // loads overlap its copy
+      Frag<Tin> xf[KS];
+      load_row(xf, cur);
+      for (int mg = 0; mg < MB; mg += kMaxMB) {
+        if (!HOLD || hset != wset) {  // (uniform)
 #pragma unroll
-      for (int mbl = 0; mbl < kMaxMB; ++mbl) {
-        const int mb = mg + mbl;
-        const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
+          for (int mbl = 0; mbl < kMaxMB; ++mbl) {
+            const int mb = mg + mbl;
+            const int prow = 16 * mb + r;  // W row this lane feeds to the A operand
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          if (mb < MB && prow < M) load8(wfr[mbl][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
-          else wfr[mbl][ks].zero();
-        }
+            for (int ks = 0; ks < KS; ++ks) {
+              if (mb < MB && prow < M) load8(wfr[mbl][ks], W + (size_t)prow * DH + 32 * ks + 8 * g);
+              else wfr[mbl][ks].zero();
+            }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
-          bz[mbl][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
-        }
-      }
-      if (mg == 0 && hset != loaded) {  // (uniform) a workgroup loads a table once per parameter set it meets
-        __syncthreads();                // every wave is done with the previous table
-        pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
-        __syncthreads();
-        loaded = hset;
-      }
-      const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
-      const float floor = tab.floor;
-
-      // the group's projections, then one search over all of them, so that the
-      // searches' dependent LDS reads overlap
-      float uu[4 * kMaxMB];
-#pragma unroll
-      for (int mbl = 0; mbl < kMaxMB; ++mbl) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mbl][ks], xf[ks]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) uu[4 * mbl + j] = acc[j] + bz[mbl][j];
-      }
-      int sg[4 * kMaxMB];
-      pwl_search(tab, steps, uu, sg);
-#pragma unroll
-      for (int mbl = 0; mbl < kMaxMB; ++mbl) {
-        const int mb = mg + mbl;
-        if (mb >= MB || !row_ok) break;
-        const int i0 = 16 * mb + 4 * g;  // projections i0 .. i0 + 3 of this lane
-        float y[4][L];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) pwl_channels<L>(tab, sg[4 * mbl + j], floor, uu[4 * mbl + j], y[j]);
-        Tout* o = out + i0 * L;
-        if (i0 + 3 < M) {  // the four projections' 4 L features are contiguous
-#pragma unroll
-          for (int q = 0; q < L; ++q) {
-            const float* f = &y[0][0] + 4 * q;  // features 4 q .. 4 q + 3 of the four
-            store4(o + 4 * q, f[0], f[1], f[2], f[3]);
+            for (int j = 0; j < 4; ++j) {
+              const int i = 16 * mb + 4 * g + j;  // projection held in acc[j]
+              bz[mbl][j] = (mb < MB && i < M) ? bias[i] : 0.0f;
+            }
           }
-        } else {
+          wset = hset;
+        }
+        if (mg == 0 && hset != loaded) {  // (uniform) a workgroup loads a table once per parameter set it meets
+          __syncthreads();                // every wave is done with the previous table
+          pwl_load(tab, a.phi.tables + (size_t)hset * kTableBytes);
+          __syncthreads();
+          loaded = hset;
+        }
+        const int steps = __builtin_amdgcn_readfirstlane(tab.steps);
+        const float floor = tab.floor;
+
+        // the group's projections, then one search over all of them, so that the
+        // searches' dependent LDS reads overlap
+        float uu[4 * kMaxMB];
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (i0 + j < M)
+        for (int mbl = 0; mbl < kMaxMB; ++mbl) {
+          f32x4 acc = zero4();
 #pragma unroll
-              for (int l = 0; l < L; ++l) o[j * L + l] = (Tout)y[j][l];
+          for (int ks = 0; ks < KS; ++ks) mma(acc, wfr[mbl][ks], xf[ks]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) uu[4 * mbl + j] = acc[j] + bz[mbl][j];
+        }
+        int sg[4 * kMaxMB];
+        pwl_search(tab, steps, uu, sg);
+#pragma unroll
+        for (int mbl = 0; mbl < kMaxMB; ++mbl) {
+          const int mb = mg + mbl;
+          if (mb >= MB || !row_ok) break;
+          const int i0 = 16 * mb + 4 * g;  // projections i0 .. i0 + 3 of this lane
+          float y[4][L];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pwl_channels<L>(tab, sg[4 * mbl + j], floor, uu[4 * mbl + j], y[j]);
+          Tout* o = out + i0 * L;
+          if (i0 + 3 < M) {  // the four projections' 4 L features are contiguous
+#pragma unroll
+            for (int q = 0; q < L; ++q) {
+              const float* f = &y[0][0] + 4 * q;  // features 4 q .. 4 q + 3 of the four
+              store4(o + 4 * q, f[0], f[1], f[2], f[3]);
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (i0 + j < M)
+#pragma unroll
+                for (int l = 0; l < L; ++l) o[j * L + l] = (Tout)y[j][l];
+          }
         }
       }
     }
   }
 }
 
+// Workgroups of `kernel` that the device holds at once (computed once per kernel).
+template <typename Kern>
+static int fm_resident(Kern kernel) {
+  static const int resident = [&]() {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess || per_cu < 1) per_cu = 1;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
+    return per_cu * cus;
+  }();
+  return resident;
+}
+
+template <typename Kern>
+static void fm_launch(Kern kernel, int64_t items, const FeatureMapArgs& a, hipStream_t s) {
+  const int64_t res = fm_resident(kernel);
+  hipLaunchKernelGGL(kernel, dim3((unsigned)(items < res ? items : res)), dim3(256), 0, s, a);
+}
+
 template <typename Tin, typename Tout, int DH>
 static hipError_t fm_dispatch_L(int L, const FeatureMapArgs& a, hipStream_t s) {
   const int64_t tiles = (a.rows_per_head + 63) / 64;
   const int64_t items = a.heads * tiles * (a.X2 != nullptr ? 2 : 1);
-  // three workgroups per CU fit next to their LDS tables; more items loop
-  const dim3 grid((unsigned)(items < 768 ? items : 768)), block(256);
+  const bool hold = a.phi.M <= 64;  // at most four 16-projection blocks
+  // as many workgroups as can be resident at once (registers and LDS table permitting);
+  // more items loop, so that no second round of workgroups starts late
+#define LUNA_FM_LAUNCH(L_)                                                                  \
+  if (hold) fm_launch(featuremap_kernel<Tin, Tout, DH, L_, true>, items, a, s);             \
+  else fm_launch(featuremap_kernel<Tin, Tout, DH, L_, false>, items, a, s);
   switch (L) {
-    case 1: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 4>), grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 8>), grid, block, 0, s, a); break;
-    case 16: hipLaunchKernelGGL((featuremap_kernel<Tin, Tout, DH, 16>), grid, block, 0, s, a); break;
+    case 1: LUNA_FM_LAUNCH(1) break;
+    case 2: LUNA_FM_LAUNCH(2) break;
+    case 4: LUNA_FM_LAUNCH(4) break;
+    case 8: LUNA_FM_LAUNCH(8) break;
+    case 16: LUNA_FM_LAUNCH(16) break;
     default: return hipErrorInvalidValue;
   }
+#undef LUNA_FM_LAUNCH
   return hipGetLastError();
 }
 

@@ -625,11 +625,14 @@ def configs_bench(args) -> int:
         tf = flops_per_token_head(w, w.causal) * th / 1e12
         mfma_peak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
         t_hbm, t_mfma = gb / HBM_PEAK_GBS, tf / mfma_peak
-        # the path, from the workspace: the fp32 GEMM path holds fp32 features of the
-        # queries and keys (8 M L bytes per token and head), the causal kernel with the
-        # features given bf16 ones (4 M L), the fused kernels neither
-        fb = plan.ws_bytes / (w.M * w.L * th)
-        path = "fp32 GEMM" if fb >= 8 else "features mapped, then scan" if fb >= 4 else "fused"
+        # the path, from the workspace beyond the tables (a feature-map call's workspace):
+        # the fp32 GEMM path holds fp32 features of the queries and keys (8 M L bytes per
+        # token and head), the causal kernel with the features given bf16 ones (4 M L),
+        # the attention kernels at most small partial statistics
+        ws_tables = luna.workspace_bytes(luna.OP_FEATUREMAP, luna.LUNA_BF16 if w.dtype == "bf16" else luna.LUNA_F32,
+                                         w.B, w.H, w.n, w.d, pt)
+        fb = (plan.ws_bytes - ws_tables) / (w.M * w.L * th)
+        path = "fp32 GEMM" if fb >= 8 else "features mapped, then scan" if fb >= 4 else "attention kernels"
         rec.update({
             "status": "ok",
             "path": path,
@@ -658,8 +661,10 @@ def configs_bench(args) -> int:
                      "TFLOP/s counts the matrix-core work (projections, S, readout, z, denominators, and for "
                      "causal the full 64x64 intra-chunk blocks); the floor is the larger of the HBM time of the "
                      "algorithmic bytes (read Q, K, V, write out) at 8 TB/s and the MFMA time at the dtype's "
-                     "dense peak. path: fused attention kernels, or the fp32 GEMM path of the shapes that have "
-                     "none (features in the workspace, all arithmetic fp32).\n\n")
+                     "dense peak. path: the attention kernels (fused, or the split state / reduce / readout kernels "
+                     "below 192 heads), the features mapped first and then the causal scan kernel, or the fp32 "
+                     "GEMM path of the shapes that have neither (features in the workspace, all arithmetic "
+                     "fp32).\n\n")
             fh.write("| config | B,H,n,d | M x L | dtype | causal | path | median us (p10-p90) | tokens/s "
                      "| head-tokens/s | TFLOP/s | GB/s | floor us | roofline |\n"
                      "|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")

@@ -3,3 +3,4 @@ the tests, the smoke check and the benchmark's CPU-baseline leg, never by the
 GPU library."""
 from .luna_oracle import *  # noqa: F401,F403
 from . import luna_oracle  # noqa: F401
+from . import luna_variants  # noqa: F401

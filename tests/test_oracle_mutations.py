@@ -307,3 +307,151 @@ def test_mutation_is_caught(name, monkeypatch):
         except Exception:
             failed.append(pin.__name__)
     assert failed, f"no pin catches the planted mistake {name}"
+
+
+# ---------------------------------------------------------------------------
+# feature-map variants: mistakes planted in oracle/luna_variants.py
+# ---------------------------------------------------------------------------
+
+import oracle_variant_pins  # noqa: E402
+from oracle import luna_variants as VAR  # noqa: E402
+
+_vorig = {k: getattr(VAR, k) for k in ("rff_cos", "rff_sincos", "performer", "_act", "ch_rms", "mlp_variant",
+                                        "attn_from_features", "_mlp_channels")}
+
+
+def _rff_cos_mut(kind):
+    def rff_cos(X, p):
+        if p.get("per_head", False):
+            return VAR._per_head(rff_cos, np.asarray(X, float), p)
+        u = np.asarray(X, float) @ np.asarray(p["W"], float).T + (0.0 if kind == "no_phase" else np.asarray(p["b"]))
+        scale = 1.0 / math.sqrt(u.shape[-1]) if kind == "no_sqrt2" else math.sqrt(2.0 / u.shape[-1])
+        return scale * (np.sin(u) if kind == "sin" else np.cos(u))
+    return rff_cos
+
+
+def _sincos_mut(kind):
+    def rff_sincos(X, p):
+        if p.get("per_head", False):
+            return VAR._per_head(rff_sincos, np.asarray(X, float), p)
+        u = np.asarray(X, float) @ np.asarray(p["W"], float).T + np.asarray(p["b"])
+        M = u.shape[-1]
+        pair = [np.cos(u), np.sin(u)] if kind == "cos_first" else [np.sin(u), np.cos(u)]
+        y = np.stack(pair, axis=-2 if kind == "channel_major" else -1)
+        return y.reshape(u.shape[:-1] + (2 * M,)) / math.sqrt(M)
+    return rff_sincos
+
+
+def _performer_mut(kind):
+    def performer(X, p):
+        X = np.asarray(X, float)
+        if p.get("per_head", False):
+            return VAR._per_head(performer, X, p)
+        d = X.shape[-1]
+        u = X @ np.asarray(p["W"], float).T + np.asarray(p["b"])
+        sq = (X * X).sum(axis=-1, keepdims=True)
+        denom = 2.0 * d if kind == "d_not_sqrt_d" else 2.0 * math.sqrt(d)
+        if kind == "plus_norm":
+            return np.exp(u + sq / denom) / math.sqrt(u.shape[-1])
+        return np.exp(u - sq / denom) / math.sqrt(u.shape[-1])
+    return performer
+
+
+def _act_mut(kind):
+    def act(name, z):
+        if name == "gelu" and kind == "gelu_as_silu":
+            return z / (1.0 + np.exp(-z))
+        if name == "silu" and kind == "silu_no_z":
+            return 1.0 / (1.0 + np.exp(-z))
+        return _vorig["_act"](name, z)
+    return act
+
+
+def _chrms_mut(kind):
+    def ch_rms(y, target, eps=1e-6):
+        y = np.asarray(y, float)
+        L = y.shape[-1]
+        if kind == "per_token":
+            rms = np.sqrt((y ** 2).mean(axis=-2, keepdims=True) + eps)
+        else:
+            rms = np.sqrt((y.reshape(-1, L) ** 2).mean(axis=0) + eps)
+        s = target / (rms + eps) if kind == "no_clamp" else np.minimum(target / (rms + eps), 1.0)
+        return y * s
+    return ch_rms
+
+
+def _mlp_channels_mut(kind):
+    def _mlp_channels(X, p):
+        u = X @ np.asarray(p["W"], float).T + np.asarray(p["b"])
+        y = VAR.psi_act(u, p["fc1_w"], p["fc1_b"], p["fc2_w"], p["fc2_b"], p["nonneg"], p.get("act", "relu"))
+        if p.get("env_w") is not None:
+            z = X @ np.asarray(p["env_w"], float).T + np.asarray(p["env_b"])
+            env = 1.0 / (1.0 + np.exp(z if kind == "env_sign" else -z))
+            if kind == "env_on_projection":  # the first L projections gated instead of the channels
+                y = y * env[..., :, None][..., : y.shape[-2], :] if env.shape[-1] >= y.shape[-2] else y * env[..., None, :] ** 2
+            else:
+                y = y * env[..., None, :]
+        return y
+    return _mlp_channels
+
+
+def _bank_mut(kind):
+    def mlp_variant(X, p):
+        if p.get("bank") is None:
+            return _vorig["mlp_variant"](X, p)
+        X = np.asarray(X, float)
+        y = VAR._per_head(VAR._mlp_channels, X, p)
+        M, L = y.shape[-2], y.shape[-1]
+        w = np.asarray(p["bank"], float)
+        if kind == "reversed":
+            w = w[::-1]
+        out = y @ w
+        return out / (M if kind == "scale_by_M" else math.sqrt(M))
+    return mlp_variant
+
+
+def _from_features_mut(kind):
+    def attn_from_features(phiQ, phiK, V, eps=1e-6, causal=False):
+        if kind == "causal_exclusive" and causal:
+            phiQ, phiK, V = (np.asarray(a, float) for a in (phiQ, phiK, V))
+            n = phiQ.shape[-2]
+            A = np.tril(phiQ @ np.swapaxes(phiK, -1, -2), -1)
+            return (A @ V) / (A.sum(-1) + eps)[..., None]
+        if kind == "no_normaliser" and not causal:
+            phiQ, phiK, V = (np.asarray(a, float) for a in (phiQ, phiK, V))
+            return phiQ @ (np.swapaxes(phiK, -1, -2) @ V)
+        return _vorig["attn_from_features"](phiQ, phiK, V, eps, causal)
+    return attn_from_features
+
+
+VARIANT_MUTATIONS = {
+    "rff_cos_as_sin": ("rff_cos", _rff_cos_mut("sin")),
+    "rff_cos_no_sqrt2": ("rff_cos", _rff_cos_mut("no_sqrt2")),
+    "rff_cos_no_phase": ("rff_cos", _rff_cos_mut("no_phase")),
+    "sincos_cos_first": ("rff_sincos", _sincos_mut("cos_first")),
+    "sincos_channel_major": ("rff_sincos", _sincos_mut("channel_major")),
+    "performer_norm_over_d": ("performer", _performer_mut("d_not_sqrt_d")),
+    "performer_norm_sign": ("performer", _performer_mut("plus_norm")),
+    "gelu_as_silu": ("_act", _act_mut("gelu_as_silu")),
+    "silu_without_z": ("_act", _act_mut("silu_no_z")),
+    "ch_rms_per_token": ("ch_rms", _chrms_mut("per_token")),
+    "ch_rms_no_clamp": ("ch_rms", _chrms_mut("no_clamp")),
+    "envelope_sign": ("_mlp_channels", _mlp_channels_mut("env_sign")),
+    "bank_reversed": ("mlp_variant", _bank_mut("reversed")),
+    "bank_scale_by_M": ("mlp_variant", _bank_mut("scale_by_M")),
+    "from_features_exclusive_prefix": ("attn_from_features", _from_features_mut("causal_exclusive")),
+    "from_features_no_normaliser": ("attn_from_features", _from_features_mut("no_normaliser")),
+}
+
+
+@pytest.mark.parametrize("name", sorted(VARIANT_MUTATIONS))
+def test_variant_mutation_is_caught(name, monkeypatch):
+    attr, fn = VARIANT_MUTATIONS[name]
+    monkeypatch.setattr(VAR, attr, fn)
+    failed = []
+    for pin in oracle_variant_pins.ALL_PINS:
+        try:
+            pin(VAR)
+        except Exception:
+            failed.append(pin.__name__)
+    assert failed, f"no pin catches the planted mistake {name}"

@@ -8,3 +8,11 @@ import oracle_pins
 @pytest.mark.parametrize("pin", oracle_pins.ALL_PINS, ids=lambda f: f.__name__)
 def test_pin(pin):
     pin(oracle.luna_oracle)
+
+
+import oracle_variant_pins  # noqa: E402
+
+
+@pytest.mark.parametrize("pin", oracle_variant_pins.ALL_PINS, ids=lambda f: f.__name__)
+def test_variant_pin(pin):
+    pin(oracle.luna_variants)

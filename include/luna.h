@@ -262,6 +262,87 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
                           int32_t causal, float eps, void* dQ, void* dK, void* dV,
                           const luna_phi_grads* grads, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Feature-map variants.  The map of eq. (11) of Section 3.2 is a template, phi(x) =
+ * h(x)/sqrt(M) [psi_l(w_i . x + b_i)]; fixing h and psi by hand gives the random-feature
+ * maps of Section 3.1, and the kernel ablation of Section 5.4 (Table 5) changes its
+ * form.  Every variant uses the projection u = W x + b of `base` (W, b, M, per_head):
+ *   LUNA_PHI_RFF_COS     sqrt(2/M) cos(u_i)                       D = M
+ *   LUNA_PHI_RFF_SINCOS  (1/sqrt(M)) (sin u_i, cos u_i)           D = 2M, feature 2i + l
+ *   LUNA_PHI_PERFORMER   (1/sqrt(M)) exp(u_i - |x|^2/(2 sqrt(d))) D = M (psi = exp, h(x) =
+ *                        exp(-|x|^2/(2 sqrt d)); with w_i = omega_i / d^(1/4), omega_i ~
+ *                        N(0, I), phi(x).phi(y) estimates exp(x.y / sqrt(d)))
+ *   LUNA_PHI_MLP         the channel MLPs of `base` (L, hidden, shared_channels, nonneg,
+ *                        fc*) with the hidden activation `act` (relu, gelu in its erf
+ *                        form, silu, tanh), evaluated directly, then optionally:
+ *                        env_w [P][L][d], env_b [P][L] (fp32): a tokenwise envelope
+ *                        sigmoid(env_w x + env_b) in [0,1]^L multiplying channel l of
+ *                        every projection (Table 5's envelope-gated map);
+ *                        ch_rms = 1: Listing 1's channel RMS normalisation over the whole
+ *                        call, y_l *= min(target / (rms_l + 1e-6), 1), rms_l = sqrt(mean
+ *                        over every (batch, head, token, projection) of y_l^2 + 1e-6)
+ *                        (a two-pass map; non-causal use only, as it pools all tokens);
+ *                        bank [P][L] (fp32): Table 5's Bank+Coef map, feature i =
+ *                        (1/sqrt(M)) sum_l bank_l y_l(u_i), D = M;
+ *                        otherwise D = M L, feature i L + l.  Order: psi, envelope,
+ *                        channel RMS, bank sum, 1/sqrt(M).
+ * The variants compute in fp32 from the call's input (no piecewise-linear tables).
+ * Limits: M <= 256, D <= 512; for LUNA_PHI_MLP L <= 16 and hidden <= 64.  The other
+ * kinds take no envelope, bank or channel RMS (LUNA_ERR_INVALID_ARG).
+ */
+typedef enum luna_phi_kind {
+  LUNA_PHI_MLP = 0,
+  LUNA_PHI_RFF_COS = 1,
+  LUNA_PHI_RFF_SINCOS = 2,
+  LUNA_PHI_PERFORMER = 3
+} luna_phi_kind;
+
+typedef enum luna_act { LUNA_ACT_RELU = 0, LUNA_ACT_GELU = 1, LUNA_ACT_SILU = 2, LUNA_ACT_TANH = 3 } luna_act;
+
+typedef struct luna_phi_variant {
+  int32_t kind;                /* luna_phi_kind */
+  int32_t act;                 /* luna_act (LUNA_PHI_MLP) */
+  const luna_phi_params* base; /* projection (and, for LUNA_PHI_MLP, the channel MLPs) */
+  const float* env_w;          /* optional envelope [P][L][d] (both or neither) */
+  const float* env_b;          /* [P][L] */
+  const float* bank;           /* optional Bank+Coef coefficients [P][L] */
+  int32_t ch_rms;              /* 0 or 1 */
+  float ch_rms_target;         /* > 0 (Listing 1's default is 0.1) */
+} luna_phi_variant;
+
+/* Features per row of a variant (D), or -1 when the description is invalid. */
+int64_t luna_phi_variant_features(const luna_phi_variant* v);
+
+/* Workspace of luna_featuremap_variant (0 bytes without channel RMS, or on invalid
+ * arguments: check the call's status). */
+size_t luna_featuremap_variant_workspace_bytes(luna_dtype x_dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                                               const luna_phi_variant* v);
+
+/* The variant map of every row of X [B, H, n, d] (x_dtype) into phi_out [B, H, n, D]
+ * (out_dtype).  W is in x_dtype; every other parameter is fp32.  d in {32, 64, 128}. */
+luna_status luna_featuremap_variant(const void* X, luna_dtype x_dtype, int64_t B, int64_t H, int64_t n,
+                                    int64_t d, const luna_phi_variant* v, void* phi_out, luna_dtype out_dtype,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace of luna_attn_fwd_features. */
+size_t luna_attn_features_workspace_bytes(luna_dtype phi_dtype, luna_dtype dtype, int64_t B, int64_t H, int64_t n,
+                                          int64_t d, int64_t D, int32_t causal, int32_t chunk);
+
+/*
+ * Kernel attention, eq. (9) of Section 3.1, for given features: phiQ, phiK [B, H, n, D]
+ * in phi_dtype (any feature map: a variant, luna_featuremap's output, ...), V and out
+ * [B, H, n, d] in dtype; out = phiQ S / (phiQ z + eps) with S, z over every token, or
+ * (causal = 1) over the prefix s <= t, evaluated as the chunked scan with chunk 64.
+ * Features may be signed: the denominator is then the caller's concern.  Runs on the
+ * fp32 GEMM path (bf16 features widened to fp32), or, for causal bf16 calls with
+ * (d, D) = (128, 256) or (64, 128), on the causal scan kernel reading the bf16 features.
+ * 1 <= d <= 256, 1 <= D <= 512.
+ */
+luna_status luna_attn_fwd_features(const void* phiQ, const void* phiK, luna_dtype phi_dtype, const void* V,
+                                   luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d, int64_t D,
+                                   int32_t causal, int32_t chunk, float eps, void* out, void* ws, size_t ws_bytes,
+                                   void* stream);
+
 /* Static description of a status code. */
 const char* luna_status_string(luna_status s);
 

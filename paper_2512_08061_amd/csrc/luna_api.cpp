@@ -90,24 +90,49 @@ struct Layout {
 // (and queries), [V | 1], [num | den - eps] and the per-chunk states, plus P for the
 // causal form.  Causal chunks are the 64-token chunks of the scan; the non-causal form
 // cuts its sums over tokens into 512-token pieces, for parallelism only.
-luna_status plan_f32_forward(const Problem& pb, bool causal, bool queries, Layout* lay, size_t* off) {
-  const int d = (int)pb.d, D = pb.p->M * pb.p->L;
+// (features: the buffers for fp32 features, or none when the caller's are used)
+luna_status plan_f32_buffers(int64_t heads, int64_t n, int d, int D, bool causal, bool queries, bool features,
+                             Layout* lay, size_t* off) {
   lay->chunk = causal ? 64 : 512;
-  const int64_t nch = (pb.n + lay->chunk - 1) / lay->chunk;
+  const int64_t nch = (n + lay->chunk - 1) / lay->chunk;
   if (nch > 65535) return fail(LUNA_ERR_UNSUPPORTED, causal ? "n must be <= 65535 * 64" : "n must be <= 65535 * 512");
   lay->nch = (int)nch;
-  const size_t rows = (size_t)(pb.B * pb.H) * (size_t)pb.n, states = (size_t)(pb.B * pb.H) * lay->nch;
+  const size_t rows = (size_t)heads * (size_t)n, states = (size_t)heads * lay->nch;
   auto take = [&](size_t& at, size_t bytes) {
     at = *off;
     *off = align256(*off + bytes);
   };
-  if (queries) take(lay->phiq, rows * D * 4);
-  take(lay->phik, rows * D * 4);
+  if (queries && features) take(lay->phiq, rows * D * 4);
+  if (features) take(lay->phik, rows * D * 4);
   take(lay->vx, rows * (d + 1) * 4);
   if (queries) take(lay->y, rows * (d + 1) * 4);
   take(lay->sx, states * D * (d + 1) * 4);
   if (causal && queries) take(lay->pm, states * 64 * 64 * 4);
   return LUNA_OK;
+}
+luna_status plan_f32_forward(const Problem& pb, bool causal, bool queries, Layout* lay, size_t* off) {
+  return plan_f32_buffers(pb.B * pb.H, pb.n, (int)pb.d, pb.p->M * pb.p->L, causal, queries, true, lay, off);
+}
+
+// The causal kernel's split.  Too few heads to fill the device: cut every head in two
+// at a chunk boundary x near n/2.  A state launch first sums the state of [0, x) in
+// pieces (one workgroup per head and piece, enough pieces to fill the device); part 1
+// of the scan launch starts from the sum of the pieces.
+void plan_causal_parts(int64_t heads, int64_t n, size_t state_floats, Layout* lay, size_t* off) {
+  if (heads < 256 && n >= 256) {
+    const int64_t cx = n / 64 / 2;  // chunks before the split
+    if (cx >= 1) {
+      lay->parts = 2;
+      lay->split = (int)(cx * 64);
+      int64_t pieces = (256 + heads - 1) / heads;
+      if (pieces > cx) pieces = cx;
+      const int64_t pc = (cx + pieces - 1) / pieces;
+      lay->piece_chunks = (int)pc;
+      lay->pieces = (int)((cx + pc - 1) / pc);  // every piece non-empty
+      lay->state = *off;
+      *off = align256(*off + (size_t)heads * lay->pieces * state_floats * sizeof(float));
+    }
+  }
 }
 
 // Token ranges of the non-causal state pass: enough state workgroups to fill the
@@ -180,24 +205,7 @@ luna_status plan(const Problem& pb, Layout* lay) {
       lay->total = off;
       return LUNA_OK;
     }
-    // Too few heads to fill the device: cut every head in two at a chunk boundary x
-    // near n/2.  A state launch first sums the state of [0, x) in pieces (one
-    // workgroup per head and piece, enough pieces to fill the device); part 1 of the
-    // scan launch starts from the sum of the pieces.
-    if (heads < 256 && pb.n >= 256) {
-      const int64_t cx = pb.n / 64 / 2;  // chunks before the split
-      if (cx >= 1) {
-        lay->parts = 2;
-        lay->split = (int)(cx * 64);
-        int64_t pieces = (256 + heads - 1) / heads;
-        if (pieces > cx) pieces = cx;
-        const int64_t pc = (cx + pieces - 1) / pieces;
-        lay->piece_chunks = (int)pc;
-        lay->pieces = (int)((cx + pc - 1) / pc);  // every piece non-empty
-        lay->state = off;
-        off = align256(off + (size_t)heads * lay->pieces * state_floats * sizeof(float));
-      }
-    }
+    plan_causal_parts(heads, pb.n, state_floats, lay, &off);
   } else if (pb.op == LUNA_OP_STATE) {
     luna::NoncausalPlan np;
     if (luna::noncausal_supported(dt, d, L, M, &np)) {
@@ -335,19 +343,16 @@ struct ChunkGemm {
   }
 };
 
-// The forward pass in fp32 (eq. (9) of Section 3.1, the causal form in 64-token
-// chunks): features of the keys (and queries), [V | 1], per-chunk [S_c | z_c] =
+// The attention part of the fp32 forward for given fp32 features (eq. (9) of
+// Section 3.1, the causal form in 64-token chunks): [V | 1], per-chunk [S_c | z_c] =
 // phi(K_c)^T [V_c | 1], their exclusive prefix over chunks (causal) or total, and with
 // queries [num | den - eps] = phi(Q_c) [S_c | z_c] (+ P_c [V_c | 1], P_c =
-// tril(phi(Q_c) phi(K_c)^T)).  Q == nullptr: the state only.
-luna_status enqueue_f32_forward(const Problem& pb, uint8_t* w, const Layout& lay, const void* Q, const void* K,
-                                const void* V, bool causal, hipStream_t s) {
-  const luna::Dt dt = pb.dt == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
-  const int L = pb.p->L, D = pb.p->M * L, dd = (int)pb.d, E = dd + 1;
-  const int heads = (int)(pb.B * pb.H), C = lay.chunk, nch = lay.nch;
-  const int64_t n = pb.n, nD = n * D, nE = n * E, st_el = (int64_t)D * E, cc = (int64_t)C * C;
-  float* phiq = reinterpret_cast<float*>(w + lay.phiq);
-  float* phik = reinterpret_cast<float*>(w + lay.phik);
+// tril(phi(Q_c) phi(K_c)^T)).  phiq == nullptr: the state only.
+luna_status enqueue_f32_attention(luna::Dt vdt, int64_t heads64, int64_t n, int dd, int D, uint8_t* w,
+                                  const Layout& lay, const float* phiq, const float* phik, const void* V, bool causal,
+                                  hipStream_t s) {
+  const int heads = (int)heads64, E = dd + 1, C = lay.chunk, nch = lay.nch;
+  const int64_t nD = n * D, nE = n * E, st_el = (int64_t)D * E, cc = (int64_t)C * C;
   float* vx = reinterpret_cast<float*>(w + lay.vx);
   float* y = reinterpret_cast<float*>(w + lay.y);
   float* sx = reinterpret_cast<float*>(w + lay.sx);
@@ -355,25 +360,13 @@ luna_status enqueue_f32_forward(const Problem& pb, uint8_t* w, const Layout& lay
   hipError_t e;
 #define LUNA_TRY(expr, what) \
   if ((e = (expr)) != hipSuccess) return hip_fail(e, what)
-  luna::FeatureMapArgs f{};  // queries and keys in one launch
-  f.phi = phi_args(pb, w, lay);
-  f.rows_per_head = n;
-  f.H = (int)pb.H;
-  f.heads = pb.B * pb.H;
-  f.X = K;
-  f.out = phik;
-  if (Q) {
-    f.X2 = Q;
-    f.out2 = phiq;
-  }
-  LUNA_TRY(luna::launch_featuremap(dt, luna::Dt::F32, dd, L, f, s), "feature-map kernel launch");
-  LUNA_TRY(luna::launch_bwd_pack(dt, V, vx, (int64_t)heads * n, dd, s), "pack kernel launch");
+  LUNA_TRY(luna::launch_bwd_pack(vdt, V, vx, heads64 * n, dd, s), "pack kernel launch");
   const ChunkGemm gemm{heads, nch, C, (int)n, s};
   const int64_t sh = (int64_t)nch * st_el;  // head stride of the per-chunk states
   LUNA_TRY(gemm(phik, nD, (int64_t)C * D, 1, D, vx, nE, (int64_t)C * E, E, 1, sx, sh, st_el, E, 1, D, E, C, 0, 0, 1,
                 0, 0), "state GEMM");
   LUNA_TRY(luna::launch_bwd_scan(sx, heads, nch, st_el, causal ? 0 : 2, s), "state scan");
-  if (!Q) return LUNA_OK;
+  if (!phiq) return LUNA_OK;
   LUNA_TRY(gemm(phiq, nD, (int64_t)C * D, D, 1, sx, sh, st_el, E, 1, y, nE, (int64_t)C * E, E, 1, C, E, D, 1, 0, 0,
                 0, 0), "readout GEMM");
   if (causal) {
@@ -384,6 +377,30 @@ luna_status enqueue_f32_forward(const Problem& pb, uint8_t* w, const Layout& lay
   }
 #undef LUNA_TRY
   return LUNA_OK;
+}
+
+// The forward pass in fp32: features of the keys (and queries) by the feature-map
+// kernel, then enqueue_f32_attention.  Q == nullptr: the state only.
+luna_status enqueue_f32_forward(const Problem& pb, uint8_t* w, const Layout& lay, const void* Q, const void* K,
+                                const void* V, bool causal, hipStream_t s) {
+  const luna::Dt dt = pb.dt == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int L = pb.p->L, D = pb.p->M * L, dd = (int)pb.d;
+  float* phiq = reinterpret_cast<float*>(w + lay.phiq);
+  float* phik = reinterpret_cast<float*>(w + lay.phik);
+  luna::FeatureMapArgs f{};  // queries and keys in one launch
+  f.phi = phi_args(pb, w, lay);
+  f.rows_per_head = pb.n;
+  f.H = (int)pb.H;
+  f.heads = pb.B * pb.H;
+  f.X = K;
+  f.out = phik;
+  if (Q) {
+    f.X2 = Q;
+    f.out2 = phiq;
+  }
+  const hipError_t e = luna::launch_featuremap(dt, luna::Dt::F32, dd, L, f, s);
+  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch");
+  return enqueue_f32_attention(dt, pb.B * pb.H, pb.n, dd, D, w, lay, Q ? phiq : nullptr, phik, V, causal, s);
 }
 
 // The generic forward: the fp32 forward, then out = num / den in the call's dtype.
@@ -425,9 +442,217 @@ luna_status scratch_address(void** out) {
   return LUNA_OK;
 }
 
+// A variant description's features per row (D) after checking it completely.
+luna_status check_variant(const luna_phi_variant* v, int64_t* D) {
+  if (v == nullptr || v->base == nullptr) return fail(LUNA_ERR_INVALID_ARG, "variant or its base parameters is NULL");
+  const luna_phi_params* p = v->base;
+  if (v->kind < LUNA_PHI_MLP || v->kind > LUNA_PHI_PERFORMER) return fail(LUNA_ERR_INVALID_ARG, "unknown variant kind");
+  if (p->M < 1 || p->M > 256) return fail(LUNA_ERR_INVALID_ARG, "M must be in [1, 256]");
+  if (p->per_head != 0 && p->per_head != 1) return fail(LUNA_ERR_INVALID_ARG, "per_head must be 0 or 1");
+  if (!p->W || !p->b) return fail(LUNA_ERR_INVALID_ARG, "W or b is NULL");
+  if ((v->env_w == nullptr) != (v->env_b == nullptr)) return fail(LUNA_ERR_INVALID_ARG, "env_w and env_b go together");
+  if (v->ch_rms != 0 && v->ch_rms != 1) return fail(LUNA_ERR_INVALID_ARG, "ch_rms must be 0 or 1");
+  if (v->kind != LUNA_PHI_MLP) {
+    if (v->env_w || v->bank || v->ch_rms)
+      return fail(LUNA_ERR_INVALID_ARG, "an envelope, bank or channel RMS needs the channel-MLP kind");
+    *D = v->kind == LUNA_PHI_RFF_SINCOS ? 2 * (int64_t)p->M : p->M;
+    return LUNA_OK;
+  }
+  if (v->act < LUNA_ACT_RELU || v->act > LUNA_ACT_TANH) return fail(LUNA_ERR_INVALID_ARG, "unknown activation");
+  if (p->L < 1 || p->L > 16) return fail(LUNA_ERR_INVALID_ARG, "L must be in [1, 16]");
+  if (p->hidden < 1 || p->hidden > 64) return fail(LUNA_ERR_INVALID_ARG, "hidden must be in [1, 64]");
+  if (p->shared_channels != 0 && p->shared_channels != 1) return fail(LUNA_ERR_INVALID_ARG, "shared_channels must be 0 or 1");
+  if (p->nonneg != 0 && p->nonneg != 1) return fail(LUNA_ERR_INVALID_ARG, "nonneg must be 0 or 1");
+  if (!p->fc1_w || !p->fc1_b || !p->fc2_w || !p->fc2_b) return fail(LUNA_ERR_INVALID_ARG, "a channel-MLP array is NULL");
+  if (v->ch_rms && !(std::isfinite(v->ch_rms_target) && v->ch_rms_target > 0.0f))
+    return fail(LUNA_ERR_INVALID_ARG, "ch_rms_target must be finite and > 0");
+  *D = v->bank ? (int64_t)p->M : (int64_t)p->M * p->L;
+  if (*D > 512) return fail(LUNA_ERR_INVALID_ARG, "a variant has at most 512 features");
+  return LUNA_OK;
+}
+
+size_t variant_ws_bytes(const luna_phi_variant* v) {
+  if (v->kind != LUNA_PHI_MLP || !v->ch_rms) return 0;
+  return align256((size_t)luna::kVariantMaxGrid * luna::kVariantMaxL * sizeof(double)) +
+         align256((size_t)luna::kVariantMaxL * sizeof(float));
+}
+
+// Buffers of luna_attn_fwd_features: the causal scan kernel on the bf16 features when
+// it is built for (d, D), else the fp32 GEMM path (fp32 copies of bf16 features).
+luna_status plan_features(luna_dtype phi_dtype, luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                          int64_t D, int32_t causal, int32_t chunk, Layout* lay) {
+  if ((phi_dtype != LUNA_F32 && phi_dtype != LUNA_BF16) || (dtype != LUNA_F32 && dtype != LUNA_BF16))
+    return fail(LUNA_ERR_INVALID_ARG, "dtypes must be LUNA_F32 or LUNA_BF16");
+  if (B < 1 || H < 1 || n < 1) return fail(LUNA_ERR_INVALID_ARG, "B, H and n must be >= 1");
+  if (n > (int64_t)1 << 30 || B * H > (int64_t)1 << 24) return fail(LUNA_ERR_UNSUPPORTED, "n or B*H too large");
+  if (d < 1 || d > 256) return fail(LUNA_ERR_UNSUPPORTED, "d must be in [1, 256]");
+  if (D < 1 || D > 512) return fail(LUNA_ERR_UNSUPPORTED, "D must be in [1, 512]");
+  if (causal != 0 && causal != 1) return fail(LUNA_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (causal && chunk != 64) return fail(LUNA_ERR_UNSUPPORTED, "chunk must be 64");
+  const int64_t heads = B * H;
+  size_t off = 0;
+  if (causal && phi_dtype == LUNA_BF16 && dtype == LUNA_BF16 && luna::causal_given_supported(luna::Dt::BF16, (int)d, (int)D)) {
+    lay->given = 1;
+    plan_causal_parts(heads, n, luna::causal_given_state_floats((int)d, (int)D), lay, &off);
+  } else {
+    lay->generic = 1;
+    luna_status st = plan_f32_buffers(heads, n, (int)d, (int)D, causal != 0, true, phi_dtype == LUNA_BF16, lay, &off);
+    if (st != LUNA_OK) return st;
+  }
+  lay->total = off;
+  return LUNA_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int64_t luna_phi_variant_features(const luna_phi_variant* v) {
+  int64_t D = -1;
+  return check_variant(v, &D) == LUNA_OK ? D : -1;
+}
+
+size_t luna_featuremap_variant_workspace_bytes(luna_dtype, int64_t, int64_t, int64_t, int64_t,
+                                               const luna_phi_variant* v) {
+  int64_t D = 0;
+  return check_variant(v, &D) == LUNA_OK ? variant_ws_bytes(v) : 0;
+}
+
+luna_status luna_featuremap_variant(const void* X, luna_dtype x_dtype, int64_t B, int64_t H, int64_t n,
+                                    int64_t d, const luna_phi_variant* v, void* phi_out, luna_dtype out_dtype,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  int64_t D = 0;
+  luna_status st = check_variant(v, &D);
+  if (st != LUNA_OK) return st;
+  if ((x_dtype != LUNA_F32 && x_dtype != LUNA_BF16) || (out_dtype != LUNA_F32 && out_dtype != LUNA_BF16))
+    return fail(LUNA_ERR_INVALID_ARG, "dtypes must be LUNA_F32 or LUNA_BF16");
+  if (B < 1 || H < 1 || n < 1) return fail(LUNA_ERR_INVALID_ARG, "B, H and n must be >= 1");
+  if (n > (int64_t)1 << 30 || B * H > (int64_t)1 << 24) return fail(LUNA_ERR_UNSUPPORTED, "n or B*H too large");
+  if (d != 32 && d != 64 && d != 128) return fail(LUNA_ERR_UNSUPPORTED, "d must be 32, 64 or 128");
+  if (!X || !phi_out) return fail(LUNA_ERR_INVALID_ARG, "X or phi_out is NULL");
+  const size_t need = variant_ws_bytes(v);
+  if (need) {
+    Layout lay;
+    lay.total = need;
+    if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  }
+  const luna_phi_params* p = v->base;
+  luna::VariantArgs a{};
+  a.X = X;
+  a.out = phi_out;
+  a.W = p->W;
+  a.b = p->b;
+  a.kind = v->kind;
+  a.M = p->M;
+  a.per_head = p->per_head;
+  a.H = (int)H;
+  a.rows_per_head = n;
+  a.heads = B * H;
+  a.L = 1;
+  a.hidden = 1;
+  a.C1 = 1;
+  if (v->kind == LUNA_PHI_MLP) {
+    a.act = v->act;
+    a.L = p->L;
+    a.hidden = p->hidden;
+    a.C1 = p->shared_channels ? 1 : p->L;
+    a.nonneg = p->nonneg;
+    a.fc1_w = p->fc1_w;
+    a.fc1_b = p->fc1_b;
+    a.fc2_w = p->fc2_w;
+    a.fc2_b = p->fc2_b;
+    a.env_w = v->env_w;
+    a.env_b = v->env_b;
+    a.bank = v->bank;
+  }
+  const luna::Dt idt = x_dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const luna::Dt odt = out_dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (need) {  // channel RMS: sums of y^2, the scales, then the map
+    uint8_t* w = static_cast<uint8_t*>(ws);
+    double* partial = reinterpret_cast<double*>(w);
+    float* scale = reinterpret_cast<float*>(w + align256((size_t)luna::kVariantMaxGrid * luna::kVariantMaxL * 8));
+    a.rms_pass = 1;
+    a.rms_partial = partial;
+    if ((e = luna::launch_variant_map(idt, odt, (int)d, a, s)) != hipSuccess) return hip_fail(e, "variant map launch");
+    const double count = (double)(B * H) * (double)n * (double)p->M;
+    if ((e = luna::launch_variant_rms(partial, luna::variant_grid(B * H, n), p->L, count, v->ch_rms_target, scale, s)) !=
+        hipSuccess)
+      return hip_fail(e, "channel RMS kernel launch");
+    a.rms_pass = 0;
+    a.rms_scale = scale;
+  }
+  e = luna::launch_variant_map(idt, odt, (int)d, a, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "variant map launch");
+}
+
+size_t luna_attn_features_workspace_bytes(luna_dtype phi_dtype, luna_dtype dtype, int64_t B, int64_t H, int64_t n,
+                                          int64_t d, int64_t D, int32_t causal, int32_t chunk) {
+  Layout lay;
+  return plan_features(phi_dtype, dtype, B, H, n, d, D, causal, chunk, &lay) == LUNA_OK ? lay.total : 0;
+}
+
+luna_status luna_attn_fwd_features(const void* phiQ, const void* phiK, luna_dtype phi_dtype, const void* V,
+                                   luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d, int64_t D,
+                                   int32_t causal, int32_t chunk, float eps, void* out, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  g_last_error.clear();
+  Layout lay;
+  luna_status st = plan_features(phi_dtype, dtype, B, H, n, d, D, causal, chunk, &lay);
+  if (st != LUNA_OK) return st;
+  if (!phiQ || !phiK || !V || !out) return fail(LUNA_ERR_INVALID_ARG, "phiQ, phiK, V or out is NULL");
+  if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (lay.total && (st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  const luna::Dt vdt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  hipError_t e;
+  if (lay.given) {  // the causal scan kernel on the bf16 features
+    luna::CausalArgs a{};
+    a.Q = phiQ;
+    a.K = phiK;
+    a.V = V;
+    a.out = out;
+    a.phi.M = (int)D;
+    a.n = (int)n;
+    a.H = (int)H;
+    a.heads = (int)(B * H);
+    a.parts = lay.parts;
+    a.split = lay.split;
+    a.eps = eps;
+    a.phiq = phiQ;
+    a.phik = phiK;
+    if (lay.parts == 2) {
+      float* stp = reinterpret_cast<float*>(w + lay.state);
+      a.pieces = lay.pieces;
+      a.piece_chunks = lay.piece_chunks;
+      a.state_out = stp;
+      if ((e = luna::launch_causal_given((int)d, (int)D, a, s)) != hipSuccess) return hip_fail(e, "state launch");
+      a.state_out = nullptr;
+      a.state_in = stp;
+    }
+    e = luna::launch_causal_given((int)d, (int)D, a, s);
+    return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention kernel launch");
+  }
+  const int64_t heads = B * H;
+  const float* fq = static_cast<const float*>(phiQ);
+  const float* fk = static_cast<const float*>(phiK);
+  if (phi_dtype == LUNA_BF16) {  // fp32 copies of the features
+    float* q32 = reinterpret_cast<float*>(w + lay.phiq);
+    float* k32 = reinterpret_cast<float*>(w + lay.phik);
+    if ((e = luna::launch_widen(luna::Dt::BF16, phiQ, q32, heads * n * D, s)) != hipSuccess) return hip_fail(e, "widen");
+    if ((e = luna::launch_widen(luna::Dt::BF16, phiK, k32, heads * n * D, s)) != hipSuccess) return hip_fail(e, "widen");
+    fq = q32;
+    fk = k32;
+  }
+  if ((st = enqueue_f32_attention(vdt, heads, n, (int)d, (int)D, w, lay, fq, fk, V, causal != 0, s)) != LUNA_OK)
+    return st;
+  e = luna::launch_fwd_out(vdt, reinterpret_cast<const float*>(w + lay.y), out, heads * n, (int)d, eps, s);
+  return e == hipSuccess ? LUNA_OK : hip_fail(e, "output kernel launch");
+}
+
 
 size_t luna_workspace_bytes(int32_t op, luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
                             const luna_phi_params* p, int32_t chunk) {

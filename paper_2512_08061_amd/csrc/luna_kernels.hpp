@@ -241,6 +241,35 @@ hipError_t launch_bwd_reduce(const float* partial, double* sum, int groups, int 
 hipError_t launch_bwd_prefix(const double* sum, double* pre, const uint8_t* tables, int M, int d, int L,
                              int part_floats, int nseg_cap, int sets, hipStream_t s);
 hipError_t launch_bwd_mlp(const BwdMlp& a, int sets, hipStream_t s);
+// Feature-map variants (random Fourier cos and sin/cos, Performer, channel MLPs with a
+// smooth activation, an envelope, channel RMS and Bank+Coef), evaluated directly.
+constexpr int kVarMlp = 0, kVarCos = 1, kVarSinCos = 2, kVarPerformer = 3;
+constexpr int kVariantMaxGrid = 2048;   // workgroups of one variant map (rows loop)
+constexpr int kVariantMaxL = 16;        // channel RMS partials per workgroup
+struct VariantArgs {
+  const void* X;        // [heads][n][d], the call's input dtype
+  void* out;            // [heads][n][D]
+  const void* W;        // [P][M][d], input dtype
+  const float* b;       // [P][M]
+  const float* fc1_w;   // [P][C1][hidden]
+  const float* fc1_b;
+  const float* fc2_w;   // [P][L][hidden]
+  const float* fc2_b;   // [P][L]
+  const float* env_w;   // [P][L][d] or null
+  const float* env_b;   // [P][L]
+  const float* bank;    // [P][L] or null
+  int kind, act, M, L, hidden, C1, nonneg, per_head, H;
+  int64_t rows_per_head, heads;
+  int rms_pass;             // 1: sums of y^2 into rms_partial only; otherwise map (rms_scale if set)
+  double* rms_partial;      // [grid][kVariantMaxL]
+  const float* rms_scale;   // [L] or null
+};
+int variant_grid(int64_t heads, int64_t rows_per_head);
+hipError_t launch_variant_map(Dt in_dt, Dt out_dt, int d, const VariantArgs& a, hipStream_t s);
+hipError_t launch_variant_rms(const double* partial, int groups, int L, double count, float target, float* scale,
+                              hipStream_t s);
+hipError_t launch_widen(Dt dt, const void* src, float* dst, int64_t n, hipStream_t s);
+
 // forward pass of the shapes without a fused kernel (fp32 GEMMs and scans as above)
 hipError_t launch_fwd_out(Dt dt, const float* Y, void* out, int64_t rows, int d, float eps, hipStream_t s);
 hipError_t launch_fwd_export(const float* X, int64_t head_stride, float* S, float* z, int heads, int D, int d,

@@ -69,6 +69,18 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.luna_attn_fwd_causal_noalloc.restype = i32
     lib.luna_noalloc_scratch_bytes.argtypes = []
     lib.luna_noalloc_scratch_bytes.restype = sz
+    PV = ctypes.POINTER(PhiVariantC)
+    lib.luna_phi_variant_features.argtypes = [PV]
+    lib.luna_phi_variant_features.restype = i64
+    lib.luna_featuremap_variant_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, PV]
+    lib.luna_featuremap_variant_workspace_bytes.restype = sz
+    lib.luna_featuremap_variant.argtypes = [vp, i32, i64, i64, i64, i64, PV, vp, i32, vp, sz, vp]
+    lib.luna_featuremap_variant.restype = i32
+    lib.luna_attn_features_workspace_bytes.argtypes = [i32, i32, i64, i64, i64, i64, i64, i32, i32]
+    lib.luna_attn_features_workspace_bytes.restype = sz
+    lib.luna_attn_fwd_features.argtypes = [vp, vp, i32, vp, i32, i64, i64, i64, i64, i64, i32, i32, ctypes.c_float,
+                                           vp, vp, sz, vp]
+    lib.luna_attn_fwd_features.restype = i32
     lib.luna_attn_state.argtypes = [vp, vp, i32, i64, i64, i64, i64, P, i32, vp, vp, vp, sz, vp]
     lib.luna_attn_state.restype = i32
     lib.luna_attn_causal_step.argtypes = [vp, vp, vp, i32, i64, i64, i64, i64, P, ctypes.c_float, i32, vp, vp, vp,
@@ -195,6 +207,100 @@ def featuremap(X, p: PhiParams, out_dtype=None):
     _check(lib.luna_featuremap(X.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), out.data_ptr(), _dt(out), wsp, wsn,
                                _stream_ptr(X.device)))
     out._luna_ws = ws  # keep the workspace alive until the output is
+    return out
+
+
+# ---------------------------------------------------------------------------
+# feature-map variants and attention from given features
+# ---------------------------------------------------------------------------
+
+PHI_MLP, PHI_RFF_COS, PHI_RFF_SINCOS, PHI_PERFORMER = 0, 1, 2, 3
+ACTS = {"relu": 0, "gelu": 1, "silu": 2, "tanh": 3}
+KINDS = {"mlp": PHI_MLP, "rff_cos": PHI_RFF_COS, "rff_sincos": PHI_RFF_SINCOS, "performer": PHI_PERFORMER}
+
+
+class PhiVariantC(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("act", ctypes.c_int32), ("base", ctypes.POINTER(PhiParamsC)),
+                ("env_w", ctypes.c_void_p), ("env_b", ctypes.c_void_p), ("bank", ctypes.c_void_p),
+                ("ch_rms", ctypes.c_int32), ("ch_rms_target", ctypes.c_float)]
+
+
+class PhiVariant:
+    """Device-resident description of a feature-map variant (luna_phi_variant)."""
+
+    def __init__(self, kind: str, base: PhiParams, act: str = "relu", env_w=None, env_b=None, bank=None,
+                 ch_rms: bool = False, ch_rms_target: float = 0.1):
+        self.kind, self.act, self.base = kind, act, base
+        self.env_w, self.env_b, self.bank = env_w, env_b, bank
+        self.ch_rms, self.ch_rms_target = bool(ch_rms), float(ch_rms_target)
+        self._pc = base.c()
+
+    @classmethod
+    def from_arrays(cls, p: dict, device, dtype):
+        """Upload a variant dict as the oracle takes it ("kind", "act", W, b, the channel
+        MLP for "mlp", optional env_w / env_b / bank / ch_rms / ch_rms_target)."""
+        import numpy as np
+
+        torch = _torch()
+        f32 = lambda x: None if x is None else torch.as_tensor(x, dtype=torch.float32).contiguous().to(device)  # noqa: E731
+        q = dict(p)
+        if q.get("kind", "mlp") != "mlp":  # the projection only: a placeholder channel MLP
+            lead = q["W"].shape[:-2]
+            q.update(fc1_w=np.zeros(lead + (1, 1)), fc1_b=np.zeros(lead + (1, 1)), fc2_w=np.zeros(lead + (1, 1)),
+                     fc2_b=np.zeros(lead + (1,)), L=1, hidden=1, M=q["W"].shape[-2])
+        base = PhiParams.from_arrays(q, device, dtype)
+        return cls(q.get("kind", "mlp"), base, q.get("act", "relu"), f32(q.get("env_w")), f32(q.get("env_b")),
+                   f32(q.get("bank")), q.get("ch_rms", False), q.get("ch_rms_target", 0.1))
+
+    def c(self) -> PhiVariantC:
+        ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+        return PhiVariantC(KINDS[self.kind], ACTS[self.act], ctypes.pointer(self._pc), ptr(self.env_w),
+                           ptr(self.env_b), ptr(self.bank), int(self.ch_rms), self.ch_rms_target)
+
+    def features(self) -> int:
+        D = int(load_library().luna_phi_variant_features(ctypes.byref(self.c())))
+        if D < 0:
+            raise LunaError(LUNA_ERR_INVALID_ARG, load_library().luna_last_error().decode())
+        return D
+
+
+def featuremap_variant(X, v: PhiVariant, out_dtype=None):
+    """The variant map of every row of X [B, H, n, d]; returns [B, H, n, D]."""
+    torch = _torch()
+    lib = load_library()
+    if X.dim() != 4 or not X.is_contiguous():
+        raise LunaError(LUNA_ERR_INVALID_ARG, "X must be a contiguous [B, H, n, d] tensor")
+    B, H, n, d = X.shape
+    vc = v.c()
+    D = int(lib.luna_phi_variant_features(ctypes.byref(vc)))
+    if D < 0:
+        raise LunaError(LUNA_ERR_INVALID_ARG, lib.luna_last_error().decode())
+    out = torch.empty((B, H, n, D), dtype=X.dtype if out_dtype is None else out_dtype, device=X.device)
+    nb = int(lib.luna_featuremap_variant_workspace_bytes(_dt(X), B, H, n, d, ctypes.byref(vc)))
+    ws, wsp, wsn = _workspace(nb, X.device)
+    _check(lib.luna_featuremap_variant(X.data_ptr(), _dt(X), B, H, n, d, ctypes.byref(vc), out.data_ptr(), _dt(out),
+                                       wsp, wsn, _stream_ptr(X.device)))
+    out._luna_ws = ws
+    return out
+
+
+def attn_fwd_features(phiQ, phiK, V, causal: bool = False, eps: float = 1e-6, chunk: int = 64, out=None):
+    """Kernel attention for given features phiQ, phiK [B, H, n, D] and V [B, H, n, d]."""
+    torch = _torch()
+    lib = load_library()
+    for t in (phiQ, phiK, V):
+        if t.dim() != 4 or not t.is_contiguous():
+            raise LunaError(LUNA_ERR_INVALID_ARG, "inputs must be contiguous [B, H, n, *] tensors")
+    B, H, n, D = phiQ.shape
+    d = V.shape[-1]
+    if phiK.shape != phiQ.shape or V.shape[:3] != phiQ.shape[:3] or phiK.dtype != phiQ.dtype:
+        raise LunaError(LUNA_ERR_INVALID_ARG, "shapes or dtypes do not match")
+    out = torch.empty_like(V) if out is None else out
+    nb = int(lib.luna_attn_features_workspace_bytes(_dt(phiQ), _dt(V), B, H, n, d, D, int(causal), chunk))
+    ws, wsp, wsn = _workspace(nb, V.device)
+    _check(lib.luna_attn_fwd_features(phiQ.data_ptr(), phiK.data_ptr(), _dt(phiQ), V.data_ptr(), _dt(V), B, H, n, d,
+                                      D, int(causal), chunk, eps, out.data_ptr(), wsp, wsn, _stream_ptr(V.device)))
+    out._luna_ws = ws
     return out
 
 

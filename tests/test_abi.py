@@ -23,7 +23,9 @@ def test_exports_every_declared_symbol(lib):
     names = luna.header_functions()
     assert set(names) == {"luna_workspace_bytes", "luna_featuremap", "luna_attn_fwd", "luna_attn_fwd_causal",
                           "luna_attn_state", "luna_attn_causal_step", "luna_status_string", "luna_last_error",
-                          "luna_attn_fwd_causal_noalloc", "luna_noalloc_scratch_bytes", "luna_attn_bwd"}
+                          "luna_attn_fwd_causal_noalloc", "luna_noalloc_scratch_bytes", "luna_attn_bwd",
+                          "luna_phi_variant_features", "luna_featuremap_variant_workspace_bytes",
+                          "luna_featuremap_variant", "luna_attn_features_workspace_bytes", "luna_attn_fwd_features"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -186,3 +188,71 @@ def test_noalloc_refuses_beyond_scratch_on_host(lib):
                                           1e-6, FAKE, None)
     assert st == luna.LUNA_ERR_WORKSPACE
     assert b"static scratch" in lib.luna_last_error()
+
+
+def _variant(lib, kind=0, act=0, M=16, L=8, hidden=64, env=False, bank=False, ch_rms=0, target=0.1, base=None):
+    base = base or _params(M=M, L=L, hidden=hidden)
+    v = luna.PhiVariantC(kind, act, ctypes.pointer(base), FAKE if env else None, FAKE if env else None,
+                         FAKE if bank else None, ch_rms, target)
+    v._base = base  # keep the parameters alive
+    return v
+
+
+def test_variant_features_and_rejects(lib):
+    """Feature counts of the variants and their argument checks, on the host."""
+    feats = lambda v: lib.luna_phi_variant_features(ctypes.byref(v))  # noqa: E731
+    assert feats(_variant(lib)) == 128                      # M L
+    assert feats(_variant(lib, bank=True)) == 16            # Bank+Coef: M
+    assert feats(_variant(lib, kind=1)) == 16               # RFF cos: M
+    assert feats(_variant(lib, kind=2)) == 32               # sin/cos: 2 M
+    assert feats(_variant(lib, kind=3)) == 16               # Performer: M
+    assert feats(_variant(lib, kind=4)) == -1               # unknown kind
+    assert feats(_variant(lib, act=7)) == -1                # unknown activation
+    assert feats(_variant(lib, kind=1, env=True)) == -1     # envelope only with the MLP kind
+    assert feats(_variant(lib, kind=3, ch_rms=1)) == -1
+    assert feats(_variant(lib, ch_rms=1, target=0.0)) == -1
+    assert feats(_variant(lib, ch_rms=1, target=float("nan"))) == -1
+    assert feats(_variant(lib, M=64, L=16)) == -1           # more than 512 features
+    assert feats(_variant(lib, M=300, L=1)) == -1
+    # workspace: the channel RMS partials, else none
+    ws = lambda v: lib.luna_featuremap_variant_workspace_bytes(luna.LUNA_BF16, 2, 3, 100, 64, ctypes.byref(v))  # noqa: E731
+    assert ws(_variant(lib)) == 0 and ws(_variant(lib, ch_rms=1)) > 0
+    v = _variant(lib)
+    st = lambda **kw: lib.luna_featuremap_variant(kw.get("x", FAKE), luna.LUNA_BF16, 2, 3, kw.get("n", 100),  # noqa: E731
+                                                   kw.get("d", 64), ctypes.byref(kw.get("v", v)), FAKE,
+                                                   kw.get("odt", luna.LUNA_BF16), FAKE, 1 << 40, None)
+    assert st(x=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(n=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(d=48) == luna.LUNA_ERR_UNSUPPORTED
+    assert st(odt=5) == luna.LUNA_ERR_INVALID_ARG
+    assert st(v=_variant(lib, kind=9)) == luna.LUNA_ERR_INVALID_ARG
+    rms = _variant(lib, ch_rms=1)
+    assert lib.luna_featuremap_variant(FAKE, luna.LUNA_BF16, 2, 3, 100, 64, ctypes.byref(rms), FAKE, luna.LUNA_BF16,
+                                       FAKE, 256, None) == luna.LUNA_ERR_WORKSPACE
+
+
+def test_attn_features_planning(lib):
+    """Attention from given features: the causal scan kernel for bf16 features with
+    (d, D) = (128, 256) (state pieces only), otherwise the fp32 GEMM path (fp32 copies
+    of bf16 features, per-chunk states); argument checks on the host."""
+    B, H, n = 8, 16, 16384
+    wsb = lambda pdt, dt, d, D, causal, chunk=64: lib.luna_attn_features_workspace_bytes(  # noqa: E731
+        pdt, dt, B, H, n, d, D, causal, chunk)
+    given = wsb(luna.LUNA_BF16, luna.LUNA_BF16, 128, 256, 1)
+    assert 0 < given < 64 << 20
+    rows = B * H * n
+    gemm32 = wsb(luna.LUNA_F32, luna.LUNA_BF16, 128, 256, 1)
+    assert rows * 2 * 129 * 4 <= gemm32 < rows * 2 * 129 * 4 + B * H * 256 * (256 * 129 * 4 + 64 * 64 * 4) + (1 << 20)
+    gemm16 = wsb(luna.LUNA_BF16, luna.LUNA_F32, 128, 256, 1)
+    assert gemm16 >= gemm32 + rows * 256 * 8 - (1 << 20)  # plus the fp32 copies
+    assert wsb(luna.LUNA_BF16, luna.LUNA_BF16, 128, 256, 1, chunk=32) == 0
+    assert wsb(luna.LUNA_BF16, luna.LUNA_BF16, 128, 600, 0) == 0
+    assert wsb(luna.LUNA_BF16, luna.LUNA_BF16, 300, 64, 0) == 0
+    assert wsb(luna.LUNA_BF16, 7, 64, 64, 0) == 0
+    call = lambda **kw: lib.luna_attn_fwd_features(FAKE, FAKE, luna.LUNA_BF16, kw.get("v", FAKE), luna.LUNA_BF16, 2,  # noqa: E731
+                                                   3, 100, 64, 64, kw.get("causal", 0), 64, kw.get("eps", 1e-6),
+                                                   FAKE, FAKE, kw.get("ws", 1 << 40), None)
+    assert call(v=0) == luna.LUNA_ERR_INVALID_ARG
+    assert call(causal=2) == luna.LUNA_ERR_INVALID_ARG
+    assert call(eps=-1.0) == luna.LUNA_ERR_INVALID_ARG
+    assert call(ws=16) == luna.LUNA_ERR_WORKSPACE

@@ -682,6 +682,154 @@ def configs_bench(args) -> int:
     return 0
 
 
+VALU_LANE_OPS = 78.6e12  # fp32 vector FMA lane-operations per second (157.3 TFLOP/s / 2)
+# (label, kind, act, M, L, options) of the variant report, on the long encoder problem's
+# queries; every map has D = 128 features per row except Bank+Coef (D = M = 16)
+VARIANT_CASES = [
+    ("rff_cos", "rff_cos", "relu", 128, 1, {}),
+    ("rff_sincos", "rff_sincos", "relu", 64, 1, {}),
+    ("performer", "performer", "relu", 128, 1, {}),
+    ("mlp_relu", "mlp", "relu", 16, 8, {}),
+    ("mlp_gelu", "mlp", "gelu", 16, 8, {}),
+    ("mlp_silu_shared", "mlp", "silu", 16, 8, {"shared": True}),
+    ("mlp_tanh_envelope", "mlp", "tanh", 16, 8, {"env": True}),
+    ("mlp_gelu_ch_rms", "mlp", "gelu", 16, 8, {"ch_rms": True}),
+    ("mlp_gelu_bank", "mlp", "gelu", 16, 8, {"bank": True}),
+]
+
+
+def _timed_calls(fn, steps, warmup, stream, flush, sink):
+    """Median, 10th and 90th percentile of HIP-event call times (ms), with a 1 GiB read
+    before every call so that the inputs come from HBM."""
+    import torch
+
+    for _ in range(warmup):
+        torch.amax(flush, dim=0, out=sink)
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in ev:
+        torch.amax(flush, dim=0, out=sink)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    times = sorted(e0.elapsed_time(e1) for e0, e1 in ev)
+    pick = lambda f: times[min(len(times) - 1, int(f * len(times)))]  # noqa: E731
+    return pick(0.5), pick(0.1), pick(0.9)
+
+
+def variants_bench(args) -> int:
+    """The feature-map variants (luna_featuremap_variant) on the long encoder problem's
+    queries (B=32, H=8, n=4096, d=64, bf16 in and out), and attention from given
+    features (luna_attn_fwd_features) at the two long problems' shapes.  One JSON line
+    per case: median call time (HIP events, caches flushed before every call), the HBM
+    floor of the algorithmic bytes (read x, write phi; channel RMS reads x twice) and,
+    for the channel MLPs, the VALU floor of their hidden units at three fp32 lane
+    operations each (the multiply-add into the unit, a relu, the multiply-add into the
+    channel: the cheapest unit; smooth activations cost more)."""
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    luna.load_library()
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    sink = torch.empty((), dtype=torch.float32, device=dev)
+    w = wl.WORKLOADS["long_noncausal"]
+    Q, _, _ = wl.make_inputs(w, args.seed)
+    x = torch.from_numpy(Q).to(dev).to(torch.bfloat16).contiguous()
+    del Q
+    rows = w.B * w.H * w.n
+    rows_out = []
+    only = set(filter(None, args.variants_only.split(",")))
+    for label, kind, act, M, L, opts in VARIANT_CASES:
+        if only and label not in only:
+            continue
+        p = wl.make_variant_params(kind, M, w.d, L=L, act=act, seed=args.seed, **opts)
+        v = luna.PhiVariant.from_arrays(p, dev, torch.bfloat16)
+        D = v.features()
+        out = torch.empty((w.B, w.H, w.n, D), dtype=torch.bfloat16, device=dev)
+        fn = lambda: luna.featuremap_variant(x, v, out=out)  # noqa: E731
+        ms, p10, p90 = _timed_calls(fn, args.steps, args.warmup, stream, flush, sink)
+        reads = 2 if opts.get("ch_rms") else 1
+        nbytes = rows * (reads * w.d + D) * 2
+        t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
+        units = rows * M * L * p.get("hidden", 0) if kind == "mlp" else 0
+        t_alu = reads * 3 * units / VALU_LANE_OPS
+        bound, floor = ("alu", t_alu) if t_alu > t_hbm else ("hbm", t_hbm)
+        rec = {"case": label, "kind": kind, "act": act, "M": M, "L": L, "D": D, "options": opts,
+               "workload": "long encoder queries B=32 H=8 n=4096 d=64, bf16 in and out",
+               "ms_median": round(ms, 5), "ms_p10": round(p10, 5), "ms_p90": round(p90, 5),
+               "rows_per_s": rows / (ms * 1e-3), "hbm_gbs": nbytes / (ms * 1e-3) / 1e9,
+               "hidden_units_per_s": units / (ms * 1e-3) if units else None,
+               "bound": bound, "floor_us": 1e6 * floor, "roofline_frac": floor / (ms * 1e-3)}
+        log(f"{label}: {1e3 * ms:.1f} us, {rec['roofline_frac']:.1%} of the {bound} floor")
+        print(json.dumps(rec), flush=True)
+        rows_out.append(rec)
+        del out
+    del x
+    # attention from given features: positive features exp(N(0, 1/4)) / sqrt(D), drawn
+    # on the device from a seeded generator
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    for label, (B, H, n, d, D, fdt, causal) in (
+            ("features_causal_bf16", (8, 16, 16384, 128, 256, torch.bfloat16, True)),
+            ("features_noncausal_f32", (32, 8, 4096, 64, 128, torch.float32, False))):
+        if only and label not in only:
+            continue
+        feats = []
+        for _ in range(2):
+            t = torch.empty((B, H, n, D), dtype=fdt, device=dev)
+            for b in range(B):  # a batch entry at a time: fp32 temporaries stay small
+                t[b] = (torch.randn((H, n, D), generator=gen, device=dev) * 0.5).exp_().div_(D ** 0.5).to(fdt)
+            feats.append(t)
+        V = torch.randn((B, H, n, d), generator=gen, device=dev).to(torch.bfloat16)
+        out = torch.empty_like(V)
+        fn = lambda: luna.attn_fwd_features(feats[0], feats[1], V, causal=causal, out=out)  # noqa: E731
+        ms, p10, p90 = _timed_calls(fn, args.steps, args.warmup, stream, flush, sink)
+        th = B * H * n
+        fb = 2 if fdt == torch.bfloat16 else 4
+        nbytes = th * (2 * D * fb + 2 * d * 2)
+        t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
+        rec = {"case": label, "shape": {"B": B, "H": H, "n": n, "d": d, "D": D, "causal": causal,
+                                        "features": "bf16" if fb == 2 else "f32", "values": "bf16"},
+               "path": "causal scan kernel" if (causal and fb == 2) else "fp32 GEMM",
+               "ms_median": round(ms, 5), "ms_p10": round(p10, 5), "ms_p90": round(p90, 5),
+               "tokens_per_s": B * n / (ms * 1e-3), "hbm_gbs": nbytes / (ms * 1e-3) / 1e9,
+               "bound": "hbm", "floor_us": 1e6 * t_hbm, "roofline_frac": t_hbm / (ms * 1e-3)}
+        log(f"{label}: {1e3 * ms:.1f} us, {rec['roofline_frac']:.1%} of the hbm floor")
+        print(json.dumps(rec), flush=True)
+        rows_out.append(rec)
+        del feats, V, out
+        torch.cuda.synchronize()
+    if args.variants_table:
+        with open(args.variants_table, "w") as fh:
+            fh.write("# Feature-map variants and attention from given features on one MI355X\n\n")
+            fh.write(f"Command: `python bench.py --variants --steps {args.steps} --warmup {args.warmup} "
+                     f"--variants-table {args.variants_table}`\n\n")
+            fh.write("One ABI call per timing, median of the timed calls with the 10th and 90th percentiles, HIP "
+                     "events on the launch stream, caches flushed by a 1 GiB read before every call. Maps: the long "
+                     "encoder problem's queries (1,048,576 rows, d = 64), bf16 in and out; the HBM floor is reading x "
+                     "(twice with channel RMS) and writing phi at 8 TB/s; the ALU floor of a channel MLP is its hidden "
+                     "units at 3 fp32 lane operations each (the relu unit) at 78.6e12 lane operations/s. Attention "
+                     "from features: read both feature matrices and V, write out.\n\n")
+            fh.write("| case | D | median us (p10-p90) | rows/s or tokens/s | GB/s | hidden units/s | floor us | "
+                     "roofline |\n|---|---|---|---|---|---|---|---|\n")
+            for r in rows_out:
+                D = r.get("D", r.get("shape", {}).get("D"))
+                rate = r.get("rows_per_s", r.get("tokens_per_s"))
+                hu = r.get("hidden_units_per_s")
+                fh.write(f"| {r['case']} | {D} | {1e3 * r['ms_median']:.1f} ({1e3 * r['ms_p10']:.1f}-"
+                         f"{1e3 * r['ms_p90']:.1f}) | {rate:.3g} | {r['hbm_gbs']:.0f} | "
+                         f"{'' if hu is None else f'{hu:.3g}'} | {r['floor_us']:.1f} | "
+                         f"{r['roofline_frac']:.1%} {r['bound']} |\n")
+        log(f"wrote {args.variants_table}")
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -721,12 +869,19 @@ def main() -> int:
                     help="with --configs: also write the results as a markdown table to PATH")
     ap.add_argument("--configs-only", default="", metavar="NAMES",
                     help="with --configs: comma-separated configuration labels to run (default: all)")
+    ap.add_argument("--variants", action="store_true",
+                    help="instead of the hot-path step: time the feature-map variants on the long encoder "
+                         "problem's queries and attention from given features, one JSON line per case")
+    ap.add_argument("--variants-table", default="", metavar="PATH",
+                    help="with --variants: also write the results as a markdown table to PATH")
+    ap.add_argument("--variants-only", default="", metavar="NAMES",
+                    help="with --variants: comma-separated case labels to run (default: all)")
     args = ap.parse_args()
     if args.traffic_from:
         return traffic_from(*args.traffic_from, args.traffic_command)
     if args.counters_from:
         return counters_from(args.counters_from, args.counters_command)
-    if args.gpus != 1 and (args.decode or args.configs or args.featuremap or args.backward):
+    if args.gpus != 1 and (args.decode or args.configs or args.featuremap or args.backward or args.variants):
         print("bench.py runs on one GPU only; use --gpus 1.", file=sys.stderr)
         return 2
     if args.decode:
@@ -737,6 +892,8 @@ def main() -> int:
         return backward_bench(args)
     if args.configs:
         return configs_bench(args)
+    if args.variants:
+        return variants_bench(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: LUNA attention shards over (batch, head) with no "

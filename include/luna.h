@@ -313,8 +313,9 @@ typedef struct luna_phi_variant {
 /* Features per row of a variant (D), or -1 when the description is invalid. */
 int64_t luna_phi_variant_features(const luna_phi_variant* v);
 
-/* Workspace of luna_featuremap_variant (0 bytes without channel RMS, or on invalid
- * arguments: check the call's status). */
+/* Workspace of luna_featuremap_variant: 0 bytes without channel RMS; with it, about
+ * 4 B H n M L bytes (y of every row in fp32, kept between the two passes) plus 256 KiB.
+ * 0 also on invalid arguments: check the call's status. */
 size_t luna_featuremap_variant_workspace_bytes(luna_dtype x_dtype, int64_t B, int64_t H, int64_t n, int64_t d,
                                                const luna_phi_variant* v);
 

@@ -471,10 +471,14 @@ luna_status check_variant(const luna_phi_variant* v, int64_t* D) {
   return LUNA_OK;
 }
 
-size_t variant_ws_bytes(const luna_phi_variant* v) {
+// Workspace of a variant map of `rows` rows: with channel RMS, the per-workgroup
+// partial sums, the channel scales and y of every row in fp32 ([row][M][L]).
+constexpr size_t kVarPartialBytes = (size_t)luna::kVariantMaxGrid * luna::kVariantMaxL * sizeof(double);
+constexpr size_t kVarScaleBytes = 256;
+size_t variant_ws_bytes(const luna_phi_variant* v, int64_t rows) {
   if (v->kind != LUNA_PHI_MLP || !v->ch_rms) return 0;
-  return align256((size_t)luna::kVariantMaxGrid * luna::kVariantMaxL * sizeof(double)) +
-         align256((size_t)luna::kVariantMaxL * sizeof(float));
+  return align256(kVarPartialBytes) + kVarScaleBytes +
+         align256((size_t)rows * (size_t)v->base->M * (size_t)v->base->L * sizeof(float));
 }
 
 // Buffers of luna_attn_fwd_features: the causal scan kernel on the bf16 features when
@@ -512,10 +516,11 @@ int64_t luna_phi_variant_features(const luna_phi_variant* v) {
   return check_variant(v, &D) == LUNA_OK ? D : -1;
 }
 
-size_t luna_featuremap_variant_workspace_bytes(luna_dtype, int64_t, int64_t, int64_t, int64_t,
+size_t luna_featuremap_variant_workspace_bytes(luna_dtype, int64_t B, int64_t H, int64_t n, int64_t,
                                                const luna_phi_variant* v) {
   int64_t D = 0;
-  return check_variant(v, &D) == LUNA_OK ? variant_ws_bytes(v) : 0;
+  if (B < 1 || H < 1 || n < 1 || n > (int64_t)1 << 30 || B * H > (int64_t)1 << 24) return 0;
+  return check_variant(v, &D) == LUNA_OK ? variant_ws_bytes(v, B * H * n) : 0;
 }
 
 luna_status luna_featuremap_variant(const void* X, luna_dtype x_dtype, int64_t B, int64_t H, int64_t n,
@@ -531,7 +536,7 @@ luna_status luna_featuremap_variant(const void* X, luna_dtype x_dtype, int64_t B
   if (n > (int64_t)1 << 30 || B * H > (int64_t)1 << 24) return fail(LUNA_ERR_UNSUPPORTED, "n or B*H too large");
   if (d != 32 && d != 64 && d != 128) return fail(LUNA_ERR_UNSUPPORTED, "d must be 32, 64 or 128");
   if (!X || !phi_out) return fail(LUNA_ERR_INVALID_ARG, "X or phi_out is NULL");
-  const size_t need = variant_ws_bytes(v);
+  const size_t need = variant_ws_bytes(v, B * H * n);
   if (need) {
     Layout lay;
     lay.total = need;
@@ -567,24 +572,25 @@ luna_status luna_featuremap_variant(const void* X, luna_dtype x_dtype, int64_t B
     a.bank = v->bank;
   }
   const luna::Dt idt = x_dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
-  const luna::Dt odt = out_dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  a.out_bf16 = out_dtype == LUNA_BF16;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipError_t e;
-  if (need) {  // channel RMS: sums of y^2, the scales, then the map
+  int grid = 0;
+  if (need) {  // channel RMS: y and the sums of y^2, the scales, then phi from y
     uint8_t* w = static_cast<uint8_t*>(ws);
     double* partial = reinterpret_cast<double*>(w);
-    float* scale = reinterpret_cast<float*>(w + align256((size_t)luna::kVariantMaxGrid * luna::kVariantMaxL * 8));
+    float* scale = reinterpret_cast<float*>(w + align256(kVarPartialBytes));
     a.rms_pass = 1;
     a.rms_partial = partial;
-    if ((e = luna::launch_variant_map(idt, odt, (int)d, a, s)) != hipSuccess) return hip_fail(e, "variant map launch");
+    a.rms_y = reinterpret_cast<float*>(w + align256(kVarPartialBytes) + kVarScaleBytes);
+    if ((e = luna::launch_variant_map(idt, (int)d, a, &grid, s)) != hipSuccess) return hip_fail(e, "variant map launch");
     const double count = (double)(B * H) * (double)n * (double)p->M;
-    if ((e = luna::launch_variant_rms(partial, luna::variant_grid(B * H, n), p->L, count, v->ch_rms_target, scale, s)) !=
-        hipSuccess)
+    if ((e = luna::launch_variant_rms(partial, grid, p->L, count, v->ch_rms_target, scale, s)) != hipSuccess)
       return hip_fail(e, "channel RMS kernel launch");
-    a.rms_pass = 0;
-    a.rms_scale = scale;
+    e = luna::launch_variant_finish(a, scale, s);
+    return e == hipSuccess ? LUNA_OK : hip_fail(e, "channel RMS output kernel launch");
   }
-  e = luna::launch_variant_map(idt, odt, (int)d, a, s);
+  e = luna::launch_variant_map(idt, (int)d, a, &grid, s);
   return e == hipSuccess ? LUNA_OK : hip_fail(e, "variant map launch");
 }
 

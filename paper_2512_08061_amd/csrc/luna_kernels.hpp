@@ -260,12 +260,16 @@ struct VariantArgs {
   const float* bank;    // [P][L] or null
   int kind, act, M, L, hidden, C1, nonneg, per_head, H;
   int64_t rows_per_head, heads;
-  int rms_pass;             // 1: sums of y^2 into rms_partial only; otherwise map (rms_scale if set)
+  int out_bf16;             // phi stored as bf16 (else fp32)
+  int rms_pass;             // 1: y into rms_y and sums of y^2 into rms_partial, no phi; 0: phi
   double* rms_partial;      // [grid][kVariantMaxL]
-  const float* rms_scale;   // [L] or null
+  float* rms_y;             // [heads][n][M][L]: y after the envelope, before the channel scales
 };
-int variant_grid(int64_t heads, int64_t rows_per_head);
-hipError_t launch_variant_map(Dt in_dt, Dt out_dt, int d, const VariantArgs& a, hipStream_t s);
+// Launch the variant map (a.out_bf16 set); *grid receives the workgroup count, the
+// number of channel-RMS partials written by a first pass.
+hipError_t launch_variant_map(Dt in_dt, int d, const VariantArgs& a, int* grid, hipStream_t s);
+// phi from rms_y: channel scales, bank sum or 1/sqrt(M), in the output dtype
+hipError_t launch_variant_finish(const VariantArgs& a, const float* scale, hipStream_t s);
 hipError_t launch_variant_rms(const double* partial, int groups, int L, double count, float target, float* scale,
                               hipStream_t s);
 hipError_t launch_widen(Dt dt, const void* src, float* dst, int64_t n, hipStream_t s);

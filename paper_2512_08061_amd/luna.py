@@ -264,8 +264,9 @@ class PhiVariant:
         return D
 
 
-def featuremap_variant(X, v: PhiVariant, out_dtype=None):
-    """The variant map of every row of X [B, H, n, d]; returns [B, H, n, D]."""
+def featuremap_variant(X, v: PhiVariant, out_dtype=None, out=None):
+    """The variant map of every row of X [B, H, n, d]; returns [B, H, n, D] (into out
+    when given: a contiguous tensor of that shape)."""
     torch = _torch()
     lib = load_library()
     if X.dim() != 4 or not X.is_contiguous():
@@ -275,7 +276,10 @@ def featuremap_variant(X, v: PhiVariant, out_dtype=None):
     D = int(lib.luna_phi_variant_features(ctypes.byref(vc)))
     if D < 0:
         raise LunaError(LUNA_ERR_INVALID_ARG, lib.luna_last_error().decode())
-    out = torch.empty((B, H, n, D), dtype=X.dtype if out_dtype is None else out_dtype, device=X.device)
+    if out is None:
+        out = torch.empty((B, H, n, D), dtype=X.dtype if out_dtype is None else out_dtype, device=X.device)
+    elif tuple(out.shape) != (B, H, n, D) or not out.is_contiguous():
+        raise LunaError(LUNA_ERR_INVALID_ARG, f"out must be a contiguous [{B}, {H}, {n}, {D}] tensor")
     nb = int(lib.luna_featuremap_variant_workspace_bytes(_dt(X), B, H, n, d, ctypes.byref(vc)))
     ws, wsp, wsn = _workspace(nb, X.device)
     _check(lib.luna_featuremap_variant(X.data_ptr(), _dt(X), B, H, n, d, ctypes.byref(vc), out.data_ptr(), _dt(out),

@@ -171,3 +171,37 @@ def make_params(w: Workload, seed: int = 0) -> dict:
     p.update(M=w.M, L=w.L, hidden=w.hidden, shared_channels=w.shared_channels,
              nonneg=w.nonneg, per_head=w.per_head)
     return p
+
+
+def make_variant_params(kind: str, M: int, d: int, L: int = 8, hidden: int = 64, act: str = "relu",
+                        shared: bool = False, env: bool = False, bank: bool = False, ch_rms: bool = False,
+                        seed: int = 0) -> dict:
+    """Parameters of a feature-map variant, as the variant calls take them.  Random
+    Fourier features: W rows N(0, I/d), phases b uniform in [0, 2 pi).  Performer:
+    W = omega / d^(1/4) with omega ~ N(0, I), b = 0.  Channel MLPs: every element
+    N(0, 1/d) as in make_params, an envelope G x + c with G N(0, 1/d) and c N(0, 1),
+    bank coefficients N(0, 1), channel RMS target 0.1."""
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 2000]))
+    s = 1.0 / np.sqrt(d)
+    p = {"kind": kind, "act": act, "M": M}
+    if kind == "performer":
+        p.update(W=(rng.standard_normal((M, d)) / d ** 0.25).astype(np.float32), b=np.zeros(M, np.float32))
+        return p
+    if kind in ("rff_cos", "rff_sincos"):
+        p.update(W=(rng.standard_normal((M, d)) * s).astype(np.float32),
+                 b=rng.uniform(0.0, 2.0 * np.pi, M).astype(np.float32))
+        return p
+    C1 = 1 if shared else L
+
+    def draw(*shape):
+        return (rng.standard_normal(shape) * s).astype(np.float32)
+
+    p.update(W=draw(M, d), b=draw(M), fc1_w=draw(C1, hidden), fc1_b=draw(C1, hidden), fc2_w=draw(L, hidden),
+             fc2_b=draw(L), L=L, hidden=hidden, nonneg=True, shared_channels=shared)
+    if env:
+        p.update(env_w=draw(L, d), env_b=rng.standard_normal(L).astype(np.float32))
+    if bank:
+        p["bank"] = rng.standard_normal(L).astype(np.float32)
+    if ch_rms:
+        p.update(ch_rms=True, ch_rms_target=0.1)
+    return p

@@ -683,6 +683,20 @@ def configs_bench(args) -> int:
 
 
 VALU_LANE_OPS = 78.6e12  # fp32 vector FMA lane-operations per second (157.3 TFLOP/s / 2)
+# VALU issue slots of a channel-MLP hidden unit beyond its two multiply-adds and a relu,
+# as the kernels evaluate the activations, a transcendental (exp2, rcp) counted as four
+# slots (quarter rate): silu z rcp(1 + 2^(-z log2 e)) and tanh 1 - 2 rcp(2^(2z log2 e) + 1)
+# take 3 + 2 x 4 more; gelu (erf by Abramowitz and Stegun 7.1.26) 12 + 2 x 4 more.
+ACT_EXTRA_SLOTS = {"relu": 0, "silu": 10, "tanh": 10, "gelu": 20}
+
+
+def mlp_slots_per_unit(act: str, shared: bool, L: int) -> float:
+    """VALU issue slots per (projection, channel, hidden unit) of a channel MLP: the
+    first layer's multiply-add, the activation and the second layer's multiply-add; with
+    a shared first layer the first two are paid once for the L channels."""
+    if shared:
+        return (2 + ACT_EXTRA_SLOTS[act] + L) / L
+    return 3 + ACT_EXTRA_SLOTS[act]
 # (label, kind, act, M, L, options) of the variant report, on the long encoder problem's
 # queries; every map has D = 128 features per row except Bank+Coef (D = M = 16)
 VARIANT_CASES = [
@@ -723,10 +737,9 @@ def variants_bench(args) -> int:
     queries (B=32, H=8, n=4096, d=64, bf16 in and out), and attention from given
     features (luna_attn_fwd_features) at the two long problems' shapes.  One JSON line
     per case: median call time (HIP events, caches flushed before every call), the HBM
-    floor of the algorithmic bytes (read x, write phi; channel RMS reads x twice) and,
-    for the channel MLPs, the VALU floor of their hidden units at three fp32 lane
-    operations each (the multiply-add into the unit, a relu, the multiply-add into the
-    channel: the cheapest unit; smooth activations cost more)."""
+    floor of the algorithmic bytes (read x, write phi; channel RMS also writes and reads
+    y in fp32 between its passes) and, for the channel MLPs, the VALU floor of their
+    hidden units (mlp_slots_per_unit issue slots each at 78.6e12 lane slots/s)."""
     import torch
 
     from paper_2512_08061_amd import luna
@@ -754,11 +767,10 @@ def variants_bench(args) -> int:
         out = torch.empty((w.B, w.H, w.n, D), dtype=torch.bfloat16, device=dev)
         fn = lambda: luna.featuremap_variant(x, v, out=out)  # noqa: E731
         ms, p10, p90 = _timed_calls(fn, args.steps, args.warmup, stream, flush, sink)
-        reads = 2 if opts.get("ch_rms") else 1
-        nbytes = rows * (reads * w.d + D) * 2
+        nbytes = rows * (w.d + D) * 2 + (rows * M * L * 4 * 2 if opts.get("ch_rms") else 0)
         t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
         units = rows * M * L * p.get("hidden", 0) if kind == "mlp" else 0
-        t_alu = reads * 3 * units / VALU_LANE_OPS
+        t_alu = units * mlp_slots_per_unit(act, bool(opts.get("shared")), L) / VALU_LANE_OPS if units else 0.0
         bound, floor = ("alu", t_alu) if t_alu > t_hbm else ("hbm", t_hbm)
         rec = {"case": label, "kind": kind, "act": act, "M": M, "L": L, "D": D, "options": opts,
                "workload": "long encoder queries B=32 H=8 n=4096 d=64, bf16 in and out",
@@ -813,9 +825,12 @@ def variants_bench(args) -> int:
             fh.write("One ABI call per timing, median of the timed calls with the 10th and 90th percentiles, HIP "
                      "events on the launch stream, caches flushed by a 1 GiB read before every call. Maps: the long "
                      "encoder problem's queries (1,048,576 rows, d = 64), bf16 in and out; the HBM floor is reading x "
-                     "(twice with channel RMS) and writing phi at 8 TB/s; the ALU floor of a channel MLP is its hidden "
-                     "units at 3 fp32 lane operations each (the relu unit) at 78.6e12 lane operations/s. Attention "
-                     "from features: read both feature matrices and V, write out.\n\n")
+                     "and writing phi at 8 TB/s (channel RMS: also y in fp32 written and read back); the ALU floor of "
+                     "a channel MLP is its hidden units at 78.6e12 VALU lane slots/s, a unit costing its two "
+                     "multiply-adds and its activation (relu 1 slot; silu and tanh 3 + two transcendentals, gelu 12 + "
+                     "two, a transcendental counted as 4 slots; with a shared first layer the first multiply-add and "
+                     "the activation are paid once for the L channels). Attention from features: read both feature "
+                     "matrices and V, write out.\n\n")
             fh.write("| case | D | median us (p10-p90) | rows/s or tokens/s | GB/s | hidden units/s | floor us | "
                      "roofline |\n|---|---|---|---|---|---|---|---|\n")
             for r in rows_out:

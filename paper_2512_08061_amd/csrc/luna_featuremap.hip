@@ -154,23 +154,20 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   }
 }
 
-// Workgroups of `kernel` that the device holds at once (computed once per kernel).
-template <typename Kern>
-static int fm_resident(Kern kernel) {
-  static const int resident = [&]() {
+// As many workgroups as the device holds at once (registers and LDS table permitting),
+// queried once per kernel (the kernel is a template argument, so that every kernel
+// has its own cached count); more items loop, so that no second round of workgroups
+// starts late.
+template <auto Kernel>
+static void fm_launch(int64_t items, const FeatureMapArgs& a, hipStream_t s) {
+  static const int resident = []() {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess || per_cu < 1) per_cu = 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, 256, 0) != hipSuccess || per_cu < 1) per_cu = 1;
     if (hipGetDevice(&dev) != hipSuccess) dev = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
     return per_cu * cus;
   }();
-  return resident;
-}
-
-template <typename Kern>
-static void fm_launch(Kern kernel, int64_t items, const FeatureMapArgs& a, hipStream_t s) {
-  const int64_t res = fm_resident(kernel);
-  hipLaunchKernelGGL(kernel, dim3((unsigned)(items < res ? items : res)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(Kernel, dim3((unsigned)(items < resident ? items : resident)), dim3(256), 0, s, a);
 }
 
 template <typename Tin, typename Tout, int DH>
@@ -178,11 +175,9 @@ static hipError_t fm_dispatch_L(int L, const FeatureMapArgs& a, hipStream_t s) {
   const int64_t tiles = (a.rows_per_head + 63) / 64;
   const int64_t items = a.heads * tiles * (a.X2 != nullptr ? 2 : 1);
   const bool hold = a.phi.M <= 64;  // at most four 16-projection blocks
-  // as many workgroups as can be resident at once (registers and LDS table permitting);
-  // more items loop, so that no second round of workgroups starts late
 #define LUNA_FM_LAUNCH(L_)                                                                  \
-  if (hold) fm_launch(featuremap_kernel<Tin, Tout, DH, L_, true>, items, a, s);             \
-  else fm_launch(featuremap_kernel<Tin, Tout, DH, L_, false>, items, a, s);
+  if (hold) fm_launch<featuremap_kernel<Tin, Tout, DH, L_, true>>(items, a, s);             \
+  else fm_launch<featuremap_kernel<Tin, Tout, DH, L_, false>>(items, a, s);
   switch (L) {
     case 1: LUNA_FM_LAUNCH(1) break;
     case 2: LUNA_FM_LAUNCH(2) break;

@@ -4,3 +4,4 @@ GPU library."""
 from .luna_oracle import *  # noqa: F401,F403
 from . import luna_oracle  # noqa: F401
 from . import luna_variants  # noqa: F401
+from . import luna_distill  # noqa: F401

@@ -455,3 +455,109 @@ def test_variant_mutation_is_caught(name, monkeypatch):
         except Exception:
             failed.append(pin.__name__)
     assert failed, f"no pin catches the planted mistake {name}"
+
+
+# ---------------------------------------------------------------------------
+# distillation oracle
+# ---------------------------------------------------------------------------
+import oracle_distill_pins  # noqa: E402
+from oracle import luna_distill as DIS  # noqa: E402
+
+_dorig = {k: getattr(DIS, k) for k in ("teacher", "student", "distill_feature_grads", "distill_backward")}
+
+
+def _teacher_mut(kind):
+    def teacher(Q, K, causal=False):
+        Q, K = np.asarray(Q, float), np.asarray(K, float)
+        n, d = Q.shape[-2], Q.shape[-1]
+        logits = Q @ np.swapaxes(K, -1, -2)
+        if kind != "no_scale":
+            logits = logits / math.sqrt(d)
+        vis = np.tril(np.ones((n, n), bool)) if (causal and kind != "no_mask") else np.ones((n, n), bool)
+        logits = np.where(vis, logits, -np.inf)
+        e = np.where(vis, np.exp(logits - logits.max(-1, keepdims=True)), 0.0)
+        return e / e.sum(-1, keepdims=True)
+    return teacher
+
+
+def _student_mut(kind):
+    def student(phiQ, phiK, causal=False, eps=1e-6):
+        phiQ, phiK = np.asarray(phiQ, float), np.asarray(phiK, float)
+        n = phiQ.shape[-2]
+        vis = np.tril(np.ones((n, n), bool)) if causal else np.ones((n, n), bool)
+        P = phiQ @ np.swapaxes(phiK, -1, -2)
+        den = (P if kind == "den_all_keys" else np.where(vis, P, 0.0)).sum(-1, keepdims=True)
+        P = np.where(vis, P, 0.0)
+        nt = vis.sum(-1, keepdims=True).astype(float)
+        smooth = eps if kind == "eps_not_over_nt" else eps / nt
+        return np.where(vis, (P + smooth) / (den + eps), 0.0)
+    return student
+
+
+def _dgrad_mut(kind):
+    def distill_feature_grads(Q, K, phiQ, phiK, causal=False, eps=1e-6):
+        gq, gk = _dorig["distill_feature_grads"](Q, K, phiQ, phiK, causal, eps)
+        phiQ, phiK = np.asarray(phiQ, float), np.asarray(phiK, float)
+        if kind == "sign":
+            return -gq, -gk
+        if kind == "sum_not_mean":
+            rows = float(np.prod(np.shape(phiQ)[:-1]))
+            return gq * rows, gk * rows
+        if kind == "k_untransposed":  # dphi(K) = G phi(Q) instead of G^T phi(Q)
+            A = DIS.teacher(Q, K, causal)
+            n = A.shape[-1]
+            vis = np.tril(np.ones((n, n), bool)) if causal else np.ones((n, n), bool)
+            P = np.where(vis, phiQ @ np.swapaxes(phiK, -1, -2), 0.0)
+            den = P.sum(-1, keepdims=True)
+            nt = vis.sum(-1, keepdims=True).astype(float)
+            G = np.where(vis, (1.0 / (den + eps) - A / (P + eps / nt)) / float(np.prod(A.shape[:-1])), 0.0)
+            return gq, G @ phiQ
+        if kind == "no_den_term":
+            A = DIS.teacher(Q, K, causal)
+            n = A.shape[-1]
+            vis = np.tril(np.ones((n, n), bool)) if causal else np.ones((n, n), bool)
+            P = np.where(vis, phiQ @ np.swapaxes(phiK, -1, -2), 0.0)
+            nt = vis.sum(-1, keepdims=True).astype(float)
+            G = np.where(vis, (-A / (P + eps / nt)) / float(np.prod(A.shape[:-1])), 0.0)
+            return G @ phiK, np.swapaxes(G, -1, -2) @ phiQ
+        return gq, gk
+    return distill_feature_grads
+
+
+def _dback_mut(kind):
+    def distill_backward(Q, K, p, causal=False, eps=1e-6):
+        phiQ, phiK = O.featuremap(Q, p), O.featuremap(K, p)
+        rows = DIS.distill_rows_features(Q, K, phiQ, phiK, causal, eps)
+        dq, dk = DIS.distill_feature_grads(Q, K, phiQ, phiK, causal, eps)
+        _, gq = O.featuremap_backward(Q, p, dq)
+        _, gk = O.featuremap_backward(K, p, dk)
+        if kind == "queries_only":
+            return rows, gq
+        return rows, {k: gq[k] + gk[k] for k in O.PARAM_NAMES}
+    return distill_backward
+
+
+DISTILL_MUTATIONS = {
+    "teacher_without_scale": ("teacher", _teacher_mut("no_scale")),
+    "teacher_without_causal_mask": ("teacher", _teacher_mut("no_mask")),
+    "student_den_over_all_keys": ("student", _student_mut("den_all_keys")),
+    "student_eps_not_over_nt": ("student", _student_mut("eps_not_over_nt")),
+    "grads_sign": ("distill_feature_grads", _dgrad_mut("sign")),
+    "grads_sum_not_mean": ("distill_feature_grads", _dgrad_mut("sum_not_mean")),
+    "grads_key_side_untransposed": ("distill_feature_grads", _dgrad_mut("k_untransposed")),
+    "grads_without_den_term": ("distill_feature_grads", _dgrad_mut("no_den_term")),
+    "backward_queries_only": ("distill_backward", _dback_mut("queries_only")),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DISTILL_MUTATIONS))
+def test_distill_mutation_is_caught(name, monkeypatch):
+    attr, fn = DISTILL_MUTATIONS[name]
+    monkeypatch.setattr(DIS, attr, fn)
+    failed = []
+    for pin in oracle_distill_pins.ALL_PINS:
+        try:
+            pin(DIS)
+        except Exception:
+            failed.append(pin.__name__)
+    assert failed, f"no pin catches the planted mistake {name}"

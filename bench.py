@@ -845,6 +845,64 @@ def variants_bench(args) -> int:
     return 0
 
 
+def distill_bench(args) -> int:
+    """luna_distill (attention-distillation loss, with and without the feature-map
+    parameter gradients) on the long encoder problem (non-causal) and the long causal
+    problem: HIP events around each call.  The algorithmic work is the matrix-core
+    products the loss needs once, S = Q K^T and P = phi(Q) phi(K)^T (2 (d + D) flops per
+    visible (query, key) pair), plus the two gradient products G phi(K) and G^T phi(Q)
+    (4 D per pair) with the gradients; the kernels compute S and P twice or three times
+    (the softmax statistics first) and split G into two bf16 parts."""
+    import torch
+
+    from paper_2512_08061_amd import luna
+    from paper_2512_08061_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    luna.load_library()
+    stream = torch.cuda.current_stream(dev)
+    for name, causal in (("long_noncausal", False), ("long_causal", True)):
+        w = wl.WORKLOADS[name]
+        Q, K, _ = wl.make_inputs(w, args.seed)
+        p = wl.make_params(w, args.seed)
+        q = torch.from_numpy(Q).to(dev).to(torch.bfloat16).contiguous()
+        k = torch.from_numpy(K).to(dev).to(torch.bfloat16).contiguous()
+        del Q, K
+        pt = luna.PhiParams.from_arrays(p, dev, torch.bfloat16)
+        D = w.M * w.L
+        pairs = w.B * w.H * (w.n * (w.n + 1) // 2 if causal else w.n * w.n)
+        for grads in (False, True):
+            fn = lambda: luna.distill(q, k, pt, causal=causal, param_grads=grads)  # noqa: E731
+            for _ in range(max(1, args.warmup // 10)):
+                fn()
+            torch.cuda.synchronize()
+            steps = max(1, args.steps // 10)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+            for e0, e1 in ev:
+                e0.record(stream)
+                fn()
+                e1.record(stream)
+            torch.cuda.synchronize()
+            ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[steps // 2]
+            flops = pairs * (2 * (w.d + D) + (4 * D if grads else 0))
+            tf = flops / (ms * 1e-3) / 1e12
+            line = {
+                "metric": "LUNA attention-distillation rows/sec (luna_distill)", "value": w.B * w.H * w.n / (ms * 1e-3),
+                "unit": "rows/s", "n_gpus": 1, "steps": steps, "ms_per_step": round(ms, 4), "higher_is_better": True,
+                "dtype": "bf16", "data": "synthetic (seeded)",
+                "config": {"workload": f"{name} B={w.B} H={w.H} n={w.n} d={w.d} M={w.M} x L={w.L} (D={D})",
+                           "causal": causal, "param_grads": grads},
+                "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                             "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "algorithmic_tflop": round(flops / 1e12, 3)},
+            }
+            log(f"{name} grads={grads}: {ms:.3f} ms, {tf:.1f} TFLOP/s")
+            print(json.dumps(line), flush=True)
+        del q, k
+        torch.cuda.synchronize()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -889,6 +947,9 @@ def main() -> int:
                          "problem's queries and attention from given features, one JSON line per case")
     ap.add_argument("--variants-table", default="", metavar="PATH",
                     help="with --variants: also write the results as a markdown table to PATH")
+    ap.add_argument("--distill", action="store_true",
+                    help="instead of the hot-path step: time luna_distill (loss, and loss with parameter gradients) "
+                         "on the two long problems")
     ap.add_argument("--variants-only", default="", metavar="NAMES",
                     help="with --variants: comma-separated case labels to run (default: all)")
     args = ap.parse_args()
@@ -896,7 +957,8 @@ def main() -> int:
         return traffic_from(*args.traffic_from, args.traffic_command)
     if args.counters_from:
         return counters_from(args.counters_from, args.counters_command)
-    if args.gpus != 1 and (args.decode or args.configs or args.featuremap or args.backward or args.variants):
+    if args.gpus != 1 and (args.decode or args.configs or args.featuremap or args.backward or args.variants
+                           or args.distill):
         print("bench.py runs on one GPU only; use --gpus 1.", file=sys.stderr)
         return 2
     if args.decode:
@@ -909,6 +971,8 @@ def main() -> int:
         return configs_bench(args)
     if args.variants:
         return variants_bench(args)
+    if args.distill:
+        return distill_bench(args)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: LUNA attention shards over (batch, head) with no "

@@ -263,6 +263,34 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
                           const luna_phi_grads* grads, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * Attention distillation, the first stage of the conversion recipe (Implementation
+ * Details appendix: every pretrained weight frozen, the feature map trained so that
+ * LUNA's attention distribution matches the teacher's softmax attention, eq. (1) of
+ * Section 2).  Per query row t, over the keys s that t sees (all, or s <= t when
+ * causal = 1; n_t of them):
+ *   teacher  A_ts = softmax_s(q_t . k_s / sqrt(d))
+ *   student  Ahat_ts = (P_ts + eps/n_t) / (den_t + eps), P = phi(Q) phi(K)^T,
+ *            den_t = sum_s P_ts: LUNA's weights of eq. (9) of Section 3.1, smoothed
+ *            into an exact distribution (a key with P_ts = 0 keeps a finite loss)
+ *   row_loss[b][h][t] = -sum_s A_ts log Ahat_ts  (fp32, device memory, [B][H][n];
+ *            the soft cross-entropy: KL(A_t || Ahat_t) plus the teacher's entropy)
+ * and, if grads is not NULL, the gradients of the mean of row_loss over the B H n rows
+ * with respect to every feature-map parameter (overwritten; the teacher is a fixed
+ * target, Q and K get no gradient).  phi is eq. (11) of Section 3.2 (Listing 1's
+ * channel MLPs) with the parameters p; eps >= 0 (with eps = 0 a visible key with
+ * P_ts = 0 gives an infinite loss).  Q, K: [B, H, n, d] in dtype.  Nothing of size
+ * n x n is stored: the work is quadratic in n, the memory linear.  bf16 calls take the
+ * features and the products in bf16 with fp32 accumulation; fp32 calls compute in fp32.
+ * Supported: d in {32, 64, 128}; D = M L in {64, 128, 256} (bf16) or {64, 128} (fp32);
+ * the feature-map and, for grads, the backward pass's limits on (d, L, M).
+ */
+size_t luna_distill_workspace_bytes(luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                                    const luna_phi_params* p, int32_t param_grads);
+luna_status luna_distill(const void* Q, const void* K, luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                         const luna_phi_params* p, int32_t causal, float eps, float* row_loss,
+                         const luna_phi_grads* grads, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Feature-map variants.  The map of eq. (11) of Section 3.2 is a template, phi(x) =
  * h(x)/sqrt(M) [psi_l(w_i . x + b_i)]; fixing h and psi by hand gives the random-feature
  * maps of Section 3.1, and the kernel ablation of Section 5.4 (Table 5) changes its

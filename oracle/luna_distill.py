@@ -102,3 +102,19 @@ def distill_backward(Q, K, p, causal=False, eps=1e-6):
     _, gq = featuremap_backward(Q, p, dphiQ)
     _, gk = featuremap_backward(K, p, dphiK)
     return rows, {k: gq[k] + gk[k] for k in PARAM_NAMES}
+
+
+def distill_rows_at(Q, K, phiQ, phiK, rows, causal=False, eps=1e-6):
+    """CE_t for the listed rows t of one head (Q, K [n, d], features [n, D]), each from
+    its own teacher and student rows: O(n) per row, for sampled rows of long sequences."""
+    Q, K, phiQ, phiK = _f64(Q), _f64(K), _f64(phiQ), _f64(phiK)
+    n, d = Q.shape
+    out = np.empty(len(rows))
+    for i, t in enumerate(rows):
+        nt = t + 1 if causal else n
+        logits = K[:nt] @ Q[t] / math.sqrt(d)
+        A = np.exp(logits - logits.max())
+        A /= A.sum()
+        P = phiK[:nt] @ phiQ[t]
+        out[i] = -(A * np.log((P + eps / nt) / (P.sum() + eps))).sum()
+    return out

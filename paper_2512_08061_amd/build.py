@@ -21,7 +21,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libluna.so")
 
 SOURCES = ["luna_prepare.hip", "luna_featuremap.hip", "luna_noncausal.hip", "luna_causal.hip", "luna_stream.hip",
-           "luna_variants.hip", "luna_variants_bf16.hip",
+           "luna_variants.hip", "luna_variants_bf16.hip", "luna_distill.hip",
            "luna_backward.hip", "luna_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -58,7 +58,7 @@ luna_status check_common(const Problem& pb) {
   if (units > luna::kMaxUnits) return fail(LUNA_ERR_UNSUPPORTED, "L*hidden must be <= 1023 (breakpoint table)");
   // the feature-map kernel (also the first stage of a streaming step) has the larger LDS table
   const bool fm_table = pb.op == LUNA_OP_FEATUREMAP || pb.op == LUNA_OP_CAUSAL_STEP || pb.op == LUNA_OP_ATTN_BWD ||
-                        pb.op == LUNA_OP_ATTN_CAUSAL_BWD;
+                        pb.op == LUNA_OP_ATTN_CAUSAL_BWD || pb.op >= 100;
   const int seg_cap = luna::nseg_cap(p->L, fm_table ? luna::kFmSegBytes : luna::kAttnSegBytes);
   if (units + 2 > seg_cap) return fail(LUNA_ERR_UNSUPPORTED, "too many breakpoints for the LDS segment table");
   if ((units + 1) * p->L > luna::kSegCap || (size_t)(units + 1) * luna::seg16_row_bytes(p->L) > luna::kSeg16Bytes)
@@ -76,6 +76,7 @@ struct Layout {
   size_t vx = 0, y = 0, sx = 0, dsx = 0, pm = 0, rm = 0, dphiq = 0, dphik = 0, dvtmp = 0;
   size_t xq = 0, xk = 0, wx = 0, uq = 0, uk = 0, duq = 0, duk = 0, dwh = 0;  // feature-map backward
   size_t bpart = 0, sum = 0, pre = 0;
+  size_t dstats = 0;  // distillation: per query row the softmax max and sum and the kernel row sum
   int chunk = 0, nch = 1, groups = 0, part_floats = 0;
   int splits = 1, tokens_per_split = 0, tile_tokens = 256, tiles = 1, fused = 0;
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
@@ -147,6 +148,36 @@ void plan_splits(const Problem& pb, int64_t heads, Layout* lay) {
   splits = (pb.n + tps - 1) / tps;
   lay->splits = (int)splits;
   lay->tokens_per_split = (int)tps;
+}
+
+// Private operation codes of the distillation loss (without and with the feature-map
+// parameter gradients).
+constexpr int kOpDistill = 100, kOpDistillGrads = 101;
+
+// Buffers of the feature-map backward (enqueue_phi_backward): [x | 1] of the queries
+// and keys, [W | b], the projections and their gradients, per-(batch, head) [dW | db],
+// the per-workgroup parameter partials, their fp64 sums and moment prefixes.
+void plan_phi_backward(const Problem& pb, Layout* lay, size_t* off) {
+  const int d = (int)pb.d, L = pb.p->L, M = pb.p->M, P = param_sets(pb);
+  const int64_t heads = pb.B * pb.H;
+  const size_t rows = (size_t)heads * (size_t)pb.n;
+  auto take = [&](size_t& at, size_t bytes) {
+    at = *off;
+    *off = align256(*off + bytes);
+  };
+  take(lay->xq, rows * (d + 1) * 4);
+  take(lay->xk, rows * (d + 1) * 4);
+  take(lay->wx, (size_t)P * M * (d + 1) * 4);
+  take(lay->uq, rows * M * 4);
+  take(lay->uk, rows * M * 4);
+  take(lay->duq, rows * M * 4);
+  take(lay->duk, rows * M * 4);
+  take(lay->dwh, (size_t)heads * M * (d + 1) * 4);
+  lay->groups = luna::bwd_phi_groups(2 * pb.n * (heads / P) * M);
+  lay->part_floats = (int)luna::bwd_part_floats(d, L, M);
+  take(lay->bpart, (size_t)P * lay->groups * lay->part_floats * 4);
+  take(lay->sum, (size_t)P * lay->part_floats * 8);
+  take(lay->pre, (size_t)P * L * (luna::bwd_nseg_cap(L) + 1) * 2 * 8);
 }
 
 luna_status plan(const Problem& pb, Layout* lay) {
@@ -258,19 +289,27 @@ luna_status plan(const Problem& pb, Layout* lay) {
     take(lay->dphiq, rows * D * 4);
     take(lay->dphik, rows * D * 4);
     if (pb.dt == LUNA_BF16) take(lay->dvtmp, rows * d * 4);
-    take(lay->xq, rows * (d + 1) * 4);
-    take(lay->xk, rows * (d + 1) * 4);
-    take(lay->wx, (size_t)P * M * (d + 1) * 4);
-    take(lay->uq, rows * M * 4);
-    take(lay->uk, rows * M * 4);
-    take(lay->duq, rows * M * 4);
-    take(lay->duk, rows * M * 4);
-    take(lay->dwh, (size_t)heads * M * (d + 1) * 4);
-    lay->groups = luna::bwd_phi_groups(2 * pb.n * (heads / P) * M);
-    lay->part_floats = (int)luna::bwd_part_floats(d, L, M);
-    take(lay->bpart, (size_t)P * lay->groups * lay->part_floats * 4);
-    take(lay->sum, (size_t)P * lay->part_floats * 8);
-    take(lay->pre, (size_t)P * L * (luna::bwd_nseg_cap(L) + 1) * 2 * 8);
+    plan_phi_backward(pb, lay, &off);
+  } else if (pb.op == kOpDistill || pb.op == kOpDistillGrads) {
+    const int D = M * L;
+    if (!luna::distill_supported(dt, d, D) || !luna::featuremap_supported(dt, d, L, M))
+      return fail(LUNA_ERR_UNSUPPORTED, "no distillation kernels for this (dtype, d, M*L)");
+    const size_t rows = (size_t)heads * (size_t)pb.n;
+    auto take = [&](size_t& at, size_t bytes) {
+      at = off;
+      off = align256(off + bytes);
+    };
+    take(lay->phiq, rows * D * (pb.dt == LUNA_BF16 ? 2 : 4));  // features in the call's dtype
+    take(lay->phik, rows * D * (pb.dt == LUNA_BF16 ? 2 : 4));
+    take(lay->dstats, rows * 4 * sizeof(float));
+    if (pb.op == kOpDistillGrads) {
+      if (!luna::bwd_supported(d, L, M)) return fail(LUNA_ERR_UNSUPPORTED, "no backward kernels for this (d, L, M)");
+      if (param_sets(pb) > 65535 || pb.H > 65535)
+        return fail(LUNA_ERR_UNSUPPORTED, "at most 65535 heads and parameter sets in the backward pass");
+      take(lay->dphiq, rows * D * 4);
+      take(lay->dphik, rows * D * 4);
+      plan_phi_backward(pb, lay, &off);
+    }
   } else {
     return fail(LUNA_ERR_INVALID_ARG, "unknown operation code");
   }
@@ -504,6 +543,116 @@ luna_status plan_features(luna_dtype phi_dtype, luna_dtype dtype, int64_t B, int
     if (st != LUNA_OK) return st;
   }
   lay->total = off;
+  return LUNA_OK;
+}
+
+// Through the feature map, from dphi(Q) and dphi(K) in the workspace (fp32, [head][n][D]):
+// u = [x | 1] [W | b]^T (GEMM), du from dphi on the tables, [dW | db] = du^T [x | 1]
+// and the channel-MLP gradients into grads (when given), dx = du [W | b] into dQ, dK
+// (when given).  Used by the backward pass and by the distillation loss.
+luna_status enqueue_phi_backward(const Problem& pb, uint8_t* w, const Layout& lay, const void* Q, const void* K,
+                                 void* dQ, void* dK, const luna_phi_grads* grads, hipStream_t s) {
+  const luna_phi_params* p = pb.p;
+  const luna::Dt dt = pb.dt == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int64_t B = pb.B, H = pb.H, n = pb.n;
+  const int M = p->M, L = p->L, dd = (int)pb.d, E = dd + 1;
+  const int heads = (int)(B * H);
+  const int64_t nE = n * E;
+  float* dphiq = reinterpret_cast<float*>(w + lay.dphiq);
+  float* dphik = reinterpret_cast<float*>(w + lay.dphik);
+  hipError_t e;
+#define LUNA_TRY(expr, what) \
+  if ((e = (expr)) != hipSuccess) return hip_fail(e, what)
+  const int P = param_sets(pb);
+  const int Hh = (int)H, Bb = (int)B;
+  float* xq = reinterpret_cast<float*>(w + lay.xq);
+  float* xk = reinterpret_cast<float*>(w + lay.xk);
+  float* wx = reinterpret_cast<float*>(w + lay.wx);
+  float* uq = reinterpret_cast<float*>(w + lay.uq);
+  float* uk = reinterpret_cast<float*>(w + lay.uk);
+  float* duq = reinterpret_cast<float*>(w + lay.duq);
+  float* duk = reinterpret_cast<float*>(w + lay.duk);
+  float* dwh = reinterpret_cast<float*>(w + lay.dwh);
+  LUNA_TRY(luna::launch_bwd_pack(dt, Q, xq, (int64_t)heads * n, dd, s), "pack kernel launch");
+  LUNA_TRY(luna::launch_bwd_pack(dt, K, xk, (int64_t)heads * n, dd, s), "pack kernel launch");
+  LUNA_TRY(luna::launch_bwd_packw(dt, p->W, p->b, wx, P * M, dd, s), "pack kernel launch");
+  // products over (batch, head) pairs: the batch index is the GEMM's head, the head its
+  // chunk, so that per-head parameters are addressed by stride
+  const int64_t wsc = p->per_head ? (int64_t)M * E : 0;
+  auto gemm_bh = [&](const float* A, int64_t ah, int64_t ac, int64_t ai, int64_t ak, const float* Bm, int64_t bh,
+                     int64_t bc, int64_t bk, int64_t bj, float* Cm, int64_t ch, int64_t c2, int64_t ci, int64_t cj, int Mm,
+                     int Nn, int Kk, int acc) {
+    luna::BwdGemm g{};
+    g.A = A; g.sAh = ah; g.sAc = ac; g.sAi = ai; g.sAk = ak;
+    g.B = Bm; g.sBh = bh; g.sBc = bc; g.sBk = bk; g.sBj = bj;
+    g.C = Cm; g.sCh = ch; g.sCc = c2; g.sCi = ci; g.sCj = cj;
+    g.M = Mm; g.N = Nn; g.K = Kk;
+    g.heads = Bb; g.chunks = Hh; g.chunk = (int)n; g.seq = (int)n;
+    g.accumulate = acc;
+    return luna::launch_bwd_gemm(g, s);
+  };
+  const int64_t nM = n * M, ME = (int64_t)M * E;
+  for (int side = 0; side < 2; ++side) {
+    const float* x = side ? xk : xq;
+    float* u = side ? uk : uq;
+    LUNA_TRY(gemm_bh(x, Hh * nE, nE, E, 1, wx, 0, wsc, 1, E, u, Hh * nM, nM, M, 1, (int)n, M, E, 0), "projection GEMM");
+  }
+  luna::BwdPhi ph{};
+  ph.uq = uq;
+  ph.uk = uk;
+  ph.dphiq = dphiq;
+  ph.dphik = dphik;
+  ph.duq = duq;
+  ph.duk = duk;
+  ph.tables = w + lay.tables;
+  ph.partial = reinterpret_cast<float*>(w + lay.bpart);
+  ph.n = n;
+  ph.heads = B * H;
+  ph.H = Hh;
+  ph.M = M;
+  ph.per_head = p->per_head;
+  ph.part_floats = lay.part_floats;
+  LUNA_TRY(luna::launch_bwd_phi(L, ph, lay.groups, P, s), "feature-map backward kernel launch");
+  for (int side = 0; side < 2; ++side) {
+    float* x = side ? xk : xq;
+    const float* du = side ? duk : duq;
+    if (grads)  // [dW | db] per (batch, head), both sides added
+      LUNA_TRY(gemm_bh(du, Hh * nM, nM, 1, M, x, Hh * nE, nE, E, 1, dwh, Hh * ME, ME, E, 1, M, E, (int)n, side),
+               "weight-gradient GEMM");
+    // dx = du [W | b] into x's rows (x is not read again), then its first d columns
+    void* dx = side ? dK : dQ;
+    if (dx == nullptr) continue;
+    LUNA_TRY(gemm_bh(du, Hh * nM, nM, M, 1, wx, 0, wsc, E, 1, x, Hh * nE, nE, E, 1, (int)n, E, M, 0), "dx GEMM");
+    LUNA_TRY(luna::launch_bwd_cols(dt, x, dx, (int64_t)heads * n, dd, s), "dx convert");
+  }
+  if (grads) {
+    LUNA_TRY(luna::launch_bwd_dw(dwh, grads->W, grads->b, Bb, Hh, M, dd, p->per_head, s), "weight-gradient sum");
+    const int units = (p->shared_channels ? 1 : L) * p->hidden;
+    const int used = 2 * (units + 1) * L;
+    double* sum = reinterpret_cast<double*>(w + lay.sum);
+    double* pre = reinterpret_cast<double*>(w + lay.pre);
+    LUNA_TRY(luna::launch_bwd_reduce(ph.partial, sum, lay.groups, lay.part_floats, used, P, s), "reduce kernel launch");
+    LUNA_TRY(luna::launch_bwd_prefix(sum, pre, w + lay.tables, M, dd, L, lay.part_floats, luna::bwd_nseg_cap(L), P, s),
+             "prefix kernel launch");
+    luna::BwdMlp m{};
+    m.sum = sum;
+    m.pre = pre;
+    m.tables = w + lay.tables;
+    m.fc1_w = p->fc1_w;
+    m.fc1_b = p->fc1_b;
+    m.fc2_w = p->fc2_w;
+    m.dfc1_w = grads->fc1_w;
+    m.dfc1_b = grads->fc1_b;
+    m.dfc2_w = grads->fc2_w;
+    m.dfc2_b = grads->fc2_b;
+    m.L = L;
+    m.hidden = p->hidden;
+    m.C1 = p->shared_channels ? 1 : L;
+    m.part_floats = lay.part_floats;
+    m.nseg_cap = luna::bwd_nseg_cap(L);
+    LUNA_TRY(luna::launch_bwd_mlp(m, P, s), "parameter-gradient kernel launch");
+  }
+#undef LUNA_TRY
   return LUNA_OK;
 }
 
@@ -997,97 +1146,67 @@ luna_status luna_attn_bwd(const void* Q, const void* K, const void* V, const voi
                   0, 1, 0, 1), "dV intra-chunk GEMM");
   }
   if (dt == luna::Dt::BF16) LUNA_TRY(luna::launch_bwd_convert(dt, dvf, dV, (int64_t)heads * n * dd, s), "dV convert");
-  // through the feature map: u = [x | 1] [W | b]^T, du (elementwise on the tables),
-  // [dW | db] = du^T [x | 1] and dx = du [W | b]
-  const int P = param_sets(pb);
-  const int Hh = (int)H, Bb = (int)B;
-  float* xq = reinterpret_cast<float*>(w + lay.xq);
-  float* xk = reinterpret_cast<float*>(w + lay.xk);
-  float* wx = reinterpret_cast<float*>(w + lay.wx);
-  float* uq = reinterpret_cast<float*>(w + lay.uq);
-  float* uk = reinterpret_cast<float*>(w + lay.uk);
-  float* duq = reinterpret_cast<float*>(w + lay.duq);
-  float* duk = reinterpret_cast<float*>(w + lay.duk);
-  float* dwh = reinterpret_cast<float*>(w + lay.dwh);
-  LUNA_TRY(luna::launch_bwd_pack(dt, Q, xq, (int64_t)heads * n, dd, s), "pack kernel launch");
-  LUNA_TRY(luna::launch_bwd_pack(dt, K, xk, (int64_t)heads * n, dd, s), "pack kernel launch");
-  LUNA_TRY(luna::launch_bwd_packw(dt, p->W, p->b, wx, P * M, dd, s), "pack kernel launch");
-  // products over (batch, head) pairs: the batch index is the GEMM's head, the head its
-  // chunk, so that per-head parameters are addressed by stride
-  const int64_t wsc = p->per_head ? (int64_t)M * E : 0;
-  auto gemm_bh = [&](const float* A, int64_t ah, int64_t ac, int64_t ai, int64_t ak, const float* Bm, int64_t bh,
-                     int64_t bc, int64_t bk, int64_t bj, float* Cm, int64_t ch, int64_t c2, int64_t ci, int64_t cj, int Mm,
-                     int Nn, int Kk, int acc) {
-    luna::BwdGemm g{};
-    g.A = A; g.sAh = ah; g.sAc = ac; g.sAi = ai; g.sAk = ak;
-    g.B = Bm; g.sBh = bh; g.sBc = bc; g.sBk = bk; g.sBj = bj;
-    g.C = Cm; g.sCh = ch; g.sCc = c2; g.sCi = ci; g.sCj = cj;
-    g.M = Mm; g.N = Nn; g.K = Kk;
-    g.heads = Bb; g.chunks = Hh; g.chunk = (int)n; g.seq = (int)n;
-    g.accumulate = acc;
-    return luna::launch_bwd_gemm(g, s);
-  };
-  const int64_t nM = n * M, ME = (int64_t)M * E;
-  for (int side = 0; side < 2; ++side) {
-    const float* x = side ? xk : xq;
-    float* u = side ? uk : uq;
-    LUNA_TRY(gemm_bh(x, Hh * nE, nE, E, 1, wx, 0, wsc, 1, E, u, Hh * nM, nM, M, 1, (int)n, M, E, 0), "projection GEMM");
-  }
-  luna::BwdPhi ph{};
-  ph.uq = uq;
-  ph.uk = uk;
-  ph.dphiq = dphiq;
-  ph.dphik = dphik;
-  ph.duq = duq;
-  ph.duk = duk;
-  ph.tables = w + lay.tables;
-  ph.partial = reinterpret_cast<float*>(w + lay.bpart);
-  ph.n = n;
-  ph.heads = B * H;
-  ph.H = Hh;
-  ph.M = M;
-  ph.per_head = p->per_head;
-  ph.part_floats = lay.part_floats;
-  LUNA_TRY(luna::launch_bwd_phi(L, ph, lay.groups, P, s), "feature-map backward kernel launch");
-  for (int side = 0; side < 2; ++side) {
-    float* x = side ? xk : xq;
-    const float* du = side ? duk : duq;
-    if (grads)  // [dW | db] per (batch, head), both sides added
-      LUNA_TRY(gemm_bh(du, Hh * nM, nM, 1, M, x, Hh * nE, nE, E, 1, dwh, Hh * ME, ME, E, 1, M, E, (int)n, side),
-               "weight-gradient GEMM");
-    // dx = du [W | b] into x's rows (x is not read again), then its first d columns
-    LUNA_TRY(gemm_bh(du, Hh * nM, nM, M, 1, wx, 0, wsc, E, 1, x, Hh * nE, nE, E, 1, (int)n, E, M, 0), "dx GEMM");
-    LUNA_TRY(luna::launch_bwd_cols(dt, x, side ? dK : dQ, (int64_t)heads * n, dd, s), "dx convert");
-  }
-  if (grads) {
-    LUNA_TRY(luna::launch_bwd_dw(dwh, grads->W, grads->b, Bb, Hh, M, dd, p->per_head, s), "weight-gradient sum");
-    const int units = (p->shared_channels ? 1 : L) * p->hidden;
-    const int used = 2 * (units + 1) * L;
-    double* sum = reinterpret_cast<double*>(w + lay.sum);
-    double* pre = reinterpret_cast<double*>(w + lay.pre);
-    LUNA_TRY(luna::launch_bwd_reduce(ph.partial, sum, lay.groups, lay.part_floats, used, P, s), "reduce kernel launch");
-    LUNA_TRY(luna::launch_bwd_prefix(sum, pre, w + lay.tables, M, dd, L, lay.part_floats, luna::bwd_nseg_cap(L), P, s),
-             "prefix kernel launch");
-    luna::BwdMlp m{};
-    m.sum = sum;
-    m.pre = pre;
-    m.tables = w + lay.tables;
-    m.fc1_w = p->fc1_w;
-    m.fc1_b = p->fc1_b;
-    m.fc2_w = p->fc2_w;
-    m.dfc1_w = grads->fc1_w;
-    m.dfc1_b = grads->fc1_b;
-    m.dfc2_w = grads->fc2_w;
-    m.dfc2_b = grads->fc2_b;
-    m.L = L;
-    m.hidden = p->hidden;
-    m.C1 = p->shared_channels ? 1 : L;
-    m.part_floats = lay.part_floats;
-    m.nseg_cap = luna::bwd_nseg_cap(L);
-    LUNA_TRY(luna::launch_bwd_mlp(m, P, s), "parameter-gradient kernel launch");
-  }
+  return enqueue_phi_backward(pb, w, lay, Q, K, dQ, dK, grads, s);
 #undef LUNA_TRY
-  return LUNA_OK;
+}
+
+size_t luna_distill_workspace_bytes(luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                                    const luna_phi_params* p, int32_t param_grads) {
+  Problem pb{param_grads ? kOpDistillGrads : kOpDistill, dtype, B, H, n, d, p, 64};
+  Layout lay;
+  return plan(pb, &lay) == LUNA_OK ? lay.total : 0;
+}
+
+luna_status luna_distill(const void* Q, const void* K, luna_dtype dtype, int64_t B, int64_t H, int64_t n, int64_t d,
+                         const luna_phi_params* p, int32_t causal, float eps, float* row_loss,
+                         const luna_phi_grads* grads, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (causal != 0 && causal != 1) return fail(LUNA_ERR_INVALID_ARG, "causal must be 0 or 1");
+  Problem pb{grads ? kOpDistillGrads : kOpDistill, dtype, B, H, n, d, p, 64};
+  Layout lay;
+  luna_status st = plan(pb, &lay);
+  if (st != LUNA_OK) return st;
+  if (!Q || !K || !row_loss) return fail(LUNA_ERR_INVALID_ARG, "Q, K or row_loss is NULL");
+  if (grads && (!grads->W || !grads->b || !grads->fc1_w || !grads->fc1_b || !grads->fc2_w || !grads->fc2_b))
+    return fail(LUNA_ERR_INVALID_ARG, "a parameter-gradient array is NULL");
+  if (!finite_nonneg(eps)) return fail(LUNA_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (B * H * ((n + 63) / 64) > ((int64_t)1 << 31) - 1) return fail(LUNA_ERR_UNSUPPORTED, "too many 64-row tiles");
+  if ((st = check_ws(lay, ws, ws_bytes)) != LUNA_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  uint8_t* w = static_cast<uint8_t*>(ws);
+  if ((st = enqueue_prepare(pb, w, lay, s)) != LUNA_OK) return st;
+  const luna::Dt dt = dtype == LUNA_BF16 ? luna::Dt::BF16 : luna::Dt::F32;
+  const int D = p->M * p->L;
+  luna::FeatureMapArgs f{};  // features of the queries and keys in the call's dtype, one launch
+  f.phi = phi_args(pb, w, lay);
+  f.rows_per_head = n;
+  f.H = (int)H;
+  f.heads = B * H;
+  f.X = K;
+  f.out = w + lay.phik;
+  f.X2 = Q;
+  f.out2 = w + lay.phiq;
+  hipError_t e = luna::launch_featuremap(dt, dt, (int)d, p->L, f, s);
+  if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch");
+  luna::DistillArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.phiq = w + lay.phiq;
+  a.phik = w + lay.phik;
+  a.stats = reinterpret_cast<float*>(w + lay.dstats);
+  a.row_loss = row_loss;
+  a.dphiq = grads ? reinterpret_cast<float*>(w + lay.dphiq) : nullptr;
+  a.dphik = grads ? reinterpret_cast<float*>(w + lay.dphik) : nullptr;
+  a.n = n;
+  a.heads = B * H;
+  a.causal = causal;
+  a.scale = 1.0f / std::sqrt((float)d);
+  a.eps = eps;
+  a.inv_rows = (float)(1.0 / ((double)B * (double)H * (double)n));
+  if ((e = luna::launch_distill(dt, (int)d, D, a, grads != nullptr, s)) != hipSuccess)
+    return hip_fail(e, "distillation kernel launch");
+  if (!grads) return LUNA_OK;
+  return enqueue_phi_backward(pb, w, lay, Q, K, nullptr, nullptr, grads, s);
 }
 
 const char* luna_status_string(luna_status s) {

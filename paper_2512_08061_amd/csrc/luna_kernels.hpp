@@ -274,6 +274,27 @@ hipError_t launch_variant_rms(const double* partial, int groups, int L, double c
                               hipStream_t s);
 hipError_t launch_widen(Dt dt, const void* src, float* dst, int64_t n, hipStream_t s);
 
+// Attention distillation (luna_distill.hip): per query row the soft cross-entropy of
+// the softmax teacher against LUNA's smoothed weights, and the gradients of its mean
+// with respect to the features.  Features are in the call's dtype, [head][n][D].
+struct DistillArgs {
+  const void* Q;       // [heads][n][d]
+  const void* K;
+  const void* phiq;    // [heads][n][D]
+  const void* phik;
+  float* stats;        // [heads][n][4]: base-2 softmax maximum, sum, den (written, then read)
+  float* row_loss;     // [heads][n]
+  float* dphiq;        // [heads][n][D] fp32 (gradients only)
+  float* dphik;
+  int64_t n, heads;
+  int causal;
+  float scale;         // 1 / sqrt(d)
+  float eps;
+  float inv_rows;      // 1 / (heads n): the gradients are of the mean
+};
+bool distill_supported(Dt dt, int d, int D);
+hipError_t launch_distill(Dt dt, int d, int D, const DistillArgs& a, bool grads, hipStream_t s);
+
 // forward pass of the shapes without a fused kernel (fp32 GEMMs and scans as above)
 hipError_t launch_fwd_out(Dt dt, const float* Y, void* out, int64_t rows, int d, float eps, hipStream_t s);
 hipError_t launch_fwd_export(const float* X, int64_t head_stride, float* S, float* z, int heads, int D, int d,

@@ -89,6 +89,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.luna_attn_bwd.argtypes = [vp, vp, vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float, vp, vp, vp,
                                   ctypes.POINTER(PhiGradsC), vp, sz, vp]
     lib.luna_attn_bwd.restype = i32
+    lib.luna_distill_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, P, i32]
+    lib.luna_distill_workspace_bytes.restype = sz
+    lib.luna_distill.argtypes = [vp, vp, i32, i64, i64, i64, i64, P, i32, ctypes.c_float, vp,
+                                 ctypes.POINTER(PhiGradsC), vp, sz, vp]
+    lib.luna_distill.restype = i32
     lib.luna_status_string.argtypes = [i32]
     lib.luna_status_string.restype = ctypes.c_char_p
     lib.luna_last_error.argtypes = []
@@ -395,6 +400,38 @@ def attn_bwd(Q, K, V, dO, p: PhiParams, causal: bool = False, eps: float = 1e-6,
     _check(lib.luna_attn_bwd(*args, wsp, wsn, _stream_ptr(Q.device)))
     dQ._luna_ws = ws
     return dQ, dK, dV, grads
+
+
+def distill(Q, K, p: PhiParams, causal: bool = False, eps: float = 1e-6, param_grads: bool = True):
+    """Attention-distillation loss (luna_distill): returns (row_loss, grads) with
+    row_loss the fp32 [B, H, n] soft cross-entropy of the softmax teacher against LUNA's
+    smoothed weights per query row, and grads a dict of fp32 gradients of its mean with
+    respect to p's arrays (None if not param_grads)."""
+    torch = _torch()
+    lib = load_library()
+    for t in (Q, K):
+        if t.dim() != 4 or not t.is_contiguous():
+            raise LunaError(LUNA_ERR_INVALID_ARG, "Q and K must be contiguous [B, H, n, d] tensors")
+    if Q.shape != K.shape or Q.dtype != K.dtype:
+        raise LunaError(LUNA_ERR_INVALID_ARG, "Q and K must have one shape and dtype")
+    B, H, n, d = Q.shape
+    row_loss = torch.empty((B, H, n), dtype=torch.float32, device=Q.device)
+    grads, gc = None, None
+    if param_grads:
+        grads = {name: torch.empty(getattr(p, name).shape, dtype=torch.float32, device=Q.device)
+                 for name in ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")}
+        gc = PhiGradsC(*(grads[k].data_ptr() for k in ("W", "b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")))
+    pc = p.c()
+    dt = _dt(Q)
+    nb = int(lib.luna_distill_workspace_bytes(dt, B, H, n, d, ctypes.byref(pc), int(param_grads)))
+    args = (Q.data_ptr(), K.data_ptr(), dt, B, H, n, d, ctypes.byref(pc), int(causal), eps, row_loss.data_ptr(),
+            ctypes.byref(gc) if gc is not None else None)
+    if nb == 0:
+        _check(lib.luna_distill(*args, None, 0, None))
+    ws, wsp, wsn = _workspace(nb, Q.device)
+    _check(lib.luna_distill(*args, wsp, wsn, _stream_ptr(Q.device)))
+    row_loss._luna_ws = ws
+    return row_loss, grads
 
 
 def _state_tensors(B, H, D, d, device, S, z):

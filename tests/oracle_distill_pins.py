@@ -197,3 +197,19 @@ ALL_PINS = [
     pin_causal_rows_ignore_later_keys,
     pin_scale_invariance,
 ]
+
+
+def pin_sampled_rows_match_the_whole_head(v):
+    """distill_rows_at (row by row, for long sequences) equals the pinned whole-head
+    losses at every row, both forms."""
+    rng = np.random.default_rng(59)
+    n, d, D = 11, 4, 5
+    Q, K = rng.standard_normal((n, d)), rng.standard_normal((n, d))
+    fq, fk = rng.uniform(0.0, 1.0, (n, D)), rng.uniform(0.0, 1.0, (n, D))
+    for causal in (False, True):
+        whole = v.distill_rows_features(Q, K, fq, fk, causal, 1e-3)
+        rows = v.distill_rows_at(Q, K, fq, fk, list(range(n)), causal, 1e-3)
+        assert np.max(np.abs(whole - rows)) < 1e-13
+
+
+ALL_PINS.append(pin_sampled_rows_match_the_whole_head)

@@ -25,7 +25,8 @@ def test_exports_every_declared_symbol(lib):
                           "luna_attn_state", "luna_attn_causal_step", "luna_status_string", "luna_last_error",
                           "luna_attn_fwd_causal_noalloc", "luna_noalloc_scratch_bytes", "luna_attn_bwd",
                           "luna_phi_variant_features", "luna_featuremap_variant_workspace_bytes",
-                          "luna_featuremap_variant", "luna_attn_features_workspace_bytes", "luna_attn_fwd_features"}
+                          "luna_featuremap_variant", "luna_attn_features_workspace_bytes", "luna_attn_fwd_features",
+                          "luna_distill_workspace_bytes", "luna_distill"}
     for name in names:
         assert hasattr(lib, name), name
 
@@ -256,3 +257,30 @@ def test_attn_features_planning(lib):
     assert call(causal=2) == luna.LUNA_ERR_INVALID_ARG
     assert call(eps=-1.0) == luna.LUNA_ERR_INVALID_ARG
     assert call(ws=16) == luna.LUNA_ERR_WORKSPACE
+
+
+def test_distill_planning_and_rejects(lib):
+    """The distillation loss: supported feature counts per dtype, a workspace that grows
+    with the gradients (feature gradients and the feature-map backward's buffers), and
+    argument checks on the host."""
+    wsb = lambda M, L, dt=luna.LUNA_BF16, d=64, grads=0, n=300: lib.luna_distill_workspace_bytes(  # noqa: E731
+        dt, 2, 3, n, d, ctypes.byref(_params(M=M, L=L)), grads)
+    assert wsb(16, 8) > 0 and wsb(8, 8) > 0 and wsb(32, 8) > 0 and wsb(256, 1) > 0   # D = 128, 64, 256, 256
+    assert wsb(16, 8, luna.LUNA_F32) > 0 and wsb(32, 8, luna.LUNA_F32) == 0          # fp32: D <= 128
+    assert wsb(12, 8) == 0 and wsb(3, 5) == 0 and wsb(16, 4) > 0                     # D = 96, 15, 64
+    rows, D = 2 * 3 * 300, 128
+    with_grads = wsb(16, 8, grads=1)
+    assert with_grads - wsb(16, 8) >= 2 * rows * D * 4  # fp32 feature gradients of Q and K
+    assert wsb(16, 8, d=48) == 0
+    p = _params()
+    st = lambda **kw: lib.luna_distill(kw.get("q", FAKE), FAKE, kw.get("dt", luna.LUNA_BF16), 2, 3,  # noqa: E731
+                                       kw.get("n", 300), 64, ctypes.byref(kw.get("p", p)), kw.get("causal", 0),
+                                       kw.get("eps", 1e-6), kw.get("loss", FAKE), None, FAKE, kw.get("ws", 1 << 40),
+                                       None)
+    assert st(q=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(loss=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(causal=2) == luna.LUNA_ERR_INVALID_ARG
+    assert st(eps=-1.0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(n=0) == luna.LUNA_ERR_INVALID_ARG
+    assert st(p=_params(M=12, L=8)) == luna.LUNA_ERR_UNSUPPORTED
+    assert st(ws=256) == luna.LUNA_ERR_WORKSPACE

@@ -14,8 +14,9 @@
 //   dphi(q_t) = sum_s G_ts phi(k_s),  dphi(k_s) = sum_t G_ts phi(q_t).
 //
 // Flash-style: nothing of size n x n is stored.  distill_q_kernel takes 64 queries per
-// workgroup (16 per wave) and walks the key tiles twice: first the softmax maximum and
-// sum (online, in base 2) and den, then the losses and dphi(Q).  distill_k_kernel takes
+// workgroup (16 per wave) and walks the key tiles once, with the softmax maximum kept
+// online (base 2) and every sum taken against it rescaled as it grows: the softmax sum,
+// den, the loss and dphi(Q).  distill_k_kernel takes
 // 64 keys per workgroup and walks the query tiles once for dphi(K), from the per-row
 // statistics the first kernel stored.  Per tile, S^T = K Q^T and P^T = phi(K) phi(Q)^T
 // run on the matrix cores with the wave's queries as the B operand held in registers,
@@ -81,7 +82,7 @@ struct GFrag {
 };
 
 template <typename T, int DH, int DF, bool GRAD>
-__global__ __launch_bounds__(256) void distill_q_kernel(DistillArgs a) {
+__global__ __launch_bounds__(256, 2) void distill_q_kernel(DistillArgs a) {
   using S = DistShape<T, DH, DF>;
   __shared__ __align__(16) T sk[64 * S::LDH];
   __shared__ __align__(16) T sf[64 * S::LDF];
@@ -90,7 +91,8 @@ __global__ __launch_bounds__(256) void distill_q_kernel(DistillArgs a) {
   const int64_t n = a.n;
   const int ntiles = (int)((n + 63) / 64);
   const int64_t head = blockIdx.x / ntiles;
-  const int qt = (int)(blockIdx.x - head * ntiles);
+  // causal: the last query tiles (the most key tiles) are dispatched first
+  const int qt = a.causal ? ntiles - 1 - (int)(blockIdx.x - head * ntiles) : (int)(blockIdx.x - head * ntiles);
   const int64_t tq = (int64_t)qt * 64 + wave * 16 + r;  // this lane's query
   const bool q_ok = tq < n;
   const T* Kh = reinterpret_cast<const T*>(a.K) + head * n * DH;
@@ -145,98 +147,145 @@ __global__ __launch_bounds__(256) void distill_q_kernel(DistillArgs a) {
     return q_ok && s < n && (!a.causal || s <= tq);
   };
 
-  // pass 1: softmax maximum and sum (one maximum per row, partial sums per lane), den
-  float m = -1e30f, lsum = 0.0f, den = 0.0f;
+  // One pass with online rescaling (a row's maximum m changes as tiles arrive; sums
+  // taken against the old maximum are multiplied by 2^(m_old - m_new)):
+  //   lsum = sum_s 2^(lg_s - m),  wl = sum_s 2^(lg_s - m) log2(pe_s),  den = sum_s P_s,
+  // so that CE = -ln 2 wl / lsum + log(den + eps).  lsum, wl and den are partial per lane
+  // (its 16 keys of a tile) against the row's common maximum, added across the row's
+  // four lane groups when a total is needed.  The gradient
+  //   dphi(q_t) = (1/N) (z_t / (den + eps) - acc / lsum),  acc = sum_s 2^(lg_s - m) / pe_s phi(k_s),
+  // with z_t the sum of phi(k_s) over the visible keys: every key tile but the last is
+  // wholly visible to all 64 queries (the last is the causal diagonal or the ragged end),
+  // so those are summed per feature column by the threads (thread: 8 features of DF / 32
+  // rows) and enter acc as above; the last tile, where m, lsum and den become final,
+  // enters with its complete coefficient G_ts (visible keys only) after acc has been
+  // scaled by -(1/N) / lsum.
+  float m = -1e30f, lsum = 0.0f, wl = 0.0f, den = 0.0f;
+  f32x4 acc[S::NFO];
+#pragma unroll
+  for (int fo = 0; fo < S::NFO; ++fo) acc[fo] = zero4();
+  constexpr int FC = DF / 8, RG = DF / 32;  // 16-byte feature chunks per row; rows per thread
+  float zc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) zc[e] = 0.0f;
+  const int zf = tid % FC, zr = (tid / FC) * RG;
   for (int kt = 0; kt <= last; ++kt) {
     stage(kt);
     f32x4 st[4], pt[4];
     products(st, pt);
+    const bool final_tile = kt == last;
+    if (GRAD && !final_tile) {  // column sums of a wholly visible tile
+#pragma unroll
+      for (int rr = 0; rr < RG; ++rr) {
+        Frag<T> v;
+        load8(v, sf + (zr + rr) * S::LDF + 8 * zf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) zc[e] += v.get(e);
+      }
+    }
     float lg[4][4], tmax = -INFINITY;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const bool ok = visible(kt, c, j);
-        lg[c][j] = ok ? st[c][j] * c2 : -INFINITY;
+        lg[c][j] = visible(kt, c, j) ? st[c][j] * c2 : -INFINITY;
         tmax = fmaxf(tmax, lg[c][j]);
-        if (ok) den += pt[c][j];
       }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
     const float mn = fmaxf(m, tmax);
-    float add = 0.0f;
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) add += exp2f(lg[c][j] - mn);
-    lsum = lsum * exp2f(m - mn) + add;
+    const float rescale = exp2f(m - mn);
     m = mn;
-  }
-  lsum += __shfl_xor(lsum, 16, kWave);
-  lsum += __shfl_xor(lsum, 32, kWave);
-  den += __shfl_xor(den, 16, kWave);
-  den += __shfl_xor(den, 32, kWave);
-  const float inv_l = 1.0f / lsum, inv_den = 1.0f / (den + a.eps);
-
-  // pass 2: the losses and dphi(Q)
-  float ce = 0.0f;
-  f32x4 dq[S::NFO];
-#pragma unroll
-  for (int fo = 0; fo < S::NFO; ++fo) dq[fo] = zero4();
-  for (int kt = 0; kt <= last; ++kt) {
-    stage(kt);
-    f32x4 st[4], pt[4];
-    products(st, pt);
-    float gv[4][4];
+    float add = 0.0f, addw = 0.0f;
+    float cv[4][4];  // gradients: this tile's coefficients of acc (not the final tile)
 #pragma unroll
     for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        gv[c][j] = 0.0f;
-        if (visible(kt, c, j)) {
-          const float A = exp2f(st[c][j] * c2 - m) * inv_l;
-          const float pe = pt[c][j] + eps_nt;
-          ce -= A * log2f(pe);
-          gv[c][j] = a.inv_rows * (inv_den - A / pe);
-        }
+        const bool ok = lg[c][j] != -INFINITY;
+        const float e = exp2f(lg[c][j] - mn);
+        const float pe = pt[c][j] + eps_nt;
+        add += e;
+        addw += ok ? e * log2f(pe) : 0.0f;
+        if (ok) den += pt[c][j];
+        cv[c][j] = e / pe;  // 0 where masked (e = 0)
       }
+    lsum = lsum * rescale + add;
+    wl = wl * rescale + addw;
     if constexpr (GRAD) {
+      float fj[4];  // the factors of acc's rows 4 g + j
+      if (!final_tile) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fj[j] = __shfl(rescale, 4 * g + j, kWave);
+      } else {
+        float lt = lsum + __shfl_xor(lsum, 16, kWave);
+        lt += __shfl_xor(lt, 32, kWave);
+        float dt = den + __shfl_xor(den, 16, kWave);
+        dt += __shfl_xor(dt, 32, kWave);
+        const float inv_lt = 1.0f / lt, inv_dt = 1.0f / (dt + a.eps);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            cv[c][j] = lg[c][j] != -INFINITY ? a.inv_rows * (inv_dt - cv[c][j] * inv_lt) : 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fj[j] = -a.inv_rows * __shfl(rescale * inv_lt, 4 * g + j, kWave);
+      }
+#pragma unroll
+      for (int fo = 0; fo < S::NFO; ++fo)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[fo][j] *= fj[j];
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2) {
         GFrag<T> gf;
-        gf.set(gv[2 * kb2], gv[2 * kb2 + 1]);
+        gf.set(cv[2 * kb2], cv[2 * kb2 + 1]);
 #pragma unroll
         for (int fo = 0; fo < S::NFO; ++fo) {
           Frag<T> bf;
           load_tr4(bf, 0, sf, S::LDF, 32 * kb2 + 4 * g, 16 * fo, lane);
           load_tr4(bf, 4, sf, S::LDF, 32 * kb2 + 16 + 4 * g, 16 * fo, lane);
-          gf.apply(dq[fo], bf);
+          gf.apply(acc[fo], bf);
         }
       }
     }
   }
-  ce += __shfl_xor(ce, 16, kWave);
-  ce += __shfl_xor(ce, 32, kWave);
+  lsum += __shfl_xor(lsum, 16, kWave);
+  lsum += __shfl_xor(lsum, 32, kWave);
+  wl += __shfl_xor(wl, 16, kWave);
+  wl += __shfl_xor(wl, 32, kWave);
+  den += __shfl_xor(den, 16, kWave);
+  den += __shfl_xor(den, 32, kWave);
   if (q_ok && g == 0) {
     const int64_t row = head * n + tq;
-    a.row_loss[row] = ce * kLn2 + logf(den + a.eps);
+    a.row_loss[row] = -kLn2 * wl / lsum + logf(den + a.eps);
     *reinterpret_cast<float4*>(a.stats + row * 4) = float4{m, lsum, den, 0.0f};
   }
   if constexpr (GRAD) {
+    // z of the wholly visible tiles: the threads' column sums added over their row groups
+    __syncthreads();
+    static_assert((64 / RG) * DF * sizeof(float) <= sizeof(sf), "column sums must fit in the feature tile");
+    float* zs = reinterpret_cast<float*>(sf);  // [64 / RG][DF] floats in the feature tile (free now)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t t = (int64_t)qt * 64 + wave * 16 + 4 * g + j;
-      if (t < n) {
-        float* o = a.dphiq + (head * n + t) * DF + r;
+    for (int e = 0; e < 8; ++e) zs[(zr / RG) * DF + 8 * zf + e] = zc[e];
+    __syncthreads();
+    float zcoef[4];  // (1/N) / (den + eps) of acc's rows 4 g + j
 #pragma unroll
-        for (int fo = 0; fo < S::NFO; ++fo) o[16 * fo] = dq[fo][j];
+    for (int j = 0; j < 4; ++j) zcoef[j] = a.inv_rows / (__shfl(den, 4 * g + j, kWave) + a.eps);
+#pragma unroll
+    for (int fo = 0; fo < S::NFO; ++fo) {
+      float z = 0.0f;
+      for (int q = 0; q < 64 / RG; ++q) z += zs[q * DF + 16 * fo + r];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t t = (int64_t)qt * 64 + wave * 16 + 4 * g + j;
+        if (t < n) a.dphiq[(head * n + t) * DF + 16 * fo + r] = acc[fo][j] + zcoef[j] * z;
       }
     }
   }
 }
 
 template <typename T, int DH, int DF>
-__global__ __launch_bounds__(256) void distill_k_kernel(DistillArgs a) {
+__global__ __launch_bounds__(256, 2) void distill_k_kernel(DistillArgs a) {
   using S = DistShape<T, DH, DF>;
   __shared__ __align__(16) T sq[64 * S::LDH];
   __shared__ __align__(16) T sf[64 * S::LDF];

@@ -82,7 +82,8 @@ __global__ __launch_bounds__(256) void bwd_convert_kernel(const float* __restric
 
 // ---------------------------------------------------------------------------
 // batched strided GEMM on the fp32 matrix cores: 64 x 64 output tiles, four waves
-// of 32 x 32 (2 x 2 blocks of 16 x 16), 32-deep k slices through LDS.  A tile is kept
+// of 32 x 32 (2 x 2 blocks of 16 x 16), 32-deep k slices through LDS, the next slice
+// read into registers during the current slice's products.  A tile is kept
 // row-major (i, k) and B transposed (j, k), so that a lane's fragment -- row (or
 // column) lane % 16, k = 8 (lane / 16) + e for e < 8 -- is two 16-byte reads.  Tile
 // loads let consecutive threads walk the operand's unit-stride index.
@@ -112,22 +113,45 @@ __global__ __launch_bounds__(256) void bwd_gemm_kernel(BwdGemm g) {
   for (int x = 0; x < 2; ++x)
 #pragma unroll
     for (int y = 0; y < 2; ++y) acc[x][y] = zero4();
-  for (int k0 = 0; k0 < Kv; k0 += kGK) {
+  // The next k slice is read into registers while the matrix cores work on the current
+  // one from LDS, so that global-load latency overlaps the products.
+  constexpr int PER = (kGK * kGT) / 256;  // elements of each operand per thread and slice
+  float ra[PER], rb[PER];
+  auto load_slice = [&](int k0) {
 #pragma unroll
-    for (int e = 0; e < (kGK * kGT) / 256; ++e) {
+    for (int e = 0; e < PER; ++e) {
       const int idx = tid + 256 * e;
       int ii, kk;
       if (a_krow) { kk = idx % kGK; ii = idx / kGK; }
       else { ii = idx % kGT; kk = idx / kGT; }
       const int ia = i0 + ii, ka = k0 + kk;
-      As[ii][kk] = (ka < Kv && ia < Mv) ? A[ia * g.sAi + ka * g.sAk] : 0.0f;
+      ra[e] = (ka < Kv && ia < Mv) ? A[ia * g.sAi + ka * g.sAk] : 0.0f;
       int jj, kb;
       if (b_jrow) { jj = idx % kGT; kb = idx / kGT; }
       else { kb = idx % kGK; jj = idx / kGK; }
       const int jb = j0 + jj, kbb = k0 + kb;
-      Bt[jj][kb] = (kbb < Kv && jb < Nv) ? B[kbb * g.sBk + jb * g.sBj] : 0.0f;
+      rb[e] = (kbb < Kv && jb < Nv) ? B[kbb * g.sBk + jb * g.sBj] : 0.0f;
     }
+  };
+  auto store_slice = [&]() {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = tid + 256 * e;
+      int ii, kk;
+      if (a_krow) { kk = idx % kGK; ii = idx / kGK; }
+      else { ii = idx % kGT; kk = idx / kGT; }
+      As[ii][kk] = ra[e];
+      int jj, kb;
+      if (b_jrow) { jj = idx % kGT; kb = idx / kGT; }
+      else { kb = idx % kGK; jj = idx / kGK; }
+      Bt[jj][kb] = rb[e];
+    }
+  };
+  load_slice(0);
+  for (int k0 = 0; k0 < Kv; k0 += kGK) {
+    store_slice();
     __syncthreads();
+    if (k0 + kGK < Kv) load_slice(k0 + kGK);
     Frag<float> af[2], bf[2];
 #pragma unroll
     for (int x = 0; x < 2; ++x) {

@@ -132,14 +132,17 @@ __device__ __forceinline__ void store_run(void* out, bool obf, const float (&f)[
 // The one-feature kinds stream rows through: registers are capped so that eight waves
 // per SIMD are resident (four for rows of 128 elements, which carry twice the bytes);
 // the channel MLPs are bound by their arithmetic.
-template <typename Tin, int DH, int KIND, int ACT, int LC>
-__global__ __launch_bounds__(256, KIND == kVarMlp ? 1 : (DH <= 64 ? 8 : 4)) void variant_map_kernel(VariantArgs a) {
+template <typename Tin, int DH, int KIND, int ACT, int LC, bool STAGED>
+__global__ __launch_bounds__(256, KIND == kVarMlp ? 1 : (DH <= 64 ? (STAGED ? 6 : 8) : 4)) void variant_map_kernel(VariantArgs a) {
   constexpr int KS = DH / 32;
   constexpr bool MLP = KIND == kVarMlp;
   // a lane's run of features: 8 projections' (sin/cos: two each) for the one-feature
   // kinds, four projections' for the channel MLPs (with a bank; per channel otherwise)
   constexpr int RUN = MLP ? 4 : (KIND == kVarSinCos ? 16 : 8);
   __shared__ float s_bias[256];  // b of the parameter set, zero past M
+  // one-feature kinds: each wave's 16 output rows (at most 256 bytes each), written back
+  // as contiguous 1 KB stores
+  __shared__ uint4 s_rows[STAGED ? 4 * 16 * 16 : 1];
   __shared__ float s_env[MLP ? LC * DH : 4];
   __shared__ double s_sum[4][LC];  // channel RMS: per-wave sums of y^2
 
@@ -162,6 +165,8 @@ __global__ __launch_bounds__(256, KIND == kVarMlp ? 1 : (DH <= 64 ? 8 : 4)) void
                    (reinterpret_cast<uintptr_t>(a.out) & 15) == 0;
   const float inv_sqrt_m = 1.0f / sqrtf((float)M);
   const float half_inv_sqrt_d = 0.5f / sqrtf((float)DH);
+  const int row_chunks = D * esz / 16;  // 16-byte pieces of an output row
+  constexpr bool staged = STAGED;  // (the host checks: one-feature kind, rows of whole 16-byte pieces, <= 256 bytes)
   const int64_t n = a.rows_per_head;
   const int tiles_per_head = (int)((n + 63) / 64);
   const int64_t items = a.heads * tiles_per_head;
@@ -284,7 +289,44 @@ __global__ __launch_bounds__(256, KIND == kVarMlp ? 1 : (DH <= 64 ? 8 : 4)) void
               f[e] = hw_exp(u - sq * half_inv_sqrt_d) * inv_sqrt_m;
             }
           }
-        store_run<RUN>(out_row + (int64_t)base * lout * esz, obf, f, nv * lout, vec && nv == 8);
+        if constexpr (staged) {  // the run's whole 16-byte pieces into the wave's row tile
+          uint4* dst = s_rows + (wave * 16 + r) * 16 + base * lout * esz / 16;
+          const int nfeat = nv * lout;
+          if (obf) {
+#pragma unroll
+            for (int k = 0; k < RUN / 8; ++k) {
+              if (8 * k < nfeat) {
+                bf16x8 v;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = (__bf16)f[8 * k + e];
+                dst[k] = __builtin_bit_cast(uint4, v);
+              }
+            }
+          } else {
+#pragma unroll
+            for (int k = 0; k < RUN / 4; ++k)
+              if (4 * k < nfeat)
+                dst[k] = make_uint4(__float_as_uint(f[4 * k]), __float_as_uint(f[4 * k + 1]),
+                                    __float_as_uint(f[4 * k + 2]), __float_as_uint(f[4 * k + 3]));
+          }
+        } else {
+          store_run<RUN>(out_row + (int64_t)base * lout * esz, obf, f, nv * lout, vec && nv == 8);
+        }
+      }
+      if constexpr (staged) {  // the wave's 16 rows back, consecutive lanes on consecutive pieces
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        const int64_t t0 = (int64_t)tile * 64 + wave * 16;
+        char* rows = reinterpret_cast<char*>(a.out) + (head * n + t0) * (int64_t)D * esz;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = lane + kWave * q;
+          if (c < 16 * row_chunks) {
+            const int row = c / row_chunks, col = c - row * row_chunks;
+            if (t0 + row < n)
+              *reinterpret_cast<uint4*>(rows + (int64_t)row * D * esz + 16 * col) = s_rows[(wave * 16 + row) * 16 + col];
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
       }
     } else {
       for (int mb = 0; mb < MB; ++mb) {
@@ -436,11 +478,11 @@ __global__ __launch_bounds__(256, KIND == kVarMlp ? 1 : (DH <= 64 ? 8 : 4)) void
 
 // As many workgroups as the device holds at once (registers and LDS permitting), at
 // most kVariantMaxGrid; more items loop.  The occupancy query runs once per kernel.
-template <typename Tin, int DH, int KIND, int ACT, int LC>
+template <typename Tin, int DH, int KIND, int ACT, int LC, bool STAGED = false>
 hipError_t variant_launch(const VariantArgs& a, int64_t items, int* grid, hipStream_t s) {
   static const int resident = []() {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, variant_map_kernel<Tin, DH, KIND, ACT, LC>, 256, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, variant_map_kernel<Tin, DH, KIND, ACT, LC, STAGED>, 256, 0) !=
             hipSuccess ||
         per_cu < 1)
       per_cu = 1;
@@ -450,16 +492,26 @@ hipError_t variant_launch(const VariantArgs& a, int64_t items, int* grid, hipStr
   }();
   const int g = (int)std::min<int64_t>(items, resident);
   *grid = g;
-  hipLaunchKernelGGL((variant_map_kernel<Tin, DH, KIND, ACT, LC>), dim3(g), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((variant_map_kernel<Tin, DH, KIND, ACT, LC, STAGED>), dim3(g), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 template <typename Tin, int DH>
 hipError_t variant_dispatch_kind(const VariantArgs& a, int64_t items, int* grid, hipStream_t s) {
+  // one-feature kinds whose output rows are whole 16-byte pieces, at most 256 bytes, at
+  // an aligned address: rows staged in LDS and written back contiguously
+  const int row_bytes = a.M * (a.kind == kVarSinCos ? 2 : 1) * (a.out_bf16 ? 2 : 4);
+  const bool stage = row_bytes % 16 == 0 && row_bytes <= 256 && (reinterpret_cast<uintptr_t>(a.out) & 15) == 0;
   switch (a.kind) {
-    case kVarCos: return variant_launch<Tin, DH, kVarCos, 0, 1>(a, items, grid, s);
-    case kVarSinCos: return variant_launch<Tin, DH, kVarSinCos, 0, 1>(a, items, grid, s);
-    case kVarPerformer: return variant_launch<Tin, DH, kVarPerformer, 0, 1>(a, items, grid, s);
+    case kVarCos:
+      return stage ? variant_launch<Tin, DH, kVarCos, 0, 1, true>(a, items, grid, s)
+                   : variant_launch<Tin, DH, kVarCos, 0, 1>(a, items, grid, s);
+    case kVarSinCos:
+      return stage ? variant_launch<Tin, DH, kVarSinCos, 0, 1, true>(a, items, grid, s)
+                   : variant_launch<Tin, DH, kVarSinCos, 0, 1>(a, items, grid, s);
+    case kVarPerformer:
+      return stage ? variant_launch<Tin, DH, kVarPerformer, 0, 1, true>(a, items, grid, s)
+                   : variant_launch<Tin, DH, kVarPerformer, 0, 1>(a, items, grid, s);
     case kVarMlp: break;
     default: return hipErrorInvalidValue;
   }

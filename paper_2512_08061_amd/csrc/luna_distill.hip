@@ -38,6 +38,32 @@ namespace {
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kLn2 = 0.693147180559945309f;
 
+// The hardware's base-2 exponential, base-2 logarithm and reciprocal (about 1 ulp on
+// normal fp32 values).  Exponentials below 2^-126 come out as 0 (a softmax weight that
+// small against the row's maximum changes no sum) and a logarithm or reciprocal of a
+// value below 2^-126 is taken as of 0: P + eps / n_t only gets there when eps is below
+// n 2^-126, i.e. in effect eps = 0, where such a key's loss is infinite either way.
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float lg2(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// Workgroups are dealt to the eight XCDs in turn (workgroup b to XCD b mod 8), each
+// XCD with its own L2.  Workgroup b's work item is renumbered so that every XCD takes
+// one contiguous run of items, first to last in dispatch order: the 64-row tiles of a
+// head, which all read the same tiles of the other side, then share one L2.  (A
+// bijection of [0, items) for any count.)
+__device__ __forceinline__ int64_t xcd_item(int64_t b, int64_t items) {
+  constexpr int64_t kXcds = 8;
+  const int64_t per = items / kXcds, rem = items % kXcds, x = b % kXcds, i = b / kXcds;
+  return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
+}
+
+// Compile-time flag of a tile in which every key is visible to every query.
+template <bool B>
+struct Whole {
+  static constexpr bool value = B;
+};
+
 template <typename T, int DH, int DF>
 struct DistShape {
   static constexpr int PAD = 16 / (int)sizeof(T);  // one 16-byte chunk per row
@@ -45,16 +71,38 @@ struct DistShape {
   static constexpr int KD = DH / 32, KF = DF / 32, NFO = DF / 16;
 };
 
-// Rows r0 .. r0 + 63 of a row-major [n][W] array of T into an LDS tile with row stride
-// LD (rows at or past n as zeros), 16 bytes per thread and step.
-template <typename T, int W, int LD>
-__device__ __forceinline__ void stage_rows(T* tile, const T* src, int64_t r0, int64_t n, int tid) {
-  constexpr int CH = W * (int)sizeof(T) / 16;
-  for (int i = tid; i < 64 * CH; i += 256) {
-    const int row = i / CH, c = i % CH;
-    uint4 v = {0u, 0u, 0u, 0u};
-    if (r0 + row < n) v = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src + (r0 + row) * W) + 16 * c);
-    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile + row * LD) + 16 * c) = v;
+// Rows r0 .. r0 + 63 of two row-major arrays, [n][W1] and [n][W2] of T, into LDS tiles
+// with row strides LD1 and LD2 (rows at or past n as zeros), 16 bytes per thread and
+// step of the 256 threads: every global read is issued before the first LDS write, so
+// the staging waits for one memory round trip.
+template <typename T, int W1, int LD1, int W2, int LD2>
+__device__ __forceinline__ void stage_rows(T* tile1, const T* src1, T* tile2, const T* src2, int64_t r0, int64_t n,
+                                           int tid) {
+  constexpr int CH1 = W1 * (int)sizeof(T) / 16, CH2 = W2 * (int)sizeof(T) / 16;
+  constexpr int IT1 = 64 * CH1 / 256, IT2 = 64 * CH2 / 256;
+  static_assert(IT1 * 256 == 64 * CH1 && IT2 * 256 == 64 * CH2, "whole 256-thread steps");
+  uint4 v1[IT1], v2[IT2];
+#pragma unroll
+  for (int it = 0; it < IT1; ++it) {
+    const int i = tid + 256 * it, row = i / CH1, c = i % CH1;
+    v1[it] = uint4{0u, 0u, 0u, 0u};
+    if (r0 + row < n) v1[it] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src1 + (r0 + row) * W1) + 16 * c);
+  }
+#pragma unroll
+  for (int it = 0; it < IT2; ++it) {
+    const int i = tid + 256 * it, row = i / CH2, c = i % CH2;
+    v2[it] = uint4{0u, 0u, 0u, 0u};
+    if (r0 + row < n) v2[it] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src2 + (r0 + row) * W2) + 16 * c);
+  }
+#pragma unroll
+  for (int it = 0; it < IT1; ++it) {
+    const int i = tid + 256 * it, row = i / CH1, c = i % CH1;
+    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile1 + row * LD1) + 16 * c) = v1[it];
+  }
+#pragma unroll
+  for (int it = 0; it < IT2; ++it) {
+    const int i = tid + 256 * it, row = i / CH2, c = i % CH2;
+    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile2 + row * LD2) + 16 * c) = v2[it];
   }
 }
 
@@ -81,8 +129,10 @@ struct GFrag {
   }
 };
 
+// Waves per SIMD: the bf16 loss alone keeps 4 (3 at D = 256, where the LDS tiles allow
+// no more); fp32 tiles and the gradients' accumulators leave room for 2.
 template <typename T, int DH, int DF, bool GRAD>
-__global__ __launch_bounds__(256, 2) void distill_q_kernel(DistillArgs a) {
+__global__ __launch_bounds__(256, GRAD || sizeof(T) == 4 ? 2 : (DF <= 128 ? 4 : 3)) void distill_q_kernel(DistillArgs a) {
   using S = DistShape<T, DH, DF>;
   __shared__ __align__(16) T sk[64 * S::LDH];
   __shared__ __align__(16) T sf[64 * S::LDF];
@@ -90,9 +140,10 @@ __global__ __launch_bounds__(256, 2) void distill_q_kernel(DistillArgs a) {
   const int g = lane / 16, r = lane % 16;
   const int64_t n = a.n;
   const int ntiles = (int)((n + 63) / 64);
-  const int64_t head = blockIdx.x / ntiles;
+  const int64_t item = xcd_item(blockIdx.x, gridDim.x);
+  const int64_t head = item / ntiles;
   // causal: the last query tiles (the most key tiles) are dispatched first
-  const int qt = a.causal ? ntiles - 1 - (int)(blockIdx.x - head * ntiles) : (int)(blockIdx.x - head * ntiles);
+  const int qt = a.causal ? ntiles - 1 - (int)(item - head * ntiles) : (int)(item - head * ntiles);
   const int64_t tq = (int64_t)qt * 64 + wave * 16 + r;  // this lane's query
   const bool q_ok = tq < n;
   const T* Kh = reinterpret_cast<const T*>(a.K) + head * n * DH;
@@ -138,13 +189,8 @@ __global__ __launch_bounds__(256, 2) void distill_q_kernel(DistillArgs a) {
   };
   auto stage = [&](int kt) {
     __syncthreads();
-    stage_rows<T, DH, S::LDH>(sk, Kh, (int64_t)kt * 64, n, tid);
-    stage_rows<T, DF, S::LDF>(sf, Fk, (int64_t)kt * 64, n, tid);
+    stage_rows<T, DH, S::LDH, DF, S::LDF>(sk, Kh, sf, Fk, (int64_t)kt * 64, n, tid);
     __syncthreads();
-  };
-  auto visible = [&](int kt, int c, int j) {
-    const int64_t s = (int64_t)kt * 64 + 16 * c + 4 * g + j;
-    return q_ok && s < n && (!a.causal || s <= tq);
   };
 
   // One pass with online rescaling (a row's maximum m changes as tiles arrive; sums
@@ -183,35 +229,56 @@ __global__ __launch_bounds__(256, 2) void distill_q_kernel(DistillArgs a) {
         for (int e = 0; e < 8; ++e) zc[e] += v.get(e);
       }
     }
-    float lg[4][4], tmax = -INFINITY;
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        lg[c][j] = visible(kt, c, j) ? st[c][j] * c2 : -INFINITY;
-        tmax = fmaxf(tmax, lg[c][j]);
-      }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-    const float mn = fmaxf(m, tmax);
-    const float rescale = exp2f(m - mn);
-    m = mn;
-    float add = 0.0f, addw = 0.0f;
+    // Keys 64 kt + [0, lim) are visible to this lane's query.  Every tile before the
+    // causal diagonal and the ragged end is wholly visible (the test is the same for the
+    // whole workgroup): its scores skip the masks.
+    const bool whole = (int64_t)kt * 64 + 64 <= n && (!a.causal || kt < qt);
+    int lim = 64;
+    if (!whole) {
+      int64_t l = n - (int64_t)kt * 64;
+      if (a.causal) l = l < tq - (int64_t)kt * 64 + 1 ? l : tq - (int64_t)kt * 64 + 1;
+      lim = q_ok ? (int)(l < 0 ? 0 : (l > 64 ? 64 : l)) : 0;
+    }
+    float rescale;
     float cv[4][4];  // gradients: this tile's coefficients of acc (not the final tile)
+    auto score = [&](auto whole_tag) {
+      constexpr bool W = decltype(whole_tag)::value;
+      float tmax = -INFINITY;  // the largest visible score (scale > 0: max commutes with it)
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
+      for (int c = 0; c < 4; ++c)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bool ok = lg[c][j] != -INFINITY;
-        const float e = exp2f(lg[c][j] - mn);
-        const float pe = pt[c][j] + eps_nt;
-        add += e;
-        addw += ok ? e * log2f(pe) : 0.0f;
-        if (ok) den += pt[c][j];
-        cv[c][j] = e / pe;  // 0 where masked (e = 0)
-      }
-    lsum = lsum * rescale + add;
-    wl = wl * rescale + addw;
+        for (int j = 0; j < 4; ++j) tmax = fmaxf(tmax, W || 16 * c + 4 * g + j < lim ? st[c][j] : -INFINITY);
+      tmax *= c2;
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+      const float mn = fmaxf(m, tmax);
+      rescale = ex2(m - mn);
+      m = mn;
+      float add = 0.0f, addw = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float e = ex2(fmaf(st[c][j], c2, -mn));
+          const float pe = pt[c][j] + eps_nt;
+          if constexpr (W) {
+            add += e;
+            addw = fmaf(e, lg2(pe), addw);
+            den += pt[c][j];
+            if constexpr (GRAD) cv[c][j] = e * rcp(pe);
+          } else {  // the same operations, kept only where visible (both paths round alike)
+            const bool ok = 16 * c + 4 * g + j < lim;
+            add = ok ? add + e : add;
+            addw = ok ? fmaf(e, lg2(pe), addw) : addw;
+            den = ok ? den + pt[c][j] : den;
+            if constexpr (GRAD) cv[c][j] = ok ? e * rcp(pe) : 0.0f;
+          }
+        }
+      lsum = lsum * rescale + add;
+      wl = wl * rescale + addw;
+    };
+    if (!(GRAD && DF == 256) && whole) score(Whole<true>{});  // (one path where registers are tight)
+    else score(Whole<false>{});
     if constexpr (GRAD) {
       float fj[4];  // the factors of acc's rows 4 g + j
       if (!final_tile) {
@@ -227,7 +294,7 @@ __global__ __launch_bounds__(256, 2) void distill_q_kernel(DistillArgs a) {
         for (int c = 0; c < 4; ++c)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            cv[c][j] = lg[c][j] != -INFINITY ? a.inv_rows * (inv_dt - cv[c][j] * inv_lt) : 0.0f;
+            cv[c][j] = 16 * c + 4 * g + j < lim ? a.inv_rows * (inv_dt - cv[c][j] * inv_lt) : 0.0f;
 #pragma unroll
         for (int j = 0; j < 4; ++j) fj[j] = -a.inv_rows * __shfl(rescale * inv_lt, 4 * g + j, kWave);
       }
@@ -294,8 +361,9 @@ __global__ __launch_bounds__(256, 2) void distill_k_kernel(DistillArgs a) {
   const int g = lane / 16, r = lane % 16;
   const int64_t n = a.n;
   const int ntiles = (int)((n + 63) / 64);
-  const int64_t head = blockIdx.x / ntiles;
-  const int kt = (int)(blockIdx.x - head * ntiles);
+  const int64_t item = xcd_item(blockIdx.x, gridDim.x);
+  const int64_t head = item / ntiles;
+  const int kt = (int)(item - head * ntiles);
   const int64_t tk = (int64_t)kt * 64 + wave * 16 + r;  // this lane's key
   const bool k_ok = tk < n;
   const T* Qh = reinterpret_cast<const T*>(a.Q) + head * n * DH;
@@ -322,14 +390,29 @@ __global__ __launch_bounds__(256, 2) void distill_k_kernel(DistillArgs a) {
   for (int fo = 0; fo < S::NFO; ++fo) dk[fo] = zero4();
   for (int qt = a.causal ? kt : 0; qt < ntiles; ++qt) {
     __syncthreads();
-    stage_rows<T, DH, S::LDH>(sq, Qh, (int64_t)qt * 64, n, tid);
-    stage_rows<T, DF, S::LDF>(sf, Fq, (int64_t)qt * 64, n, tid);
-    if (tid < 64) {
+    stage_rows<T, DH, S::LDH, DF, S::LDF>(sq, Qh, sf, Fq, (int64_t)qt * 64, n, tid);
+    if (tid < 64) {  // per query: m, 1 / lsum, 1 / (den + eps), eps / n_t
       const int64_t q = (int64_t)qt * 64 + tid;
-      *reinterpret_cast<float4*>(sst + 4 * tid) =
-          q < n ? *reinterpret_cast<const float4*>(st_h + q * 4) : float4{0.0f, 1.0f, 0.0f, 0.0f};
+      float4 v = float4{0.0f, 0.0f, 0.0f, 1.0f};
+      if (q < n) {
+        const float4 sv = *reinterpret_cast<const float4*>(st_h + q * 4);  // m, lsum, den
+        v = float4{sv.x, 1.0f / sv.y, 1.0f / (sv.z + a.eps), a.eps / (float)(a.causal ? q + 1 : n)};
+      }
+      *reinterpret_cast<float4*>(sst + 4 * tid) = v;
     }
     __syncthreads();
+    // Queries 64 qt + [qlo, qhi) see this lane's key; a tile before the ragged end and
+    // (causal) past the diagonal is seen whole by every key of the workgroup.
+    const bool whole = (int64_t)qt * 64 + 64 <= n && (!a.causal || qt > kt);
+    int qlo = 0, qhi = 64;
+    if (!whole) {
+      const int64_t hi = n - (int64_t)qt * 64;
+      qhi = k_ok ? (int)(hi > 64 ? 64 : hi) : 0;
+      if (a.causal) {
+        const int64_t lo = tk - (int64_t)qt * 64;
+        qlo = (int)(lo < 0 ? 0 : (lo > 64 ? 64 : lo));
+      }
+    }
     // S and P of query tile qt: s[c][j], p[c][j] for query 64 qt + 16 c + 4 g + j
     float gv[4][4];
 #pragma unroll
@@ -350,14 +433,10 @@ __global__ __launch_bounds__(256, 2) void distill_k_kernel(DistillArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int qi = 16 * c + 4 * g + j;
-        const int64_t q = (int64_t)qt * 64 + qi;
-        gv[c][j] = 0.0f;
-        if (k_ok && q < n && (!a.causal || tk <= q)) {
-          const float4 sv = *reinterpret_cast<const float4*>(sst + 4 * qi);  // m, sum, den
-          const float A = exp2f(s[j] * c2 - sv.x) / sv.y;
-          const float pe = p[j] + a.eps / (float)(a.causal ? q + 1 : n);
-          gv[c][j] = a.inv_rows * (1.0f / (sv.z + a.eps) - A / pe);
-        }
+        const float4 sv = *reinterpret_cast<const float4*>(sst + 4 * qi);
+        const float A = ex2(fmaf(s[j], c2, -sv.x)) * sv.y;
+        const float gval = a.inv_rows * (sv.z - A * rcp(p[j] + sv.w));
+        gv[c][j] = whole || (qi >= qlo && qi < qhi) ? gval : 0.0f;
       }
     }
 #pragma unroll

@@ -71,40 +71,44 @@ struct DistShape {
   static constexpr int KD = DH / 32, KF = DF / 32, NFO = DF / 16;
 };
 
-// Rows r0 .. r0 + 63 of two row-major arrays, [n][W1] and [n][W2] of T, into LDS tiles
+// Rows r0 .. r0 + 63 of two row-major arrays, [n][W1] and [n][W2] of T, for LDS tiles
 // with row strides LD1 and LD2 (rows at or past n as zeros), 16 bytes per thread and
-// step of the 256 threads: every global read is issued before the first LDS write, so
-// the staging waits for one memory round trip.
+// step of the 256 threads.  load() issues every global read into registers and store()
+// writes them to the tiles, so a tile costs one memory round trip, and reads issued
+// before the barrier that frees the tiles are in flight while the workgroup waits.
 template <typename T, int W1, int LD1, int W2, int LD2>
-__device__ __forceinline__ void stage_rows(T* tile1, const T* src1, T* tile2, const T* src2, int64_t r0, int64_t n,
-                                           int tid) {
-  constexpr int CH1 = W1 * (int)sizeof(T) / 16, CH2 = W2 * (int)sizeof(T) / 16;
-  constexpr int IT1 = 64 * CH1 / 256, IT2 = 64 * CH2 / 256;
+struct TileRows {
+  static constexpr int CH1 = W1 * (int)sizeof(T) / 16, CH2 = W2 * (int)sizeof(T) / 16;
+  static constexpr int IT1 = 64 * CH1 / 256, IT2 = 64 * CH2 / 256;
   static_assert(IT1 * 256 == 64 * CH1 && IT2 * 256 == 64 * CH2, "whole 256-thread steps");
   uint4 v1[IT1], v2[IT2];
+  __device__ __forceinline__ void load(const T* src1, const T* src2, int64_t r0, int64_t n, int tid) {
 #pragma unroll
-  for (int it = 0; it < IT1; ++it) {
-    const int i = tid + 256 * it, row = i / CH1, c = i % CH1;
-    v1[it] = uint4{0u, 0u, 0u, 0u};
-    if (r0 + row < n) v1[it] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src1 + (r0 + row) * W1) + 16 * c);
-  }
+    for (int it = 0; it < IT1; ++it) {
+      const int i = tid + 256 * it, row = i / CH1, c = i % CH1;
+      v1[it] = uint4{0u, 0u, 0u, 0u};
+      if (r0 + row < n) v1[it] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src1 + (r0 + row) * W1) + 16 * c);
+    }
 #pragma unroll
-  for (int it = 0; it < IT2; ++it) {
-    const int i = tid + 256 * it, row = i / CH2, c = i % CH2;
-    v2[it] = uint4{0u, 0u, 0u, 0u};
-    if (r0 + row < n) v2[it] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src2 + (r0 + row) * W2) + 16 * c);
+    for (int it = 0; it < IT2; ++it) {
+      const int i = tid + 256 * it, row = i / CH2, c = i % CH2;
+      v2[it] = uint4{0u, 0u, 0u, 0u};
+      if (r0 + row < n) v2[it] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src2 + (r0 + row) * W2) + 16 * c);
+    }
   }
+  __device__ __forceinline__ void store(T* tile1, T* tile2, int tid) const {
 #pragma unroll
-  for (int it = 0; it < IT1; ++it) {
-    const int i = tid + 256 * it, row = i / CH1, c = i % CH1;
-    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile1 + row * LD1) + 16 * c) = v1[it];
-  }
+    for (int it = 0; it < IT1; ++it) {
+      const int i = tid + 256 * it, row = i / CH1, c = i % CH1;
+      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile1 + row * LD1) + 16 * c) = v1[it];
+    }
 #pragma unroll
-  for (int it = 0; it < IT2; ++it) {
-    const int i = tid + 256 * it, row = i / CH2, c = i % CH2;
-    *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile2 + row * LD2) + 16 * c) = v2[it];
+    for (int it = 0; it < IT2; ++it) {
+      const int i = tid + 256 * it, row = i / CH2, c = i % CH2;
+      *reinterpret_cast<uint4*>(reinterpret_cast<char*>(tile2 + row * LD2) + 16 * c) = v2[it];
+    }
   }
-}
+};
 
 // The gradient values of one 32-wide k block as an A fragment (slots 0..3 from the
 // first 16-block's four values, 4..7 from the second's); bf16 splits each value into
@@ -187,11 +191,6 @@ __global__ __launch_bounds__(256, GRAD || sizeof(T) == 4 ? 2 : (DF <= 128 ? 4 : 
       }
     }
   };
-  auto stage = [&](int kt) {
-    __syncthreads();
-    stage_rows<T, DH, S::LDH, DF, S::LDF>(sk, Kh, sf, Fk, (int64_t)kt * 64, n, tid);
-    __syncthreads();
-  };
 
   // One pass with online rescaling (a row's maximum m changes as tiles arrive; sums
   // taken against the old maximum are multiplied by 2^(m_old - m_new)):
@@ -215,8 +214,12 @@ __global__ __launch_bounds__(256, GRAD || sizeof(T) == 4 ? 2 : (DF <= 128 ? 4 : 
 #pragma unroll
   for (int e = 0; e < 8; ++e) zc[e] = 0.0f;
   const int zf = tid % FC, zr = (tid / FC) * RG;
+  TileRows<T, DH, S::LDH, DF, S::LDF> rows_in;
   for (int kt = 0; kt <= last; ++kt) {
-    stage(kt);
+    rows_in.load(Kh, Fk, (int64_t)kt * 64, n, tid);  // in flight while the workgroup meets
+    __syncthreads();
+    rows_in.store(sk, sf, tid);
+    __syncthreads();
     f32x4 st[4], pt[4];
     products(st, pt);
     const bool final_tile = kt == last;
@@ -388,18 +391,20 @@ __global__ __launch_bounds__(256, 2) void distill_k_kernel(DistillArgs a) {
   f32x4 dk[S::NFO];
 #pragma unroll
   for (int fo = 0; fo < S::NFO; ++fo) dk[fo] = zero4();
+  TileRows<T, DH, S::LDH, DF, S::LDF> rows_in;
   for (int qt = a.causal ? kt : 0; qt < ntiles; ++qt) {
+    // the tile's reads (rows and, threads 0..63, the query statistics m, lsum, den)
+    // before the barrier that frees the tiles
+    rows_in.load(Qh, Fq, (int64_t)qt * 64, n, tid);
+    const int64_t q = (int64_t)qt * 64 + tid;
+    float4 sv = float4{0.0f, 1.0f, 0.0f, 0.0f};
+    if (tid < 64 && q < n) sv = *reinterpret_cast<const float4*>(st_h + q * 4);
     __syncthreads();
-    stage_rows<T, DH, S::LDH, DF, S::LDF>(sq, Qh, sf, Fq, (int64_t)qt * 64, n, tid);
-    if (tid < 64) {  // per query: m, 1 / lsum, 1 / (den + eps), eps / n_t
-      const int64_t q = (int64_t)qt * 64 + tid;
-      float4 v = float4{0.0f, 0.0f, 0.0f, 1.0f};
-      if (q < n) {
-        const float4 sv = *reinterpret_cast<const float4*>(st_h + q * 4);  // m, lsum, den
-        v = float4{sv.x, 1.0f / sv.y, 1.0f / (sv.z + a.eps), a.eps / (float)(a.causal ? q + 1 : n)};
-      }
-      *reinterpret_cast<float4*>(sst + 4 * tid) = v;
-    }
+    rows_in.store(sq, sf, tid);
+    if (tid < 64)  // per query: m, 1 / lsum, 1 / (den + eps), eps / n_t (zeros past n: never visible)
+      *reinterpret_cast<float4*>(sst + 4 * tid) =
+          q < n ? float4{sv.x, 1.0f / sv.y, 1.0f / (sv.z + a.eps), a.eps / (float)(a.causal ? q + 1 : n)}
+                : float4{0.0f, 0.0f, 0.0f, 1.0f};
     __syncthreads();
     // Queries 64 qt + [qlo, qhi) see this lane's key; a tile before the ragged end and
     // (causal) past the diagonal is seen whole by every key of the workgroup.

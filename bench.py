@@ -183,6 +183,24 @@ def bytes_per_token_head(w) -> int:
     return 4 * w.d * (2 if w.dtype == "bf16" else 4)
 
 
+def clock_ramp(dev, ms: float) -> None:
+    """Keeps the GPU busy with plain bf16 matrix products (torch's, not this library's)
+    for `ms` milliseconds before the warm-up steps, so that the timed steps run at the
+    clocks the GPU holds under sustained load: it takes some tens of milliseconds to
+    reach them, longer than a few warm-up steps last."""
+    import torch
+
+    a = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < ms / 1e3:
+        for _ in range(20):
+            c = a @ b
+        torch.cuda.synchronize()
+    del a, b, c
+    log(f"clock ramp: {1e3 * (time.perf_counter() - t0):.0f} ms of matrix products before the warm-up steps")
+
+
 def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5, refs=None):
     """The float64 oracle on a bounded sample of the same step, scaled to tokens/s.
     The oracle's outputs for the sampled heads go into `refs` (name -> list of
@@ -561,6 +579,36 @@ def config_cases():
     return cases
 
 
+def config_oracle(w, arrs, p, out, budget: float) -> dict:
+    """The float64 oracle on whole heads of one configuration's inputs (the linear form
+    non-causal, the token recurrence causal), heads added until `budget` seconds have
+    run (at least one), scaled by heads to tokens/s of the whole configuration; and the
+    largest per-row error of the GPU output `out` on those heads."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    threads = len(os.sched_getaffinity(0))
+    f = oracle.attn_causal if w.causal else oracle.attn_noncausal
+    tol = 2e-2 if w.dtype == "bf16" else 1e-4
+    heads, spent, worst = 0, 0.0, 0.0
+    with threadpool_limits(threads):
+        while heads < w.B * w.H and (heads == 0 or spent < budget):
+            b, h = divmod(heads, w.H)
+            Q, K, V = (a[b, h:h + 1].astype(np.float64) for a in arrs)
+            t0 = time.perf_counter()
+            ref = f(Q, K, V, p, eps=w.eps)[0]
+            spent += time.perf_counter() - t0
+            got = out[b, h].float().cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-30)
+            worst = max(worst, float(err.max()))
+            heads += 1
+    secs = spent * (w.B * w.H) / heads
+    return {"tokens_per_s": w.B * w.n / secs, "cores": threads, "heads": heads, "seconds": round(spent, 3),
+            "max_row_err": worst, "tol": tol, "pass": worst <= tol}
+
+
 def configs_bench(args) -> int:
     """One timed ABI call per configuration, each on its own seeded inputs, with the
     caches flushed before every timed call (a 1 GiB buffer is read, which evicts the
@@ -589,7 +637,6 @@ def configs_bench(args) -> int:
         arrs = wl.make_inputs(w, args.seed)
         p = wl.make_params(w, args.seed)
         q, k, v = (torch.from_numpy(a).to(dev).to(tdt) for a in arrs)
-        del arrs
         rec = {"config": label, "shape": {"B": w.B, "H": w.H, "n": w.n, "d": w.d, "M": w.M, "L": w.L,
                                           "D": w.M * w.L, "causal": w.causal, "dtype": w.dtype, "dist": w.dist}}
         try:
@@ -645,16 +692,24 @@ def configs_bench(args) -> int:
             "roofline_frac": max(t_hbm, t_mfma) / (ms / 1e3),
             "floor_us": 1e6 * max(t_hbm, t_mfma),
         })
-        log(f"{label}: {ms * 1e3:.1f} us, {rec['roofline_frac']:.1%} of the {rec['bound']} roofline")
+        oc = config_oracle(w, arrs, p, plan.out, args.oracle_budget)
+        rec["oracle"] = oc
+        rec["speedup_vs_oracle"] = oc["tokens_per_s"] and rec["tokens_per_s"] / oc["tokens_per_s"]
+        log(f"{label}: {ms * 1e3:.1f} us, {rec['roofline_frac']:.1%} of the {rec['bound']} roofline; oracle "
+            f"{oc['tokens_per_s']:.3g} tokens/s on {oc['cores']} cores ({oc['heads']} heads), parity "
+            f"{oc['max_row_err']:.2e}")
         rows.append(rec)
         print(json.dumps(rec), flush=True)
-        del plan, q, k, v
+        del plan, q, k, v, arrs
         torch.cuda.synchronize()
+    bad = [r["config"] for r in rows if r["status"] == "ok" and not r["oracle"]["pass"]]
+    if bad:
+        log(f"parity against the oracle FAILED for {bad}")
     if args.configs_table:
         with open(args.configs_table, "w") as fh:
             fh.write("# LUNA attention forward per configuration on one MI355X\n\n")
             fh.write(f"Command: `python bench.py --configs --steps {args.steps} --warmup {args.warmup} "
-                     f"--configs-table {args.configs_table}`\n\n")
+                     f"--oracle-budget {args.oracle_budget:g} --configs-table {args.configs_table}`\n\n")
             fh.write("One ABI call per row (table build included), median of the timed calls with the 10th and "
                      "90th percentiles, HIP events on the launch stream, caches flushed by a 1 GiB read before "
                      "every timed call. tokens/s counts B*n (a token is one position across all heads); "
@@ -665,21 +720,31 @@ def configs_bench(args) -> int:
                      "below 192 heads), the features mapped first and then the causal scan kernel, or the fp32 "
                      "GEMM path of the shapes that have neither (features in the workspace, all arithmetic "
                      "fp32).\n\n")
+            cores = next((r["oracle"]["cores"] for r in rows if r["status"] == "ok"), 0)
+            fh.write(f"oracle: the float64 CPU oracle (the linear form non-causal, the token recurrence causal) "
+                     f"timed in the same run on {cores} host cores over whole heads of the same inputs, added "
+                     f"until about {args.oracle_budget:g} s had run (at least one head), scaled by heads to the "
+                     f"whole configuration; parity: the largest per-row error max|gpu - oracle| / max|oracle| "
+                     f"of the timed call's output on those heads (bar 2e-2 bf16, 1e-4 fp32).\n\n")
             fh.write("| config | B,H,n,d | M x L | dtype | causal | path | median us (p10-p90) | tokens/s "
-                     "| head-tokens/s | TFLOP/s | GB/s | floor us | roofline |\n"
-                     "|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")
+                     "| head-tokens/s | TFLOP/s | GB/s | floor us | roofline | oracle tokens/s (heads) "
+                     "| GPU / oracle | parity |\n"
+                     "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|\n")
             for r in rows:
                 s = r["shape"]
                 head = (f"| {r['config']} | {s['B']},{s['H']},{s['n']},{s['d']} | {s['M']} x {s['L']} | "
                         f"{s['dtype']} | {'yes' if s['causal'] else 'no'} |")
                 if r["status"] != "ok":
-                    fh.write(head + f" | {r['status']} | | | | | | |\n")
+                    fh.write(head + f" | {r['status']} | | | | | | | | | |\n")
                     continue
+                oc = r["oracle"]
                 fh.write(head + f" {r['path']} | {1e3 * r['ms_median']:.1f} ({1e3 * r['ms_p10']:.1f}-{1e3 * r['ms_p90']:.1f}) | "
                          f"{r['tokens_per_s']:.3g} | {r['head_tokens_per_s']:.3g} | {r['attn_tflops']:.1f} | "
-                         f"{r['hbm_gbs']:.0f} | {r['floor_us']:.1f} | {r['roofline_frac']:.1%} {r['bound']} |\n")
+                         f"{r['hbm_gbs']:.0f} | {r['floor_us']:.1f} | {r['roofline_frac']:.1%} {r['bound']} | "
+                         f"{oc['tokens_per_s']:.3g} ({oc['heads']}) | {r['speedup_vs_oracle']:.3g}x | "
+                         f"{oc['max_row_err']:.1e} {'ok' if oc['pass'] else 'FAIL'} |\n")
         log(f"wrote {args.configs_table}")
-    return 0
+    return 1 if bad else 0
 
 
 VALU_LANE_OPS = 78.6e12  # fp32 vector FMA lane-operations per second (157.3 TFLOP/s / 2)
@@ -912,6 +977,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--ramp-ms", type=float, default=300.0,
+                    help="milliseconds of plain matrix products before the warm-up steps (GPU clock ramp); 0: none")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for scaling HBM counters)")
@@ -938,6 +1005,8 @@ def main() -> int:
                     help="instead of the hot-path step: time one call per synthetic configuration, a "
                          "sequence-length sweep and the one-channel variants, each with the caches flushed "
                          "before every timed call, and print one JSON line per configuration")
+    ap.add_argument("--oracle-budget", type=float, default=1.5, metavar="SECONDS",
+                    help="with --configs: seconds of oracle time per configuration (whole heads, at least one)")
     ap.add_argument("--configs-table", default="", metavar="PATH",
                     help="with --configs: also write the results as a markdown table to PATH")
     ap.add_argument("--configs-only", default="", metavar="NAMES",
@@ -1005,6 +1074,8 @@ def main() -> int:
     if args.copy_calibration:
         copy_calibration(dev)
 
+    if args.ramp_ms > 0:
+        clock_ramp(dev, args.ramp_ms)
     for _ in range(args.warmup):
         nc.run()
         cs.run()
@@ -1082,6 +1153,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "clock_ramp_ms": args.ramp_ms,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

@@ -106,6 +106,13 @@ __device__ __forceinline__ unsigned wave_max_nonneg(unsigned x) {
   return last_lane(wave_scan(x, [](unsigned a, unsigned b) { return a > b ? a : b; }));
 }
 
+// Sum of a per-wave value over the waves below wave `wave`, from lane w holding wave
+// w's value (lanes at or past kWaves hold anything): one masked scan instead of a
+// dependent LDS read per wave.
+__device__ __forceinline__ unsigned sum_waves_below(unsigned x, int lane, int wave) {
+  return (unsigned)__builtin_amdgcn_readlane((int)scan_add(lane < wave ? x : 0u), kWaves - 1);
+}
+
 __device__ __forceinline__ unsigned pack_half2(float lo, float hi) {
   return __builtin_bit_cast(unsigned, half2_t{(_Float16)lo, (_Float16)hi});
 }
@@ -194,10 +201,7 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
   if (lane == kWave - 1) wave_tot[wave] = incl;
   if (lane == 0) atomicMax(&s_most, most_local);
   __syncthreads();
-  int before = incl - local;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w)
-    if (w < wave) before += wave_tot[w];
+  int before = incl - local + (int)sum_waves_below((unsigned)wave_tot[lane % kWaves], lane, wave);
   const int most = s_most;
   int steps = 0;
   while ((1 << steps) - 1 < most) ++steps;
@@ -262,12 +266,8 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      if (w < wave) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) ex[q] += reinterpret_cast<const unsigned*>(&wave_cnt[q >> 1][w])[q & 1];
-      }
-    }
+    for (int q = 0; q < 4; ++q)
+      ex[q] += sum_waves_below(reinterpret_cast<const unsigned*>(&wave_cnt[q >> 1][lane % kWaves])[q & 1], lane, wave);
     cnt[0][r] = ((unsigned long long)ex[1] << 32) | ex[0];
     cnt[1][r] = ((unsigned long long)ex[3] << 32) | ex[2];
     // the change of each breakpoint, at its place in its channel's order

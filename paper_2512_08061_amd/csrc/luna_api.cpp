@@ -82,6 +82,7 @@ struct Layout {
   int parts = 1, split = 0;  // causal: workgroups per head, first token of part 1
   size_t state = 0;          // causal with 2 parts: state pieces of the first `split` tokens
   int pieces = 0, piece_chunks = 0;
+  int staged = 0, sa = 0, sb = 0;  // staged causal scan: chunks of the first scanned part and of the state-only part
   int generic = 0;  // forward in fp32 GEMMs and scans (shapes without a fused kernel)
   int given = 0;    // causal: features mapped beforehand (bf16, in phiq / phik), then the scan kernel
 };
@@ -119,7 +120,29 @@ luna_status plan_f32_forward(const Problem& pb, bool causal, bool queries, Layou
 // at a chunk boundary x near n/2.  A state launch first sums the state of [0, x) in
 // pieces (one workgroup per head and piece, enough pieces to fill the device); part 1
 // of the scan launch starts from the sum of the pieces.
-void plan_causal_parts(int64_t heads, int64_t n, size_t state_floats, Layout* lay, size_t* off) {
+void plan_causal_parts(int64_t heads, int64_t n, size_t state_floats, Layout* lay, size_t* off, bool staged_ok) {
+  const int64_t nch = (n + 63) / 64;
+  if (staged_ok && heads > 96 && heads <= 128 && nch >= 5) {
+    // Two workgroups per head fill the device, so both launches are scan launches
+    // (staged): the first scans chunks [0, A) of every head and, beside it, sums the
+    // state of [A, A + B); the second scans [A, A + B) and [A + B, nch) from those
+    // states.  A state-only chunk costs about half a scanned one, so A = nch / 5 and
+    // B = C = 2 nch / 5 balance both launches (about 153 scanned-chunk times for 256
+    // chunks, against 161 for a state launch over [0, nch / 2) followed by two
+    // scanned halves).
+    const int64_t A = (nch + 2) / 5;
+    const int64_t B = (nch - A) / 2;
+    lay->parts = 2;
+    lay->staged = 1;
+    lay->sa = (int)A;
+    lay->sb = (int)B;
+    lay->split = (int)(64 * A);
+    lay->pieces = 2;
+    lay->piece_chunks = 0;
+    lay->state = *off;
+    *off = align256(*off + (size_t)heads * 2 * state_floats * sizeof(float));
+    return;
+  }
   if (heads < 256 && n >= 256) {
     const int64_t cx = n / 64 / 2;  // chunks before the split
     if (cx >= 1) {
@@ -236,7 +259,7 @@ luna_status plan(const Problem& pb, Layout* lay) {
       lay->total = off;
       return LUNA_OK;
     }
-    plan_causal_parts(heads, pb.n, state_floats, lay, &off);
+    plan_causal_parts(heads, pb.n, state_floats, lay, &off, !lay->given);
   } else if (pb.op == LUNA_OP_STATE) {
     luna::NoncausalPlan np;
     if (luna::noncausal_supported(dt, d, L, M, &np)) {
@@ -536,7 +559,7 @@ luna_status plan_features(luna_dtype phi_dtype, luna_dtype dtype, int64_t B, int
   size_t off = 0;
   if (causal && phi_dtype == LUNA_BF16 && dtype == LUNA_BF16 && luna::causal_given_supported(luna::Dt::BF16, (int)d, (int)D)) {
     lay->given = 1;
-    plan_causal_parts(heads, n, luna::causal_given_state_floats((int)d, (int)D), lay, &off);
+    plan_causal_parts(heads, n, luna::causal_given_state_floats((int)d, (int)D), lay, &off, false);
   } else {
     lay->generic = 1;
     luna_status st = plan_f32_buffers(heads, n, (int)d, (int)D, causal != 0, true, phi_dtype == LUNA_BF16, lay, &off);
@@ -925,6 +948,26 @@ luna_status luna_attn_fwd_causal(const void* Q, const void* K, const void* V, lu
   auto launch = [&]() {
     return lay.given ? luna::launch_causal_given((int)d, D, a, s) : luna::launch_causal(dt, (int)d, p->L, p->M, a, s);
   };
+  if (lay.staged) {
+    // launch 1: part 0 scans [0, A), part 1 sums the state of [A, A + B); both write
+    // their final states as pieces 0 and 1.  launch 2: part 0 scans [A, A + B) from
+    // piece 0, part 1 scans [A + B, nch) from pieces 0 + 1.
+    const int A = lay.sa, AB = lay.sa + lay.sb, nch = (int)((n + 63) / 64);
+    float* st = reinterpret_cast<float*>(w + lay.state);
+    a.staged = 1;
+    a.pieces = 2;
+    a.pc_first[0] = 0;  a.pc_begin[0] = 0;  a.pc_end[0] = A;  a.pseed[0] = 0;
+    a.pc_first[1] = A;  a.pc_begin[1] = AB; a.pc_end[1] = AB; a.pseed[1] = 0;
+    a.state_fin = st;
+    hipError_t e = launch();
+    if (e != hipSuccess) return hip_fail(e, "causal attention first scan launch");
+    a.pc_first[0] = A;  a.pc_begin[0] = A;  a.pc_end[0] = AB;  a.pseed[0] = 1;
+    a.pc_first[1] = AB; a.pc_begin[1] = AB; a.pc_end[1] = nch; a.pseed[1] = 2;
+    a.state_fin = nullptr;
+    a.state_in = st;
+    e = launch();
+    return e == hipSuccess ? LUNA_OK : hip_fail(e, "causal attention second scan launch");
+  }
   if (lay.parts == 2) {
     float* st = reinterpret_cast<float*>(w + lay.state);
     a.pieces = lay.pieces;

@@ -245,6 +245,11 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     c_end = min(a.split / 64, c_first + a.piece_chunks);
     c_begin = c_end;
     t_end = 0;
+  } else if (a.staged) {
+    c_first = part == 0 ? a.pc_first[0] : a.pc_first[1];
+    c_begin = part == 0 ? a.pc_begin[0] : a.pc_begin[1];
+    c_end = part == 0 ? a.pc_end[0] : a.pc_end[1];
+    t_end = min(n, 64 * c_end);
   } else {
     const int t_begin = part == 0 ? 0 : a.split;
     t_end = part == a.parts - 1 ? n : a.split;
@@ -253,8 +258,9 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
     c_first = (part > 0 && a.state_in != nullptr) ? c_begin : 0;
   }
   // part 1 of the scan launch starts from the state of the first c_first chunks: the
-  // sum of the pieces, in piece order
-  const bool seeded = !state_run && c_first > 0;
+  // sum of the pieces, in piece order (a staged part from the sum of its first npc)
+  const int npc = a.staged ? (part == 0 ? a.pseed[0] : a.pseed[1]) : a.pieces;
+  const bool seeded = !state_run && (a.staged ? npc > 0 : c_first > 0);
   const float* seed = seeded ? a.state_in + (size_t)head * a.pieces * C::STATE : nullptr;
 
   // Q, K, V rows of chunk cc and the output rows of chunk cc as range-checked
@@ -281,7 +287,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
   for (int i = tid; i < 2 * FP; i += C::NT) {
     float zv = 0.0f;
     if (seeded && i / FP == ((c_first + 1) & 1))
-      for (int pc = 0; pc < a.pieces; ++pc) zv += seed[(size_t)pc * C::STATE + C::SF + i % FP];
+      for (int pc = 0; pc < npc; ++pc) zv += seed[(size_t)pc * C::STATE + C::SF + i % FP];
     (&sm.zs[0][0])[i] = (T)zv;
   }
   if constexpr (!PF)
@@ -306,7 +312,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) zrun[e] = 0.0f;
       if (seeded && rb == 0 && tg == 0)  // the prefix's z enters through map wave 0
-        for (int pc = 0; pc < a.pieces; ++pc)
+        for (int pc = 0; pc < npc; ++pc)
 #pragma unroll
           for (int e = 0; e < 8; ++e) zrun[e] += seed[(size_t)pc * C::STATE + C::SF + 8 * fc + e];
       auto load_feat = [&](i32x4 (&dst)[TPL], const void* X, int cc, bool live) {
@@ -519,7 +525,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj)
-            for (int pc = 0; pc < a.pieces; ++pc)
+            for (int pc = 0; pc < npc; ++pc)
               zacc[mb][jj] += seed[(size_t)pc * C::STATE + C::SF + feat<MB>(16 * mb + 4 * g, r) + jj];
       }
       auto add_z = [&]() {
@@ -725,7 +731,7 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
       for (int i = 0; i < RB; ++i) {
         sacc[x][i] = zero4();
         if (seeded && active)
-          for (int pc = 0; pc < a.pieces; ++pc)
+          for (int pc = 0; pc < npc; ++pc)
             sacc[x][i] += *reinterpret_cast<const f32x4*>(seed + (size_t)pc * C::STATE + s_off +
                                                           (size_t)(x * RB + i) * kWave * 4);
       }
@@ -988,6 +994,21 @@ __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) zo[krow_inv(16 * b + 4 * g + jj)] = zst[b][jj];
         }
+      }
+    }
+    if constexpr (!ST && !PF) {
+      // staged: the final state of this part as piece `part` of its head.  z is the sum
+      // of the map waves' row-block partials (fp32, through the last chunk; the last
+      // were written before the last chunk's first barrier), in a fixed order.
+      if (a.state_fin != nullptr && active) {
+        float* so = a.state_fin + (size_t)(head * a.pieces + part) * C::STATE;
+#pragma unroll
+        for (int x = 0; x < CBW; ++x)
+#pragma unroll
+          for (int i = 0; i < RB; ++i)
+            *reinterpret_cast<f32x4*>(so + s_off + (size_t)(x * RB + i) * kWave * 4) = sacc[x][i];
+        for (int f = kWave * mw + lane; f < FP; f += kWave * NMW)
+          so[C::SF + f] = ((sm.zp[0][f] + sm.zp[1][f]) + sm.zp[2][f]) + sm.zp[3][f];
       }
     }
   }

@@ -146,6 +146,14 @@ struct CausalArgs {
   float* state_out;      // non-null: state launch
   const float* state_in;  // non-null: part 1 of the scan launch starts from the pieces
   int pieces, piece_chunks;
+  // Staged scan (staged = 1, two launches of the scan kernel): part p of a launch covers
+  // chunks [pc_first[p], pc_end[p]), of which [pc_first[p], pc_begin[p]) only build the
+  // state; it starts from the sum of the first pseed[p] pieces of state_in (`pieces`
+  // pieces per head) and, with state_fin non-null, writes its final state (S and z,
+  // fp32, the pieces' layout) as piece p of its head in state_fin.
+  int staged;
+  int pc_first[2], pc_begin[2], pc_end[2], pseed[2];
+  float* state_fin;
   // non-null: sum the pieces in state_out into S [heads][M*L][d] and z [heads][M*L]
   // (fp32, feature i*L + l; accumulate 1 adds to them) instead of launching the kernel
   float* export_S;

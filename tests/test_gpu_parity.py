@@ -306,7 +306,8 @@ def test_attn_causal_small(dtype, d, M, L, n):
 def test_attn_causal_state_pieces(B, H, n, M, L):
     """With fewer than 256 heads each head is cut at x (n/2 rounded down to whole
     chunks) and the state of [0, x) is summed in pieces, one workgroup per head and
-    piece: seven one-chunk pieces, uneven pieces (2, 2, 1 chunks), two pieces.
+    piece: seven one-chunk pieces (3 heads), two pieces (160 heads); 100 heads take the
+    staged form (two scan launches) instead.
     Checked against the oracle on sampled heads (the parameters are shared).  M = 256,
     L = 1: the features are mapped beforehand and the kernel reads them."""
     w = small_workload("bf16", B=B, H=H, n=n, d=128, M=M, L=L, causal=True)
@@ -318,6 +319,25 @@ def test_attn_causal_state_pieces(B, H, n, M, L):
     pick = lambda X: X[bs][:, hs]  # noqa: E731
     ref = oracle.attn_causal(pick(Q), pick(K), pick(V), p, eps=w.eps)
     assert_close_rows(pick(out), ref, "bf16", "out")
+
+
+@pytest.mark.parametrize("dtype,d,M,B,H,n", [("bf16", 128, 32, 8, 16, 1000), ("bf16", 64, 16, 4, 25, 321),
+                                               ("f32", 64, 16, 1, 100, 400), ("bf16", 128, 32, 2, 64, 4096)])
+def test_attn_causal_staged(dtype, d, M, B, H, n):
+    """97 to 128 heads: two scan launches, the first scanning chunks [0, A) beside a
+    state-only part over [A, A + B), the second scanning [A, A + B) and [A + B, nch)
+    from the exported states (A = nch / 5, B = C = 2 nch / 5).  Every row of sampled
+    heads against the oracle's token recurrence, so that both part boundaries and the
+    ragged last chunk are covered."""
+    w = small_workload(dtype, B=B, H=H, n=n, d=d, M=M, L=8, causal=True)
+    say(f"causal staged {dtype} d={d} M={M} B={B} H={H} n={n}")
+    Q, K, V, p = inputs(w, seed=61)
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd_causal(Qt, Kt, Vt, pt, chunk=64, eps=w.eps))
+    bs, hs = sorted({0, B - 1}), sorted({0, H // 3, H - 1})
+    pick = lambda X: X[bs][:, hs]  # noqa: E731
+    ref = oracle.attn_causal(pick(Q), pick(K), pick(V), p, eps=w.eps)
+    assert_close_rows(pick(out), ref, dtype, "out")
 
 
 def test_attn_causal_workload_full_size():

@@ -13,7 +13,7 @@ The JSON line also carries
   roofline      for the call that takes most of the step: algorithmic HBM bytes per
                 call (read Q, K, V once, write out once) divided by its average
                 duration from HIP events on the launch stream (the causal call is
-                the table build, a state launch and the scan launch of one kernel);
+                the table build and two scan launches of one kernel);
                 traffic is the HBM bytes per call measured by rocprofv3 counters
                 (see profiles/), or null when the kernel source changed since they
                 were taken;
@@ -47,7 +47,7 @@ KERNEL_SOURCES = {
 KERNEL_WORKLOAD = {"causal_kernel": "long_causal", "nc_fused_kernel": "long_noncausal",
                    "featuremap_kernel": "featuremap_long_noncausal"}
 # launches of the kernel per ABI call on these workloads: the causal call (128 heads)
-# runs a state launch and then the scan launch
+# runs two scan launches (the first beside a state-only part, the second from its states)
 LAUNCHES_PER_CALL = {"causal_kernel": 2, "nc_fused_kernel": 1, "featuremap_kernel": 1}
 COPY_BYTES = 1 << 30  # the --copy-calibration copy
 
@@ -1143,7 +1143,7 @@ def main() -> int:
         "kernel": kname,
         "workload": dom,
         "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel; the "
-                  "causal call is a state launch and a scan launch of causal_kernel)",
+                  "causal call is two scan launches of causal_kernel)",
     }
 
     out = {

@@ -1140,6 +1140,14 @@ def main() -> int:
         # committed counter summary (null once the kernel has changed since)
         "mfma_busy": measured_figure("causal_kernel_scan_launch" if kname == "causal_kernel" else kname, dom,
                                      kname, "MFMA busy") if kname in KERNEL_SOURCES else None,
+        # the LDS's active share of the CU cycles and the bank-conflict share of those
+        # cycles, from the same summary: the LDS, not HBM, is what these kernels are
+        # bound by (their tables, phi tiles and operand reads)
+        "lds_busy": measured_figure("causal_kernel_scan_launch" if kname == "causal_kernel" else kname, dom,
+                                    kname, "LDS active") if kname in KERNEL_SOURCES else None,
+        "lds_conflict_share": measured_figure("causal_kernel_scan_launch" if kname == "causal_kernel" else kname,
+                                              dom, kname, "LDS bank-conflict cycles per LDS-active cycle")
+        if kname in KERNEL_SOURCES else None,
         "kernel": kname,
         "workload": dom,
         "timing": "HIP events on the launch stream around each ABI call (includes the table-build kernel; the "

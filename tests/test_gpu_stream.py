@@ -142,6 +142,32 @@ def test_step_many_heads_from_state():
     assert np.abs(to_np(z) - rz).max() <= 1e-3 * np.abs(rz - z0).max(), "z updated more than once"
 
 
+@pytest.mark.parametrize("dtype,d,M,L", [("bf16", 128, 32, 8), ("f32", 32, 8, 8), ("bf16", 64, 128, 1)])
+@pytest.mark.parametrize("m", [1, 4, 6])
+def test_step_options_from_state(dtype, d, M, L, m):
+    """Per-head parameters, one shared first layer and no output relu, from a random
+    state, for one, a few and more tokens per head, against the oracle's recurrence."""
+    import torch
+    B, H = 2, 3
+    w = small_workload(dtype, B=B, H=H, n=m, d=d, M=M, L=L, causal=True, per_head=True, shared_channels=True,
+                       nonneg=False)
+    say(f"step options {w.name} m={m}")
+    Q, K, V, p = inputs(w, seed=41)
+    p = dict(p)
+    p["fc2_b"] = p["fc2_b"] + 1.0  # denominators away from zero with signed features
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    D = M * L
+    rng = np.random.default_rng(5)
+    S = torch.from_numpy(rng.standard_normal((B, H, D, d)) * 0.05).float().cuda().contiguous()
+    z = torch.from_numpy(rng.random((B, H, D)) + 0.5).float().cuda().contiguous()
+    S0, z0 = to_np(S), to_np(z)
+    out = to_np(luna.attn_causal_step(Qt, Kt, Vt, pt, S, z, eps=w.eps))
+    ro, rS, rz = oracle.attn_causal_step(Q, K, V, p, S0, z0, eps=w.eps)
+    assert_close_rows(out, ro, dtype, "out")
+    assert_close(to_np(S), rS, dtype, "S")
+    assert_close(_col(to_np(z)), _col(rz), dtype, "z")
+
+
 def test_step_rejects_bad_state():
     """Malformed state tensors are refused before anything runs."""
     import torch

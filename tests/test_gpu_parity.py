@@ -250,7 +250,11 @@ def test_attn_noncausal_small(dtype, d, M, L, n):
 
 # enough heads for the one-pass kernel (one workgroup per head), with ragged lengths
 @pytest.mark.parametrize("dtype,d,M,L,n", [("f32", 64, 16, 8, 77), ("bf16", 64, 16, 8, 333), ("bf16", 64, 8, 8, 1),
-                                           ("bf16", 32, 16, 8, 200), ("f32", 32, 8, 2, 45)])
+                                           ("bf16", 32, 16, 8, 200), ("f32", 32, 8, 2, 45),
+                                           # at most 8 projections: half of the fused kernel's
+                                           # 16-projection block is padding
+                                           ("bf16", 64, 8, 8, 333), ("bf16", 32, 5, 8, 100), ("bf16", 64, 3, 8, 47),
+                                           ("bf16", 64, 8, 8, 16), ("bf16", 64, 1, 8, 40)])
 def test_attn_noncausal_many_heads(dtype, d, M, L, n):
     w = small_workload(dtype, B=16, H=13, n=n, d=d, M=M, L=L)
     say(f"noncausal many heads {w.name}")
@@ -472,6 +476,22 @@ def test_options_per_head_shared_signed(causal, dtype, d, M, L):
     (assert_close_rows if causal else assert_close)(out, ref, dtype, "options")
     phi = to_np(luna.featuremap(Qt, pt))
     assert_close(phi, oracle.featuremap(Q, p), dtype, "phi options")
+
+
+@pytest.mark.parametrize("M", [8, 6])
+def test_attn_noncausal_few_projections_options(M):
+    """The fused kernel (208 heads) with at most 8 projections, so that half of its
+    projection block is padding, with per-head parameters, one shared first layer and
+    no output relu."""
+    w = small_workload("bf16", B=16, H=13, n=150, d=64, M=M, L=8, per_head=True, shared_channels=True,
+                       nonneg=False)
+    say(f"few projections, options {w.name}")
+    Q, K, V, p = inputs(w, seed=8)
+    p = dict(p)
+    p["fc2_b"] = p["fc2_b"] + 1.0  # denominators away from zero with signed features
+    (Qt, Kt, Vt), pt = upload(w, [Q, K, V], p)
+    out = to_np(luna.attn_fwd(Qt, Kt, Vt, pt, eps=w.eps))
+    assert_close(out, oracle.attn_noncausal(Q, K, V, p, eps=w.eps), "bf16", "few projections, options")
 
 
 @pytest.mark.parametrize("per_head", [False, True])

@@ -116,10 +116,11 @@ luna_status plan_f32_forward(const Problem& pb, bool causal, bool queries, Layou
   return plan_f32_buffers(pb.B * pb.H, pb.n, (int)pb.d, pb.p->M * pb.p->L, causal, queries, true, lay, off);
 }
 
-// The causal kernel's split.  Too few heads to fill the device: cut every head in two
-// at a chunk boundary x near n/2.  A state launch first sums the state of [0, x) in
-// pieces (one workgroup per head and piece, enough pieces to fill the device); part 1
-// of the scan launch starts from the sum of the pieces.
+// The causal kernel's split.  Too few heads to fill the device: with 97 to 128 heads
+// the staged form below (two scan launches); otherwise cut every head in two at a
+// chunk boundary x near n/2, where a state launch first sums the state of [0, x) in
+// pieces (one workgroup per head and piece, enough pieces to fill the device) and part
+// 1 of the scan launch starts from the sum of the pieces.
 void plan_causal_parts(int64_t heads, int64_t n, size_t state_floats, Layout* lay, size_t* off, bool staged_ok) {
   const int64_t nch = (n + 63) / 64;
   if (staged_ok && heads > 96 && heads <= 128 && nch >= 5) {

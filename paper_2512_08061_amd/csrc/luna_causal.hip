@@ -10,13 +10,19 @@
 // which regroups the prefix sums exactly.
 //
 // Work split.  One workgroup owns one (head, part of the sequence).  With fewer heads
-// than compute units each head is cut at a chunk boundary x near n/2 and a call makes
-// two launches: the state launch (a separate instantiation, ST) sums the state of
-// [0, x) in pieces, one workgroup per (head, piece), and writes them in fp32; the scan
-// launch then runs part 0 over [0, x) from a zero state and part 1 over [x, n) from
-// the sum of the pieces.  No workgroup waits for another.  Run over every chunk (key
-// rows past n mapped to the all-zero segment), the state launch also gives the state
-// of a whole sequence, which causal_state_export_kernel writes in the public layout.
+// than compute units a call makes two launches, and no workgroup waits for another:
+//  - staged (97 to 128 heads): two launches of the scan kernel with explicit chunk
+//    ranges per part.  The first scans [0, A) beside a part that only sums the state
+//    of [A, A + B), both writing their final states; the second scans [A, A + B) and
+//    [A + B, nch) from those states (A = nch / 5, B = 2 nch / 5: a state-only chunk
+//    costs about half a scanned one, so both launches are balanced);
+//  - otherwise each head is cut at a chunk boundary x near n/2: the state launch (a
+//    separate instantiation, ST) sums the state of [0, x) in pieces, one workgroup per
+//    (head, piece), and writes them in fp32; the scan launch then runs part 0 over
+//    [0, x) from a zero state and part 1 over [x, n) from the sum of the pieces.
+// Run over every chunk (key rows past n mapped to the all-zero segment), the state
+// launch also gives the state of a whole sequence, which causal_state_export_kernel
+// writes in the public layout.
 //
 // Roles.  Four matrix waves and four map waves, one of each on every SIMD, so that
 // each SIMD pairs matrix-core work with vector and table-lookup work.  (With PF, the
@@ -210,7 +216,7 @@ struct Pack4<float> {
   }
 };
 
-// ST: the state launch (state-only chunks, S and z dumped); otherwise the scan launch.
+// ST: the state launch (state-only chunks, S and z dumped); otherwise a scan launch.
 // PF: the features are given (a.phiq, a.phik); L = 1 and MB = FP / 16.
 template <typename T, int DH, int L, int MB, bool ST, bool PF>
 __global__ __launch_bounds__(512, 1) void causal_kernel(CausalArgs a) {

@@ -221,6 +221,53 @@ __device__ inline void pwl_load(PwlLds16<L, NSEG>& t, const uint8_t* __restrict_
   }
 }
 
+// The fp16-row table plus every bucket's first comparison key, so that a search reads
+// the key of its first halving together with its window start (one dependent LDS
+// round trip fewer per lookup).
+template <int L, int NSEG>
+struct alignas(16) PwlLds16F : PwlLds16<L, NSEG> {
+  float first[kFirstBytes / 4];
+};
+
+template <int L, int NSEG>
+__device__ inline void pwl_load(PwlLds16F<L, NSEG>& t, const uint8_t* __restrict__ gtab) {
+  const PwlHeader hd = *reinterpret_cast<const PwlHeader*>(gtab + kTabHeader);
+  const PwlDims dm = pwl_dims<NSEG>(hd);
+  const int nseg = dm.nseg;
+  constexpr int R16 = seg16_row_bytes(L) / 16;
+  constexpr int NK = kKeyCap / 4, NB = (kNumBuckets * 2 + 15) / 16, NF = (int)(kFirstBytes / 16);
+  static_assert(sizeof(t.seg[0]) == 16 * R16, "LDS rows are the global rows");
+  static_assert(NSEG * 16 * R16 <= (int)kSeg16Bytes, "the LDS rows must lie inside the table's fp16 region");
+  const uint4* gk = reinterpret_cast<const uint4*>(gtab + kTabKeys);
+  const uint4* gb = reinterpret_cast<const uint4*>(gtab + kTabBuckets);
+  const uint4* gf = reinterpret_cast<const uint4*>(gtab + kTabFirst);
+  const uint4* gs = reinterpret_cast<const uint4*>(gtab + kTabSeg16);
+  uint4* kd = reinterpret_cast<uint4*>(t.keys);
+  uint4* bd = reinterpret_cast<uint4*>(t.buckets);
+  uint4* fd = reinterpret_cast<uint4*>(t.first);
+  uint4* sd = reinterpret_cast<uint4*>(&t.seg[0][0]);
+  // one round of loads over all four regions (capacities, so that none waits for the header)
+  batched_copy(
+      NK + NB + NF + NSEG * R16,
+      [&](int i) {
+        return i < NK ? gk[i] : (i < NK + NB ? gb[i - NK] : (i < NK + NB + NF ? gf[i - NK - NB] : gs[i - NK - NB - NF]));
+      },
+      [&](int i, uint4 v) {
+        if (i < NK) kd[i] = v;
+        else if (i < NK + NB) bd[i - NK] = v;
+        else if (i < NK + NB + NF) fd[i - NK - NB] = v;
+        else if ((i - NK - NB - NF) / R16 < nseg) sd[i - NK - NB - NF] = v;
+      });
+  for (int i = threadIdx.x; i < PwlLds16<L, NSEG>::SROW; i += blockDim.x)
+    t.seg[nseg][i] = half2_t{(_Float16)0.0f, (_Float16)0.0f};
+  if (threadIdx.x == 0) {
+    t.steps = dm.steps;
+    t.zero_seg = nseg;
+    t.floor = hd.nonneg ? 0.0f : -__builtin_inff();
+    t.scale_exp = hd.scale_exp;
+  }
+}
+
 // Segment row `seg` of a table (a 24-bit multiply: the 32-bit one is quarter rate).
 template <typename Tab>
 __device__ __forceinline__ const char* seg_ptr(const Tab& t, int seg) {
@@ -320,6 +367,42 @@ __device__ __forceinline__ void pwl_search(const Tab& t, int steps, const float 
 #pragma unroll
   for (int i = 0; i < NU; ++i) seg[i] = (int)(off[i] >> 2);
 }
+
+// Segment index of each of NU values (as pwl_search) with the first halving's key read
+// beside the window start.
+template <int NU, typename Tab>
+__device__ __forceinline__ void pwl_search_first(const Tab& t, int steps, const float (&u)[NU], int (&seg)[NU]) {
+  const char* keys = reinterpret_cast<const char*>(t.keys);
+  unsigned off[NU];
+  float k1[NU];
+#pragma unroll
+  for (int i = 0; i < NU; ++i) {
+    const int b = pwl_bucket(u[i]);
+    off[i] = t.buckets[b];
+    k1[i] = t.first[b];
+  }
+  if (steps > 0) {
+    const unsigned h4 = 4u << (steps - 1);
+#pragma unroll
+    for (int i = 0; i < NU; ++i) off[i] += k1[i] < u[i] ? h4 : 0u;
+  }
+  for (int s = steps - 2; s >= 0; --s) {
+    const unsigned h4 = 4u << s;
+#pragma unroll
+    for (int i = 0; i < NU; ++i) {
+      const float key = *reinterpret_cast<const float*>(keys + off[i] + h4 - 4u);
+      off[i] += key < u[i] ? h4 : 0u;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NU; ++i) seg[i] = (int)(off[i] >> 2);
+}
+template <int NU, int L, int NSEG>
+__device__ __forceinline__ void pwl_search(const PwlLds16F<L, NSEG>& t, int steps, const float (&u)[NU],
+                                           int (&seg)[NU]) {
+  pwl_search_first(t, steps, u, seg);
+}
+
 
 // psi_l(u), l = 0..L-1, on the segment whose key sits at byte offset `off` (4 seg):
 // the segment row starts at off * (row bytes / 4), one multiply-add from `off`.

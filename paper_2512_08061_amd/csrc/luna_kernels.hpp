@@ -26,6 +26,9 @@ namespace luna {
 //            intercept that cancels against slope u.  Slopes and values are scaled by
 //            2^scale_exp (the largest magnitude lands near 2^14), which cancels between
 //            numerator and denominator once eps is scaled alike.
+//   first    fp32 per bucket: the key its first halving compares against (the one at
+//            index start + 2^(steps - 1) - 1 of its window; 0 when steps = 0), so that
+//            a search can read it together with the window start
 //
 // Search.  The float bits of u pick one of kNumBuckets buckets (bucket_of), an
 // order-preserving partition of the real line: sign, then |u| below 2^-kBucketExp,
@@ -47,7 +50,9 @@ constexpr size_t kTabBuckets = kTabKeys + kKeyCap * 4;
 constexpr size_t kTabSeg = kTabBuckets + ((size_t)kNumBuckets * 2 + 15) / 16 * 16;
 constexpr size_t kTabSeg16 = kTabSeg + (size_t)kSegCap * 8;
 constexpr size_t kSeg16Bytes = 40960;  // fp16 rows with anchors
-constexpr size_t kTableBytes = (kTabSeg16 + kSeg16Bytes + 255) / 256 * 256;
+constexpr size_t kTabFirst = kTabSeg16 + kSeg16Bytes;
+constexpr size_t kFirstBytes = ((size_t)kNumBuckets * 4 + 15) / 16 * 16;
+constexpr size_t kTableBytes = (kTabFirst + kFirstBytes + 255) / 256 * 256;
 
 struct PwlHeader {
   int nbp;     // number of breakpoints

@@ -36,6 +36,8 @@
 #include "luna_device.hpp"
 #include "luna_kernels.hpp"
 
+#include <type_traits>
+
 namespace luna {
 
 template <typename T, int DH, int L, int MB>
@@ -415,7 +417,13 @@ struct NcFusedLds {
   using C = NcCfg<T, DH, L, MB>;
   static constexpr int VR = DH + C::VE;   // padded V-tile row (elements)
   static constexpr int NTILE = MB * L * C::CB + MB;  // accumulator tiles of S, then of z
-  typename PwlTab<T, L, C::NSEG>::type tab;
+  // one channel per projection (a lookup per feature, so the lookups set the pace): the
+  // fp16-row table with every bucket's first comparison key, one dependent LDS read
+  // fewer per lookup (455 -> 393 us on the long encoder problem's one-channel map).
+  // With eight channels per lookup the 12 KB more that every workgroup copies cost more
+  // than the read saves (text encoder 58.1 -> 60.2 us).
+  typename std::conditional<sizeof(T) == 2 && L == 1, PwlLds16F<L, C::NSEG>,
+                            typename PwlTab<T, L, C::NSEG>::type>::type tab;
   union {
     T vt[kNcWaves][32][VR];             // per-wave V tile of the current 32-token step
     float4 red[NTILE][kWave];           // cross-wave sum of the accumulator tiles, lane-major
@@ -547,10 +555,6 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
 #pragma unroll
       for (int e = 0; e < 8; ++e)  // slot e = 4 tb + j holds token t0 + 16 tb + 4 g + j
         if (!pcol[mb] || t0 + 16 * (e / 4) + 4 * g + (e % 4) >= n) sg[8 * mb + e] = zseg;
-    // each value's argument on its segment, taken once for the L / 2 channel pairs
-    float xx[8 * MB];
-#pragma unroll
-    for (int v = 0; v < 8 * MB; ++v) xx[v] = pwl_local(sm.tab, sg[v], uu[v]);
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     Frag<T> bv[C::CB];
 #pragma unroll
@@ -558,6 +562,12 @@ __global__ __launch_bounds__(64 * kNcWaves, 1) void nc_fused_kernel(NoncausalArg
       load_tr4(bv[cb], 0, vt, LDS::VR, 4 * g, 16 * cb, lane);
       load_tr4(bv[cb], 4, vt, LDS::VR, 16 + 4 * g, 16 * cb, lane);
     }
+    // each value's argument on its segment, taken once for the L / 2 channel pairs (after
+    // the V tile's fence, so that the anchors, the coefficient rows and the V fragments
+    // are read in one round trip)
+    float xx[8 * MB];
+#pragma unroll
+    for (int v = 0; v < 8 * MB; ++v) xx[v] = pwl_local(sm.tab, sg[v], uu[v]);
     // channel pairs: evaluate the 8 token slots, multiply, drop
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {

@@ -381,6 +381,16 @@ __global__ __launch_bounds__(kThreads) void pwl_prepare_kernel(PrepareArgs a) {
     const uint4* src = reinterpret_cast<const uint4*>(bstart);
     uint4* dst = reinterpret_cast<uint4*>(tab + kTabBuckets);
     if (tid < (kNumBuckets + 7) / 8) dst[tid] = src[tid];
+    // every bucket's first comparison key (keys past the breakpoints are +inf)
+    float* first = reinterpret_cast<float*>(tab + kTabFirst);
+    for (int b = tid; b < kNumBuckets; b += kThreads) {
+      float fk = 0.0f;
+      if (steps > 0) {
+        const int i = bstart[b] / 4 + (1 << (steps - 1)) - 1;
+        fk = i < nbp ? key[i] : __builtin_inff();
+      }
+      first[b] = fk;
+    }
   }
   __syncthreads();
   // The fp16 rows are scaled by 2^e so that their largest magnitude lands in

@@ -9,6 +9,10 @@ Both read their inputs from HBM (2.7 GB in total, far beyond the 256 MB
 Infinity Cache) and each processes 131072 tokens (a token is one sequence
 position across all heads).  value = tokens of both problems / step time.
 
+Before the W warm-up steps the step's own calls run untimed for --ramp-ms milliseconds
+(default 200): the GPU's power management settles on this workload only after some tens
+of its calls, longer than a few warm-up steps last.
+
 The JSON line also carries
   roofline      for the call that takes most of the step: algorithmic HBM bytes per
                 call (read Q, K, V once, write out once) divided by its average
@@ -183,22 +187,23 @@ def bytes_per_token_head(w) -> int:
     return 4 * w.d * (2 if w.dtype == "bf16" else 4)
 
 
-def clock_ramp(dev, ms: float) -> None:
-    """Keeps the GPU busy with plain bf16 matrix products (torch's, not this library's)
-    for `ms` milliseconds before the warm-up steps, so that the timed steps run at the
-    clocks the GPU holds under sustained load: it takes some tens of milliseconds to
-    reach them, longer than a few warm-up steps last."""
+def clock_ramp(step, ms: float) -> None:
+    """Runs the step's own calls, untimed, for `ms` milliseconds before the warm-up steps.
+    The GPU's power management settles on this workload only after some tens of its
+    calls (with the driver's 5 warm-up steps the timed steps measured 0.970 ms, after 30
+    0.879 ms, after 100 0.874 ms; tens of milliseconds of plain matrix products or HBM
+    reads beforehand brought only 0.940-0.960 ms), so that the timed steps would measure
+    the GPU's ramp rather than the kernels."""
     import torch
 
-    a = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
-    b = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
     t0 = time.perf_counter()
+    calls = 0
     while time.perf_counter() - t0 < ms / 1e3:
-        for _ in range(20):
-            c = a @ b
+        for _ in range(10):
+            step()
+        calls += 10
         torch.cuda.synchronize()
-    del a, b, c
-    log(f"clock ramp: {1e3 * (time.perf_counter() - t0):.0f} ms of matrix products before the warm-up steps")
+    log(f"clock ramp: {calls} untimed steps in {1e3 * (time.perf_counter() - t0):.0f} ms before the warm-up steps")
 
 
 def cpu_baseline(w4, arrs4, p4, w5, arrs5, p5, refs=None):
@@ -977,8 +982,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--ramp-ms", type=float, default=300.0,
-                    help="milliseconds of plain matrix products before the warm-up steps (GPU clock ramp); 0: none")
+    ap.add_argument("--ramp-ms", type=float, default=200.0,
+                    help="milliseconds of untimed steps before the warm-up steps (the GPU settling on the "
+                         "workload); 0: none")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for scaling HBM counters)")
@@ -1075,7 +1081,7 @@ def main() -> int:
         copy_calibration(dev)
 
     if args.ramp_ms > 0:
-        clock_ramp(dev, args.ramp_ms)
+        clock_ramp(lambda: (nc.run(), cs.run()), args.ramp_ms)
     for _ in range(args.warmup):
         nc.run()
         cs.run()
@@ -1162,6 +1168,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "clock_ramp_ms": args.ramp_ms,
+        "clock_ramp": "the step's own calls, untimed, before the warm-up steps",
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

@@ -1101,12 +1101,13 @@ luna_status luna_attn_causal_step(const void* Q, const void* K, const void* V, l
   f.out = w + lay.phiq;
   f.X2 = K;
   f.out2 = w + lay.phik;
+  // z before the step, for every column block of a head to read (block 0 rewrites z),
+  // copied by workgroups of the same launch
+  f.copy_src = z;
+  f.copy_dst = reinterpret_cast<float*>(w + lay.zcopy);
+  f.copy_n = (B * H) * (int64_t)(p->M * p->L);
   hipError_t e = luna::launch_featuremap(dt, luna::Dt::F32, (int)d, p->L, f, s);
   if (e != hipSuccess) return hip_fail(e, "feature-map kernel launch");
-  // z before the step, for every column block of a head to read (block 0 rewrites z)
-  const size_t zbytes = (size_t)(B * H) * (size_t)(p->M * p->L) * sizeof(float);
-  e = hipMemcpyAsync(w + lay.zcopy, z, zbytes, hipMemcpyDeviceToDevice, s);
-  if (e != hipSuccess) return hip_fail(e, "copy of z");
   luna::StepArgs a{};
   a.phiq = reinterpret_cast<const float*>(w + lay.phiq);
   a.phik = reinterpret_cast<const float*>(w + lay.phik);

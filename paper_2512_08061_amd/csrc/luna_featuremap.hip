@@ -11,6 +11,8 @@
 
 namespace luna {
 
+constexpr int kFmCopyPerBlock = 1024;  // floats per copying workgroup (four per thread)
+
 // HOLD: at most four 16-projection blocks, whose W fragments and biases stay in
 // registers for every item of the parameter set; maps with more blocks reload them
 // per group (held across items they would cost the registers that keep those maps'
@@ -20,10 +22,25 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   constexpr int KS = DH / 32;
   __shared__ PwlLds<L, nseg_cap(L, kFmSegBytes)> tab;
 
+  if ((int)blockIdx.x >= a.map_grid) {  // (uniform) a copying workgroup: kFmCopyPerBlock floats
+    const int64_t base = (int64_t)(blockIdx.x - a.map_grid) * kFmCopyPerBlock + threadIdx.x;
+    float v[kFmCopyPerBlock / 256];
+#pragma unroll
+    for (int j = 0; j < kFmCopyPerBlock / 256; ++j) {
+      const int64_t i = base + 256 * j;
+      v[j] = i < a.copy_n ? a.copy_src[i] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kFmCopyPerBlock / 256; ++j) {
+      const int64_t i = base + 256 * j;
+      if (i < a.copy_n) a.copy_dst[i] = v[j];
+    }
+    return;
+  }
   const int tiles_per_head = (int)((a.rows_per_head + 63) / 64);
   // work items: 64-row tiles of every head; with a second input the items double and
   // the second half maps X2 into out2.  A workgroup takes items blockIdx.x,
-  // blockIdx.x + gridDim.x, ..., so that its table copy serves many tiles.
+  // blockIdx.x + map_grid, ..., so that its table copy serves many tiles.
   const int64_t per_input = a.heads * tiles_per_head;
   const int64_t items = per_input * (a.X2 != nullptr ? 2 : 1);
   const int wave = wave_id(), lane = threadIdx.x % kWave;
@@ -74,7 +91,7 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
     int wset = -1;
     Frag<Tin> wfr[kMaxMB][KS];
     float bz[kMaxMB][4];
-    for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+    for (int64_t item = blockIdx.x; item < items; item += a.map_grid) {
       const Item cur = locate(item);
       const int hset = cur.hset;
       const bool row_ok = cur.row_ok;
@@ -154,12 +171,12 @@ __global__ __launch_bounds__(256) void featuremap_kernel(FeatureMapArgs a) {
   }
 }
 
-// As many workgroups as the device holds at once (registers and LDS table permitting),
-// queried once per kernel (the kernel is a template argument, so that every kernel
-// has its own cached count); more items loop, so that no second round of workgroups
-// starts late.
+// As many mapping workgroups as the device holds at once (registers and LDS table
+// permitting), queried once per kernel (the kernel is a template argument, so that
+// every kernel has its own cached count); more items loop, so that no second round of
+// workgroups starts late.  The copying workgroups, if any, follow them in the grid.
 template <auto Kernel>
-static void fm_launch(int64_t items, const FeatureMapArgs& a, hipStream_t s) {
+static void fm_launch(int64_t items, const FeatureMapArgs& args, hipStream_t s) {
   static const int resident = []() {
     int per_cu = 0, dev = 0, cus = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, 256, 0) != hipSuccess || per_cu < 1) per_cu = 1;
@@ -167,7 +184,10 @@ static void fm_launch(int64_t items, const FeatureMapArgs& a, hipStream_t s) {
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
     return per_cu * cus;
   }();
-  hipLaunchKernelGGL(Kernel, dim3((unsigned)(items < resident ? items : resident)), dim3(256), 0, s, a);
+  FeatureMapArgs a = args;
+  a.map_grid = (int)(items < resident ? items : resident);
+  const int64_t copy_blocks = a.copy_n > 0 ? (a.copy_n + kFmCopyPerBlock - 1) / kFmCopyPerBlock : 0;
+  hipLaunchKernelGGL(Kernel, dim3((unsigned)(a.map_grid + copy_blocks)), dim3(256), 0, s, a);
 }
 
 template <typename Tin, typename Tout, int DH>

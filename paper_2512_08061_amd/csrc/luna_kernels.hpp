@@ -104,6 +104,12 @@ struct FeatureMapArgs {
   int64_t rows_per_head;  // n
   int H;
   int64_t heads;          // B * H
+  // optional copy of copy_n floats from copy_src to copy_dst, done by workgroups of
+  // the same launch beside the mapping ones (the streaming step's z before the step)
+  const float* copy_src;
+  float* copy_dst;
+  int64_t copy_n;
+  int map_grid;           // workgroups that map rows (set by the launcher)
 };
 
 struct NoncausalArgs {

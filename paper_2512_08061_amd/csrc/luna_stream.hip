@@ -17,8 +17,8 @@
 // and the four waves through LDS, in a fixed order (deterministic), one barrier per
 // token.  The state is read once at the start and written once at the end (16-byte
 // accesses), so a step of m tokens costs one pass over S whatever m is.  z is read
-// from a copy taken before the launch: the column blocks of a head are not ordered
-// against one another, and block 0 writes the new z in place.
+// from a copy that the feature-map launch takes: the column blocks of a head are not
+// ordered against one another, and block 0 writes the new z in place.
 #include "luna_device.hpp"
 #include "luna_kernels.hpp"
 

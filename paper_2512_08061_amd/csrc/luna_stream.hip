@@ -13,9 +13,10 @@
 // wave read consecutive LDS words of a feature row), the four columns 4q .. 4q + 3 of
 // S as float4 and the same features of z, in fp32 registers for the whole step.  Per
 // token it adds the key's outer product and forms its partial numerator (four
-// columns) and denominator; the eight groups of a wave are added with lane shuffles
-// and the four waves through LDS, in a fixed order (deterministic), one barrier per
-// token.  The state is read once at the start and written once at the end (16-byte
+// columns) and denominator; the eight groups of a wave are added across lanes on the VALU
+// and the four waves through LDS, in a fixed order (deterministic), for all of a
+// stage's tokens after one barrier, so that the tokens' shuffles overlap the next
+// tokens' updates.  The state is read once at the start and written once at the end (16-byte
 // accesses), so a step of m tokens costs one pass over S whatever m is.  z is read
 // from a copy that the feature-map launch takes: the column blocks of a head are not
 // ordered against one another, and block 0 writes the new z in place.
@@ -31,13 +32,35 @@ constexpr int kStepQuads = kStepCols / 4;           // column quads per workgrou
 constexpr int kStepGroups = 256 / kStepQuads;       // feature groups
 constexpr int kStepFeat = kStepMaxD / kStepGroups;  // features per thread
 constexpr int kStepTokens = 16;                     // tokens staged in LDS at a time
+static_assert(kStepMaxD == 256, "one thread per feature row of the staged tokens");
+static_assert(kStepTokens * kStepCols % 256 == 0, "whole value entries per thread");
+
+// x plus the x of lane l ^ 8, ^ 16 and ^ 32, on the VALU: a rotation by 8 within each
+// row of 16 lanes (data-parallel primitive) pairs lane l with l ^ 8; a permlane swap of a
+// value with itself leaves every lane its own value in one result and its partner's in
+// the other.  Each step adds a pair of values, so both lanes of a pair get the same sum.
+__device__ __forceinline__ float step_sum_xor8(float x) {
+  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float step_sum_xor16(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float step_sum_xor32(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float step_sum_groups(float x) {
+  static_assert(kStepQuads == 8, "the groups of a wave are lane bits 3..5");
+  return step_sum_xor32(step_sum_xor16(step_sum_xor8(x)));
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   __shared__ float sq[kStepTokens][kStepMaxD];
   __shared__ float sk[kStepTokens][kStepMaxD];
   __shared__ __attribute__((aligned(16))) float sv[kStepTokens][kStepCols];
-  __shared__ float red[2][4][kStepQuads][5];  // per wave and column quad: four numerators, the denominator
+  __shared__ float red[kStepTokens][4][kStepQuads][5];  // per token, wave and column quad: four numerators, the denominator
 
   const int nblk = a.d / kStepCols;
   const int head = blockIdx.x / nblk;
@@ -65,18 +88,30 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
 
   for (int t0 = 0; t0 < m; t0 += kStepTokens) {
     const int tn = min(kStepTokens, m - t0);
+    // thread tid stages feature tid of every token of the stage (features past D and
+    // tokens past the step as zeros) and two value entries; all loads are issued
+    // before the first store, so that their latencies overlap
+    float rq[kStepTokens], rk[kStepTokens], rv[kStepTokens * kStepCols / 256];
+#pragma unroll
+    for (int tt = 0; tt < kStepTokens; ++tt) {
+      const bool ok = tt < tn && tid < D;
+      rq[tt] = ok ? PQ[(size_t)(t0 + tt) * D + tid] : 0.0f;
+      rk[tt] = ok ? PK[(size_t)(t0 + tt) * D + tid] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kStepTokens * kStepCols / 256; ++j) {
+      const int tt = tid / kStepCols + (256 / kStepCols) * j, c = tid % kStepCols;
+      rv[j] = tt < tn ? (float)V[(size_t)(t0 + tt) * d + cblk * kStepCols + c] : 0.0f;
+    }
     __syncthreads();  // the previous stage's tokens are no longer read
-    // features past D and tokens past the step stage as zeros
-    for (int idx = tid; idx < kStepTokens * kStepMaxD; idx += blockDim.x) {
-      const int tt = idx / kStepMaxD, f = idx % kStepMaxD;
-      const bool ok = tt < tn && f < D;
-      sq[tt][f] = ok ? PQ[(size_t)(t0 + tt) * D + f] : 0.0f;
-      sk[tt][f] = ok ? PK[(size_t)(t0 + tt) * D + f] : 0.0f;
+#pragma unroll
+    for (int tt = 0; tt < kStepTokens; ++tt) {
+      sq[tt][tid] = rq[tt];
+      sk[tt][tid] = rk[tt];
     }
-    for (int idx = tid; idx < kStepTokens * kStepCols; idx += blockDim.x) {
-      const int tt = idx / kStepCols, c = idx % kStepCols;
-      sv[tt][c] = tt < tn ? (float)V[(size_t)(t0 + tt) * d + cblk * kStepCols + c] : 0.0f;
-    }
+#pragma unroll
+    for (int j = 0; j < kStepTokens * kStepCols / 256; ++j)
+      sv[tid / kStepCols + (256 / kStepCols) * j][tid % kStepCols] = rv[j];
     __syncthreads();
 #pragma unroll
     for (int tt = 0; tt < kStepTokens; ++tt) {
@@ -100,33 +135,31 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
           den = fmaf(qf, zz[i], den);
         }
         // the eight groups of this wave (lane bits 3..5)
-#pragma unroll
-        for (int off = kStepQuads; off < kWave; off *= 2) {
-          num.x += __shfl_xor(num.x, off);
-          num.y += __shfl_xor(num.y, off);
-          num.z += __shfl_xor(num.z, off);
-          num.w += __shfl_xor(num.w, off);
-          den += __shfl_xor(den, off);
-        }
-        const int b = (t0 + tt) & 1;  // alternating buffers: one barrier per token
+        num.x = step_sum_groups(num.x);
+        num.y = step_sum_groups(num.y);
+        num.z = step_sum_groups(num.z);
+        num.w = step_sum_groups(num.w);
+        den = step_sum_groups(den);
         if (lane < kStepQuads) {
-          red[b][wave][q][0] = num.x;
-          red[b][wave][q][1] = num.y;
-          red[b][wave][q][2] = num.z;
-          red[b][wave][q][3] = num.w;
-          red[b][wave][q][4] = den;
-        }
-        __syncthreads();
-        if (tid < kStepCols) {
-          float nu = 0.0f, de = 0.0f;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            nu += red[b][w][tid / 4][tid % 4];
-            de += red[b][w][tid / 4][4];
-          }
-          out[(size_t)(t0 + tt) * d + cblk * kStepCols + tid] = (T)(nu / (de + a.eps));
+          red[tt][wave][q][0] = num.x;
+          red[tt][wave][q][1] = num.y;
+          red[tt][wave][q][2] = num.z;
+          red[tt][wave][q][3] = num.w;
+          red[tt][wave][q][4] = den;
         }
       }
+    }
+    // the four waves of every staged token at once: one barrier per stage, not per token
+    __syncthreads();
+    for (int idx = tid; idx < tn * kStepCols; idx += blockDim.x) {
+      const int tt = idx / kStepCols, c = idx % kStepCols;
+      float nu = 0.0f, de = 0.0f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        nu += red[tt][w][c / 4][c % 4];
+        de += red[tt][w][c / 4][4];
+      }
+      out[(size_t)(t0 + tt) * d + cblk * kStepCols + c] = (T)(nu / (de + a.eps));
     }
   }
 

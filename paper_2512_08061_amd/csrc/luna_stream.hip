@@ -32,6 +32,7 @@ constexpr int kStepQuads = kStepCols / 4;           // column quads per workgrou
 constexpr int kStepGroups = 256 / kStepQuads;       // feature groups
 constexpr int kStepFeat = kStepMaxD / kStepGroups;  // features per thread
 constexpr int kStepTokens = 16;                     // tokens staged in LDS at a time
+constexpr int kStepMfmaMinTokens = 16;              // steps this long run on the matrix cores
 static_assert(kStepMaxD == 256, "one thread per feature row of the staged tokens");
 static_assert(kStepTokens * kStepCols % 256 == 0, "whole value entries per thread");
 
@@ -173,15 +174,177 @@ __global__ __launch_bounds__(256) void causal_step_kernel(StepArgs a) {
   }
 }
 
+// The same step for longer steps, on the matrix cores in fp32 (v_mfma_f32_16x16x4_f32):
+// per stage of 16 tokens, in the chunked form of the prefix sums,
+//
+//   out = (phi(Q) S + mask(phi(Q) phi(K)^T) V) / (phi(Q) z + mask(phi(Q) phi(K)^T) 1 + eps),
+//   S += phi(K)^T V,  z += phi(K)^T 1,
+//
+// with S and z the state before the stage and mask keeping key <= query.  Wave w holds
+// the rows 64w .. 64w + 63 of S (four 16-feature tiles by the workgroup's two 16-column
+// tiles) and of z (as a tile of 16 equal columns) as accumulator tiles: lane (g, c) holds
+// features 16t + 4g + j, column c.  The readout contracts over features in the order
+// that makes those registers its B operand as they are (k-slot g of k-step j is feature
+// 16t + 4g + j); the update contracts over tokens and writes the same tiles.  Each wave
+// forms its features' share of the readout and of the 16 x 16 scores; the shares are
+// added through LDS in a fixed order, and waves 0 and 1 finish one column tile each.
+constexpr int kStepRow = kStepMaxD + 4;  // padded LDS row of a staged token's features
+
+template <typename T>
+__global__ __launch_bounds__(256) void causal_step_mfma_kernel(StepArgs a) {
+  __shared__ __attribute__((aligned(16))) float sq[kStepTokens][kStepRow];
+  __shared__ __attribute__((aligned(16))) float sk[kStepTokens][kStepRow];
+  __shared__ float sv[kStepTokens][kStepCols];
+  __shared__ float rnum[4][kStepTokens][kStepCols + 1];     // per wave: readout numerators
+  __shared__ float rden[4][kStepTokens];                    // per wave: phi(q) . z
+  __shared__ float rsc[4][kStepTokens][kStepTokens + 1];    // per wave: scores [key][query]
+
+  const int nblk = a.d / kStepCols;
+  const int head = blockIdx.x / nblk;
+  const int cblk = blockIdx.x - head * nblk;
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int g = lane / 16, c = lane % 16;
+  const int D = a.D, d = a.d, m = a.m;
+  const int col0 = cblk * kStepCols;
+  const int fw = 64 * wave;  // this wave's first feature
+  float* S = a.S + (size_t)head * D * d;
+  float* z = a.z + (size_t)head * D;
+  const float* z0 = a.z_in + (size_t)head * D;
+  const float* PQ = a.phiq + (size_t)head * m * D;
+  const float* PK = a.phik + (size_t)head * m * D;
+  const T* V = reinterpret_cast<const T*>(a.V) + (size_t)head * m * d;
+  T* out = reinterpret_cast<T*>(a.out) + (size_t)head * m * d;
+
+  f32x4 sc[4][2], zc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int f = fw + 16 * t + 4 * g + j;
+      sc[t][0][j] = f < D ? S[(size_t)f * d + col0 + c] : 0.0f;
+      sc[t][1][j] = f < D ? S[(size_t)f * d + col0 + 16 + c] : 0.0f;
+      zc[t][j] = f < D ? z0[f] : 0.0f;
+    }
+  }
+
+  for (int t0 = 0; t0 < m; t0 += kStepTokens) {
+    const int tn = min(kStepTokens, m - t0);
+    // thread tid stages feature tid of every token of the stage (features past D and
+    // tokens past the step as zeros, which add nothing below) and two value entries
+    float rq[kStepTokens], rk[kStepTokens], rv[kStepTokens * kStepCols / 256];
+#pragma unroll
+    for (int tt = 0; tt < kStepTokens; ++tt) {
+      const bool ok = tt < tn && tid < D;
+      rq[tt] = ok ? PQ[(size_t)(t0 + tt) * D + tid] : 0.0f;
+      rk[tt] = ok ? PK[(size_t)(t0 + tt) * D + tid] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kStepTokens * kStepCols / 256; ++j) {
+      const int tt = tid / kStepCols + (256 / kStepCols) * j;
+      rv[j] = tt < tn ? (float)V[(size_t)(t0 + tt) * d + col0 + tid % kStepCols] : 0.0f;
+    }
+    __syncthreads();  // the previous stage's tokens and shares are no longer read
+#pragma unroll
+    for (int tt = 0; tt < kStepTokens; ++tt) {
+      sq[tt][tid] = rq[tt];
+      sk[tt][tid] = rk[tt];
+    }
+#pragma unroll
+    for (int j = 0; j < kStepTokens * kStepCols / 256; ++j)
+      sv[tid / kStepCols + (256 / kStepCols) * j][tid % kStepCols] = rv[j];
+    __syncthreads();
+
+    // this wave's features' share of phi(Q) S, phi(Q) z and the scores phi(K) phi(Q)^T,
+    // from the state before the stage
+    f32x4 np0 = zero4(), np1 = zero4(), dp = zero4(), gp = zero4();
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const float4 qa = *reinterpret_cast<const float4*>(&sq[c][fw + 16 * t + 4 * g]);
+      const float4 ka = *reinterpret_cast<const float4*>(&sk[c][fw + 16 * t + 4 * g]);
+      const float qv[4] = {qa.x, qa.y, qa.z, qa.w}, kv[4] = {ka.x, ka.y, ka.z, ka.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        np0 = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[j], sc[t][0][j], np0, 0, 0, 0);
+        np1 = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[j], sc[t][1][j], np1, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[j], zc[t][j], dp, 0, 0, 0);
+        gp = __builtin_amdgcn_mfma_f32_16x16x4f32(kv[j], qv[j], gp, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {  // row 4g + j: a token (readout) or a key (scores)
+      rnum[wave][4 * g + j][c] = np0[j];
+      rnum[wave][4 * g + j][16 + c] = np1[j];
+      rsc[wave][4 * g + j][c] = gp[j];
+      if (c == 0) rden[wave][4 * g + j] = dp[j];
+    }
+
+    // the stage's keys into the state (k-slot g of k-step j is token 4g + j)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tk = 4 * g + j;
+      const float v0 = sv[tk][c], v1 = sv[tk][16 + c];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float kf = sk[tk][fw + 16 * t + c];  // A operand: row = feature fw + 16t + c
+        sc[t][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(kf, v0, sc[t][0], 0, 0, 0);
+        sc[t][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(kf, v1, sc[t][1], 0, 0, 0);
+        zc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(kf, 1.0f, zc[t], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+
+    if (wave < 2) {  // (uniform) wave ct finishes column tile ct
+      const int ct = wave;
+      // the masked scores as A operand (row = query c, k-slot g of k-step j = key 4g + j)
+      f32x4 ni = zero4(), di = zero4();
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = 4 * g + j;
+        float sg = ((rsc[0][key][c] + rsc[1][key][c]) + rsc[2][key][c]) + rsc[3][key][c];
+        sg = key <= c ? sg : 0.0f;
+        ni = __builtin_amdgcn_mfma_f32_16x16x4f32(sg, sv[key][16 * ct + c], ni, 0, 0, 0);
+        di = __builtin_amdgcn_mfma_f32_16x16x4f32(sg, 1.0f, di, 0, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int tt = 4 * g + j;  // C row: token
+        if (tt < tn) {
+          const int col = 16 * ct + c;
+          const float nu = ((rnum[0][tt][col] + rnum[1][tt][col]) + (rnum[2][tt][col] + rnum[3][tt][col])) + ni[j];
+          const float de = ((rden[0][tt] + rden[1][tt]) + (rden[2][tt] + rden[3][tt])) + di[j];
+          out[(size_t)(t0 + tt) * d + col0 + col] = (T)(nu / (de + a.eps));
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int f = fw + 16 * t + 4 * g + j;
+      if (f < D) {
+        S[(size_t)f * d + col0 + c] = sc[t][0][j];
+        S[(size_t)f * d + col0 + 16 + c] = sc[t][1][j];
+        if (cblk == 0 && c == 0) z[f] = zc[t][j];  // every column block carries the same z
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_causal_step(Dt dt, const StepArgs& a, hipStream_t s) {
   if (a.d % kStepCols != 0 || a.D > kStepMaxD) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(a.heads * (a.d / kStepCols)));
-  if (dt == Dt::BF16)
-    hipLaunchKernelGGL(causal_step_kernel<__bf16>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(causal_step_kernel<float>, grid, dim3(256), 0, s, a);
+  const bool mfma = a.m >= kStepMfmaMinTokens;
+  if (dt == Dt::BF16) {
+    if (mfma) hipLaunchKernelGGL(causal_step_mfma_kernel<__bf16>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(causal_step_kernel<__bf16>, grid, dim3(256), 0, s, a);
+  } else {
+    if (mfma) hipLaunchKernelGGL(causal_step_mfma_kernel<float>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(causal_step_kernel<float>, grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

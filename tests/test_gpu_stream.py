@@ -62,10 +62,14 @@ def test_attn_state(dtype, d, M, L, n, B, H):
     assert_close(_col(to_np(zt)), _col(z0 + zr), dtype, "z accumulated")
 
 
-# (dtype, d, M, L, n, m): every step but the last has m tokens
+# (dtype, d, M, L, n, m): every step but the last has m tokens; steps of 16 tokens or
+# more run on the matrix cores (stages of 16 tokens, the last ragged), shorter ones on
+# the VALU
 STEP_CASES = [
     ("f32", 32, 8, 8, 37, 5), ("f32", 64, 16, 8, 20, 1), ("bf16", 64, 16, 8, 100, 16), ("bf16", 128, 32, 8, 70, 33),
     ("bf16", 32, 5, 4, 20, 1), ("bf16", 64, 64, 4, 40, 17), ("bf16", 128, 3, 8, 9, 4),
+    ("f32", 32, 8, 8, 37, 16), ("bf16", 32, 5, 4, 40, 16), ("f32", 128, 32, 8, 50, 64), ("bf16", 64, 7, 2, 30, 8),
+    ("bf16", 64, 7, 2, 45, 22),
 ]
 
 
@@ -113,13 +117,15 @@ def test_prefill_then_decode(dtype, d, M, L, n0):
     assert_close_rows(out, scan, dtype, "decoded rows against the chunked scan")
 
 
-def test_step_many_heads_from_state():
+@pytest.mark.parametrize("m", [3, 20])
+def test_step_many_heads_from_state(m):
     """Enough heads that the step kernel's grid runs in several rounds of workgroups
     (2048 heads x 4 column blocks): every column block of a head must read z as it was
     before the call, although the head's block 0 rewrites z in place.  Started from a
-    random state, against the oracle's recurrence."""
+    random state, against the oracle's recurrence; 3 tokens on the VALU, 20 on the
+    matrix cores."""
     import torch
-    B, H, m, d, M, L = 16, 128, 3, 128, 32, 8
+    B, H, d, M, L = 16, 128, 128, 32, 8
     w = small_workload("bf16", B=B, H=H, n=m, d=d, M=M, L=L, causal=True)
     say(f"step from a random state, {B * H} heads: {w.name}")
     Q, K, V, p = inputs(w, seed=29)

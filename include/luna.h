@@ -208,8 +208,11 @@ luna_status luna_attn_state(const void* K, const void* V, luna_dtype dtype, int6
  * S [B, H, M*L, d] and z [B, H, M*L] (fp32, feature i*L + l) are read and updated in
  * place; they must not alias Q, K, V, out or the workspace, and S must be 16-byte
  * aligned.  Q, K, V, out:
- * [B, H, m, d] in dtype.  The state is carried in fp32 throughout.  Stepping a
- * sequence from zeros gives what luna_attn_fwd_causal computes, up to rounding.
+ * [B, H, m, d] in dtype.  The state is carried in fp32 throughout.  Steps of 16
+ * tokens or more run per 16-token stage in the chunked form of the same prefix sums
+ * (fp32 matrix products), shorter ones token by token; the two agree up to rounding.
+ * Stepping a sequence from zeros gives what luna_attn_fwd_causal computes, up to
+ * rounding.
  * tables_ready 0: the call builds the channel tables in the workspace, as every
  * other entry point does; 1: it uses the tables an earlier luna_attn_causal_step
  * left in the same workspace, enqueued before it on the same stream, with the same

@@ -192,8 +192,16 @@ constexpr int kStepRow = kStepMaxD + 4;  // padded LDS row of a staged token's f
 
 template <typename T>
 __global__ __launch_bounds__(256) void causal_step_mfma_kernel(StepArgs a) {
-  __shared__ __attribute__((aligned(16))) float sq[kStepTokens][kStepRow];
-  __shared__ __attribute__((aligned(16))) float sk[kStepTokens][kStepRow];
+  // the staged tokens' features; before the first stage and after the last they hold
+  // the workgroup's S columns [feature][32], 16-byte chunks swapped between the two
+  // column halves on every other group of four rows (two lane groups of an accumulator
+  // read then hit different banks)
+  __shared__ __attribute__((aligned(16))) float sqk[2][kStepTokens][kStepRow];
+  static_assert(2 * kStepTokens * kStepRow >= kStepMaxD * kStepCols, "S columns fit the token buffers");
+  float (&sq)[kStepTokens][kStepRow] = sqk[0];
+  float (&sk)[kStepTokens][kStepRow] = sqk[1];
+  float* const st = &sqk[0][0][0];
+  auto st_at = [](int f, int col) { return f * kStepCols + (col ^ (16 * ((f >> 2) & 1))); };
   __shared__ float sv[kStepTokens][kStepCols];
   __shared__ float rnum[4][kStepTokens][kStepCols + 1];     // per wave: readout numerators
   __shared__ float rden[4][kStepTokens];                    // per wave: phi(q) . z
@@ -215,14 +223,24 @@ __global__ __launch_bounds__(256) void causal_step_mfma_kernel(StepArgs a) {
   const T* V = reinterpret_cast<const T*>(a.V) + (size_t)head * m * d;
   T* out = reinterpret_cast<T*>(a.out) + (size_t)head * m * d;
 
+  // S columns into LDS with 16-byte loads (features past D as zeros), then into the
+  // accumulator tiles
+#pragma unroll
+  for (int i = 0; i < kStepMaxD * kStepCols / 4 / 256; ++i) {
+    const int idx = tid + 256 * i, f = idx / (kStepCols / 4), q4 = 4 * (idx % (kStepCols / 4));
+    const float4 v = f < D ? *reinterpret_cast<const float4*>(&S[(size_t)f * d + col0 + q4])
+                           : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    *reinterpret_cast<float4*>(&st[st_at(f, q4)]) = v;
+  }
+  __syncthreads();
   f32x4 sc[4][2], zc[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int f = fw + 16 * t + 4 * g + j;
-      sc[t][0][j] = f < D ? S[(size_t)f * d + col0 + c] : 0.0f;
-      sc[t][1][j] = f < D ? S[(size_t)f * d + col0 + 16 + c] : 0.0f;
+      sc[t][0][j] = st[st_at(f, c)];
+      sc[t][1][j] = st[st_at(f, 16 + c)];
       zc[t][j] = f < D ? z0[f] : 0.0f;
     }
   }
@@ -318,17 +336,23 @@ __global__ __launch_bounds__(256) void causal_step_mfma_kernel(StepArgs a) {
     }
   }
 
+  // the accumulator tiles back through LDS (no wave reads the token buffers after the
+  // last stage's update), then 16-byte stores of the rows below D
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int f = fw + 16 * t + 4 * g + j;
-      if (f < D) {
-        S[(size_t)f * d + col0 + c] = sc[t][0][j];
-        S[(size_t)f * d + col0 + 16 + c] = sc[t][1][j];
-        if (cblk == 0 && c == 0) z[f] = zc[t][j];  // every column block carries the same z
-      }
+      st[st_at(f, c)] = sc[t][0][j];
+      st[st_at(f, 16 + c)] = sc[t][1][j];
+      if (f < D && cblk == 0 && c == 0) z[f] = zc[t][j];  // every column block carries the same z
     }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kStepMaxD * kStepCols / 4 / 256; ++i) {
+    const int idx = tid + 256 * i, f = idx / (kStepCols / 4), q4 = 4 * (idx % (kStepCols / 4));
+    if (f < D) *reinterpret_cast<float4*>(&S[(size_t)f * d + col0 + q4]) = *reinterpret_cast<const float4*>(&st[st_at(f, q4)]);
   }
 }
 
